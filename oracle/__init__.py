@@ -1,0 +1,176 @@
+"""fp64 CPU oracle for the CacheBridge mapper path -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  The product library
+(``paper_2609_00891_amd``) never imports it, and it imports nothing from the
+product.  The arithmetic lives in ``cb_oracle.c`` (plain loops, fp64); this
+module only marshals numpy arrays through ctypes.
+
+Functions follow the paper (CacheBridge, "Efficient Cross-Model KV Cache
+Transfer"):
+
+* :func:`stats` -- augmented weighted moments G, C (Sec. 3.4, Eq. fusedstats,
+  over the head-local feature of Sec. 3.2, Eq. localfeature, with k = 1).
+* :func:`ridge_solve` -- (G + lambda D)^-1 C (Sec. 3.1, Eq. closedform; Sec. 3.4).
+* :func:`apply` -- RNE_bf16([x;1] W~) per token (Sec. 1; Sec. 2.3, Eq. support-cost).
+* :func:`coefficient_count` -- C(f) = 2 L_t H_t (k f d_s) d_t (Sec. 2.3, Eq. support-cost).
+
+Parity status: pinned by ``tests/test_oracle_pins.py``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Mapping, Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+_i32p = ctypes.POINTER(ctypes.c_int32)
+_i64p = ctypes.POINTER(ctypes.c_int64)
+_u16p = ctypes.POINTER(ctypes.c_uint16)
+_f32p = ctypes.POINTER(ctypes.c_float)
+_f64p = ctypes.POINTER(ctypes.c_double)
+
+HEAD_MAP_FIELDS = ("tgt_layer", "tgt_head", "kv", "src_layer", "src_head", "weight_row")
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        from . import build as _b  # noqa: PLC0415
+        _b.build()
+    lib = ctypes.CDLL(_LIB_PATH)
+    lib.oracle_stats.restype = ctypes.c_int
+    lib.oracle_stats.argtypes = [ctypes.c_int] + [_i32p] * 6 + [
+        _u16p, _i64p, ctypes.c_int, _u16p, _i64p, ctypes.c_int,
+        _f32p, ctypes.c_int64, ctypes.c_int, ctypes.c_int, _f64p, _f64p, ctypes.c_int]
+    lib.oracle_ridge_solve.restype = ctypes.c_int
+    lib.oracle_ridge_solve.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, _f64p, _f64p,
+                                       ctypes.c_double, ctypes.c_int, ctypes.c_int, _f64p, _i32p,
+                                       ctypes.c_int]
+    lib.oracle_apply.restype = ctypes.c_int
+    lib.oracle_apply.argtypes = [ctypes.c_int] + [_i32p] * 5 + [
+        _f64p, _u16p, _i64p, ctypes.c_int, _u16p, _i64p, ctypes.c_int,
+        ctypes.c_int, ctypes.c_int, ctypes.c_int]
+    lib.oracle_double_to_bf16_array.restype = ctypes.c_int
+    lib.oracle_double_to_bf16_array.argtypes = [ctypes.c_int64, _f64p, _u16p]
+    _lib = lib
+    return lib
+
+
+def _ptr(a: np.ndarray, ctype):
+    return a.ctypes.data_as(ctype)
+
+
+def _hm_arrays(head_map: Mapping[str, np.ndarray], fields=HEAD_MAP_FIELDS):
+    out = []
+    n = None
+    for f in fields:
+        a = np.ascontiguousarray(np.asarray(head_map[f], dtype=np.int32))
+        if n is None:
+            n = a.shape[0]
+        if a.shape != (n,):
+            raise ValueError(f"head_map field {f} has shape {a.shape}, expected ({n},)")
+        out.append(a)
+    return n, out
+
+
+def _strides5(strides) -> np.ndarray:
+    s = np.ascontiguousarray(np.asarray(strides, dtype=np.int64))
+    if s.shape != (5,):
+        raise ValueError("strides must be (layer, kv, seq, head, tok) element strides")
+    return s
+
+
+def _u16(a: np.ndarray) -> np.ndarray:
+    if a.dtype != np.uint16:
+        raise TypeError("caches are passed as uint16 arrays holding bfloat16 bits")
+    return a
+
+
+def stats(head_map, src, src_strides, d_s, tgt, tgt_strides, d_t, weights, w_row_stride,
+          n_seqs, seq_len, G: Optional[np.ndarray] = None, C: Optional[np.ndarray] = None,
+          n_threads: int = 0):
+    """Accumulate G += sum w x~ x~^T and C += sum w x~ y^T in fp64 for every map.
+
+    ``src``/``tgt`` are flat (or any-shaped, C-contiguous) uint16 arrays of
+    bfloat16 bits addressed with the given element strides
+    (layer, kv, seq, head, tok); channel stride is 1.  ``weights`` is fp32,
+    indexed ``row * w_row_stride + seq * seq_len + tok``.  Returns (G, C).
+    """
+    lib = _load()
+    n, hm = _hm_arrays(head_map)
+    P = d_s + 1
+    if G is None:
+        G = np.zeros((n, P, P), dtype=np.float64)
+    if C is None:
+        C = np.zeros((n, P, d_t), dtype=np.float64)
+    assert G.dtype == np.float64 and G.flags.c_contiguous and G.shape == (n, P, P)
+    assert C.dtype == np.float64 and C.flags.c_contiguous and C.shape == (n, P, d_t)
+    src = np.ascontiguousarray(_u16(src))
+    tgt = np.ascontiguousarray(_u16(tgt))
+    w = np.ascontiguousarray(np.asarray(weights, dtype=np.float32))
+    ss, ts = _strides5(src_strides), _strides5(tgt_strides)
+    lib.oracle_stats(n, *[_ptr(a, _i32p) for a in hm], _ptr(src, _u16p), _ptr(ss, _i64p), d_s,
+                     _ptr(tgt, _u16p), _ptr(ts, _i64p), d_t, _ptr(w, _f32p), int(w_row_stride),
+                     int(n_seqs), int(seq_len), _ptr(G, _f64p), _ptr(C, _f64p), int(n_threads))
+    return G, C
+
+
+def ridge_solve(G, C, lam, relative=True, bias_unpenalized=False, n_threads: int = 0):
+    """Solve (G + lambda_m D) W~ = C per map in fp64; returns (W~, info)."""
+    lib = _load()
+    G = np.ascontiguousarray(np.asarray(G, dtype=np.float64))
+    C = np.ascontiguousarray(np.asarray(C, dtype=np.float64))
+    n, P, P2 = G.shape
+    assert P == P2 and C.shape[:2] == (n, P)
+    d_t = C.shape[2]
+    W = np.zeros((n, P, d_t), dtype=np.float64)
+    info = np.zeros((n,), dtype=np.int32)
+    lib.oracle_ridge_solve(n, P, d_t, _ptr(G, _f64p), _ptr(C, _f64p), float(lam), int(bool(relative)),
+                           int(bool(bias_unpenalized)), _ptr(W, _f64p), _ptr(info, _i32p),
+                           int(n_threads))
+    return W, info
+
+
+def apply(head_map, W, src, src_strides, d_s, out, out_strides, d_t, n_seqs, seq_len,
+          n_threads: int = 0):
+    """Write RNE_bf16([x;1] W~) for every map and token into ``out`` (uint16 bits)."""
+    lib = _load()
+    n, hm = _hm_arrays(head_map, HEAD_MAP_FIELDS[:5])
+    W = np.ascontiguousarray(np.asarray(W, dtype=np.float64))
+    assert W.shape == (n, d_s + 1, d_t)
+    src = np.ascontiguousarray(_u16(src))
+    if not (out.dtype == np.uint16 and out.flags.c_contiguous):
+        raise TypeError("out must be a C-contiguous uint16 array")
+    ss, os_ = _strides5(src_strides), _strides5(out_strides)
+    lib.oracle_apply(n, *[_ptr(a, _i32p) for a in hm], _ptr(W, _f64p), _ptr(src, _u16p),
+                     _ptr(ss, _i64p), d_s, _ptr(out, _u16p), _ptr(os_, _i64p), d_t,
+                     int(n_seqs), int(seq_len), int(n_threads))
+    return out
+
+
+def double_to_bf16(v) -> np.ndarray:
+    """Round fp64 values once to bfloat16 (nearest, ties to even); returns uint16 bits."""
+    lib = _load()
+    v = np.ascontiguousarray(np.asarray(v, dtype=np.float64))
+    out = np.empty(v.shape, dtype=np.uint16)
+    lib.oracle_double_to_bf16_array(v.size, _ptr(v, _f64p), _ptr(out, _u16p))
+    return out
+
+
+def bf16_to_double(bits) -> np.ndarray:
+    """bfloat16 bits -> fp64 (exact)."""
+    b = np.asarray(bits, dtype=np.uint16)
+    return (b.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def coefficient_count(L_t: int, H_t: int, k: int, f: int, d_s: int, d_t: int) -> int:
+    """Non-bias coefficient count over K and V, C(f) = 2 L_t H_t (k f d_s) d_t (Eq. support-cost)."""
+    return 2 * L_t * H_t * (k * f * d_s) * d_t

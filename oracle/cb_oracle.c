@@ -1,0 +1,252 @@
+/*
+ * cb_oracle.c -- plain fp64 CPU oracle for the CacheBridge mapper path.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the reference that the GPU library is
+ * checked against.  Only the test suite, the smoke check and the benchmark's
+ * CPU-baseline leg may load it; the product library never links, includes or
+ * calls anything here, and this file includes nothing from the product.
+ *
+ * What it computes (CacheBridge, "Efficient Cross-Model KV Cache Transfer"):
+ *
+ *   Head-local feature (Sec. 3.2, Eq. localfeature, one selected source layer):
+ *     the map for target (layer l, head h, component z in {K,V}) reads the
+ *     source row Z^S[src_layer, z, seq, src_head, t] (width d_s) and the
+ *     target row Z^T[l, z, seq, h, t] (width d_t).
+ *
+ *   Sufficient statistics (Sec. 3.4, Eq. fusedstats, in augmented form):
+ *     x~ = [x ; 1] (width P = d_s + 1), w = weights[weight_row][token],
+ *       G += sum_t w x~ x~^T        (P x P)
+ *       C += sum_t w x~ y^T         (P x d_t)
+ *     The centered A_h, B_h and the weighted means of the paper are all
+ *     contained in G and C (the last row/column holds sum w, sum w x, sum w y).
+ *
+ *   Ridge solve (Sec. 3.1 Eq. closedform; Sec. 3.4 solver):
+ *     M = G + lambda_m * D,  W~ = M^{-1} C   (fp64 Cholesky)
+ *     D = I (bias penalized)  or  diag(1,..,1,0) (bias not penalized, which is
+ *     exactly the centered weighted ridge of Eq. closedform by a Schur
+ *     complement on the bias row).  lambda_m = lambda * tr(G)/P when relative.
+ *     Rows 0..d_s-1 of W~ are W, row d_s is the bias b^T.
+ *
+ *   Online application (Sec. 1 pipeline; Sec. 2.3 Eq. support-cost):
+ *     out[l, z, seq, h, t, :] = RNE_bf16( x~ W~ ) with the sum taken in fp64 and
+ *     rounded once, to nearest with ties to even, to bfloat16.
+ *
+ * Parity status: stats, solve and apply are pinned by the tests in
+ * tests/test_oracle_pins.py (closed forms, invariants, library special cases,
+ * brute-force minimality of the paper's objective).  No worked numerical
+ * example exists in the paper, so no value of the paper itself pins them.
+ *
+ * Everything is plain loops in fp64, parallel over maps only (OpenMP), with no
+ * blocking or reordering beyond the definitions above.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* bfloat16 bits -> double (exact: bf16 is the top half of an IEEE binary32). */
+static double bf16_bits_to_double(uint16_t b) {
+    uint32_t u = ((uint32_t)b) << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+/*
+ * double -> bfloat16 bits, rounded once to nearest with ties to even.
+ * bfloat16 carries 8 significant bits and the binary32 exponent range
+ * (normals from 2^-126, subnormal quantum 2^-133, largest finite
+ * (2 - 2^-7) * 2^127).  The value is scaled by a power of two so that the
+ * retained bits become an integer, rounded with nearbyint (round-half-even in
+ * the default floating-point environment), and scaled back; both scalings are
+ * exact.  The result is representable in binary32, whose top 16 bits are the
+ * bfloat16 encoding.
+ */
+uint16_t oracle_double_to_bf16(double v) {
+    if (isnan(v)) return (uint16_t)0x7FC0u;
+    if (isinf(v)) return v > 0 ? (uint16_t)0x7F80u : (uint16_t)0xFF80u;
+    if (v == 0.0) return signbit(v) ? (uint16_t)0x8000u : (uint16_t)0x0000u;
+    double a = fabs(v);
+    int e;
+    (void)frexp(a, &e);            /* a = m * 2^e, m in [0.5, 1): leading bit is 2^(e-1) */
+    int q = e - 8;                 /* weight of the 8th significant bit */
+    if (q < -133) q = -133;        /* below the normal range the quantum is fixed */
+    double r = ldexp(nearbyint(ldexp(a, -q)), q);
+    const double bf16_max = ldexp(255.0, 120);   /* (2 - 2^-7) * 2^127 */
+    uint16_t bits;
+    if (r > bf16_max) {
+        bits = 0x7F80u;            /* rounds past the largest finite value */
+    } else {
+        float f = (float)r;        /* exact */
+        uint32_t u;
+        memcpy(&u, &f, sizeof u);
+        bits = (uint16_t)(u >> 16);
+    }
+    return signbit(v) ? (uint16_t)(bits | 0x8000u) : bits;
+}
+
+/* Element offset of row (layer, kv, seq, head, tok) in a strided cache view. */
+static int64_t row_offset(const int64_t *s, int layer, int kv, int seq, int head, int tok) {
+    return (int64_t)layer * s[0] + (int64_t)kv * s[1] + (int64_t)seq * s[2] +
+           (int64_t)head * s[3] + (int64_t)tok * s[4];
+}
+
+static void set_threads(int n_threads) {
+#ifdef _OPENMP
+    if (n_threads > 0) omp_set_num_threads(n_threads);
+#else
+    (void)n_threads;
+#endif
+}
+
+/*
+ * Weighted augmented moments, accumulated into G [n_maps][P][P] and
+ * C [n_maps][P][d_t] (both fp64, row-major, P = d_s + 1).
+ *   src/tgt: bf16 bits, strides {layer, kv, seq, head, tok} in elements,
+ *            channel stride 1.
+ *   weights: fp32, weights[row * w_row_stride + seq * seq_len + tok].
+ * Every token of every sequence is visited.  Returns 0.
+ */
+int oracle_stats(int n_maps,
+                 const int32_t *tgt_layer, const int32_t *tgt_head, const int32_t *kv,
+                 const int32_t *src_layer, const int32_t *src_head, const int32_t *weight_row,
+                 const uint16_t *src, const int64_t *src_strides, int d_s,
+                 const uint16_t *tgt, const int64_t *tgt_strides, int d_t,
+                 const float *weights, int64_t w_row_stride,
+                 int n_seqs, int seq_len,
+                 double *G, double *C, int n_threads) {
+    const int P = d_s + 1;
+    set_threads(n_threads);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int m = 0; m < n_maps; ++m) {
+        double *Gm = G + (int64_t)m * P * P;
+        double *Cm = C + (int64_t)m * P * d_t;
+        double *xt = (double *)malloc(sizeof(double) * (size_t)P);
+        double *y = (double *)malloc(sizeof(double) * (size_t)d_t);
+        for (int b = 0; b < n_seqs; ++b) {
+            for (int t = 0; t < seq_len; ++t) {
+                const uint16_t *xr = src + row_offset(src_strides, src_layer[m], kv[m], b, src_head[m], t);
+                const uint16_t *yr = tgt + row_offset(tgt_strides, tgt_layer[m], kv[m], b, tgt_head[m], t);
+                const double w = (double)weights[(int64_t)weight_row[m] * w_row_stride +
+                                                 (int64_t)b * seq_len + t];
+                for (int i = 0; i < d_s; ++i) xt[i] = bf16_bits_to_double(xr[i]);
+                xt[d_s] = 1.0;
+                for (int j = 0; j < d_t; ++j) y[j] = bf16_bits_to_double(yr[j]);
+                for (int i = 0; i < P; ++i) {
+                    const double wi = w * xt[i];
+                    for (int j = 0; j < P; ++j) Gm[(int64_t)i * P + j] += wi * xt[j];
+                    for (int j = 0; j < d_t; ++j) Cm[(int64_t)i * d_t + j] += wi * y[j];
+                }
+            }
+        }
+        free(xt);
+        free(y);
+    }
+    return 0;
+}
+
+/*
+ * Batched ridge solve in fp64.
+ *   G [n_maps][P][P], C [n_maps][P][d_t]  ->  W [n_maps][P][d_t]
+ *   lambda_relative != 0: lambda_m = lambda * trace(G_m) / P, else lambda.
+ *   bias_unpenalized != 0: the ridge term is left off the last diagonal entry.
+ * Cholesky M = L L^T (row by row), then L Z = C and L^T W = Z.
+ * info[m] = 0 on success, else the 1-based index of the first pivot that is not
+ * positive and finite; W_m is then zero-filled.  Returns 0.
+ */
+int oracle_ridge_solve(int n_maps, int P, int d_t, const double *G, const double *C,
+                       double lambda, int lambda_relative, int bias_unpenalized,
+                       double *W, int32_t *info, int n_threads) {
+    set_threads(n_threads);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int m = 0; m < n_maps; ++m) {
+        const double *Gm = G + (int64_t)m * P * P;
+        const double *Cm = C + (int64_t)m * P * d_t;
+        double *Wm = W + (int64_t)m * P * d_t;
+        double *L = (double *)calloc((size_t)P * P, sizeof(double));
+        double *Z = (double *)calloc((size_t)P * d_t, sizeof(double));
+        double tr = 0.0;
+        for (int i = 0; i < P; ++i) tr += Gm[(int64_t)i * P + i];
+        const double lam = lambda_relative ? lambda * tr / (double)P : lambda;
+        int bad = 0;
+        for (int i = 0; i < P && !bad; ++i) {
+            for (int j = 0; j <= i; ++j) {
+                double s = Gm[(int64_t)i * P + j];
+                if (i == j && !(bias_unpenalized && i == P - 1)) s += lam;
+                for (int k = 0; k < j; ++k) s -= L[(int64_t)i * P + k] * L[(int64_t)j * P + k];
+                if (i == j) {
+                    if (!(s > 0.0) || !isfinite(s)) { bad = i + 1; break; }
+                    L[(int64_t)i * P + i] = sqrt(s);
+                } else {
+                    L[(int64_t)i * P + j] = s / L[(int64_t)j * P + j];
+                }
+            }
+        }
+        info[m] = bad;
+        if (bad) {
+            memset(Wm, 0, sizeof(double) * (size_t)P * d_t);
+        } else {
+            for (int c = 0; c < d_t; ++c) {
+                for (int i = 0; i < P; ++i) {          /* forward: L z = c */
+                    double s = Cm[(int64_t)i * d_t + c];
+                    for (int k = 0; k < i; ++k) s -= L[(int64_t)i * P + k] * Z[(int64_t)k * d_t + c];
+                    Z[(int64_t)i * d_t + c] = s / L[(int64_t)i * P + i];
+                }
+                for (int i = P - 1; i >= 0; --i) {     /* backward: L^T w = z */
+                    double s = Z[(int64_t)i * d_t + c];
+                    for (int k = i + 1; k < P; ++k) s -= L[(int64_t)k * P + i] * Wm[(int64_t)k * d_t + c];
+                    Wm[(int64_t)i * d_t + c] = s / L[(int64_t)i * P + i];
+                }
+            }
+        }
+        free(L);
+        free(Z);
+    }
+    return 0;
+}
+
+/*
+ * Online application of the fitted maps.
+ *   W [n_maps][P][d_t] (fp64 copies of the coefficients; row d_s is the bias)
+ *   out[tgt_layer, kv, seq, tgt_head, tok, j] = RNE_bf16( sum_k x~_k W[k][j] )
+ * for every token of every sequence.  Returns 0.
+ */
+int oracle_apply(int n_maps,
+                 const int32_t *tgt_layer, const int32_t *tgt_head, const int32_t *kv,
+                 const int32_t *src_layer, const int32_t *src_head,
+                 const double *W,
+                 const uint16_t *src, const int64_t *src_strides, int d_s,
+                 uint16_t *out, const int64_t *out_strides, int d_t,
+                 int n_seqs, int seq_len, int n_threads) {
+    const int P = d_s + 1;
+    set_threads(n_threads);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int m = 0; m < n_maps; ++m) {
+        const double *Wm = W + (int64_t)m * P * d_t;
+        double *xt = (double *)malloc(sizeof(double) * (size_t)P);
+        for (int b = 0; b < n_seqs; ++b) {
+            for (int t = 0; t < seq_len; ++t) {
+                const uint16_t *xr = src + row_offset(src_strides, src_layer[m], kv[m], b, src_head[m], t);
+                uint16_t *orow = out + row_offset(out_strides, tgt_layer[m], kv[m], b, tgt_head[m], t);
+                for (int i = 0; i < d_s; ++i) xt[i] = bf16_bits_to_double(xr[i]);
+                xt[d_s] = 1.0;
+                for (int j = 0; j < d_t; ++j) {
+                    double s = 0.0;
+                    for (int k = 0; k < P; ++k) s += xt[k] * Wm[(int64_t)k * d_t + j];
+                    orow[j] = oracle_double_to_bf16(s);
+                }
+            }
+        }
+        free(xt);
+    }
+    return 0;
+}
+
+/* Element-wise oracle_double_to_bf16 over n values.  Returns 0. */
+int oracle_double_to_bf16_array(int64_t n, const double *v, uint16_t *out) {
+    for (int64_t i = 0; i < n; ++i) out[i] = oracle_double_to_bf16(v[i]);
+    return 0;
+}

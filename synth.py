@@ -1,0 +1,272 @@
+"""Seeded synthetic workloads for the CacheBridge mapper path.
+
+This module only *generates inputs*: KV-cache-shaped tensors, calibration
+weights, head maps and planted affine maps.  It holds none of the method's
+arithmetic (no moments, no solve, no application) and is shared by the tests,
+the benchmark and the oracle checks, which is its only role.
+
+The real inputs of the paper (Qwen3 14B/32B traces over FineWeb-Edu, Sec. 4.1)
+are not available; these stand-ins take the paper's shapes (8 KV heads x 128
+dims, a 64-layer target, fp32 maps) and the structure each workload below names.
+
+Workloads (``WORKLOADS``):
+
+* ``tiny``  -- src 1x2x64, tgt 1x2x64, identity head map, 4 seqs x 256 tokens,
+  x ~ N(0,1), y = xA + b + 0.05 N(0,1), w ~ lognormal(0,1) mean-one.
+* ``qwen50`` -- Qwen3-14B->32B-shaped: src 40x8x128, tgt 64x8x128, 1024 maps,
+  src_layer = round(l*39/63), same head; 50 seqs x 2048 tokens; per-channel
+  lognormal(0,1) scales with 4 outlier channels x20; y = xA + b + 0.1 N(0,1);
+  weights = causal-attention column mass of Gaussian q, k with a position-0
+  sink (logit bonus 4 on key 0), mean-one.
+* ``qwen500`` -- as ``qwen50`` with 500 seqs, streamed as 5 batches of 100.
+* ``mismatch`` -- src 26x8x96, tgt 40x4x128, src_head = 2h,
+  src_layer = round(l*25/39); 200 seqs x 4096 tokens; w = exp(2z)/sqrt(t+1)
+  mean-one.
+* ``apply`` -- maps [1024][129][128] fp32 (planted, ``qwen`` statistics) applied
+  to a sender cache of 8 x 32768 tokens x 40 layers x 8 heads x 128.
+
+Cache layout everywhere: ``[layer][kv][seq][head][tok][dim]`` bfloat16.
+Weights: fp32 ``[row][seq * seq_len + tok]``; row = tgt_layer * H_t + tgt_head
+(one row per target head, shared by K and V).  Map order:
+``m = (tgt_layer * 2 + kv) * H_t + tgt_head``.
+
+Seeding: master seed 0; every draw has its own generator keyed by
+(workload, tensor, indices), so results do not depend on chunking.
+"""
+from __future__ import annotations
+
+import dataclasses
+import hashlib
+import math
+from typing import Dict, Optional
+
+import numpy as np
+import torch
+
+MASTER_SEED = 0
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    L_s: int
+    H_s: int
+    d_s: int
+    L_t: int
+    H_t: int
+    d_t: int
+    n_seqs: int
+    seq_len: int
+    head_map_kind: str          # "identity" | "qwen" | "mismatch"
+    source_kind: str            # "gauss" | "scaled"
+    noise: float
+    weight_kind: str            # "lognormal" | "colmass" | "decay"
+    lam_rel: float = 1e-2
+    batch_seqs: Optional[int] = None   # streamed batch size (None = all at once)
+
+    @property
+    def P(self) -> int:
+        return self.d_s + 1
+
+    @property
+    def n_maps(self) -> int:
+        return 2 * self.L_t * self.H_t
+
+    @property
+    def n_weight_rows(self) -> int:
+        return self.L_t * self.H_t
+
+    def with_(self, **kw) -> "Workload":
+        return dataclasses.replace(self, **kw)
+
+
+WORKLOADS: Dict[str, Workload] = {
+    "tiny": Workload("tiny", 1, 2, 64, 1, 2, 64, 4, 256, "identity", "gauss", 0.05, "lognormal"),
+    "qwen50": Workload("qwen50", 40, 8, 128, 64, 8, 128, 50, 2048, "qwen", "scaled", 0.1, "colmass"),
+    "qwen500": Workload("qwen500", 40, 8, 128, 64, 8, 128, 500, 2048, "qwen", "scaled", 0.1, "colmass",
+                        batch_seqs=100),
+    "mismatch": Workload("mismatch", 26, 8, 96, 40, 4, 128, 200, 4096, "mismatch", "scaled", 0.1, "decay"),
+}
+
+# Online application workload: maps from the qwen shapes, sender 8 x 32768.
+APPLY = Workload("apply", 40, 8, 128, 64, 8, 128, 8, 32768, "qwen", "scaled", 0.1, "colmass")
+
+SINK_LOGIT = 4.0          # position-0 sink strength for the column-mass weights
+N_OUTLIERS = 4            # outlier channels per (source layer, kv, head)
+OUTLIER_SCALE = 20.0
+
+
+def _seed(*key) -> int:
+    h = hashlib.sha256(("|".join(str(k) for k in (MASTER_SEED,) + key)).encode()).digest()
+    return int.from_bytes(h[:8], "little") & ((1 << 63) - 1)
+
+
+def _gen(device, *key) -> torch.Generator:
+    g = torch.Generator(device=device)
+    g.manual_seed(_seed(*key))
+    return g
+
+
+def _round_ratio(l: int, num: int, den: int) -> int:
+    """round(l * num / den) in exact integer arithmetic (no ties occur for the
+    ratios used here: a tie would need an even number to equal an odd one)."""
+    return (2 * l * num + den) // (2 * den)
+
+
+def head_map(wl: Workload) -> Dict[str, np.ndarray]:
+    """Per-map (tgt_layer, tgt_head, kv, src_layer, src_head, weight_row), int32."""
+    rows = {k: [] for k in ("tgt_layer", "tgt_head", "kv", "src_layer", "src_head", "weight_row")}
+    for l in range(wl.L_t):
+        for z in range(2):
+            for h in range(wl.H_t):
+                if wl.head_map_kind == "identity":
+                    sl, sh = l, h
+                elif wl.head_map_kind == "qwen":
+                    sl, sh = _round_ratio(l, wl.L_s - 1, wl.L_t - 1) if wl.L_t > 1 else 0, h
+                elif wl.head_map_kind == "mismatch":
+                    sl, sh = _round_ratio(l, wl.L_s - 1, wl.L_t - 1) if wl.L_t > 1 else 0, 2 * h
+                elif wl.head_map_kind.startswith("cyclic"):
+                    shift = int(wl.head_map_kind[len("cyclic"):])
+                    sl, sh = (_round_ratio(l, wl.L_s - 1, wl.L_t - 1) if wl.L_t > 1 else 0,
+                              (h + shift) % wl.H_s)
+                else:
+                    raise ValueError(wl.head_map_kind)
+                rows["tgt_layer"].append(l)
+                rows["tgt_head"].append(h)
+                rows["kv"].append(z)
+                rows["src_layer"].append(sl)
+                rows["src_head"].append(sh)
+                rows["weight_row"].append(l * wl.H_t + h)
+    return {k: np.asarray(v, dtype=np.int32) for k, v in rows.items()}
+
+
+def cache_strides(L: int, H: int, n_seqs: int, seq_len: int, d: int):
+    """Element strides (layer, kv, seq, head, tok) of the canonical layout."""
+    s_tok = d
+    s_head = seq_len * d
+    s_seq = H * s_head
+    s_kv = n_seqs * s_seq
+    s_layer = 2 * s_kv
+    return (s_layer, s_kv, s_seq, s_head, s_tok)
+
+
+def _channel_scales(wl: Workload, device) -> torch.Tensor:
+    """[L_s][2][H_s][d_s] fp32 per-channel scales: lognormal(0,1), 4 outliers x20."""
+    out = torch.empty((wl.L_s, 2, wl.H_s, wl.d_s), dtype=torch.float32, device=device)
+    for l in range(wl.L_s):
+        for z in range(2):
+            for g in range(wl.H_s):
+                gen = _gen(device, wl.name, "scale", l, z, g)
+                s = torch.exp(torch.randn(wl.d_s, generator=gen, device=device))
+                idx = torch.randperm(wl.d_s, generator=gen, device=device)[:N_OUTLIERS]
+                s[idx] *= OUTLIER_SCALE
+                out[l, z, g] = s
+    return out
+
+
+def gen_source(wl: Workload, seq0: int = 0, n_seqs: Optional[int] = None, seq_len: Optional[int] = None,
+               device="cpu", out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Source cache [L_s][2][B][H_s][T][d_s] bf16 for sequences seq0 .. seq0+B-1."""
+    B = wl.n_seqs if n_seqs is None else n_seqs
+    T = wl.seq_len if seq_len is None else seq_len
+    if out is None:
+        out = torch.empty((wl.L_s, 2, B, wl.H_s, T, wl.d_s), dtype=torch.bfloat16, device=device)
+    scales = _channel_scales(wl, device) if wl.source_kind == "scaled" else None
+    for l in range(wl.L_s):
+        for z in range(2):
+            for g in range(wl.H_s):
+                for b in range(B):
+                    gen = _gen(device, wl.name, "x", l, z, g, seq0 + b, T)
+                    x = torch.randn((T, wl.d_s), generator=gen, device=device, dtype=torch.float32)
+                    if scales is not None:
+                        x *= scales[l, z, g]
+                    out[l, z, b, g] = x.to(torch.bfloat16)
+    return out
+
+
+def planted_maps(wl: Workload, device="cpu") -> torch.Tensor:
+    """Planted affine maps [n_maps][P][d_t] fp32: rows 0..d_s-1 ~ N(0, 1/d_s), row d_s ~ N(0,1)."""
+    hm = head_map(wl)
+    n = hm["kv"].shape[0]
+    W = torch.empty((n, wl.P, wl.d_t), dtype=torch.float32, device=device)
+    for m in range(n):
+        gen = _gen(device, wl.name, "map", int(hm["tgt_layer"][m]), int(hm["kv"][m]), int(hm["tgt_head"][m]))
+        W[m, : wl.d_s] = torch.randn((wl.d_s, wl.d_t), generator=gen, device=device) / math.sqrt(wl.d_s)
+        W[m, wl.d_s] = torch.randn((wl.d_t,), generator=gen, device=device)
+    return W
+
+
+def gen_target(wl: Workload, src: torch.Tensor, seq0: int = 0, device="cpu",
+               out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Target cache [L_t][2][B][H_t][T][d_t] bf16: y = x A + b + noise * N(0,1) per map,
+    with x the mapped source row (bf16 values), computed in fp32 and rounded to bf16."""
+    B, T = src.shape[2], src.shape[4]
+    if out is None:
+        out = torch.empty((wl.L_t, 2, B, wl.H_t, T, wl.d_t), dtype=torch.bfloat16, device=device)
+    hm = head_map(wl)
+    W = planted_maps(wl, device=device)
+    for m in range(hm["kv"].shape[0]):
+        l, z, h = int(hm["tgt_layer"][m]), int(hm["kv"][m]), int(hm["tgt_head"][m])
+        sl, sh = int(hm["src_layer"][m]), int(hm["src_head"][m])
+        for b in range(B):
+            x = src[sl, z, b, sh].to(torch.float32)                       # [T, d_s]
+            gen = _gen(device, wl.name, "noise", l, z, h, seq0 + b, T)
+            e = torch.randn((T, wl.d_t), generator=gen, device=device, dtype=torch.float32)
+            y = torch.addmm(W[m, wl.d_s].unsqueeze(0), x, W[m, : wl.d_s]) + wl.noise * e
+            out[l, z, b, h] = y.to(torch.bfloat16)
+    return out
+
+
+def _column_mass(gen: torch.Generator, n: int, T: int, d: int, device) -> torch.Tensor:
+    """Causal softmax column mass of Gaussian q, k (n independent draws), with a
+    logit bonus on key 0.  Every query row sums to one, so the mean is one."""
+    q = torch.randn((n, T, d), generator=gen, device=device, dtype=torch.float32)
+    k = torch.randn((n, T, d), generator=gen, device=device, dtype=torch.float32)
+    s = torch.bmm(q, k.transpose(1, 2).contiguous()) * (1.0 / math.sqrt(d))
+    s[:, :, 0] += SINK_LOGIT
+    causal = torch.ones((T, T), dtype=torch.bool, device=device).triu(1)
+    s.masked_fill_(causal, float("-inf"))
+    a = torch.softmax(s, dim=-1)
+    return a.sum(dim=1)                                                  # [n, T]
+
+
+def gen_weights(wl: Workload, seq0: int = 0, n_seqs: Optional[int] = None, seq_len: Optional[int] = None,
+                device="cpu", out: Optional[torch.Tensor] = None, chunk: int = 16) -> torch.Tensor:
+    """Weights [R][B*T] fp32, non-negative, mean one per (row, sequence)."""
+    B = wl.n_seqs if n_seqs is None else n_seqs
+    T = wl.seq_len if seq_len is None else seq_len
+    R = wl.n_weight_rows
+    if out is None:
+        out = torch.empty((R, B * T), dtype=torch.float32, device=device)
+    for r in range(R):
+        if wl.weight_kind == "colmass":
+            for b0 in range(0, B, chunk):
+                nb = min(chunk, B - b0)
+                gen = _gen(device, wl.name, "colmass", r, seq0 + b0, nb, T)
+                m = _column_mass(gen, nb, T, wl.d_t, device)
+                m = m / m.mean(dim=1, keepdim=True)
+                out[r, b0 * T:(b0 + nb) * T] = m.reshape(-1)
+            continue
+        for b in range(B):
+            gen = _gen(device, wl.name, "w", r, seq0 + b, T)
+            z = torch.randn((T,), generator=gen, device=device, dtype=torch.float32)
+            if wl.weight_kind == "lognormal":
+                w = torch.exp(z)
+            elif wl.weight_kind == "decay":
+                t = torch.arange(T, device=device, dtype=torch.float32)
+                w = torch.exp(2.0 * z) / torch.sqrt(t + 1.0)
+            else:
+                raise ValueError(wl.weight_kind)
+            out[r, b * T:(b + 1) * T] = w / w.mean()
+    return out
+
+
+def gen_apply_source(wl: Workload = APPLY, n_seqs: Optional[int] = None, seq_len: Optional[int] = None,
+                     device="cpu", out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Sender cache for the online application workload (same recipe as the source cache)."""
+    return gen_source(wl, 0, n_seqs, seq_len, device=device, out=out)
+
+
+def bf16_bits(t: torch.Tensor) -> np.ndarray:
+    """Host uint16 copy of a bfloat16 tensor's bits."""
+    return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)

@@ -1,0 +1,501 @@
+"""Pins for the fp64 oracle, each against something other than the oracle itself.
+
+Citations are to the CacheBridge paper.  What pins what:
+
+* bf16 rounding      -- torch's float32->bfloat16 conversion (round to nearest even),
+                        hand-built ties, and doubles that sit just off a tie.
+* moments G, C        -- Sec. 3.4 Eq. fusedstats in augmented form: numpy matrix
+                        products for w == 1 and for general w, exact integer
+                        brute force, closed-form last row/column (sum w, sum w x,
+                        sum w y), symmetry, PSD, scaling, additivity over
+                        sequence splits, token-permutation invariance, and the
+                        head-local gather of Sec. 3.2 Eq. localfeature.
+* ridge solve         -- Sec. 3.1 Eq. closedform (centered weighted ridge,
+                        computed here from X, Y, w by numpy), brute-force
+                        minimality of the penalized objective, weighted least
+                        squares as lambda -> 0, lambda -> infinity asymptotics,
+                        exact planted-map recovery, d_eff <= P (Sec. 2.2 Eq.
+                        ridge-effective-dimension), scipy's dense solve, and the
+                        non-positive-definite report.
+* application         -- identity map copies bits, a pure bias gives RNE(b),
+                        a cyclic head assignment permutes outputs (Sec. 4.3),
+                        numpy fp64 products.
+* coefficient counts  -- numbers printed in the paper (tests/golden/paper_values.json).
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+import scipy.linalg
+import torch
+
+import oracle
+import synth
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "paper_values.json")
+
+
+# ----------------------------------------------------------------------------- helpers
+
+def to_bf16_bits(a) -> np.ndarray:
+    t = torch.as_tensor(np.asarray(a, dtype=np.float32)).to(torch.bfloat16)
+    return t.view(torch.int16).numpy().view(np.uint16)
+
+
+def bf16_val(bits) -> np.ndarray:
+    return oracle.bf16_to_double(bits)
+
+
+class Problem:
+    """Small explicit problem in the canonical [layer][kv][seq][head][tok][dim] layout."""
+
+    def __init__(self, rng, L_s=2, H_s=3, d_s=8, L_t=2, H_t=2, d_t=5, B=3, T=17,
+                 hm=None, values="gauss", wkind="lognormal"):
+        self.L_s, self.H_s, self.d_s, self.L_t, self.H_t, self.d_t, self.B, self.T = \
+            L_s, H_s, d_s, L_t, H_t, d_t, B, T
+        if values == "gauss":
+            xs = rng.standard_normal((L_s, 2, B, H_s, T, d_s)) * (1 + np.arange(H_s))[None, None, None, :, None, None]
+            ys = rng.standard_normal((L_t, 2, B, H_t, T, d_t)) + 3.0
+        else:  # small integers, exact in bf16 and in every fp64 sum
+            xs = rng.integers(-4, 5, size=(L_s, 2, B, H_s, T, d_s))
+            ys = rng.integers(-4, 5, size=(L_t, 2, B, H_t, T, d_t))
+        self.src = to_bf16_bits(xs)
+        self.tgt = to_bf16_bits(ys)
+        self.X = bf16_val(self.src)
+        self.Y = bf16_val(self.tgt)
+        if hm is None:
+            hm = {"tgt_layer": [], "tgt_head": [], "kv": [], "src_layer": [], "src_head": [], "weight_row": []}
+            for l in range(L_t):
+                for z in range(2):
+                    for h in range(H_t):
+                        hm["tgt_layer"].append(l)
+                        hm["tgt_head"].append(h)
+                        hm["kv"].append(z)
+                        hm["src_layer"].append((l + 1) % L_s)
+                        hm["src_head"].append((2 * h + 1) % H_s)
+                        hm["weight_row"].append(l * H_t + h)
+            hm = {k: np.asarray(v, np.int32) for k, v in hm.items()}
+        self.hm = hm
+        R = int(hm["weight_row"].max()) + 1
+        if wkind == "lognormal":
+            w = np.exp(rng.standard_normal((R, B * T)))
+        elif wkind == "ones":
+            w = np.ones((R, B * T))
+        else:
+            w = rng.choice([0.0, 0.5, 1.0, 2.0, 0.25], size=(R, B * T))
+        self.w = w.astype(np.float32)
+        self.src_strides = synth.cache_strides(L_s, H_s, B, T, d_s)
+        self.tgt_strides = synth.cache_strides(L_t, H_t, B, T, d_t)
+
+    @property
+    def n_maps(self):
+        return self.hm["kv"].shape[0]
+
+    def stats(self, w=None, src=None):
+        return oracle.stats(self.hm, self.src if src is None else src, self.src_strides, self.d_s,
+                            self.tgt, self.tgt_strides, self.d_t, self.w if w is None else w,
+                            self.B * self.T, self.B, self.T)
+
+    def design(self, m):
+        """X~ (n x P), Y (n x d_t), w (n) of map m, gathered with numpy indexing."""
+        hm = self.hm
+        x = self.X[hm["src_layer"][m], hm["kv"][m], :, hm["src_head"][m]].reshape(-1, self.d_s)
+        y = self.Y[hm["tgt_layer"][m], hm["kv"][m], :, hm["tgt_head"][m]].reshape(-1, self.d_t)
+        w = self.w[hm["weight_row"][m]].astype(np.float64)
+        xt = np.concatenate([x, np.ones((x.shape[0], 1))], axis=1)
+        return xt, y, w
+
+
+def relF(a, b):
+    return np.linalg.norm(np.asarray(a) - np.asarray(b)) / max(np.linalg.norm(np.asarray(b)), 1e-300)
+
+
+# ----------------------------------------------------------------------------- bf16 rounding
+
+def test_bf16_rne_matches_torch_on_float32_values():
+    rng = np.random.default_rng(1)
+    mags = np.concatenate([rng.standard_normal(20000) * 10.0 ** rng.integers(-40, 38, 20000),
+                           rng.standard_normal(2000) * 1e-39,          # bf16 subnormal range
+                           np.array([0.0, -0.0, 3.3895314e38, -3.3895314e38, 1.0, -2.0])])
+    f32 = mags.astype(np.float32)
+    f32 = f32[np.isfinite(f32)]
+    ours = oracle.double_to_bf16(f32.astype(np.float64))
+    ref = to_bf16_bits(f32)
+    assert np.array_equal(ours, ref)
+
+
+def test_bf16_rne_ties_and_double_rounding():
+    # 1 + 2^-8 is exactly halfway between 1 and 1 + 2^-7: ties go to the even (1.0).
+    assert oracle.double_to_bf16(1.0 + 2.0 ** -8)[()] == 0x3F80
+    # 1 + 3*2^-8 is halfway between 1+2^-7 (odd) and 1+2^-6 (even): rounds up.
+    assert oracle.double_to_bf16(1.0 + 3 * 2.0 ** -8)[()] == 0x3F82
+    # Just above the tie (not representable in float32): must round up, which a
+    # detour through float32 (that would land on the tie) gets wrong.
+    assert oracle.double_to_bf16(1.0 + 2.0 ** -8 + 2.0 ** -40)[()] == 0x3F81
+    assert oracle.double_to_bf16(-(1.0 + 2.0 ** -8 + 2.0 ** -40))[()] == 0xBF81
+    # Overflow past the largest finite bf16 -> inf; NaN stays NaN.
+    assert oracle.double_to_bf16(3.4e38)[()] == 0x7F80
+    assert (oracle.double_to_bf16(float("nan"))[()] & 0x7FC0) == 0x7FC0
+
+
+# ----------------------------------------------------------------------------- moments
+
+def test_stats_unit_weights_equal_plain_gram():
+    p = Problem(np.random.default_rng(2), wkind="ones")
+    G, C = p.stats()
+    for m in range(p.n_maps):
+        xt, y, _ = p.design(m)
+        np.testing.assert_allclose(G[m], xt.T @ xt, rtol=1e-12, atol=1e-9)
+        np.testing.assert_allclose(C[m], xt.T @ y, rtol=1e-12, atol=1e-9)
+
+
+def test_stats_weighted_equal_matrix_form_and_closed_form_entries():
+    p = Problem(np.random.default_rng(3))
+    G, C = p.stats()
+    P = p.d_s + 1
+    for m in range(p.n_maps):
+        xt, y, w = p.design(m)
+        np.testing.assert_allclose(G[m], (xt * w[:, None]).T @ xt, rtol=1e-12, atol=1e-9)
+        np.testing.assert_allclose(C[m], (xt * w[:, None]).T @ y, rtol=1e-12, atol=1e-9)
+        # last row / column: sum w, sum w x, sum w y
+        np.testing.assert_allclose(G[m][P - 1, P - 1], w.sum(), rtol=1e-13)
+        np.testing.assert_allclose(G[m][: P - 1, P - 1], (w[:, None] * xt[:, :-1]).sum(0), rtol=1e-12, atol=1e-10)
+        np.testing.assert_allclose(G[m][P - 1, : P - 1], (w[:, None] * xt[:, :-1]).sum(0), rtol=1e-12, atol=1e-10)
+        np.testing.assert_allclose(C[m][P - 1], (w[:, None] * y).sum(0), rtol=1e-12, atol=1e-10)
+
+
+def test_stats_exact_integer_brute_force():
+    rng = np.random.default_rng(4)
+    p = Problem(rng, d_s=4, d_t=3, B=2, T=5, values="int", wkind="dyadic")
+    G, C = p.stats()
+    for m in range(p.n_maps):
+        xt, y, w = p.design(m)
+        n = xt.shape[0]
+        # exact rational arithmetic: every value is a small integer or dyadic
+        for i in range(p.d_s + 1):
+            for j in range(p.d_s + 1):
+                exact = sum(float(w[t]) * int(xt[t, i]) * int(xt[t, j]) for t in range(n))
+                assert G[m][i, j] == exact
+            for j in range(p.d_t):
+                exact = sum(float(w[t]) * int(xt[t, i]) * int(y[t, j]) for t in range(n))
+                assert C[m][i, j] == exact
+
+
+def test_stats_symmetric_psd_and_scaling():
+    p = Problem(np.random.default_rng(5))
+    G, C = p.stats()
+    for m in range(p.n_maps):
+        np.testing.assert_allclose(G[m], G[m].T, rtol=1e-14, atol=1e-12)
+        ev = np.linalg.eigvalsh(0.5 * (G[m] + G[m].T))
+        assert ev.min() >= -1e-12 * np.trace(G[m])
+    G4, C4 = p.stats(w=p.w * 4.0)           # power of two: exact
+    assert np.array_equal(G4, 4.0 * G) and np.array_equal(C4, 4.0 * C)
+    G3, C3 = p.stats(w=(p.w.astype(np.float64) * 3.0).astype(np.float32))
+    assert relF(G3, 3.0 * G) < 1e-6 and relF(C3, 3.0 * C) < 1e-6
+
+
+def test_stats_additive_over_sequence_splits_and_accumulates():
+    p = Problem(np.random.default_rng(6), B=4)
+    G, C = p.stats()
+    half = 2
+    s = np.asarray(p.src_strides)
+    t = np.asarray(p.tgt_strides)
+    # The same buffers viewed from sequence 2 on: offset pointers, same strides.
+    src_b = p.src.reshape(-1)[half * s[2]:]
+    tgt_b = p.tgt.reshape(-1)[half * t[2]:]
+    w_a = np.ascontiguousarray(p.w[:, : half * p.T])
+    w_b = np.ascontiguousarray(p.w[:, half * p.T:])
+    Ga, Ca = oracle.stats(p.hm, p.src, p.src_strides, p.d_s, p.tgt, p.tgt_strides, p.d_t,
+                          w_a, half * p.T, half, p.T)
+    Gab, Cab = oracle.stats(p.hm, src_b, p.src_strides, p.d_s, tgt_b, p.tgt_strides, p.d_t,
+                            w_b, (p.B - half) * p.T, p.B - half, p.T, G=Ga.copy(), C=Ca.copy())
+    np.testing.assert_allclose(Gab, G, rtol=1e-12, atol=1e-9)
+    np.testing.assert_allclose(Cab, C, rtol=1e-12, atol=1e-9)
+
+
+def test_stats_token_permutation_invariance():
+    rng = np.random.default_rng(7)
+    p = Problem(rng, B=1, T=40)
+    G, C = p.stats()
+    perm = rng.permutation(p.T)
+    src = p.src.copy()
+    tgt = p.tgt.copy()
+    src[:, :, :, :, :, :] = p.src[:, :, :, :, perm, :]
+    tgt[:, :, :, :, :, :] = p.tgt[:, :, :, :, perm, :]
+    w = p.w[:, perm]
+    Gp, Cp = oracle.stats(p.hm, src, p.src_strides, p.d_s, tgt, p.tgt_strides, p.d_t, w, p.T, 1, p.T)
+    np.testing.assert_allclose(Gp, G, rtol=1e-12, atol=1e-9)
+    np.testing.assert_allclose(Cp, C, rtol=1e-12, atol=1e-9)
+
+
+def test_stats_head_local_gather_selects_the_mapped_source_head():
+    # Each source head has a very different scale, so reading a wrong head or
+    # layer changes G by orders of magnitude (Sec. 3.2 Eq. localfeature).
+    p = Problem(np.random.default_rng(8), L_s=3, H_s=4, L_t=3, H_t=2)
+    G, _ = p.stats()
+    for m in range(p.n_maps):
+        xt, _, w = p.design(m)
+        ref = (xt * w[:, None]).T @ xt
+        np.testing.assert_allclose(G[m], ref, rtol=1e-12, atol=1e-9)
+        for other in range(p.H_s):
+            if other != p.hm["src_head"][m]:
+                xo = p.X[p.hm["src_layer"][m], p.hm["kv"][m], :, other].reshape(-1, p.d_s)
+                assert abs(np.trace(G[m][:-1, :-1]) - (w[:, None] * xo * xo).sum()) > 1e-3 * np.trace(G[m])
+
+
+# ----------------------------------------------------------------------------- ridge solve
+
+def centered_closed_form(xt, y, w, lam):
+    """Sec. 3.1 Eq. closedform written from X, Y, w (weights rescaled to mean one)."""
+    n = xt.shape[0]
+    w = w * (n / w.sum())
+    x = xt[:, :-1]
+    xbar = (w[:, None] * x).sum(0) / n
+    ybar = (w[:, None] * y).sum(0) / n
+    xc, yc = x - xbar, y - ybar
+    Wh = np.linalg.solve((xc * w[:, None]).T @ xc + lam * np.eye(x.shape[1]), (xc * w[:, None]).T @ yc)
+    bh = ybar - xbar @ Wh
+    return Wh, bh
+
+
+def test_solve_bias_unpenalized_equals_paper_centered_ridge():
+    rng = np.random.default_rng(9)
+    p = Problem(rng, B=4, T=50)
+    # rescale weights to mean one per map row, as the paper assumes
+    p.w = (p.w / p.w.mean(axis=1, keepdims=True)).astype(np.float32)
+    G, C = p.stats()
+    lam = 0.37
+    W, info = oracle.ridge_solve(G, C, lam, relative=False, bias_unpenalized=True)
+    assert (info == 0).all()
+    for m in range(p.n_maps):
+        xt, y, w = p.design(m)
+        Wh, bh = centered_closed_form(xt, y, w, lam)
+        # the paper's centering uses n^-1 sum w x, equal to the true weighted
+        # mean only up to the float32 mean-one rescaling; compare at 1e-6
+        np.testing.assert_allclose(W[m][:-1], Wh, rtol=1e-6, atol=1e-8)
+        np.testing.assert_allclose(W[m][-1], bh, rtol=1e-6, atol=1e-8)
+
+
+def objective(Wt, xt, y, w, lam, bias_penalized):
+    r = y - xt @ Wt
+    pen = (Wt ** 2).sum() if bias_penalized else (Wt[:-1] ** 2).sum()
+    return float((w[:, None] * r * r).sum() + lam * pen)
+
+
+@pytest.mark.parametrize("unpen", [False, True])
+def test_solve_is_brute_force_minimizer(unpen):
+    rng = np.random.default_rng(10)
+    p = Problem(rng, d_s=5, d_t=3, B=2, T=30)
+    G, C = p.stats()
+    lam = 2.5
+    W, info = oracle.ridge_solve(G, C, lam, relative=False, bias_unpenalized=unpen)
+    assert (info == 0).all()
+    for m in range(p.n_maps):
+        xt, y, w = p.design(m)
+        j0 = objective(W[m], xt, y, w, lam, not unpen)
+        for _ in range(50):
+            d = rng.standard_normal(W[m].shape)
+            for eps in (1e-2, 1e-4):
+                assert objective(W[m] + eps * d, xt, y, w, lam, not unpen) > j0
+        # first-order optimality along coordinate directions (central differences)
+        h = 1e-5
+        for (i, j) in [(0, 0), (p.d_s, 1), (2, 2)]:
+            e = np.zeros_like(W[m])
+            e[i, j] = h
+            g = (objective(W[m] + e, xt, y, w, lam, not unpen) - objective(W[m] - e, xt, y, w, lam, not unpen)) / (2 * h)
+            assert abs(g) <= 1e-6 * max(1.0, j0)
+
+
+def test_solve_small_lambda_is_weighted_least_squares():
+    rng = np.random.default_rng(11)
+    p = Problem(rng, B=3, T=60)
+    G, C = p.stats()
+    W, info = oracle.ridge_solve(G, C, 1e-10, relative=False, bias_unpenalized=False)
+    for m in range(p.n_maps):
+        xt, y, w = p.design(m)
+        sw = np.sqrt(w)[:, None]
+        ref = np.linalg.lstsq(sw * xt, sw * y, rcond=None)[0]
+        np.testing.assert_allclose(W[m], ref, rtol=1e-7, atol=1e-8)
+
+
+def test_solve_matches_dense_library_solve_and_relative_lambda():
+    rng = np.random.default_rng(12)
+    p = Problem(rng)
+    G, C = p.stats()
+    P = p.d_s + 1
+    for unpen in (False, True):
+        W, info = oracle.ridge_solve(G, C, 1e-2, relative=True, bias_unpenalized=unpen)
+        for m in range(p.n_maps):
+            lam = 1e-2 * np.trace(G[m]) / P
+            D = np.eye(P)
+            if unpen:
+                D[-1, -1] = 0.0
+            ref = scipy.linalg.solve(G[m] + lam * D, C[m], assume_a="pos")
+            np.testing.assert_allclose(W[m], ref, rtol=1e-10, atol=1e-12)
+    # relative lambda makes the maps invariant to a rescaling of the weights
+    G7, C7 = p.stats(w=(p.w.astype(np.float64) * 7.0).astype(np.float32))
+    W1, _ = oracle.ridge_solve(G, C, 1e-2, relative=True)
+    W7, _ = oracle.ridge_solve(G7, C7, 1e-2, relative=True)
+    np.testing.assert_allclose(W7, W1, rtol=1e-5, atol=1e-7)
+
+
+def test_solve_recovers_planted_map_exactly():
+    rng = np.random.default_rng(13)
+    d_s, d_t, n = 6, 4, 400
+    Wstar = rng.choice([-1.0, -0.5, 0.0, 0.5, 1.0, 2.0], size=(d_s + 1, d_t))
+    x = rng.integers(-6, 7, size=(n, d_s)).astype(np.float64)
+    y = np.concatenate([x, np.ones((n, 1))], 1) @ Wstar          # small dyadics: exact in bf16
+    assert np.array_equal(bf16_val(to_bf16_bits(y)), y)
+    hm = {k: np.zeros(1, np.int32) for k in oracle.HEAD_MAP_FIELDS}
+    src = to_bf16_bits(x.reshape(1, 1, 1, 1, n, d_s))
+    tgt = to_bf16_bits(y.reshape(1, 1, 1, 1, n, d_t))
+    w = np.exp(rng.standard_normal((1, n))).astype(np.float32)
+    G, C = oracle.stats(hm, src, synth.cache_strides(1, 1, 1, n, d_s), d_s, tgt,
+                        synth.cache_strides(1, 1, 1, n, d_t), d_t, w, n, 1, n)
+    for unpen in (False, True):
+        W, info = oracle.ridge_solve(G, C, 1e-13, relative=True, bias_unpenalized=unpen)
+        assert info[0] == 0
+        np.testing.assert_allclose(W[0], Wstar, rtol=0, atol=1e-8)
+
+
+def test_solve_large_lambda_and_effective_dof():
+    rng = np.random.default_rng(14)
+    p = Problem(rng)
+    G, C = p.stats()
+    P = p.d_s + 1
+    lam = 1e9 * np.abs(G).max()
+    W, _ = oracle.ridge_solve(G, C, lam, relative=False, bias_unpenalized=False)
+    for m in range(p.n_maps):
+        assert relF(lam * W[m], C[m]) < 1e-6
+    # d_eff = tr[G (G + lam I)^-1] <= P  (solve with right-hand side G)
+    for lr in (1e-4, 1e-2, 1.0):
+        R, info = oracle.ridge_solve(G, G, lr, relative=True)
+        for m in range(p.n_maps):
+            d_eff = np.trace(R[m])
+            assert 0 < d_eff <= P + 1e-9
+            ev = np.linalg.eigvalsh(G[m])
+            lam_m = lr * np.trace(G[m]) / P
+            np.testing.assert_allclose(d_eff, (ev / (ev + lam_m)).sum(), rtol=1e-9)
+
+
+def test_solve_reports_non_positive_definite():
+    P, d_t = 5, 3
+    G = np.zeros((2, P, P))
+    C = np.zeros((2, P, d_t))
+    G[1] = np.eye(P)
+    G[1][2, 2] = -5.0                     # indefinite even after the ridge term
+    C[1] = 1.0
+    W, info = oracle.ridge_solve(G, C, 1e-2, relative=True)
+    assert info[0] == 1                    # all-zero weights: G = 0 and lambda = 0
+    assert info[1] == 3
+    assert not W.any()
+
+
+# ----------------------------------------------------------------------------- application
+
+def apply_problem(rng, d_s=8, d_t=8, hm_kind="identity"):
+    wl = synth.Workload("pin", 2, 4, d_s, 3, 4, d_t, 2, 11, hm_kind, "gauss", 0.1, "lognormal")
+    hm = synth.head_map(wl)
+    xs = rng.standard_normal((wl.L_s, 2, wl.n_seqs, wl.H_s, wl.seq_len, d_s)) * 3
+    src = to_bf16_bits(xs)
+    out = np.zeros((wl.L_t, 2, wl.n_seqs, wl.H_t, wl.seq_len, d_t), dtype=np.uint16)
+    return wl, hm, src, out
+
+
+def test_apply_identity_map_copies_bits():
+    rng = np.random.default_rng(15)
+    wl, hm, src, out = apply_problem(rng)
+    n = hm["kv"].shape[0]
+    W = np.zeros((n, wl.P, wl.d_t))
+    W[:, : wl.d_s, :] = np.eye(wl.d_s)
+    wl = wl.with_(head_map_kind="qwen")
+    hm = synth.head_map(wl)
+    oracle.apply(hm, W, src, synth.cache_strides(wl.L_s, wl.H_s, wl.n_seqs, wl.seq_len, wl.d_s), wl.d_s,
+                 out, synth.cache_strides(wl.L_t, wl.H_t, wl.n_seqs, wl.seq_len, wl.d_t), wl.d_t,
+                 wl.n_seqs, wl.seq_len)
+    for m in range(n):
+        a = out[hm["tgt_layer"][m], hm["kv"][m], :, hm["tgt_head"][m]]
+        b = src[hm["src_layer"][m], hm["kv"][m], :, hm["src_head"][m]]
+        assert np.array_equal(a, b)
+
+
+def test_apply_pure_bias_is_rounded_bias_and_matches_fp64_products():
+    rng = np.random.default_rng(16)
+    wl, hm, src, out = apply_problem(rng, d_s=6, d_t=5, hm_kind="qwen")
+    n = hm["kv"].shape[0]
+    ss = synth.cache_strides(wl.L_s, wl.H_s, wl.n_seqs, wl.seq_len, wl.d_s)
+    os_ = synth.cache_strides(wl.L_t, wl.H_t, wl.n_seqs, wl.seq_len, wl.d_t)
+    W = np.zeros((n, wl.P, wl.d_t))
+    bias = rng.standard_normal((n, wl.d_t)).astype(np.float32)
+    W[:, -1, :] = bias
+    oracle.apply(hm, W, src, ss, wl.d_s, out, os_, wl.d_t, wl.n_seqs, wl.seq_len)
+    for m in range(n):
+        a = out[hm["tgt_layer"][m], hm["kv"][m], :, hm["tgt_head"][m]]
+        assert (a == to_bf16_bits(bias[m])[None, None, :]).all()
+    # general maps against numpy fp64 products rounded by the pinned rounding
+    W = rng.standard_normal((n, wl.P, wl.d_t))
+    oracle.apply(hm, W, src, ss, wl.d_s, out, os_, wl.d_t, wl.n_seqs, wl.seq_len)
+    X = bf16_val(src)
+    for m in range(n):
+        x = X[hm["src_layer"][m], hm["kv"][m], :, hm["src_head"][m]]
+        xt = np.concatenate([x, np.ones(x.shape[:-1] + (1,))], -1)
+        ref = oracle.double_to_bf16(xt @ W[m])
+        assert np.array_equal(out[hm["tgt_layer"][m], hm["kv"][m], :, hm["tgt_head"][m]], ref)
+
+
+def test_apply_cyclic_head_assignment_permutes_outputs():
+    rng = np.random.default_rng(17)
+    wl, _, src, out0 = apply_problem(rng, hm_kind="qwen")
+    ss = synth.cache_strides(wl.L_s, wl.H_s, wl.n_seqs, wl.seq_len, wl.d_s)
+    os_ = synth.cache_strides(wl.L_t, wl.H_t, wl.n_seqs, wl.seq_len, wl.d_t)
+    hm0 = synth.head_map(wl)
+    hm1 = synth.head_map(wl.with_(head_map_kind="cyclic1"))
+    n = hm0["kv"].shape[0]
+    W = rng.standard_normal((n, wl.P, wl.d_t))
+    out1 = np.zeros_like(out0)
+    oracle.apply(hm0, W, src, ss, wl.d_s, out0, os_, wl.d_t, wl.n_seqs, wl.seq_len)
+    # shifting the source head by one with the maps moved along gives the
+    # outputs of the shifted heads
+    W1 = W.reshape(wl.L_t, 2, wl.H_t, wl.P, wl.d_t)
+    W1 = np.roll(W1, -1, axis=2).reshape(n, wl.P, wl.d_t)
+    oracle.apply(hm1, W1, src, ss, wl.d_s, out1, os_, wl.d_t, wl.n_seqs, wl.seq_len)
+    assert np.array_equal(np.roll(out1, 1, axis=3)[:, :, :, :], out0)
+
+
+# ----------------------------------------------------------------------------- paper values
+
+def test_coefficient_counts_reproduce_printed_sizes():
+    g = json.load(open(GOLDEN))
+    q = g["qwen3_14b_to_32b"]
+    local = oracle.coefficient_count(q["L_t"], q["H_t"], q["k"], 1, q["d_s"], q["d_t"])
+    full = oracle.coefficient_count(q["L_t"], q["H_t"], q["k"], q["H_s"], q["d_s"], q["d_t"])
+    assert local == 134_217_728
+    assert full // local == q["H_s"]                      # C_full / C_local = H_s (Sec. 3.2)
+    # fp32 coefficients: the printed sizes (3 decimals) are the coefficient bytes
+    # plus about 1 MB of per-map vectors (2 x 128 fp32 per map)
+    extra = 2 * q["L_t"] * q["H_t"] * 2 * q["d_t"] * 4
+    assert round((4 * local + extra) / 1e9, 3) == q["head_local_GB"]
+    assert round((4 * full + extra) / 1e9, 3) == q["full_head_GB"]
+    wd = g["input_widths"]
+    for k, f_w, l_w in zip(wd["k"], wd["full"], wd["local"]):
+        assert oracle.coefficient_count(1, 1, k, wd["H_s"], wd["d_s"], 1) // 2 == f_w
+        assert oracle.coefficient_count(1, 1, k, 1, wd["d_s"], 1) // 2 == l_w
+
+
+# ----------------------------------------------------------------------------- workload generators
+
+def test_generators_mean_one_weights_and_head_maps():
+    wl = synth.WORKLOADS["qwen50"]
+    hm = synth.head_map(wl)
+    assert hm["kv"].shape[0] == 1024
+    assert hm["src_layer"].max() == 39 and len(set(hm["src_layer"].tolist())) == 40
+    wm = synth.WORKLOADS["mismatch"]
+    hmm = synth.head_map(wm)
+    assert hmm["kv"].shape[0] == 320 and set(hmm["src_head"].tolist()) == {0, 2, 4, 6}
+    small = wl.with_(L_t=2, H_t=2, n_seqs=2, seq_len=128)
+    w = synth.gen_weights(small).numpy()
+    assert w.shape == (4, 256) and (w >= 0).all()
+    np.testing.assert_allclose(w.reshape(4, 2, 128).mean(-1), 1.0, rtol=1e-5)
+    # the sink makes position 0 the heaviest column
+    assert (w.reshape(4, 2, 128)[:, :, 0] > 10).all()
