@@ -1,0 +1,233 @@
+#!/usr/bin/env python3
+"""Benchmark of the CacheBridge mapper path on one MI355X.
+
+One step = one pass of the whole hot path on resident synthetic inputs:
+  * a 500-sequence statistics build in the Qwen3-14B->32B shape
+    (source 40 x 8 x 128, target 64 x 8 x 128, 1024 maps, 2048-token
+    sequences), streamed as 5 cb_stats_accumulate calls of 100 sequences
+    (the 438 GB of calibration rows do not fit in HBM at once, so one
+    resident 100-sequence batch is streamed five times per build);
+  * the 1024-system 129 x 129 ridge solve (cb_ridge_solve);
+  * the online application of the 1024 maps to a sender cache of
+    8 x 32768 tokens (cb_apply).
+Each leg is timed with HIP events on the stream the library launches on.
+
+Output: one JSON line.  value = calibration tokens per second of the
+construction (500 x 2048 tokens / (statistics + solve time)).
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "calib tokens/s + seconds per 500-seq stats build (14B→32B shape); apply GB/s"
+HBM_PEAK_GBPS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "stats_kernel_qwen500_traffic.json")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes_per_token(hm, d_s, d_t):
+    """Every used source row once, every target row once, every used weight row once."""
+    src_blocks = {(int(l), int(z), int(h)) for l, z, h in zip(hm["src_layer"], hm["kv"], hm["src_head"])}
+    n_maps = len(hm["kv"])
+    w_rows = len(set(int(r) for r in hm["weight_row"]))
+    return len(src_blocks) * d_s * 2 + n_maps * d_t * 2 + w_rows * 4
+
+
+def stats_kernel_sha():
+    h = hashlib.sha256()
+    for f in ("cb_stats.hip", "cb_internal.h"):
+        h.update(open(os.path.join(ROOT, "paper_2609_00891_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per statistics launch from committed rocprofv3 counters, if they
+    were taken on the current kernel source; else None."""
+    try:
+        t = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_sha") != stats_kernel_sha():
+        return None
+    return t.get("bytes_per_launch")
+
+
+def cpu_baseline(wl, src, tgt, w, hm, n_threads):
+    """The fp64 oracle, as it stands, on a bounded sample: every map over the
+    first sequence's first `tokens` tokens of the resident batch."""
+    import numpy as np
+    import oracle
+    import synth
+    tokens = int(os.environ.get("CB_CPU_SAMPLE_TOKENS", "1024"))
+    s = src[:, :, :1, :, :tokens].contiguous()
+    t = tgt[:, :, :1, :, :tokens].contiguous()
+    ww = w[:, :tokens].contiguous().cpu().numpy()
+    sb, tb = synth.bf16_bits(s), synth.bf16_bits(t)
+    t0 = time.perf_counter()
+    oracle.stats(hm, sb, s.stride()[:5], wl.d_s, tb, t.stride()[:5], wl.d_t, ww, tokens, 1, tokens,
+                 n_threads=n_threads)
+    dt = time.perf_counter() - t0
+    return {"value": tokens / dt, "unit": "calib tokens/s", "cores": n_threads, "kind": "oracle",
+            "sample": f"statistics of all {wl.n_maps} maps over {tokens} tokens of one sequence "
+                      f"(fp64 loops, OpenMP over maps); {dt:.2f} s",
+            "seconds": dt}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-apply", action="store_true", help=argparse.SUPPRESS)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); "
+              "the path is single-GPU by design (see DESIGN.md, 'Sharding').", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2609_00891_amd as cb
+    import synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    dev = "cuda"
+    wl = synth.WORKLOADS["qwen500"]
+    B = wl.batch_seqs
+    n_calls = wl.n_seqs // B
+    bw = wl.with_(n_seqs=B)
+    hm = synth.head_map(wl)
+    n, P = wl.n_maps, wl.P
+
+    log(f"generating resident batch: {B} x {wl.seq_len} tokens")
+    t0 = time.time()
+    src = synth.gen_source(bw, 0, device=dev)
+    tgt = synth.gen_target(bw, src, 0, device=dev)
+    w = synth.gen_weights(bw, 0, device=dev, chunk=50)
+    log(f"  done in {time.time() - t0:.1f} s")
+    aw = synth.APPLY
+    log(f"generating sender cache: {aw.n_seqs} x {aw.seq_len} tokens")
+    asrc = synth.gen_apply_source(aw, device=dev)
+    aout = torch.empty((aw.L_t, 2, aw.n_seqs, aw.H_t, aw.seq_len, aw.d_t), dtype=torch.bfloat16, device=dev)
+    torch.cuda.synchronize()
+    log(f"  done in {time.time() - t0:.1f} s")
+
+    plan = cb.cb_plan_create(hm, src, tgt, B * wl.seq_len)
+    G = torch.empty((n, P, P), dtype=torch.float32, device=dev)
+    C = torch.empty((n, P, wl.d_t), dtype=torch.float32, device=dev)
+    maps = torch.empty_like(C)
+    info = torch.empty((n,), dtype=torch.int32, device=dev)
+    flags = cb.CB_LAMBDA_RELATIVE | cb.CB_RIDGE_BIAS_UNPENALIZED
+    stream = torch.cuda.current_stream()
+
+    def ev():
+        return torch.cuda.Event(enable_timing=True)
+
+    def step(record):
+        e = [ev() for _ in range(n_calls + 4)]
+        e[n_calls + 3].record(stream)
+        cb.cb_stats_zero(plan, G, C)
+        e[0].record(stream)
+        for i in range(n_calls):
+            cb.cb_stats_accumulate(plan, src, tgt, w, G, C)
+            e[i + 1].record(stream)
+        cb.cb_ridge_solve(G, C, wl.lam_rel, flags, maps, info)
+        e[n_calls + 1].record(stream)
+        if not args.no_apply:
+            cb.cb_apply(plan, maps, asrc, aout)
+        e[n_calls + 2].record(stream)
+        if record is not None:
+            record.append(e)
+
+    for i in range(args.warmup):
+        step(None)
+    torch.cuda.synchronize()
+    log(f"timing {args.steps} steps")
+    rec = []
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    for i in range(args.steps):
+        step(rec)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    bad = int((info != 0).sum().item())
+    if bad:
+        log(f"WARNING: {bad} systems reported a non-positive pivot")
+
+    call_ms, solve_ms, apply_ms, step_ms = [], [], [], []
+    for e in rec:
+        for i in range(n_calls):
+            call_ms.append(e[i].elapsed_time(e[i + 1]))
+        solve_ms.append(e[n_calls].elapsed_time(e[n_calls + 1]))
+        apply_ms.append(e[n_calls + 1].elapsed_time(e[n_calls + 2]))
+        step_ms.append(e[n_calls + 3].elapsed_time(e[n_calls + 2]))
+    mean = lambda v: sum(v) / len(v)  # noqa: E731
+    med = lambda v: sorted(v)[len(v) // 2]  # noqa: E731
+    stats_build_ms = mean(step_ms) - mean(apply_ms) - mean(solve_ms)      # zero fill + 5 calls
+    build_s = (stats_build_ms + mean(solve_ms)) / 1e3
+    tokens_per_build = wl.n_seqs * wl.seq_len
+    bpt = algorithmic_bytes_per_token(hm, wl.d_s, wl.d_t)
+    bytes_per_call = bpt * B * wl.seq_len
+    call_s = mean(call_ms) / 1e3
+    achieved = bytes_per_call / call_s / 1e9
+    traffic = measured_traffic()
+    apply_bytes = (algorithmic_bytes_per_token(
+        {k: v for k, v in hm.items()}, aw.d_s, aw.d_t) - len(set(hm["weight_row"].tolist())) * 4) \
+        * aw.n_seqs * aw.seq_len + n * P * aw.d_t * 4
+    apply_gbps = apply_bytes / (mean(apply_ms) / 1e3) / 1e9 if not args.no_apply else None
+    flop_per_token = 2 * n * (P * P + P * wl.d_t)
+
+    res = {
+        "metric": METRIC,
+        "value": tokens_per_build / build_s,
+        "unit": "calib tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": mean(step_ms),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": "qwen3-14b->32b-shaped 500-seq build (5 x 100-seq resident batch, 2048 tok/seq, "
+                        "1024 maps, P=129) + 1024-system ridge solve + apply to 8 x 32768-token sender",
+            "src_cache": "40 layers x 8 KV heads x 128", "tgt_cache": "64 layers x 8 KV heads x 128",
+            "calib_tokens_per_build": tokens_per_build, "ridge": "lambda = 1e-2 tr(G)/P, bias unpenalized",
+        },
+        "s_per_500seq_build": build_s,
+        "apply_GBps": apply_gbps,
+        "legs_ms": {"stats_call_mean": mean(call_ms), "stats_call_median": med(call_ms),
+                    "stats_call_min": min(call_ms), "stats_call_max": max(call_ms),
+                    "stats_build": stats_build_ms, "solve": mean(solve_ms), "apply": mean(apply_ms)},
+        "wall_ms_per_step": t_wall * 1e3 / args.steps,
+        "roofline": {"bound": "hbm", "kernel": "stats_kernel (+ its partial-sum reduction) per 100-seq call",
+                     "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
+                     "traffic": traffic, "algorithmic_bytes_per_launch": bytes_per_call},
+        "apply_roofline": {"bound": "hbm", "achieved": apply_gbps, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                           "frac": (apply_gbps / HBM_PEAK_GBPS) if apply_gbps else None,
+                           "algorithmic_bytes_per_launch": apply_bytes},
+        "mfma": {"algorithmic_tflops": flop_per_token * B * wl.seq_len / call_s / 1e12, "peak_tflops": 2500.0},
+        "nonpositive_pivots": bad,
+    }
+    if not args.no_cpu_baseline:
+        n_threads = int(os.environ.get("OMP_NUM_THREADS", str(os.cpu_count() or 1)))
+        log(f"cpu baseline on {n_threads} threads")
+        res["cpu_baseline"] = cpu_baseline(bw, src, tgt, w, hm, n_threads)
+    plan.close()
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,186 @@
+/*
+ * cachebridge.h -- C ABI of the MI355X (gfx950) CacheBridge mapper library.
+ *
+ * The library builds and applies head-local affine ridge maps between the KV
+ * caches of a source model and a target model, following CacheBridge
+ * ("Efficient Cross-Model KV Cache Transfer"):
+ *
+ *   cb_stats_accumulate  weighted augmented sufficient statistics
+ *                        (Sec. 3.4, Eq. fusedstats; head-local support of
+ *                        Sec. 3.2, Eq. localfeature, one source layer per map)
+ *   cb_ridge_solve       batched ridge solve (Sec. 3.1, Eq. closedform; Sec. 3.4)
+ *   cb_apply             online application of the maps to a sender cache,
+ *                        writing a decode-ready target cache (Sec. 1 pipeline;
+ *                        Sec. 2.3, Eq. support-cost)
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Row vectors: a map is W~ = [W ; b^T], a P x d_t fp32 matrix with
+ *   P = d_s + 1 whose last row is the bias; the mapped row is [x, 1] W~.
+ * - Device memory: every data pointer (caches, weights, G, C, maps, info) is a
+ *   device pointer on the current HIP device, allocated and owned by the
+ *   caller.  The library never frees caller memory.  A plan owns its own
+ *   workspace, allocated in cb_plan_create and freed in cb_plan_destroy; no
+ *   other call allocates.
+ * - Streams: `stream` is a hipStream_t passed as void* (NULL = the null
+ *   stream).  Calls enqueue work and return without waiting.
+ * - Errors: argument, shape and alignment problems are found on the host,
+ *   before anything is enqueued, and returned as a cb_status; cb_last_error()
+ *   then returns a message for the calling thread.  A failed launch returns
+ *   CB_ERR_DEVICE.  Numerical failure of one ridge system is not a call error:
+ *   it is reported per map in `info` (LAPACK style).
+ * - Determinism: for a given plan, inputs and sequence of calls, results are
+ *   bitwise reproducible (fixed reduction order, no floating-point atomics).
+ * - Thread safety: a plan may be used by one thread / stream at a time.
+ * - Supported widths: d_s and d_t in {64, 96, 128} (P <= 129).  Cache rows are
+ *   bfloat16, channel stride 1, every row 16-byte aligned.
+ */
+#ifndef CACHEBRIDGE_H
+#define CACHEBRIDGE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    CB_OK = 0,
+    CB_ERR_INVALID_ARGUMENT = 1, /* null pointer, bad index, bad flag, duplicate map */
+    CB_ERR_SHAPE = 2,            /* geometry does not match the plan or the call  */
+    CB_ERR_MISALIGNED = 3,       /* a pointer or stride breaks 16-byte row alignment */
+    CB_ERR_OUT_OF_MEMORY = 4,    /* plan workspace allocation failed               */
+    CB_ERR_DEVICE = 5,           /* a HIP call or kernel launch failed             */
+    CB_ERR_UNSUPPORTED = 6       /* head width outside {64, 96, 128}, too many tokens */
+} cb_status;
+
+/*
+ * A KV cache of one model (Sec. 2.1: K and V per layer, token and KV head).
+ * Element (layer, kv, seq, head, tok, ch) lives at
+ *   data[layer*s_layer + kv*s_kv + seq*s_seq + head*s_head + tok*s_tok + ch]
+ * (kv 0 = K, 1 = V; strides in elements; channel stride 1).  The canonical
+ * layout is [layer][kv][seq][head][tok][ch].  `data` and every stride must
+ * keep each row 16-byte aligned (multiples of 8 elements).  The same struct
+ * describes inputs (read) and the output of cb_apply (written).
+ */
+typedef struct {
+    void *data;                 /* device memory, bfloat16 elements            */
+    int32_t n_layers;
+    int32_t n_heads;            /* KV heads                                     */
+    int32_t head_dim;
+    int32_t n_seqs;
+    int32_t seq_len;
+    int64_t s_layer, s_kv, s_seq, s_head, s_tok;
+} cb_cache;
+
+/*
+ * Mapper support (Sec. 2.1; Sec. 3.2 Eq. localfeature with k = 1): map m
+ * predicts target (tgt_layer[m], tgt_head[m], kv[m]) from source
+ * (src_layer[m], src_head[m], kv[m]) -- K from K, V from V -- using calibration
+ * weight row weight_row[m].  Host arrays of n_maps entries, read during
+ * cb_plan_create only.  Map m owns G[m], C[m] and maps[m].  Every target
+ * (layer, kv, head) may appear at most once.
+ */
+typedef struct {
+    int32_t n_maps;
+    const int32_t *tgt_layer;
+    const int32_t *tgt_head;
+    const int32_t *kv;
+    const int32_t *src_layer;
+    const int32_t *src_head;
+    const int32_t *weight_row;
+} cb_head_map;
+
+/* Validated head map, static gather schedule and workspace (opaque). */
+typedef struct cb_plan cb_plan;
+
+/* cb_ridge_solve flags. */
+#define CB_LAMBDA_RELATIVE 1u        /* lambda_m = lambda * trace(G_m) / P          */
+#define CB_RIDGE_BIAS_UNPENALIZED 2u /* no ridge on the bias row: Eq. closedform    */
+
+/*
+ * Compile the head map into a static gather schedule (Sec. 2.3: the support
+ * is fixed before fitting and can be compiled into a static gather schedule)
+ * and allocate the plan's workspace on the current device.
+ *   src_geom / tgt_geom: only n_layers, n_heads and head_dim are read.
+ *   max_tokens_per_call: upper bound on n_seqs * seq_len of any later
+ *     cb_stats_accumulate call (sizes the per-workgroup partial sums).
+ * Errors: CB_ERR_INVALID_ARGUMENT (null, index out of range, kv not 0/1,
+ * negative weight row, duplicate target), CB_ERR_UNSUPPORTED (head width),
+ * CB_ERR_OUT_OF_MEMORY, CB_ERR_DEVICE.  On error *out is set to NULL.
+ */
+cb_status cb_plan_create(const cb_head_map *map, const cb_cache *src_geom, const cb_cache *tgt_geom,
+                         int64_t max_tokens_per_call, cb_plan **out);
+
+/* Free the plan and its workspace (waits for the device).  NULL is accepted. */
+cb_status cb_plan_destroy(cb_plan *plan);
+
+/* Number of maps, source width d_s and target width d_t of a plan. */
+cb_status cb_plan_shape(const cb_plan *plan, int32_t *n_maps, int32_t *d_s, int32_t *d_t);
+
+/*
+ * Set G [n_maps][P][P] and C [n_maps][P][d_t] (fp32, row-major) to zero on
+ * `stream`, with a fill kernel (safe under stream capture).
+ */
+cb_status cb_stats_zero(const cb_plan *plan, float *G, float *C, void *stream);
+
+/*
+ * Add one batch of calibration tokens to the statistics (Sec. 3.4, Eq.
+ * fusedstats, in the augmented uncentered form that contains A_h, B_h and the
+ * weighted means):  for every map m and every token (seq, tok) of the batch,
+ *   x~ = [ src(src_layer, kv, seq, src_head, tok) ; 1 ]      (P = d_s + 1)
+ *   y  =   tgt(tgt_layer, kv, seq, tgt_head, tok)            (d_t)
+ *   w  =   weights[weight_row * w_row_stride + seq * seq_len + tok]   (fp32)
+ *   G[m] += w x~ x~^T      C[m] += w x~ y^T
+ * src and tgt must have the plan's layers / heads / widths and the same
+ * n_seqs and seq_len; n_seqs * seq_len <= max_tokens_per_call; 0 tokens is a
+ * no-op.  G is written exactly symmetric.  Weights are non-negative by the
+ * paper's definition (Sec. 3.1); NaN propagates.  Accuracy: products are
+ * formed from the exact bf16 inputs and an fp32 weight split into two bf16
+ * terms, summed in fp32 (relative Frobenius error ~1e-6 against fp64).
+ */
+cb_status cb_stats_accumulate(cb_plan *plan, const cb_cache *src, const cb_cache *tgt,
+                              const float *weights, int64_t w_row_stride,
+                              float *G, float *C, void *stream);
+
+/*
+ * Batched ridge solve (Sec. 3.1, Eq. closedform; Sec. 3.4):
+ *   maps[m] = (G[m] + lambda_m D)^{-1} C[m]
+ * G [n_maps][P][P], C [n_maps][P][d_t], maps [n_maps][P][d_t] (fp32,
+ * row-major), info [n_maps] (int32, device).  lambda_m = lambda, or
+ * lambda * trace(G[m]) / P with CB_LAMBDA_RELATIVE.  D = I by default (the
+ * bias row is penalized too); with CB_RIDGE_BIAS_UNPENALIZED the last
+ * diagonal entry of D is 0, which equals the paper's centered weighted ridge
+ * (weights rescaled to mean one).  Only the lower triangle of G is read.
+ * Cholesky in fp64, one workgroup per system.  info[m] = 0 on success, else
+ * the 1-based index of the first pivot that is not positive and finite, and
+ * maps[m] is zero-filled.  P in {65, 97, 129}, d_t in {64, 96, 128}.
+ */
+cb_status cb_ridge_solve(int32_t n_maps, int32_t P, int32_t d_t, const float *G, const float *C,
+                         float lambda, uint32_t flags, float *maps, int32_t *info, void *stream);
+
+/*
+ * Online mapping (Sec. 1 pipeline; Sec. 2.3 Eq. support-cost): for every map
+ * m of the plan and every token of the sender cache,
+ *   tgt_out(tgt_layer, kv, seq, tgt_head, tok, :) =
+ *       RNE_bf16( [ src(src_layer, kv, seq, src_head, tok) , 1 ] maps[m] )
+ * maps [n_maps][P][d_t] fp32 (bias in the last row).  src has the plan's source
+ * geometry, tgt_out its target geometry, both with the same n_seqs and
+ * seq_len.  Target positions not named by any map are left untouched.  The
+ * coefficients are split into two bf16 terms and products accumulate in fp32,
+ * then the bias is added and the sum is rounded once to bfloat16.
+ */
+cb_status cb_apply(cb_plan *plan, const float *maps, const cb_cache *src, const cb_cache *tgt_out,
+                   void *stream);
+
+/* Static name of a status code. */
+const char *cb_status_string(cb_status status);
+
+/* Message describing the last error returned to the calling thread ("" if none). */
+const char *cb_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CACHEBRIDGE_H */

@@ -1,0 +1,217 @@
+"""Python binding of libcachebridge (CacheBridge mapper path on MI355X / gfx950).
+
+Argument marshalling only: every step of the path runs in the HIP kernels of
+``libcachebridge.so`` behind the C ABI of ``include/cachebridge.h``.  torch
+tensors are used only as device memory (``data_ptr``/``stride``) and for the
+current HIP stream.  The functions keep the C names:
+
+* :func:`cb_plan_create` / :func:`cb_plan_destroy`
+* :func:`cb_stats_zero`, :func:`cb_stats_accumulate` -- augmented weighted moments
+  G, C (CacheBridge Sec. 3.4, Eq. fusedstats)
+* :func:`cb_ridge_solve` -- (G + lambda D)^-1 C (Sec. 3.1, Eq. closedform)
+* :func:`cb_apply` -- online application of the maps (Sec. 1; Sec. 2.3)
+
+Caches are bfloat16 tensors indexed ``[layer][kv][seq][head][tok][dim]`` (any
+strides with a unit channel stride).  Importing this package fails if the
+library has not been built: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Mapping, Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libcachebridge.so")
+
+CB_LAMBDA_RELATIVE = 1
+CB_RIDGE_BIAS_UNPENALIZED = 2
+
+STATUS_NAMES = {0: "CB_OK", 1: "CB_ERR_INVALID_ARGUMENT", 2: "CB_ERR_SHAPE", 3: "CB_ERR_MISALIGNED",
+                4: "CB_ERR_OUT_OF_MEMORY", 5: "CB_ERR_DEVICE", 6: "CB_ERR_UNSUPPORTED"}
+
+HEAD_MAP_FIELDS = ("tgt_layer", "tgt_head", "kv", "src_layer", "src_head", "weight_row")
+
+
+class CbCache(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("n_layers", ctypes.c_int32), ("n_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("n_seqs", ctypes.c_int32), ("seq_len", ctypes.c_int32),
+                ("s_layer", ctypes.c_int64), ("s_kv", ctypes.c_int64), ("s_seq", ctypes.c_int64),
+                ("s_head", ctypes.c_int64), ("s_tok", ctypes.c_int64)]
+
+
+_i32p = ctypes.POINTER(ctypes.c_int32)
+
+
+class CbHeadMap(ctypes.Structure):
+    _fields_ = [("n_maps", ctypes.c_int32)] + [(f, _i32p) for f in HEAD_MAP_FIELDS]
+
+
+class CacheBridgeError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        self.status = status
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
+
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python -c 'import __graft_entry__ as g; g.build()'`")
+
+_lib = ctypes.CDLL(LIB_PATH)
+_vp = ctypes.c_void_p
+_lib.cb_plan_create.restype = ctypes.c_int
+_lib.cb_plan_create.argtypes = [ctypes.POINTER(CbHeadMap), ctypes.POINTER(CbCache), ctypes.POINTER(CbCache),
+                                ctypes.c_int64, ctypes.POINTER(_vp)]
+_lib.cb_plan_destroy.restype = ctypes.c_int
+_lib.cb_plan_destroy.argtypes = [_vp]
+_lib.cb_plan_shape.restype = ctypes.c_int
+_lib.cb_plan_shape.argtypes = [_vp, _i32p, _i32p, _i32p]
+_lib.cb_stats_zero.restype = ctypes.c_int
+_lib.cb_stats_zero.argtypes = [_vp, _vp, _vp, _vp]
+_lib.cb_stats_accumulate.restype = ctypes.c_int
+_lib.cb_stats_accumulate.argtypes = [_vp, ctypes.POINTER(CbCache), ctypes.POINTER(CbCache), _vp, ctypes.c_int64,
+                                     _vp, _vp, _vp]
+_lib.cb_ridge_solve.restype = ctypes.c_int
+_lib.cb_ridge_solve.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp, _vp, ctypes.c_float,
+                                ctypes.c_uint32, _vp, _vp, _vp]
+_lib.cb_apply.restype = ctypes.c_int
+_lib.cb_apply.argtypes = [_vp, _vp, ctypes.POINTER(CbCache), ctypes.POINTER(CbCache), _vp]
+_lib.cb_status_string.restype = ctypes.c_char_p
+_lib.cb_status_string.argtypes = [ctypes.c_int]
+_lib.cb_last_error.restype = ctypes.c_char_p
+_lib.cb_last_error.argtypes = []
+
+
+def library() -> ctypes.CDLL:
+    """The loaded libcachebridge handle."""
+    return _lib
+
+
+def cb_status_string(status: int) -> str:
+    return _lib.cb_status_string(int(status)).decode()
+
+
+def cb_last_error() -> str:
+    return _lib.cb_last_error().decode()
+
+
+def _check(status: int):
+    if status != 0:
+        raise CacheBridgeError(status, cb_last_error())
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream if torch.cuda.is_available() else None
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else t.data_ptr()
+
+
+def cache_view(t: Optional[torch.Tensor], n_layers=None, n_heads=None, head_dim=None) -> CbCache:
+    """Describe a [layer][kv][seq][head][tok][dim] bfloat16 tensor (any strides, unit channel stride)."""
+    c = CbCache()
+    if t is None:
+        c.n_layers, c.n_heads, c.head_dim = n_layers, n_heads, head_dim
+        return c
+    if t.dtype != torch.bfloat16 or t.dim() != 6 or t.shape[1] != 2:
+        raise ValueError("cache tensors are bfloat16 [layer][2][seq][head][tok][dim]")
+    if t.shape[5] > 1 and t.stride(5) != 1:
+        raise ValueError("cache channel stride must be 1")
+    L, _, B, H, T, d = t.shape
+    c.data = t.data_ptr()
+    c.n_layers, c.n_heads, c.head_dim, c.n_seqs, c.seq_len = L, H, d, B, T
+    c.s_layer, c.s_kv, c.s_seq, c.s_head, c.s_tok = t.stride(0), t.stride(1), t.stride(2), t.stride(3), t.stride(4)
+    return c
+
+
+class Plan:
+    """Owning handle of a cb_plan (validated head map, gather schedule, workspace)."""
+
+    def __init__(self, handle: int, n_maps: int, d_s: int, d_t: int, keep):
+        self.handle = handle
+        self.n_maps, self.d_s, self.d_t = n_maps, d_s, d_t
+        self.P = d_s + 1
+        self._keep = keep
+
+    def close(self):
+        if self.handle:
+            _check(_lib.cb_plan_destroy(self.handle))
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def cb_plan_create(head_map: Mapping[str, object], src_geom, tgt_geom, max_tokens_per_call: int) -> Plan:
+    """Compile ``head_map`` (six int arrays) for source/target geometries given as
+    ``(n_layers, n_heads, head_dim)`` tuples or cache tensors."""
+    import numpy as np  # noqa: PLC0415
+
+    arrays = [np.ascontiguousarray(np.asarray(head_map[f], dtype=np.int32)) for f in HEAD_MAP_FIELDS]
+    n = arrays[0].shape[0]
+    hm = CbHeadMap()
+    hm.n_maps = n
+    for f, a in zip(HEAD_MAP_FIELDS, arrays):
+        setattr(hm, f, a.ctypes.data_as(_i32p))
+
+    def geom(g):
+        if isinstance(g, torch.Tensor):
+            return cache_view(g)
+        return cache_view(None, *g)
+
+    sg, tg = geom(src_geom), geom(tgt_geom)
+    out = _vp()
+    _check(_lib.cb_plan_create(ctypes.byref(hm), ctypes.byref(sg), ctypes.byref(tg), int(max_tokens_per_call),
+                               ctypes.byref(out)))
+    nm, ds, dt = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    _check(_lib.cb_plan_shape(out.value, ctypes.byref(nm), ctypes.byref(ds), ctypes.byref(dt)))
+    return Plan(out.value, nm.value, ds.value, dt.value, arrays)
+
+
+def cb_plan_destroy(plan: Plan):
+    plan.close()
+
+
+def cb_stats_zero(plan: Plan, G: torch.Tensor, C: torch.Tensor, stream=None):
+    _check(_lib.cb_stats_zero(plan.handle, _ptr(G), _ptr(C), _stream(stream)))
+
+
+def cb_stats_accumulate(plan: Plan, src: torch.Tensor, tgt: torch.Tensor, weights: torch.Tensor,
+                        G: torch.Tensor, C: torch.Tensor, w_row_stride: Optional[int] = None, stream=None):
+    """G[m] += sum_t w x~ x~^T, C[m] += sum_t w x~ y^T over the batch (fp32 outputs)."""
+    if weights.dtype != torch.float32 or G.dtype != torch.float32 or C.dtype != torch.float32:
+        raise ValueError("weights, G and C are float32")
+    if w_row_stride is None:
+        w_row_stride = weights.stride(0) if weights.dim() == 2 else weights.numel()
+    sv, tv = cache_view(src), cache_view(tgt)
+    _check(_lib.cb_stats_accumulate(plan.handle, ctypes.byref(sv), ctypes.byref(tv), _ptr(weights),
+                                    int(w_row_stride), _ptr(G), _ptr(C), _stream(stream)))
+
+
+def cb_ridge_solve(G: torch.Tensor, C: torch.Tensor, lam: float, flags: int, maps: torch.Tensor,
+                   info: torch.Tensor, stream=None):
+    """maps[m] = (G[m] + lambda_m D)^-1 C[m]; info[m] = 0 or the first failing pivot (1-based)."""
+    n, P, P2 = G.shape
+    if P != P2 or C.shape[:2] != (n, P) or maps.shape != C.shape or info.shape != (n,):
+        raise ValueError("G [n][P][P], C/maps [n][P][d_t], info [n]")
+    if info.dtype != torch.int32:
+        raise ValueError("info is int32")
+    _check(_lib.cb_ridge_solve(n, P, C.shape[2], _ptr(G), _ptr(C), float(lam), int(flags), _ptr(maps), _ptr(info),
+                               _stream(stream)))
+
+
+def cb_apply(plan: Plan, maps: torch.Tensor, src: torch.Tensor, tgt_out: torch.Tensor, stream=None):
+    """tgt_out[l, z, b, h, t, :] = RNE_bf16([x, 1] maps[m]) for every map and token."""
+    if maps.dtype != torch.float32:
+        raise ValueError("maps are float32")
+    sv, ov = cache_view(src), cache_view(tgt_out)
+    _check(_lib.cb_apply(plan.handle, _ptr(maps), ctypes.byref(sv), ctypes.byref(ov), _stream(stream)))

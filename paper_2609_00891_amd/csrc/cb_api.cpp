@@ -1,0 +1,420 @@
+// cb_api.cpp -- host side of the C ABI declared in include/cachebridge.h.
+//
+// Validation happens here, before anything is enqueued.  cb_plan_create turns
+// the head map into the static gather schedule of the statistics kernel
+// (CacheBridge Sec. 2.3: the support is fixed before fitting and is compiled
+// into a static gather schedule) and into the source-block groups of the
+// application kernel, and allocates the plan's workspace.  No other call
+// allocates.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <map>
+#include <set>
+#include <string>
+#include <tuple>
+#include <vector>
+
+#include "cb_internal.h"
+
+struct cb_plan {
+    int device = 0;
+    int n_cu = 256;
+    int32_t n_maps = 0, L_s = 0, H_s = 0, d_s = 0, L_t = 0, H_t = 0, d_t = 0;
+    int64_t max_tokens = 0;
+    // statistics schedule
+    int32_t n_items = 0;
+    int32_t max_chunks = 1;
+    cb::StatsItem *d_items = nullptr;
+    int32_t *d_map_item = nullptr;
+    int32_t *d_map_slot = nullptr;
+    float *d_partials = nullptr;
+    // application schedule and split coefficients
+    int32_t n_groups = 0;
+    cb::ApplyGroup *d_groups = nullptr;
+    uint16_t *d_whi = nullptr;
+    uint16_t *d_wlo = nullptr;
+    float *d_bias = nullptr;
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+cb_status fail(cb_status s, const char *fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return s;
+}
+
+cb_status ok() {
+    g_last_error.clear();
+    return CB_OK;
+}
+
+bool supported_width(int d) { return d == 64 || d == 96 || d == 128; }
+
+// Chunking of a call's tokens: enough (item, chunk) work units to give every
+// compute unit several, chunks of whole 64-token tiles, and at most 64Ki
+// tokens per fp32 partial.
+void choose_chunks(int64_t N, int n_items, int n_cu, int *n_chunks, int *chunk_tokens) {
+    const int64_t KT = cb::kStatsTileTokens;
+    const int64_t tiles = (N + KT - 1) / KT;
+    if (tiles == 0) {
+        *n_chunks = 0;
+        *chunk_tokens = (int)KT;
+        return;
+    }
+    const int64_t target_units = 8LL * n_cu;
+    int64_t nc = (target_units + n_items - 1) / n_items;
+    nc = std::max<int64_t>(nc, (N + 65535) / 65536);
+    nc = std::min<int64_t>(nc, tiles);
+    nc = std::max<int64_t>(nc, 1);
+    const int64_t chunk_tiles = (tiles + nc - 1) / nc;
+    *chunk_tokens = (int)(chunk_tiles * KT);
+    *n_chunks = (int)((tiles + chunk_tiles - 1) / chunk_tiles);
+}
+
+cb_status check_device(const cb_plan *p) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return fail(CB_ERR_DEVICE, "hipGetDevice failed");
+    if (dev != p->device)
+        return fail(CB_ERR_INVALID_ARGUMENT, "plan was created on device %d but device %d is current", p->device, dev);
+    return CB_OK;
+}
+
+// Geometry and alignment of a cache used in a call.
+cb_status check_cache(const char *name, const cb_cache *c, int L, int H, int d) {
+    if (!c) return fail(CB_ERR_INVALID_ARGUMENT, "%s is NULL", name);
+    if (c->n_layers != L || c->n_heads != H || c->head_dim != d)
+        return fail(CB_ERR_SHAPE, "%s is %d layers x %d heads x %d, plan expects %d x %d x %d", name, c->n_layers,
+                    c->n_heads, c->head_dim, L, H, d);
+    if (c->n_seqs < 0 || c->seq_len < 0) return fail(CB_ERR_SHAPE, "%s has negative n_seqs or seq_len", name);
+    if ((int64_t)c->n_seqs * c->seq_len > 0 && !c->data) return fail(CB_ERR_INVALID_ARGUMENT, "%s->data is NULL", name);
+    const int64_t s[5] = {c->s_layer, c->s_kv, c->s_seq, c->s_head, c->s_tok};
+    for (int i = 0; i < 5; ++i) {
+        if (s[i] < 0) return fail(CB_ERR_SHAPE, "%s has a negative stride", name);
+        if (s[i] % 8 != 0) return fail(CB_ERR_MISALIGNED, "%s strides must be multiples of 8 elements (16 bytes)", name);
+    }
+    if (((uintptr_t)c->data) % 16 != 0) return fail(CB_ERR_MISALIGNED, "%s->data is not 16-byte aligned", name);
+    return CB_OK;
+}
+
+cb::Strides strides_of(const cb_cache *c) { return {c->s_layer, c->s_kv, c->s_seq, c->s_head, c->s_tok}; }
+
+}  // namespace
+
+extern "C" {
+
+const char *cb_status_string(cb_status s) {
+    switch (s) {
+        case CB_OK: return "CB_OK";
+        case CB_ERR_INVALID_ARGUMENT: return "CB_ERR_INVALID_ARGUMENT";
+        case CB_ERR_SHAPE: return "CB_ERR_SHAPE";
+        case CB_ERR_MISALIGNED: return "CB_ERR_MISALIGNED";
+        case CB_ERR_OUT_OF_MEMORY: return "CB_ERR_OUT_OF_MEMORY";
+        case CB_ERR_DEVICE: return "CB_ERR_DEVICE";
+        case CB_ERR_UNSUPPORTED: return "CB_ERR_UNSUPPORTED";
+    }
+    return "CB_ERR_UNKNOWN";
+}
+
+const char *cb_last_error(void) { return g_last_error.c_str(); }
+
+cb_status cb_plan_destroy(cb_plan *p) {
+    if (!p) return ok();
+    (void)hipDeviceSynchronize();
+    hipFree(p->d_items);
+    hipFree(p->d_map_item);
+    hipFree(p->d_map_slot);
+    hipFree(p->d_partials);
+    hipFree(p->d_groups);
+    hipFree(p->d_whi);
+    hipFree(p->d_wlo);
+    hipFree(p->d_bias);
+    delete p;
+    return ok();
+}
+
+cb_status cb_plan_create(const cb_head_map *map, const cb_cache *src_geom, const cb_cache *tgt_geom,
+                         int64_t max_tokens_per_call, cb_plan **out) {
+    if (!out) return fail(CB_ERR_INVALID_ARGUMENT, "out is NULL");
+    *out = nullptr;
+    if (!map || !src_geom || !tgt_geom) return fail(CB_ERR_INVALID_ARGUMENT, "map, src_geom and tgt_geom must be non-NULL");
+    if (map->n_maps <= 0) return fail(CB_ERR_INVALID_ARGUMENT, "n_maps must be positive (got %d)", map->n_maps);
+    if (!map->tgt_layer || !map->tgt_head || !map->kv || !map->src_layer || !map->src_head || !map->weight_row)
+        return fail(CB_ERR_INVALID_ARGUMENT, "every head map array must be non-NULL");
+    const int L_s = src_geom->n_layers, H_s = src_geom->n_heads, d_s = src_geom->head_dim;
+    const int L_t = tgt_geom->n_layers, H_t = tgt_geom->n_heads, d_t = tgt_geom->head_dim;
+    if (L_s <= 0 || H_s <= 0 || L_t <= 0 || H_t <= 0)
+        return fail(CB_ERR_SHAPE, "layer and head counts must be positive");
+    if (!supported_width(d_s) || !supported_width(d_t))
+        return fail(CB_ERR_UNSUPPORTED, "head widths must be 64, 96 or 128 (got d_s=%d, d_t=%d)", d_s, d_t);
+    if (max_tokens_per_call < 0 || max_tokens_per_call > (int64_t)INT32_MAX - 65536)
+        return fail(CB_ERR_UNSUPPORTED, "max_tokens_per_call must be in [0, 2^31 - 65537]");
+
+    const int n = map->n_maps;
+    std::set<std::tuple<int, int, int>> targets;
+    for (int m = 0; m < n; ++m) {
+        const int tl = map->tgt_layer[m], th = map->tgt_head[m], z = map->kv[m];
+        const int sl = map->src_layer[m], sh = map->src_head[m], wr = map->weight_row[m];
+        if (tl < 0 || tl >= L_t || th < 0 || th >= H_t)
+            return fail(CB_ERR_INVALID_ARGUMENT, "map %d: target (%d, %d) outside %d x %d", m, tl, th, L_t, H_t);
+        if (sl < 0 || sl >= L_s || sh < 0 || sh >= H_s)
+            return fail(CB_ERR_INVALID_ARGUMENT, "map %d: source (%d, %d) outside %d x %d", m, sl, sh, L_s, H_s);
+        if (z != 0 && z != 1) return fail(CB_ERR_INVALID_ARGUMENT, "map %d: kv must be 0 or 1 (got %d)", m, z);
+        if (wr < 0) return fail(CB_ERR_INVALID_ARGUMENT, "map %d: negative weight row", m);
+        if (!targets.insert(std::make_tuple(tl, z, th)).second)
+            return fail(CB_ERR_INVALID_ARGUMENT, "map %d: target (layer %d, kv %d, head %d) appears twice", m, tl, z, th);
+    }
+
+    cb_plan *p = new cb_plan();
+    if (hipGetDevice(&p->device) != hipSuccess) {
+        delete p;
+        return fail(CB_ERR_DEVICE, "hipGetDevice failed (no HIP device?)");
+    }
+    int ncu = 0;
+    if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, p->device) == hipSuccess && ncu > 0)
+        p->n_cu = ncu;
+    p->n_maps = n;
+    p->L_s = L_s; p->H_s = H_s; p->d_s = d_s;
+    p->L_t = L_t; p->H_t = H_t; p->d_t = d_t;
+    p->max_tokens = max_tokens_per_call;
+
+    // ---- group maps by source block, in order of first appearance
+    std::map<std::tuple<int, int, int>, int> gid;
+    std::vector<std::vector<int>> groups;
+    for (int m = 0; m < n; ++m) {
+        auto key = std::make_tuple(map->src_layer[m], map->kv[m], map->src_head[m]);
+        auto it = gid.find(key);
+        if (it == gid.end()) {
+            gid.emplace(key, (int)groups.size());
+            groups.push_back({m});
+        } else {
+            groups[it->second].push_back(m);
+        }
+    }
+
+    auto fill_slot = [&](cb::StatsItem &it, int s, int m) {
+        it.map[s] = m;
+        it.src_layer[s] = map->src_layer[m];
+        it.src_head[s] = map->src_head[m];
+        it.kv[s] = map->kv[m];
+        it.tgt_layer[s] = map->tgt_layer[m];
+        it.tgt_head[s] = map->tgt_head[m];
+        it.wrow[s] = map->weight_row[m];
+    };
+    std::vector<cb::StatsItem> items;
+    std::vector<int> singles;
+    for (const auto &g : groups) {
+        size_t i = 0;
+        for (; i + 1 < g.size(); i += 2) {
+            cb::StatsItem it = {};
+            it.n_slots = 2;
+            it.shared_x = 1;
+            fill_slot(it, 0, g[i]);
+            fill_slot(it, 1, g[i + 1]);
+            items.push_back(it);
+        }
+        if (i < g.size()) singles.push_back(g[i]);
+    }
+    for (size_t i = 0; i < singles.size(); i += 2) {
+        cb::StatsItem it = {};
+        fill_slot(it, 0, singles[i]);
+        if (i + 1 < singles.size()) {
+            it.n_slots = 2;
+            fill_slot(it, 1, singles[i + 1]);
+        } else {
+            it.n_slots = 1;
+            fill_slot(it, 1, singles[i]);   // unused slot mirrors slot 0 (never read)
+        }
+        it.shared_x = 0;
+        items.push_back(it);
+    }
+    p->n_items = (int)items.size();
+    std::vector<int32_t> map_item(n), map_slot(n);
+    for (int i = 0; i < p->n_items; ++i)
+        for (int s = 0; s < items[i].n_slots; ++s) {
+            map_item[items[i].map[s]] = i;
+            map_slot[items[i].map[s]] = s;
+        }
+    int nc = 1, ct = 64;
+    choose_chunks(std::max<int64_t>(max_tokens_per_call, 1), p->n_items, p->n_cu, &nc, &ct);
+    p->max_chunks = std::max(nc, 1);
+
+    std::vector<cb::ApplyGroup> agroups;
+    for (const auto &g : groups) {
+        for (size_t i = 0; i < g.size(); i += 2) {
+            cb::ApplyGroup ag = {};
+            ag.n_slots = (i + 1 < g.size()) ? 2 : 1;
+            ag.src_layer = map->src_layer[g[i]];
+            ag.src_head = map->src_head[g[i]];
+            ag.kv = map->kv[g[i]];
+            for (int s = 0; s < 2; ++s) {
+                const int m = g[std::min(i + s, g.size() - 1)];
+                ag.map[s] = m;
+                ag.tgt_layer[s] = map->tgt_layer[m];
+                ag.tgt_head[s] = map->tgt_head[m];
+            }
+            agroups.push_back(ag);
+        }
+    }
+    p->n_groups = (int)agroups.size();
+
+    // ---- device allocations
+    const int64_t slot_floats = cb::stats_slot_floats(d_s, d_t);
+    const size_t partial_bytes = (size_t)p->n_items * p->max_chunks * 2 * slot_floats * sizeof(float);
+    const size_t wsplit = (size_t)n * d_t * d_s * sizeof(uint16_t);
+    bool okm = hipMalloc(&p->d_items, sizeof(cb::StatsItem) * items.size()) == hipSuccess &&
+               hipMalloc(&p->d_map_item, sizeof(int32_t) * n) == hipSuccess &&
+               hipMalloc(&p->d_map_slot, sizeof(int32_t) * n) == hipSuccess &&
+               hipMalloc(&p->d_partials, partial_bytes) == hipSuccess &&
+               hipMalloc(&p->d_groups, sizeof(cb::ApplyGroup) * agroups.size()) == hipSuccess &&
+               hipMalloc(&p->d_whi, wsplit) == hipSuccess && hipMalloc(&p->d_wlo, wsplit) == hipSuccess &&
+               hipMalloc(&p->d_bias, sizeof(float) * n * d_t) == hipSuccess;
+    if (!okm) {
+        (void)hipGetLastError();
+        cb_plan_destroy(p);
+        return fail(CB_ERR_OUT_OF_MEMORY, "plan workspace allocation failed (%zu bytes of partial sums)", partial_bytes);
+    }
+    bool okc = hipMemcpy(p->d_items, items.data(), sizeof(cb::StatsItem) * items.size(), hipMemcpyHostToDevice) == hipSuccess &&
+               hipMemcpy(p->d_map_item, map_item.data(), sizeof(int32_t) * n, hipMemcpyHostToDevice) == hipSuccess &&
+               hipMemcpy(p->d_map_slot, map_slot.data(), sizeof(int32_t) * n, hipMemcpyHostToDevice) == hipSuccess &&
+               hipMemcpy(p->d_groups, agroups.data(), sizeof(cb::ApplyGroup) * agroups.size(), hipMemcpyHostToDevice) == hipSuccess;
+    if (!okc) {
+        cb_plan_destroy(p);
+        return fail(CB_ERR_DEVICE, "copying the schedule to the device failed");
+    }
+    *out = p;
+    return ok();
+}
+
+cb_status cb_plan_shape(const cb_plan *p, int32_t *n_maps, int32_t *d_s, int32_t *d_t) {
+    if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
+    if (n_maps) *n_maps = p->n_maps;
+    if (d_s) *d_s = p->d_s;
+    if (d_t) *d_t = p->d_t;
+    return ok();
+}
+
+cb_status cb_stats_zero(const cb_plan *p, float *G, float *C, void *stream) {
+    if (!p || !G || !C) return fail(CB_ERR_INVALID_ARGUMENT, "plan, G and C must be non-NULL");
+    if (cb_status s = check_device(p)) return s;
+    const int P = p->d_s + 1;
+    hipStream_t st = (hipStream_t)stream;
+    if (cb::launch_fill_zero(G, (int64_t)p->n_maps * P * P, st) != hipSuccess ||
+        cb::launch_fill_zero(C, (int64_t)p->n_maps * P * p->d_t, st) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "fill kernel launch failed");
+    return ok();
+}
+
+cb_status cb_stats_accumulate(cb_plan *p, const cb_cache *src, const cb_cache *tgt, const float *weights,
+                              int64_t w_row_stride, float *G, float *C, void *stream) {
+    if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
+    if (!G || !C) return fail(CB_ERR_INVALID_ARGUMENT, "G and C must be non-NULL");
+    if (cb_status s = check_cache("src", src, p->L_s, p->H_s, p->d_s)) return s;
+    if (cb_status s = check_cache("tgt", tgt, p->L_t, p->H_t, p->d_t)) return s;
+    if (src->n_seqs != tgt->n_seqs || src->seq_len != tgt->seq_len)
+        return fail(CB_ERR_SHAPE, "src and tgt disagree on n_seqs / seq_len");
+    const int64_t N = (int64_t)src->n_seqs * src->seq_len;
+    if (N > p->max_tokens)
+        return fail(CB_ERR_UNSUPPORTED, "call has %lld tokens, plan allows %lld", (long long)N, (long long)p->max_tokens);
+    if (N == 0) return ok();
+    if (!weights) return fail(CB_ERR_INVALID_ARGUMENT, "weights is NULL");
+    if (w_row_stride < N) return fail(CB_ERR_SHAPE, "w_row_stride (%lld) < tokens in the call (%lld)",
+                                      (long long)w_row_stride, (long long)N);
+    if (((uintptr_t)weights) % 4 || ((uintptr_t)G) % 4 || ((uintptr_t)C) % 4)
+        return fail(CB_ERR_MISALIGNED, "weights, G and C must be 4-byte aligned");
+    if (cb_status s = check_device(p)) return s;
+
+    cb::StatsArgs a = {};
+    a.src = (const uint16_t *)src->data;
+    a.tgt = (const uint16_t *)tgt->data;
+    a.w = weights;
+    a.ss = strides_of(src);
+    a.ts = strides_of(tgt);
+    a.w_row_stride = w_row_stride;
+    a.T = cb::make_fastdiv((uint32_t)src->seq_len);
+    a.N = (int32_t)N;
+    choose_chunks(N, p->n_items, p->n_cu, &a.n_chunks, &a.chunk_tokens);
+    if (a.n_chunks > p->max_chunks) return fail(CB_ERR_UNSUPPORTED, "internal: chunk count exceeds workspace");
+    a.n_items = p->n_items;
+    a.items = p->d_items;
+    a.partials = p->d_partials;
+    hipStream_t st = (hipStream_t)stream;
+    if (cb::launch_stats(p->d_s, p->d_t, a, st) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "statistics kernel launch failed");
+    cb::ReduceArgs r = {};
+    r.partials = p->d_partials;
+    r.map_item = p->d_map_item;
+    r.map_slot = p->d_map_slot;
+    r.n_items = p->n_items;
+    r.n_chunks = a.n_chunks;
+    r.n_maps = p->n_maps;
+    r.G = G;
+    r.C = C;
+    if (cb::launch_reduce(p->d_s, p->d_t, r, st) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "reduction kernel launch failed");
+    return ok();
+}
+
+cb_status cb_ridge_solve(int32_t n_maps, int32_t P, int32_t d_t, const float *G, const float *C, float lambda,
+                         uint32_t flags, float *maps, int32_t *info, void *stream) {
+    if (n_maps < 0) return fail(CB_ERR_INVALID_ARGUMENT, "n_maps is negative");
+    if (!supported_width(P - 1) || !supported_width(d_t))
+        return fail(CB_ERR_UNSUPPORTED, "P must be 65, 97 or 129 and d_t 64, 96 or 128 (got P=%d, d_t=%d)", P, d_t);
+    if (flags & ~(uint32_t)(CB_LAMBDA_RELATIVE | CB_RIDGE_BIAS_UNPENALIZED))
+        return fail(CB_ERR_INVALID_ARGUMENT, "unknown flag bits 0x%x", flags);
+    if (!std::isfinite(lambda) || lambda < 0.f) return fail(CB_ERR_INVALID_ARGUMENT, "lambda must be finite and >= 0");
+    if (n_maps == 0) return ok();
+    if (!G || !C || !maps || !info) return fail(CB_ERR_INVALID_ARGUMENT, "G, C, maps and info must be non-NULL");
+    if (((uintptr_t)G) % 4 || ((uintptr_t)C) % 4 || ((uintptr_t)maps) % 4 || ((uintptr_t)info) % 4)
+        return fail(CB_ERR_MISALIGNED, "G, C, maps and info must be 4-byte aligned");
+    if (cb::launch_solve(n_maps, P, d_t, G, C, lambda, flags, maps, info, (hipStream_t)stream) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "ridge solve launch failed");
+    return ok();
+}
+
+cb_status cb_apply(cb_plan *p, const float *maps, const cb_cache *src, const cb_cache *tgt_out, void *stream) {
+    if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
+    if (!maps) return fail(CB_ERR_INVALID_ARGUMENT, "maps is NULL");
+    if (cb_status s = check_cache("src", src, p->L_s, p->H_s, p->d_s)) return s;
+    if (cb_status s = check_cache("tgt_out", tgt_out, p->L_t, p->H_t, p->d_t)) return s;
+    if (src->n_seqs != tgt_out->n_seqs || src->seq_len != tgt_out->seq_len)
+        return fail(CB_ERR_SHAPE, "src and tgt_out disagree on n_seqs / seq_len");
+    if (((uintptr_t)maps) % 4) return fail(CB_ERR_MISALIGNED, "maps must be 4-byte aligned");
+    const int64_t N = (int64_t)src->n_seqs * src->seq_len;
+    if (N > (int64_t)INT32_MAX - 4096) return fail(CB_ERR_UNSUPPORTED, "too many tokens in one call");
+    if (cb_status s = check_device(p)) return s;
+    hipStream_t st = (hipStream_t)stream;
+    if (cb::launch_split_maps(p->n_maps, p->d_s, p->d_t, maps, p->d_whi, p->d_wlo, p->d_bias, st) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "map split launch failed");
+    if (N == 0) return ok();
+    cb::ApplyArgs a = {};
+    a.src = (const uint16_t *)src->data;
+    a.out = (uint16_t *)tgt_out->data;
+    a.ss = strides_of(src);
+    a.os = strides_of(tgt_out);
+    a.T = cb::make_fastdiv((uint32_t)src->seq_len);
+    a.N = (int32_t)N;
+    a.tile_tokens = 1024;
+    a.n_tiles = (int32_t)((N + a.tile_tokens - 1) / a.tile_tokens);
+    a.groups = p->d_groups;
+    a.w_hi = p->d_whi;
+    a.w_lo = p->d_wlo;
+    a.bias = p->d_bias;
+    if ((int64_t)p->n_groups * a.n_tiles > (int64_t)INT32_MAX)
+        return fail(CB_ERR_UNSUPPORTED, "too many application workgroups");
+    if (cb::launch_apply(p->d_s, p->d_t, p->n_groups, a, st) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "application kernel launch failed");
+    return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,108 @@
+// cb_internal.h -- structures shared by the host library and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "cachebridge.h"
+
+namespace cb {
+
+// One unit of the static gather schedule for the statistics: up to two maps
+// that are processed by one workgroup over a token range.  When both maps read
+// the same source block (a source layer feeding two target layers) the source
+// rows are loaded once ("shared").
+struct StatsItem {
+    int32_t n_slots;      // 1 or 2
+    int32_t shared_x;     // slot 1 reads slot 0's source rows
+    int32_t map[2];
+    int32_t src_layer[2], src_head[2], kv[2];
+    int32_t tgt_layer[2], tgt_head[2], wrow[2];
+};
+
+// One source block (src_layer, kv, src_head) and up to two target maps that
+// read it, for the online application.
+struct ApplyGroup {
+    int32_t n_slots;
+    int32_t src_layer, src_head, kv;
+    int32_t map[2];
+    int32_t tgt_layer[2], tgt_head[2];
+};
+
+struct Strides {
+    int64_t layer, kv, seq, head, tok;
+};
+
+// Exact unsigned division by a runtime constant d >= 1 (round-up multiplier
+// method of Granlund and Montgomery, "Division by invariant integers using
+// multiplication", 1994): q = (t + ((n - t) >> sh1)) >> sh2, t = mulhi(m, n).
+struct FastDiv {
+    uint32_t d, m, sh1, sh2;
+};
+
+inline FastDiv make_fastdiv(uint32_t d) {
+    uint32_t l = 0;
+    while ((1ull << l) < d) ++l;
+    FastDiv f;
+    f.d = d;
+    f.m = (uint32_t)((((1ull << 32) * ((1ull << l) - d)) / d) + 1);
+    f.sh1 = l > 0 ? 1u : 0u;
+    f.sh2 = l > 0 ? l - 1 : 0u;
+    return f;
+}
+
+struct StatsArgs {
+    const uint16_t *src;
+    const uint16_t *tgt;
+    const float *w;
+    Strides ss, ts;
+    int64_t w_row_stride;
+    FastDiv T;            // seq_len
+    int32_t N;            // tokens in this call (n_seqs * seq_len)
+    int32_t chunk_tokens; // multiple of the token tile
+    int32_t n_chunks;
+    int32_t n_items;
+    const StatsItem *items;
+    float *partials;      // [n_chunks * n_items][2][slot_floats]
+};
+
+struct ReduceArgs {
+    const float *partials;
+    const int32_t *map_item;  // [n_maps]
+    const int32_t *map_slot;  // [n_maps]
+    int32_t n_items, n_chunks, n_maps;
+    float *G, *C;
+};
+
+struct ApplyArgs {
+    const uint16_t *src;
+    uint16_t *out;
+    Strides ss, os;
+    FastDiv T;
+    int32_t N;            // tokens (n_seqs * seq_len)
+    int32_t tile_tokens;  // tokens per workgroup
+    int32_t n_tiles;      // per group
+    const ApplyGroup *groups;
+    const uint16_t *w_hi; // [n_maps][d_t][d_s] bf16, transposed maps
+    const uint16_t *w_lo;
+    const float *bias;    // [n_maps][d_t]
+};
+
+// Launchers (return hipError_t of the launch).
+hipError_t launch_stats(int d_s, int d_t, const StatsArgs &a, hipStream_t s);
+hipError_t launch_reduce(int d_s, int d_t, const ReduceArgs &a, hipStream_t s);
+hipError_t launch_fill_zero(float *p, int64_t n, hipStream_t s);
+hipError_t launch_solve(int32_t n_maps, int32_t P, int32_t d_t, const float *G, const float *C,
+                        float lambda, uint32_t flags, float *maps, int32_t *info, hipStream_t s);
+hipError_t launch_split_maps(int32_t n_maps, int32_t d_s, int32_t d_t, const float *maps,
+                             uint16_t *w_hi, uint16_t *w_lo, float *bias, hipStream_t s);
+hipError_t launch_apply(int d_s, int d_t, int n_groups, const ApplyArgs &a, hipStream_t s);
+
+// Geometry of the statistics kernel, shared with the host for workspace sizing.
+constexpr int kStatsTileTokens = 64;
+inline int64_t stats_slot_floats(int d_s, int d_t) {
+    const int rb = d_s / 32, rbt = d_t / 32;
+    return (int64_t)(rb * (rb + 1) / 2 + rb * rbt) * 1024 + (int64_t)(rb + rbt + 1) * 64;
+}
+
+}  // namespace cb

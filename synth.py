@@ -166,7 +166,8 @@ def _channel_scales(wl: Workload, device) -> torch.Tensor:
 
 def gen_source(wl: Workload, seq0: int = 0, n_seqs: Optional[int] = None, seq_len: Optional[int] = None,
                device="cpu", out: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """Source cache [L_s][2][B][H_s][T][d_s] bf16 for sequences seq0 .. seq0+B-1."""
+    """Source cache [L_s][2][B][H_s][T][d_s] bf16 for sequences seq0 .. seq0+B-1
+    (one generator per (layer, kv, head, batch))."""
     B = wl.n_seqs if n_seqs is None else n_seqs
     T = wl.seq_len if seq_len is None else seq_len
     if out is None:
@@ -175,12 +176,11 @@ def gen_source(wl: Workload, seq0: int = 0, n_seqs: Optional[int] = None, seq_le
     for l in range(wl.L_s):
         for z in range(2):
             for g in range(wl.H_s):
-                for b in range(B):
-                    gen = _gen(device, wl.name, "x", l, z, g, seq0 + b, T)
-                    x = torch.randn((T, wl.d_s), generator=gen, device=device, dtype=torch.float32)
-                    if scales is not None:
-                        x *= scales[l, z, g]
-                    out[l, z, b, g] = x.to(torch.bfloat16)
+                gen = _gen(device, wl.name, "x", l, z, g, seq0, B, T)
+                x = torch.randn((B, T, wl.d_s), generator=gen, device=device, dtype=torch.float32)
+                if scales is not None:
+                    x *= scales[l, z, g]
+                out[l, z, :, g] = x.to(torch.bfloat16)
     return out
 
 
@@ -208,12 +208,11 @@ def gen_target(wl: Workload, src: torch.Tensor, seq0: int = 0, device="cpu",
     for m in range(hm["kv"].shape[0]):
         l, z, h = int(hm["tgt_layer"][m]), int(hm["kv"][m]), int(hm["tgt_head"][m])
         sl, sh = int(hm["src_layer"][m]), int(hm["src_head"][m])
-        for b in range(B):
-            x = src[sl, z, b, sh].to(torch.float32)                       # [T, d_s]
-            gen = _gen(device, wl.name, "noise", l, z, h, seq0 + b, T)
-            e = torch.randn((T, wl.d_t), generator=gen, device=device, dtype=torch.float32)
-            y = torch.addmm(W[m, wl.d_s].unsqueeze(0), x, W[m, : wl.d_s]) + wl.noise * e
-            out[l, z, b, h] = y.to(torch.bfloat16)
+        x = src[sl, z, :, sh].reshape(B * T, wl.d_s).to(torch.float32)
+        gen = _gen(device, wl.name, "noise", l, z, h, seq0, B, T)
+        e = torch.randn((B * T, wl.d_t), generator=gen, device=device, dtype=torch.float32)
+        y = torch.addmm(W[m, wl.d_s].unsqueeze(0), x, W[m, : wl.d_s]).add_(e, alpha=wl.noise)
+        out[l, z, :, h] = y.reshape(B, T, wl.d_t).to(torch.bfloat16)
     return out
 
 
@@ -247,17 +246,16 @@ def gen_weights(wl: Workload, seq0: int = 0, n_seqs: Optional[int] = None, seq_l
                 m = m / m.mean(dim=1, keepdim=True)
                 out[r, b0 * T:(b0 + nb) * T] = m.reshape(-1)
             continue
-        for b in range(B):
-            gen = _gen(device, wl.name, "w", r, seq0 + b, T)
-            z = torch.randn((T,), generator=gen, device=device, dtype=torch.float32)
-            if wl.weight_kind == "lognormal":
-                w = torch.exp(z)
-            elif wl.weight_kind == "decay":
-                t = torch.arange(T, device=device, dtype=torch.float32)
-                w = torch.exp(2.0 * z) / torch.sqrt(t + 1.0)
-            else:
-                raise ValueError(wl.weight_kind)
-            out[r, b * T:(b + 1) * T] = w / w.mean()
+        gen = _gen(device, wl.name, "w", r, seq0, B, T)
+        z = torch.randn((B, T), generator=gen, device=device, dtype=torch.float32)
+        if wl.weight_kind == "lognormal":
+            w = torch.exp(z)
+        elif wl.weight_kind == "decay":
+            t = torch.arange(T, device=device, dtype=torch.float32)
+            w = torch.exp(2.0 * z) / torch.sqrt(t + 1.0)
+        else:
+            raise ValueError(wl.weight_kind)
+        out[r] = (w / w.mean(dim=1, keepdim=True)).reshape(-1)
     return out
 
 

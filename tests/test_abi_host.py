@@ -1,0 +1,94 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports every
+function declared in include/cachebridge.h, and rejects bad arguments on the host
+before touching a device."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "cachebridge.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(cb_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for required in ("cb_plan_create", "cb_plan_destroy", "cb_stats_zero", "cb_stats_accumulate",
+                     "cb_ridge_solve", "cb_apply", "cb_status_string", "cb_last_error"):
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol():
+    import paper_2609_00891_amd as cb
+    lib = cb.library()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+    # and nothing torch-typed: the library links only the HIP runtime
+    import subprocess
+    out = subprocess.run(["ldd", cb.LIB_PATH], capture_output=True, text=True).stdout
+    assert "libtorch" not in out and "libc10" not in out
+
+
+def test_status_strings():
+    import paper_2609_00891_amd as cb
+    for code, name in cb.STATUS_NAMES.items():
+        assert cb.cb_status_string(code) == name
+
+
+def _hm(n=2):
+    return {"tgt_layer": np.zeros(n, np.int32), "tgt_head": np.arange(n, dtype=np.int32),
+            "kv": np.zeros(n, np.int32), "src_layer": np.zeros(n, np.int32),
+            "src_head": np.arange(n, dtype=np.int32), "weight_row": np.arange(n, dtype=np.int32)}
+
+
+@pytest.mark.parametrize("mutate,status", [
+    (lambda h: h.update(kv=np.array([0, 2], np.int32)), "CB_ERR_INVALID_ARGUMENT"),
+    (lambda h: h.update(src_head=np.array([0, 9], np.int32)), "CB_ERR_INVALID_ARGUMENT"),
+    (lambda h: h.update(tgt_layer=np.array([0, -1], np.int32)), "CB_ERR_INVALID_ARGUMENT"),
+    (lambda h: h.update(weight_row=np.array([0, -3], np.int32)), "CB_ERR_INVALID_ARGUMENT"),
+    (lambda h: h.update(tgt_head=np.array([1, 1], np.int32)), "CB_ERR_INVALID_ARGUMENT"),   # duplicate target
+])
+def test_plan_create_rejects_bad_head_maps(mutate, status):
+    import paper_2609_00891_amd as cb
+    h = _hm()
+    mutate(h)
+    with pytest.raises(cb.CacheBridgeError) as e:
+        cb.cb_plan_create(h, (1, 2, 64), (1, 2, 64), 1024)
+    assert status in str(e.value)
+
+
+def test_plan_create_rejects_unsupported_widths_and_token_limits():
+    import paper_2609_00891_amd as cb
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_UNSUPPORTED"):
+        cb.cb_plan_create(_hm(), (1, 2, 80), (1, 2, 64), 1024)
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_UNSUPPORTED"):
+        cb.cb_plan_create(_hm(), (1, 2, 64), (1, 2, 256), 1024)
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_UNSUPPORTED"):
+        cb.cb_plan_create(_hm(), (1, 2, 64), (1, 2, 64), 2 ** 31)
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_INVALID_ARGUMENT"):
+        cb.cb_plan_create({k: v[:0] for k, v in _hm().items()}, (1, 2, 64), (1, 2, 64), 16)
+
+
+def test_null_arguments_are_rejected_before_any_launch():
+    import paper_2609_00891_amd as cb
+    lib = cb.library()
+    assert lib.cb_plan_create(None, None, None, 0, None) == 1
+    assert lib.cb_stats_accumulate(None, None, None, None, 0, None, None, None) == 1
+    assert lib.cb_apply(None, None, None, None, None) == 1
+    assert lib.cb_stats_zero(None, None, None, None) == 1
+    assert lib.cb_plan_destroy(None) == 0
+    # solve: unsupported sizes, bad flags, bad lambda -- all host-side
+    assert lib.cb_ridge_solve(4, 100, 128, None, None, ctypes.c_float(0.1), 0, None, None, None) == 6
+    assert lib.cb_ridge_solve(4, 129, 128, None, None, ctypes.c_float(0.1), 8, None, None, None) == 1
+    assert lib.cb_ridge_solve(4, 129, 128, None, None, ctypes.c_float(-1.0), 0, None, None, None) == 1
+    assert lib.cb_ridge_solve(4, 129, 128, None, None, ctypes.c_float(float("nan")), 1, None, None, None) == 1
+    assert lib.cb_ridge_solve(4, 129, 128, None, None, ctypes.c_float(0.1), 1, None, None, None) == 1
+    assert lib.cb_ridge_solve(0, 129, 128, None, None, ctypes.c_float(0.1), 1, None, None, None) == 0
+    assert "NULL" in cb.cb_last_error() or cb.cb_last_error() == ""

@@ -1,0 +1,355 @@
+"""GPU parity of libcachebridge against the fp64 oracle (MI355X / gfx950).
+
+Every call goes through the C ABI (via the thin binding).  Inputs are seeded
+synthetic workloads; the oracle always consumes the exact bits the GPU consumed,
+copied back from the device.  Tolerances (relative Frobenius error):
+G and C 1e-4, solved maps 1e-3, applied bf16 caches 1e-3 -- checked per map.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+TOL_STATS = 1e-4
+TOL_MAPS = 1e-3
+TOL_APPLY = 1e-3
+NTHREADS = min(16, os.cpu_count() or 1)
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def cb():
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    import paper_2609_00891_amd as cbmod
+    return cbmod
+
+
+@pytest.fixture(autouse=True)
+def _free_memory():
+    yield
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def relF(a, b):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
+
+
+def bits(t: torch.Tensor) -> np.ndarray:
+    return synth.bf16_bits(t)
+
+
+def make_inputs(wl, device="cuda", seq0=0):
+    src = synth.gen_source(wl, seq0, device=device)
+    tgt = synth.gen_target(wl, src, seq0, device=device)
+    w = synth.gen_weights(wl, seq0, device=device)
+    return src, tgt, w
+
+
+def gpu_stats(cb, plan, src, tgt, w, G=None, C=None):
+    n, P, dt = plan.n_maps, plan.P, plan.d_t
+    if G is None:
+        G = torch.empty((n, P, P), dtype=torch.float32, device="cuda")
+        C = torch.empty((n, P, dt), dtype=torch.float32, device="cuda")
+        cb.cb_stats_zero(plan, G, C)
+    cb.cb_stats_accumulate(plan, src, tgt, w, G, C)
+    torch.cuda.synchronize()
+    return G, C
+
+
+def compact(hm, sel, src, tgt, w):
+    """Host copies of the rows the sampled maps read, with a head map onto them."""
+    B, T = src.shape[2], src.shape[4]
+    xs = torch.stack([src[hm["src_layer"][m], hm["kv"][m], :, hm["src_head"][m]] for m in sel])
+    ys = torch.stack([tgt[hm["tgt_layer"][m], hm["kv"][m], :, hm["tgt_head"][m]] for m in sel])
+    ws = torch.stack([w[hm["weight_row"][m]] for m in sel]).cpu().numpy()
+    n = len(sel)
+    d_s, d_t = xs.shape[-1], ys.shape[-1]
+    xb = bits(xs).reshape(n, 1, B, 1, T, d_s)
+    yb = bits(ys).reshape(n, 1, B, 1, T, d_t)
+    chm = {"tgt_layer": np.arange(n, dtype=np.int32), "tgt_head": np.zeros(n, np.int32),
+           "kv": np.zeros(n, np.int32), "src_layer": np.arange(n, dtype=np.int32),
+           "src_head": np.zeros(n, np.int32), "weight_row": np.arange(n, dtype=np.int32)}
+    ss = (B * T * d_s, 0, T * d_s, 0, d_s)
+    ts = (B * T * d_t, 0, T * d_t, 0, d_t)
+    return chm, xb, ss, yb, ts, np.ascontiguousarray(ws), B, T
+
+
+def oracle_stats_sel(hm, sel, src, tgt, w):
+    chm, xb, ss, yb, ts, ws, B, T = compact(hm, sel, src, tgt, w)
+    return oracle.stats(chm, xb, ss, xb.shape[-1], yb, ts, yb.shape[-1], ws, B * T, B, T, n_threads=NTHREADS)
+
+
+def check_stats(G, C, Go, Co, sel, tol=TOL_STATS):
+    Gg = G[torch.as_tensor(sel, device=G.device)].double().cpu().numpy()
+    Cg = C[torch.as_tensor(sel, device=C.device)].double().cpu().numpy()
+    eg = max(relF(Gg[i], Go[i]) for i in range(len(sel)))
+    ec = max(relF(Cg[i], Co[i]) for i in range(len(sel)))
+    say(f"  stats parity: max relF G {eg:.3e}, C {ec:.3e}")
+    assert eg <= tol and ec <= tol
+    assert np.array_equal(Gg, np.transpose(Gg, (0, 2, 1))), "G must be exactly symmetric"
+    return eg, ec
+
+
+def gpu_solve(cb, G, C, lam=1e-2, flags=None):
+    if flags is None:
+        flags = cb.CB_LAMBDA_RELATIVE
+    maps = torch.empty_like(C)
+    info = torch.empty((G.shape[0],), dtype=torch.int32, device="cuda")
+    cb.cb_ridge_solve(G, C, lam, flags, maps, info)
+    torch.cuda.synchronize()
+    return maps, info
+
+
+# ----------------------------------------------------------------------------- small, all maps
+
+def test_tiny_end_to_end(cb):
+    wl = synth.WORKLOADS["tiny"]
+    say("tiny: generating")
+    src, tgt, w = make_inputs(wl)
+    hm = synth.head_map(wl)
+    plan = cb.cb_plan_create(hm, src, tgt, wl.n_seqs * wl.seq_len)
+    G, C = gpu_stats(cb, plan, src, tgt, w)
+    sel = list(range(wl.n_maps))
+    Go, Co = oracle_stats_sel(hm, sel, src, tgt, w)
+    check_stats(G, C, Go, Co, sel)
+    for flags, unpen in ((cb.CB_LAMBDA_RELATIVE, False),
+                         (cb.CB_LAMBDA_RELATIVE | cb.CB_RIDGE_BIAS_UNPENALIZED, True)):
+        maps, info = gpu_solve(cb, G, C, wl.lam_rel, flags)
+        assert (info.cpu().numpy() == 0).all()
+        Wo, io = oracle.ridge_solve(Go, Co, wl.lam_rel, relative=True, bias_unpenalized=unpen)
+        Wg = maps.double().cpu().numpy()
+        e = max(relF(Wg[i], Wo[i]) for i in sel)
+        # the solver alone, on the very fp32 moments the GPU produced
+        Ws, _ = oracle.ridge_solve(G.double().cpu().numpy(), C.double().cpu().numpy(), wl.lam_rel,
+                                   relative=True, bias_unpenalized=unpen)
+        es = max(relF(Wg[i], Ws[i]) for i in sel)
+        say(f"  maps parity (unpen={unpen}): end-to-end {e:.3e}, solver alone {es:.3e}")
+        assert e <= TOL_MAPS and es <= 1e-6
+    # apply the fitted maps back to the source cache
+    out = torch.zeros_like(tgt)
+    cb.cb_apply(plan, maps, src, out)
+    torch.cuda.synchronize()
+    ref = np.zeros(tuple(out.shape), dtype=np.uint16)
+    oracle.apply(hm, maps.double().cpu().numpy(), bits(src), src.stride()[:5], wl.d_s, ref, out.stride()[:5],
+                 wl.d_t, wl.n_seqs, wl.seq_len)
+    ob = bits(out).reshape(ref.shape)
+    e = relF(oracle.bf16_to_double(ob), oracle.bf16_to_double(ref))
+    same = float((ob == ref).mean())
+    say(f"  apply parity: relF {e:.3e}, bitwise-equal fraction {same:.6f}")
+    assert e <= TOL_APPLY and same > 0.999
+    plan.close()
+
+
+WIDTHS = [(ds, dt) for ds in (64, 96, 128) for dt in (64, 96, 128)]
+
+
+@pytest.mark.parametrize("d_s,d_t", WIDTHS)
+def test_widths_ragged_tokens_and_shared_sources(cb, d_s, d_t):
+    # 3 target layers over 2 source layers: some source blocks feed two maps
+    # (shared items), others one (paired singles); 3 x 45 tokens leave a
+    # ragged last tile and sequences that start inside a tile.
+    wl = synth.Workload("ragged", 2, 3, d_s, 3, 2, d_t, 3, 45, "cyclic1", "scaled", 0.1, "lognormal")
+    src, tgt, w = make_inputs(wl)
+    hm = synth.head_map(wl)
+    plan = cb.cb_plan_create(hm, src, tgt, 4096)
+    G, C = gpu_stats(cb, plan, src, tgt, w)
+    sel = list(range(wl.n_maps))
+    Go, Co = oracle_stats_sel(hm, sel, src, tgt, w)
+    check_stats(G, C, Go, Co, sel)
+    maps, info = gpu_solve(cb, G, C)
+    assert (info.cpu().numpy() == 0).all()
+    Wo, _ = oracle.ridge_solve(Go, Co, 1e-2, relative=True)
+    assert max(relF(maps[i].double().cpu().numpy(), Wo[i]) for i in sel) <= TOL_MAPS
+    out = torch.zeros_like(tgt)
+    cb.cb_apply(plan, maps, src, out)
+    torch.cuda.synchronize()
+    ref = np.zeros(tuple(out.shape), dtype=np.uint16)
+    oracle.apply(hm, maps.double().cpu().numpy(), bits(src), src.stride()[:5], d_s, ref, out.stride()[:5],
+                 d_t, wl.n_seqs, wl.seq_len)
+    ob = bits(out).reshape(ref.shape)
+    assert relF(oracle.bf16_to_double(ob), oracle.bf16_to_double(ref)) <= TOL_APPLY
+    plan.close()
+
+
+def test_strided_views_match_canonical_layout(cb):
+    wl = synth.Workload("strided", 2, 2, 128, 2, 2, 128, 2, 130, "qwen", "scaled", 0.1, "lognormal")
+    src, tgt, w = make_inputs(wl)
+    hm = synth.head_map(wl)
+    # the same values stored [L][2][H][B][T][d] and viewed as [L][2][B][H][T][d]
+    src_p = src.permute(0, 1, 3, 2, 4, 5).contiguous().permute(0, 1, 3, 2, 4, 5)
+    tgt_p = tgt.permute(0, 1, 3, 2, 4, 5).contiguous().permute(0, 1, 3, 2, 4, 5)
+    assert src_p.stride() != src.stride()
+    plan = cb.cb_plan_create(hm, src, tgt, 4096)
+    G1, C1 = gpu_stats(cb, plan, src, tgt, w)
+    G2, C2 = gpu_stats(cb, plan, src_p, tgt_p, w)
+    assert torch.equal(G1, G2) and torch.equal(C1, C2)
+    maps, _ = gpu_solve(cb, G1, C1)
+    o1 = torch.zeros_like(tgt)
+    o2 = torch.zeros_like(tgt_p)
+    cb.cb_apply(plan, maps, src, o1)
+    cb.cb_apply(plan, maps, src_p, o2)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2)
+    plan.close()
+
+
+def test_invariants_determinism_scaling_additivity(cb):
+    wl = synth.Workload("inv", 3, 2, 128, 4, 2, 128, 4, 300, "qwen", "scaled", 0.1, "lognormal")
+    src, tgt, w = make_inputs(wl)
+    hm = synth.head_map(wl)
+    plan = cb.cb_plan_create(hm, src, tgt, 4096)
+    G1, C1 = gpu_stats(cb, plan, src, tgt, w)
+    G2, C2 = gpu_stats(cb, plan, src, tgt, w)
+    assert torch.equal(G1, G2) and torch.equal(C1, C2), "bitwise run-to-run determinism"
+    G4, C4 = gpu_stats(cb, plan, src, tgt, w * 4.0)
+    assert torch.equal(G4, 4.0 * G1) and torch.equal(C4, 4.0 * C1), "power-of-two weight scaling is exact"
+    # additivity over sequence splits: two calls (seqs 0-1, 2-3) vs one
+    Ga, Ca = gpu_stats(cb, plan, src[:, :, :2], tgt[:, :, :2], w.view(-1, 4, 300)[:, :2].reshape(w.shape[0], -1))
+    Ga, Ca = gpu_stats(cb, plan, src[:, :, 2:], tgt[:, :, 2:], w.view(-1, 4, 300)[:, 2:].reshape(w.shape[0], -1),
+                       Ga, Ca)
+    assert relF(Ga.double().cpu(), G1.double().cpu()) < 1e-6
+    assert relF(Ca.double().cpu(), C1.double().cpu()) < 1e-6
+    # empty call is a no-op
+    Gb = G1.clone()
+    Cb = C1.clone()
+    cb.cb_stats_accumulate(plan, src[:, :, :0], tgt[:, :, :0], w[:, :0].contiguous(), Gb, Cb, w_row_stride=1)
+    torch.cuda.synchronize()
+    assert torch.equal(Gb, G1) and torch.equal(Cb, C1)
+    # all-zero weights: zero moments, relative lambda 0 -> first pivot fails
+    Gz, Cz = gpu_stats(cb, plan, src, tgt, torch.zeros_like(w))
+    assert not Gz.any() and not Cz.any()
+    maps, info = gpu_solve(cb, Gz, Cz)
+    assert (info.cpu().numpy() == 1).all() and not maps.any()
+    plan.close()
+
+
+def test_apply_identity_map_copies_and_bias_only(cb):
+    wl = synth.Workload("ident", 3, 2, 128, 5, 2, 128, 2, 77, "qwen", "scaled", 0.1, "lognormal")
+    src = synth.gen_source(wl, device="cuda")
+    hm = synth.head_map(wl)
+    plan = cb.cb_plan_create(hm, (wl.L_s, wl.H_s, wl.d_s), (wl.L_t, wl.H_t, wl.d_t), 1024)
+    n = wl.n_maps
+    maps = torch.zeros((n, wl.P, wl.d_t), dtype=torch.float32, device="cuda")
+    maps[:, :wl.d_s, :] = torch.eye(wl.d_s, device="cuda")
+    out = torch.zeros((wl.L_t, 2, wl.n_seqs, wl.H_t, wl.seq_len, wl.d_t), dtype=torch.bfloat16, device="cuda")
+    cb.cb_apply(plan, maps, src, out)
+    torch.cuda.synchronize()
+    for m in range(n):
+        a = out[hm["tgt_layer"][m], hm["kv"][m], :, hm["tgt_head"][m]]
+        b = src[hm["src_layer"][m], hm["kv"][m], :, hm["src_head"][m]]
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    bias = torch.randn((n, wl.d_t), device="cuda")
+    maps.zero_()
+    maps[:, wl.d_s, :] = bias
+    cb.cb_apply(plan, maps, src, out)
+    torch.cuda.synchronize()
+    for m in range(n):
+        a = out[hm["tgt_layer"][m], hm["kv"][m], :, hm["tgt_head"][m]]
+        assert torch.equal(a.view(torch.int16), bias[m].to(torch.bfloat16).expand_as(a).view(torch.int16))
+    plan.close()
+
+
+def test_device_side_argument_errors(cb):
+    wl = synth.Workload("err", 1, 2, 64, 1, 2, 64, 2, 64, "identity", "gauss", 0.1, "lognormal")
+    src, tgt, w = make_inputs(wl)
+    hm = synth.head_map(wl)
+    plan = cb.cb_plan_create(hm, src, tgt, 100)
+    G = torch.zeros((4, 65, 65), device="cuda")
+    C = torch.zeros((4, 65, 64), device="cuda")
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_UNSUPPORTED"):
+        cb.cb_stats_accumulate(plan, src, tgt, w, G, C)                  # 128 tokens > 100
+    flat = torch.zeros(src.numel() + 8, dtype=torch.bfloat16, device="cuda")
+    mis = flat[1:1 + src.numel()].view(src.shape)
+    plan2 = cb.cb_plan_create(hm, src, tgt, 4096)
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_MISALIGNED"):
+        cb.cb_stats_accumulate(plan2, mis, tgt, w, G, C)
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_SHAPE"):
+        cb.cb_stats_accumulate(plan2, src[:, :, :1], tgt, w, G, C)
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_SHAPE"):
+        cb.cb_stats_accumulate(plan2, src, tgt, w, G, C, w_row_stride=10)
+    plan.close()
+    plan2.close()
+
+
+# ----------------------------------------------------------------------------- full-size workloads
+
+def sample_maps(n, k, seed=0):
+    return sorted(np.random.default_rng(seed).choice(n, size=k, replace=False).tolist())
+
+
+def _full_size_stats(cb, wl, n_sample, seq0=0):
+    say(f"{wl.name}: generating {wl.n_seqs} x {wl.seq_len} tokens")
+    src, tgt, w = make_inputs(wl, seq0=seq0)
+    hm = synth.head_map(wl)
+    plan = cb.cb_plan_create(hm, src, tgt, wl.n_seqs * wl.seq_len)
+    say(f"{wl.name}: GPU statistics")
+    G, C = gpu_stats(cb, plan, src, tgt, w)
+    sel = sample_maps(wl.n_maps, n_sample)
+    say(f"{wl.name}: oracle on maps {sel}")
+    Go, Co = oracle_stats_sel(hm, sel, src, tgt, w)
+    check_stats(G, C, Go, Co, sel)
+    maps, info = gpu_solve(cb, G, C, wl.lam_rel, cb.CB_LAMBDA_RELATIVE | cb.CB_RIDGE_BIAS_UNPENALIZED)
+    assert (info.cpu().numpy() == 0).all()
+    Wo, _ = oracle.ridge_solve(Go, Co, wl.lam_rel, relative=True, bias_unpenalized=True, n_threads=NTHREADS)
+    e = max(relF(maps[m].double().cpu().numpy(), Wo[i]) for i, m in enumerate(sel))
+    say(f"  maps parity: {e:.3e}")
+    assert e <= TOL_MAPS
+    del src, tgt, w
+    plan.close()
+
+
+def test_qwen50_full_size_sampled_maps(cb):
+    _full_size_stats(cb, synth.WORKLOADS["qwen50"], 16)
+
+
+def test_qwen500_batch_full_size_sampled_maps(cb):
+    wl = synth.WORKLOADS["qwen500"]
+    _full_size_stats(cb, wl.with_(n_seqs=wl.batch_seqs), 8, seq0=0)
+
+
+def test_mismatch_full_size_sampled_maps(cb):
+    _full_size_stats(cb, synth.WORKLOADS["mismatch"], 4)
+
+
+def test_apply_full_size_sampled_tokens(cb):
+    wl = synth.APPLY
+    say("apply: generating sender cache 8 x 32768")
+    src = synth.gen_apply_source(wl, device="cuda")
+    hm = synth.head_map(wl)
+    maps = synth.planted_maps(wl, device="cuda")
+    plan = cb.cb_plan_create(hm, (wl.L_s, wl.H_s, wl.d_s), (wl.L_t, wl.H_t, wl.d_t), 1024)
+    out = torch.empty((wl.L_t, 2, wl.n_seqs, wl.H_t, wl.seq_len, wl.d_t), dtype=torch.bfloat16, device="cuda")
+    say("apply: GPU")
+    cb.cb_apply(plan, maps, src, out)
+    torch.cuda.synchronize()
+    Wd = maps.double().cpu().numpy()
+    for (b, t0, t1) in ((0, 0, 1536), (wl.n_seqs - 1, wl.seq_len - 1024, wl.seq_len)):
+        say(f"apply: oracle on batch row {b}, tokens {t0}..{t1}")
+        s_sub = src[:, :, b:b + 1, :, t0:t1].contiguous()
+        ref = np.zeros((wl.L_t, 2, 1, wl.H_t, t1 - t0, wl.d_t), dtype=np.uint16)
+        oracle.apply(hm, Wd, bits(s_sub), s_sub.stride()[:5], wl.d_s, ref,
+                     synth.cache_strides(wl.L_t, wl.H_t, 1, t1 - t0, wl.d_t), wl.d_t, 1, t1 - t0,
+                     n_threads=NTHREADS)
+        ob = bits(out[:, :, b:b + 1, :, t0:t1].contiguous()).reshape(ref.shape)
+        worst = 0.0
+        for m in range(wl.n_maps):
+            l, z, h = hm["tgt_layer"][m], hm["kv"][m], hm["tgt_head"][m]
+            worst = max(worst, relF(oracle.bf16_to_double(ob[l, z, 0, h]), oracle.bf16_to_double(ref[l, z, 0, h])))
+        same = float((ob == ref).mean())
+        say(f"  apply parity: worst per-map relF {worst:.3e}, bitwise-equal fraction {same:.6f}")
+        assert worst <= TOL_APPLY and same > 0.999
+    plan.close()
