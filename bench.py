@@ -62,24 +62,45 @@ def measured_traffic():
 
 
 def cpu_baseline(wl, src, tgt, w, hm, n_threads):
-    """The fp64 oracle, as it stands, on a bounded sample: every map over the
-    first sequence's first `tokens` tokens of the resident batch."""
-    import numpy as np
+    """The fp64 oracle, as it stands, on a bounded sample of the resident batch:
+    every map over the first `CB_CPU_SAMPLE_SEQS` full sequences."""
     import oracle
     import synth
-    tokens = int(os.environ.get("CB_CPU_SAMPLE_TOKENS", "1024"))
-    s = src[:, :, :1, :, :tokens].contiguous()
-    t = tgt[:, :, :1, :, :tokens].contiguous()
-    ww = w[:, :tokens].contiguous().cpu().numpy()
+    seqs = int(os.environ.get("CB_CPU_SAMPLE_SEQS", "16"))
+    T = wl.seq_len
+    s = src[:, :, :seqs].contiguous()
+    t = tgt[:, :, :seqs].contiguous()
+    ww = w[:, :seqs * T].contiguous().cpu().numpy()
     sb, tb = synth.bf16_bits(s), synth.bf16_bits(t)
+    del s, t
     t0 = time.perf_counter()
-    oracle.stats(hm, sb, s.stride()[:5], wl.d_s, tb, t.stride()[:5], wl.d_t, ww, tokens, 1, tokens,
+    oracle.stats(hm, sb, synth.cache_strides(wl.L_s, wl.H_s, seqs, T, wl.d_s), wl.d_s, tb,
+                 synth.cache_strides(wl.L_t, wl.H_t, seqs, T, wl.d_t), wl.d_t, ww, seqs * T, seqs, T,
                  n_threads=n_threads)
     dt = time.perf_counter() - t0
-    return {"value": tokens / dt, "unit": "calib tokens/s", "cores": n_threads, "kind": "oracle",
-            "sample": f"statistics of all {wl.n_maps} maps over {tokens} tokens of one sequence "
-                      f"(fp64 loops, OpenMP over maps); {dt:.2f} s",
+    return {"value": seqs * T / dt, "unit": "calib tokens/s", "cores": n_threads, "kind": "oracle",
+            "sample": f"statistics of all {wl.n_maps} maps over {seqs} sequences x {T} tokens of the "
+                      f"resident batch (fp64 loops, OpenMP over maps); {dt:.1f} s",
             "seconds": dt}
+
+
+def hbm_copy_probe(gib):
+    """A plain device-to-device copy of a known size (calibrates the HBM
+    byte counters of rocprofv3 against a kernel whose traffic is known)."""
+    import torch
+    n = int(gib * (1 << 30))
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty(n, dtype=torch.uint8, device="cuda")
+    a.fill_(1)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "ms": ms,
+                      "GBps_read_plus_write": 2 * n / ms / 1e6}), flush=True)
 
 
 def main():
@@ -89,11 +110,17 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-apply", action="store_true", help=argparse.SUPPRESS)
+    ap.add_argument("--hbm-copy-probe", type=float, default=None, metavar="GIB",
+                    help="only time a plain copy of GIB GiB (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); "
               "the path is single-GPU by design (see DESIGN.md, 'Sharding').", file=sys.stderr)
         sys.exit(2)
+
+    if args.hbm_copy_probe:
+        hbm_copy_probe(args.hbm_copy_probe)
+        return
 
     import torch
     import paper_2609_00891_amd as cb

@@ -104,6 +104,32 @@ def check_stats(G, C, Go, Co, sel, tol=TOL_STATS):
     return eg, ec
 
 
+def ulp_distance(a_bits, b_bits) -> np.ndarray:
+    """Distance in bf16 units in the last place between two bit arrays."""
+    def ordered(x):
+        x = x.astype(np.int32)
+        return np.where(x < 0x8000, x, 0x8000 - x)
+    return np.abs(ordered(a_bits) - ordered(b_bits))
+
+
+def check_apply(ob, ref, label=""):
+    """relF within the bar, and every element within one bf16 ulp of the oracle's
+    value plus 1e-4 of its map's RMS output (near-zero outputs see the ~2^-17
+    relative error of the split coefficients as several ulps).  Caches are
+    [layer][kv][seq][head][tok][dim]; a map is one (layer, kv, head) slice."""
+    g = oracle.bf16_to_double(ob)
+    r = oracle.bf16_to_double(ref)
+    e = relF(g, r)
+    rms = np.sqrt((r * r).mean(axis=(2, 4, 5), keepdims=True))
+    ulp = np.spacing(np.abs(r).astype(np.float32)).astype(np.float64) * 65536.0
+    bound = ulp + 1e-4 * rms
+    worst = float((np.abs(g - r) / bound).max())
+    same = float((ob == ref).mean())
+    say(f"  apply parity{label}: relF {e:.3e}, bitwise-equal {same:.6f}, worst err/bound {worst:.3f}")
+    assert e <= TOL_APPLY and worst <= 1.0
+    return e
+
+
 def gpu_solve(cb, G, C, lam=1e-2, flags=None):
     if flags is None:
         flags = cb.CB_LAMBDA_RELATIVE
@@ -146,11 +172,7 @@ def test_tiny_end_to_end(cb):
     ref = np.zeros(tuple(out.shape), dtype=np.uint16)
     oracle.apply(hm, maps.double().cpu().numpy(), bits(src), src.stride()[:5], wl.d_s, ref, out.stride()[:5],
                  wl.d_t, wl.n_seqs, wl.seq_len)
-    ob = bits(out).reshape(ref.shape)
-    e = relF(oracle.bf16_to_double(ob), oracle.bf16_to_double(ref))
-    same = float((ob == ref).mean())
-    say(f"  apply parity: relF {e:.3e}, bitwise-equal fraction {same:.6f}")
-    assert e <= TOL_APPLY and same > 0.999
+    check_apply(bits(out).reshape(ref.shape), ref)
     plan.close()
 
 
@@ -180,8 +202,7 @@ def test_widths_ragged_tokens_and_shared_sources(cb, d_s, d_t):
     ref = np.zeros(tuple(out.shape), dtype=np.uint16)
     oracle.apply(hm, maps.double().cpu().numpy(), bits(src), src.stride()[:5], d_s, ref, out.stride()[:5],
                  d_t, wl.n_seqs, wl.seq_len)
-    ob = bits(out).reshape(ref.shape)
-    assert relF(oracle.bf16_to_double(ob), oracle.bf16_to_double(ref)) <= TOL_APPLY
+    check_apply(bits(out).reshape(ref.shape), ref)
     plan.close()
 
 
@@ -349,7 +370,7 @@ def test_apply_full_size_sampled_tokens(cb):
         for m in range(wl.n_maps):
             l, z, h = hm["tgt_layer"][m], hm["kv"][m], hm["tgt_head"][m]
             worst = max(worst, relF(oracle.bf16_to_double(ob[l, z, 0, h]), oracle.bf16_to_double(ref[l, z, 0, h])))
-        same = float((ob == ref).mean())
-        say(f"  apply parity: worst per-map relF {worst:.3e}, bitwise-equal fraction {same:.6f}")
-        assert worst <= TOL_APPLY and same > 0.999
+        say(f"  worst per-map relF {worst:.3e}")
+        assert worst <= TOL_APPLY
+        check_apply(ob, ref, f" (row {b}, tokens {t0}..{t1})")
     plan.close()
