@@ -32,6 +32,7 @@ struct cb_plan {
     int32_t *d_map_item = nullptr;
     int32_t *d_map_slot = nullptr;
     float *d_partials = nullptr;
+    void *d_zero = nullptr;        // zero bytes: source of copies for absent tokens
     // application schedule and split coefficients
     int32_t n_groups = 0;
     cb::ApplyGroup *d_groups = nullptr;
@@ -135,6 +136,7 @@ cb_status cb_plan_destroy(cb_plan *p) {
     hipFree(p->d_map_item);
     hipFree(p->d_map_slot);
     hipFree(p->d_partials);
+    hipFree(p->d_zero);
     hipFree(p->d_groups);
     hipFree(p->d_whi);
     hipFree(p->d_wlo);
@@ -276,6 +278,7 @@ cb_status cb_plan_create(const cb_head_map *map, const cb_cache *src_geom, const
                hipMalloc(&p->d_map_item, sizeof(int32_t) * n) == hipSuccess &&
                hipMalloc(&p->d_map_slot, sizeof(int32_t) * n) == hipSuccess &&
                hipMalloc(&p->d_partials, partial_bytes) == hipSuccess &&
+               hipMalloc(&p->d_zero, 256) == hipSuccess &&
                hipMalloc(&p->d_groups, sizeof(cb::ApplyGroup) * agroups.size()) == hipSuccess &&
                hipMalloc(&p->d_whi, wsplit) == hipSuccess && hipMalloc(&p->d_wlo, wsplit) == hipSuccess &&
                hipMalloc(&p->d_bias, sizeof(float) * n * d_t) == hipSuccess;
@@ -284,7 +287,8 @@ cb_status cb_plan_create(const cb_head_map *map, const cb_cache *src_geom, const
         cb_plan_destroy(p);
         return fail(CB_ERR_OUT_OF_MEMORY, "plan workspace allocation failed (%zu bytes of partial sums)", partial_bytes);
     }
-    bool okc = hipMemcpy(p->d_items, items.data(), sizeof(cb::StatsItem) * items.size(), hipMemcpyHostToDevice) == hipSuccess &&
+    bool okc = hipMemset(p->d_zero, 0, 256) == hipSuccess &&
+               hipMemcpy(p->d_items, items.data(), sizeof(cb::StatsItem) * items.size(), hipMemcpyHostToDevice) == hipSuccess &&
                hipMemcpy(p->d_map_item, map_item.data(), sizeof(int32_t) * n, hipMemcpyHostToDevice) == hipSuccess &&
                hipMemcpy(p->d_map_slot, map_slot.data(), sizeof(int32_t) * n, hipMemcpyHostToDevice) == hipSuccess &&
                hipMemcpy(p->d_groups, agroups.data(), sizeof(cb::ApplyGroup) * agroups.size(), hipMemcpyHostToDevice) == hipSuccess;
@@ -348,6 +352,8 @@ cb_status cb_stats_accumulate(cb_plan *p, const cb_cache *src, const cb_cache *t
     a.n_items = p->n_items;
     a.items = p->d_items;
     a.partials = p->d_partials;
+    a.zero = p->d_zero;
+    a.fast_tiles = (src->seq_len % cb::kStatsTileTokens) == 0;
     hipStream_t st = (hipStream_t)stream;
     if (cb::launch_stats(p->d_s, p->d_t, a, st) != hipSuccess)
         return fail(CB_ERR_DEVICE, "statistics kernel launch failed");

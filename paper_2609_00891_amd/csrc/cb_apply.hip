@@ -26,6 +26,16 @@ typedef __attribute__((ext_vector_type(16))) float f32x16_t;
 typedef __attribute__((ext_vector_type(2))) float f32x2_t;
 typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
 
+// Workgroup barrier for LDS double buffering: waits for this wave's LDS
+// operations only (lgkmcnt), not for global loads still in flight, then
+// s_barrier.  (A plain __syncthreads() also drains every outstanding global
+// load, which would expose the full HBM latency once per tile.)
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // vmcnt = max, expcnt = max, lgkmcnt = 0
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
 __device__ __forceinline__ uint32_t fastdiv(uint32_t n, const FastDiv &f) {
     const uint32_t t = __umulhi(n, f.m);
     return (t + ((n - t) >> f.sh1)) >> f.sh2;
@@ -160,7 +170,7 @@ void apply_kernel(ApplyArgs a) {
     if (n_sb > 0) {
         load_sb(0);
         store_sb(0);
-        __syncthreads();
+        lds_barrier();
         for (int sb = 0; sb < n_sb; ++sb) {
             if (sb + 1 < n_sb) load_sb(sb + 1);
             if (active) {
@@ -204,7 +214,7 @@ void apply_kernel(ApplyArgs a) {
                 }
             }
             if (sb + 1 < n_sb) store_sb((sb + 1) & 1);
-            __syncthreads();
+            lds_barrier();
         }
     }
 }

@@ -64,6 +64,8 @@ struct StatsArgs {
     int32_t n_items;
     const StatsItem *items;
     float *partials;      // [n_chunks * n_items][2][slot_floats]
+    const void *zero;     // >= 16 zero bytes: source of copies for absent tokens
+    int32_t fast_tiles;   // seq_len is a multiple of the token tile: tiles never straddle sequences
 };
 
 struct ReduceArgs {
@@ -99,7 +101,7 @@ hipError_t launch_split_maps(int32_t n_maps, int32_t d_s, int32_t d_t, const flo
 hipError_t launch_apply(int d_s, int d_t, int n_groups, const ApplyArgs &a, hipStream_t s);
 
 // Geometry of the statistics kernel, shared with the host for workspace sizing.
-constexpr int kStatsTileTokens = 64;
+constexpr int kStatsTileTokens = 32;
 inline int64_t stats_slot_floats(int d_s, int d_t) {
     const int rb = d_s / 32, rbt = d_t / 32;
     return (int64_t)(rb * (rb + 1) / 2 + rb * rbt) * 1024 + (int64_t)(rb + rbt + 1) * 64;

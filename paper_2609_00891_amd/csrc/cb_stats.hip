@@ -11,10 +11,8 @@
 // stats_kernel (one workgroup per (item, token chunk)):
 //   * an item is one or two maps; two maps that read the same source block
 //     load its rows once;
-//   * 64-token tiles are loaded with 128-bit global loads (16 lanes cover one
-//     256-byte row), transposed in registers to channel-major order and
-//     stored in LDS with an XOR swizzle (double buffered, one barrier per
-//     tile);
+//   * token tiles stream HBM -> LDS by direct-to-LDS copies through a
+//     four-stage ring (see the comment above Cfg);
 //   * wave (slot, rb) owns rows rb*32..rb*32+31 of one map: it folds the
 //     per-token weight into its x rows in fp32, splits w*x into two bf16 terms
 //     (hi = RNE(w x), lo = RNE(w x - hi)) and runs v_mfma_f32_32x32x16_bf16
@@ -52,51 +50,67 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
     return __builtin_bit_cast(uint32_t, p);
 }
 
-// Byte offset of 16-byte token block kb (8 tokens) of channel ch in a
-// [channel][64 tokens] bf16 tile.  The block index is XORed with a function of
-// the channel so that 16 consecutive channels reading the same block land in
-// distinct LDS banks, and channels 8 apart (written together by the
-// transposing stores) are spread as well.
-__device__ __forceinline__ uint32_t tile_off(uint32_t ch, uint32_t kb) {
-    const uint32_t h = ((ch >> 1) ^ (ch >> 3)) & 7u;
-    return ch * 128u + ((kb ^ h) << 4);
-}
-
-// Per-workgroup context of the statistics kernel (wave-uniform values).
-struct StatsCtx {
-    int unit, tok_begin, tok_end, n_tiles, n_slots, total_jobs, nj2;
-    bool shared_x;
-    const uint16_t *tp[4];
-    const float *wrow[2];
-};
-
-// Every workgroup has four waves, two per map slot, at one wave per SIMD
-// (512-VGPR budget).  The two waves of a slot split the row blocks of the
-// Gram/cross tiles so that their MFMA work is as even as the widths allow:
-// d_s = 128: (0,3) and (1,2), 13 tiles each; d_s = 96: (0,2) and (1);
-// d_s = 64: (0) and (1).
-template <int DS> struct WaveShape;
-template <> struct WaveShape<128> { static constexpr int A1 = 0, A2 = 3, B1 = 1, B2 = 2; };
-template <> struct WaveShape<96> { static constexpr int A1 = 0, A2 = 2, B1 = 1, B2 = -1; };
-template <> struct WaveShape<64> { static constexpr int A1 = 0, A2 = -1, B1 = 1, B2 = -1; };
+// ---------------------------------------------------------------------------
+// Streaming statistics kernel.
+//
+// Token tiles of KT = 32 tokens flow through an NST = 4 stage LDS ring.  Each
+// stage holds the tile's rows in their natural [token][channel] order:
+// x (source) and y (target) rows of the item's one or two maps, plus the two
+// weight rows.  The rows are copied HBM -> LDS by global_load_lds_dwordx4
+// (direct-to-LDS DMA, no VGPR staging), three tiles ahead of the tile being
+// computed.  Every wave issues the same number of DMA instructions per tile
+// (tiles past the end load from a zero buffer), so one explicit vmcnt wait
+// plus one barrier per tile tells every wave that the tile has landed.
+//
+// The MFMA operands are read with ds_read_b64_tr_b16, which transposes 16-bit
+// elements across each group of 16 lanes: lane j = a + 4k of a group points
+// at channels 4a..4a+3 of token k, and output lane i of the group receives
+// channel i of the four tokens.  Two such reads give a lane the eight
+// consecutive tokens of one channel that v_mfma_f32_32x32x16_bf16 expects,
+// for the x operand of the fold and for every B operand alike.
+//
+// The 16-byte chunk c of token row t is stored at chunk c ^ h(t), h(t) a
+// multiple of 4 chunks that depends on t mod 4 only: the four tokens read by
+// one 16-lane group fall in different 64-byte windows (no bank conflict), and
+// the column-block offset stays a per-lane XOR.
+// ---------------------------------------------------------------------------
 
 template <int DS, int DT>
 struct Cfg {
     static constexpr int RB = DS / 32, RBT = DT / 32;
-    static constexpr int NW = 4, NT = 64 * NW;
-    static constexpr int KT = kStatsTileTokens;               // tokens per tile
-    static constexpr int NCGX = DS / 8, NCGY = DT / 8;         // 16-byte channel groups per row
-    static constexpr int XB = DS * KT * 2, YB = DT * KT * 2;   // bytes of one tile
-    static constexpr int OX0 = 0, OX1 = XB, OY0 = 2 * XB, OY1 = 2 * XB + YB;
-    static constexpr int OW0 = 2 * XB + 2 * YB, OW1 = OW0 + KT * 4;
-    static constexpr int BUF = OW1 + KT * 4;                   // one LDS buffer
-    static constexpr int JX = (KT / 4) * NCGX, JY = (KT / 4) * NCGY;  // load jobs per tensor
-    static constexpr int MAXJ = (2 * JX + 2 * JY + NT - 1) / NT;
+    static constexpr int NW = 2 * RB, NT = 64 * NW;            // waves: (slot, row block)
+    static constexpr int KT = kStatsTileTokens;                 // tokens per tile
+    static constexpr int NST = 4;                               // LDS ring stages
+    static constexpr int NCBX = DS / 8, NCBY = DT / 8;          // 16-byte chunks per row
+    static constexpr int ROWX = DS * 2, ROWY = DT * 2;          // bytes per row
+    static constexpr int CHX = KT * NCBX, CHY = KT * NCBY;      // chunks per tensor tile
+    static constexpr int XB = CHX * 16, YB = CHY * 16;
+    static constexpr int OFF_W = 2 * XB + 2 * YB;               // weights: [2 slots][KT] fp32
+    static constexpr int OFF_DUMMY = OFF_W + 2 * KT * 4;        // 16 bytes no one reads
+    static constexpr int STAGE = OFF_DUMMY + 16;
+    static constexpr int LDS = NST * STAGE;
+    static constexpr int EPW = (2 * KT + NW - 1) / NW;          // weight entries per wave
+    static constexpr int LMAX = (2 * CHX + 2 * CHY + NT - 1) / NT;   // DMA loads per wave per tile
     static constexpr int NTG = RB * (RB + 1) / 2, NTC = RB * RBT;
     static constexpr int SUMX = (NTG + NTC) * 1024, SUMY = SUMX + RB * 64, SUMW = SUMY + RBT * 64;
     static constexpr int SLOT = SUMW + 64;
-    static_assert(KT == 64, "tile_off assumes 64-token tiles");
+    static_assert(KT == 32, "the transposed-read addressing assumes 32-token tiles");
+    static_assert(CHX % 64 == 0 && CHY % 64 == 0, "a DMA instruction must stay inside one tensor");
+
+    __host__ __device__ static constexpr int chunks(int nt) {
+        return nt == 2 ? CHX + CHY : nt == 3 ? CHX + 2 * CHY : 2 * CHX + 2 * CHY;
+    }
+    __host__ __device__ static constexpr int loads(int nt) { return (chunks(nt) + NT - 1) / NT; }
 };
+
+// Token-dependent chunk swizzle h(t) (a multiple of 4 chunks), for rows of
+// NCB 16-byte chunks.  Depends on t mod 4 only.
+template <int NCB>
+__device__ __forceinline__ uint32_t swz(uint32_t t) {
+    if constexpr (NCB == 16) return 4u * (t & 3u);
+    else if constexpr (NCB == 8) return 4u * ((t >> 1) & 1u);
+    else return 0u;
+}
 
 // Index of accumulator element (row i, col j) of a 32x32 tile stored as
 // [v][lane]: v_mfma_f32_32x32x16 leaves D[i][j] in lane j + 32*((i>>2)&1),
@@ -110,92 +124,159 @@ __host__ __device__ constexpr int tri_tile(int r, int c) {  // upper-triangle ti
     return r * RB - (r * (r - 1)) / 2 + (c - r);
 }
 
-// Streaming loader: every thread stages its share of the next tile in
-// registers (global -> VGPR), then transposes it into LDS.
-template <int DS, int DT>
-struct Loader {
-    using K = Cfg<DS, DT>;
-    uint4 stage[K::MAXJ][4];
-    float wstage;
+typedef __attribute__((ext_vector_type(4))) short s16x4_t;
+typedef __attribute__((ext_vector_type(4))) float f32x4_t;
+typedef __attribute__((address_space(3))) f32x4_t lds_f32x4_t;
+typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
+typedef __attribute__((address_space(3))) char lds_char_t;
 
-    __device__ __forceinline__ static void decode(const StatsCtx &c, int j, int &t, int &jj) {
-        if (j < K::JX) { t = 0; jj = j; }
-        else if (j < K::JX + K::JY) { t = 1; jj = j - K::JX; }
-        else if (j < K::JX + K::JY + c.nj2) { t = 2; jj = j - K::JX - K::JY; }
-        else { t = 3; jj = j - K::JX - K::JY - c.nj2; }
-    }
+// HBM -> LDS copies.  The LDS destination of lane l is M0 + 16 l (4 l for the
+// dword form).  They are issued through inline assembly so that the compiler
+// does not add its own conservative waits between them and the LDS reads of
+// other ring stages; completion is tracked with explicit vmcnt waits below.
+// M0 is saved and restored around each copy, so the compiler's own use of it
+// is unaffected.
+__device__ __forceinline__ void dma16(const void *gaddr, uint32_t m0) {
+    uint32_t keep;
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
+                 : "=&s"(keep)
+                 : "v"(gaddr), "s"(m0)
+                 : "memory");
+}
+__device__ __forceinline__ void dma16_sbase(uint32_t voff, const void *sbase, uint32_t m0) {
+    uint32_t keep;
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\tglobal_load_lds_dwordx4 %1, %2\n\ts_mov_b32 m0, %0"
+                 : "=&s"(keep)
+                 : "v"(voff), "s"(sbase), "s"(m0)
+                 : "memory");
+}
+__device__ __forceinline__ void dma4(const void *gaddr, uint32_t m0) {
+    uint32_t keep;
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\tglobal_load_lds_dword %1, off\n\ts_mov_b32 m0, %0"
+                 : "=&s"(keep)
+                 : "v"(gaddr), "s"(m0)
+                 : "memory");
+}
 
-    __device__ __forceinline__ void load(const StatsArgs &a, const StatsCtx &c, int tid, int tile) {
-        const int t0 = c.tok_begin + tile * K::KT;
-#pragma unroll
-        for (int s = 0; s < K::MAXJ; ++s) {
-            const int j = tid + s * K::NT;
-            if (j < c.total_jobs) {
-                int t, jj;
-                decode(c, j, t, jj);
-                const bool isx = (t == 0 || t == 2);
-                const int ncg = isx ? K::NCGX : K::NCGY;
-                const int cg = jj % ncg, q = jj / ncg;
-                const int64_t sseq = isx ? a.ss.seq : a.ts.seq;
-                const int64_t stok = isx ? a.ss.tok : a.ts.tok;
-                const int tau = t0 + 4 * q;
-                uint32_t b = fastdiv((uint32_t)tau, a.T);
-                uint32_t tt = (uint32_t)tau - b * a.T.d;
-                const uint16_t *tb = t == 0 ? c.tp[0] : t == 1 ? c.tp[1] : t == 2 ? c.tp[2] : c.tp[3];
-                const uint16_t *base = tb + cg * 8;
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    uint4 v = make_uint4(0, 0, 0, 0);
-                    if (tau + r < c.tok_end)
-                        v = *reinterpret_cast<const uint4 *>(base + (int64_t)b * sseq + (int64_t)tt * stok);
-                    stage[s][r] = v;
-                    if (++tt == a.T.d) { tt = 0; ++b; }
-                }
-            }
-        }
-        if (tid < 2 * K::KT) {
-            const int ws = tid / K::KT, k = tid % K::KT;
-            const int tau = t0 + k;
-            wstage = 0.f;
-            if (ws < c.n_slots && tau < c.tok_end) wstage = (ws ? c.wrow[1] : c.wrow[0])[tau];
-        }
-    }
+// A pointer that is the same in every lane, placed in SGPRs.
+__device__ __forceinline__ const void *uniform_ptr(const void *p) {
+    const uint64_t v = (uint64_t)(uintptr_t)p;
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+    return (const void *)(uintptr_t)(((uint64_t)hi << 32) | lo);
+}
 
-    __device__ __forceinline__ void store(const StatsCtx &c, int tid, char *B) {
-#pragma unroll
-        for (int s = 0; s < K::MAXJ; ++s) {
-            const int j = tid + s * K::NT;
-            if (j < c.total_jobs) {
-                int t, jj;
-                decode(c, j, t, jj);
-                const bool isx = (t == 0 || t == 2);
-                const int ncg = isx ? K::NCGX : K::NCGY;
-                const int cg = jj % ncg, q = jj / ncg;
-                const int dst = t == 0 ? K::OX0 : t == 1 ? K::OY0 : t == 2 ? K::OX1 : K::OY1;
-                const uint32_t v0[4] = {stage[s][0].x, stage[s][0].y, stage[s][0].z, stage[s][0].w};
-                const uint32_t v1[4] = {stage[s][1].x, stage[s][1].y, stage[s][1].z, stage[s][1].w};
-                const uint32_t v2[4] = {stage[s][2].x, stage[s][2].y, stage[s][2].z, stage[s][2].w};
-                const uint32_t v3[4] = {stage[s][3].x, stage[s][3].y, stage[s][3].z, stage[s][3].w};
-#pragma unroll
-                for (int ch8 = 0; ch8 < 8; ++ch8) {
-                    const int d = ch8 >> 1;
-                    const uint32_t sel = (ch8 & 1) ? 0x07060302u : 0x05040100u;
-                    uint2 o;
-                    o.x = __builtin_amdgcn_perm(v1[d], v0[d], sel);   // tokens 4q, 4q+1
-                    o.y = __builtin_amdgcn_perm(v3[d], v2[d], sel);   // tokens 4q+2, 4q+3
-                    const uint32_t ch = cg * 8 + ch8;
-                    *reinterpret_cast<uint2 *>(B + dst + tile_off(ch, q >> 1) + ((q & 1) << 3)) = o;
-                }
-            }
-        }
-        if (tid < 2 * K::KT) {
-            const int ws = tid / K::KT, k = tid % K::KT;
-            reinterpret_cast<float *>(B + (ws ? K::OW1 : K::OW0))[k] = wstage;
-        }
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+// vmcnt wait with a run-time count (the possible counts are small and even).
+__device__ __forceinline__ void wait_vm_rt(int n) {
+    switch (n) {
+        case 0: wait_vm<0>(); break;
+        case 2: wait_vm<2>(); break;
+        case 4: wait_vm<4>(); break;
+        case 6: wait_vm<6>(); break;
+        case 8: wait_vm<8>(); break;
+        case 10: wait_vm<10>(); break;
+        case 12: wait_vm<12>(); break;
+        case 14: wait_vm<14>(); break;
+        case 16: wait_vm<16>(); break;
+        case 18: wait_vm<18>(); break;
+        default: wait_vm<0>(); break;
     }
+}
+
+__device__ __forceinline__ bf16x8_t tr_read8(const lds_char_t *p0, const lds_char_t *p1) {
+    const s16x4_t a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t *)p0);
+    const s16x4_t b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t *)p1);
+    typedef __attribute__((ext_vector_type(8))) short s16x8_t;
+    const s16x8_t c = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+    return __builtin_bit_cast(bf16x8_t, c);
+}
+
+// Per-workgroup context (wave-uniform values).
+struct StatsCtx {
+    int unit, tok_begin, tok_end, n_tiles, n_slots, nt;
+    bool shared_x;
+    const uint16_t *tp[4];       // x0, y0, x1, y1 block bases
+    const float *wrow[2];
 };
 
-// Accumulators and MFMA work of one row block R of one map.
+// Issue the DMA copies of tile `tile` (any index; tiles past the end copy zeros)
+// into ring stage `st`.  Every wave issues exactly loads(nt) + 1 instructions.
+template <int DS, int DT>
+__device__ __forceinline__ void issue_tile(const StatsArgs &a, const StatsCtx c, lds_char_t *lds, int wave,
+                                           int lane, int tile, int st, const uint32_t *fast_off) {
+    using K = Cfg<DS, DT>;
+    const int t0 = c.tok_begin + tile * K::KT;
+    const bool in_range = tile < c.n_tiles;
+    const bool fast = a.fast_tiles && in_range && (t0 + K::KT <= c.tok_end);
+    const uint32_t stage = (uint32_t)(uintptr_t)(lds + st * K::STAGE);
+    const int total = K::chunks(c.nt);
+    uint32_t b_tile = 0, tt_tile = 0;
+    if (fast) {
+        b_tile = fastdiv((uint32_t)t0, a.T);
+        tt_tile = (uint32_t)t0 - b_tile * a.T.d;
+    }
+#pragma unroll
+    for (int i = 0; i < K::LMAX; ++i) {
+        if (i < K::loads(c.nt)) {
+            const int q0 = (i * K::NW + wave) * 64;         // first chunk of this instruction
+            const uint32_t m0 = __builtin_amdgcn_readfirstlane(stage + q0 * 16);
+            if (q0 < total) {
+                // tensor of this instruction (uniform)
+                int ten, qs;
+                if (q0 < K::CHX) { ten = 0; qs = 0; }
+                else if (q0 < K::CHX + K::CHY) { ten = 1; qs = K::CHX; }
+                else if (c.nt == 3) { ten = 3; qs = K::CHX + K::CHY; }
+                else if (q0 < 2 * K::CHX + K::CHY) { ten = 2; qs = K::CHX + K::CHY; }
+                else { ten = 3; qs = 2 * K::CHX + K::CHY; }
+                const bool isx = (ten == 0 || ten == 2);
+                const uint16_t *tb = ten == 0 ? c.tp[0] : ten == 1 ? c.tp[1] : ten == 2 ? c.tp[2] : c.tp[3];
+                const int64_t sseq = isx ? a.ss.seq : a.ts.seq;
+                const int64_t stok = isx ? a.ss.tok : a.ts.tok;
+                if (fast) {
+                    const uint16_t *base = tb + (int64_t)b_tile * sseq + (int64_t)tt_tile * stok;
+                    dma16_sbase(fast_off[i], uniform_ptr(base), m0);
+                } else {
+                    const int ncb = isx ? K::NCBX : K::NCBY;
+                    const int q = q0 - qs + lane;
+                    const int t = q / ncb, p = q - (q / ncb) * ncb;
+                    const uint32_t h = isx ? swz<K::NCBX>(t) : swz<K::NCBY>(t);
+                    const int cch = p ^ (int)h;
+                    const int tau = t0 + t;
+                    const void *g = a.zero;
+                    if (in_range && tau < c.tok_end) {
+                        const uint32_t b = fastdiv((uint32_t)tau, a.T);
+                        const uint32_t tt = (uint32_t)tau - b * a.T.d;
+                        g = tb + (int64_t)b * sseq + (int64_t)tt * stok + cch * 8;
+                    }
+                    dma16(g, m0);
+                }
+            } else {
+                // no chunk left for this instruction: keep the count uniform by
+                // copying 16 zero bytes into the stage's unused slot
+                const uint32_t md = __builtin_amdgcn_readfirstlane(stage + K::OFF_DUMMY);
+                if (lane == 0) dma16(a.zero, md);
+            }
+        }
+    }
+    // weights: entries e = lane of [2 slots][KT tokens], this wave's share only
+    const uint32_t mw = __builtin_amdgcn_readfirstlane(stage + K::OFF_W);
+    const int e = lane;
+    if (e >= wave * K::EPW && e < (wave + 1) * K::EPW && e < 2 * K::KT) {
+        const int sl = e / K::KT, t = e % K::KT;
+        const void *g = a.zero;
+        if (in_range && sl < c.n_slots && t0 + t < c.tok_end) g = (sl ? c.wrow[1] : c.wrow[0]) + t0 + t;
+        dma4(g, mw);
+    } else if (wave * K::EPW >= 2 * K::KT && lane == 0) {
+        // waves without weight entries still issue one copy (into the unused slot)
+        dma4(a.zero, __builtin_amdgcn_readfirstlane(stage + K::OFF_DUMMY));
+    }
+}
+
+// Accumulators and MFMA work of row block R of one map.
 template <int DS, int DT, int R>
 struct RowBlock {
     using K = Cfg<DS, DT>;
@@ -221,12 +302,10 @@ struct RowBlock {
         for (int c = 0; c < K::RBT; ++c) sumy[c] = 0.f;
     }
 
-    // One 16-token K step.  bx[c] holds x columns c*32.. for c >= RMIN (the
-    // smallest row block of this wave), by[] the y columns, w the weights of
-    // this lane's 8 tokens.
-    template <int RMIN>
+    // One 16-token K step: bx[c] holds x columns (R + c)*32.. (bx[0] is also the
+    // A operand's x), by[] the y columns, w the weights of this lane's 8 tokens.
     __device__ __forceinline__ void step(const bf16x8_t *bx, const bf16x8_t *by, const float *w) {
-        const uint4 ax = __builtin_bit_cast(uint4, bx[R - RMIN]);
+        const uint4 ax = __builtin_bit_cast(uint4, bx[0]);
         const uint32_t xv[4] = {ax.x, ax.y, ax.z, ax.w};
         float av[8];
 #pragma unroll
@@ -268,13 +347,13 @@ struct RowBlock {
         const bf16x8_t alo = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
 #pragma unroll
         for (int c = 0; c < NG; ++c)
-            accg[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ahi, bx[R + c - RMIN], accg[c], 0, 0, 0);
+            accg[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ahi, bx[c], accg[c], 0, 0, 0);
 #pragma unroll
         for (int c = 0; c < K::RBT; ++c)
             accc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ahi, by[c], accc[c], 0, 0, 0);
 #pragma unroll
         for (int c = 0; c < NG; ++c)
-            accg[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(alo, bx[R + c - RMIN], accg[c], 0, 0, 0);
+            accg[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(alo, bx[c], accg[c], 0, 0, 0);
 #pragma unroll
         for (int c = 0; c < K::RBT; ++c)
             accc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(alo, by[c], accc[c], 0, 0, 0);
@@ -301,74 +380,107 @@ struct RowBlock {
     }
 };
 
-// The whole token loop of one wave whose row blocks are R1 (and R2 >= 0 when
-// the wave owns two).  All waves run the same loads, stores and barriers.
-template <int DS, int DT, int R1, int R2>
-__device__ __forceinline__ void stats_wave(const StatsArgs &a, const StatsCtx &c, char *lds, int tid,
-                                           int slot) {
+// The token loop of one wave owning row block R of map slot `slot`.
+template <int DS, int DT, int R>
+__device__ __forceinline__ void stats_wave(const StatsArgs &a, const StatsCtx c, lds_char_t *lds, int wave,
+                                           int lane, int slot) {
     using K = Cfg<DS, DT>;
-    constexpr int RMIN = (R2 >= 0 && R2 < R1) ? R2 : R1;
-    constexpr int NBX = K::RB - RMIN;
-    const int lane = tid & 63;
+    constexpr int NBX = K::RB - R;
     const bool active = slot < c.n_slots;
-    RowBlock<DS, DT, R1> blk1;
-    RowBlock<DS, DT, (R2 >= 0 ? R2 : R1)> blk2;
-    blk1.zero();
-    if (R2 >= 0) blk2.zero();
+    RowBlock<DS, DT, R> blk;
+    blk.zero();
 
-    const int xoff = (slot == 0 || c.shared_x) ? K::OX0 : K::OX1;
-    const int yoff = slot == 0 ? K::OY0 : K::OY1;
-    const int woff = slot == 0 ? K::OW0 : K::OW1;
-    const uint32_t lrow = lane & 31, lhalf = lane >> 5;
+    // LDS offsets of this slot's tensors inside a stage
+    const int xoff = (slot == 0 || c.nt != 4) ? 0 : K::XB + K::YB;
+    const int yoff = slot == 0 ? K::XB : (c.nt == 4 ? 2 * K::XB + K::YB : K::XB + K::YB);
+    const int woff = K::OFF_W + slot * K::KT * 4;
 
-    Loader<DS, DT> ld;
-    if (c.n_tiles > 0) {
-        ld.load(a, c, tid, 0);
-        ld.store(c, tid, lds);
-        if (c.n_tiles > 1) ld.load(a, c, tid, 1);
-        __syncthreads();
-        for (int tile = 0; tile < c.n_tiles; ++tile) {
-            if (active) {
-                const char *B = lds + (tile & 1) * K::BUF;
-#pragma unroll 1
-                for (int ks = 0; ks < K::KT / 16; ++ks) {
-                    const uint32_t kb = 2 * ks + lhalf;
-                    bf16x8_t bx[NBX], by[K::RBT];
+    // Transposed-read lane geometry (see the file comment): group g = lane/16,
+    // j = a + 4k inside the group.
+    const int g = lane >> 4, j = lane & 15, aa = j & 3, kk = j >> 2;
+    const int tok_l = 8 * (g >> 1) + kk;                       // token within the 16-token step
+    const int cl = 2 * (g & 1) + (aa >> 1);                    // chunk within the 64-byte window
+    const uint32_t lx = tok_l * K::ROWX + cl * 16 + (aa & 1) * 8;
+    const uint32_t ly = tok_l * K::ROWY + cl * 16 + (aa & 1) * 8;
+    const uint32_t hx = swz<K::NCBX>(kk) >> 2, hy = swz<K::NCBY>(kk) >> 2;
+    const uint32_t wl = (lane >> 5) * 32;                      // byte offset of this lane's 8 weights
+
+    // Per-lane source offsets of the fast DMA path: chunk (t, p) of the
+    // instruction's tensor comes from global chunk p ^ h(t) of token t.
+    uint32_t fast_off[K::LMAX];
 #pragma unroll
-                    for (int cc = 0; cc < NBX; ++cc)
-                        bx[cc] = *reinterpret_cast<const bf16x8_t *>(B + xoff + tile_off((RMIN + cc) * 32 + lrow, kb));
-#pragma unroll
-                    for (int cc = 0; cc < K::RBT; ++cc)
-                        by[cc] = *reinterpret_cast<const bf16x8_t *>(B + yoff + tile_off(cc * 32 + lrow, kb));
-                    const float4 w0 = *reinterpret_cast<const float4 *>(B + woff + kb * 32);
-                    const float4 w1 = *reinterpret_cast<const float4 *>(B + woff + kb * 32 + 16);
-                    const float w[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-                    blk1.template step<RMIN>(bx, by, w);
-                    if (R2 >= 0) blk2.template step<RMIN>(bx, by, w);
-                }
+    for (int i = 0; i < K::LMAX; ++i) {
+        fast_off[i] = 0;
+        if (i < K::loads(c.nt)) {
+            const int q0 = (i * K::NW + wave) * 64;
+            if (q0 < K::chunks(c.nt)) {
+                int qs;
+                bool isx;
+                if (q0 < K::CHX) { qs = 0; isx = true; }
+                else if (q0 < K::CHX + K::CHY) { qs = K::CHX; isx = false; }
+                else if (c.nt == 3) { qs = K::CHX + K::CHY; isx = false; }
+                else if (q0 < 2 * K::CHX + K::CHY) { qs = K::CHX + K::CHY; isx = true; }
+                else { qs = 2 * K::CHX + K::CHY; isx = false; }
+                const int ncb = isx ? K::NCBX : K::NCBY;
+                const int q = q0 - qs + lane;
+                const int t = q / ncb, p = q - (q / ncb) * ncb;
+                const uint32_t h = isx ? swz<K::NCBX>(t) : swz<K::NCBY>(t);
+                const int64_t stok = isx ? a.ss.tok : a.ts.tok;
+                fast_off[i] = (uint32_t)(((int64_t)t * stok + (int64_t)((p ^ (int)h) * 8)) * 2);
             }
-            if (tile + 1 < c.n_tiles) {
-                ld.store(c, tid, lds + ((tile + 1) & 1) * K::BUF);
-                if (tile + 2 < c.n_tiles) ld.load(a, c, tid, tile + 2);
-            }
-            __syncthreads();
         }
     }
+
+    const int vm_per_tile = K::loads(c.nt) + 1;
+    // prologue: tiles 0, 1, 2
+#pragma unroll
+    for (int t = 0; t < K::NST - 1; ++t) issue_tile<DS, DT>(a, c, lds, wave, lane, t, t, fast_off);
+
+    for (int tile = 0; tile < c.n_tiles; ++tile) {
+        wait_vm_rt(2 * vm_per_tile);              // this wave's copies of `tile` have landed
+        __builtin_amdgcn_s_waitcnt(0xC07F);       // and its LDS reads of the previous tile are done
+        __builtin_amdgcn_s_barrier();
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        issue_tile<DS, DT>(a, c, lds, wave, lane, tile + K::NST - 1, (tile + K::NST - 1) % K::NST, fast_off);
+        if (active) {
+            const lds_char_t *S = lds + (tile % K::NST) * K::STAGE;
+#pragma unroll
+            for (int ks = 0; ks < K::KT / 16; ++ks) {
+                bf16x8_t bx[NBX], by[K::RBT];
+#pragma unroll
+                for (int cc = 0; cc < NBX; ++cc) {
+                    const lds_char_t *p = S + xoff + lx + 64u * ((uint32_t)(R + cc) ^ hx) + 16 * ks * K::ROWX;
+                    bx[cc] = tr_read8(p, p + 4 * K::ROWX);
+                }
+#pragma unroll
+                for (int cc = 0; cc < K::RBT; ++cc) {
+                    const lds_char_t *p = S + yoff + ly + 64u * ((uint32_t)cc ^ hy) + 16 * ks * K::ROWY;
+                    by[cc] = tr_read8(p, p + 4 * K::ROWY);
+                }
+                const f32x4_t w0 = *(const lds_f32x4_t *)(S + woff + 64 * ks + wl);
+                const f32x4_t w1 = *(const lds_f32x4_t *)(S + woff + 64 * ks + wl + 16);
+                const float w[8] = {w0[0], w0[1], w0[2], w0[3], w1[0], w1[1], w1[2], w1[3]};
+                blk.step(bx, by, w);
+            }
+        }
+    }
+    wait_vm<0>();                                  // drain the trailing copies before leaving
     if (active) {
         float *P = a.partials + ((int64_t)c.unit * 2 + slot) * K::SLOT;
-        blk1.flush(P, lane);
-        if (R2 >= 0) blk2.flush(P, lane);
+        blk.flush(P, lane);
     }
 }
 
 template <int DS, int DT>
 __global__ __attribute__((amdgpu_flat_work_group_size(Cfg<DS, DT>::NT, Cfg<DS, DT>::NT),
-                          amdgpu_waves_per_eu(1, 1)))
+                          amdgpu_waves_per_eu(2, 2)))
 void stats_kernel(StatsArgs a) {
     using K = Cfg<DS, DT>;
-    __shared__ __attribute__((aligned(16))) char lds[2 * K::BUF];
+    __shared__ __attribute__((aligned(16))) char lds_raw[K::LDS];
+    lds_char_t *lds = (lds_char_t *)lds_raw;
 
     const int tid = threadIdx.x;
+    const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     StatsCtx c;
     c.unit = blockIdx.x;
@@ -377,12 +489,10 @@ void stats_kernel(StatsArgs a) {
     const StatsItem it = a.items[item_id];
     c.n_slots = it.n_slots;
     c.shared_x = it.shared_x != 0;
-    const bool has_x1 = (c.n_slots == 2) && !c.shared_x;
+    c.nt = c.n_slots == 1 ? 2 : (c.shared_x ? 3 : 4);
     c.tok_begin = chunk * a.chunk_tokens;
     c.tok_end = min(a.N, c.tok_begin + a.chunk_tokens);
     c.n_tiles = c.tok_end > c.tok_begin ? (c.tok_end - c.tok_begin + K::KT - 1) / K::KT : 0;
-    c.nj2 = has_x1 ? K::JX : 0;
-    c.total_jobs = K::JX + K::JY + c.nj2 + (c.n_slots == 2 ? K::JY : 0);
     c.tp[0] = a.src + it.src_layer[0] * a.ss.layer + it.kv[0] * a.ss.kv + it.src_head[0] * a.ss.head;
     c.tp[1] = a.tgt + it.tgt_layer[0] * a.ts.layer + it.kv[0] * a.ts.kv + it.tgt_head[0] * a.ts.head;
     c.tp[2] = a.src + it.src_layer[1] * a.ss.layer + it.kv[1] * a.ss.kv + it.src_head[1] * a.ss.head;
@@ -390,10 +500,21 @@ void stats_kernel(StatsArgs a) {
     c.wrow[0] = a.w + (int64_t)it.wrow[0] * a.w_row_stride;
     c.wrow[1] = a.w + (int64_t)it.wrow[1] * a.w_row_stride;
 
-    using WS = WaveShape<DS>;
-    const int slot = wave >> 1;
-    if ((wave & 1) == 0) stats_wave<DS, DT, WS::A1, WS::A2>(a, c, lds, tid, slot);
-    else stats_wave<DS, DT, WS::B1, WS::B2>(a, c, lds, tid, slot);
+    // wave -> (slot, row block).  With four row blocks the two waves sharing a
+    // SIMD (w, w + 4) get blocks (0,3) or (1,2), which balances MFMA work.
+    int slot, rb;
+    if (K::RB == 4) {
+        slot = (wave >> 1) & 1;
+        const int r = wave & 1;
+        rb = wave < 4 ? r : 3 - r;
+    } else {
+        slot = wave / K::RB;
+        rb = wave % K::RB;
+    }
+    if (rb == 0) stats_wave<DS, DT, 0>(a, c, lds, wave, lane, slot);
+    else if (rb == 1) stats_wave<DS, DT, 1>(a, c, lds, wave, lane, slot);
+    else if (rb == 2) stats_wave<DS, DT, (K::RB > 2 ? 2 : 0)>(a, c, lds, wave, lane, slot);
+    else stats_wave<DS, DT, (K::RB > 3 ? 3 : 0)>(a, c, lds, wave, lane, slot);
 }
 
 template <int DS, int DT>
