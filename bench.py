@@ -143,9 +143,11 @@ def main():
     w = synth.gen_weights(bw, 0, device=dev, chunk=50)
     log(f"  done in {time.time() - t0:.1f} s")
     aw = synth.APPLY
-    log(f"generating sender cache: {aw.n_seqs} x {aw.seq_len} tokens")
-    asrc = synth.gen_apply_source(aw, device=dev)
-    aout = torch.empty((aw.L_t, 2, aw.n_seqs, aw.H_t, aw.seq_len, aw.d_t), dtype=torch.bfloat16, device=dev)
+    asrc = aout = None
+    if not args.no_apply:
+        log(f"generating sender cache: {aw.n_seqs} x {aw.seq_len} tokens")
+        asrc = synth.gen_apply_source(aw, device=dev)
+        aout = torch.empty((aw.L_t, 2, aw.n_seqs, aw.H_t, aw.seq_len, aw.d_t), dtype=torch.bfloat16, device=dev)
     torch.cuda.synchronize()
     log(f"  done in {time.time() - t0:.1f} s")
 
