@@ -62,25 +62,26 @@ cb_status ok() {
 
 bool supported_width(int d) { return d == 64 || d == 96 || d == 128; }
 
-// Chunking of a call's tokens: enough (item, chunk) work units to give every
-// compute unit several, chunks of whole 64-token tiles, and at most 64Ki
-// tokens per fp32 partial.
-void choose_chunks(int64_t N, int n_items, int n_cu, int *n_chunks, int *chunk_tokens) {
-    const int64_t KT = cb::kStatsTileTokens;
-    const int64_t tiles = (N + KT - 1) / KT;
-    if (tiles == 0) {
+// Work units of a call: each item's token tiles (KT tokens of one sequence)
+// are cut into n_chunks chunks of chunk_tiles tiles.  Enough (item, chunk)
+// units to give every compute unit several, at most 2048 tiles (64Ki tokens)
+// per fp32 partial, and never more chunks than the plan's workspace holds
+// (max_chunks <= 0: no such limit).
+void choose_chunks(int64_t tiles, int n_items, int n_cu, int max_chunks, int *n_chunks, int *chunk_tiles) {
+    if (tiles <= 0) {
         *n_chunks = 0;
-        *chunk_tokens = (int)KT;
+        *chunk_tiles = 1;
         return;
     }
     const int64_t target_units = 8LL * n_cu;
     int64_t nc = (target_units + n_items - 1) / n_items;
-    nc = std::max<int64_t>(nc, (N + 65535) / 65536);
+    nc = std::max<int64_t>(nc, (tiles + 2047) / 2048);
     nc = std::min<int64_t>(nc, tiles);
+    if (max_chunks > 0) nc = std::min<int64_t>(nc, max_chunks);
     nc = std::max<int64_t>(nc, 1);
-    const int64_t chunk_tiles = (tiles + nc - 1) / nc;
-    *chunk_tokens = (int)(chunk_tiles * KT);
-    *n_chunks = (int)((tiles + chunk_tiles - 1) / chunk_tiles);
+    const int64_t ct = (tiles + nc - 1) / nc;
+    *chunk_tiles = (int)ct;
+    *n_chunks = (int)((tiles + ct - 1) / ct);
 }
 
 cb_status check_device(const cb_plan *p) {
@@ -247,8 +248,9 @@ cb_status cb_plan_create(const cb_head_map *map, const cb_cache *src_geom, const
             map_item[items[i].map[s]] = i;
             map_slot[items[i].map[s]] = s;
         }
-    int nc = 1, ct = 64;
-    choose_chunks(std::max<int64_t>(max_tokens_per_call, 1), p->n_items, p->n_cu, &nc, &ct);
+    int nc = 1, ct = 1;
+    const int64_t KT = cb::kStatsTileTokens;
+    choose_chunks((std::max<int64_t>(max_tokens_per_call, 1) + KT - 1) / KT, p->n_items, p->n_cu, 0, &nc, &ct);
     p->max_chunks = std::max(nc, 1);
 
     std::vector<cb::ApplyGroup> agroups;
@@ -345,15 +347,21 @@ cb_status cb_stats_accumulate(cb_plan *p, const cb_cache *src, const cb_cache *t
     a.ss = strides_of(src);
     a.ts = strides_of(tgt);
     a.w_row_stride = w_row_stride;
-    a.T = cb::make_fastdiv((uint32_t)src->seq_len);
-    a.N = (int32_t)N;
-    choose_chunks(N, p->n_items, p->n_cu, &a.n_chunks, &a.chunk_tokens);
+    const int64_t KT = cb::kStatsTileTokens;
+    const int64_t tps = (src->seq_len + KT - 1) / KT;
+    const int64_t tiles = (int64_t)src->n_seqs * tps;
+    if (tiles > INT32_MAX) return fail(CB_ERR_UNSUPPORTED, "too many token tiles in one call");
+    if (a.ss.tok * 2 * KT >= (1LL << 31) || a.ts.tok * 2 * KT >= (1LL << 31))
+        return fail(CB_ERR_UNSUPPORTED, "token strides must be below 2^25 elements");
+    a.seq_len = (uint32_t)src->seq_len;
+    a.TPS = cb::make_fastdiv((uint32_t)tps);
+    a.n_tiles = (int32_t)tiles;
+    choose_chunks(tiles, p->n_items, p->n_cu, p->max_chunks, &a.n_chunks, &a.chunk_tiles);
     if (a.n_chunks > p->max_chunks) return fail(CB_ERR_UNSUPPORTED, "internal: chunk count exceeds workspace");
     a.n_items = p->n_items;
     a.items = p->d_items;
     a.partials = p->d_partials;
     a.zero = p->d_zero;
-    a.fast_tiles = (src->seq_len % cb::kStatsTileTokens) == 0;
     hipStream_t st = (hipStream_t)stream;
     if (cb::launch_stats(p->d_s, p->d_t, a, st) != hipSuccess)
         return fail(CB_ERR_DEVICE, "statistics kernel launch failed");

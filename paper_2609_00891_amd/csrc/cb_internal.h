@@ -57,15 +57,15 @@ struct StatsArgs {
     const float *w;
     Strides ss, ts;
     int64_t w_row_stride;
-    FastDiv T;            // seq_len
-    int32_t N;            // tokens in this call (n_seqs * seq_len)
-    int32_t chunk_tokens; // multiple of the token tile
+    uint32_t seq_len;     // tokens per sequence
+    FastDiv TPS;          // token tiles per sequence (the last one may be partial)
+    int32_t n_tiles;      // token tiles in this call (n_seqs * TPS)
+    int32_t chunk_tiles;  // tiles per work unit
     int32_t n_chunks;
     int32_t n_items;
     const StatsItem *items;
     float *partials;      // [n_chunks * n_items][2][slot_floats]
-    const void *zero;     // >= 16 zero bytes: source of copies for absent tokens
-    int32_t fast_tiles;   // seq_len is a multiple of the token tile: tiles never straddle sequences
+    const void *zero;     // >= 256 zero bytes: source of the weights of absent tokens
 };
 
 struct ReduceArgs {
