@@ -2,138 +2,143 @@
 //
 // CacheBridge Sec. 3.1 (Eq. closedform) and Sec. 3.4: the maps are the ridge
 // solutions W~ = (G + lambda D)^{-1} C of the augmented moments.  For each map
-// the workgroup
-//   1. copies the lower triangle of G into LDS as packed fp64 and adds
-//      lambda_m on the diagonal (lambda_m = lambda or lambda * tr(G) / P;
-//      the last diagonal entry is skipped when the bias is not penalized),
-//   2. factors M = L L^T column by column (left-looking; two lanes per row
-//      share each dot product, one barrier per phase),
-//   3. solves L Z = C and L^T W~ = Z on 64-column panels of C held in LDS as
-//      fp64, four lanes per column,
-//   4. writes W~ in fp32 and the per-map status info (0, or the 1-based index
-//      of the first pivot that is not positive and finite; W~ is then zero).
+// the workgroup holds the augmented matrix [M | C], M = G + lambda_m D, in
+// registers as fp64 (512 threads, a cyclic 16 x 32 thread grid, up to 9 x 9
+// elements each) and runs Gauss-Jordan elimination without pivoting:
+//   step k publishes row k and column k through LDS (double buffered, one
+//   barrier per step), and every thread subtracts (A[i][k] / A[k][k]) A[k][j]
+//   from its elements of the other rows.
+// M is symmetric positive definite, for which elimination in the natural
+// order is stable and the pivot of step k is the k-th squared diagonal
+// entry of the Cholesky factor; a pivot that is not positive and finite
+// stops the system with info = k + 1 (1-based) and zero maps, the failure
+// the Cholesky factorization would report at the same column.  At the end
+// row i of the C part divided by the pivot of row i is row i of W~.
+//   lambda_m = lambda, or lambda * tr(G) / P with CB_LAMBDA_RELATIVE; with
+//   CB_RIDGE_BIAS_UNPENALIZED the last (bias) diagonal entry gets no lambda.
 #include "cb_internal.h"
 
 namespace cb {
 namespace {
 
-constexpr int kMaxP = 129;
-constexpr int kPanel = 64;
-constexpr int kPackedMax = kMaxP * (kMaxP + 1) / 2;
-constexpr int kZStride = kPanel + 1;   // fp64 elements per panel row (padded)
+constexpr int kTR = 16, kTC = 32;                 // thread grid: rows x columns
+constexpr int kThreads = kTR * kTC;
+constexpr int kMaxP = 129, kMaxCols = 129 + 128;  // M and C columns
+constexpr int kRA = (kMaxP + kTR - 1) / kTR;      // rows per thread (9)
+constexpr int kCB = (kMaxCols + kTC - 1) / kTC;   // columns per thread (9)
 
-__device__ __forceinline__ int pk(int i, int j) { return i * (i + 1) / 2 + j; }  // j <= i
-
-__global__ __launch_bounds__(256) void ridge_solve_kernel(int P, int d_t, const float *__restrict__ G,
-                                                          const float *__restrict__ C, float lambda,
-                                                          uint32_t flags, float *__restrict__ maps,
-                                                          int32_t *__restrict__ info) {
-    __shared__ double L[kPackedMax];
-    __shared__ double Z[kMaxP * kZStride];
-    __shared__ double red[256];
-    __shared__ int fail;
+__global__ __launch_bounds__(kThreads) void ridge_solve_kernel(int P, int d_t, const float *__restrict__ G,
+                                                               const float *__restrict__ C, float lambda,
+                                                               uint32_t flags, float *__restrict__ maps,
+                                                               int32_t *__restrict__ info) {
+    __shared__ double rowbuf[2][kCB * kTC];
+    __shared__ double colbuf[2][kRA * kTR];
+    __shared__ double red[kThreads / 64];
 
     const int m = blockIdx.x;
     const int tid = threadIdx.x;
+    const int r = tid / kTC, c = tid % kTC;       // element (i, j): i = r + kTR a, j = c + kTC b
+    const int NC = P + d_t;
     const float *Gm = G + (int64_t)m * P * P;
     const float *Cm = C + (int64_t)m * P * d_t;
     float *Wm = maps + (int64_t)m * P * d_t;
 
-    // 1. lower triangle of G -> LDS (fp64), trace
+    // load [G | C] (fp32 -> fp64) and sum the diagonal of G
+    double A[kRA][kCB];
+    double trp = 0.0;
+#pragma unroll
+    for (int a = 0; a < kRA; ++a) {
+        const int i = r + kTR * a;
+#pragma unroll
+        for (int b = 0; b < kCB; ++b) {
+            const int j = c + kTC * b;
+            double v = 0.0;
+            if (i < P && j < NC) v = j < P ? (double)Gm[(int64_t)i * P + j] : (double)Cm[(int64_t)i * d_t + (j - P)];
+            A[a][b] = v;
+            if (i == j && i < P) trp += v;
+        }
+    }
+    // block sum of the trace parts (wave shuffles, then one value per wave)
+    for (int o = 32; o > 0; o >>= 1) trp += __shfl_xor(trp, o);
+    if ((tid & 63) == 0) red[tid >> 6] = trp;
+    __syncthreads();
     double tr = 0.0;
-    for (int idx = tid; idx < P * P; idx += 256) {
-        const int i = idx / P, j = idx - (idx / P) * P;
-        if (j <= i) {
-            const double g = (double)Gm[idx];
-            L[pk(i, j)] = g;
-            if (i == j) tr += g;
-        }
-    }
-    red[tid] = tr;
-    if (tid == 0) fail = 0;
-    __syncthreads();
-    for (int s = 128; s > 0; s >>= 1) {
-        if (tid < s) red[tid] += red[tid + s];
-        __syncthreads();
-    }
-    const double lam = (flags & CB_LAMBDA_RELATIVE) ? (double)lambda * red[0] / (double)P : (double)lambda;
+#pragma unroll
+    for (int w = 0; w < kThreads / 64; ++w) tr += red[w];
+    const double lam = (flags & CB_LAMBDA_RELATIVE) ? (double)lambda * tr / (double)P : (double)lambda;
     const int n_pen = (flags & CB_RIDGE_BIAS_UNPENALIZED) ? P - 1 : P;
-    for (int i = tid; i < n_pen; i += 256) L[pk(i, i)] += lam;
-    __syncthreads();
+#pragma unroll
+    for (int a = 0; a < kRA; ++a)
+#pragma unroll
+        for (int b = 0; b < kCB; ++b) {
+            const int i = r + kTR * a, j = c + kTC * b;
+            if (i == j && i < n_pen) A[a][b] += lam;
+        }
 
-    // 2. Cholesky, left-looking: column j of L from rows i >= j.  Thread t
-    //    takes rows j + t/2 and j + t/2 + 128 (P <= 129), lane pairs split k.
-    const int half = tid & 1;
-    for (int j = 0; j < P; ++j) {
-        double v[2];
+    // Gauss-Jordan elimination
+    int fail = 0;
+    for (int k = 0; k < P; ++k) {
+        double *rb = rowbuf[k & 1];
+        double *cb = colbuf[k & 1];
 #pragma unroll
-        for (int rr = 0; rr < 2; ++rr) {
-            const int i = j + (tid >> 1) + 128 * rr;
-            double s = 0.0;
-            if (i < P) {
-                const double *Li = L + pk(i, 0);
-                const double *Lj = L + pk(j, 0);
-                for (int k = half; k < j; k += 2) s += Li[k] * Lj[k];
-            }
-            s += __shfl_xor(s, 1);
-            v[rr] = (i < P) ? L[pk(i, j)] - s : 0.0;
-        }
-        __syncthreads();                       // all reads of column-j inputs done
-        if (tid == 0) {
-            if (!(v[0] > 0.0) || !isfinite(v[0])) fail = j + 1;
-            else L[pk(j, j)] = sqrt(v[0]);
-        }
-        __syncthreads();
-        if (fail) break;
-        if (half == 0) {
-            const double d = L[pk(j, j)];
+        for (int a = 0; a < kRA; ++a)
+            if (r + kTR * a == k) {
 #pragma unroll
-            for (int rr = 0; rr < 2; ++rr) {
-                const int i = j + (tid >> 1) + 128 * rr;
-                if (i > j && i < P) L[pk(i, j)] = v[rr] / d;
+                for (int b = 0; b < kCB; ++b) rb[c + kTC * b] = A[a][b];
             }
-        }
+#pragma unroll
+        for (int b = 0; b < kCB; ++b)
+            if (c + kTC * b == k) {
+#pragma unroll
+                for (int a = 0; a < kRA; ++a) cb[r + kTR * a] = A[a][b];
+            }
         __syncthreads();
+        const double p = rb[k];
+        if (!(p > 0.0) || !isfinite(p)) {       // same value in every thread
+            fail = k + 1;
+            break;
+        }
+        const double inv = 1.0 / p;
+        double f[kRA], rv[kCB];
+#pragma unroll
+        for (int a = 0; a < kRA; ++a) {
+            const int i = r + kTR * a;
+            f[a] = (i == k || i >= P) ? 0.0 : cb[i] * inv;
+        }
+#pragma unroll
+        for (int b = 0; b < kCB; ++b) rv[b] = rb[c + kTC * b];
+#pragma unroll
+        for (int a = 0; a < kRA; ++a)
+#pragma unroll
+            for (int b = 0; b < kCB; ++b) A[a][b] = __builtin_fma(-f[a], rv[b], A[a][b]);
     }
 
     if (fail) {
-        for (int idx = tid; idx < P * d_t; idx += 256) Wm[idx] = 0.f;
+        for (int idx = tid; idx < P * d_t; idx += kThreads) Wm[idx] = 0.f;
         if (tid == 0) info[m] = fail;
         return;
     }
 
-    // 3. triangular solves on 64-column panels; lane q of each quad sums the
-    //    k == q (mod 4) terms, every lane of the quad writes the result.
-    const int q = tid & 3, col = tid >> 2;
-    for (int p0 = 0; p0 < d_t; p0 += kPanel) {
-        const int ncol = min(kPanel, d_t - p0);
-        __syncthreads();
-        for (int idx = tid; idx < P * kPanel; idx += 256) {
-            const int i = idx / kPanel, c = idx - (idx / kPanel) * kPanel;
-            Z[i * kZStride + c] = c < ncol ? (double)Cm[(int64_t)i * d_t + p0 + c] : 0.0;
+    // W~[i][:] = C part of row i / pivot of row i (the pivots sit on the
+    // diagonal of the eliminated M part; colbuf is free again)
+    __syncthreads();
+#pragma unroll
+    for (int a = 0; a < kRA; ++a)
+#pragma unroll
+        for (int b = 0; b < kCB; ++b) {
+            const int i = r + kTR * a, j = c + kTC * b;
+            if (i == j && i < P) colbuf[0][i] = 1.0 / A[a][b];
         }
-        __syncthreads();
-        // forward: L z = c
-        for (int i = 0; i < P; ++i) {
-            double s = 0.0;
-            const double *Li = L + pk(i, 0);
-            for (int k = q; k < i; k += 4) s += Li[k] * Z[k * kZStride + col];
-            s += __shfl_xor(s, 1);
-            s += __shfl_xor(s, 2);
-            Z[i * kZStride + col] = (Z[i * kZStride + col] - s) / Li[i];
-        }
-        // backward: L^T w = z
-        for (int i = P - 1; i >= 0; --i) {
-            double s = 0.0;
-            for (int k = i + 1 + q; k < P; k += 4) s += L[pk(k, i)] * Z[k * kZStride + col];
-            s += __shfl_xor(s, 1);
-            s += __shfl_xor(s, 2);
-            Z[i * kZStride + col] = (Z[i * kZStride + col] - s) / L[pk(i, i)];
-        }
-        __syncthreads();
-        for (int idx = tid; idx < P * ncol; idx += 256) {
-            const int i = idx / ncol, c = idx - (idx / ncol) * ncol;
-            Wm[(int64_t)i * d_t + p0 + c] = (float)Z[i * kZStride + c];
+    __syncthreads();
+#pragma unroll
+    for (int a = 0; a < kRA; ++a) {
+        const int i = r + kTR * a;
+        if (i >= P) continue;
+        const double inv = colbuf[0][i];
+#pragma unroll
+        for (int b = 0; b < kCB; ++b) {
+            const int j = c + kTC * b;
+            if (j >= P && j < NC) Wm[(int64_t)i * d_t + (j - P)] = (float)(A[a][b] * inv);
         }
     }
     if (tid == 0) info[m] = 0;
@@ -144,7 +149,8 @@ __global__ __launch_bounds__(256) void ridge_solve_kernel(int P, int d_t, const 
 hipError_t launch_solve(int32_t n_maps, int32_t P, int32_t d_t, const float *G, const float *C,
                         float lambda, uint32_t flags, float *maps, int32_t *info, hipStream_t s) {
     if (n_maps == 0) return hipSuccess;
-    hipLaunchKernelGGL(ridge_solve_kernel, dim3(n_maps), dim3(256), 0, s, P, d_t, G, C, lambda, flags,
+    if (P > kMaxP || P + d_t > kMaxCols) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(ridge_solve_kernel, dim3(n_maps), dim3(kThreads), 0, s, P, d_t, G, C, lambda, flags,
                        maps, info);
     return hipGetLastError();
 }
