@@ -418,7 +418,16 @@ cb_status cb_apply(cb_plan *p, const float *maps, const cb_cache *src, const cb_
     a.os = strides_of(tgt_out);
     a.T = cb::make_fastdiv((uint32_t)src->seq_len);
     a.N = (int32_t)N;
-    a.tile_tokens = 1024;
+    // Token tiles of whole 32-token sub-blocks: about 16 workgroups per
+    // compute unit in total, at most 8192 tokens (a workgroup streams its
+    // tile through a ring, so longer tiles amortize the ring's fill).
+    {
+        const int64_t target = 16LL * p->n_cu;
+        int64_t tt = ((int64_t)N * std::max(p->n_groups, 1) + target - 1) / target;
+        tt = std::min<int64_t>(std::max<int64_t>(tt, 256), 8192);
+        tt = (tt + 31) / 32 * 32;
+        a.tile_tokens = (int32_t)tt;
+    }
     a.n_tiles = (int32_t)((N + a.tile_tokens - 1) / a.tile_tokens);
     a.groups = p->d_groups;
     a.w_hi = p->d_whi;

@@ -9,9 +9,9 @@
 // split_maps_kernel: W (fp32) -> W^T as two bf16 planes, hi = RNE(W) and
 //   lo = RNE(W - hi), plus the fp32 bias.  The pair carries ~16 significant
 //   bits, so the bf16 MFMA products match an fp32 product to ~2^-17.
-// apply_kernel: one workgroup per (source block, token tile).  The tile's
-//   source rows are staged in LDS in 32-token sub-blocks (one 128-bit load per
-//   thread, double buffered); wave (slot, rb) keeps its 32 rows of
+// apply_kernel: one workgroup per (source block, token tile).  A copy wave
+//   streams the tile's source rows HBM -> LDS in 32-token sub-blocks through
+//   a ring of direct-to-LDS copies; wave (slot, rb) keeps its 32 rows of
 //   W_hi^T / W_lo^T for its map in registers and computes the 32x32 output
 //   tile D = W^T x^T with v_mfma_f32_32x32x16_bf16 (K = source channels),
 //   adds the bias, rounds once to bf16 and stores 16-byte chunks of target
@@ -73,13 +73,16 @@ template <int DS, int DT>
 struct ACfg {
     static constexpr int KS = DS / 16;              // MFMA K steps over source channels
     static constexpr int RBT = DT / 32;             // 32-row blocks of target channels
-    static constexpr int NW = 2 * RBT, NT = 64 * NW;
+    static constexpr int NWC = 2 * RBT;             // computing waves: (slot, rb)
+    static constexpr int NW = NWC + 1;              // plus one copy wave
+    static constexpr int NT = 64 * NW;
     static constexpr int SB = 32;                   // tokens per sub-block
     static constexpr int NCB = DS / 8;              // 16-byte blocks per source row
     static constexpr int ROWB = DS * 2;             // bytes per source row
-    static constexpr int BUFB = SB * ROWB;          // bytes per sub-block buffer
-    static constexpr int LOADS = SB * NCB;          // 16-byte loads per sub-block
-    static constexpr int LPT = (LOADS + NT - 1) / NT;
+    static constexpr int BUFB = SB * ROWB;          // bytes per ring stage
+    static constexpr int COPIES = BUFB / 1024;      // copy instructions per stage (64 lanes x 16 B)
+    static constexpr int NST = 8;                   // ring stages
+    static_assert(BUFB % 1024 == 0, "a stage is a whole number of copy instructions");
 };
 
 // Rotated position of 16-byte block cb of token row t in LDS: 16 consecutive
@@ -89,35 +92,83 @@ __device__ __forceinline__ uint32_t xoff(uint32_t t, uint32_t cb) {
     return t * (NCB * 16) + ((cb + t) % NCB) * 16;
 }
 
+// HBM -> LDS copy of 16 bytes per lane to M0 + 16 lane (direct-to-LDS load).
+// M0 is saved and restored inside the statement.
+__device__ __forceinline__ void dma16(const void *gaddr, uint32_t m0) {
+    uint32_t keep;
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
+                 : "=&s"(keep)
+                 : "v"(gaddr), "s"(m0)
+                 : "memory");
+}
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// One workgroup per (group, token tile).  The copy wave streams 32-token
+// sub-blocks of the group's source rows HBM -> LDS through an NST-stage ring
+// (NST - 1 sub-blocks ahead); since it issues nothing but these copies, its
+// vmcnt waits are exact.  One barrier per sub-block publishes the landed
+// stage to the computing waves and tells the copy wave that the stage read
+// one sub-block earlier is free again.
 template <int DS, int DT>
-__global__ __attribute__((amdgpu_flat_work_group_size(ACfg<DS, DT>::NT, ACfg<DS, DT>::NT),
-                          amdgpu_waves_per_eu(2, 2)))
-void apply_kernel(ApplyArgs a) {
+__global__ __attribute__((amdgpu_flat_work_group_size(ACfg<DS, DT>::NT, ACfg<DS, DT>::NT))) void apply_kernel(ApplyArgs a) {
     using K = ACfg<DS, DT>;
-    __shared__ __attribute__((aligned(16))) char lds[2 * K::BUFB];
+    __shared__ __attribute__((aligned(16))) char lds[K::NST * K::BUFB];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int slot = wave / K::RBT, rb = wave % K::RBT;
     const int g = blockIdx.x / a.n_tiles;
     const int tile = blockIdx.x % a.n_tiles;
-    const ApplyGroup grp = a.groups[g];
-    const bool active = slot < grp.n_slots;
+    const ApplyGroup *grp = a.groups + g;                     // read field by field (uniform)
     const int tok0 = tile * a.tile_tokens;
     const int tok1 = min(a.N, tok0 + a.tile_tokens);
     const int n_sb = (tok1 - tok0 + K::SB - 1) / K::SB;
+    if (n_sb <= 0) return;
+    const int kv = grp->kv;
+    const uint16_t *xsrc = a.src + grp->src_layer * a.ss.layer + kv * a.ss.kv + grp->src_head * a.ss.head;
 
-    const uint16_t *xsrc = a.src + grp.src_layer * a.ss.layer + grp.kv * a.ss.kv + grp.src_head * a.ss.head;
-    const int m = grp.map[slot < grp.n_slots ? slot : 0];
-    uint16_t *obase = a.out + grp.tgt_layer[slot < grp.n_slots ? slot : 0] * a.os.layer + grp.kv * a.os.kv +
-                      grp.tgt_head[slot < grp.n_slots ? slot : 0] * a.os.head + rb * 32;
+    if (wave == K::NWC) {
+        // ---- copy wave: copy i of a stage moves LDS chunks 64 i + lane
+        const uint32_t lds_base = (uint32_t)(uintptr_t)lds;
+        auto issue = [&](int sb, int st) {
+#pragma unroll
+            for (int i = 0; i < K::COPIES; ++i) {
+                const int q = 64 * i + lane;
+                const int t = q / K::NCB, p = q - (q / K::NCB) * K::NCB;
+                const int cb = (p + K::NCB - t % K::NCB) % K::NCB;     // inverse of the rotation
+                const int tau = min(tok0 + sb * K::SB + t, tok1 - 1);  // past the tile: any valid row
+                const uint32_t b = fastdiv((uint32_t)tau, a.T);
+                const uint32_t tt = (uint32_t)tau - b * a.T.d;
+                const uint16_t *src = xsrc + (int64_t)b * a.ss.seq + (int64_t)tt * a.ss.tok + cb * 8;
+                dma16(src, __builtin_amdgcn_readfirstlane(lds_base + st * K::BUFB + i * 1024));
+            }
+        };
+#pragma unroll
+        for (int s = 0; s < K::NST - 1; ++s) issue(s, s);
+        for (int sb = 0; sb < n_sb; ++sb) {
+            wait_vm<(K::NST - 2) * K::COPIES>();               // sub-block sb has landed
+            lds_barrier();
+            issue(sb + K::NST - 1, (sb + K::NST - 1) % K::NST);
+        }
+        wait_vm<0>();                                          // drain before the LDS is released
+        return;
+    }
+
+    // ---- computing wave (slot, rb)
+    const int slot = wave / K::RBT, rb = wave % K::RBT;
+    const bool active = slot < grp->n_slots;
+    const int sl = active ? slot : 0;
+    const int m = grp->map[sl];
+    uint16_t *obase = a.out + grp->tgt_layer[sl] * a.os.layer + kv * a.os.kv + grp->tgt_head[sl] * a.os.head + rb * 32;
 
     // coefficients of this wave's 32 target channels, kept in registers
     const uint32_t lrow = lane & 31, lhalf = lane >> 5;
     bf16x8_t ahi[K::KS], alo[K::KS];
     float bias[16];
-    if (active) {
+    {
         const uint16_t *wh = a.w_hi + ((int64_t)m * DT + rb * 32 + lrow) * DS + 8 * lhalf;
         const uint16_t *wl = a.w_lo + ((int64_t)m * DT + rb * 32 + lrow) * DS + 8 * lhalf;
 #pragma unroll
@@ -136,85 +187,49 @@ void apply_kernel(ApplyArgs a) {
         }
     }
 
-    uint4 stage[K::LPT];
-    auto load_sb = [&](int sb) {
-        const int t0 = tok0 + sb * K::SB;
+    for (int sb = 0; sb < n_sb; ++sb) {
+        lds_barrier();                                         // sub-block sb has landed
+        if (!active) continue;
+        const char *B = lds + (sb % K::NST) * K::BUFB;
+        // hi and lo terms in two accumulators: two independent MFMA chains
+        f32x16_t acc, acl;
 #pragma unroll
-        for (int s = 0; s < K::LPT; ++s) {
-            const int i = tid + s * K::NT;
-            uint4 v = make_uint4(0, 0, 0, 0);
-            if (i < K::LOADS) {
-                const int t = i / K::NCB, cb = i % K::NCB;
-                const int tau = t0 + t;
-                if (tau < tok1) {
-                    const uint32_t b = fastdiv((uint32_t)tau, a.T);
-                    const uint32_t tt = (uint32_t)tau - b * a.T.d;
-                    v = *reinterpret_cast<const uint4 *>(xsrc + (int64_t)b * a.ss.seq + (int64_t)tt * a.ss.tok + cb * 8);
-                }
-            }
-            stage[s] = v;
+        for (int v = 0; v < 16; ++v) acc[v] = acl[v] = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < K::KS; ++ks) {
+            const bf16x8_t bx = *reinterpret_cast<const bf16x8_t *>(B + xoff<K::NCB>(lrow, 2 * ks + lhalf));
+            acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ahi[ks], bx, acc, 0, 0, 0);
+            acl = __builtin_amdgcn_mfma_f32_32x32x16_bf16(alo[ks], bx, acl, 0, 0, 0);
         }
-    };
-    auto store_sb = [&](int buf) {
-        char *B = lds + buf * K::BUFB;
 #pragma unroll
-        for (int s = 0; s < K::LPT; ++s) {
-            const int i = tid + s * K::NT;
-            if (i < K::LOADS) {
-                const int t = i / K::NCB, cb = i % K::NCB;
-                *reinterpret_cast<uint4 *>(B + xoff<K::NCB>(t, cb)) = stage[s];
-            }
+        for (int v = 0; v < 16; ++v) acc[v] += acl[v];
+        // D[i][t]: t = lane & 31, i = 8*(v/4) + 4*(lane/32) + (v&3)
+        uint32_t pk[8];
+#pragma unroll
+        for (int gq = 0; gq < 4; ++gq) {
+            pk[2 * gq] = pack_bf16(acc[4 * gq + 0] + bias[4 * gq + 0], acc[4 * gq + 1] + bias[4 * gq + 1]);
+            pk[2 * gq + 1] = pack_bf16(acc[4 * gq + 2] + bias[4 * gq + 2], acc[4 * gq + 3] + bias[4 * gq + 3]);
         }
-    };
-
-    if (n_sb > 0) {
-        load_sb(0);
-        store_sb(0);
-        lds_barrier();
-        for (int sb = 0; sb < n_sb; ++sb) {
-            if (sb + 1 < n_sb) load_sb(sb + 1);
-            if (active) {
-                const char *B = lds + (sb & 1) * K::BUFB;
-                f32x16_t acc;
+        // Exchange with lane ^ 32 so that each lane owns 8 consecutive
+        // channels: lanes < 32 get channels 0-7 and 16-23, lanes >= 32 get
+        // 8-15 and 24-31 of the 32-channel block.
+        uint4 o[2];
 #pragma unroll
-                for (int v = 0; v < 16; ++v) acc[v] = 0.f;
-#pragma unroll
-                for (int ks = 0; ks < K::KS; ++ks) {
-                    const bf16x8_t bx = *reinterpret_cast<const bf16x8_t *>(B + xoff<K::NCB>(lrow, 2 * ks + lhalf));
-                    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ahi[ks], bx, acc, 0, 0, 0);
-                    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(alo[ks], bx, acc, 0, 0, 0);
-                }
-                // D[i][t]: t = lane & 31, i = 8*(v/4) + 4*(lane/32) + (v&3)
-                uint32_t pk[8];
-#pragma unroll
-                for (int gq = 0; gq < 4; ++gq) {
-                    pk[2 * gq] = pack_bf16(acc[4 * gq + 0] + bias[4 * gq + 0], acc[4 * gq + 1] + bias[4 * gq + 1]);
-                    pk[2 * gq + 1] = pack_bf16(acc[4 * gq + 2] + bias[4 * gq + 2], acc[4 * gq + 3] + bias[4 * gq + 3]);
-                }
-                // Exchange with lane ^ 32 so that each lane owns 8 consecutive
-                // channels: lanes < 32 get channels 0-7 and 16-23, lanes >= 32
-                // get 8-15 and 24-31 of the 32-channel block.
-                uint4 o[2];
-#pragma unroll
-                for (int p = 0; p < 2; ++p) {
-                    const uint32_t s0 = lhalf ? pk[4 * p + 0] : pk[4 * p + 2];
-                    const uint32_t s1 = lhalf ? pk[4 * p + 1] : pk[4 * p + 3];
-                    const uint32_t r0 = (uint32_t)__shfl_xor((int)s0, 32);
-                    const uint32_t r1 = (uint32_t)__shfl_xor((int)s1, 32);
-                    o[p] = lhalf ? make_uint4(r0, r1, pk[4 * p + 2], pk[4 * p + 3])
-                                 : make_uint4(pk[4 * p + 0], pk[4 * p + 1], r0, r1);
-                }
-                const int tau = tok0 + sb * K::SB + (int)lrow;
-                if (tau < tok1) {
-                    const uint32_t b = fastdiv((uint32_t)tau, a.T);
-                    const uint32_t tt = (uint32_t)tau - b * a.T.d;
-                    uint16_t *orow = obase + (int64_t)b * a.os.seq + (int64_t)tt * a.os.tok + 8 * lhalf;
-                    *reinterpret_cast<uint4 *>(orow) = o[0];
-                    *reinterpret_cast<uint4 *>(orow + 16) = o[1];
-                }
-            }
-            if (sb + 1 < n_sb) store_sb((sb + 1) & 1);
-            lds_barrier();
+        for (int p = 0; p < 2; ++p) {
+            const uint32_t s0 = lhalf ? pk[4 * p + 0] : pk[4 * p + 2];
+            const uint32_t s1 = lhalf ? pk[4 * p + 1] : pk[4 * p + 3];
+            const uint32_t r0 = (uint32_t)__shfl_xor((int)s0, 32);
+            const uint32_t r1 = (uint32_t)__shfl_xor((int)s1, 32);
+            o[p] = lhalf ? make_uint4(r0, r1, pk[4 * p + 2], pk[4 * p + 3])
+                         : make_uint4(pk[4 * p + 0], pk[4 * p + 1], r0, r1);
+        }
+        const int tau = tok0 + sb * K::SB + (int)lrow;
+        if (tau < tok1) {
+            const uint32_t b = fastdiv((uint32_t)tau, a.T);
+            const uint32_t tt = (uint32_t)tau - b * a.T.d;
+            uint16_t *orow = obase + (int64_t)b * a.os.seq + (int64_t)tt * a.os.tok + 8 * lhalf;
+            *reinterpret_cast<uint4 *>(orow) = o[0];
+            *reinterpret_cast<uint4 *>(orow + 16) = o[1];
         }
     }
 }
