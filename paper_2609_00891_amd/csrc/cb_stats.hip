@@ -166,21 +166,6 @@ template <> struct Own<2, 1> {
     static constexpr int gr[5] = {0, 0, 0, 0, 0}, gx[5] = {0, 0, 0, 0, 0};
 };
 
-// Gram tile slot of block (a, b) in the partial layout (pair 0's tiles, then
-// pair 1's), or -1 when that block is stored as its transpose (b, a).
-template <int RB>
-__device__ __forceinline__ int gram_slot(int a, int b) {
-    using O0 = Own<RB, 0>;
-    using O1 = Own<RB, 1>;
-#pragma unroll
-    for (int g = 0; g < O0::NG; ++g)
-        if (O0::row[O0::gr[g]] == a && O0::xc[O0::gx[g]] == b) return g;
-#pragma unroll
-    for (int g = 0; g < O1::NG; ++g)
-        if (O1::row[O1::gr[g]] == a && O1::xc[O1::gx[g]] == b) return O0::NG + g;
-    return -1;
-}
-
 // HBM -> LDS copies.  The LDS destination of lane l is M0 + 16 l (4 l for the
 // dword form).  They are issued through inline assembly so that the compiler
 // does not add its own conservative waits between them and the LDS reads of
@@ -717,53 +702,106 @@ void stats_kernel(StatsArgs a) {
 #undef CB_WAVE
 }
 
+// Block (a, b) of Gram tile slot k in the partial layout (pair 0's tiles,
+// then pair 1's).
+template <int RB>
+__device__ __forceinline__ void gram_block(int k, int &a, int &b) {
+    using O0 = Own<RB, 0>;
+    using O1 = Own<RB, 1>;
+    a = b = 0;
+#pragma unroll
+    for (int g = 0; g < O0::NG; ++g)
+        if (k == g) { a = O0::row[O0::gr[g]]; b = O0::xc[O0::gx[g]]; }
+#pragma unroll
+    for (int g = 0; g < O1::NG; ++g)
+        if (k == O0::NG + g) { a = O1::row[O1::gr[g]]; b = O1::xc[O1::gx[g]]; }
+}
+
+// One workgroup per (map, job): jobs 0 .. NTG-1 are the Gram tiles, NTG ..
+// NTG+NTC-1 the cross tiles, the last one the bias sums.  A tile's partials
+// are summed over the chunks in a fixed order (coalesced reads of the [v][lane]
+// accumulator layout) and added into G / C; an off-diagonal Gram tile is also
+// added, transposed through LDS, into the mirrored block, and a diagonal one
+// only contributes its upper triangle (mirrored), so G is exactly symmetric.
 template <int DS, int DT>
 __global__ __launch_bounds__(256) void reduce_kernel(ReduceArgs a) {
     using K = Cfg<DS, DT>;
     constexpr int P = DS + 1;
-    const int m = blockIdx.x;
+    __shared__ float tile[32][33];
+    const int m = blockIdx.x, job = blockIdx.y;
+    const int tid = threadIdx.x;
     const int item = a.map_item[m], slot = a.map_slot[m];
     float *G = a.G + (int64_t)m * P * P;
     float *Cm = a.C + (int64_t)m * P * DT;
     const int64_t chunk_stride = (int64_t)a.n_items * 2 * K::SLOT;
     const float *base = a.partials + ((int64_t)item * 2 + slot) * K::SLOT;
-    for (int e = threadIdx.x; e < P * P + P * DT; e += blockDim.x) {
-        int i0, i1 = -1;
-        float *dst;
-        if (e < P * P) {
-            const int i = e / P, j = e - (e / P) * P;
-            const int r = min(i, j), c = max(i, j);
-            if (c < DS) {
-                const int br = r >> 5, bc = c >> 5;
-                const int k = gram_slot<K::RB>(br, bc);
-                if (k >= 0) i0 = acc_index(k, r & 31, c & 31);
-                else i0 = acc_index(gram_slot<K::RB>(bc, br), c & 31, r & 31);
-            } else if (r < DS) {
-                i0 = K::SUMX + (r >> 5) * 64 + (r & 31);
-                i1 = i0 + 32;
-            } else {
-                i0 = K::SUMW;
-                i1 = K::SUMW + 32;
-            }
-            dst = G + e;
-        } else {
-            const int f = e - P * P;
-            const int i = f / DT, j = f - (f / DT) * DT;
-            if (i < DS) {
-                i0 = acc_index(K::NTG + (i >> 5) * K::RBT + (j >> 5), i & 31, j & 31);
-            } else {
-                i0 = K::SUMY + (j >> 5) * 64 + (j & 31);
-                i1 = i0 + 32;
-            }
-            dst = Cm + f;
+
+    if (job < K::NTG + K::NTC) {
+        float sum[4];
+        int ii[4], jj[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int f = tid + 256 * q;                      // [v][lane] position in the tile
+            const int v = f >> 6, l = f & 63;
+            ii[q] = 8 * (v >> 2) + 4 * (l >> 5) + (v & 3);
+            jj[q] = l & 31;
+            float acc = 0.f;
+            for (int ch = 0; ch < a.n_chunks; ++ch) acc += base[ch * chunk_stride + job * 1024 + f];
+            sum[q] = acc;
         }
-        float s = 0.f;
+        if (job >= K::NTG) {
+            const int c = job - K::NTG, rb = c / K::RBT, cb = c - (c / K::RBT) * K::RBT;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) Cm[(rb * 32 + ii[q]) * DT + cb * 32 + jj[q]] += sum[q];
+            return;
+        }
+        int ba, bb;
+        gram_block<K::RB>(job, ba, bb);
+        if (ba == bb) {
+            // upper triangle of the diagonal block and its mirror
+#pragma unroll
+            for (int q = 0; q < 4; ++q) tile[ii[q]][jj[q]] = sum[q];
+            __syncthreads();
+            for (int e = tid; e < 1024; e += 256) {
+                const int i = e >> 5, j = e & 31;
+                const float val = i <= j ? tile[i][j] : tile[j][i];
+                G[(ba * 32 + i) * P + ba * 32 + j] += val;
+            }
+            return;
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            G[(ba * 32 + ii[q]) * P + bb * 32 + jj[q]] += sum[q];
+            tile[jj[q]][ii[q]] = sum[q];
+        }
+        __syncthreads();
+        for (int e = tid; e < 1024; e += 256) {
+            const int i = e >> 5, j = e & 31;               // row bb*32 + i, column ba*32 + j
+            G[(bb * 32 + i) * P + ba * 32 + j] += tile[i][j];
+        }
+        return;
+    }
+
+    // bias sums: row / column P-1 of G and row P-1 of C (two lane halves each)
+    for (int e = tid; e < DS + DT + 1; e += 256) {
+        int i0;
+        if (e < DS) i0 = K::SUMX + (e >> 5) * 64 + (e & 31);
+        else if (e < DS + DT) i0 = K::SUMY + ((e - DS) >> 5) * 64 + ((e - DS) & 31);
+        else i0 = K::SUMW;
+        float acc = 0.f;
         for (int ch = 0; ch < a.n_chunks; ++ch) {
-            const float *p = base + ch * chunk_stride;
-            s += p[i0];
-            if (i1 >= 0) s += p[i1];
+            const float *pp = base + ch * chunk_stride;
+            acc += pp[i0];
+            acc += pp[i0 + 32];
         }
-        *dst += s;
+        if (e < DS) {
+            G[(int64_t)(P - 1) * P + e] += acc;
+            G[(int64_t)e * P + (P - 1)] += acc;
+        } else if (e < DS + DT) {
+            Cm[(int64_t)(P - 1) * DT + (e - DS)] += acc;
+        } else {
+            G[(int64_t)(P - 1) * P + (P - 1)] += acc;
+        }
     }
 }
 
@@ -787,7 +825,8 @@ hipError_t launch_stats_t(const StatsArgs &a, hipStream_t s) {
 template <int DS, int DT>
 hipError_t launch_reduce_t(const ReduceArgs &a, hipStream_t s) {
     if (a.n_maps == 0) return hipSuccess;
-    hipLaunchKernelGGL((reduce_kernel<DS, DT>), dim3(a.n_maps), dim3(256), 0, s, a);
+    using K = Cfg<DS, DT>;
+    hipLaunchKernelGGL((reduce_kernel<DS, DT>), dim3(a.n_maps, K::NTG + K::NTC + 1), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
