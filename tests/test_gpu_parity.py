@@ -206,6 +206,34 @@ def test_widths_ragged_tokens_and_shared_sources(cb, d_s, d_t):
     plan.close()
 
 
+@pytest.mark.parametrize("d_s,d_t,T", [(64, 64, 45), (96, 128, 64), (128, 128, 96)])
+def test_single_map_items(cb, d_s, d_t, T):
+    # Three maps on three different source blocks: the plan pairs two of them
+    # and leaves an item with a single map, whose other waves only copy.
+    wl = synth.Workload("single", 1, 2, d_s, 1, 2, d_t, 3, T, "identity", "scaled", 0.1, "lognormal")
+    src, tgt, w = make_inputs(wl)
+    full = synth.head_map(wl)
+    keep = [0, 1, 3]
+    hm = {k: np.ascontiguousarray(np.asarray(v)[keep]) for k, v in full.items()}
+    plan = cb.cb_plan_create(hm, src, tgt, 4096)
+    G, C = gpu_stats(cb, plan, src, tgt, w)
+    sel = list(range(len(keep)))
+    Go, Co = oracle_stats_sel(hm, sel, src, tgt, w)
+    check_stats(G, C, Go, Co, sel)
+    maps, info = gpu_solve(cb, G, C)
+    assert (info.cpu().numpy() == 0).all()
+    Wo, _ = oracle.ridge_solve(Go, Co, 1e-2, relative=True)
+    assert max(relF(maps[i].double().cpu().numpy(), Wo[i]) for i in sel) <= TOL_MAPS
+    out = torch.zeros_like(tgt)
+    cb.cb_apply(plan, maps, src, out)
+    torch.cuda.synchronize()
+    ref = np.zeros(tuple(out.shape), dtype=np.uint16)
+    oracle.apply(hm, maps.double().cpu().numpy(), bits(src), src.stride()[:5], d_s, ref, out.stride()[:5],
+                 d_t, wl.n_seqs, wl.seq_len)
+    check_apply(bits(out).reshape(ref.shape), ref)
+    plan.close()
+
+
 def test_strided_views_match_canonical_layout(cb):
     wl = synth.Workload("strided", 2, 2, 128, 2, 2, 128, 2, 130, "qwen", "scaled", 0.1, "lognormal")
     src, tgt, w = make_inputs(wl)
