@@ -12,6 +12,10 @@ Transfer"):
 * :func:`stats` -- augmented weighted moments G, C (Sec. 3.4, Eq. fusedstats,
   over the head-local feature of Sec. 3.2, Eq. localfeature, with k = 1).
 * :func:`ridge_solve` -- (G + lambda D)^-1 C (Sec. 3.1, Eq. closedform; Sec. 3.4).
+* :func:`stats_centered` -- two-pass weighted means and centered moments A, B
+  (Sec. 3.4, Eq. fusedstats as stated: means first, then centered panels).
+* :func:`ridge_solve_centered` -- W = (A + lambda I)^-1 B, b = mu_y - W^T mu_x
+  (Sec. 3.1, Eq. closedform).
 * :func:`apply` -- RNE_bf16([x;1] W~) per token (Sec. 1; Sec. 2.3, Eq. support-cost).
 * :func:`coefficient_count` -- C(f) = 2 L_t H_t (k f d_s) d_t (Sec. 2.3, Eq. support-cost).
 
@@ -58,6 +62,13 @@ def _load():
     lib.oracle_apply.argtypes = [ctypes.c_int] + [_i32p] * 5 + [
         _f64p, _u16p, _i64p, ctypes.c_int, _u16p, _i64p, ctypes.c_int,
         ctypes.c_int, ctypes.c_int, ctypes.c_int]
+    lib.oracle_stats_centered.restype = ctypes.c_int
+    lib.oracle_stats_centered.argtypes = [ctypes.c_int] + [_i32p] * 6 + [
+        _u16p, _i64p, ctypes.c_int, _u16p, _i64p, ctypes.c_int,
+        _f32p, ctypes.c_int64, ctypes.c_int, ctypes.c_int, _f64p, _f64p, _f64p, ctypes.c_int]
+    lib.oracle_ridge_solve_centered.restype = ctypes.c_int
+    lib.oracle_ridge_solve_centered.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, _f64p, _f64p, _f64p,
+                                                ctypes.c_double, ctypes.c_int, _f64p, _i32p, ctypes.c_int]
     lib.oracle_double_to_bf16_array.restype = ctypes.c_int
     lib.oracle_double_to_bf16_array.argtypes = [ctypes.c_int64, _f64p, _u16p]
     _lib = lib
@@ -136,6 +147,46 @@ def ridge_solve(G, C, lam, relative=True, bias_unpenalized=False, n_threads: int
     lib.oracle_ridge_solve(n, P, d_t, _ptr(G, _f64p), _ptr(C, _f64p), float(lam), int(bool(relative)),
                            int(bool(bias_unpenalized)), _ptr(W, _f64p), _ptr(info, _i32p),
                            int(n_threads))
+    return W, info
+
+
+def stats_centered(head_map, src, src_strides, d_s, tgt, tgt_strides, d_t, weights, w_row_stride,
+                   n_seqs, seq_len, n_threads: int = 0):
+    """Two-pass centered statistics in fp64: returns (sums, A, B) with
+    sums[m] = (sum w, sum w x, sum w y), A[m] = sum w (x-mu_x)(x-mu_x)^T and
+    B[m] = sum w (x-mu_x)(y-mu_y)^T.  Same input conventions as :func:`stats`."""
+    lib = _load()
+    n, hm = _hm_arrays(head_map)
+    sums = np.zeros((n, 1 + d_s + d_t), dtype=np.float64)
+    A = np.zeros((n, d_s, d_s), dtype=np.float64)
+    B = np.zeros((n, d_s, d_t), dtype=np.float64)
+    src = np.ascontiguousarray(_u16(src))
+    tgt = np.ascontiguousarray(_u16(tgt))
+    w = np.ascontiguousarray(np.asarray(weights, dtype=np.float32))
+    ss, ts = _strides5(src_strides), _strides5(tgt_strides)
+    lib.oracle_stats_centered(n, *[_ptr(a, _i32p) for a in hm], _ptr(src, _u16p), _ptr(ss, _i64p), d_s,
+                              _ptr(tgt, _u16p), _ptr(ts, _i64p), d_t, _ptr(w, _f32p), int(w_row_stride),
+                              int(n_seqs), int(seq_len), _ptr(sums, _f64p), _ptr(A, _f64p), _ptr(B, _f64p),
+                              int(n_threads))
+    return sums, A, B
+
+
+def ridge_solve_centered(sums, A, B, lam, relative=True, n_threads: int = 0):
+    """Centered ridge: W = (A + lambda_m I)^-1 B, b = mu_y - W^T mu_x; returns
+    (W~ [n][d_s+1][d_t] with the bias as the last row, info)."""
+    lib = _load()
+    sums = np.ascontiguousarray(np.asarray(sums, dtype=np.float64))
+    A = np.ascontiguousarray(np.asarray(A, dtype=np.float64))
+    B = np.ascontiguousarray(np.asarray(B, dtype=np.float64))
+    n, d_s, d_s2 = A.shape
+    assert d_s == d_s2 and B.shape[:2] == (n, d_s)
+    d_t = B.shape[2]
+    assert sums.shape == (n, 1 + d_s + d_t)
+    W = np.zeros((n, d_s + 1, d_t), dtype=np.float64)
+    info = np.zeros((n,), dtype=np.int32)
+    lib.oracle_ridge_solve_centered(n, d_s, d_t, _ptr(sums, _f64p), _ptr(A, _f64p), _ptr(B, _f64p),
+                                    float(lam), int(bool(relative)), _ptr(W, _f64p), _ptr(info, _i32p),
+                                    int(n_threads))
     return W, info
 
 

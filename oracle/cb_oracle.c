@@ -209,6 +209,139 @@ int oracle_ridge_solve(int n_maps, int P, int d_t, const double *G, const double
 }
 
 /*
+ * Two-pass centered statistics of Sec. 3.4 for every map: pass 1 accumulates
+ * sum w, sum w x, sum w y over all tokens; pass 2 revisits the tokens and
+ * accumulates A = sum w (x - mu_x)(x - mu_x)^T and B = sum w (x - mu_x)(y - mu_y)^T
+ * with the means of pass 1.  Outputs (overwritten, fp64):
+ *   sums [n_maps][1 + d_s + d_t] = (sum w, sum w x, sum w y),
+ *   A [n_maps][d_s][d_s], B [n_maps][d_s][d_t].
+ * A map whose weights sum to zero gets zero means.  Returns 0.
+ */
+int oracle_stats_centered(int n_maps,
+                          const int32_t *tgt_layer, const int32_t *tgt_head, const int32_t *kv,
+                          const int32_t *src_layer, const int32_t *src_head, const int32_t *weight_row,
+                          const uint16_t *src, const int64_t *src_strides, int d_s,
+                          const uint16_t *tgt, const int64_t *tgt_strides, int d_t,
+                          const float *weights, int64_t w_row_stride,
+                          int n_seqs, int seq_len,
+                          double *sums, double *A, double *B, int n_threads) {
+    const int NS = 1 + d_s + d_t;
+    set_threads(n_threads);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int m = 0; m < n_maps; ++m) {
+        double *sm = sums + (int64_t)m * NS;
+        double *Am = A + (int64_t)m * d_s * d_s;
+        double *Bm = B + (int64_t)m * d_s * d_t;
+        double *x = (double *)malloc(sizeof(double) * (size_t)d_s);
+        double *y = (double *)malloc(sizeof(double) * (size_t)d_t);
+        memset(sm, 0, sizeof(double) * (size_t)NS);
+        memset(Am, 0, sizeof(double) * (size_t)d_s * d_s);
+        memset(Bm, 0, sizeof(double) * (size_t)d_s * d_t);
+        /* pass 1: weighted sums */
+        for (int b = 0; b < n_seqs; ++b) {
+            for (int t = 0; t < seq_len; ++t) {
+                const uint16_t *xr = src + row_offset(src_strides, src_layer[m], kv[m], b, src_head[m], t);
+                const uint16_t *yr = tgt + row_offset(tgt_strides, tgt_layer[m], kv[m], b, tgt_head[m], t);
+                const double w = (double)weights[(int64_t)weight_row[m] * w_row_stride +
+                                                 (int64_t)b * seq_len + t];
+                sm[0] += w;
+                for (int i = 0; i < d_s; ++i) sm[1 + i] += w * bf16_bits_to_double(xr[i]);
+                for (int j = 0; j < d_t; ++j) sm[1 + d_s + j] += w * bf16_bits_to_double(yr[j]);
+            }
+        }
+        const double sw = sm[0];
+        /* pass 2: centered moments */
+        for (int b = 0; b < n_seqs; ++b) {
+            for (int t = 0; t < seq_len; ++t) {
+                const uint16_t *xr = src + row_offset(src_strides, src_layer[m], kv[m], b, src_head[m], t);
+                const uint16_t *yr = tgt + row_offset(tgt_strides, tgt_layer[m], kv[m], b, tgt_head[m], t);
+                const double w = (double)weights[(int64_t)weight_row[m] * w_row_stride +
+                                                 (int64_t)b * seq_len + t];
+                for (int i = 0; i < d_s; ++i)
+                    x[i] = bf16_bits_to_double(xr[i]) - (sw != 0.0 ? sm[1 + i] / sw : 0.0);
+                for (int j = 0; j < d_t; ++j)
+                    y[j] = bf16_bits_to_double(yr[j]) - (sw != 0.0 ? sm[1 + d_s + j] / sw : 0.0);
+                for (int i = 0; i < d_s; ++i) {
+                    const double wi = w * x[i];
+                    for (int j = 0; j < d_s; ++j) Am[(int64_t)i * d_s + j] += wi * x[j];
+                    for (int j = 0; j < d_t; ++j) Bm[(int64_t)i * d_t + j] += wi * y[j];
+                }
+            }
+        }
+        free(x);
+        free(y);
+    }
+    return 0;
+}
+
+/*
+ * Centered ridge solve (Sec. 3.1, Eq. closedform) in fp64:
+ *   W = (A + lambda_m I)^{-1} B  (Cholesky),  b = mu_y - W^T mu_x,
+ * written as W~ [n_maps][d_s + 1][d_t] (rows 0..d_s-1 = W, row d_s = b^T).
+ * lambda_m as in the file comment; info as in oracle_ridge_solve (first pivot of
+ * A + lambda_m I that is not positive and finite, 1-based; W~ zero-filled).
+ */
+int oracle_ridge_solve_centered(int n_maps, int d_s, int d_t, const double *sums, const double *A,
+                                const double *B, double lambda, int lambda_relative,
+                                double *W, int32_t *info, int n_threads) {
+    const int NS = 1 + d_s + d_t, P = d_s + 1;
+    set_threads(n_threads);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int m = 0; m < n_maps; ++m) {
+        const double *sm = sums + (int64_t)m * NS;
+        const double *Am = A + (int64_t)m * d_s * d_s;
+        const double *Bm = B + (int64_t)m * d_s * d_t;
+        double *Wm = W + (int64_t)m * P * d_t;
+        double *L = (double *)calloc((size_t)d_s * d_s, sizeof(double));
+        double *Z = (double *)calloc((size_t)d_s * d_t, sizeof(double));
+        const double sw = sm[0];
+        double tr = sw;
+        for (int i = 0; i < d_s; ++i) {
+            const double mu = sw != 0.0 ? sm[1 + i] / sw : 0.0;
+            tr += Am[(int64_t)i * d_s + i] + sw * mu * mu;
+        }
+        const double lam = lambda_relative ? lambda * tr / (double)P : lambda;
+        int bad = 0;
+        for (int i = 0; i < d_s && !bad; ++i) {
+            for (int j = 0; j <= i; ++j) {
+                double s = Am[(int64_t)i * d_s + j];
+                if (i == j) s += lam;
+                for (int k = 0; k < j; ++k) s -= L[(int64_t)i * d_s + k] * L[(int64_t)j * d_s + k];
+                if (i == j) {
+                    if (!(s > 0.0) || !isfinite(s)) { bad = i + 1; break; }
+                    L[(int64_t)i * d_s + i] = sqrt(s);
+                } else {
+                    L[(int64_t)i * d_s + j] = s / L[(int64_t)j * d_s + j];
+                }
+            }
+        }
+        info[m] = bad;
+        if (bad) {
+            memset(Wm, 0, sizeof(double) * (size_t)P * d_t);
+        } else {
+            for (int c = 0; c < d_t; ++c) {
+                for (int i = 0; i < d_s; ++i) {
+                    double s = Bm[(int64_t)i * d_t + c];
+                    for (int k = 0; k < i; ++k) s -= L[(int64_t)i * d_s + k] * Z[(int64_t)k * d_t + c];
+                    Z[(int64_t)i * d_t + c] = s / L[(int64_t)i * d_s + i];
+                }
+                for (int i = d_s - 1; i >= 0; --i) {
+                    double s = Z[(int64_t)i * d_t + c];
+                    for (int k = i + 1; k < d_s; ++k) s -= L[(int64_t)k * d_s + i] * Wm[(int64_t)k * d_t + c];
+                    Wm[(int64_t)i * d_t + c] = s / L[(int64_t)i * d_s + i];
+                }
+                double bias = sw != 0.0 ? sm[1 + d_s + c] / sw : 0.0;
+                for (int i = 0; i < d_s; ++i) bias -= Wm[(int64_t)i * d_t + c] * (sw != 0.0 ? sm[1 + i] / sw : 0.0);
+                Wm[(int64_t)d_s * d_t + c] = bias;
+            }
+        }
+        free(L);
+        free(Z);
+    }
+    return 0;
+}
+
+/*
  * Online application of the fitted maps.
  *   W [n_maps][P][d_t] (fp64 copies of the coefficients; row d_s is the bias)
  *   out[tgt_layer, kv, seq, tgt_head, tok, j] = RNE_bf16( sum_k x~_k W[k][j] )

@@ -277,6 +277,86 @@ def test_solve_bias_unpenalized_equals_paper_centered_ridge():
         np.testing.assert_allclose(W[m][-1], bh, rtol=1e-6, atol=1e-8)
 
 
+# ----------------------------------------------------------------------------- two-pass centered path
+
+def _centered(p, w=None):
+    return oracle.stats_centered(p.hm, p.src, p.src_strides, p.d_s, p.tgt, p.tgt_strides, p.d_t,
+                                 p.w if w is None else w, p.B * p.T, p.B, p.T)
+
+
+def test_centered_moments_equal_numpy_weighted_covariances():
+    rng = np.random.default_rng(21)
+    p = Problem(rng, B=3, T=40)
+    sums, A, B = _centered(p)
+    for m in range(p.n_maps):
+        xt, y, w = p.design(m)
+        x = xt[:, :-1]
+        assert sums[m, 0] == pytest.approx(w.sum(), rel=1e-14)
+        np.testing.assert_allclose(sums[m, 1:1 + p.d_s], w @ x, rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(sums[m, 1 + p.d_s:], w @ y, rtol=1e-12, atol=1e-12)
+        # numpy's weighted covariance (a library routine), rescaled from mean to sum
+        cov = np.cov(np.concatenate([x, y], axis=1).T, aweights=w, bias=True) * w.sum()
+        np.testing.assert_allclose(A[m], cov[:p.d_s, :p.d_s], rtol=1e-10, atol=1e-10)
+        np.testing.assert_allclose(B[m], cov[:p.d_s, p.d_s:], rtol=1e-10, atol=1e-10)
+
+
+def test_centered_moments_shift_invariant_exactly():
+    # integer data: every sum is exact, so shifting every source row by a
+    # constant vector (and the target rows by another) leaves A and B unchanged
+    rng = np.random.default_rng(22)
+    p = Problem(rng, values="int", wkind="choice", B=2, T=20)
+    sums0, A0, B0 = _centered(p)
+    shift_x = rng.integers(-8, 9, size=p.d_s)
+    shift_y = rng.integers(-8, 9, size=p.d_t)
+    p2 = Problem(np.random.default_rng(22), values="int", wkind="choice", B=2, T=20)
+    p2.src = to_bf16_bits(bf16_val(p.src) + shift_x)
+    p2.tgt = to_bf16_bits(bf16_val(p.tgt) + shift_y)
+    sums1, A1, B1 = _centered(p2)
+    # the means move by the shifts (where weights are nonzero), the moments not at all
+    ok = sums0[:, 0] != 0
+    np.testing.assert_allclose(A1[ok], A0[ok], rtol=1e-12, atol=1e-9)
+    np.testing.assert_allclose(B1[ok], B0[ok], rtol=1e-12, atol=1e-9)
+
+
+def test_centered_ridge_equals_unpenalized_augmented_ridge():
+    # Schur complement on the bias row: the paper's centered ridge with the
+    # trace-of-augmented-moments lambda is the unpenalized augmented solution
+    rng = np.random.default_rng(23)
+    p = Problem(rng, B=3, T=45)
+    G, C = p.stats()
+    sums, A, B = _centered(p)
+    for relative, lam in ((True, 1e-2), (False, 0.3)):
+        Wa, ia = oracle.ridge_solve(G, C, lam, relative=relative, bias_unpenalized=True)
+        Wc, ic = oracle.ridge_solve_centered(sums, A, B, lam, relative=relative)
+        assert (ia == 0).all() and (ic == 0).all()
+        assert relF(Wc, Wa) < 1e-10
+
+
+def test_centered_ridge_matches_closed_form_and_handles_zero_weights():
+    rng = np.random.default_rng(24)
+    p = Problem(rng, B=2, T=60)
+    sums, A, B = _centered(p)
+    lam = 0.21
+    W, info = oracle.ridge_solve_centered(sums, A, B, lam, relative=False)
+    for m in range(p.n_maps):
+        xt, y, w = p.design(m)
+        # Eq. closedform with the raw weights (absolute lambda, no mean-one rescaling)
+        x = xt[:, :-1]
+        xbar, ybar = (w @ x) / w.sum(), (w @ y) / w.sum()
+        xc, yc = x - xbar, y - ybar
+        Wh = np.linalg.solve((xc * w[:, None]).T @ xc + lam * np.eye(p.d_s), (xc * w[:, None]).T @ yc)
+        bh = ybar - xbar @ Wh
+        np.testing.assert_allclose(W[m][:-1], Wh, rtol=1e-8, atol=1e-10)
+        np.testing.assert_allclose(W[m][-1], bh, rtol=1e-8, atol=1e-10)
+    # all-zero weights: zero means and moments; relative lambda is zero too,
+    # so the first pivot fails and the maps are zero
+    z = np.zeros_like(p.w)
+    sz, Az, Bz = _centered(p, w=z)
+    assert not sz.any() and not Az.any() and not Bz.any()
+    Wz, iz = oracle.ridge_solve_centered(sz, Az, Bz, 1e-2, relative=True)
+    assert (iz == 1).all() and not Wz.any()
+
+
 def objective(Wt, xt, y, w, lam, bias_penalized):
     r = y - xt @ Wt
     pen = (Wt ** 2).sum() if bias_penalized else (Wt[:-1] ** 2).sum()
