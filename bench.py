@@ -44,7 +44,7 @@ def algorithmic_bytes_per_token(hm, d_s, d_t):
 
 def stats_kernel_sha():
     h = hashlib.sha256()
-    for f in ("cb_stats.hip", "cb_internal.h"):
+    for f in ("cb_stats.hip", "cb_stats_kernel.h", "cb_internal.h"):
         h.update(open(os.path.join(ROOT, "paper_2609_00891_amd", "csrc", f), "rb").read())
     return h.hexdigest()[:16]
 
@@ -103,6 +103,53 @@ def hbm_copy_probe(gib):
                       "GBps_read_plus_write": 2 * n / ms / 1e6}), flush=True)
 
 
+def centered_leg(cb, plan, wl, src, tgt, w, n_calls, maps_plain, bytes_per_call, steps):
+    """The same 500-sequence build in the two-pass centered form: pass 1 (means)
+    over the five batches, pass 2 (centered moments) over the five batches, then
+    the centered solve.  Timed with events on the launch stream, after the main
+    timing (one warm-up build)."""
+    import torch
+    n, d_s, d_t = wl.n_maps, wl.d_s, wl.d_t
+    sums = torch.empty((n, 1 + d_s + d_t), dtype=torch.float64, device="cuda")
+    A = torch.empty((n, d_s, d_s), dtype=torch.float32, device="cuda")
+    B = torch.empty((n, d_s, d_t), dtype=torch.float32, device="cuda")
+    maps = torch.empty((n, d_s + 1, d_t), dtype=torch.float32, device="cuda")
+    info = torch.empty((n,), dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+    recs = []
+    for it in range(steps + 1):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(2 * n_calls + 3)]
+        e[0].record(stream)
+        cb.cb_stats_zero_centered(plan, sums, A, B)
+        e[1].record(stream)
+        for i in range(n_calls):
+            cb.cb_stats_means(plan, src, tgt, w, sums)
+            e[2 + i].record(stream)
+        for i in range(n_calls):
+            cb.cb_stats_accumulate_centered(plan, src, tgt, w, sums, A, B)
+            e[2 + n_calls + i].record(stream)
+        cb.cb_ridge_solve_centered(sums, A, B, wl.lam_rel, cb.CB_LAMBDA_RELATIVE, maps, info)
+        e[2 * n_calls + 2].record(stream)
+        if it > 0:
+            recs.append(e)
+    torch.cuda.synchronize()
+    mean = lambda v: sum(v) / len(v)  # noqa: E731
+    means_ms = mean([e[1 + i].elapsed_time(e[2 + i]) for e in recs for i in range(n_calls)])
+    stats_ms = mean([e[1 + n_calls + i].elapsed_time(e[2 + n_calls + i]) for e in recs for i in range(n_calls)])
+    solve_ms = mean([e[2 * n_calls + 1].elapsed_time(e[2 * n_calls + 2]) for e in recs])
+    build_ms = mean([e[0].elapsed_time(e[2 * n_calls + 2]) for e in recs])
+    diff = (maps - maps_plain).double().norm() / maps_plain.double().norm()
+    return {
+        "s_per_500seq_build": build_ms / 1e3,
+        "calib_tokens_per_s": wl.n_seqs * wl.seq_len / (build_ms / 1e3),
+        "legs_ms": {"means_call": means_ms, "centered_stats_call": stats_ms, "solve": solve_ms},
+        "means_GBps": bytes_per_call / (means_ms / 1e3) / 1e9,
+        "centered_stats_GBps": bytes_per_call / (stats_ms / 1e3) / 1e9,
+        "maps_relF_vs_uncentered_form": float(diff),
+        "nonpositive_pivots": int((info != 0).sum().item()),
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -110,6 +157,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-apply", action="store_true", help=argparse.SUPPRESS)
+    ap.add_argument("--centered-steps", type=int, default=3,
+                    help="timed builds of the two-pass centered form, after the main timing (0: skip)")
     ap.add_argument("--hbm-copy-probe", type=float, default=None, metavar="GIB",
                     help="only time a plain copy of GIB GiB (counter calibration)")
     args = ap.parse_args()
@@ -250,6 +299,8 @@ def main():
         "mfma": {"algorithmic_tflops": flop_per_token * B * wl.seq_len / call_s / 1e12, "peak_tflops": 2500.0},
         "nonpositive_pivots": bad,
     }
+    if args.centered_steps > 0:
+        res["centered"] = centered_leg(cb, plan, wl, src, tgt, w, n_calls, maps, bytes_per_call, args.centered_steps)
     if not args.no_cpu_baseline:
         n_threads = int(os.environ.get("OMP_NUM_THREADS", str(os.cpu_count() or 1)))
         log(f"cpu baseline on {n_threads} threads")

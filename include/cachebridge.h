@@ -13,6 +13,12 @@
  *                        writing a decode-ready target cache (Sec. 1 pipeline;
  *                        Sec. 2.3, Eq. support-cost)
  *
+ * and the paper's two-pass centered form of the same fit (Sec. 3.4, Eq.
+ * fusedstats; Sec. 3.1, Eq. closedform):
+ *
+ *   cb_stats_zero_centered, cb_stats_means, cb_stats_accumulate_centered,
+ *   cb_ridge_solve_centered
+ *
  * Conventions shared by every call
  * --------------------------------
  * - Row vectors: a map is W~ = [W ; b^T], a P x d_t fp32 matrix with
@@ -151,13 +157,74 @@ cb_status cb_stats_accumulate(cb_plan *plan, const cb_cache *src, const cb_cache
  * lambda * trace(G[m]) / P with CB_LAMBDA_RELATIVE.  D = I by default (the
  * bias row is penalized too); with CB_RIDGE_BIAS_UNPENALIZED the last
  * diagonal entry of D is 0, which equals the paper's centered weighted ridge
- * (weights rescaled to mean one).  Only the lower triangle of G is read.
- * Cholesky in fp64, one workgroup per system.  info[m] = 0 on success, else
- * the 1-based index of the first pivot that is not positive and finite, and
+ * (weights rescaled to mean one).  G is read in full and must be symmetric
+ * (cb_stats_accumulate writes it so).  Gauss-Jordan elimination without
+ * pivoting in fp64, one workgroup per system; for the symmetric positive
+ * definite G + lambda_m D its pivots are the squared diagonal of the Cholesky
+ * factor.  info[m] = 0 on success, else the 1-based index of the first pivot
+ * that is not positive and finite (the column where Cholesky would stop), and
  * maps[m] is zero-filled.  P in {65, 97, 129}, d_t in {64, 96, 128}.
  */
 cb_status cb_ridge_solve(int32_t n_maps, int32_t P, int32_t d_t, const float *G, const float *C,
                          float lambda, uint32_t flags, float *maps, int32_t *info, void *stream);
+
+/*
+ * Two-pass centered statistics (Sec. 3.4, Eq. fusedstats): pass 1 sums the
+ * weights and weighted rows over every calibration batch (cb_stats_means),
+ * pass 2 revisits the batches and accumulates the moments about the means of
+ * pass 1 (cb_stats_accumulate_centered).  Centering before the products keeps
+ * A and B accurate when channels carry large means, where the uncentered
+ * moments of cb_stats_accumulate lose digits to cancellation.  Per map m:
+ *   sums [n_maps][1 + d_s + d_t] fp64 = (sum w, sum w x, sum w y)
+ *   mu_x = (sum w x) / (sum w),  mu_y = (sum w y) / (sum w)   (0 if sum w = 0)
+ *   A [n_maps][d_s][d_s] fp32 = sum w (x - mu_x)(x - mu_x)^T
+ *   B [n_maps][d_s][d_t] fp32 = sum w (x - mu_x)(y - mu_y)^T
+ * with x, y, w read as in cb_stats_accumulate.  All pointers are device
+ * pointers owned by the caller; sums is 8-byte aligned.
+ *
+ * cb_stats_zero_centered: set sums, A and B to zero on `stream` (fill kernels).
+ */
+cb_status cb_stats_zero_centered(const cb_plan *plan, double *sums, float *A, float *B, void *stream);
+
+/*
+ * Pass 1: sums[m] += (sum w, sum w x, sum w y) over the batch, with the
+ * products and sums formed in fp64 (exact products; summation order fixed).
+ * Call it on every batch before the first cb_stats_accumulate_centered.
+ * Arguments, limits and errors as in cb_stats_accumulate.
+ */
+cb_status cb_stats_means(cb_plan *plan, const cb_cache *src, const cb_cache *tgt, const float *weights,
+                         int64_t w_row_stride, double *sums, void *stream);
+
+/*
+ * Pass 2: A[m] += sum w (x - mu_x)(x - mu_x)^T and B[m] += sum w (x - mu_x)(y - mu_y)^T
+ * over the batch, with the means taken from the complete pass-1 sums (read,
+ * not modified; they must not change between the pass-2 calls of one fit).
+ * Each product pairs w (x - mu_x), formed in fp32 and split into two bf16
+ * terms, with the exact bf16 x or y; the sums run in fp32, and the term
+ * (sum w (x - mu_x)) mu^T that the uncentered right operand contributes is
+ * subtracted at the end.  A is written exactly symmetric.  Arguments, limits
+ * and errors as in cb_stats_accumulate.
+ */
+cb_status cb_stats_accumulate_centered(cb_plan *plan, const cb_cache *src, const cb_cache *tgt,
+                                       const float *weights, int64_t w_row_stride, const double *sums,
+                                       float *A, float *B, void *stream);
+
+/*
+ * Centered ridge solve (Sec. 3.1, Eq. closedform):
+ *   W = (A[m] + lambda_m I)^{-1} B[m],   b = mu_y - W^T mu_x,
+ * written as maps[m] = [W ; b^T], [n_maps][d_s + 1][d_t] fp32 (the layout of
+ * cb_ridge_solve and cb_apply).  The bias is never penalized.  lambda_m =
+ * lambda, or with CB_LAMBDA_RELATIVE lambda * (tr A + S |mu_x|^2 + S) / (d_s + 1),
+ * S = sum w: the relative lambda of cb_ridge_solve on the uncentered moments
+ * of the same data, so both forms solve the same problem
+ * (CB_RIDGE_BIAS_UNPENALIZED is accepted and changes nothing).  Gauss-Jordan
+ * elimination in fp64, one workgroup per system.  info[m] = 0 on success, else
+ * the 1-based index of the first pivot of A + lambda_m I that is not positive
+ * and finite, and maps[m] is zero-filled.  d_s, d_t in {64, 96, 128}.
+ */
+cb_status cb_ridge_solve_centered(int32_t n_maps, int32_t d_s, int32_t d_t, const double *sums, const float *A,
+                                  const float *B, float lambda, uint32_t flags, float *maps, int32_t *info,
+                                  void *stream);
 
 /*
  * Online mapping (Sec. 1 pipeline; Sec. 2.3 Eq. support-cost): for every map

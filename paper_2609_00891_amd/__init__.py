@@ -10,6 +10,10 @@ current HIP stream.  The functions keep the C names:
   G, C (CacheBridge Sec. 3.4, Eq. fusedstats)
 * :func:`cb_ridge_solve` -- (G + lambda D)^-1 C (Sec. 3.1, Eq. closedform)
 * :func:`cb_apply` -- online application of the maps (Sec. 1; Sec. 2.3)
+* :func:`cb_stats_zero_centered`, :func:`cb_stats_means`,
+  :func:`cb_stats_accumulate_centered`, :func:`cb_ridge_solve_centered` -- the
+  two-pass centered form: weighted sums, centered moments A, B (Sec. 3.4) and
+  W = (A + lambda I)^-1 B, b = mu_y - W^T mu_x (Sec. 3.1)
 
 Caches are bfloat16 tensors indexed ``[layer][kv][seq][head][tok][dim]`` (any
 strides with a unit channel stride).  Importing this package fails if the
@@ -75,6 +79,16 @@ _lib.cb_stats_accumulate.argtypes = [_vp, ctypes.POINTER(CbCache), ctypes.POINTE
 _lib.cb_ridge_solve.restype = ctypes.c_int
 _lib.cb_ridge_solve.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp, _vp, ctypes.c_float,
                                 ctypes.c_uint32, _vp, _vp, _vp]
+_lib.cb_stats_zero_centered.restype = ctypes.c_int
+_lib.cb_stats_zero_centered.argtypes = [_vp, _vp, _vp, _vp, _vp]
+_lib.cb_stats_means.restype = ctypes.c_int
+_lib.cb_stats_means.argtypes = [_vp, ctypes.POINTER(CbCache), ctypes.POINTER(CbCache), _vp, ctypes.c_int64, _vp, _vp]
+_lib.cb_stats_accumulate_centered.restype = ctypes.c_int
+_lib.cb_stats_accumulate_centered.argtypes = [_vp, ctypes.POINTER(CbCache), ctypes.POINTER(CbCache), _vp,
+                                              ctypes.c_int64, _vp, _vp, _vp, _vp]
+_lib.cb_ridge_solve_centered.restype = ctypes.c_int
+_lib.cb_ridge_solve_centered.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp, _vp, _vp,
+                                         ctypes.c_float, ctypes.c_uint32, _vp, _vp, _vp]
 _lib.cb_apply.restype = ctypes.c_int
 _lib.cb_apply.argtypes = [_vp, _vp, ctypes.POINTER(CbCache), ctypes.POINTER(CbCache), _vp]
 _lib.cb_status_string.restype = ctypes.c_char_p
@@ -207,6 +221,56 @@ def cb_ridge_solve(G: torch.Tensor, C: torch.Tensor, lam: float, flags: int, map
         raise ValueError("info is int32")
     _check(_lib.cb_ridge_solve(n, P, C.shape[2], _ptr(G), _ptr(C), float(lam), int(flags), _ptr(maps), _ptr(info),
                                _stream(stream)))
+
+
+def _row_stride(weights: torch.Tensor, w_row_stride: Optional[int]) -> int:
+    if w_row_stride is not None:
+        return int(w_row_stride)
+    return weights.stride(0) if weights.dim() == 2 else weights.numel()
+
+
+def cb_stats_zero_centered(plan: Plan, sums: torch.Tensor, A: torch.Tensor, B: torch.Tensor, stream=None):
+    """Zero sums [n][1 + d_s + d_t] (float64), A [n][d_s][d_s] and B [n][d_s][d_t] (float32)."""
+    if sums.dtype != torch.float64 or A.dtype != torch.float32 or B.dtype != torch.float32:
+        raise ValueError("sums is float64, A and B are float32")
+    _check(_lib.cb_stats_zero_centered(plan.handle, _ptr(sums), _ptr(A), _ptr(B), _stream(stream)))
+
+
+def cb_stats_means(plan: Plan, src: torch.Tensor, tgt: torch.Tensor, weights: torch.Tensor, sums: torch.Tensor,
+                   w_row_stride: Optional[int] = None, stream=None):
+    """Pass 1: sums[m] += (sum w, sum w x, sum w y) over the batch (float64)."""
+    if weights.dtype != torch.float32 or sums.dtype != torch.float64:
+        raise ValueError("weights are float32, sums float64")
+    sv, tv = cache_view(src), cache_view(tgt)
+    _check(_lib.cb_stats_means(plan.handle, ctypes.byref(sv), ctypes.byref(tv), _ptr(weights),
+                               _row_stride(weights, w_row_stride), _ptr(sums), _stream(stream)))
+
+
+def cb_stats_accumulate_centered(plan: Plan, src: torch.Tensor, tgt: torch.Tensor, weights: torch.Tensor,
+                                 sums: torch.Tensor, A: torch.Tensor, B: torch.Tensor,
+                                 w_row_stride: Optional[int] = None, stream=None):
+    """Pass 2: A[m] += sum w (x - mu_x)(x - mu_x)^T, B[m] += sum w (x - mu_x)(y - mu_y)^T."""
+    if weights.dtype != torch.float32 or sums.dtype != torch.float64 or A.dtype != torch.float32 \
+            or B.dtype != torch.float32:
+        raise ValueError("weights, A and B are float32, sums float64")
+    sv, tv = cache_view(src), cache_view(tgt)
+    _check(_lib.cb_stats_accumulate_centered(plan.handle, ctypes.byref(sv), ctypes.byref(tv), _ptr(weights),
+                                             _row_stride(weights, w_row_stride), _ptr(sums), _ptr(A), _ptr(B),
+                                             _stream(stream)))
+
+
+def cb_ridge_solve_centered(sums: torch.Tensor, A: torch.Tensor, B: torch.Tensor, lam: float, flags: int,
+                            maps: torch.Tensor, info: torch.Tensor, stream=None):
+    """maps[m] = [W; b^T] with W = (A[m] + lambda_m I)^-1 B[m] and b = mu_y - W^T mu_x."""
+    n, d_s, d_s2 = A.shape
+    d_t = B.shape[2] if B.dim() == 3 else -1
+    if d_s != d_s2 or B.shape[:2] != (n, d_s) or sums.shape != (n, 1 + d_s + d_t) \
+            or maps.shape != (n, d_s + 1, d_t) or info.shape != (n,):
+        raise ValueError("sums [n][1+d_s+d_t], A [n][d_s][d_s], B [n][d_s][d_t], maps [n][d_s+1][d_t], info [n]")
+    if sums.dtype != torch.float64 or info.dtype != torch.int32:
+        raise ValueError("sums is float64, info int32")
+    _check(_lib.cb_ridge_solve_centered(n, d_s, d_t, _ptr(sums), _ptr(A), _ptr(B), float(lam), int(flags),
+                                        _ptr(maps), _ptr(info), _stream(stream)))
 
 
 def cb_apply(plan: Plan, maps: torch.Tensor, src: torch.Tensor, tgt_out: torch.Tensor, stream=None):

@@ -111,6 +111,60 @@ cb_status check_cache(const char *name, const cb_cache *c, int L, int H, int d) 
 
 cb::Strides strides_of(const cb_cache *c) { return {c->s_layer, c->s_kv, c->s_seq, c->s_head, c->s_tok}; }
 
+// Validation and work units shared by the statistics calls.  *empty is set
+// for a call without tokens (nothing to enqueue).
+cb_status prepare_stats(const cb_plan *p, const cb_cache *src, const cb_cache *tgt, const float *weights,
+                        int64_t w_row_stride, cb::StatsArgs &a, bool &empty) {
+    if (cb_status s = check_cache("src", src, p->L_s, p->H_s, p->d_s)) return s;
+    if (cb_status s = check_cache("tgt", tgt, p->L_t, p->H_t, p->d_t)) return s;
+    if (src->n_seqs != tgt->n_seqs || src->seq_len != tgt->seq_len)
+        return fail(CB_ERR_SHAPE, "src and tgt disagree on n_seqs / seq_len");
+    const int64_t N = (int64_t)src->n_seqs * src->seq_len;
+    if (N > p->max_tokens)
+        return fail(CB_ERR_UNSUPPORTED, "call has %lld tokens, plan allows %lld", (long long)N, (long long)p->max_tokens);
+    empty = N == 0;
+    if (empty) return CB_OK;
+    if (!weights) return fail(CB_ERR_INVALID_ARGUMENT, "weights is NULL");
+    if (w_row_stride < N) return fail(CB_ERR_SHAPE, "w_row_stride (%lld) < tokens in the call (%lld)",
+                                      (long long)w_row_stride, (long long)N);
+    if (((uintptr_t)weights) % 4) return fail(CB_ERR_MISALIGNED, "weights must be 4-byte aligned");
+    if (cb_status s = check_device(p)) return s;
+
+    a.src = (const uint16_t *)src->data;
+    a.tgt = (const uint16_t *)tgt->data;
+    a.w = weights;
+    a.ss = strides_of(src);
+    a.ts = strides_of(tgt);
+    a.w_row_stride = w_row_stride;
+    const int64_t KT = cb::kStatsTileTokens;
+    const int64_t tps = (src->seq_len + KT - 1) / KT;
+    const int64_t tiles = (int64_t)src->n_seqs * tps;
+    if (tiles > INT32_MAX) return fail(CB_ERR_UNSUPPORTED, "too many token tiles in one call");
+    if (a.ss.tok * 2 * KT >= (1LL << 31) || a.ts.tok * 2 * KT >= (1LL << 31))
+        return fail(CB_ERR_UNSUPPORTED, "token strides must be below 2^25 elements");
+    a.seq_len = (uint32_t)src->seq_len;
+    a.TPS = cb::make_fastdiv((uint32_t)tps);
+    a.n_tiles = (int32_t)tiles;
+    choose_chunks(tiles, p->n_items, p->n_cu, p->max_chunks, &a.n_chunks, &a.chunk_tiles);
+    if (a.n_chunks > p->max_chunks) return fail(CB_ERR_UNSUPPORTED, "internal: chunk count exceeds workspace");
+    a.n_items = p->n_items;
+    a.items = p->d_items;
+    a.partials = p->d_partials;
+    a.zero = p->d_zero;
+    return CB_OK;
+}
+
+cb::ReduceArgs reduce_args(const cb_plan *p, const cb::StatsArgs &a) {
+    cb::ReduceArgs r = {};
+    r.partials = p->d_partials;
+    r.map_item = p->d_map_item;
+    r.map_slot = p->d_map_slot;
+    r.n_items = p->n_items;
+    r.n_chunks = a.n_chunks;
+    r.n_maps = p->n_maps;
+    return r;
+}
+
 }  // namespace
 
 extern "C" {
@@ -325,57 +379,72 @@ cb_status cb_stats_accumulate(cb_plan *p, const cb_cache *src, const cb_cache *t
                               int64_t w_row_stride, float *G, float *C, void *stream) {
     if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
     if (!G || !C) return fail(CB_ERR_INVALID_ARGUMENT, "G and C must be non-NULL");
-    if (cb_status s = check_cache("src", src, p->L_s, p->H_s, p->d_s)) return s;
-    if (cb_status s = check_cache("tgt", tgt, p->L_t, p->H_t, p->d_t)) return s;
-    if (src->n_seqs != tgt->n_seqs || src->seq_len != tgt->seq_len)
-        return fail(CB_ERR_SHAPE, "src and tgt disagree on n_seqs / seq_len");
-    const int64_t N = (int64_t)src->n_seqs * src->seq_len;
-    if (N > p->max_tokens)
-        return fail(CB_ERR_UNSUPPORTED, "call has %lld tokens, plan allows %lld", (long long)N, (long long)p->max_tokens);
-    if (N == 0) return ok();
-    if (!weights) return fail(CB_ERR_INVALID_ARGUMENT, "weights is NULL");
-    if (w_row_stride < N) return fail(CB_ERR_SHAPE, "w_row_stride (%lld) < tokens in the call (%lld)",
-                                      (long long)w_row_stride, (long long)N);
-    if (((uintptr_t)weights) % 4 || ((uintptr_t)G) % 4 || ((uintptr_t)C) % 4)
-        return fail(CB_ERR_MISALIGNED, "weights, G and C must be 4-byte aligned");
-    if (cb_status s = check_device(p)) return s;
-
+    if (((uintptr_t)G) % 4 || ((uintptr_t)C) % 4) return fail(CB_ERR_MISALIGNED, "G and C must be 4-byte aligned");
     cb::StatsArgs a = {};
-    a.src = (const uint16_t *)src->data;
-    a.tgt = (const uint16_t *)tgt->data;
-    a.w = weights;
-    a.ss = strides_of(src);
-    a.ts = strides_of(tgt);
-    a.w_row_stride = w_row_stride;
-    const int64_t KT = cb::kStatsTileTokens;
-    const int64_t tps = (src->seq_len + KT - 1) / KT;
-    const int64_t tiles = (int64_t)src->n_seqs * tps;
-    if (tiles > INT32_MAX) return fail(CB_ERR_UNSUPPORTED, "too many token tiles in one call");
-    if (a.ss.tok * 2 * KT >= (1LL << 31) || a.ts.tok * 2 * KT >= (1LL << 31))
-        return fail(CB_ERR_UNSUPPORTED, "token strides must be below 2^25 elements");
-    a.seq_len = (uint32_t)src->seq_len;
-    a.TPS = cb::make_fastdiv((uint32_t)tps);
-    a.n_tiles = (int32_t)tiles;
-    choose_chunks(tiles, p->n_items, p->n_cu, p->max_chunks, &a.n_chunks, &a.chunk_tiles);
-    if (a.n_chunks > p->max_chunks) return fail(CB_ERR_UNSUPPORTED, "internal: chunk count exceeds workspace");
-    a.n_items = p->n_items;
-    a.items = p->d_items;
-    a.partials = p->d_partials;
-    a.zero = p->d_zero;
+    bool empty = false;
+    if (cb_status s = prepare_stats(p, src, tgt, weights, w_row_stride, a, empty)) return s;
+    if (empty) return ok();
     hipStream_t st = (hipStream_t)stream;
     if (cb::launch_stats(p->d_s, p->d_t, a, st) != hipSuccess)
         return fail(CB_ERR_DEVICE, "statistics kernel launch failed");
-    cb::ReduceArgs r = {};
-    r.partials = p->d_partials;
-    r.map_item = p->d_map_item;
-    r.map_slot = p->d_map_slot;
-    r.n_items = p->n_items;
-    r.n_chunks = a.n_chunks;
-    r.n_maps = p->n_maps;
+    cb::ReduceArgs r = reduce_args(p, a);
     r.G = G;
     r.C = C;
     if (cb::launch_reduce(p->d_s, p->d_t, r, st) != hipSuccess)
         return fail(CB_ERR_DEVICE, "reduction kernel launch failed");
+    return ok();
+}
+
+cb_status cb_stats_zero_centered(const cb_plan *p, double *sums, float *A, float *B, void *stream) {
+    if (!p || !sums || !A || !B) return fail(CB_ERR_INVALID_ARGUMENT, "plan, sums, A and B must be non-NULL");
+    if (cb_status s = check_device(p)) return s;
+    const int64_t n = p->n_maps, ds = p->d_s, dt = p->d_t;
+    hipStream_t st = (hipStream_t)stream;
+    if (cb::launch_fill_zero((float *)sums, 2 * n * (1 + ds + dt), st) != hipSuccess ||
+        cb::launch_fill_zero(A, n * ds * ds, st) != hipSuccess || cb::launch_fill_zero(B, n * ds * dt, st) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "fill kernel launch failed");
+    return ok();
+}
+
+cb_status cb_stats_means(cb_plan *p, const cb_cache *src, const cb_cache *tgt, const float *weights,
+                         int64_t w_row_stride, double *sums, void *stream) {
+    if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
+    if (!sums) return fail(CB_ERR_INVALID_ARGUMENT, "sums must be non-NULL");
+    if (((uintptr_t)sums) % 8) return fail(CB_ERR_MISALIGNED, "sums must be 8-byte aligned");
+    cb::StatsArgs a = {};
+    bool empty = false;
+    if (cb_status s = prepare_stats(p, src, tgt, weights, w_row_stride, a, empty)) return s;
+    if (empty) return ok();
+    hipStream_t st = (hipStream_t)stream;
+    if (cb::launch_means(p->d_s, p->d_t, a, st) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "means kernel launch failed");
+    cb::ReduceArgs r = reduce_args(p, a);
+    r.sums = sums;
+    if (cb::launch_means_reduce(p->d_s, p->d_t, r, st) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "means reduction launch failed");
+    return ok();
+}
+
+cb_status cb_stats_accumulate_centered(cb_plan *p, const cb_cache *src, const cb_cache *tgt, const float *weights,
+                                       int64_t w_row_stride, const double *sums, float *A, float *B, void *stream) {
+    if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
+    if (!sums || !A || !B) return fail(CB_ERR_INVALID_ARGUMENT, "sums, A and B must be non-NULL");
+    if (((uintptr_t)sums) % 8 || ((uintptr_t)A) % 4 || ((uintptr_t)B) % 4)
+        return fail(CB_ERR_MISALIGNED, "sums must be 8-byte and A, B 4-byte aligned");
+    cb::StatsArgs a = {};
+    bool empty = false;
+    if (cb_status s = prepare_stats(p, src, tgt, weights, w_row_stride, a, empty)) return s;
+    if (empty) return ok();
+    a.sums = sums;
+    hipStream_t st = (hipStream_t)stream;
+    if (cb::launch_stats_centered(p->d_s, p->d_t, a, st) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "centered statistics kernel launch failed");
+    cb::ReduceArgs r = reduce_args(p, a);
+    r.G = A;
+    r.C = B;
+    r.sums = const_cast<double *>(sums);      // read only by the centered reduction
+    if (cb::launch_reduce_centered(p->d_s, p->d_t, r, st) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "centered reduction launch failed");
     return ok();
 }
 
@@ -393,6 +462,27 @@ cb_status cb_ridge_solve(int32_t n_maps, int32_t P, int32_t d_t, const float *G,
         return fail(CB_ERR_MISALIGNED, "G, C, maps and info must be 4-byte aligned");
     if (cb::launch_solve(n_maps, P, d_t, G, C, lambda, flags, maps, info, (hipStream_t)stream) != hipSuccess)
         return fail(CB_ERR_DEVICE, "ridge solve launch failed");
+    return ok();
+}
+
+cb_status cb_ridge_solve_centered(int32_t n_maps, int32_t d_s, int32_t d_t, const double *sums, const float *A,
+                                  const float *B, float lambda, uint32_t flags, float *maps, int32_t *info,
+                                  void *stream) {
+    if (n_maps < 0) return fail(CB_ERR_INVALID_ARGUMENT, "n_maps is negative");
+    if (!supported_width(d_s) || !supported_width(d_t))
+        return fail(CB_ERR_UNSUPPORTED, "d_s and d_t must be 64, 96 or 128 (got d_s=%d, d_t=%d)", d_s, d_t);
+    if (flags & ~(uint32_t)(CB_LAMBDA_RELATIVE | CB_RIDGE_BIAS_UNPENALIZED))
+        return fail(CB_ERR_INVALID_ARGUMENT, "unknown flag bits 0x%x", flags);
+    if (!std::isfinite(lambda) || lambda < 0.f) return fail(CB_ERR_INVALID_ARGUMENT, "lambda must be finite and >= 0");
+    if (n_maps == 0) return ok();
+    if (!sums || !A || !B || !maps || !info)
+        return fail(CB_ERR_INVALID_ARGUMENT, "sums, A, B, maps and info must be non-NULL");
+    if (((uintptr_t)sums) % 8 || ((uintptr_t)A) % 4 || ((uintptr_t)B) % 4 || ((uintptr_t)maps) % 4 ||
+        ((uintptr_t)info) % 4)
+        return fail(CB_ERR_MISALIGNED, "sums must be 8-byte and A, B, maps, info 4-byte aligned");
+    if (cb::launch_solve_centered(n_maps, d_s, d_t, sums, A, B, lambda, flags, maps, info, (hipStream_t)stream) !=
+        hipSuccess)
+        return fail(CB_ERR_DEVICE, "centered ridge solve launch failed");
     return ok();
 }
 

@@ -66,6 +66,7 @@ struct StatsArgs {
     const StatsItem *items;
     float *partials;      // [n_chunks * n_items][2][slot_floats]
     const void *zero;     // >= 256 zero bytes: source of the weights of absent tokens
+    const double *sums;   // centered statistics only: [n_maps][1 + d_s + d_t] = (sum w, sum w x, sum w y)
 };
 
 struct ReduceArgs {
@@ -73,7 +74,8 @@ struct ReduceArgs {
     const int32_t *map_item;  // [n_maps]
     const int32_t *map_slot;  // [n_maps]
     int32_t n_items, n_chunks, n_maps;
-    float *G, *C;
+    float *G, *C;         // plain: G [n][P][P], C [n][P][d_t]; centered: A [n][d_s][d_s], B [n][d_s][d_t]
+    double *sums;         // centered: read; means: added to.  [n_maps][1 + d_s + d_t] = (sum w, sum w x, sum w y)
 };
 
 struct ApplyArgs {
@@ -93,6 +95,13 @@ struct ApplyArgs {
 // Launchers (return hipError_t of the launch).
 hipError_t launch_stats(int d_s, int d_t, const StatsArgs &a, hipStream_t s);
 hipError_t launch_reduce(int d_s, int d_t, const ReduceArgs &a, hipStream_t s);
+hipError_t launch_stats_centered(int d_s, int d_t, const StatsArgs &a, hipStream_t s);
+hipError_t launch_reduce_centered(int d_s, int d_t, const ReduceArgs &a, hipStream_t s);
+hipError_t launch_means(int d_s, int d_t, const StatsArgs &a, hipStream_t s);
+hipError_t launch_means_reduce(int d_s, int d_t, const ReduceArgs &a, hipStream_t s);
+hipError_t launch_solve_centered(int32_t n_maps, int32_t d_s, int32_t d_t, const double *sums, const float *A,
+                                 const float *B, float lambda, uint32_t flags, float *maps, int32_t *info,
+                                 hipStream_t s);
 hipError_t launch_fill_zero(float *p, int64_t n, hipStream_t s);
 hipError_t launch_solve(int32_t n_maps, int32_t P, int32_t d_t, const float *G, const float *C,
                         float lambda, uint32_t flags, float *maps, int32_t *info, hipStream_t s);

@@ -25,6 +25,11 @@ Workloads (``WORKLOADS``):
 * ``apply`` -- maps [1024][129][128] fp32 (planted, ``qwen`` statistics) applied
   to a sender cache of 8 x 32768 tokens x 40 layers x 8 heads x 128.
 
+Source kinds: ``gauss`` x ~ N(0,1); ``scaled`` x = s_c z (per-channel lognormal
+scales s_c with outliers); ``offset`` x = mu_c + s_c z with per-channel means
+mu_c = 30 s_c u_c, u_c ~ N(0,1) (channels whose mean dwarfs their spread, as
+in the large-magnitude key channels of real caches).
+
 Cache layout everywhere: ``[layer][kv][seq][head][tok][dim]`` bfloat16.
 Weights: fp32 ``[row][seq * seq_len + tok]``; row = tgt_layer * H_t + tgt_head
 (one row per target head, shared by K and V).  Map order:
@@ -58,7 +63,7 @@ class Workload:
     n_seqs: int
     seq_len: int
     head_map_kind: str          # "identity" | "qwen" | "mismatch"
-    source_kind: str            # "gauss" | "scaled"
+    source_kind: str            # "gauss" | "scaled" | "offset"
     noise: float
     weight_kind: str            # "lognormal" | "colmass" | "decay"
     lam_rel: float = 1e-2
@@ -94,6 +99,7 @@ APPLY = Workload("apply", 40, 8, 128, 64, 8, 128, 8, 32768, "qwen", "scaled", 0.
 SINK_LOGIT = 4.0          # position-0 sink strength for the column-mass weights
 N_OUTLIERS = 4            # outlier channels per (source layer, kv, head)
 OUTLIER_SCALE = 20.0
+OFFSET_RATIO = 30.0       # channel mean / channel scale of the ``offset`` source kind
 
 
 def _seed(*key) -> int:
@@ -164,6 +170,17 @@ def _channel_scales(wl: Workload, device) -> torch.Tensor:
     return out
 
 
+def _channel_offsets(wl: Workload, scales: torch.Tensor, device) -> torch.Tensor:
+    """[L_s][2][H_s][d_s] fp32 per-channel means OFFSET_RATIO * s_c * N(0,1)."""
+    out = torch.empty_like(scales)
+    for l in range(wl.L_s):
+        for z in range(2):
+            for g in range(wl.H_s):
+                gen = _gen(device, wl.name, "offset", l, z, g)
+                out[l, z, g] = OFFSET_RATIO * scales[l, z, g] * torch.randn(wl.d_s, generator=gen, device=device)
+    return out
+
+
 def gen_source(wl: Workload, seq0: int = 0, n_seqs: Optional[int] = None, seq_len: Optional[int] = None,
                device="cpu", out: Optional[torch.Tensor] = None) -> torch.Tensor:
     """Source cache [L_s][2][B][H_s][T][d_s] bf16 for sequences seq0 .. seq0+B-1
@@ -172,7 +189,10 @@ def gen_source(wl: Workload, seq0: int = 0, n_seqs: Optional[int] = None, seq_le
     T = wl.seq_len if seq_len is None else seq_len
     if out is None:
         out = torch.empty((wl.L_s, 2, B, wl.H_s, T, wl.d_s), dtype=torch.bfloat16, device=device)
-    scales = _channel_scales(wl, device) if wl.source_kind == "scaled" else None
+    if wl.source_kind not in ("gauss", "scaled", "offset"):
+        raise ValueError(wl.source_kind)
+    scales = _channel_scales(wl, device) if wl.source_kind in ("scaled", "offset") else None
+    offsets = _channel_offsets(wl, scales, device) if wl.source_kind == "offset" else None
     for l in range(wl.L_s):
         for z in range(2):
             for g in range(wl.H_s):
@@ -180,6 +200,8 @@ def gen_source(wl: Workload, seq0: int = 0, n_seqs: Optional[int] = None, seq_le
                 x = torch.randn((B, T, wl.d_s), generator=gen, device=device, dtype=torch.float32)
                 if scales is not None:
                     x *= scales[l, z, g]
+                if offsets is not None:
+                    x += offsets[l, z, g]
                 out[l, z, :, g] = x.to(torch.bfloat16)
     return out
 

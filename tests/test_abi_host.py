@@ -92,3 +92,22 @@ def test_null_arguments_are_rejected_before_any_launch():
     assert lib.cb_ridge_solve(4, 129, 128, None, None, ctypes.c_float(0.1), 1, None, None, None) == 1
     assert lib.cb_ridge_solve(0, 129, 128, None, None, ctypes.c_float(0.1), 1, None, None, None) == 0
     assert "NULL" in cb.cb_last_error() or cb.cb_last_error() == ""
+
+
+def test_centered_entry_points_reject_bad_arguments_on_the_host():
+    import paper_2609_00891_amd as cb
+    lib = cb.library()
+    assert lib.cb_stats_zero_centered(None, None, None, None, None) == 1
+    assert lib.cb_stats_means(None, None, None, None, 0, None, None) == 1
+    assert lib.cb_stats_accumulate_centered(None, None, None, None, 0, None, None, None, None) == 1
+    f = ctypes.c_float
+    solve = lib.cb_ridge_solve_centered
+    assert solve(4, 80, 128, None, None, None, f(0.1), 0, None, None, None) == 6      # d_s not supported
+    assert solve(4, 128, 256, None, None, None, f(0.1), 0, None, None, None) == 6     # d_t not supported
+    assert solve(4, 128, 128, None, None, None, f(0.1), 4, None, None, None) == 1     # unknown flag
+    assert solve(4, 128, 128, None, None, None, f(-1.0), 1, None, None, None) == 1
+    assert solve(4, 128, 128, None, None, None, f(float("inf")), 1, None, None, None) == 1
+    assert solve(4, 128, 128, None, None, None, f(0.1), 1, None, None, None) == 1     # NULL pointers
+    assert solve(-1, 128, 128, None, None, None, f(0.1), 1, None, None, None) == 1
+    assert solve(0, 128, 128, None, None, None, f(0.1), 3, None, None, None) == 0     # nothing to do
+    assert "NULL" in cb.cb_last_error() or cb.cb_last_error() == ""

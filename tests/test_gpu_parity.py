@@ -402,3 +402,218 @@ def test_apply_full_size_sampled_tokens(cb):
         assert worst <= TOL_APPLY
         check_apply(ob, ref, f" (row {b}, tokens {t0}..{t1})")
     plan.close()
+
+
+# ----------------------------------------------------------------------------- two-pass centered form
+
+TOL_SUMS = 1e-9        # fp64 sums of exact fp64 products: only the summation order differs
+
+
+def gpu_centered(cb, plan, batches):
+    """Pass 1 (means) over every batch, then pass 2 (centered moments) over every
+    batch; ``batches`` holds (src, tgt, weights) views of one workload."""
+    n, ds, dt = plan.n_maps, plan.d_s, plan.d_t
+    sums = torch.empty((n, 1 + ds + dt), dtype=torch.float64, device="cuda")
+    A = torch.empty((n, ds, ds), dtype=torch.float32, device="cuda")
+    B = torch.empty((n, ds, dt), dtype=torch.float32, device="cuda")
+    cb.cb_stats_zero_centered(plan, sums, A, B)
+    for s, t, w in batches:
+        cb.cb_stats_means(plan, s, t, w, sums)
+    for s, t, w in batches:
+        cb.cb_stats_accumulate_centered(plan, s, t, w, sums, A, B)
+    torch.cuda.synchronize()
+    return sums, A, B
+
+
+def seq_batches(src, tgt, w, bounds):
+    """Views of sequences [b0, b1) for each (b0, b1): the weights keep their row stride."""
+    T = src.shape[4]
+    return [(src[:, :, b0:b1], tgt[:, :, b0:b1], w[:, b0 * T:b1 * T]) for b0, b1 in bounds]
+
+
+def gpu_solve_centered(cb, sums, A, B, lam, flags):
+    maps = torch.empty((A.shape[0], A.shape[1] + 1, B.shape[2]), dtype=torch.float32, device="cuda")
+    info = torch.empty((A.shape[0],), dtype=torch.int32, device="cuda")
+    cb.cb_ridge_solve_centered(sums, A, B, lam, flags, maps, info)
+    torch.cuda.synchronize()
+    return maps, info
+
+
+def oracle_centered_sel(hm, sel, src, tgt, w):
+    chm, xb, ss, yb, ts, ws, B, T = compact(hm, sel, src, tgt, w)
+    return oracle.stats_centered(chm, xb, ss, xb.shape[-1], yb, ts, yb.shape[-1], ws, B * T, B, T,
+                                 n_threads=NTHREADS)
+
+
+def check_centered(sums, A, B, so, Ao, Bo, sel, tol=TOL_STATS):
+    idx = torch.as_tensor(sel, device=A.device)
+    sg = sums[idx].cpu().numpy()
+    Ag = A[idx].double().cpu().numpy()
+    Bg = B[idx].double().cpu().numpy()
+    es = max(relF(sg[i], so[i]) for i in range(len(sel)))
+    ea = max(relF(Ag[i], Ao[i]) for i in range(len(sel)))
+    eb = max(relF(Bg[i], Bo[i]) for i in range(len(sel)))
+    say(f"  centered parity: max relF sums {es:.3e}, A {ea:.3e}, B {eb:.3e}")
+    assert es <= TOL_SUMS and ea <= tol and eb <= tol
+    assert np.array_equal(Ag, np.transpose(Ag, (0, 2, 1))), "A must be exactly symmetric"
+    return es, ea, eb
+
+
+def check_centered_maps(cb, sums, A, B, so, Ao, Bo, sel, lam):
+    maps, info = gpu_solve_centered(cb, sums, A, B, lam, cb.CB_LAMBDA_RELATIVE)
+    assert (info[torch.as_tensor(sel, device=info.device)].cpu().numpy() == 0).all()
+    Wo, io = oracle.ridge_solve_centered(so, Ao, Bo, lam, relative=True, n_threads=NTHREADS)
+    assert (io == 0).all()
+    Wg = maps.double().cpu().numpy()
+    e = max(relF(Wg[m], Wo[i]) for i, m in enumerate(sel))
+    # the solver alone, on the very moments the GPU produced
+    idx = torch.as_tensor(sel, device=A.device)
+    Ws, _ = oracle.ridge_solve_centered(sums[idx].cpu().numpy(), A[idx].double().cpu().numpy(),
+                                        B[idx].double().cpu().numpy(), lam, relative=True, n_threads=NTHREADS)
+    es = max(relF(Wg[m], Ws[i]) for i, m in enumerate(sel))
+    say(f"  centered maps parity: end-to-end {e:.3e}, solver alone {es:.3e}")
+    assert e <= TOL_MAPS and es <= 1e-6
+    return maps
+
+
+def test_centered_tiny_end_to_end(cb):
+    wl = synth.WORKLOADS["tiny"]
+    src, tgt, w = make_inputs(wl)
+    hm = synth.head_map(wl)
+    plan = cb.cb_plan_create(hm, src, tgt, wl.n_seqs * wl.seq_len)
+    sums, A, B = gpu_centered(cb, plan, seq_batches(src, tgt, w, [(0, 1), (1, 4)]))
+    sel = list(range(wl.n_maps))
+    so, Ao, Bo = oracle_centered_sel(hm, sel, src, tgt, w)
+    check_centered(sums, A, B, so, Ao, Bo, sel)
+    maps = check_centered_maps(cb, sums, A, B, so, Ao, Bo, sel, wl.lam_rel)
+    # the uncentered augmented form with an unpenalized bias solves the same problem
+    G, C = gpu_stats(cb, plan, src, tgt, w)
+    mu, _ = gpu_solve(cb, G, C, wl.lam_rel, cb.CB_LAMBDA_RELATIVE | cb.CB_RIDGE_BIAS_UNPENALIZED)
+    ex = max(relF(maps[m].double().cpu().numpy(), mu[m].double().cpu().numpy()) for m in sel)
+    say(f"  centered vs uncentered-augmented maps: {ex:.3e}")
+    assert ex <= 2 * TOL_MAPS
+    out = torch.zeros_like(tgt)
+    cb.cb_apply(plan, maps, src, out)
+    torch.cuda.synchronize()
+    ref = np.zeros(tuple(out.shape), dtype=np.uint16)
+    oracle.apply(hm, maps.double().cpu().numpy(), bits(src), src.stride()[:5], wl.d_s, ref, out.stride()[:5],
+                 wl.d_t, wl.n_seqs, wl.seq_len)
+    check_apply(bits(out).reshape(ref.shape), ref)
+    plan.close()
+
+
+@pytest.mark.parametrize("d_s,d_t", WIDTHS)
+def test_centered_widths_ragged_batches_and_shared_sources(cb, d_s, d_t):
+    # shared-source items and paired singles, a ragged last tile, and three
+    # streamed batches that split the sequences unevenly
+    wl = synth.Workload("cragged", 2, 3, d_s, 3, 2, d_t, 4, 45, "cyclic1", "offset", 0.1, "lognormal")
+    src, tgt, w = make_inputs(wl)
+    hm = synth.head_map(wl)
+    plan = cb.cb_plan_create(hm, src, tgt, 4096)
+    sums, A, B = gpu_centered(cb, plan, seq_batches(src, tgt, w, [(0, 1), (1, 3), (3, 4)]))
+    sel = list(range(wl.n_maps))
+    so, Ao, Bo = oracle_centered_sel(hm, sel, src, tgt, w)
+    check_centered(sums, A, B, so, Ao, Bo, sel)
+    check_centered_maps(cb, sums, A, B, so, Ao, Bo, sel, 1e-2)
+    plan.close()
+
+
+@pytest.mark.parametrize("d_s,d_t,T", [(64, 64, 45), (96, 128, 64), (128, 128, 96)])
+def test_centered_single_map_items(cb, d_s, d_t, T):
+    wl = synth.Workload("csingle", 1, 2, d_s, 1, 2, d_t, 3, T, "identity", "offset", 0.1, "lognormal")
+    src, tgt, w = make_inputs(wl)
+    full = synth.head_map(wl)
+    keep = [0, 1, 3]
+    hm = {k: np.ascontiguousarray(np.asarray(v)[keep]) for k, v in full.items()}
+    plan = cb.cb_plan_create(hm, src, tgt, 4096)
+    sums, A, B = gpu_centered(cb, plan, [(src, tgt, w)])
+    sel = list(range(len(keep)))
+    so, Ao, Bo = oracle_centered_sel(hm, sel, src, tgt, w)
+    check_centered(sums, A, B, so, Ao, Bo, sel)
+    check_centered_maps(cb, sums, A, B, so, Ao, Bo, sel, 1e-2)
+    plan.close()
+
+
+def test_centered_large_channel_means(cb):
+    # channel means 30 x their spread (median |mu|/sigma ~ 18): the centered
+    # moments stay at the stats bar, where the uncentered moments of the same
+    # data lose digits to cancellation when A is recovered from G
+    wl = synth.Workload("coffset", 2, 2, 128, 3, 2, 128, 8, 2048, "qwen", "offset", 0.1, "colmass")
+    src, tgt, w = make_inputs(wl)
+    hm = synth.head_map(wl)
+    plan = cb.cb_plan_create(hm, src, tgt, wl.n_seqs * wl.seq_len)
+    sums, A, B = gpu_centered(cb, plan, seq_batches(src, tgt, w, [(0, 4), (4, 8)]))
+    sel = list(range(wl.n_maps))
+    so, Ao, Bo = oracle_centered_sel(hm, sel, src, tgt, w)
+    es, ea, eb = check_centered(sums, A, B, so, Ao, Bo, sel)
+    check_centered_maps(cb, sums, A, B, so, Ao, Bo, sel, wl.lam_rel)
+    # the same A from the uncentered moments, for comparison (reported only)
+    G, _ = gpu_stats(cb, plan, src, tgt, w)
+    Gd = G.double().cpu().numpy()
+    d = wl.d_s
+    eu = max(relF(Gd[m, :d, :d] - np.outer(Gd[m, d, :d], Gd[m, d, :d]) / Gd[m, d, d], Ao[m]) for m in sel)
+    say(f"  A from uncentered G: relF {eu:.3e} (centered {ea:.3e})")
+    assert ea * 10 < eu
+    plan.close()
+
+
+def test_centered_zero_weights_empty_calls_and_determinism(cb):
+    wl = synth.Workload("czero", 2, 2, 128, 2, 2, 96, 3, 70, "qwen", "offset", 0.1, "lognormal")
+    src, tgt, w = make_inputs(wl)
+    w[1].zero_()                                    # weight row 1: target head 1 of layer 0, K and V
+    hm = synth.head_map(wl)
+    zero_maps = [m for m in range(wl.n_maps) if hm["weight_row"][m] == 1]
+    plan = cb.cb_plan_create(hm, src, tgt, 4096)
+    s1, A1, B1 = gpu_centered(cb, plan, [(src, tgt, w)])
+    s2, A2, B2 = gpu_centered(cb, plan, [(src, tgt, w)])
+    assert torch.equal(s1, s2) and torch.equal(A1, A2) and torch.equal(B1, B2), "bitwise determinism"
+    # empty calls change nothing
+    cb.cb_stats_means(plan, src[:, :, :0], tgt[:, :, :0], w[:, :0], s2, w_row_stride=1)
+    cb.cb_stats_accumulate_centered(plan, src[:, :, :0], tgt[:, :, :0], w[:, :0], s2, A2, B2, w_row_stride=1)
+    torch.cuda.synchronize()
+    assert torch.equal(s1, s2) and torch.equal(A1, A2) and torch.equal(B1, B2)
+    for m in zero_maps:
+        assert not s1[m].any() and not A1[m].any() and not B1[m].any()
+    sel = list(range(wl.n_maps))
+    so, Ao, Bo = oracle_centered_sel(hm, sel, src, tgt, w)
+    check_centered(s1, A1, B1, so, Ao, Bo, sel)
+    # absolute lambda (the largest mean diagonal of A: a strong ridge keeps
+    # every system well conditioned, so the moments' error is not amplified):
+    # zero-weight maps solve to W = 0 and b = 0
+    lam = float(max(np.trace(Ao[m]) for m in sel) / wl.d_s)
+    maps, info = gpu_solve_centered(cb, s1, A1, B1, lam, 0)
+    assert (info.cpu().numpy() == 0).all()
+    Wo, _ = oracle.ridge_solve_centered(so, Ao, Bo, lam, relative=False)
+    Ws, _ = oracle.ridge_solve_centered(s1.cpu().numpy(), A1.double().cpu().numpy(), B1.double().cpu().numpy(),
+                                        lam, relative=False)
+    live = [m for m in sel if m not in zero_maps]
+    e = max(relF(maps[m].double().cpu().numpy(), Wo[m]) for m in live)
+    es = max(relF(maps[m].double().cpu().numpy(), Ws[m]) for m in live)
+    say(f"  centered maps parity (absolute lambda): end-to-end {e:.3e}, solver alone {es:.3e}")
+    assert e <= TOL_MAPS and es <= 1e-6
+    for m in zero_maps:
+        assert not maps[m].any()
+    # relative lambda is zero for them: the first pivot fails, maps are zero-filled
+    maps, info = gpu_solve_centered(cb, s1, A1, B1, 1e-2, cb.CB_LAMBDA_RELATIVE)
+    inf = info.cpu().numpy()
+    assert all(inf[m] == 1 for m in zero_maps) and all(inf[m] == 0 for m in sel if m not in zero_maps)
+    for m in zero_maps:
+        assert not maps[m].any()
+    plan.close()
+
+
+def test_centered_qwen50_full_size_sampled_maps(cb):
+    wl = synth.WORKLOADS["qwen50"]
+    say(f"{wl.name}: generating {wl.n_seqs} x {wl.seq_len} tokens")
+    src, tgt, w = make_inputs(wl)
+    hm = synth.head_map(wl)
+    plan = cb.cb_plan_create(hm, src, tgt, wl.n_seqs * wl.seq_len)
+    say(f"{wl.name}: GPU centered statistics")
+    sums, A, B = gpu_centered(cb, plan, [(src, tgt, w)])
+    sel = sample_maps(wl.n_maps, 8, seed=1)
+    say(f"{wl.name}: centered oracle on maps {sel}")
+    so, Ao, Bo = oracle_centered_sel(hm, sel, src, tgt, w)
+    check_centered(sums, A, B, so, Ao, Bo, sel)
+    check_centered_maps(cb, sums, A, B, so, Ao, Bo, sel, wl.lam_rel)
+    del src, tgt, w
+    plan.close()
