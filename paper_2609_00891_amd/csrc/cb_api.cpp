@@ -64,16 +64,17 @@ bool supported_width(int d) { return d == 64 || d == 96 || d == 128; }
 
 // Work units of a call: each item's token tiles (KT tokens of one sequence)
 // are cut into n_chunks chunks of chunk_tiles tiles.  Enough (item, chunk)
-// units to give every compute unit several, at most 2048 tiles (64Ki tokens)
-// per fp32 partial, and never more chunks than the plan's workspace holds
-// (max_chunks <= 0: no such limit).
-void choose_chunks(int64_t tiles, int n_items, int n_cu, int max_chunks, int *n_chunks, int *chunk_tiles) {
+// units to give every compute unit `per_cu` of them, at most 2048 tiles (64Ki
+// tokens) per fp32 partial, and never more chunks than the plan's workspace
+// holds (max_chunks <= 0: no such limit).
+void choose_chunks(int64_t tiles, int n_items, int n_cu, int max_chunks, int *n_chunks, int *chunk_tiles,
+                   int per_cu = 8) {
     if (tiles <= 0) {
         *n_chunks = 0;
         *chunk_tiles = 1;
         return;
     }
-    const int64_t target_units = 8LL * n_cu;
+    const int64_t target_units = (int64_t)per_cu * n_cu;
     int64_t nc = (target_units + n_items - 1) / n_items;
     nc = std::max<int64_t>(nc, (tiles + 2047) / 2048);
     nc = std::min<int64_t>(nc, tiles);
@@ -416,6 +417,14 @@ cb_status cb_stats_means(cb_plan *p, const cb_cache *src, const cb_cache *tgt, c
     if (cb_status s = prepare_stats(p, src, tgt, weights, w_row_stride, a, empty)) return s;
     if (empty) return ok();
     hipStream_t st = (hipStream_t)stream;
+    // The means partials are small ([unit][2][1 + d_s + d_t] fp64), so pass 1
+    // cuts the tiles finer than the moments pass, within the same workspace.
+    {
+        const int64_t ns = 1 + p->d_s + p->d_t;
+        const int64_t cap = (int64_t)p->max_chunks * cb::stats_slot_floats(p->d_s, p->d_t) / (2 * ns);
+        choose_chunks(a.n_tiles, p->n_items, p->n_cu, (int)std::min<int64_t>(cap, 1 << 20), &a.n_chunks,
+                      &a.chunk_tiles, 16);
+    }
     if (cb::launch_means(p->d_s, p->d_t, a, st) != hipSuccess)
         return fail(CB_ERR_DEVICE, "means kernel launch failed");
     cb::ReduceArgs r = reduce_args(p, a);
