@@ -17,6 +17,11 @@ Transfer"):
 * :func:`ridge_solve_centered` -- W = (A + lambda I)^-1 B, b = mu_y - W^T mu_x
   (Sec. 3.1, Eq. closedform).
 * :func:`apply` -- RNE_bf16([x;1] W~) per token (Sec. 1; Sec. 2.3, Eq. support-cost).
+* :func:`weighted_squares` -- sum w x_i^2, sum w y_j^2 per channel.
+* :func:`probe_r2` -- held-in R^2 = 1 - RSS/TSS of fitted probes, from explicit
+  residuals (Sec. 3.1, layer selection).
+* :func:`select_layers` -- mean probe R^2 per (target, source) layer pair over
+  KV heads and K/V, ranked; the first k source layers form S_l (Sec. 3.1).
 * :func:`coefficient_count` -- C(f) = 2 L_t H_t (k f d_s) d_t (Sec. 2.3, Eq. support-cost).
 
 Parity status: pinned by ``tests/test_oracle_pins.py``.
@@ -69,6 +74,14 @@ def _load():
     lib.oracle_ridge_solve_centered.restype = ctypes.c_int
     lib.oracle_ridge_solve_centered.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, _f64p, _f64p, _f64p,
                                                 ctypes.c_double, ctypes.c_int, _f64p, _i32p, ctypes.c_int]
+    lib.oracle_weighted_squares.restype = ctypes.c_int
+    lib.oracle_weighted_squares.argtypes = [ctypes.c_int] + [_i32p] * 6 + [
+        _u16p, _i64p, ctypes.c_int, _u16p, _i64p, ctypes.c_int,
+        _f32p, ctypes.c_int64, ctypes.c_int, ctypes.c_int, _f64p, ctypes.c_int]
+    lib.oracle_probe_r2.restype = ctypes.c_int
+    lib.oracle_probe_r2.argtypes = [ctypes.c_int] + [_i32p] * 6 + [
+        _f64p, _u16p, _i64p, ctypes.c_int, _u16p, _i64p, ctypes.c_int,
+        _f32p, ctypes.c_int64, ctypes.c_int, ctypes.c_int, _f64p, ctypes.c_int]
     lib.oracle_double_to_bf16_array.restype = ctypes.c_int
     lib.oracle_double_to_bf16_array.argtypes = [ctypes.c_int64, _f64p, _u16p]
     _lib = lib
@@ -205,6 +218,64 @@ def apply(head_map, W, src, src_strides, d_s, out, out_strides, d_t, n_seqs, seq
                      _ptr(ss, _i64p), d_s, _ptr(out, _u16p), _ptr(os_, _i64p), d_t,
                      int(n_seqs), int(seq_len), int(n_threads))
     return out
+
+
+def weighted_squares(head_map, src, src_strides, d_s, tgt, tgt_strides, d_t, weights, w_row_stride,
+                     n_seqs, seq_len, n_threads: int = 0):
+    """sq[m] = (sum w x_i^2 (d_s), sum w y_j^2 (d_t)) in fp64; conventions of :func:`stats`."""
+    lib = _load()
+    n, hm = _hm_arrays(head_map)
+    sq = np.zeros((n, d_s + d_t), dtype=np.float64)
+    src = np.ascontiguousarray(_u16(src))
+    tgt = np.ascontiguousarray(_u16(tgt))
+    w = np.ascontiguousarray(np.asarray(weights, dtype=np.float32))
+    ss, ts = _strides5(src_strides), _strides5(tgt_strides)
+    lib.oracle_weighted_squares(n, *[_ptr(a, _i32p) for a in hm], _ptr(src, _u16p), _ptr(ss, _i64p), d_s,
+                                _ptr(tgt, _u16p), _ptr(ts, _i64p), d_t, _ptr(w, _f32p), int(w_row_stride),
+                                int(n_seqs), int(seq_len), _ptr(sq, _f64p), int(n_threads))
+    return sq
+
+
+def probe_r2(head_map, W, src, src_strides, d_s, tgt, tgt_strides, d_t, weights, w_row_stride,
+             n_seqs, seq_len, n_threads: int = 0):
+    """r2[m] = 1 - RSS/TSS of the fitted map W~[m] ([n][d_s+1][d_t], bias last) on the
+    same weighted tokens, pooled over output channels (0 when TSS = 0)."""
+    lib = _load()
+    n, hm = _hm_arrays(head_map)
+    W = np.ascontiguousarray(np.asarray(W, dtype=np.float64))
+    assert W.shape == (n, d_s + 1, d_t)
+    r2 = np.zeros((n,), dtype=np.float64)
+    src = np.ascontiguousarray(_u16(src))
+    tgt = np.ascontiguousarray(_u16(tgt))
+    w = np.ascontiguousarray(np.asarray(weights, dtype=np.float32))
+    ss, ts = _strides5(src_strides), _strides5(tgt_strides)
+    lib.oracle_probe_r2(n, *[_ptr(a, _i32p) for a in hm], _ptr(W, _f64p), _ptr(src, _u16p), _ptr(ss, _i64p),
+                        d_s, _ptr(tgt, _u16p), _ptr(ts, _i64p), d_t, _ptr(w, _f32p), int(w_row_stride),
+                        int(n_seqs), int(seq_len), _ptr(r2, _f64p), int(n_threads))
+    return r2
+
+
+def select_layers(head_map, r2, n_tgt_layers: int, n_src_layers: int, k: int):
+    """Sec. 3.1 layer selection: score[l][j] = mean r2 over the maps with target
+    layer l and source layer j (every KV head, K and V); for each l the source
+    layers in decreasing score (equal scores: smaller j first), first k of them.
+    Pairs without maps get score -inf and are never chosen (-1 pads the list).
+    Returns (selected [L_t][k] int32, score [L_t][L_s])."""
+    tl = np.asarray(head_map["tgt_layer"])
+    sl = np.asarray(head_map["src_layer"])
+    r2 = np.asarray(r2, dtype=np.float64)
+    score = np.full((n_tgt_layers, n_src_layers), -np.inf)
+    for l in range(n_tgt_layers):
+        for j in range(n_src_layers):
+            sel = (tl == l) & (sl == j)
+            if sel.any():
+                score[l, j] = r2[sel].mean()
+    selected = np.full((n_tgt_layers, k), -1, dtype=np.int32)
+    for l in range(n_tgt_layers):
+        order = sorted(range(n_src_layers), key=lambda j: (-score[l, j], j))
+        chosen = [j for j in order if np.isfinite(score[l, j])][:k]
+        selected[l, :len(chosen)] = chosen
+    return selected, score
 
 
 def double_to_bf16(v) -> np.ndarray:

@@ -342,6 +342,102 @@ int oracle_ridge_solve_centered(int n_maps, int d_s, int d_t, const double *sums
 }
 
 /*
+ * Weighted sums of squares per channel (the diagonal second moments that the
+ * total sum of squares of a probe needs):
+ *   sq [n_maps][d_s + d_t] = (sum w x_i^2 for i < d_s, sum w y_j^2 for j < d_t).
+ * Same input conventions as oracle_stats.  Overwrites sq.  Returns 0.
+ */
+int oracle_weighted_squares(int n_maps,
+                            const int32_t *tgt_layer, const int32_t *tgt_head, const int32_t *kv,
+                            const int32_t *src_layer, const int32_t *src_head, const int32_t *weight_row,
+                            const uint16_t *src, const int64_t *src_strides, int d_s,
+                            const uint16_t *tgt, const int64_t *tgt_strides, int d_t,
+                            const float *weights, int64_t w_row_stride,
+                            int n_seqs, int seq_len, double *sq, int n_threads) {
+    set_threads(n_threads);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int m = 0; m < n_maps; ++m) {
+        double *q = sq + (int64_t)m * (d_s + d_t);
+        memset(q, 0, sizeof(double) * (size_t)(d_s + d_t));
+        for (int b = 0; b < n_seqs; ++b) {
+            for (int t = 0; t < seq_len; ++t) {
+                const uint16_t *xr = src + row_offset(src_strides, src_layer[m], kv[m], b, src_head[m], t);
+                const uint16_t *yr = tgt + row_offset(tgt_strides, tgt_layer[m], kv[m], b, tgt_head[m], t);
+                const double w = (double)weights[(int64_t)weight_row[m] * w_row_stride +
+                                                 (int64_t)b * seq_len + t];
+                for (int i = 0; i < d_s; ++i) {
+                    const double v = bf16_bits_to_double(xr[i]);
+                    q[i] += w * v * v;
+                }
+                for (int j = 0; j < d_t; ++j) {
+                    const double v = bf16_bits_to_double(yr[j]);
+                    q[d_s + j] += w * v * v;
+                }
+            }
+        }
+    }
+    return 0;
+}
+
+/*
+ * Held-in R^2 of fitted probes (Sec. 3.1, layer selection), from its
+ * definition: with the map's weighted target mean mu_y,
+ *   RSS = sum_t w_t |y_t - [x_t, 1] W~|^2,   TSS = sum_t w_t |y_t - mu_y|^2,
+ *   r2[m] = 1 - RSS / TSS   (0 when TSS = 0),
+ * pooled over the d_t output channels.  W [n_maps][d_s + 1][d_t] fp64 with the
+ * bias as the last row; same input conventions as oracle_stats.  Two passes over
+ * the tokens: the mean, then the residuals.  Returns 0.
+ */
+int oracle_probe_r2(int n_maps,
+                    const int32_t *tgt_layer, const int32_t *tgt_head, const int32_t *kv,
+                    const int32_t *src_layer, const int32_t *src_head, const int32_t *weight_row,
+                    const double *W,
+                    const uint16_t *src, const int64_t *src_strides, int d_s,
+                    const uint16_t *tgt, const int64_t *tgt_strides, int d_t,
+                    const float *weights, int64_t w_row_stride,
+                    int n_seqs, int seq_len, double *r2, int n_threads) {
+    const int P = d_s + 1;
+    set_threads(n_threads);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int m = 0; m < n_maps; ++m) {
+        const double *Wm = W + (int64_t)m * P * d_t;
+        double *x = (double *)malloc(sizeof(double) * (size_t)d_s);
+        double *mu = (double *)calloc((size_t)d_t, sizeof(double));
+        double sw = 0.0, rss = 0.0, tss = 0.0;
+        for (int b = 0; b < n_seqs; ++b) {
+            for (int t = 0; t < seq_len; ++t) {
+                const uint16_t *yr = tgt + row_offset(tgt_strides, tgt_layer[m], kv[m], b, tgt_head[m], t);
+                const double w = (double)weights[(int64_t)weight_row[m] * w_row_stride +
+                                                 (int64_t)b * seq_len + t];
+                sw += w;
+                for (int j = 0; j < d_t; ++j) mu[j] += w * bf16_bits_to_double(yr[j]);
+            }
+        }
+        for (int j = 0; j < d_t; ++j) mu[j] = sw != 0.0 ? mu[j] / sw : 0.0;
+        for (int b = 0; b < n_seqs; ++b) {
+            for (int t = 0; t < seq_len; ++t) {
+                const uint16_t *xr = src + row_offset(src_strides, src_layer[m], kv[m], b, src_head[m], t);
+                const uint16_t *yr = tgt + row_offset(tgt_strides, tgt_layer[m], kv[m], b, tgt_head[m], t);
+                const double w = (double)weights[(int64_t)weight_row[m] * w_row_stride +
+                                                 (int64_t)b * seq_len + t];
+                for (int i = 0; i < d_s; ++i) x[i] = bf16_bits_to_double(xr[i]);
+                for (int j = 0; j < d_t; ++j) {
+                    double pred = Wm[(int64_t)d_s * d_t + j];
+                    for (int i = 0; i < d_s; ++i) pred += x[i] * Wm[(int64_t)i * d_t + j];
+                    const double y = bf16_bits_to_double(yr[j]);
+                    rss += w * (y - pred) * (y - pred);
+                    tss += w * (y - mu[j]) * (y - mu[j]);
+                }
+            }
+        }
+        r2[m] = tss > 0.0 ? 1.0 - rss / tss : 0.0;
+        free(x);
+        free(mu);
+    }
+    return 0;
+}
+
+/*
  * Online application of the fitted maps.
  *   W [n_maps][P][d_t] (fp64 copies of the coefficients; row d_s is the bias)
  *   out[tgt_layer, kv, seq, tgt_head, tok, j] = RNE_bf16( sum_k x~_k W[k][j] )

@@ -579,3 +579,132 @@ def test_generators_mean_one_weights_and_head_maps():
     np.testing.assert_allclose(w.reshape(4, 2, 128).mean(-1), 1.0, rtol=1e-5)
     # the sink makes position 0 the heaviest column
     assert (w.reshape(4, 2, 128)[:, :, 0] > 10).all()
+
+
+# ----------------------------------------------------------------------------- layer-selection probes
+
+def _probe_fit(p, lam=0.0):
+    """Centered fit of every map of ``p`` (absolute lambda) and its oracle R^2."""
+    sums, A, B = _centered(p)
+    W, info = oracle.ridge_solve_centered(sums, A, B, lam, relative=False)
+    assert (info == 0).all()
+    r2 = oracle.probe_r2(p.hm, W, p.src, p.src_strides, p.d_s, p.tgt, p.tgt_strides, p.d_t, p.w,
+                         p.B * p.T, p.B, p.T)
+    return sums, A, B, W, r2
+
+
+def test_weighted_squares_match_centered_moments_and_numpy_variance():
+    rng = np.random.default_rng(31)
+    p = Problem(rng, B=2, T=30)
+    sums, A, B = _centered(p)
+    sq = oracle.weighted_squares(p.hm, p.src, p.src_strides, p.d_s, p.tgt, p.tgt_strides, p.d_t, p.w,
+                                 p.B * p.T, p.B, p.T)
+    for m in range(p.n_maps):
+        xt, y, w = p.design(m)
+        S = sums[m, 0]
+        mu_x = sums[m, 1:1 + p.d_s] / S
+        # sum w x^2 = diag(A) + S mu^2 (A from the two-pass centered statistics)
+        np.testing.assert_allclose(sq[m, :p.d_s], np.diag(A[m]) + S * mu_x ** 2, rtol=1e-11)
+        # numpy's weighted variance of y (a library routine), rescaled from mean to sum
+        var_y = np.cov(y.T, aweights=w, bias=True).diagonal() * w.sum()
+        mu_y = sums[m, 1 + p.d_s:] / S
+        np.testing.assert_allclose(sq[m, p.d_s:] - S * mu_y ** 2, var_y, rtol=1e-9)
+
+
+def test_probe_r2_matches_sklearn_weighted_variance_weighted_score():
+    from sklearn.metrics import r2_score
+    rng = np.random.default_rng(32)
+    p = Problem(rng, B=2, T=40, d_s=6, d_t=4)
+    _, _, _, W, r2 = _probe_fit(p, lam=0.3)
+    for m in range(p.n_maps):
+        xt, y, w = p.design(m)
+        pred = xt @ W[m]
+        ref = r2_score(y, pred, sample_weight=w, multioutput="variance_weighted")
+        assert r2[m] == pytest.approx(ref, abs=1e-12)
+
+
+def test_probe_r2_scalar_ols_is_squared_weighted_correlation():
+    # one source and one target channel, lambda = 0: R^2 = corr_w(x, y)^2
+    rng = np.random.default_rng(33)
+    p = Problem(rng, B=2, T=50, d_s=1, d_t=1)
+    _, _, _, _, r2 = _probe_fit(p, lam=0.0)
+    for m in range(p.n_maps):
+        xt, y, w = p.design(m)
+        c = np.cov(np.stack([xt[:, 0], y[:, 0]]), aweights=w)
+        assert r2[m] == pytest.approx(c[0, 1] ** 2 / (c[0, 0] * c[1, 1]), rel=1e-10)
+
+
+def test_probe_r2_is_one_for_an_exact_planted_map_and_zero_for_constant_targets():
+    rng = np.random.default_rng(34)
+    p = Problem(rng, values="int", B=2, T=60, d_s=4, d_t=3)
+    # y = x M + c exactly (small integers: exact in bf16 and in every sum)
+    for m in range(p.n_maps):
+        hm = p.hm
+        x = p.X[hm["src_layer"][m], hm["kv"][m], :, hm["src_head"][m]]
+        M = rng.integers(-2, 3, size=(p.d_s, p.d_t))
+        c = rng.integers(-3, 4, size=p.d_t)
+        p.Y[hm["tgt_layer"][m], hm["kv"][m], :, hm["tgt_head"][m]] = x @ M + c
+    p.tgt = to_bf16_bits(p.Y)
+    _, _, _, _, r2 = _probe_fit(p, lam=0.0)
+    np.testing.assert_allclose(r2, 1.0, atol=1e-10)
+    p.Y[...] = 3.0
+    p.tgt = to_bf16_bits(p.Y)
+    _, _, _, _, r2 = _probe_fit(p, lam=0.1)
+    assert (r2 == 0.0).all()
+
+
+def test_probe_r2_equals_the_moment_identity():
+    # RSS = TSS - 2 tr(W^T B) + tr(W^T A W) with the centered moments: the route
+    # that needs no second pass over the tokens
+    rng = np.random.default_rng(35)
+    p = Problem(rng, B=3, T=35)
+    sums, A, B, W, r2 = _probe_fit(p, lam=0.7)
+    sq = oracle.weighted_squares(p.hm, p.src, p.src_strides, p.d_s, p.tgt, p.tgt_strides, p.d_t, p.w,
+                                 p.B * p.T, p.B, p.T)
+    for m in range(p.n_maps):
+        S = sums[m, 0]
+        tss = (sq[m, p.d_s:] - sums[m, 1 + p.d_s:] ** 2 / S).sum()
+        Wm = W[m, :p.d_s]
+        rss = tss - 2 * np.sum(Wm * B[m]) + np.trace(Wm.T @ A[m] @ Wm)
+        assert r2[m] == pytest.approx(1 - rss / tss, abs=1e-11)
+
+
+def test_select_layers_ranks_mean_r2_with_ties_to_the_smaller_layer():
+    hm = {"tgt_layer": np.array([0, 0, 0, 0, 0, 0, 1, 1], np.int32),
+          "src_layer": np.array([0, 0, 1, 1, 2, 2, 2, 0], np.int32)}
+    r2 = np.array([0.2, 0.4, 0.9, 0.1, 0.5, 0.1, 0.7, 0.7])
+    sel, score = oracle.select_layers(hm, r2, n_tgt_layers=2, n_src_layers=3, k=2)
+    np.testing.assert_allclose(score[0], [0.3, 0.5, 0.3])
+    assert sel[0].tolist() == [1, 0]                       # 0.5, then the 0.3 tie goes to layer 0
+    assert sel[1].tolist() == [0, 2]                       # equal scores: smaller layer first
+    assert np.isneginf(score[1, 1])
+    sel3, _ = oracle.select_layers(hm, r2, n_tgt_layers=2, n_src_layers=3, k=3)
+    assert sel3[1].tolist() == [0, 2, -1]                  # a pair without probes is never chosen
+
+
+def test_select_layers_recovers_the_planted_source_layer():
+    # every target layer is generated from one source layer; probes over all
+    # (target, source) pairs must rank that layer first
+    rng = np.random.default_rng(36)
+    L_s, L_t, H, d, B, T = 4, 3, 2, 6, 2, 80
+    planted = [2, 0, 3]
+    hm = {k: [] for k in ("tgt_layer", "tgt_head", "kv", "src_layer", "src_head", "weight_row")}
+    for l in range(L_t):
+        for j in range(L_s):
+            for z in range(2):
+                for h in range(H):
+                    for k, v in zip(hm, (l, h, z, j, h, l * H + h)):
+                        hm[k].append(v)
+    hm = {k: np.asarray(v, np.int32) for k, v in hm.items()}
+    p = Problem(rng, L_s=L_s, H_s=H, d_s=d, L_t=L_t, H_t=H, d_t=d, B=B, T=T, hm=hm)
+    for l in range(L_t):
+        for z in range(2):
+            for h in range(H):
+                x = p.X[planted[l], z, :, h]
+                p.Y[l, z, :, h] = x @ rng.standard_normal((d, d)) + 0.3 * rng.standard_normal(x.shape[:-1] + (d,))
+    p.tgt = to_bf16_bits(p.Y)
+    _, _, _, _, r2 = _probe_fit(p, lam=1e-3)
+    sel, score = oracle.select_layers(hm, r2, L_t, L_s, k=2)
+    assert sel[:, 0].tolist() == planted
+    for l in range(L_t):
+        assert score[l, planted[l]] > 0.8 and np.sort(score[l])[-2] < 0.3
