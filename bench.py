@@ -150,6 +150,68 @@ def centered_leg(cb, plan, wl, src, tgt, w, n_calls, maps_plain, bytes_per_call,
     }
 
 
+def probe_leg(cb, wl, src, tgt, w, n_seqs, steps):
+    """Layer-selection probes (Sec. 3.1) over every (target layer, source layer)
+    pair of the qwen shape: 64 x 40 x 8 heads x K/V = 40,960 centered OLS probes
+    on the first n_seqs sequences of the resident batch (means with sums of
+    squares, centered statistics, centered solve, R^2), then the host ranking.
+    Timed with events on the launch stream after one warm-up run."""
+    import numpy as np
+    import torch
+    hm = {k: [] for k in ("tgt_layer", "tgt_head", "kv", "src_layer", "src_head", "weight_row")}
+    for l in range(wl.L_t):
+        for j in range(wl.L_s):
+            for z in range(2):
+                for h in range(wl.H_t):
+                    for k, v in zip(hm, (l, h, z, j, h, l * wl.H_t + h)):
+                        hm[k].append(v)
+    hm = {k: np.asarray(v, np.int32) for k, v in hm.items()}
+    n, d_s, d_t = len(hm["kv"]), wl.d_s, wl.d_t
+    s_, t_ = src[:, :, :n_seqs], tgt[:, :, :n_seqs]
+    w_ = w[:, :n_seqs * wl.seq_len]
+    plan = cb.cb_plan_create(hm, s_, t_, n_seqs * wl.seq_len)
+    sums = torch.empty((n, 1 + d_s + d_t), dtype=torch.float64, device="cuda")
+    sq = torch.empty((n, d_s + d_t), dtype=torch.float64, device="cuda")
+    A = torch.empty((n, d_s, d_s), dtype=torch.float32, device="cuda")
+    Bm = torch.empty((n, d_s, d_t), dtype=torch.float32, device="cuda")
+    maps = torch.empty((n, d_s + 1, d_t), dtype=torch.float32, device="cuda")
+    info = torch.empty((n,), dtype=torch.int32, device="cuda")
+    r2 = torch.empty((n,), dtype=torch.float64, device="cuda")
+    stream = torch.cuda.current_stream()
+    recs = []
+    for it in range(steps + 1):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+        e[0].record(stream)
+        cb.cb_stats_zero_centered(plan, sums, A, Bm, sq=sq)
+        cb.cb_stats_means(plan, s_, t_, w_, sums, sq=sq)
+        e[1].record(stream)
+        cb.cb_stats_accumulate_centered(plan, s_, t_, w_, sums, A, Bm)
+        e[2].record(stream)
+        cb.cb_ridge_solve_centered(sums, A, Bm, 1e-2, cb.CB_LAMBDA_RELATIVE, maps, info)
+        e[3].record(stream)
+        cb.cb_probe_r2(sums, sq, A, Bm, maps, r2)
+        e[4].record(stream)
+        if it > 0:
+            recs.append(e)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    sel, _ = cb.cb_select_layers(hm, r2.cpu().numpy(), wl.L_t, wl.L_s, 8)
+    select_ms = (time.perf_counter() - t0) * 1e3
+    mean = lambda v: sum(v) / len(v)  # noqa: E731
+    legs = [mean([e[i].elapsed_time(e[i + 1]) for e in recs]) for i in range(4)]
+    planted = [(2 * l * (wl.L_s - 1) + (wl.L_t - 1)) // (2 * (wl.L_t - 1)) for l in range(wl.L_t)]
+    plan.close()
+    return {
+        "probes": n, "calib_tokens": n_seqs * wl.seq_len,
+        "s_per_probe_run": sum(legs) / 1e3,
+        "legs_ms": {"means_with_squares": legs[0], "centered_stats": legs[1], "solve": legs[2], "r2": legs[3],
+                    "host_selection": select_ms},
+        "planted_layer_ranked_first": int(sum(int(sel[l, 0]) == planted[l] for l in range(wl.L_t))),
+        "target_layers": wl.L_t,
+        "nonpositive_pivots": int((info != 0).sum().item()),
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -159,6 +221,9 @@ def main():
     ap.add_argument("--no-apply", action="store_true", help=argparse.SUPPRESS)
     ap.add_argument("--centered-steps", type=int, default=3,
                     help="timed builds of the two-pass centered form, after the main timing (0: skip)")
+    ap.add_argument("--probe-steps", type=int, default=2,
+                    help="timed layer-selection probe runs over all layer pairs (0: skip)")
+    ap.add_argument("--probe-seqs", type=int, default=10, help="calibration sequences of the probe leg")
     ap.add_argument("--hbm-copy-probe", type=float, default=None, metavar="GIB",
                     help="only time a plain copy of GIB GiB (counter calibration)")
     args = ap.parse_args()
@@ -301,6 +366,9 @@ def main():
     }
     if args.centered_steps > 0:
         res["centered"] = centered_leg(cb, plan, wl, src, tgt, w, n_calls, maps, bytes_per_call, args.centered_steps)
+    if args.probe_steps > 0:
+        del G, C
+        res["probes"] = probe_leg(cb, wl, src, tgt, w, min(args.probe_seqs, B), args.probe_steps)
     if not args.no_cpu_baseline:
         n_threads = int(os.environ.get("OMP_NUM_THREADS", str(os.cpu_count() or 1)))
         log(f"cpu baseline on {n_threads} threads")

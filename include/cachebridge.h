@@ -19,6 +19,11 @@
  *   cb_stats_zero_centered, cb_stats_means, cb_stats_accumulate_centered,
  *   cb_ridge_solve_centered
  *
+ * and the layer-selection probes of Sec. 3.1 (centered single-source-layer
+ * fits ranked by held-in R^2):
+ *
+ *   cb_probe_r2, cb_select_layers
+ *
  * Conventions shared by every call
  * --------------------------------
  * - Row vectors: a map is W~ = [W ; b^T], a P x d_t fp32 matrix with
@@ -84,8 +89,9 @@ typedef struct {
  * predicts target (tgt_layer[m], tgt_head[m], kv[m]) from source
  * (src_layer[m], src_head[m], kv[m]) -- K from K, V from V -- using calibration
  * weight row weight_row[m].  Host arrays of n_maps entries, read during
- * cb_plan_create only.  Map m owns G[m], C[m] and maps[m].  Every target
- * (layer, kv, head) may appear at most once.
+ * cb_plan_create only.  Map m owns G[m], C[m] and maps[m].  A target (layer,
+ * kv, head) may appear in several maps (layer-selection probes fit every
+ * candidate source layer); cb_apply needs it at most once.
  */
 typedef struct {
     int32_t n_maps;
@@ -112,7 +118,7 @@ typedef struct cb_plan cb_plan;
  *   max_tokens_per_call: upper bound on n_seqs * seq_len of any later
  *     cb_stats_accumulate call (sizes the per-workgroup partial sums).
  * Errors: CB_ERR_INVALID_ARGUMENT (null, index out of range, kv not 0/1,
- * negative weight row, duplicate target), CB_ERR_UNSUPPORTED (head width),
+ * negative weight row), CB_ERR_UNSUPPORTED (head width),
  * CB_ERR_OUT_OF_MEMORY, CB_ERR_DEVICE.  On error *out is set to NULL.
  */
 cb_status cb_plan_create(const cb_head_map *map, const cb_cache *src_geom, const cb_cache *tgt_geom,
@@ -182,18 +188,21 @@ cb_status cb_ridge_solve(int32_t n_maps, int32_t P, int32_t d_t, const float *G,
  * with x, y, w read as in cb_stats_accumulate.  All pointers are device
  * pointers owned by the caller; sums is 8-byte aligned.
  *
- * cb_stats_zero_centered: set sums, A and B to zero on `stream` (fill kernels).
+ * cb_stats_zero_centered: set sums, A, B and, if not NULL, sq (see
+ * cb_stats_means) to zero on `stream` (fill kernels).
  */
-cb_status cb_stats_zero_centered(const cb_plan *plan, double *sums, float *A, float *B, void *stream);
+cb_status cb_stats_zero_centered(const cb_plan *plan, double *sums, double *sq, float *A, float *B, void *stream);
 
 /*
  * Pass 1: sums[m] += (sum w, sum w x, sum w y) over the batch, with the
  * products and sums formed in fp64 (exact products; summation order fixed).
+ * If sq is not NULL, also sq[m] += (sum w x_i^2, sum w y_j^2), [n_maps][d_s + d_t]
+ * fp64 (8-byte aligned): the sums of squares that cb_probe_r2 needs.
  * Call it on every batch before the first cb_stats_accumulate_centered.
  * Arguments, limits and errors as in cb_stats_accumulate.
  */
 cb_status cb_stats_means(cb_plan *plan, const cb_cache *src, const cb_cache *tgt, const float *weights,
-                         int64_t w_row_stride, double *sums, void *stream);
+                         int64_t w_row_stride, double *sums, double *sq, void *stream);
 
 /*
  * Pass 2: A[m] += sum w (x - mu_x)(x - mu_x)^T and B[m] += sum w (x - mu_x)(y - mu_y)^T
@@ -227,13 +236,49 @@ cb_status cb_ridge_solve_centered(int32_t n_maps, int32_t d_s, int32_t d_t, cons
                                   void *stream);
 
 /*
+ * Held-in R^2 of layer-selection probes (Sec. 3.1: for each target layer,
+ * centered single-source-layer fits under the same head assignment, scored by
+ * held-in R^2).  A probe is an ordinary map of a plan that pairs target heads
+ * with candidate source layers; fit it with cb_stats_means (with sq),
+ * cb_stats_accumulate_centered and cb_ridge_solve_centered, then
+ *   r2[m] = 1 - RSS / TSS,   pooled over the d_t output channels, where
+ *   TSS = sum_j (sum w y_j^2 - (sum w y_j)^2 / S),
+ *   RSS = sum_t w |y - [x, 1] maps[m]|^2 = TSS - 2 tr(W^T B) + tr(W^T A W)
+ * (the bias row of maps is mu_y - W^T mu_x, so the residual has weighted mean
+ * zero).  r2[m] = 0 when S = 0 or TSS = 0.  sums, sq: fp64 as written by
+ * cb_stats_means; A, B: fp32 as written by cb_stats_accumulate_centered; maps:
+ * [n_maps][d_s + 1][d_t] fp32; r2: [n_maps] fp64.  Device pointers; one
+ * workgroup per map, fp32 products of A W, fp64 traces.  d_s, d_t in
+ * {64, 96, 128}.
+ */
+cb_status cb_probe_r2(int32_t n_maps, int32_t d_s, int32_t d_t, const double *sums, const double *sq, const float *A,
+                      const float *B, const float *maps, double *r2, void *stream);
+
+/*
+ * Layer selection (Sec. 3.1), on the host: score[l][j] = the mean of r2 over
+ * the maps with target layer l and source layer j (every KV head, K and V);
+ * for each target layer the source layers in decreasing score, equal scores in
+ * increasing j; the first k of them are selected[l][0..k-1] (S_l).  Pairs
+ * without maps get score -HUGE_VAL and are never selected; missing entries
+ * are -1.  map: host head map (only n_maps, tgt_layer and src_layer are read);
+ * r2: host [n_maps]; selected: host [n_tgt_layers][k]; score: host
+ * [n_tgt_layers][n_src_layers] or NULL.  Runs synchronously on the calling
+ * thread.  Errors: CB_ERR_INVALID_ARGUMENT (NULL, non-positive counts, a layer
+ * outside the given counts).
+ */
+cb_status cb_select_layers(const cb_head_map *map, const double *r2, int32_t n_tgt_layers, int32_t n_src_layers,
+                           int32_t k, int32_t *selected, double *score);
+
+/*
  * Online mapping (Sec. 1 pipeline; Sec. 2.3 Eq. support-cost): for every map
  * m of the plan and every token of the sender cache,
  *   tgt_out(tgt_layer, kv, seq, tgt_head, tok, :) =
  *       RNE_bf16( [ src(src_layer, kv, seq, src_head, tok) , 1 ] maps[m] )
  * maps [n_maps][P][d_t] fp32 (bias in the last row).  src has the plan's source
  * geometry, tgt_out its target geometry, both with the same n_seqs and
- * seq_len.  Target positions not named by any map are left untouched.  The
+ * seq_len.  Target positions not named by any map are left untouched; a plan
+ * that maps some target more than once is rejected (CB_ERR_INVALID_ARGUMENT,
+ * before anything is enqueued).  The
  * coefficients are split into two bf16 terms and products accumulate in fp32,
  * then the bias is added and the sum is rounded once to bfloat16.
  */

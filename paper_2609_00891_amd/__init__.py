@@ -14,6 +14,8 @@ current HIP stream.  The functions keep the C names:
   :func:`cb_stats_accumulate_centered`, :func:`cb_ridge_solve_centered` -- the
   two-pass centered form: weighted sums, centered moments A, B (Sec. 3.4) and
   W = (A + lambda I)^-1 B, b = mu_y - W^T mu_x (Sec. 3.1)
+* :func:`cb_probe_r2`, :func:`cb_select_layers` -- layer-selection probes: held-in
+  R^2 per probe map and the top-k source layers per target layer (Sec. 3.1)
 
 Caches are bfloat16 tensors indexed ``[layer][kv][seq][head][tok][dim]`` (any
 strides with a unit channel stride).  Importing this package fails if the
@@ -80,9 +82,15 @@ _lib.cb_ridge_solve.restype = ctypes.c_int
 _lib.cb_ridge_solve.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp, _vp, ctypes.c_float,
                                 ctypes.c_uint32, _vp, _vp, _vp]
 _lib.cb_stats_zero_centered.restype = ctypes.c_int
-_lib.cb_stats_zero_centered.argtypes = [_vp, _vp, _vp, _vp, _vp]
+_lib.cb_stats_zero_centered.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp]
 _lib.cb_stats_means.restype = ctypes.c_int
-_lib.cb_stats_means.argtypes = [_vp, ctypes.POINTER(CbCache), ctypes.POINTER(CbCache), _vp, ctypes.c_int64, _vp, _vp]
+_lib.cb_stats_means.argtypes = [_vp, ctypes.POINTER(CbCache), ctypes.POINTER(CbCache), _vp, ctypes.c_int64, _vp, _vp,
+                                _vp]
+_lib.cb_probe_r2.restype = ctypes.c_int
+_lib.cb_probe_r2.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
+_lib.cb_select_layers.restype = ctypes.c_int
+_lib.cb_select_layers.argtypes = [ctypes.POINTER(CbHeadMap), _vp, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                  _vp, _vp]
 _lib.cb_stats_accumulate_centered.restype = ctypes.c_int
 _lib.cb_stats_accumulate_centered.argtypes = [_vp, ctypes.POINTER(CbCache), ctypes.POINTER(CbCache), _vp,
                                               ctypes.c_int64, _vp, _vp, _vp, _vp]
@@ -229,21 +237,25 @@ def _row_stride(weights: torch.Tensor, w_row_stride: Optional[int]) -> int:
     return weights.stride(0) if weights.dim() == 2 else weights.numel()
 
 
-def cb_stats_zero_centered(plan: Plan, sums: torch.Tensor, A: torch.Tensor, B: torch.Tensor, stream=None):
-    """Zero sums [n][1 + d_s + d_t] (float64), A [n][d_s][d_s] and B [n][d_s][d_t] (float32)."""
-    if sums.dtype != torch.float64 or A.dtype != torch.float32 or B.dtype != torch.float32:
-        raise ValueError("sums is float64, A and B are float32")
-    _check(_lib.cb_stats_zero_centered(plan.handle, _ptr(sums), _ptr(A), _ptr(B), _stream(stream)))
+def cb_stats_zero_centered(plan: Plan, sums: torch.Tensor, A: torch.Tensor, B: torch.Tensor,
+                           sq: Optional[torch.Tensor] = None, stream=None):
+    """Zero sums [n][1 + d_s + d_t] (float64), A [n][d_s][d_s], B [n][d_s][d_t] (float32)
+    and, if given, sq [n][d_s + d_t] (float64)."""
+    if sums.dtype != torch.float64 or A.dtype != torch.float32 or B.dtype != torch.float32 \
+            or (sq is not None and sq.dtype != torch.float64):
+        raise ValueError("sums and sq are float64, A and B are float32")
+    _check(_lib.cb_stats_zero_centered(plan.handle, _ptr(sums), _ptr(sq), _ptr(A), _ptr(B), _stream(stream)))
 
 
 def cb_stats_means(plan: Plan, src: torch.Tensor, tgt: torch.Tensor, weights: torch.Tensor, sums: torch.Tensor,
-                   w_row_stride: Optional[int] = None, stream=None):
-    """Pass 1: sums[m] += (sum w, sum w x, sum w y) over the batch (float64)."""
-    if weights.dtype != torch.float32 or sums.dtype != torch.float64:
-        raise ValueError("weights are float32, sums float64")
+                   sq: Optional[torch.Tensor] = None, w_row_stride: Optional[int] = None, stream=None):
+    """Pass 1: sums[m] += (sum w, sum w x, sum w y) and, if given, sq[m] += (sum w x^2, sum w y^2)
+    over the batch (float64)."""
+    if weights.dtype != torch.float32 or sums.dtype != torch.float64 or (sq is not None and sq.dtype != torch.float64):
+        raise ValueError("weights are float32, sums and sq float64")
     sv, tv = cache_view(src), cache_view(tgt)
     _check(_lib.cb_stats_means(plan.handle, ctypes.byref(sv), ctypes.byref(tv), _ptr(weights),
-                               _row_stride(weights, w_row_stride), _ptr(sums), _stream(stream)))
+                               _row_stride(weights, w_row_stride), _ptr(sums), _ptr(sq), _stream(stream)))
 
 
 def cb_stats_accumulate_centered(plan: Plan, src: torch.Tensor, tgt: torch.Tensor, weights: torch.Tensor,
@@ -271,6 +283,39 @@ def cb_ridge_solve_centered(sums: torch.Tensor, A: torch.Tensor, B: torch.Tensor
         raise ValueError("sums is float64, info int32")
     _check(_lib.cb_ridge_solve_centered(n, d_s, d_t, _ptr(sums), _ptr(A), _ptr(B), float(lam), int(flags),
                                         _ptr(maps), _ptr(info), _stream(stream)))
+
+
+def cb_probe_r2(sums: torch.Tensor, sq: torch.Tensor, A: torch.Tensor, B: torch.Tensor, maps: torch.Tensor,
+                r2: torch.Tensor, stream=None):
+    """r2[m] = 1 - RSS/TSS of the fitted probe maps[m] on its calibration data (float64)."""
+    n, d_s, _ = A.shape
+    d_t = B.shape[2]
+    if sums.shape != (n, 1 + d_s + d_t) or sq.shape != (n, d_s + d_t) or B.shape != (n, d_s, d_t) \
+            or maps.shape != (n, d_s + 1, d_t) or r2.shape != (n,):
+        raise ValueError("sums [n][1+d_s+d_t], sq [n][d_s+d_t], A [n][d_s][d_s], B [n][d_s][d_t], "
+                         "maps [n][d_s+1][d_t], r2 [n]")
+    if sums.dtype != torch.float64 or sq.dtype != torch.float64 or r2.dtype != torch.float64:
+        raise ValueError("sums, sq and r2 are float64")
+    _check(_lib.cb_probe_r2(n, d_s, d_t, _ptr(sums), _ptr(sq), _ptr(A), _ptr(B), _ptr(maps), _ptr(r2),
+                            _stream(stream)))
+
+
+def cb_select_layers(head_map: Mapping[str, object], r2, n_tgt_layers: int, n_src_layers: int, k: int):
+    """Host layer selection: returns (selected [L_t][k] int32, score [L_t][L_s] float64) as numpy arrays."""
+    import numpy as np  # noqa: PLC0415
+
+    tl = np.ascontiguousarray(np.asarray(head_map["tgt_layer"], dtype=np.int32))
+    sl = np.ascontiguousarray(np.asarray(head_map["src_layer"], dtype=np.int32))
+    r = np.ascontiguousarray(np.asarray(r2.cpu() if isinstance(r2, torch.Tensor) else r2, dtype=np.float64))
+    hm = CbHeadMap()
+    hm.n_maps = tl.shape[0]
+    hm.tgt_layer = tl.ctypes.data_as(_i32p)
+    hm.src_layer = sl.ctypes.data_as(_i32p)
+    selected = np.zeros((n_tgt_layers, k), dtype=np.int32)
+    score = np.zeros((n_tgt_layers, n_src_layers), dtype=np.float64)
+    _check(_lib.cb_select_layers(ctypes.byref(hm), r.ctypes.data, n_tgt_layers, n_src_layers, k,
+                                 selected.ctypes.data, score.ctypes.data))
+    return selected, score
 
 
 def cb_apply(plan: Plan, maps: torch.Tensor, src: torch.Tensor, tgt_out: torch.Tensor, stream=None):

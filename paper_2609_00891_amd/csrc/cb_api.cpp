@@ -25,6 +25,7 @@ struct cb_plan {
     int n_cu = 256;
     int32_t n_maps = 0, L_s = 0, H_s = 0, d_s = 0, L_t = 0, H_t = 0, d_t = 0;
     int64_t max_tokens = 0;
+    bool duplicate_targets = false;   // some target (layer, kv, head) has several maps (probes)
     // statistics schedule
     int32_t n_items = 0;
     int32_t max_chunks = 1;
@@ -220,6 +221,7 @@ cb_status cb_plan_create(const cb_head_map *map, const cb_cache *src_geom, const
 
     const int n = map->n_maps;
     std::set<std::tuple<int, int, int>> targets;
+    bool duplicate = false;
     for (int m = 0; m < n; ++m) {
         const int tl = map->tgt_layer[m], th = map->tgt_head[m], z = map->kv[m];
         const int sl = map->src_layer[m], sh = map->src_head[m], wr = map->weight_row[m];
@@ -229,8 +231,7 @@ cb_status cb_plan_create(const cb_head_map *map, const cb_cache *src_geom, const
             return fail(CB_ERR_INVALID_ARGUMENT, "map %d: source (%d, %d) outside %d x %d", m, sl, sh, L_s, H_s);
         if (z != 0 && z != 1) return fail(CB_ERR_INVALID_ARGUMENT, "map %d: kv must be 0 or 1 (got %d)", m, z);
         if (wr < 0) return fail(CB_ERR_INVALID_ARGUMENT, "map %d: negative weight row", m);
-        if (!targets.insert(std::make_tuple(tl, z, th)).second)
-            return fail(CB_ERR_INVALID_ARGUMENT, "map %d: target (layer %d, kv %d, head %d) appears twice", m, tl, z, th);
+        if (!targets.insert(std::make_tuple(tl, z, th)).second) duplicate = true;
     }
 
     cb_plan *p = new cb_plan();
@@ -245,6 +246,7 @@ cb_status cb_plan_create(const cb_head_map *map, const cb_cache *src_geom, const
     p->L_s = L_s; p->H_s = H_s; p->d_s = d_s;
     p->L_t = L_t; p->H_t = H_t; p->d_t = d_t;
     p->max_tokens = max_tokens_per_call;
+    p->duplicate_targets = duplicate;
 
     // ---- group maps by source block, in order of first appearance
     std::map<std::tuple<int, int, int>, int> gid;
@@ -396,39 +398,41 @@ cb_status cb_stats_accumulate(cb_plan *p, const cb_cache *src, const cb_cache *t
     return ok();
 }
 
-cb_status cb_stats_zero_centered(const cb_plan *p, double *sums, float *A, float *B, void *stream) {
+cb_status cb_stats_zero_centered(const cb_plan *p, double *sums, double *sq, float *A, float *B, void *stream) {
     if (!p || !sums || !A || !B) return fail(CB_ERR_INVALID_ARGUMENT, "plan, sums, A and B must be non-NULL");
     if (cb_status s = check_device(p)) return s;
     const int64_t n = p->n_maps, ds = p->d_s, dt = p->d_t;
     hipStream_t st = (hipStream_t)stream;
     if (cb::launch_fill_zero((float *)sums, 2 * n * (1 + ds + dt), st) != hipSuccess ||
+        (sq && cb::launch_fill_zero((float *)sq, 2 * n * (ds + dt), st) != hipSuccess) ||
         cb::launch_fill_zero(A, n * ds * ds, st) != hipSuccess || cb::launch_fill_zero(B, n * ds * dt, st) != hipSuccess)
         return fail(CB_ERR_DEVICE, "fill kernel launch failed");
     return ok();
 }
 
 cb_status cb_stats_means(cb_plan *p, const cb_cache *src, const cb_cache *tgt, const float *weights,
-                         int64_t w_row_stride, double *sums, void *stream) {
+                         int64_t w_row_stride, double *sums, double *sq, void *stream) {
     if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
     if (!sums) return fail(CB_ERR_INVALID_ARGUMENT, "sums must be non-NULL");
-    if (((uintptr_t)sums) % 8) return fail(CB_ERR_MISALIGNED, "sums must be 8-byte aligned");
+    if (((uintptr_t)sums) % 8 || ((uintptr_t)sq) % 8) return fail(CB_ERR_MISALIGNED, "sums and sq must be 8-byte aligned");
     cb::StatsArgs a = {};
     bool empty = false;
     if (cb_status s = prepare_stats(p, src, tgt, weights, w_row_stride, a, empty)) return s;
     if (empty) return ok();
     hipStream_t st = (hipStream_t)stream;
-    // The means partials are small ([unit][2][1 + d_s + d_t] fp64), so pass 1
-    // cuts the tiles finer than the moments pass, within the same workspace.
+    // The means partials are small ([unit][2][entries] fp64), so pass 1 cuts
+    // the tiles finer than the moments pass, within the same workspace.
     {
-        const int64_t ns = 1 + p->d_s + p->d_t;
-        const int64_t cap = (int64_t)p->max_chunks * cb::stats_slot_floats(p->d_s, p->d_t) / (2 * ns);
+        const int64_t ne = 1 + p->d_s + p->d_t + (sq ? p->d_s + p->d_t : 0);
+        const int64_t cap = (int64_t)p->max_chunks * cb::stats_slot_floats(p->d_s, p->d_t) / (2 * ne);
         choose_chunks(a.n_tiles, p->n_items, p->n_cu, (int)std::min<int64_t>(cap, 1 << 20), &a.n_chunks,
                       &a.chunk_tiles, 16);
     }
-    if (cb::launch_means(p->d_s, p->d_t, a, st) != hipSuccess)
+    if (cb::launch_means(p->d_s, p->d_t, a, sq != nullptr, st) != hipSuccess)
         return fail(CB_ERR_DEVICE, "means kernel launch failed");
     cb::ReduceArgs r = reduce_args(p, a);
     r.sums = sums;
+    r.sq = sq;
     if (cb::launch_means_reduce(p->d_s, p->d_t, r, st) != hipSuccess)
         return fail(CB_ERR_DEVICE, "means reduction launch failed");
     return ok();
@@ -495,8 +499,62 @@ cb_status cb_ridge_solve_centered(int32_t n_maps, int32_t d_s, int32_t d_t, cons
     return ok();
 }
 
+cb_status cb_probe_r2(int32_t n_maps, int32_t d_s, int32_t d_t, const double *sums, const double *sq, const float *A,
+                      const float *B, const float *maps, double *r2, void *stream) {
+    if (n_maps < 0) return fail(CB_ERR_INVALID_ARGUMENT, "n_maps is negative");
+    if (!supported_width(d_s) || !supported_width(d_t))
+        return fail(CB_ERR_UNSUPPORTED, "d_s and d_t must be 64, 96 or 128 (got d_s=%d, d_t=%d)", d_s, d_t);
+    if (n_maps == 0) return ok();
+    if (!sums || !sq || !A || !B || !maps || !r2)
+        return fail(CB_ERR_INVALID_ARGUMENT, "sums, sq, A, B, maps and r2 must be non-NULL");
+    if (((uintptr_t)sums) % 8 || ((uintptr_t)sq) % 8 || ((uintptr_t)r2) % 8 || ((uintptr_t)A) % 4 ||
+        ((uintptr_t)B) % 4 || ((uintptr_t)maps) % 4)
+        return fail(CB_ERR_MISALIGNED, "sums, sq, r2 must be 8-byte and A, B, maps 4-byte aligned");
+    if (cb::launch_probe_r2(n_maps, d_s, d_t, sums, sq, A, B, maps, r2, (hipStream_t)stream) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "probe R^2 launch failed");
+    return ok();
+}
+
+cb_status cb_select_layers(const cb_head_map *map, const double *r2, int32_t n_tgt_layers, int32_t n_src_layers,
+                           int32_t k, int32_t *selected, double *score) {
+    if (!map || !r2 || !selected) return fail(CB_ERR_INVALID_ARGUMENT, "map, r2 and selected must be non-NULL");
+    if (!map->tgt_layer || !map->src_layer) return fail(CB_ERR_INVALID_ARGUMENT, "map->tgt_layer and src_layer must be non-NULL");
+    if (map->n_maps < 0 || n_tgt_layers <= 0 || n_src_layers <= 0 || k <= 0)
+        return fail(CB_ERR_INVALID_ARGUMENT, "n_maps >= 0 and positive layer counts and k are required");
+    const int64_t cells = (int64_t)n_tgt_layers * n_src_layers;
+    std::vector<double> sum(cells, 0.0);
+    std::vector<int64_t> cnt(cells, 0);
+    for (int m = 0; m < map->n_maps; ++m) {
+        const int l = map->tgt_layer[m], j = map->src_layer[m];
+        if (l < 0 || l >= n_tgt_layers || j < 0 || j >= n_src_layers)
+            return fail(CB_ERR_INVALID_ARGUMENT, "map %d: layer pair (%d, %d) outside %d x %d", m, l, j, n_tgt_layers,
+                        n_src_layers);
+        sum[(int64_t)l * n_src_layers + j] += r2[m];
+        cnt[(int64_t)l * n_src_layers + j] += 1;
+    }
+    std::vector<int> order(n_src_layers);
+    for (int l = 0; l < n_tgt_layers; ++l) {
+        std::vector<double> sc(n_src_layers);
+        for (int j = 0; j < n_src_layers; ++j) {
+            const int64_t c = (int64_t)l * n_src_layers + j;
+            sc[j] = cnt[c] ? sum[c] / (double)cnt[c] : -HUGE_VAL;
+            if (score) score[c] = sc[j];
+        }
+        for (int j = 0; j < n_src_layers; ++j) order[j] = j;
+        std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return sc[a] > sc[b]; });
+        int n = 0;
+        for (int j : order)
+            if (n < k && cnt[(int64_t)l * n_src_layers + j]) selected[(int64_t)l * k + n++] = j;
+        for (; n < k; ++n) selected[(int64_t)l * k + n] = -1;
+    }
+    return ok();
+}
+
 cb_status cb_apply(cb_plan *p, const float *maps, const cb_cache *src, const cb_cache *tgt_out, void *stream) {
     if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
+    if (p->duplicate_targets)
+        return fail(CB_ERR_INVALID_ARGUMENT, "the plan maps some target (layer, kv, head) more than once; "
+                                             "cb_apply needs one map per target");
     if (!maps) return fail(CB_ERR_INVALID_ARGUMENT, "maps is NULL");
     if (cb_status s = check_cache("src", src, p->L_s, p->H_s, p->d_s)) return s;
     if (cb_status s = check_cache("tgt_out", tgt_out, p->L_t, p->H_t, p->d_t)) return s;

@@ -76,6 +76,7 @@ struct ReduceArgs {
     int32_t n_items, n_chunks, n_maps;
     float *G, *C;         // plain: G [n][P][P], C [n][P][d_t]; centered: A [n][d_s][d_s], B [n][d_s][d_t]
     double *sums;         // centered: read; means: added to.  [n_maps][1 + d_s + d_t] = (sum w, sum w x, sum w y)
+    double *sq;           // means only, optional: added to.  [n_maps][d_s + d_t] = (sum w x^2, sum w y^2)
 };
 
 struct ApplyArgs {
@@ -97,7 +98,9 @@ hipError_t launch_stats(int d_s, int d_t, const StatsArgs &a, hipStream_t s);
 hipError_t launch_reduce(int d_s, int d_t, const ReduceArgs &a, hipStream_t s);
 hipError_t launch_stats_centered(int d_s, int d_t, const StatsArgs &a, hipStream_t s);
 hipError_t launch_reduce_centered(int d_s, int d_t, const ReduceArgs &a, hipStream_t s);
-hipError_t launch_means(int d_s, int d_t, const StatsArgs &a, hipStream_t s);
+hipError_t launch_means(int d_s, int d_t, const StatsArgs &a, bool sq, hipStream_t s);
+hipError_t launch_probe_r2(int32_t n_maps, int32_t d_s, int32_t d_t, const double *sums, const double *sq,
+                           const float *A, const float *B, const float *maps, double *r2, hipStream_t s);
 hipError_t launch_means_reduce(int d_s, int d_t, const ReduceArgs &a, hipStream_t s);
 hipError_t launch_solve_centered(int32_t n_maps, int32_t d_s, int32_t d_t, const double *sums, const float *A,
                                  const float *B, float lambda, uint32_t flags, float *maps, int32_t *info,

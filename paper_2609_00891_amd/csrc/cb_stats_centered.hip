@@ -24,10 +24,13 @@
 namespace cb {
 namespace {
 
-template <int DS, int DT>
+// SQ: also the per-channel sums of squares (sum w x^2, sum w y^2).
+template <int DS, int DT, bool SQ>
 struct MCfg {
     static constexpr int NCBX = DS / 8, NCBY = DT / 8;          // 16-byte chunks per row
     static constexpr int NS = 1 + DS + DT;                      // sums per map
+    static constexpr int NQ = SQ ? DS + DT : 0;                 // sums of squares per map
+    static constexpr int NE = NS + NQ;                          // partial entries per map
     static constexpr int MAXR = 256 / (NCBX + NCBY);            // token rows of an item with one map
 };
 
@@ -49,12 +52,12 @@ struct MGeo {
 // repeated lines do not reach HBM twice.  Tiles are whole 32-token runs of
 // one sequence, so their position is computed once per tile (the same in
 // every thread).
-template <int DS, int DT, int NSL>
+template <int DS, int DT, bool SQ, int NSL>
 __device__ __forceinline__ void means_unit(const StatsArgs &a, const StatsItem *it, int tile_begin, int n_tiles,
-                                           double (*red)[2 * MCfg<DS, DT>::NS]) {
-    using M = MCfg<DS, DT>;
+                                           double (*red)[2 * MCfg<DS, DT, SQ>::NE]) {
+    using M = MCfg<DS, DT, SQ>;
     using Gm = MGeo<DS, DT, NSL>;
-    constexpr int NCBX = M::NCBX, NCBY = M::NCBY, NS = M::NS, R = Gm::R, J = Gm::J;
+    constexpr int NCBX = M::NCBX, NCBY = M::NCBY, NS = M::NS, NE = M::NE, R = Gm::R, J = Gm::J;
     const int tid = threadIdx.x;
     const int col = tid % Gm::NCOL, row = tid / Gm::NCOL;
     if (row >= R) return;
@@ -71,9 +74,9 @@ __device__ __forceinline__ void means_unit(const StatsArgs &a, const StatsItem *
     const float *wp = a.w + (int64_t)it->wrow[slot] * a.w_row_stride + row;
     const int64_t jstep = (int64_t)R * st.tok;                  // elements between a thread's tokens
 
-    double acc[8], sw = 0.0;
+    double acc[8], acq[8], sw = 0.0;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] = 0.0;
+    for (int e = 0; e < 8; ++e) acc[e] = acq[e] = 0.0;
     for (int t = 0; t < n_tiles; ++t) {
         const uint32_t u = (uint32_t)(tile_begin + t);
         const uint32_t seq = fastdiv(u, a.TPS);
@@ -99,26 +102,40 @@ __device__ __forceinline__ void means_unit(const StatsArgs &a, const StatsItem *
             sw += ww;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                acc[2 * e] = __builtin_fma(ww, (double)bf_lo(xv[e]), acc[2 * e]);
-                acc[2 * e + 1] = __builtin_fma(ww, (double)bf_hi(xv[e]), acc[2 * e + 1]);
+                const double v0 = (double)bf_lo(xv[e]), v1 = (double)bf_hi(xv[e]);
+                if constexpr (SQ) {
+                    const double t0 = ww * v0, t1 = ww * v1;        // exact: 24 + 8 significant bits
+                    acc[2 * e] += t0;
+                    acc[2 * e + 1] += t1;
+                    acq[2 * e] = __builtin_fma(t0, v0, acq[2 * e]);   // exact product, rounded sum
+                    acq[2 * e + 1] = __builtin_fma(t1, v1, acq[2 * e + 1]);
+                } else {
+                    acc[2 * e] = __builtin_fma(ww, v0, acc[2 * e]);
+                    acc[2 * e + 1] = __builtin_fma(ww, v1, acc[2 * e + 1]);
+                }
             }
         }
     }
-    // this thread's entries of the unit's sums (slot, index)
-    const int off = slot * NS + (isx ? 1 + 8 * cc : 1 + DS + 8 * cc);
+    // this thread's entries of the unit's partial: per slot [sums (NS) | squares (NQ)]
+    const int off = slot * NE + (isx ? 1 + 8 * cc : 1 + DS + 8 * cc);
 #pragma unroll
     for (int e = 0; e < 8; ++e) red[row][off + e] = acc[e];
-    if (!isx && cc == 0) red[row][slot * NS] = sw;            // sum w of the slot, once per slot
+    if constexpr (SQ) {
+        const int offq = slot * NE + NS + (isx ? 8 * cc : DS + 8 * cc);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) red[row][offq + e] = acq[e];
+    }
+    if (!isx && cc == 0) red[row][slot * NE] = sw;            // sum w of the slot, once per slot
 }
 
 // One workgroup per (item, chunk) unit: the unit's rows are combined through
-// LDS in a fixed order and written as an fp64 partial [unit][2][NS].
-template <int DS, int DT>
+// LDS in a fixed order and written as an fp64 partial [unit][2][NE].
+template <int DS, int DT, bool SQ>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(4)))
 void means_kernel(StatsArgs a) {
-    using M = MCfg<DS, DT>;
-    constexpr int NS = M::NS;
-    __shared__ double red[M::MAXR][2 * NS];
+    using M = MCfg<DS, DT, SQ>;
+    constexpr int NE = M::NE;
+    __shared__ double red[M::MAXR][2 * NE];
     const int unit = blockIdx.x;
     const int item_id = unit % a.n_items, chunk = unit / a.n_items;
     const StatsItem *it = a.items + item_id;
@@ -127,44 +144,47 @@ void means_kernel(StatsArgs a) {
     const int n_tiles = min(a.n_tiles, tile_begin + a.chunk_tiles) - tile_begin;
     if (n_tiles <= 0) return;                                  // the same in every thread
     int R;
-    if (n_slots == 1) { means_unit<DS, DT, 1>(a, it, tile_begin, n_tiles, red); R = MGeo<DS, DT, 1>::R; }
-    else { means_unit<DS, DT, 2>(a, it, tile_begin, n_tiles, red); R = MGeo<DS, DT, 2>::R; }
+    if (n_slots == 1) { means_unit<DS, DT, SQ, 1>(a, it, tile_begin, n_tiles, red); R = MGeo<DS, DT, 1>::R; }
+    else { means_unit<DS, DT, SQ, 2>(a, it, tile_begin, n_tiles, red); R = MGeo<DS, DT, 2>::R; }
     __syncthreads();
-    double *dst = (double *)a.partials + (int64_t)unit * 2 * NS;
-    for (int idx = threadIdx.x; idx < n_slots * NS; idx += 256) {
+    double *dst = (double *)a.partials + (int64_t)unit * 2 * NE;
+    for (int idx = threadIdx.x; idx < n_slots * NE; idx += 256) {
         double s = 0.0;
         for (int r = 0; r < R; ++r) s += red[r][idx];
         dst[idx] = s;
     }
 }
 
-// sums[m] += the fp64 partials of map m over all chunks, in chunk order.
-template <int DS, int DT>
+// sums[m] (and sq[m]) += the fp64 partials of map m over all chunks, in chunk order.
+template <int DS, int DT, bool SQ>
 __global__ __launch_bounds__(256) void means_reduce_kernel(ReduceArgs a) {
-    using M = MCfg<DS, DT>;
+    using M = MCfg<DS, DT, SQ>;
     const int m = blockIdx.x;
     const int item = a.map_item[m], slot = a.map_slot[m];
-    const double *part = (const double *)a.partials + ((int64_t)item * 2 + slot) * M::NS;
-    const int64_t chunk_stride = (int64_t)a.n_items * 2 * M::NS;
-    for (int e = threadIdx.x; e < M::NS; e += 256) {
+    const double *part = (const double *)a.partials + ((int64_t)item * 2 + slot) * M::NE;
+    const int64_t chunk_stride = (int64_t)a.n_items * 2 * M::NE;
+    for (int e = threadIdx.x; e < M::NE; e += 256) {
         double s = 0.0;
         for (int ch = 0; ch < a.n_chunks; ++ch) s += part[ch * chunk_stride + e];
-        a.sums[(int64_t)m * M::NS + e] += s;
+        if (e < M::NS) a.sums[(int64_t)m * M::NS + e] += s;
+        else a.sq[(int64_t)m * M::NQ + (e - M::NS)] += s;
     }
 }
 
 template <int DS, int DT>
-hipError_t launch_means_t(const StatsArgs &a, hipStream_t s) {
+hipError_t launch_means_t(const StatsArgs &a, bool sq, hipStream_t s) {
     const int grid = a.n_items * a.n_chunks;
     if (grid == 0) return hipSuccess;
-    hipLaunchKernelGGL((means_kernel<DS, DT>), dim3(grid), dim3(256), 0, s, a);
+    if (sq) hipLaunchKernelGGL((means_kernel<DS, DT, true>), dim3(grid), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((means_kernel<DS, DT, false>), dim3(grid), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
 template <int DS, int DT>
 hipError_t launch_means_reduce_t(const ReduceArgs &a, hipStream_t s) {
     if (a.n_maps == 0) return hipSuccess;
-    hipLaunchKernelGGL((means_reduce_kernel<DS, DT>), dim3(a.n_maps), dim3(256), 0, s, a);
+    if (a.sq) hipLaunchKernelGGL((means_reduce_kernel<DS, DT, true>), dim3(a.n_maps), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((means_reduce_kernel<DS, DT, false>), dim3(a.n_maps), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
@@ -182,8 +202,8 @@ hipError_t launch_stats_centered_t(const StatsArgs &a, hipStream_t s) {
 
 }  // namespace
 
-hipError_t launch_means(int d_s, int d_t, const StatsArgs &a, hipStream_t s) {
-    CB_DISPATCH(launch_means_t, d_s, d_t, a, s);
+hipError_t launch_means(int d_s, int d_t, const StatsArgs &a, bool sq, hipStream_t s) {
+    CB_DISPATCH(launch_means_t, d_s, d_t, a, sq, s);
 }
 
 hipError_t launch_means_reduce(int d_s, int d_t, const ReduceArgs &a, hipStream_t s) {

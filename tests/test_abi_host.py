@@ -53,7 +53,6 @@ def _hm(n=2):
     (lambda h: h.update(src_head=np.array([0, 9], np.int32)), "CB_ERR_INVALID_ARGUMENT"),
     (lambda h: h.update(tgt_layer=np.array([0, -1], np.int32)), "CB_ERR_INVALID_ARGUMENT"),
     (lambda h: h.update(weight_row=np.array([0, -3], np.int32)), "CB_ERR_INVALID_ARGUMENT"),
-    (lambda h: h.update(tgt_head=np.array([1, 1], np.int32)), "CB_ERR_INVALID_ARGUMENT"),   # duplicate target
 ])
 def test_plan_create_rejects_bad_head_maps(mutate, status):
     import paper_2609_00891_amd as cb
@@ -97,8 +96,8 @@ def test_null_arguments_are_rejected_before_any_launch():
 def test_centered_entry_points_reject_bad_arguments_on_the_host():
     import paper_2609_00891_amd as cb
     lib = cb.library()
-    assert lib.cb_stats_zero_centered(None, None, None, None, None) == 1
-    assert lib.cb_stats_means(None, None, None, None, 0, None, None) == 1
+    assert lib.cb_stats_zero_centered(None, None, None, None, None, None) == 1
+    assert lib.cb_stats_means(None, None, None, None, 0, None, None, None) == 1
     assert lib.cb_stats_accumulate_centered(None, None, None, None, 0, None, None, None, None) == 1
     f = ctypes.c_float
     solve = lib.cb_ridge_solve_centered
@@ -111,3 +110,21 @@ def test_centered_entry_points_reject_bad_arguments_on_the_host():
     assert solve(-1, 128, 128, None, None, None, f(0.1), 1, None, None, None) == 1
     assert solve(0, 128, 128, None, None, None, f(0.1), 3, None, None, None) == 0     # nothing to do
     assert "NULL" in cb.cb_last_error() or cb.cb_last_error() == ""
+
+
+def test_probe_entry_points_reject_bad_arguments_and_rank_on_the_host():
+    import paper_2609_00891_amd as cb
+    lib = cb.library()
+    assert lib.cb_probe_r2(4, 80, 128, None, None, None, None, None, None, None) == 6
+    assert lib.cb_probe_r2(4, 128, 128, None, None, None, None, None, None, None) == 1
+    assert lib.cb_probe_r2(0, 128, 128, None, None, None, None, None, None, None) == 0
+    assert lib.cb_select_layers(None, None, 1, 1, 1, None, None) == 1
+    # the host ranking: mean R^2 per (target, source) layer pair, ties to the smaller layer
+    hm = {"tgt_layer": [0, 0, 0, 0, 0, 0, 1, 1], "src_layer": [0, 0, 1, 1, 2, 2, 2, 0]}
+    r2 = np.array([0.2, 0.4, 0.9, 0.1, 0.5, 0.1, 0.7, 0.7])
+    sel, score = cb.cb_select_layers(hm, r2, 2, 3, 3)
+    np.testing.assert_allclose(score[0], [0.3, 0.5, 0.3])
+    assert sel.tolist() == [[1, 0, 2], [0, 2, -1]]
+    assert score[1, 1] == -np.inf
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_INVALID_ARGUMENT"):
+        cb.cb_select_layers({"tgt_layer": [0], "src_layer": [5]}, np.zeros(1), 1, 3, 1)

@@ -617,3 +617,110 @@ def test_centered_qwen50_full_size_sampled_maps(cb):
     check_centered_maps(cb, sums, A, B, so, Ao, Bo, sel, wl.lam_rel)
     del src, tgt, w
     plan.close()
+
+
+# ----------------------------------------------------------------------------- layer-selection probes
+
+TOL_R2 = 1e-5          # absolute, R^2 in [0, 1]
+
+
+def probe_head_map(L_t, L_s, H):
+    """Every target (layer, head, K/V) paired with every source layer, same head."""
+    hm = {k: [] for k in ("tgt_layer", "tgt_head", "kv", "src_layer", "src_head", "weight_row")}
+    for l in range(L_t):
+        for j in range(L_s):
+            for z in range(2):
+                for h in range(H):
+                    for k, v in zip(hm, (l, h, z, j, h, l * H + h)):
+                        hm[k].append(v)
+    return {k: np.asarray(v, np.int32) for k, v in hm.items()}
+
+
+def gpu_probe(cb, plan, src, tgt, w, lam=0.0, flags=0):
+    n, ds, dt = plan.n_maps, plan.d_s, plan.d_t
+    sums = torch.empty((n, 1 + ds + dt), dtype=torch.float64, device="cuda")
+    sq = torch.empty((n, ds + dt), dtype=torch.float64, device="cuda")
+    A = torch.empty((n, ds, ds), dtype=torch.float32, device="cuda")
+    B = torch.empty((n, ds, dt), dtype=torch.float32, device="cuda")
+    cb.cb_stats_zero_centered(plan, sums, A, B, sq=sq)
+    cb.cb_stats_means(plan, src, tgt, w, sums, sq=sq)
+    cb.cb_stats_accumulate_centered(plan, src, tgt, w, sums, A, B)
+    maps, info = gpu_solve_centered(cb, sums, A, B, lam, flags)
+    r2 = torch.empty((n,), dtype=torch.float64, device="cuda")
+    cb.cb_probe_r2(sums, sq, A, B, maps, r2)
+    torch.cuda.synchronize()
+    return sums, sq, A, B, maps, info, r2
+
+
+@pytest.mark.parametrize("d_s,d_t", [(64, 64), (128, 96)])
+def test_probe_r2_and_layer_selection(cb, d_s, d_t):
+    # targets are generated from source layers round(l * 3 / 2) = [0, 2, 3];
+    # the probes fit every (target layer, source layer) pair by OLS
+    L_s, L_t, H = 4, 3, 2
+    wl = synth.Workload("probe", L_s, H, d_s, L_t, H, d_t, 4, 300, "qwen", "offset", 0.3, "lognormal")
+    src, tgt, w = make_inputs(wl)
+    hm = probe_head_map(L_t, L_s, H)
+    plan = cb.cb_plan_create(hm, src, tgt, wl.n_seqs * wl.seq_len)
+    sums, sq, A, B, maps, info, r2 = gpu_probe(cb, plan, src, tgt, w)
+    assert (info.cpu().numpy() == 0).all()
+    n = len(hm["kv"])
+    sel = list(range(n))
+    chm, xb, ss, yb, ts, ws, Bn, T = compact(hm, sel, src, tgt, w)
+    sqo = oracle.weighted_squares(chm, xb, ss, d_s, yb, ts, d_t, ws, Bn * T, Bn, T, n_threads=NTHREADS)
+    esq = max(relF(sq[m].cpu().numpy(), sqo[m]) for m in sel)
+    so, Ao, Bo = oracle.stats_centered(chm, xb, ss, d_s, yb, ts, d_t, ws, Bn * T, Bn, T, n_threads=NTHREADS)
+    Wo, io = oracle.ridge_solve_centered(so, Ao, Bo, 0.0, relative=False, n_threads=NTHREADS)
+    assert (io == 0).all()
+    r2o = oracle.probe_r2(chm, Wo, xb, ss, d_s, yb, ts, d_t, ws, Bn * T, Bn, T, n_threads=NTHREADS)
+    # the R^2 kernel alone: the oracle's residual pass on the GPU's own maps
+    r2s = oracle.probe_r2(chm, maps.double().cpu().numpy(), xb, ss, d_s, yb, ts, d_t, ws, Bn * T, Bn, T,
+                          n_threads=NTHREADS)
+    g = r2.cpu().numpy()
+    e_end, e_alone = float(np.abs(g - r2o).max()), float(np.abs(g - r2s).max())
+    say(f"  probes: sq relF {esq:.3e}; R^2 max |diff| end-to-end {e_end:.3e}, kernel alone {e_alone:.3e}")
+    assert esq <= TOL_SUMS and e_end <= TOL_R2 and e_alone <= TOL_R2
+    # selection: the planted layer first on both sides; the full order agrees
+    # wherever the oracle's scores are separated by more than the R^2 bar
+    selg, scg = cb.cb_select_layers(hm, g, L_t, L_s, L_s)
+    selo, sco = oracle.select_layers(hm, r2o, L_t, L_s, L_s)
+    planted = [synth._round_ratio(l, L_s - 1, L_t - 1) for l in range(L_t)]
+    assert selg[:, 0].tolist() == planted and selo[:, 0].tolist() == planted
+    for l in range(L_t):
+        for a in range(L_s - 1):
+            if sco[l, selo[l, a]] - sco[l, selo[l, a + 1]] > 4 * TOL_R2:
+                assert selg[l, a] == selo[l, a]
+    assert np.abs(scg - sco).max() <= TOL_R2
+    # a plan with repeated targets fits probes but cannot apply them
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_INVALID_ARGUMENT"):
+        cb.cb_apply(plan, maps, src, torch.zeros_like(tgt))
+    plan.close()
+
+
+def test_probe_qwen_shape_all_layer_pairs_sampled_maps(cb):
+    # the selector's real size: 64 target layers x 40 source layers x 8 heads x
+    # K/V = 40,960 probes over a 2 x 1024-token calibration slice
+    wl = synth.WORKLOADS["qwen50"].with_(n_seqs=2, seq_len=1024)
+    say(f"probe: generating {wl.n_seqs} x {wl.seq_len} tokens")
+    src, tgt, w = make_inputs(wl)
+    hm = probe_head_map(wl.L_t, wl.L_s, wl.H_t)
+    n = len(hm["kv"])
+    plan = cb.cb_plan_create(hm, src, tgt, wl.n_seqs * wl.seq_len)
+    say(f"probe: GPU fit of {n} probes")
+    sums, sq, A, B, maps, info, r2 = gpu_probe(cb, plan, src, tgt, w, lam=1e-2, flags=cb.CB_LAMBDA_RELATIVE)
+    assert (info.cpu().numpy() == 0).all()
+    sel = sample_maps(n, 8, seed=2)
+    say(f"probe: oracle on probes {sel}")
+    chm, xb, ss, yb, ts, ws, Bn, T = compact(hm, sel, src, tgt, w)
+    so, Ao, Bo = oracle.stats_centered(chm, xb, ss, wl.d_s, yb, ts, wl.d_t, ws, Bn * T, Bn, T, n_threads=NTHREADS)
+    Wo, _ = oracle.ridge_solve_centered(so, Ao, Bo, 1e-2, relative=True, n_threads=NTHREADS)
+    r2o = oracle.probe_r2(chm, Wo, xb, ss, wl.d_s, yb, ts, wl.d_t, ws, Bn * T, Bn, T, n_threads=NTHREADS)
+    g = r2.cpu().numpy()[sel]
+    e = float(np.abs(g - r2o).max())
+    say(f"  probe R^2 max |diff| {e:.3e} (values {np.round(g, 4).tolist()})")
+    assert e <= TOL_R2
+    # the planted source layer of every target layer ranks first
+    selg, _ = cb.cb_select_layers(hm, r2.cpu().numpy(), wl.L_t, wl.L_s, 8)
+    planted = [synth._round_ratio(l, wl.L_s - 1, wl.L_t - 1) for l in range(wl.L_t)]
+    assert selg[:, 0].tolist() == planted
+    del src, tgt, w
+    plan.close()
