@@ -22,6 +22,10 @@ Transfer"):
   residuals (Sec. 3.1, layer selection).
 * :func:`select_layers` -- mean probe R^2 per (target, source) layer pair over
   KV heads and K/V, ranked; the first k source layers form S_l (Sec. 3.1).
+* :func:`attn_sensitivity` -- raw attention-aligned sensitivities r^K, r^V at
+  causal prefix boundaries (Sec. 3.3, Eq. attentionlinearization, Eq. sensitivity).
+* :func:`attn_weights` -- mean-one normalization and the ESS-floor shrinkage
+  w = 1 + alpha* (r - 1) (Sec. 3.3).
 * :func:`coefficient_count` -- C(f) = 2 L_t H_t (k f d_s) d_t (Sec. 2.3, Eq. support-cost).
 
 Parity status: pinned by ``tests/test_oracle_pins.py``.
@@ -82,6 +86,11 @@ def _load():
     lib.oracle_probe_r2.argtypes = [ctypes.c_int] + [_i32p] * 6 + [
         _f64p, _u16p, _i64p, ctypes.c_int, _u16p, _i64p, ctypes.c_int,
         _f32p, ctypes.c_int64, ctypes.c_int, ctypes.c_int, _f64p, ctypes.c_int]
+    lib.oracle_attn_sensitivity.restype = ctypes.c_int
+    lib.oracle_attn_sensitivity.argtypes = [ctypes.c_int] * 6 + [_u16p, _i64p, _u16p, _i64p, _i32p, ctypes.c_int,
+                                                                 ctypes.c_int, _f64p, ctypes.c_int]
+    lib.oracle_attn_weights.restype = ctypes.c_int
+    lib.oracle_attn_weights.argtypes = [ctypes.c_int] * 4 + [_f64p, ctypes.c_int, _f64p, _f64p]
     lib.oracle_double_to_bf16_array.restype = ctypes.c_int
     lib.oracle_double_to_bf16_array.argtypes = [ctypes.c_int64, _f64p, _u16p]
     _lib = lib
@@ -276,6 +285,44 @@ def select_layers(head_map, r2, n_tgt_layers: int, n_src_layers: int, k: int):
         chosen = [j for j in order if np.isfinite(score[l, j])][:k]
         selected[l, :len(chosen)] = chosen
     return selected, score
+
+
+def attn_sensitivity(kv_cache, kv_strides, n_layers: int, n_heads: int, d: int, n_seqs: int, seq_len: int,
+                     q, q_strides, n_qheads: int, boundaries, sample_stride: int = 1, n_threads: int = 0):
+    """Raw sensitivities r [n_layers][2][n_heads][n_seqs*seq_len] (component 0 = K, 1 = V).
+
+    ``kv_cache``: uint16 bf16 bits of a target cache addressed with ``kv_strides``
+    (layer, kv, seq, head, tok); ``q``: uint16 bf16 bits of the boundary queries,
+    element (layer, seq, boundary, query head, j) at the dot product with
+    ``q_strides`` (4 strides).  ``boundaries``: increasing query positions."""
+    lib = _load()
+    kvc = np.ascontiguousarray(_u16(kv_cache))
+    qa = np.ascontiguousarray(_u16(q))
+    ks = _strides5(kv_strides)
+    qs = np.ascontiguousarray(np.asarray(q_strides, dtype=np.int64))
+    assert qs.shape == (4,)
+    bd = np.ascontiguousarray(np.asarray(boundaries, dtype=np.int32))
+    assert n_qheads % n_heads == 0 and (np.diff(bd) > 0).all() and bd[0] >= 0 and bd[-1] < seq_len
+    r = np.zeros((n_layers, 2, n_heads, n_seqs * seq_len), dtype=np.float64)
+    lib.oracle_attn_sensitivity(n_layers, n_heads, n_qheads, d, n_seqs, seq_len, _ptr(kvc, _u16p), _ptr(ks, _i64p),
+                                _ptr(qa, _u16p), _ptr(qs, _i64p), _ptr(bd, _i32p), int(bd.shape[0]),
+                                int(sample_stride), _ptr(r, _f64p), int(n_threads))
+    return r
+
+
+def attn_weights(r, n_seqs: int, seq_len: int, sample_stride: int, p: int):
+    """ESS-floor shrinkage per row of r [..., n_seqs*seq_len]: returns (w, alpha) with
+    w = 1 + alpha (r/mean - 1) on calibration rows (t mod sample_stride = 0), 0 elsewhere."""
+    lib = _load()
+    r = np.ascontiguousarray(np.asarray(r, dtype=np.float64))
+    shape = r.shape
+    rows = int(np.prod(shape[:-1]))
+    assert shape[-1] == n_seqs * seq_len
+    w = np.zeros(shape, dtype=np.float64)
+    alpha = np.zeros(shape[:-1], dtype=np.float64)
+    lib.oracle_attn_weights(rows, n_seqs, seq_len, sample_stride, _ptr(r, _f64p), int(p), _ptr(w, _f64p),
+                            _ptr(alpha, _f64p))
+    return w, alpha
 
 
 def double_to_bf16(v) -> np.ndarray:

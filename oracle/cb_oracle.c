@@ -438,6 +438,159 @@ int oracle_probe_r2(int n_maps,
 }
 
 /*
+ * Attention-aligned sensitivities (Sec. 3.3, Eq. attentionlinearization and
+ * Eq. sensitivity), raw and before the global normalization.
+ * For every target layer l, KV head h and sequence b, every boundary
+ * c = boundaries[k] (the position of the first query after the prefix
+ * [0, c)) and every query head u of h's group (u = h*G .. h*G + G-1,
+ * G = n_qheads / n_heads):
+ *   s_i = q_u . k_i / sqrt(d),  a_i = softmax over keys i = 0 .. c (causal,
+ *   the query's own position included),  o_u = sum_i a_i v_i,
+ * and for the eligible prefix positions E_c = {i < c : i mod sample_stride = 0}:
+ *   p^V_i += a_i^2,   p^K_i += a_i^2 |v_i - o_u|^2 |q_u|^2 / d   (summed over u).
+ * Each boundary's p^V and p^K are scaled to unit mass over E_c (skipped when
+ * the mass is zero) and added into r:
+ *   r [n_layers][2][n_heads][n_seqs * seq_len] (fp64, overwritten), component
+ *   0 = K (from p^K), 1 = V (from p^V); the row of (l, z, h) is (l*2 + z)*H + h.
+ * K, V: bf16 bits of the target cache, kv 0 and 1 of the strides
+ * {layer, kv, seq, head, tok}.  q: bf16 bits, element (l, b, k, u, j) at
+ * l*q_strides[0] + b*q_strides[1] + k*q_strides[2] + u*q_strides[3] + j.
+ * Returns 0.
+ */
+int oracle_attn_sensitivity(int n_layers, int n_heads, int n_qheads, int d, int n_seqs, int seq_len,
+                            const uint16_t *kvc, const int64_t *kv_strides, const uint16_t *q,
+                            const int64_t *q_strides, const int32_t *boundaries, int n_bounds,
+                            int sample_stride, double *r, int n_threads) {
+    const int G = n_qheads / n_heads;
+    const int64_t N = (int64_t)n_seqs * seq_len;
+    set_threads(n_threads);
+#pragma omp parallel for collapse(2) schedule(dynamic, 1)
+    for (int l = 0; l < n_layers; ++l) {
+        for (int h = 0; h < n_heads; ++h) {
+            double *rK = r + ((int64_t)(l * 2 + 0) * n_heads + h) * N;
+            double *rV = r + ((int64_t)(l * 2 + 1) * n_heads + h) * N;
+            memset(rK, 0, sizeof(double) * (size_t)N);
+            memset(rV, 0, sizeof(double) * (size_t)N);
+            double *a = (double *)malloc(sizeof(double) * (size_t)seq_len);
+            double *pK = (double *)malloc(sizeof(double) * (size_t)seq_len);
+            double *pV = (double *)malloc(sizeof(double) * (size_t)seq_len);
+            double *qv = (double *)malloc(sizeof(double) * (size_t)d);
+            double *o = (double *)malloc(sizeof(double) * (size_t)d);
+            for (int b = 0; b < n_seqs; ++b) {
+                for (int k = 0; k < n_bounds; ++k) {
+                    const int c = boundaries[k];
+                    for (int i = 0; i < seq_len; ++i) pK[i] = pV[i] = 0.0;
+                    for (int u = h * G; u < (h + 1) * G; ++u) {
+                        const uint16_t *qr = q + (int64_t)l * q_strides[0] + (int64_t)b * q_strides[1] +
+                                             (int64_t)k * q_strides[2] + (int64_t)u * q_strides[3];
+                        double qq = 0.0;
+                        for (int j = 0; j < d; ++j) {
+                            qv[j] = bf16_bits_to_double(qr[j]);
+                            qq += qv[j] * qv[j];
+                        }
+                        double mx = -HUGE_VAL;
+                        for (int i = 0; i <= c; ++i) {
+                            const uint16_t *kr = kvc + row_offset(kv_strides, l, 0, b, h, i);
+                            double sc = 0.0;
+                            for (int j = 0; j < d; ++j) sc += qv[j] * bf16_bits_to_double(kr[j]);
+                            a[i] = sc / sqrt((double)d);
+                            if (a[i] > mx) mx = a[i];
+                        }
+                        double z = 0.0;
+                        for (int i = 0; i <= c; ++i) {
+                            a[i] = exp(a[i] - mx);
+                            z += a[i];
+                        }
+                        for (int j = 0; j < d; ++j) o[j] = 0.0;
+                        for (int i = 0; i <= c; ++i) {
+                            a[i] /= z;
+                            const uint16_t *vr = kvc + row_offset(kv_strides, l, 1, b, h, i);
+                            for (int j = 0; j < d; ++j) o[j] += a[i] * bf16_bits_to_double(vr[j]);
+                        }
+                        for (int i = 0; i < c; i += sample_stride) {
+                            const uint16_t *vr = kvc + row_offset(kv_strides, l, 1, b, h, i);
+                            double dv = 0.0;
+                            for (int j = 0; j < d; ++j) {
+                                const double e = bf16_bits_to_double(vr[j]) - o[j];
+                                dv += e * e;
+                            }
+                            pV[i] += a[i] * a[i];
+                            pK[i] += a[i] * a[i] * dv * qq / (double)d;
+                        }
+                    }
+                    double mK = 0.0, mV = 0.0;
+                    for (int i = 0; i < c; i += sample_stride) {
+                        mK += pK[i];
+                        mV += pV[i];
+                    }
+                    for (int i = 0; i < c; i += sample_stride) {
+                        if (mK > 0.0) rK[(int64_t)b * seq_len + i] += pK[i] / mK;
+                        if (mV > 0.0) rV[(int64_t)b * seq_len + i] += pV[i] / mV;
+                    }
+                }
+            }
+            free(a);
+            free(pK);
+            free(pV);
+            free(qv);
+            free(o);
+        }
+    }
+    return 0;
+}
+
+/*
+ * Shrinkage of the raw sensitivities toward uniform weights (Sec. 3.3), per
+ * row of r [n_rows][n_seqs * seq_len]: over the n calibration rows (positions
+ * t with t mod sample_stride = 0 of every sequence),
+ *   r_i <- r_i / mean(r)                       (mean one; all ones if the mean is 0)
+ *   CV^2 = mean((r_i - 1)^2),  tau = min(n, 2 p),
+ *   alpha = 1 if CV^2 = 0, else min(1, sqrt((n / tau - 1) / CV^2)),
+ *   w_i = 1 + alpha (r_i - 1),
+ * the largest alpha whose Kish effective sample size n / (1 + alpha^2 CV^2)
+ * is at least tau.  Positions that are not calibration rows get w = 0.
+ * Outputs w (same shape as r) and alpha [n_rows], fp64.  Returns 0.
+ */
+int oracle_attn_weights(int n_rows, int n_seqs, int seq_len, int sample_stride, const double *r, int p,
+                        double *w, double *alpha) {
+    const int64_t N = (int64_t)n_seqs * seq_len;
+    for (int row = 0; row < n_rows; ++row) {
+        const double *rr = r + (int64_t)row * N;
+        double *ww = w + (int64_t)row * N;
+        double sum = 0.0;
+        int64_t n = 0;
+        for (int b = 0; b < n_seqs; ++b)
+            for (int t = 0; t < seq_len; t += sample_stride) {
+                sum += rr[(int64_t)b * seq_len + t];
+                ++n;
+            }
+        const double mean = n > 0 ? sum / (double)n : 0.0;
+        double cv2 = 0.0;
+        for (int b = 0; b < n_seqs; ++b)
+            for (int t = 0; t < seq_len; t += sample_stride) {
+                const double x = mean > 0.0 ? rr[(int64_t)b * seq_len + t] / mean : 1.0;
+                cv2 += (x - 1.0) * (x - 1.0);
+            }
+        cv2 = n > 0 ? cv2 / (double)n : 0.0;
+        const double tau = (double)(n < 2 * (int64_t)p ? n : 2 * (int64_t)p);
+        double al = 1.0;
+        if (cv2 > 0.0) {
+            al = sqrt(((double)n / tau - 1.0) / cv2);
+            if (al > 1.0) al = 1.0;
+        }
+        alpha[row] = al;
+        for (int64_t i = 0; i < N; ++i) ww[i] = 0.0;
+        for (int b = 0; b < n_seqs; ++b)
+            for (int t = 0; t < seq_len; t += sample_stride) {
+                const int64_t i = (int64_t)b * seq_len + t;
+                const double x = mean > 0.0 ? rr[i] / mean : 1.0;
+                ww[i] = 1.0 + al * (x - 1.0);
+            }
+    }
+    return 0;
+}
+
+/*
  * Online application of the fitted maps.
  *   W [n_maps][P][d_t] (fp64 copies of the coefficients; row d_s is the bias)
  *   out[tgt_layer, kv, seq, tgt_head, tok, j] = RNE_bf16( sum_k x~_k W[k][j] )

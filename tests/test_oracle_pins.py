@@ -708,3 +708,102 @@ def test_select_layers_recovers_the_planted_source_layer():
     assert sel[:, 0].tolist() == planted
     for l in range(L_t):
         assert score[l, planted[l]] > 0.8 and np.sort(score[l])[-2] < 0.3
+
+
+# ----------------------------------------------------------------------------- attention-aligned weights
+
+def _attn_problem(rng, L=1, H=2, Hq=4, d=8, B=2, T=14, equal_keys=False):
+    kv = rng.standard_normal((L, 2, B, H, T, d))
+    if equal_keys:
+        kv[:, 0] = kv[:, 0, :, :, :1]
+    q = rng.standard_normal((L, B, 3, Hq, d)) * 1.5
+    kvb, qb = to_bf16_bits(kv), to_bf16_bits(q)
+    return kvb, synth.cache_strides(L, H, B, T, d), qb, (B * 3 * Hq * d, 3 * Hq * d, Hq * d, d)
+
+
+def test_attn_sensitivity_equals_autograd_jacobian_norms():
+    # Sec. 3.3: r^V_i and r^K_i are the squared Frobenius norms of the Jacobians
+    # of the attention output with respect to v_i (up to the factor d) and k_i
+    rng = np.random.default_rng(41)
+    L, H, Hq, d, B, T = 1, 2, 4, 8, 2, 14
+    bounds, stride = [3, 8, 13], 2
+    kvb, ks, qb, qs = _attn_problem(rng, L, H, Hq, d, B, T)
+    r = oracle.attn_sensitivity(kvb, ks, L, H, d, B, T, qb, qs, Hq, bounds, stride)
+    kv = torch.as_tensor(bf16_val(kvb).reshape(L, 2, B, H, T, d))
+    qv = torch.as_tensor(bf16_val(qb).reshape(L, B, 3, Hq, d))
+    G = Hq // H
+    ref = np.zeros_like(r)
+    for b in range(B):
+        for h in range(H):
+            for k, c in enumerate(bounds):
+                pV, pK = np.zeros(T), np.zeros(T)
+                for u in range(h * G, (h + 1) * G):
+                    qu = qv[0, b, k, u]
+
+                    def out(K, V):
+                        a = torch.softmax(K[:c + 1] @ qu / np.sqrt(d), dim=0)
+                        return a @ V[:c + 1]
+                    JK, JV = torch.autograd.functional.jacobian(out, (kv[0, 0, b, h], kv[0, 1, b, h]))
+                    # JK, JV: [d_out][T][d]
+                    pK += (JK ** 2).sum(dim=(0, 2)).numpy()
+                    pV += (JV ** 2).sum(dim=(0, 2)).numpy() / d
+                elig = [i for i in range(c) if i % stride == 0]
+                for z, pz in ((0, pK), (1, pV)):
+                    ref[0, z, h, b * T + np.array(elig)] += pz[elig] / pz[elig].sum()
+    np.testing.assert_allclose(r, ref, rtol=1e-10, atol=1e-13)
+    # positions outside every prefix, and non-sampled positions, get nothing
+    assert not r[..., 13::T].any() and not r[..., 1::2].any()
+
+
+def test_attn_sensitivity_equal_keys_is_uniform_over_each_prefix():
+    rng = np.random.default_rng(42)
+    L, H, Hq, d, B, T = 1, 2, 4, 8, 2, 14
+    bounds, stride = [2, 5, 13], 3
+    kvb, ks, qb, qs = _attn_problem(rng, L, H, Hq, d, B, T, equal_keys=True)
+    r = oracle.attn_sensitivity(kvb, ks, L, H, d, B, T, qb, qs, Hq, bounds, stride)
+    ref = np.zeros(T)
+    for c in bounds:
+        elig = [i for i in range(c) if i % stride == 0]
+        ref[elig] += 1.0 / len(elig)
+    np.testing.assert_allclose(r[0, 1, :, :T], np.broadcast_to(ref, (H, T)), rtol=1e-12)   # r^V
+    # each boundary contributes unit mass
+    np.testing.assert_allclose(r.reshape(L, 2, H, B, T).sum(axis=-1), len(bounds), rtol=1e-12)
+
+
+def test_attn_weights_reach_the_printed_ess_floors():
+    # Sec. 4.1: n = 128,000 calibration rows (500 x 1,024 tokens, every fourth),
+    # tau = min(n, 2 p_l) gives floors 5,120 / 3,072 / 2,048 for p_l = 2,560 / 1,536 / 1,024
+    g = json.load(open(GOLDEN))
+    ar, widths = g["attn_repair"], g["input_widths"]["local"]
+    B, T, s = ar["n_seqs"], ar["seq_len"], ar["sample_stride"]
+    rng = np.random.default_rng(43)
+    r = np.exp(2.5 * rng.standard_normal((len(widths), B * T)))         # concentrated raw weights
+    for row, (p, floor) in enumerate(zip(widths, ar["floors"])):
+        w, alpha = oracle.attn_weights(r[row:row + 1], B, T, s, p)
+        cal = w[0].reshape(B, T)[:, ::s].ravel()
+        assert cal.size == ar["n"]
+        assert 0.0 < alpha[0] < 1.0
+        n_eff = cal.sum() ** 2 / (cal ** 2).sum()
+        assert n_eff == pytest.approx(floor, rel=1e-9)
+        assert cal.mean() == pytest.approx(1.0, rel=1e-12)
+        assert not w[0].reshape(B, T)[:, 1::s].any()                    # not calibration rows
+
+
+def test_attn_weights_kish_closed_form_and_degenerate_rows():
+    rng = np.random.default_rng(44)
+    B, T, s, p = 3, 40, 1, 8                                            # n = 120, tau = 16
+    r = np.stack([np.exp(0.3 * rng.standard_normal(B * T)),           # mild: alpha = 1
+                  np.exp(3.0 * rng.standard_normal(B * T)),           # concentrated: alpha < 1
+                  np.full(B * T, 2.5),                                # constant: CV^2 = 0
+                  np.zeros(B * T)])                                   # no mass: uniform
+    w, alpha = oracle.attn_weights(r, B, T, s, p)
+    n = B * T
+    for row in range(2):
+        x = r[row] / r[row].mean()
+        cv2 = ((x - 1) ** 2).mean()
+        n_eff = w[row].sum() ** 2 / (w[row] ** 2).sum()
+        assert n_eff == pytest.approx(n / (1 + alpha[row] ** 2 * cv2), rel=1e-12)
+    assert alpha[0] == 1.0 and n / (1 + ((r[0] / r[0].mean() - 1) ** 2).mean()) >= 16
+    assert alpha[1] < 1.0 and (w[1].sum() ** 2 / (w[1] ** 2).sum()) == pytest.approx(16, rel=1e-12)
+    assert alpha[2] == 1.0 and np.allclose(w[2], 1.0)
+    assert alpha[3] == 1.0 and np.allclose(w[3], 1.0)
