@@ -212,6 +212,51 @@ def probe_leg(cb, wl, src, tgt, w, n_seqs, steps):
     }
 
 
+def attn_leg(cb, synth, bw, tgt, steps):
+    """Attention-aligned calibration weights (Sec. 3.3) for the resident batch:
+    64 target layers x 8 KV heads x 8 query heads each, 32 log-spaced boundaries
+    from 12 to 2,047, every token a calibration row; the sensitivity pass over
+    all (sequence, layer, KV head) units, then the ESS-floor shrinkage of the
+    1,024 rows.  Timed with events after one warm-up pass."""
+    import torch
+    L, _, B, H, T, d = tgt.shape
+    G = 8
+    bounds = synth.attn_boundaries(T)
+    q = synth.gen_queries(bw, tgt, G * H, len(bounds), device="cuda")
+    r = torch.empty((2 * L * H, B * T), dtype=torch.float32, device="cuda")
+    wts = torch.empty_like(r)
+    alpha = torch.empty((2 * L * H,), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    recs = []
+    for it in range(steps + 1):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        e[0].record(stream)
+        cb.cb_attn_sensitivity(tgt, q, bounds, 1, r)
+        e[1].record(stream)
+        cb.cb_attn_weights(r, B, T, 1, bw.d_s, wts, alpha)
+        e[2].record(stream)
+        if it > 0:
+            recs.append(e)
+    torch.cuda.synchronize()
+    mean = lambda v: sum(v) / len(v)  # noqa: E731
+    sens_ms = mean([e[0].elapsed_time(e[1]) for e in recs])
+    fin_ms = mean([e[1].elapsed_time(e[2]) for e in recs])
+    units = B * L * H
+    # algorithmic work: every (query, key <= boundary) pair needs q.k, a v and v.o (2 d flops each);
+    # every unit reads its K and V rows up to the last boundary once, its queries, and writes 2 rows of r
+    pairs = units * G * sum(int(c) + 1 for c in bounds)
+    flops = pairs * 3 * 2 * d
+    bytes_ = units * (2 * (int(bounds[-1]) + 1) * d * 2 + len(bounds) * G * d * 2 + 2 * T * 4)
+    a = alpha.double()
+    return {
+        "units": units, "query_rows_per_unit": G * len(bounds), "calib_tokens": B * T,
+        "legs_ms": {"sensitivity": sens_ms, "shrinkage": fin_ms},
+        "sensitivity_algorithmic_TFLOPs": flops / (sens_ms / 1e3) / 1e12,
+        "sensitivity_algorithmic_GBps": bytes_ / (sens_ms / 1e3) / 1e9,
+        "alpha_min_mean_max": [float(a.min()), float(a.mean()), float(a.max())],
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -224,6 +269,8 @@ def main():
     ap.add_argument("--probe-steps", type=int, default=2,
                     help="timed layer-selection probe runs over all layer pairs (0: skip)")
     ap.add_argument("--probe-seqs", type=int, default=10, help="calibration sequences of the probe leg")
+    ap.add_argument("--attn-steps", type=int, default=2,
+                    help="timed attention-aligned weight passes over the resident batch (0: skip)")
     ap.add_argument("--hbm-copy-probe", type=float, default=None, metavar="GIB",
                     help="only time a plain copy of GIB GiB (counter calibration)")
     args = ap.parse_args()
@@ -366,9 +413,12 @@ def main():
     }
     if args.centered_steps > 0:
         res["centered"] = centered_leg(cb, plan, wl, src, tgt, w, n_calls, maps, bytes_per_call, args.centered_steps)
-    if args.probe_steps > 0:
+    if args.probe_steps > 0 or args.attn_steps > 0:
         del G, C
+    if args.probe_steps > 0:
         res["probes"] = probe_leg(cb, wl, src, tgt, w, min(args.probe_seqs, B), args.probe_steps)
+    if args.attn_steps > 0:
+        res["attn_weights"] = attn_leg(cb, synth, bw, tgt, args.attn_steps)
     if not args.no_cpu_baseline:
         n_threads = int(os.environ.get("OMP_NUM_THREADS", str(os.cpu_count() or 1)))
         log(f"cpu baseline on {n_threads} threads")

@@ -24,6 +24,10 @@
  *
  *   cb_probe_r2, cb_select_layers
  *
+ * and the attention-aligned calibration weights of Sec. 3.3:
+ *
+ *   cb_attn_sensitivity, cb_attn_weights
+ *
  * Conventions shared by every call
  * --------------------------------
  * - Row vectors: a map is W~ = [W ; b^T], a P x d_t fp32 matrix with
@@ -102,6 +106,23 @@ typedef struct {
     const int32_t *src_head;
     const int32_t *weight_row;
 } cb_head_map;
+
+/*
+ * Queries of the target model at the calibration boundaries (Sec. 3.3): the
+ * query of head u at boundary k of sequence seq in layer l, element j at
+ *   data[l*s_layer + seq*s_seq + k*s_bnd + u*s_head + j]   (bfloat16, j stride 1).
+ * Query head u belongs to KV head u / (n_qheads / n_heads) of the target cache.
+ * data and every stride must keep each row 16-byte aligned.
+ */
+typedef struct {
+    const void *data;
+    int32_t n_layers;
+    int32_t n_qheads;
+    int32_t head_dim;
+    int32_t n_seqs;
+    int32_t n_bounds;
+    int64_t s_layer, s_seq, s_bnd, s_head;
+} cb_queries;
 
 /* Validated head map, static gather schedule and workspace (opaque). */
 typedef struct cb_plan cb_plan;
@@ -268,6 +289,51 @@ cb_status cb_probe_r2(int32_t n_maps, int32_t d_s, int32_t d_t, const double *su
  */
 cb_status cb_select_layers(const cb_head_map *map, const double *r2, int32_t n_tgt_layers, int32_t n_src_layers,
                            int32_t k, int32_t *selected, double *score);
+
+/*
+ * Attention-aligned sensitivities (Sec. 3.3, Eq. attentionlinearization and
+ * Eq. sensitivity).  For every sequence, target layer l and KV head h of `tgt`
+ * (K = kv 0, V = kv 1), every boundary c = boundaries[k] (the position of the
+ * first query after the prefix [0, c)) and every query head u of h's group:
+ *   a_i = softmax_i(q_u . k_i / sqrt(d)) over the keys i = 0 .. c,  o_u = sum_i a_i v_i,
+ * and for the sampled prefix positions E_c = {i < c : i mod sample_stride = 0}
+ *   p^V_i = sum_u a_i^2,   p^K_i = sum_u a_i^2 |v_i - o_u|^2 |q_u|^2 / d;
+ * every boundary's p^K and p^V are scaled to unit mass over E_c (a boundary
+ * with zero mass adds nothing) and the boundaries are summed:
+ *   r[((l*2 + z)*H + h) * r_row_stride + seq*seq_len + tok] = r^K (z = 0) or r^V (z = 1),
+ * written for every token of the call (0 outside every E_c) -- the row order
+ * of the maps of a plan built on all target heads, so weight_row = map index.
+ * Sequences are independent: a batch of sequences is one call with r offset
+ * to its first column.  tgt: the target cache (head_dim d in {64, 128}); q:
+ * n_layers and n_seqs equal to tgt's, n_qheads = G * n_heads with G a power of
+ * two <= 32, 1 <= n_bounds <= 64 and n_bounds * G <= 256; boundaries: host
+ * array of n_bounds strictly increasing positions in [0, seq_len).  r: device
+ * fp32, r_row_stride >= n_seqs * seq_len.  Scores and outputs are fp32 sums of
+ * exact bf16 products; a and o enter the products as two bf16 terms each.
+ * Errors: CB_ERR_INVALID_ARGUMENT, CB_ERR_SHAPE, CB_ERR_MISALIGNED,
+ * CB_ERR_UNSUPPORTED, CB_ERR_DEVICE.
+ */
+cb_status cb_attn_sensitivity(const cb_cache *tgt, const cb_queries *q, const int32_t *boundaries,
+                              int32_t sample_stride, float *r, int64_t r_row_stride, void *stream);
+
+/*
+ * Attention-aligned weights (Sec. 3.3): for each of n_rows rows of r (as
+ * written by cb_attn_sensitivity over all calibration batches), over the n
+ * calibration rows (positions tok with tok mod sample_stride = 0 of all
+ * n_seqs sequences):
+ *   r_i <- r_i / mean(r)   (all ones if the mean is zero),
+ *   CV^2 = mean((r_i - 1)^2),  tau = min(n, 2 p),
+ *   alpha = 1 if CV^2 = 0, else min(1, sqrt((n / tau - 1) / CV^2)),
+ *   w_i = 1 + alpha (r_i - 1),
+ * the largest alpha whose Kish effective sample size n / (1 + alpha^2 CV^2) is
+ * at least tau; positions that are not calibration rows get w = 0, so the
+ * statistics calls see only the sampled tokens.  p: the map's input width
+ * (k d_s).  r, w: device fp32 with row strides >= n_seqs * seq_len; alpha:
+ * device fp32 [n_rows].  Sums in fp64, one workgroup per row.
+ */
+cb_status cb_attn_weights(int32_t n_rows, int32_t n_seqs, int32_t seq_len, int32_t sample_stride, const float *r,
+                          int64_t r_row_stride, int32_t p, float *w, int64_t w_row_stride, float *alpha,
+                          void *stream);
 
 /*
  * Online mapping (Sec. 1 pipeline; Sec. 2.3 Eq. support-cost): for every map

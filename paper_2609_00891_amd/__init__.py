@@ -16,6 +16,9 @@ current HIP stream.  The functions keep the C names:
   W = (A + lambda I)^-1 B, b = mu_y - W^T mu_x (Sec. 3.1)
 * :func:`cb_probe_r2`, :func:`cb_select_layers` -- layer-selection probes: held-in
   R^2 per probe map and the top-k source layers per target layer (Sec. 3.1)
+* :func:`cb_attn_sensitivity`, :func:`cb_attn_weights` -- attention-aligned
+  calibration weights: raw sensitivities at causal prefix boundaries and the
+  ESS-floor shrinkage (Sec. 3.3)
 
 Caches are bfloat16 tensors indexed ``[layer][kv][seq][head][tok][dim]`` (any
 strides with a unit channel stride).  Importing this package fails if the
@@ -49,6 +52,13 @@ class CbCache(ctypes.Structure):
 
 
 _i32p = ctypes.POINTER(ctypes.c_int32)
+
+
+class CbQueries(ctypes.Structure):
+    _fields_ = [("data", ctypes.c_void_p), ("n_layers", ctypes.c_int32), ("n_qheads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("n_seqs", ctypes.c_int32), ("n_bounds", ctypes.c_int32),
+                ("s_layer", ctypes.c_int64), ("s_seq", ctypes.c_int64), ("s_bnd", ctypes.c_int64),
+                ("s_head", ctypes.c_int64)]
 
 
 class CbHeadMap(ctypes.Structure):
@@ -97,6 +107,12 @@ _lib.cb_stats_accumulate_centered.argtypes = [_vp, ctypes.POINTER(CbCache), ctyp
 _lib.cb_ridge_solve_centered.restype = ctypes.c_int
 _lib.cb_ridge_solve_centered.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp, _vp, _vp,
                                          ctypes.c_float, ctypes.c_uint32, _vp, _vp, _vp]
+_lib.cb_attn_sensitivity.restype = ctypes.c_int
+_lib.cb_attn_sensitivity.argtypes = [ctypes.POINTER(CbCache), ctypes.POINTER(CbQueries), _vp, ctypes.c_int32, _vp,
+                                     ctypes.c_int64, _vp]
+_lib.cb_attn_weights.restype = ctypes.c_int
+_lib.cb_attn_weights.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp, ctypes.c_int64,
+                                 ctypes.c_int32, _vp, ctypes.c_int64, _vp, _vp]
 _lib.cb_apply.restype = ctypes.c_int
 _lib.cb_apply.argtypes = [_vp, _vp, ctypes.POINTER(CbCache), ctypes.POINTER(CbCache), _vp]
 _lib.cb_status_string.restype = ctypes.c_char_p
@@ -316,6 +332,43 @@ def cb_select_layers(head_map: Mapping[str, object], r2, n_tgt_layers: int, n_sr
     _check(_lib.cb_select_layers(ctypes.byref(hm), r.ctypes.data, n_tgt_layers, n_src_layers, k,
                                  selected.ctypes.data, score.ctypes.data))
     return selected, score
+
+
+def queries_view(q: torch.Tensor) -> CbQueries:
+    """Describe a [layer][seq][boundary][query head][dim] bfloat16 tensor (unit dim stride)."""
+    if q.dtype != torch.bfloat16 or q.dim() != 5 or (q.shape[4] > 1 and q.stride(4) != 1):
+        raise ValueError("queries are bfloat16 [layer][seq][boundary][query head][dim] with unit dim stride")
+    v = CbQueries()
+    v.data = q.data_ptr()
+    v.n_layers, v.n_seqs, v.n_bounds, v.n_qheads, v.head_dim = q.shape
+    v.s_layer, v.s_seq, v.s_bnd, v.s_head = q.stride(0), q.stride(1), q.stride(2), q.stride(3)
+    return v
+
+
+def cb_attn_sensitivity(tgt: torch.Tensor, q: torch.Tensor, boundaries, sample_stride: int, r: torch.Tensor,
+                        r_row_stride: Optional[int] = None, stream=None):
+    """Raw sensitivities into r [(l*2 + z)*H + h][seq*seq_len + tok] (float32; z = 0 K, 1 V)."""
+    import numpy as np  # noqa: PLC0415
+
+    if r.dtype != torch.float32:
+        raise ValueError("r is float32")
+    b = np.ascontiguousarray(np.asarray(boundaries, dtype=np.int32))
+    tv, qv = cache_view(tgt), queries_view(q)
+    rs = r.stride(0) if r_row_stride is None else int(r_row_stride)
+    _check(_lib.cb_attn_sensitivity(ctypes.byref(tv), ctypes.byref(qv), b.ctypes.data, int(sample_stride), _ptr(r),
+                                    rs, _stream(stream)))
+
+
+def cb_attn_weights(r: torch.Tensor, n_seqs: int, seq_len: int, sample_stride: int, p: int, w: torch.Tensor,
+                    alpha: torch.Tensor, stream=None):
+    """w = 1 + alpha (r/mean - 1) on calibration rows, 0 elsewhere; alpha per row (float32)."""
+    if r.dtype != torch.float32 or w.dtype != torch.float32 or alpha.dtype != torch.float32:
+        raise ValueError("r, w and alpha are float32")
+    n_rows = r.shape[0]
+    if w.shape[0] != n_rows or alpha.shape != (n_rows,):
+        raise ValueError("r, w [rows][...], alpha [rows]")
+    _check(_lib.cb_attn_weights(n_rows, int(n_seqs), int(seq_len), int(sample_stride), _ptr(r), r.stride(0), int(p),
+                                _ptr(w), w.stride(0), _ptr(alpha), _stream(stream)))
 
 
 def cb_apply(plan: Plan, maps: torch.Tensor, src: torch.Tensor, tgt_out: torch.Tensor, stream=None):

@@ -550,6 +550,77 @@ cb_status cb_select_layers(const cb_head_map *map, const double *r2, int32_t n_t
     return ok();
 }
 
+cb_status cb_attn_sensitivity(const cb_cache *tgt, const cb_queries *q, const int32_t *boundaries,
+                              int32_t sample_stride, float *r, int64_t r_row_stride, void *stream) {
+    if (!tgt || !q || !boundaries || !r) return fail(CB_ERR_INVALID_ARGUMENT, "tgt, q, boundaries and r must be non-NULL");
+    const int d = tgt->head_dim;
+    if (d != 64 && d != 128) return fail(CB_ERR_UNSUPPORTED, "head_dim must be 64 or 128 (got %d)", d);
+    if (tgt->n_layers <= 0 || tgt->n_heads <= 0) return fail(CB_ERR_SHAPE, "tgt needs positive layer and head counts");
+    if (cb_status s = check_cache("tgt", tgt, tgt->n_layers, tgt->n_heads, d)) return s;
+    if (q->n_layers != tgt->n_layers || q->n_seqs != tgt->n_seqs || q->head_dim != d)
+        return fail(CB_ERR_SHAPE, "q is %d layers x %d seqs x %d, tgt %d x %d x %d", q->n_layers, q->n_seqs, q->head_dim,
+                    tgt->n_layers, tgt->n_seqs, d);
+    if (q->n_qheads <= 0 || q->n_qheads % tgt->n_heads != 0)
+        return fail(CB_ERR_SHAPE, "n_qheads (%d) must be a positive multiple of n_heads (%d)", q->n_qheads, tgt->n_heads);
+    const int G = q->n_qheads / tgt->n_heads;
+    if (G > 32 || (G & (G - 1)) != 0) return fail(CB_ERR_UNSUPPORTED, "query heads per KV head must be a power of two <= 32");
+    const int nb = q->n_bounds;
+    if (nb < 1 || nb > 64 || nb * G > 256)
+        return fail(CB_ERR_UNSUPPORTED, "need 1 <= n_bounds <= 64 and n_bounds * G <= 256 (got %d, G = %d)", nb, G);
+    if (sample_stride < 1) return fail(CB_ERR_INVALID_ARGUMENT, "sample_stride must be >= 1");
+    for (int k = 0; k < nb; ++k) {
+        if (boundaries[k] < 0 || boundaries[k] >= tgt->seq_len || (k > 0 && boundaries[k] <= boundaries[k - 1]))
+            return fail(CB_ERR_INVALID_ARGUMENT, "boundaries must increase strictly within [0, seq_len)");
+    }
+    const int64_t N = (int64_t)tgt->n_seqs * tgt->seq_len;
+    if (r_row_stride < N) return fail(CB_ERR_SHAPE, "r_row_stride (%lld) < tokens in the call (%lld)", (long long)r_row_stride,
+                                      (long long)N);
+    if (N == 0) return ok();
+    if (!q->data) return fail(CB_ERR_INVALID_ARGUMENT, "q->data is NULL");
+    const int64_t qs[4] = {q->s_layer, q->s_seq, q->s_bnd, q->s_head};
+    for (int i = 0; i < 4; ++i)
+        if (qs[i] < 0 || qs[i] % 8) return fail(CB_ERR_MISALIGNED, "q strides must be non-negative multiples of 8 elements");
+    if (((uintptr_t)q->data) % 16 || ((uintptr_t)r) % 4) return fail(CB_ERR_MISALIGNED, "q->data must be 16-byte and r 4-byte aligned");
+    if ((int64_t)tgt->n_seqs * tgt->n_layers * tgt->n_heads > INT32_MAX)
+        return fail(CB_ERR_UNSUPPORTED, "too many (sequence, layer, head) units in one call");
+    cb::AttnLaunch L = {};
+    L.kv = (const uint16_t *)tgt->data;
+    L.ts = strides_of(tgt);
+    L.q = (const uint16_t *)q->data;
+    for (int i = 0; i < 4; ++i) L.q_strides[i] = qs[i];
+    L.n_layers = tgt->n_layers;
+    L.n_heads = tgt->n_heads;
+    L.G = G;
+    L.n_bounds = nb;
+    L.seq_len = tgt->seq_len;
+    L.n_seqs = tgt->n_seqs;
+    L.stride = sample_stride;
+    L.d = d;
+    L.bounds = boundaries;
+    L.r = r;
+    L.r_row_stride = r_row_stride;
+    if (cb::launch_attn_sensitivity(L, (hipStream_t)stream) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "attention sensitivity launch failed");
+    return ok();
+}
+
+cb_status cb_attn_weights(int32_t n_rows, int32_t n_seqs, int32_t seq_len, int32_t sample_stride, const float *r,
+                          int64_t r_row_stride, int32_t p, float *w, int64_t w_row_stride, float *alpha,
+                          void *stream) {
+    if (n_rows < 0 || n_seqs < 0 || seq_len < 0) return fail(CB_ERR_INVALID_ARGUMENT, "negative size");
+    if (sample_stride < 1 || p < 1) return fail(CB_ERR_INVALID_ARGUMENT, "sample_stride and p must be >= 1");
+    const int64_t N = (int64_t)n_seqs * seq_len;
+    if (r_row_stride < N || w_row_stride < N) return fail(CB_ERR_SHAPE, "row strides must be >= n_seqs * seq_len");
+    if (n_rows == 0) return ok();
+    if (!r || !w || !alpha) return fail(CB_ERR_INVALID_ARGUMENT, "r, w and alpha must be non-NULL");
+    if (((uintptr_t)r) % 4 || ((uintptr_t)w) % 4 || ((uintptr_t)alpha) % 4)
+        return fail(CB_ERR_MISALIGNED, "r, w and alpha must be 4-byte aligned");
+    if (cb::launch_attn_weights(n_rows, n_seqs, seq_len, sample_stride, r, r_row_stride, p, w, w_row_stride, alpha,
+                                (hipStream_t)stream) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "attention weights launch failed");
+    return ok();
+}
+
 cb_status cb_apply(cb_plan *p, const float *maps, const cb_cache *src, const cb_cache *tgt_out, void *stream) {
     if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
     if (p->duplicate_targets)

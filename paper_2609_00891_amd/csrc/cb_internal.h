@@ -93,7 +93,23 @@ struct ApplyArgs {
     const float *bias;    // [n_maps][d_t]
 };
 
+// Attention-aligned sensitivities of one call (host side of the launch).
+struct AttnLaunch {
+    const uint16_t *kv;
+    Strides ts;
+    const uint16_t *q;
+    int64_t q_strides[4];     // layer, seq, boundary, query head (elements)
+    int32_t n_layers, n_heads, G, n_bounds, seq_len, n_seqs, stride, d;
+    const int32_t *bounds;    // host, n_bounds increasing positions
+    float *r;
+    int64_t r_row_stride;
+};
+
 // Launchers (return hipError_t of the launch).
+hipError_t launch_attn_sensitivity(const AttnLaunch &L, hipStream_t s);
+hipError_t launch_attn_weights(int32_t n_rows, int32_t n_seqs, int32_t seq_len, int32_t stride, const float *r,
+                               int64_t r_row_stride, int32_t p, float *w, int64_t w_row_stride, float *alpha,
+                               hipStream_t s);
 hipError_t launch_stats(int d_s, int d_t, const StatsArgs &a, hipStream_t s);
 hipError_t launch_reduce(int d_s, int d_t, const ReduceArgs &a, hipStream_t s);
 hipError_t launch_stats_centered(int d_s, int d_t, const StatsArgs &a, hipStream_t s);

@@ -281,6 +281,35 @@ def gen_weights(wl: Workload, seq0: int = 0, n_seqs: Optional[int] = None, seq_l
     return out
 
 
+def attn_boundaries(seq_len: int, n: int = 32, first: int = 12):
+    """Logarithmically spaced query positions from ``first`` through seq_len - 1
+    (rounded to the nearest integer, repeats dropped): the calibration boundaries
+    of Sec. 4.1 (32 from token 12 through 1,023 for 1,024-token sequences)."""
+    b = np.unique(np.rint(np.geomspace(first, seq_len - 1, n)).astype(np.int64))
+    return b.astype(np.int32)
+
+
+QUERY_SCORE_STD = 2.0     # target standard deviation of q . k / sqrt(d) for the generated queries
+
+
+def gen_queries(wl: Workload, tgt: torch.Tensor, n_qheads: int, n_bounds: int, seq0: int = 0,
+                device="cpu") -> torch.Tensor:
+    """Queries [L_t][B][n_bounds][n_qheads][d_t] bf16 for the attention-aligned weights:
+    N(0,1) scaled per (layer, KV head) so that q . k / sqrt(d) has standard
+    deviation QUERY_SCORE_STD against that head's keys (one generator per layer
+    and batch)."""
+    L, B, H, d = wl.L_t, tgt.shape[2], wl.H_t, wl.d_t
+    G = n_qheads // H
+    out = torch.empty((L, B, n_bounds, n_qheads, d), dtype=torch.bfloat16, device=device)
+    for l in range(L):
+        gen = _gen(device, wl.name, "q", l, seq0, B, n_bounds)
+        q = torch.randn((B, n_bounds, n_qheads, d), generator=gen, device=device, dtype=torch.float32)
+        k2 = tgt[l, 0].to(torch.float32).pow(2).mean(dim=(0, 2, 3))                       # [H]
+        scale = (QUERY_SCORE_STD / torch.sqrt(k2.clamp_min(1e-12))).repeat_interleave(G)   # [n_qheads]
+        out[l] = (q * scale[None, None, :, None]).to(torch.bfloat16)
+    return out
+
+
 def gen_apply_source(wl: Workload = APPLY, n_seqs: Optional[int] = None, seq_len: Optional[int] = None,
                      device="cpu", out: Optional[torch.Tensor] = None) -> torch.Tensor:
     """Sender cache for the online application workload (same recipe as the source cache)."""

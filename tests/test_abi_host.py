@@ -128,3 +128,37 @@ def test_probe_entry_points_reject_bad_arguments_and_rank_on_the_host():
     assert score[1, 1] == -np.inf
     with pytest.raises(cb.CacheBridgeError, match="CB_ERR_INVALID_ARGUMENT"):
         cb.cb_select_layers({"tgt_layer": [0], "src_layer": [5]}, np.zeros(1), 1, 3, 1)
+
+
+def test_attn_entry_points_reject_bad_arguments_on_the_host():
+    import paper_2609_00891_amd as cb
+    lib = cb.library()
+    assert lib.cb_attn_sensitivity(None, None, None, 1, None, 0, None) == 1
+    bounds = (ctypes.c_int32 * 3)(4, 9, 20)
+    tgt = cb.CbCache()
+    tgt.n_layers, tgt.n_heads, tgt.head_dim, tgt.n_seqs, tgt.seq_len = 2, 2, 96, 1, 32
+    q = cb.CbQueries()
+    q.n_layers, q.n_qheads, q.head_dim, q.n_seqs, q.n_bounds = 2, 4, 96, 1, 3
+    fake = ctypes.c_void_p(256)
+    call = lambda: lib.cb_attn_sensitivity(ctypes.byref(tgt), ctypes.byref(q), bounds, 1, fake, 64, None)  # noqa: E731
+    assert call() == 6                                            # head_dim 96
+    tgt.head_dim = q.head_dim = 64
+    tgt.data = 256                                                # never dereferenced: every case fails first
+    q.n_qheads = 5
+    assert call() == 2                                            # 5 query heads over 2 KV heads
+    q.n_qheads = 6
+    assert call() == 6                                            # 3 per KV head: not a power of two
+    q.n_qheads = 4
+    bounds[2] = 40                                                # past the sequence
+    assert call() == 1
+    bounds[2] = 9                                                 # not increasing
+    assert call() == 1
+    bounds[2] = 20
+    assert lib.cb_attn_sensitivity(ctypes.byref(tgt), ctypes.byref(q), bounds, 0, fake, 64, None) == 1   # stride 0
+    assert lib.cb_attn_sensitivity(ctypes.byref(tgt), ctypes.byref(q), bounds, 1, fake, 16, None) == 2   # row stride
+    q.n_seqs = 2
+    assert call() == 2                                            # q and tgt disagree
+    assert lib.cb_attn_weights(4, 1, 32, 1, None, 32, 8, None, 32, None, None) == 1
+    assert lib.cb_attn_weights(4, 1, 32, 0, fake, 32, 8, fake, 32, fake, None) == 1
+    assert lib.cb_attn_weights(4, 1, 32, 1, fake, 16, 8, fake, 32, fake, None) == 2
+    assert lib.cb_attn_weights(0, 1, 32, 1, None, 32, 8, None, 32, None, None) == 0

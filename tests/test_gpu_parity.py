@@ -724,3 +724,91 @@ def test_probe_qwen_shape_all_layer_pairs_sampled_maps(cb):
     assert selg[:, 0].tolist() == planted
     del src, tgt, w
     plan.close()
+
+
+# ----------------------------------------------------------------------------- attention-aligned weights
+
+TOL_ATTN = 1e-4        # raw sensitivities and weights: relative Frobenius error per row
+
+
+def gpu_attn(cb, tgt, q, bounds, stride, p):
+    L, _, B, H, T, _ = tgt.shape
+    r = torch.empty((2 * L * H, B * T), dtype=torch.float32, device="cuda")
+    cb.cb_attn_sensitivity(tgt, q, bounds, stride, r)
+    w = torch.empty_like(r)
+    alpha = torch.empty((2 * L * H,), dtype=torch.float32, device="cuda")
+    cb.cb_attn_weights(r, B, T, stride, p, w, alpha)
+    torch.cuda.synchronize()
+    return r.double().cpu().numpy(), w.double().cpu().numpy(), alpha.double().cpu().numpy()
+
+
+def oracle_attn(tgt, q, bounds, stride, p):
+    L, _, B, H, T, d = tgt.shape
+    tc, qc = tgt.contiguous(), q.contiguous()
+    r = oracle.attn_sensitivity(bits(tc), tc.stride()[:5], L, H, d, B, T, bits(qc), qc.stride()[:4], q.shape[3],
+                                bounds, stride, n_threads=NTHREADS).reshape(2 * L * H, B * T)
+    w, alpha = oracle.attn_weights(r, B, T, stride, p)
+    return r, w, alpha
+
+
+def check_attn(rg, wg, ag, ro, wo, ao, label=""):
+    er = max(relF(rg[i], ro[i]) for i in range(ro.shape[0]))
+    ew = max(relF(wg[i], wo[i]) for i in range(wo.shape[0]))
+    ea = float(np.abs(ag - ao).max())
+    say(f"  attention weights{label}: max relF r {er:.3e}, w {ew:.3e}; max |alpha diff| {ea:.2e} "
+        f"(alpha {ao.min():.3f}..{ao.max():.3f})")
+    assert er <= TOL_ATTN and ew <= TOL_ATTN and ea <= 1e-5
+
+
+@pytest.mark.parametrize("d,G,stride", [(64, 2, 1), (64, 8, 4), (128, 2, 4), (128, 8, 1)])
+def test_attn_weights_small(cb, d, G, stride):
+    # 100-token sequences (a ragged last key tile), 8 boundaries from 3 to 99
+    wl = synth.Workload("attn", 2, 2, d, 2, 2, d, 2, 100, "qwen", "scaled", 0.1, "lognormal")
+    src, tgt, _ = make_inputs(wl)
+    bounds = synth.attn_boundaries(wl.seq_len, 8, 3)
+    q = synth.gen_queries(wl, tgt, G * wl.H_t, len(bounds), device="cuda")
+    rg, wg, ag = gpu_attn(cb, tgt, q, bounds, stride, p=d)
+    ro, wo, ao = oracle_attn(tgt, q, bounds, stride, p=d)
+    check_attn(rg, wg, ag, ro, wo, ao)
+    assert not rg[:, (wl.seq_len - 1)::wl.seq_len].any()      # the last token is in no prefix
+
+
+def test_attn_weights_paper_configuration(cb):
+    # Sec. 4.1: 1,024-token sequences, 32 boundaries from 12 to 1,023, every
+    # fourth token; eight query heads per KV head (64 / 8), d = 128
+    wl = synth.Workload("attnp", 2, 2, 128, 2, 2, 128, 2, 1024, "qwen", "scaled", 0.1, "lognormal")
+    src, tgt, _ = make_inputs(wl)
+    bounds = synth.attn_boundaries(1024)
+    assert len(bounds) == 32 and bounds[0] == 12 and bounds[-1] == 1023
+    q = synth.gen_queries(wl, tgt, 8 * wl.H_t, len(bounds), device="cuda")
+    rg, wg, ag = gpu_attn(cb, tgt, q, bounds, 4, p=128)
+    ro, wo, ao = oracle_attn(tgt, q, bounds, 4, p=128)
+    check_attn(rg, wg, ag, ro, wo, ao)
+    # the weights feed the statistics unchanged: G, C with them match the oracle
+    hm = synth.head_map(wl)
+    hm["weight_row"] = np.arange(wl.n_maps, dtype=np.int32)   # map m = (l*2 + z)*H + h uses row m
+    plan = cb.cb_plan_create(hm, src, tgt, wl.n_seqs * wl.seq_len)
+    wt = torch.as_tensor(wg, dtype=torch.float32, device="cuda")
+    G_, C_ = gpu_stats(cb, plan, src, tgt, wt)
+    sel = list(range(wl.n_maps))
+    Go, Co = oracle_stats_sel(hm, sel, src, tgt, wt)
+    check_stats(G_, C_, Go, Co, sel)
+    plan.close()
+
+
+def test_attn_weights_qwen_shape_sampled_heads(cb):
+    # the 64-layer x 8-KV-head target of the qwen workloads at 2,048 tokens,
+    # 32 boundaries from 12 to 2,047, every token; oracle on sampled (layer, head)
+    wl = synth.WORKLOADS["qwen50"].with_(n_seqs=2)
+    say(f"attn: generating {wl.n_seqs} x {wl.seq_len} tokens")
+    src, tgt, _ = make_inputs(wl)
+    del src
+    bounds = synth.attn_boundaries(wl.seq_len)
+    q = synth.gen_queries(wl, tgt, 8 * wl.H_t, len(bounds), device="cuda")
+    say("attn: GPU")
+    rg, wg, ag = gpu_attn(cb, tgt, q, bounds, 1, p=wl.d_s)
+    for (l, h) in ((0, 0), (37, 5), (63, 7)):
+        say(f"attn: oracle on layer {l}, head {h}")
+        ro, wo, ao = oracle_attn(tgt[l:l + 1, :, :, h:h + 1], q[l:l + 1, :, :, 8 * h:8 * h + 8], bounds, 1, p=wl.d_s)
+        rows = [(l * 2 + z) * wl.H_t + h for z in (0, 1)]
+        check_attn(rg[rows], wg[rows], ag[rows], ro, wo, ao, f" (layer {l}, head {h})")
