@@ -26,6 +26,8 @@ Transfer"):
   causal prefix boundaries (Sec. 3.3, Eq. attentionlinearization, Eq. sensitivity).
 * :func:`attn_weights` -- mean-one normalization and the ESS-floor shrinkage
   w = 1 + alpha* (r - 1) (Sec. 3.3).
+* :func:`rope` -- rotary position transform of the K rows of a cache, forward or
+  inverse (Sec. 2.1, Sec. 3.1: RoPE removed before fitting, restored after mapping).
 * :func:`coefficient_count` -- C(f) = 2 L_t H_t (k f d_s) d_t (Sec. 2.3, Eq. support-cost).
 
 Parity status: pinned by ``tests/test_oracle_pins.py``.
@@ -91,6 +93,9 @@ def _load():
                                                                  ctypes.c_int, _f64p, ctypes.c_int]
     lib.oracle_attn_weights.restype = ctypes.c_int
     lib.oracle_attn_weights.argtypes = [ctypes.c_int] * 4 + [_f64p, ctypes.c_int, _f64p, _f64p]
+    lib.oracle_rope.restype = ctypes.c_int
+    lib.oracle_rope.argtypes = [ctypes.c_int] * 5 + [_u16p, _i64p, _u16p, _i64p, ctypes.c_double, ctypes.c_int,
+                                                     ctypes.c_int, ctypes.c_int]
     lib.oracle_double_to_bf16_array.restype = ctypes.c_int
     lib.oracle_double_to_bf16_array.argtypes = [ctypes.c_int64, _f64p, _u16p]
     _lib = lib
@@ -323,6 +328,22 @@ def attn_weights(r, n_seqs: int, seq_len: int, sample_stride: int, p: int):
     lib.oracle_attn_weights(rows, n_seqs, seq_len, sample_stride, _ptr(r, _f64p), int(p), _ptr(w, _f64p),
                             _ptr(alpha, _f64p))
     return w, alpha
+
+
+def rope(cache, strides, n_layers: int, n_heads: int, d: int, n_seqs: int, seq_len: int, theta: float,
+         style: int = 0, inverse: bool = False, pos_offset: int = 0):
+    """Rotate (or, with inverse, de-rotate) the K rows of a bf16 cache (uint16 bits, canonical
+    contiguous layout for the output); V rows are copied.  style 0: pairs (i, i + d/2);
+    style 1: pairs (2i, 2i + 1).  Returns the output bits."""
+    lib = _load()
+    src = np.ascontiguousarray(_u16(cache))
+    ss = _strides5(strides)
+    out = np.zeros((n_layers, 2, n_seqs, n_heads, seq_len, d), dtype=np.uint16)
+    os_ = np.asarray([2 * n_seqs * n_heads * seq_len * d, n_seqs * n_heads * seq_len * d, n_heads * seq_len * d,
+                      seq_len * d, d], dtype=np.int64)
+    lib.oracle_rope(n_layers, n_heads, d, n_seqs, seq_len, _ptr(src, _u16p), _ptr(ss, _i64p), _ptr(out, _u16p),
+                    _ptr(os_, _i64p), float(theta), int(style), int(bool(inverse)), int(pos_offset))
+    return out
 
 
 def double_to_bf16(v) -> np.ndarray:

@@ -591,6 +591,46 @@ int oracle_attn_weights(int n_rows, int n_seqs, int seq_len, int sample_stride, 
 }
 
 /*
+ * Rotary position transform of the keys (Sec. 2.1, Sec. 3.1: source RoPE is
+ * inverted before fitting and target RoPE applied after mapping; RoFormer's
+ * rotation).  For every K row (kv = 0) of a cache at position
+ * pos = pos_offset + tok, channel pairs are rotated by the angle pos * f_i,
+ * f_i = theta^(-2 i / d), i < d/2:
+ *   style 0 (half split): pair (i, i + d/2);  style 1 (interleaved): pair (2i, 2i + 1);
+ *   (a, b) -> (a cos - b sin, b cos + a sin), with the angle negated when inverse.
+ * Angles, sines and products in fp64, one rounding to bf16 (RNE).  V rows
+ * (kv = 1) are copied unchanged.  in/out: bf16 bits with strides {layer, kv,
+ * seq, head, tok}.  Returns 0.
+ */
+int oracle_rope(int n_layers, int n_heads, int d, int n_seqs, int seq_len, const uint16_t *in,
+                const int64_t *in_strides, uint16_t *out, const int64_t *out_strides, double theta, int style,
+                int inverse, int pos_offset) {
+    const int h = d / 2;
+    for (int l = 0; l < n_layers; ++l)
+        for (int z = 0; z < 2; ++z)
+            for (int b = 0; b < n_seqs; ++b)
+                for (int g = 0; g < n_heads; ++g)
+                    for (int t = 0; t < seq_len; ++t) {
+                        const uint16_t *xr = in + row_offset(in_strides, l, z, b, g, t);
+                        uint16_t *yr = out + row_offset(out_strides, l, z, b, g, t);
+                        if (z == 1) {
+                            for (int j = 0; j < d; ++j) yr[j] = xr[j];
+                            continue;
+                        }
+                        const double pos = (double)(pos_offset + t);
+                        for (int i = 0; i < h; ++i) {
+                            const double ang = (inverse ? -pos : pos) * pow(theta, -2.0 * i / (double)d);
+                            const double c = cos(ang), s = sin(ang);
+                            const int ia = style == 0 ? i : 2 * i, ib = style == 0 ? i + h : 2 * i + 1;
+                            const double a = bf16_bits_to_double(xr[ia]), bb = bf16_bits_to_double(xr[ib]);
+                            yr[ia] = oracle_double_to_bf16(a * c - bb * s);
+                            yr[ib] = oracle_double_to_bf16(bb * c + a * s);
+                        }
+                    }
+    return 0;
+}
+
+/*
  * Online application of the fitted maps.
  *   W [n_maps][P][d_t] (fp64 copies of the coefficients; row d_s is the bias)
  *   out[tgt_layer, kv, seq, tgt_head, tok, j] = RNE_bf16( sum_k x~_k W[k][j] )

@@ -807,3 +807,63 @@ def test_attn_weights_kish_closed_form_and_degenerate_rows():
     assert alpha[1] < 1.0 and (w[1].sum() ** 2 / (w[1] ** 2).sum()) == pytest.approx(16, rel=1e-12)
     assert alpha[2] == 1.0 and np.allclose(w[2], 1.0)
     assert alpha[3] == 1.0 and np.allclose(w[3], 1.0)
+
+
+# ----------------------------------------------------------------------------- rotary positions
+
+def _rope_f64(x, pos, theta, style):
+    """Exact rotation of fp64 rows x [..., d] at positions pos (for the pins only)."""
+    d = x.shape[-1]
+    h = d // 2
+    f = theta ** (-2.0 * np.arange(h) / d)
+    ang = np.asarray(pos, dtype=np.float64)[..., None] * f
+    c, s = np.cos(ang), np.sin(ang)
+    ia = np.arange(h) if style == 0 else 2 * np.arange(h)
+    ib = ia + h if style == 0 else ia + 1
+    y = x.copy()
+    y[..., ia] = x[..., ia] * c - x[..., ib] * s
+    y[..., ib] = x[..., ib] * c + x[..., ia] * s
+    return y
+
+
+@pytest.mark.parametrize("style", [0, 1])
+def test_rope_relative_position_property_and_identity_at_zero(style):
+    # RoFormer's defining property: <R_p q, R_r k> = <q, R_(r-p) k>, for any
+    # positions; it fixes the frequencies, the pairing and the signs
+    rng = np.random.default_rng(51)
+    d, theta = 16, 10000.0
+    L, H, B, T = 1, 1, 1, 40
+    x = rng.integers(-8, 9, size=(L, 2, B, H, T, d)).astype(np.float64)
+    bits = to_bf16_bits(x)
+    st = synth.cache_strides(L, H, B, T, d)
+    rot = bf16_val(oracle.rope(bits, st, L, H, d, B, T, theta, style))
+    # the oracle's rotated rows are the exact rotation rounded once to bf16
+    exact = _rope_f64(x[0, 0, 0, 0], np.arange(T), theta, style)
+    np.testing.assert_array_equal(rot[0, 0, 0, 0], bf16_val(oracle.double_to_bf16(exact)))
+    np.testing.assert_array_equal(rot[0, 1], x[0, 1])                   # V rows untouched
+    np.testing.assert_array_equal(rot[0, 0, 0, 0, 0], x[0, 0, 0, 0, 0])  # position 0: identity
+    q, k = rng.standard_normal(d), rng.standard_normal(d)
+    for p, r in ((3, 17), (29, 5), (0, 39)):
+        lhs = _rope_f64(q, p, theta, style) @ _rope_f64(k, r, theta, style)
+        assert lhs == pytest.approx(q @ _rope_f64(k, r - p, theta, style), abs=1e-12)
+    # and pair 0 turns by exactly one radian per position (f_0 = 1)
+    e = np.zeros(d)
+    e[0] = 1.0
+    y = _rope_f64(e, 1, theta, style)
+    assert y[0] == pytest.approx(np.cos(1.0)) and y[d // 2 if style == 0 else 1] == pytest.approx(np.sin(1.0))
+
+
+def test_rope_inverse_undoes_forward_up_to_bf16_rounding():
+    rng = np.random.default_rng(52)
+    L, H, B, T, d = 2, 2, 2, 33, 64
+    x = rng.standard_normal((L, 2, B, H, T, d))
+    bits = to_bf16_bits(x)
+    st = synth.cache_strides(L, H, B, T, d)
+    fwd = oracle.rope(bits, st, L, H, d, B, T, 1e6, 0, pos_offset=100)
+    back = oracle.rope(fwd, st, L, H, d, B, T, 1e6, 0, inverse=True, pos_offset=100)
+    a, b = bf16_val(bits), bf16_val(back)
+    assert relF(b, a) < 2 ** -8                                        # two roundings
+    # norms of every pair are preserved up to the same rounding
+    na = np.hypot(a[:, 0, ..., :d // 2], a[:, 0, ..., d // 2:])
+    nb = np.hypot(bf16_val(fwd)[:, 0, ..., :d // 2], bf16_val(fwd)[:, 0, ..., d // 2:])
+    assert np.abs(nb - na).max() <= 2 ** -7 * na.max()
