@@ -257,6 +257,28 @@ def attn_leg(cb, synth, bw, tgt, steps):
     }
 
 
+def rope_leg(cb, cache, steps):
+    """Target RoPE restored on mapped keys (Sec. 3.1): an in-place rotation of the
+    K rows of the applied 8 x 32,768-token target cache (base 1e6, half-split
+    pairs), timed with events after one warm-up pass (the cache is not used
+    afterwards)."""
+    import torch
+    L, _, B, H, T, d = cache.shape
+    table = torch.empty((T, d // 2, 2), dtype=torch.float32, device="cuda")
+    cb.cb_rope_table(1e6, d, T, table)
+    stream = torch.cuda.current_stream()
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 2)]
+    cb.cb_rope(cache, cache, table)
+    e[0].record(stream)
+    for i in range(steps):
+        cb.cb_rope(cache, cache, table, inverse=(i % 2 == 0))
+        e[i + 1].record(stream)
+    torch.cuda.synchronize()
+    ms = sum(e[i].elapsed_time(e[i + 1]) for i in range(steps)) / steps
+    bytes_ = 2 * L * B * H * T * d * 2                       # K rows read and written once
+    return {"ms": ms, "GBps": bytes_ / (ms / 1e3) / 1e9, "bytes_per_pass": bytes_}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -271,6 +293,8 @@ def main():
     ap.add_argument("--probe-seqs", type=int, default=10, help="calibration sequences of the probe leg")
     ap.add_argument("--attn-steps", type=int, default=2,
                     help="timed attention-aligned weight passes over the resident batch (0: skip)")
+    ap.add_argument("--rope-steps", type=int, default=3,
+                    help="timed in-place RoPE passes over the applied target cache (0: skip)")
     ap.add_argument("--hbm-copy-probe", type=float, default=None, metavar="GIB",
                     help="only time a plain copy of GIB GiB (counter calibration)")
     args = ap.parse_args()
@@ -419,6 +443,8 @@ def main():
         res["probes"] = probe_leg(cb, wl, src, tgt, w, min(args.probe_seqs, B), args.probe_steps)
     if args.attn_steps > 0:
         res["attn_weights"] = attn_leg(cb, synth, bw, tgt, args.attn_steps)
+    if args.rope_steps > 0 and aout is not None:
+        res["rope"] = rope_leg(cb, aout, args.rope_steps)
     if not args.no_cpu_baseline:
         n_threads = int(os.environ.get("OMP_NUM_THREADS", str(os.cpu_count() or 1)))
         log(f"cpu baseline on {n_threads} threads")

@@ -28,6 +28,11 @@
  *
  *   cb_attn_sensitivity, cb_attn_weights
  *
+ * and the rotary position transform of cached keys (Sec. 2.1, Sec. 3.1: RoPE
+ * removed before fitting, restored after mapping):
+ *
+ *   cb_rope_table, cb_rope
+ *
  * Conventions shared by every call
  * --------------------------------
  * - Row vectors: a map is W~ = [W ; b^T], a P x d_t fp32 matrix with
@@ -334,6 +339,38 @@ cb_status cb_attn_sensitivity(const cb_cache *tgt, const cb_queries *q, const in
 cb_status cb_attn_weights(int32_t n_rows, int32_t n_seqs, int32_t seq_len, int32_t sample_stride, const float *r,
                           int64_t r_row_stride, int32_t p, float *w, int64_t w_row_stride, float *alpha,
                           void *stream);
+
+/* cb_rope styles: which channels of a head form the rotated pairs. */
+#define CB_ROPE_HALF_SPLIT 0   /* (i, i + d/2): the split used by Qwen3 and most decoders */
+#define CB_ROPE_INTERLEAVED 1  /* (2i, 2i + 1): RoFormer's original pairing               */
+
+/*
+ * Rotary frequency table: table[pos][i] = (cos, sin)(pos * theta^(-2 i / d))
+ * for 0 <= pos < n_pos and i < d / 2, as fp32 pairs ([n_pos][d/2][2], device,
+ * caller-owned).  Angles and sines are formed in fp64.  d even, 2..256.
+ */
+cb_status cb_rope_table(double theta, int32_t head_dim, int32_t n_pos, float *table, void *stream);
+
+/*
+ * Rotary position transform of the keys (Sec. 2.1; Sec. 3.1: the maps act in
+ * content coordinates, so source RoPE is removed before fitting and the
+ * target's RoPE is applied to the mapped keys).  For every K row (kv = 0) of
+ * `in`, at position pos = pos_offset + tok, each channel pair (style
+ * CB_ROPE_HALF_SPLIT or CB_ROPE_INTERLEAVED) is turned by the table's angle
+ * of pos (negated when `inverse` is non-zero):
+ *   (a, b) -> (a cos - b sin, b cos + a sin),
+ * in fp32 from the exact bf16 values, rounded once to bf16, and written to the
+ * same element of `out`.  V rows (kv = 1) carry no position: they are copied
+ * when out->data differs from in->data and left alone otherwise.  `out` may be
+ * `in` (same data and strides) for an in-place transform; other overlaps are
+ * not allowed.  in and out: the same geometry, head_dim a multiple of 16 up to
+ * 256; table: from cb_rope_table with this head_dim and n_pos >= pos_offset +
+ * seq_len.  Use: fit on cb_rope(inverse) copies of the source and target
+ * caches; apply on a cb_rope(inverse) copy of the sender's cache, then
+ * cb_rope (forward, target table) on the output in place.
+ */
+cb_status cb_rope(const cb_cache *in, const cb_cache *out, const float *table, int32_t n_pos, int32_t style,
+                  int32_t inverse, int32_t pos_offset, void *stream);
 
 /*
  * Online mapping (Sec. 1 pipeline; Sec. 2.3 Eq. support-cost): for every map

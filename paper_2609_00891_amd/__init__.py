@@ -19,6 +19,8 @@ current HIP stream.  The functions keep the C names:
 * :func:`cb_attn_sensitivity`, :func:`cb_attn_weights` -- attention-aligned
   calibration weights: raw sensitivities at causal prefix boundaries and the
   ESS-floor shrinkage (Sec. 3.3)
+* :func:`cb_rope_table`, :func:`cb_rope` -- rotary position transform of cached
+  keys (RoPE removed before fitting, restored after mapping; Sec. 2.1, 3.1)
 
 Caches are bfloat16 tensors indexed ``[layer][kv][seq][head][tok][dim]`` (any
 strides with a unit channel stride).  Importing this package fails if the
@@ -37,6 +39,8 @@ LIB_PATH = os.path.join(_HERE, "libcachebridge.so")
 
 CB_LAMBDA_RELATIVE = 1
 CB_RIDGE_BIAS_UNPENALIZED = 2
+CB_ROPE_HALF_SPLIT = 0
+CB_ROPE_INTERLEAVED = 1
 
 STATUS_NAMES = {0: "CB_OK", 1: "CB_ERR_INVALID_ARGUMENT", 2: "CB_ERR_SHAPE", 3: "CB_ERR_MISALIGNED",
                 4: "CB_ERR_OUT_OF_MEMORY", 5: "CB_ERR_DEVICE", 6: "CB_ERR_UNSUPPORTED"}
@@ -113,6 +117,11 @@ _lib.cb_attn_sensitivity.argtypes = [ctypes.POINTER(CbCache), ctypes.POINTER(CbQ
 _lib.cb_attn_weights.restype = ctypes.c_int
 _lib.cb_attn_weights.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp, ctypes.c_int64,
                                  ctypes.c_int32, _vp, ctypes.c_int64, _vp, _vp]
+_lib.cb_rope_table.restype = ctypes.c_int
+_lib.cb_rope_table.argtypes = [ctypes.c_double, ctypes.c_int32, ctypes.c_int32, _vp, _vp]
+_lib.cb_rope.restype = ctypes.c_int
+_lib.cb_rope.argtypes = [ctypes.POINTER(CbCache), ctypes.POINTER(CbCache), _vp, ctypes.c_int32, ctypes.c_int32,
+                         ctypes.c_int32, ctypes.c_int32, _vp]
 _lib.cb_apply.restype = ctypes.c_int
 _lib.cb_apply.argtypes = [_vp, _vp, ctypes.POINTER(CbCache), ctypes.POINTER(CbCache), _vp]
 _lib.cb_status_string.restype = ctypes.c_char_p
@@ -369,6 +378,22 @@ def cb_attn_weights(r: torch.Tensor, n_seqs: int, seq_len: int, sample_stride: i
         raise ValueError("r, w [rows][...], alpha [rows]")
     _check(_lib.cb_attn_weights(n_rows, int(n_seqs), int(seq_len), int(sample_stride), _ptr(r), r.stride(0), int(p),
                                 _ptr(w), w.stride(0), _ptr(alpha), _stream(stream)))
+
+
+def cb_rope_table(theta: float, head_dim: int, n_pos: int, table: torch.Tensor, stream=None):
+    """table [n_pos][head_dim/2][2] float32 = (cos, sin)(pos * theta^(-2i/d))."""
+    if table.dtype != torch.float32 or table.numel() < n_pos * head_dim:
+        raise ValueError("table is float32 with n_pos * head_dim elements")
+    _check(_lib.cb_rope_table(float(theta), int(head_dim), int(n_pos), _ptr(table), _stream(stream)))
+
+
+def cb_rope(cache_in: torch.Tensor, cache_out: torch.Tensor, table: torch.Tensor, style: int = CB_ROPE_HALF_SPLIT,
+            inverse: bool = False, pos_offset: int = 0, stream=None):
+    """Rotate (inverse: de-rotate) the K rows of a cache into cache_out (may be cache_in); V rows copied."""
+    n_pos = table.shape[0]
+    iv, ov = cache_view(cache_in), cache_view(cache_out)
+    _check(_lib.cb_rope(ctypes.byref(iv), ctypes.byref(ov), _ptr(table), int(n_pos), int(style), int(bool(inverse)),
+                        int(pos_offset), _stream(stream)))
 
 
 def cb_apply(plan: Plan, maps: torch.Tensor, src: torch.Tensor, tgt_out: torch.Tensor, stream=None):

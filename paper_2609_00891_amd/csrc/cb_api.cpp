@@ -621,6 +621,59 @@ cb_status cb_attn_weights(int32_t n_rows, int32_t n_seqs, int32_t seq_len, int32
     return ok();
 }
 
+cb_status cb_rope_table(double theta, int32_t head_dim, int32_t n_pos, float *table, void *stream) {
+    if (!(theta > 0.0) || !std::isfinite(theta)) return fail(CB_ERR_INVALID_ARGUMENT, "theta must be finite and > 0");
+    if (head_dim < 2 || head_dim > 256 || head_dim % 2) return fail(CB_ERR_UNSUPPORTED, "head_dim must be even, 2..256");
+    if (n_pos < 0) return fail(CB_ERR_INVALID_ARGUMENT, "n_pos is negative");
+    if (n_pos == 0) return ok();
+    if (!table) return fail(CB_ERR_INVALID_ARGUMENT, "table is NULL");
+    if (((uintptr_t)table) % 8) return fail(CB_ERR_MISALIGNED, "table must be 8-byte aligned");
+    if (cb::launch_rope_table(head_dim, n_pos, theta, table, (hipStream_t)stream) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "rope table launch failed");
+    return ok();
+}
+
+cb_status cb_rope(const cb_cache *in, const cb_cache *out, const float *table, int32_t n_pos, int32_t style,
+                  int32_t inverse, int32_t pos_offset, void *stream) {
+    if (!in || !out) return fail(CB_ERR_INVALID_ARGUMENT, "in and out must be non-NULL");
+    const int d = in->head_dim;
+    if (d < 16 || d > 256 || d % 16) return fail(CB_ERR_UNSUPPORTED, "head_dim must be a multiple of 16 up to 256");
+    if (style != CB_ROPE_HALF_SPLIT && style != CB_ROPE_INTERLEAVED)
+        return fail(CB_ERR_INVALID_ARGUMENT, "unknown rope style %d", style);
+    if (in->n_layers <= 0 || in->n_heads <= 0) return fail(CB_ERR_SHAPE, "in needs positive layer and head counts");
+    if (cb_status s = check_cache("in", in, in->n_layers, in->n_heads, d)) return s;
+    if (cb_status s = check_cache("out", out, in->n_layers, in->n_heads, d)) return s;
+    if (out->n_seqs != in->n_seqs || out->seq_len != in->seq_len)
+        return fail(CB_ERR_SHAPE, "in and out disagree on n_seqs / seq_len");
+    if (pos_offset < 0 || (int64_t)pos_offset + in->seq_len > n_pos)
+        return fail(CB_ERR_SHAPE, "positions %d .. %lld need a table of that many rows (n_pos = %d)", pos_offset,
+                    (long long)pos_offset + in->seq_len - 1, n_pos);
+    if ((int64_t)in->n_seqs * in->seq_len == 0) return ok();
+    if (!table) return fail(CB_ERR_INVALID_ARGUMENT, "table is NULL");
+    if (((uintptr_t)table) % 8) return fail(CB_ERR_MISALIGNED, "table must be 8-byte aligned");
+    const bool same = in->data == out->data;
+    if (same && (in->s_layer != out->s_layer || in->s_kv != out->s_kv || in->s_seq != out->s_seq ||
+                 in->s_head != out->s_head || in->s_tok != out->s_tok))
+        return fail(CB_ERR_INVALID_ARGUMENT, "an in-place transform needs out to have in's strides");
+    cb::RopeLaunch L = {};
+    L.in = (const uint16_t *)in->data;
+    L.out = (uint16_t *)out->data;
+    L.is = strides_of(in);
+    L.os = strides_of(out);
+    L.table = table;
+    L.n_layers = in->n_layers;
+    L.n_heads = in->n_heads;
+    L.n_seqs = in->n_seqs;
+    L.seq_len = in->seq_len;
+    L.d = d;
+    L.style = style;
+    L.pos_offset = pos_offset;
+    L.inverse = inverse ? 1 : 0;
+    L.copy_v = same ? 0 : 1;
+    if (cb::launch_rope(L, (hipStream_t)stream) != hipSuccess) return fail(CB_ERR_DEVICE, "rope launch failed");
+    return ok();
+}
+
 cb_status cb_apply(cb_plan *p, const float *maps, const cb_cache *src, const cb_cache *tgt_out, void *stream) {
     if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
     if (p->duplicate_targets)

@@ -105,7 +105,18 @@ struct AttnLaunch {
     int64_t r_row_stride;
 };
 
+// Rotary transform of one call (host side of the launch).
+struct RopeLaunch {
+    const uint16_t *in;
+    uint16_t *out;
+    Strides is, os;
+    const float *table;       // [n_pos][d/2][2] (cos, sin)
+    int32_t n_layers, n_heads, n_seqs, seq_len, d, style, pos_offset, inverse, copy_v;
+};
+
 // Launchers (return hipError_t of the launch).
+hipError_t launch_rope_table(int32_t d, int32_t n_pos, double theta, float *table, hipStream_t s);
+hipError_t launch_rope(const RopeLaunch &L, hipStream_t s);
 hipError_t launch_attn_sensitivity(const AttnLaunch &L, hipStream_t s);
 hipError_t launch_attn_weights(int32_t n_rows, int32_t n_seqs, int32_t seq_len, int32_t stride, const float *r,
                                int64_t r_row_stride, int32_t p, float *w, int64_t w_row_stride, float *alpha,

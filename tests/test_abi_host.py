@@ -162,3 +162,22 @@ def test_attn_entry_points_reject_bad_arguments_on_the_host():
     assert lib.cb_attn_weights(4, 1, 32, 0, fake, 32, 8, fake, 32, fake, None) == 1
     assert lib.cb_attn_weights(4, 1, 32, 1, fake, 16, 8, fake, 32, fake, None) == 2
     assert lib.cb_attn_weights(0, 1, 32, 1, None, 32, 8, None, 32, None, None) == 0
+
+
+def test_rope_entry_points_reject_bad_arguments_on_the_host():
+    import paper_2609_00891_amd as cb
+    lib = cb.library()
+    assert lib.cb_rope_table(ctypes.c_double(0.0), 128, 16, None, None) == 1
+    assert lib.cb_rope_table(ctypes.c_double(1e4), 127, 16, None, None) == 6
+    assert lib.cb_rope_table(ctypes.c_double(1e4), 128, 16, None, None) == 1
+    assert lib.cb_rope_table(ctypes.c_double(1e4), 128, 0, None, None) == 0
+    c = cb.CbCache()
+    c.data, c.n_layers, c.n_heads, c.head_dim, c.n_seqs, c.seq_len = 256, 1, 1, 40, 1, 8
+    c.s_layer, c.s_kv, c.s_seq, c.s_head, c.s_tok = 640, 320, 320, 320, 40
+    call = lambda style=0, n_pos=64, off=0: lib.cb_rope(ctypes.byref(c), ctypes.byref(c), ctypes.c_void_p(256),  # noqa
+                                                        n_pos, style, 0, off, None)
+    assert call() == 6                                   # head_dim 40 is not a multiple of 16
+    c.head_dim, c.s_tok, c.s_head, c.s_seq, c.s_kv, c.s_layer = 64, 64, 512, 512, 512, 1024
+    assert call(style=2) == 1
+    assert call(n_pos=6) == 2                            # positions 0..7 need 8 table rows
+    assert call(off=60) == 2

@@ -812,3 +812,115 @@ def test_attn_weights_qwen_shape_sampled_heads(cb):
         ro, wo, ao = oracle_attn(tgt[l:l + 1, :, :, h:h + 1], q[l:l + 1, :, :, 8 * h:8 * h + 8], bounds, 1, p=wl.d_s)
         rows = [(l * 2 + z) * wl.H_t + h for z in (0, 1)]
         check_attn(rg[rows], wg[rows], ag[rows], ro, wo, ao, f" (layer {l}, head {h})")
+
+
+# ----------------------------------------------------------------------------- rotary positions
+
+def gpu_rope_table(cb, theta, d, n_pos):
+    t = torch.empty((n_pos, d // 2, 2), dtype=torch.float32, device="cuda")
+    cb.cb_rope_table(theta, d, n_pos, t)
+    return t
+
+
+def check_bits_close(g, o, label, min_equal=0.999):
+    dist = ulp_distance(g, o)
+    same = float((dist == 0).mean())
+    say(f"  rope{label}: bitwise-equal {same:.6f}, max ulp distance {int(dist.max())}")
+    assert dist.max() <= 1 and same >= min_equal
+
+
+@pytest.mark.parametrize("d,style,inverse", [(64, 0, False), (128, 0, True), (128, 1, False), (64, 1, True)])
+def test_rope_matches_oracle(cb, d, style, inverse):
+    wl = synth.Workload("rope", 2, 3, d, 1, 1, 64, 2, 77, "qwen", "scaled", 0.1, "lognormal")
+    x = synth.gen_source(wl, device="cuda")
+    theta, off = (1e6 if style == 0 else 1e4), 7
+    table = gpu_rope_table(cb, theta, d, off + wl.seq_len)
+    ref = oracle.rope(bits(x), x.stride()[:5], wl.L_s, wl.H_s, d, wl.n_seqs, wl.seq_len, theta, style,
+                      inverse=inverse, pos_offset=off)
+    out = torch.empty_like(x)
+    cb.cb_rope(x, out, table, style, inverse, off)
+    torch.cuda.synchronize()
+    check_bits_close(bits(out).reshape(ref.shape), ref, f" d={d} style={style} inverse={inverse}")
+    # permuted-layout views give the same bits, and so does the in-place form
+    xp = x.permute(0, 1, 3, 2, 4, 5).contiguous().permute(0, 1, 3, 2, 4, 5)
+    op = torch.empty_like(xp)
+    cb.cb_rope(xp, op, table, style, inverse, off)
+    cb.cb_rope(xp, xp, table, style, inverse, off)
+    torch.cuda.synchronize()
+    assert torch.equal(op, out) and torch.equal(xp, out)
+
+
+def check_apply_rotated(ob, ref, label=""):
+    """check_apply for caches whose K rows (kv 0) were rotated after rounding:
+    a difference of one bf16 ulp in a pair before the rotation moves both rotated
+    elements by up to one ulp of the pair's norm, which can be many ulps of a
+    small element, so K rows get ulp(element) + ulp(pair norm) + 1e-4 of the
+    map's RMS; V rows keep the bound of check_apply."""
+    g = oracle.bf16_to_double(ob)
+    r = oracle.bf16_to_double(ref)
+    e = relF(g, r)
+    h = r.shape[-1] // 2
+    pn = np.hypot(r[..., :h], r[..., h:])
+    pn = np.concatenate([pn, pn], axis=-1)
+    ulp = lambda x: np.spacing(np.abs(x).astype(np.float32)).astype(np.float64) * 65536.0  # noqa: E731
+    rms = np.sqrt((r * r).mean(axis=(2, 4, 5), keepdims=True))
+    bound = ulp(r) + 1e-4 * rms
+    bound[:, 0] += ulp(pn[:, 0])
+    worst = float((np.abs(g - r) / bound).max())
+    same = float((ob == ref).mean())
+    say(f"  apply parity{label}: relF {e:.3e}, bitwise-equal {same:.6f}, worst err/bound {worst:.3f}")
+    assert e <= TOL_APPLY and worst <= 1.0
+
+
+def test_rope_fit_and_apply_end_to_end(cb):
+    # caches as a model holds them: keys carry RoPE (source base 1e4, target base
+    # 1e6).  Fit on de-rotated keys, apply on the de-rotated sender, then
+    # restore the target's rotation on the mapped keys.
+    wl = synth.Workload("ropee", 2, 2, 128, 2, 2, 128, 8, 96, "qwen", "gauss", 0.05, "lognormal")
+    src_c, tgt_c, w = make_inputs(wl)
+    ts, tt = 1e4, 1e6
+    src_rot_b = oracle.rope(bits(src_c), src_c.stride()[:5], wl.L_s, wl.H_s, wl.d_s, wl.n_seqs, wl.seq_len, ts)
+    tgt_rot_b = oracle.rope(bits(tgt_c), tgt_c.stride()[:5], wl.L_t, wl.H_t, wl.d_t, wl.n_seqs, wl.seq_len, tt)
+    as_bf16 = lambda b: torch.from_numpy(b.view(np.int16)).to("cuda").view(torch.bfloat16)  # noqa: E731
+    src_rot, tgt_rot = as_bf16(src_rot_b), as_bf16(tgt_rot_b)
+    tab_s = gpu_rope_table(cb, ts, wl.d_s, wl.seq_len)
+    tab_t = gpu_rope_table(cb, tt, wl.d_t, wl.seq_len)
+    src_g, tgt_g = torch.empty_like(src_rot), torch.empty_like(tgt_rot)
+    cb.cb_rope(src_rot, src_g, tab_s, inverse=True)
+    cb.cb_rope(tgt_rot, tgt_g, tab_t, inverse=True)
+    hm = synth.head_map(wl)
+    plan = cb.cb_plan_create(hm, src_g, tgt_g, wl.n_seqs * wl.seq_len)
+    G, C = gpu_stats(cb, plan, src_g, tgt_g, w)
+    maps, info = gpu_solve(cb, G, C, wl.lam_rel, cb.CB_LAMBDA_RELATIVE | cb.CB_RIDGE_BIAS_UNPENALIZED)
+    assert (info.cpu().numpy() == 0).all()
+    out = torch.zeros_like(tgt_rot)
+    cb.cb_apply(plan, maps, src_g, out)
+    cb.cb_rope(out, out, tab_t)
+    torch.cuda.synchronize()
+    # oracle: de-rotation, statistics, solve, apply, rotation -- the same steps in fp64
+    src_o = oracle.rope(src_rot_b, src_c.stride()[:5], wl.L_s, wl.H_s, wl.d_s, wl.n_seqs, wl.seq_len, ts, inverse=True)
+    tgt_o = oracle.rope(tgt_rot_b, tgt_c.stride()[:5], wl.L_t, wl.H_t, wl.d_t, wl.n_seqs, wl.seq_len, tt, inverse=True)
+    check_bits_close(bits(src_g).reshape(src_o.shape), src_o, " (source de-rotation)")
+    sel = list(range(wl.n_maps))
+    Go, Co = oracle.stats(hm, src_o, src_c.stride()[:5], wl.d_s, tgt_o, tgt_c.stride()[:5], wl.d_t,
+                          w.cpu().numpy(), wl.n_seqs * wl.seq_len, wl.n_seqs, wl.seq_len, n_threads=NTHREADS)
+    check_stats(G, C, Go, Co, sel)
+    Wo, _ = oracle.ridge_solve(Go, Co, wl.lam_rel, relative=True, bias_unpenalized=True)
+    e = max(relF(maps[i].double().cpu().numpy(), Wo[i]) for i in sel)
+    say(f"  maps parity on de-rotated keys: {e:.3e}")
+    assert e <= TOL_MAPS
+    mapped = np.zeros(tuple(out.shape), dtype=np.uint16)
+    oracle.apply(hm, maps.double().cpu().numpy(), src_o, src_c.stride()[:5], wl.d_s, mapped,
+                 tuple(out.stride()[:5]), wl.d_t, wl.n_seqs, wl.seq_len)
+    ref = oracle.rope(mapped, tuple(out.stride()[:5]), wl.L_t, wl.H_t, wl.d_t, wl.n_seqs, wl.seq_len, tt)
+    check_apply_rotated(bits(out).reshape(ref.shape), ref, " (rotated keys)")
+    # the K maps recover the planted content map: fitted without de-rotation they do not
+    Gr, Cr = gpu_stats(cb, plan, src_rot, tgt_rot, w)
+    mr, _ = gpu_solve(cb, Gr, Cr, wl.lam_rel, cb.CB_LAMBDA_RELATIVE | cb.CB_RIDGE_BIAS_UNPENALIZED)
+    planted = synth.planted_maps(wl, device="cuda").cpu()    # the generator make_inputs used
+    kmaps = [m for m in sel if hm["kv"][m] == 0]
+    e_c = max(relF(maps[m].cpu().numpy(), planted[m].numpy()) for m in kmaps)
+    e_r = min(relF(mr[m].cpu().numpy(), planted[m].numpy()) for m in kmaps)
+    say(f"  K maps vs the planted content map: de-rotated fit (worst) {e_c:.3e}, rotated fit (best) {e_r:.3e}")
+    assert e_c < 0.1 and e_r > 5 * e_c
+    plan.close()
