@@ -28,6 +28,10 @@ Transfer"):
   w = 1 + alpha* (r - 1) (Sec. 3.3).
 * :func:`rope` -- rotary position transform of the K rows of a cache, forward or
   inverse (Sec. 2.1, Sec. 3.1: RoPE removed before fitting, restored after mapping).
+* :func:`stats_multi` -- G, C over the multi-layer head-local feature
+  x~ = [x_0; ...; x_{k-1}; 1] (Sec. 3.2, Eq. localfeature with k selected
+  source layers), on every ``sample_stride``-th token (Sec. 4.1).
+* :func:`apply_multi` -- RNE_bf16(x~ W~) for multi-layer maps.
 * :func:`coefficient_count` -- C(f) = 2 L_t H_t (k f d_s) d_t (Sec. 2.3, Eq. support-cost).
 
 Parity status: pinned by ``tests/test_oracle_pins.py``.
@@ -96,6 +100,14 @@ def _load():
     lib.oracle_rope.restype = ctypes.c_int
     lib.oracle_rope.argtypes = [ctypes.c_int] * 5 + [_u16p, _i64p, _u16p, _i64p, ctypes.c_double, ctypes.c_int,
                                                      ctypes.c_int, ctypes.c_int]
+    lib.oracle_stats_multi.restype = ctypes.c_int
+    lib.oracle_stats_multi.argtypes = [ctypes.c_int, ctypes.c_int] + [_i32p] * 6 + [
+        _u16p, _i64p, ctypes.c_int, _u16p, _i64p, ctypes.c_int,
+        _f32p, ctypes.c_int64, ctypes.c_int, ctypes.c_int, ctypes.c_int, _f64p, _f64p, ctypes.c_int]
+    lib.oracle_apply_multi.restype = ctypes.c_int
+    lib.oracle_apply_multi.argtypes = [ctypes.c_int, ctypes.c_int] + [_i32p] * 5 + [
+        _f64p, _u16p, _i64p, ctypes.c_int, _u16p, _i64p, ctypes.c_int,
+        ctypes.c_int, ctypes.c_int, ctypes.c_int]
     lib.oracle_double_to_bf16_array.restype = ctypes.c_int
     lib.oracle_double_to_bf16_array.argtypes = [ctypes.c_int64, _f64p, _u16p]
     _lib = lib
@@ -364,3 +376,67 @@ def bf16_to_double(bits) -> np.ndarray:
 def coefficient_count(L_t: int, H_t: int, k: int, f: int, d_s: int, d_t: int) -> int:
     """Non-bias coefficient count over K and V, C(f) = 2 L_t H_t (k f d_s) d_t (Eq. support-cost)."""
     return 2 * L_t * H_t * (k * f * d_s) * d_t
+
+
+MULTI_MAP_FIELDS = ("tgt_layer", "tgt_head", "kv", "src_layers", "src_head", "weight_row")
+
+
+def _multi_arrays(head_map, fields=MULTI_MAP_FIELDS):
+    n, k, out = None, None, []
+    for f in fields:
+        a = np.ascontiguousarray(np.asarray(head_map[f], dtype=np.int32))
+        if f == "src_layers":
+            if a.ndim != 2:
+                raise ValueError("src_layers must be [n_maps][k]")
+            k = a.shape[1]
+        if n is None:
+            n = a.shape[0]
+        if a.shape[0] != n:
+            raise ValueError(f"head_map field {f} has {a.shape[0]} entries, expected {n}")
+        out.append(a)
+    return n, k, out
+
+
+def stats_multi(head_map, src, src_strides, d_s, tgt, tgt_strides, d_t, weights, w_row_stride,
+                n_seqs, seq_len, sample_stride=1, G: Optional[np.ndarray] = None,
+                C: Optional[np.ndarray] = None, n_threads: int = 0):
+    """Accumulate G += sum w x~ x~^T, C += sum w x~ y^T in fp64 over the
+    multi-layer feature x~ = [x_0; ...; x_{k-1}; 1] (P = k d_s + 1), visiting
+    the tokens t with t mod sample_stride == 0.  ``head_map["src_layers"]`` is
+    [n_maps][k]; other conventions as in :func:`stats`.  Returns (G, C)."""
+    lib = _load()
+    n, k, hm = _multi_arrays(head_map)
+    P = k * d_s + 1
+    if G is None:
+        G = np.zeros((n, P, P), dtype=np.float64)
+    if C is None:
+        C = np.zeros((n, P, d_t), dtype=np.float64)
+    assert G.dtype == np.float64 and G.flags.c_contiguous and G.shape == (n, P, P)
+    assert C.dtype == np.float64 and C.flags.c_contiguous and C.shape == (n, P, d_t)
+    assert int(sample_stride) >= 1
+    src = np.ascontiguousarray(_u16(src))
+    tgt = np.ascontiguousarray(_u16(tgt))
+    w = np.ascontiguousarray(np.asarray(weights, dtype=np.float32))
+    ss, ts = _strides5(src_strides), _strides5(tgt_strides)
+    lib.oracle_stats_multi(n, k, *[_ptr(a, _i32p) for a in hm], _ptr(src, _u16p), _ptr(ss, _i64p), d_s,
+                           _ptr(tgt, _u16p), _ptr(ts, _i64p), d_t, _ptr(w, _f32p), int(w_row_stride),
+                           int(n_seqs), int(seq_len), int(sample_stride), _ptr(G, _f64p), _ptr(C, _f64p),
+                           int(n_threads))
+    return G, C
+
+
+def apply_multi(head_map, W, src, src_strides, d_s, out, out_strides, d_t, n_seqs, seq_len,
+                n_threads: int = 0):
+    """Write RNE_bf16(x~ W~) for every multi-layer map and every token into ``out``."""
+    lib = _load()
+    n, k, hm = _multi_arrays(head_map, MULTI_MAP_FIELDS[:5])
+    W = np.ascontiguousarray(np.asarray(W, dtype=np.float64))
+    assert W.shape == (n, k * d_s + 1, d_t)
+    src = np.ascontiguousarray(_u16(src))
+    if not (out.dtype == np.uint16 and out.flags.c_contiguous):
+        raise TypeError("out must be a C-contiguous uint16 array")
+    ss, os_ = _strides5(src_strides), _strides5(out_strides)
+    lib.oracle_apply_multi(n, k, *[_ptr(a, _i32p) for a in hm], _ptr(W, _f64p), _ptr(src, _u16p),
+                           _ptr(ss, _i64p), d_s, _ptr(out, _u16p), _ptr(os_, _i64p), d_t,
+                           int(n_seqs), int(seq_len), int(n_threads))
+    return out

@@ -31,6 +31,11 @@
  *     out[l, z, seq, h, t, :] = RNE_bf16( x~ W~ ) with the sum taken in fp64 and
  *     rounded once, to nearest with ties to even, to bfloat16.
  *
+ *   Multi-layer feature (Sec. 3.2, Eq. localfeature with k selected source
+ *   layers): x~ = [x_0 ; ... ; x_{k-1} ; 1], P = k d_s + 1, over the sampled
+ *   calibration rows (oracle_stats_multi, oracle_apply_multi); the solve above
+ *   takes any P.
+ *
  * Parity status: stats, solve and apply are pinned by the tests in
  * tests/test_oracle_pins.py (closed forms, invariants, library special cases,
  * brute-force minimality of the paper's objective).  No worked numerical
@@ -658,6 +663,101 @@ int oracle_apply(int n_maps,
                 for (int j = 0; j < d_t; ++j) {
                     double s = 0.0;
                     for (int k = 0; k < P; ++k) s += xt[k] * Wm[(int64_t)k * d_t + j];
+                    orow[j] = oracle_double_to_bf16(s);
+                }
+            }
+        }
+        free(xt);
+    }
+    return 0;
+}
+
+/*
+ * Multi-layer head-local feature (Sec. 3.2, Eq. localfeature with k selected
+ * source layers).  Map m reads, for each calibration row, the k source rows
+ *   Z^S[src_layers[m*k + i], kv[m], seq, src_head[m], t],  i = 0..k-1,
+ * concatenated in that order, and appends 1:
+ *   x~ = [x_0 ; x_1 ; ... ; x_{k-1} ; 1]   (width P = k d_s + 1).
+ * The calibration rows are the tokens t of every sequence with
+ * t mod sample_stride == 0 (Sec. 4.1 samples every fourth token).
+ *   G [n_maps][P][P] += sum w x~ x~^T,   C [n_maps][P][d_t] += sum w x~ y^T
+ * with w = weights[weight_row[m] * w_row_stride + seq * seq_len + t].
+ * Returns 0.
+ */
+int oracle_stats_multi(int n_maps, int k,
+                       const int32_t *tgt_layer, const int32_t *tgt_head, const int32_t *kv,
+                       const int32_t *src_layers, const int32_t *src_head, const int32_t *weight_row,
+                       const uint16_t *src, const int64_t *src_strides, int d_s,
+                       const uint16_t *tgt, const int64_t *tgt_strides, int d_t,
+                       const float *weights, int64_t w_row_stride,
+                       int n_seqs, int seq_len, int sample_stride,
+                       double *G, double *C, int n_threads) {
+    const int P = k * d_s + 1;
+    set_threads(n_threads);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int m = 0; m < n_maps; ++m) {
+        double *Gm = G + (int64_t)m * P * P;
+        double *Cm = C + (int64_t)m * P * d_t;
+        double *xt = (double *)malloc(sizeof(double) * (size_t)P);
+        double *y = (double *)malloc(sizeof(double) * (size_t)d_t);
+        for (int b = 0; b < n_seqs; ++b) {
+            for (int t = 0; t < seq_len; t += sample_stride) {
+                for (int i = 0; i < k; ++i) {
+                    const uint16_t *xr = src + row_offset(src_strides, src_layers[(int64_t)m * k + i], kv[m], b,
+                                                          src_head[m], t);
+                    for (int c = 0; c < d_s; ++c) xt[i * d_s + c] = bf16_bits_to_double(xr[c]);
+                }
+                xt[k * d_s] = 1.0;
+                const uint16_t *yr = tgt + row_offset(tgt_strides, tgt_layer[m], kv[m], b, tgt_head[m], t);
+                for (int j = 0; j < d_t; ++j) y[j] = bf16_bits_to_double(yr[j]);
+                const double w = (double)weights[(int64_t)weight_row[m] * w_row_stride + (int64_t)b * seq_len + t];
+                for (int i = 0; i < P; ++i) {
+                    const double wi = w * xt[i];
+                    double *gr = Gm + (int64_t)i * P;
+                    double *cr = Cm + (int64_t)i * d_t;
+                    for (int j = 0; j < P; ++j) gr[j] += wi * xt[j];
+                    for (int j = 0; j < d_t; ++j) cr[j] += wi * y[j];
+                }
+            }
+        }
+        free(xt);
+        free(y);
+    }
+    return 0;
+}
+
+/*
+ * Online application of multi-layer maps (Sec. 3.2 feature, Sec. 1 pipeline):
+ *   W [n_maps][P][d_t], P = k d_s + 1, rows i d_s .. (i+1) d_s - 1 act on the
+ *   source row of src_layers[m*k + i], the last row is the bias;
+ *   out[tgt_layer, kv, seq, tgt_head, tok, j] = RNE_bf16( sum_p x~_p W[p][j] )
+ * for every token of every sequence, the sum in fp64, rounded once.  Returns 0.
+ */
+int oracle_apply_multi(int n_maps, int k,
+                       const int32_t *tgt_layer, const int32_t *tgt_head, const int32_t *kv,
+                       const int32_t *src_layers, const int32_t *src_head,
+                       const double *W,
+                       const uint16_t *src, const int64_t *src_strides, int d_s,
+                       uint16_t *out, const int64_t *out_strides, int d_t,
+                       int n_seqs, int seq_len, int n_threads) {
+    const int P = k * d_s + 1;
+    set_threads(n_threads);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int m = 0; m < n_maps; ++m) {
+        const double *Wm = W + (int64_t)m * P * d_t;
+        double *xt = (double *)malloc(sizeof(double) * (size_t)P);
+        for (int b = 0; b < n_seqs; ++b) {
+            for (int t = 0; t < seq_len; ++t) {
+                for (int i = 0; i < k; ++i) {
+                    const uint16_t *xr = src + row_offset(src_strides, src_layers[(int64_t)m * k + i], kv[m], b,
+                                                          src_head[m], t);
+                    for (int c = 0; c < d_s; ++c) xt[i * d_s + c] = bf16_bits_to_double(xr[c]);
+                }
+                xt[k * d_s] = 1.0;
+                uint16_t *orow = out + row_offset(out_strides, tgt_layer[m], kv[m], b, tgt_head[m], t);
+                for (int j = 0; j < d_t; ++j) {
+                    double s = 0.0;
+                    for (int p = 0; p < P; ++p) s += xt[p] * Wm[(int64_t)p * d_t + j];
                     orow[j] = oracle_double_to_bf16(s);
                 }
             }

@@ -22,6 +22,12 @@ Workloads (``WORKLOADS``):
 * ``mismatch`` -- src 26x8x96, tgt 40x4x128, src_head = 2h,
   src_layer = round(l*25/39); 200 seqs x 4096 tokens; w = exp(2z)/sqrt(t+1)
   mean-one.
+* ``tiny_k3`` -- multi-layer feature, k = 3: src 4x2x128, tgt 3x2x128,
+  S_l = 3 consecutive source layers (``window``), 3 seqs x 200 tokens, every
+  fourth token a calibration row (ragged tiles), P = 385.
+* ``qwen_k8`` -- the paper's Qwen3-14B->32B construction shape: k = 8
+  (P = 1025), 500 seqs x 1024 tokens, every fourth token (128,000 rows),
+  streamed as 5 batches of 100; sources and weights as ``qwen50``.
 * ``apply`` -- maps [1024][129][128] fp32 (planted, ``qwen`` statistics) applied
   to a sender cache of 8 x 32768 tokens x 40 layers x 8 heads x 128.
 
@@ -68,10 +74,12 @@ class Workload:
     weight_kind: str            # "lognormal" | "colmass" | "decay"
     lam_rel: float = 1e-2
     batch_seqs: Optional[int] = None   # streamed batch size (None = all at once)
+    k: int = 1                         # selected source layers per map (multi-layer feature)
+    sample_stride: int = 1             # calibration rows: tokens t with t % sample_stride == 0
 
     @property
     def P(self) -> int:
-        return self.d_s + 1
+        return self.k * self.d_s + 1
 
     @property
     def n_maps(self) -> int:
@@ -92,6 +100,14 @@ WORKLOADS: Dict[str, Workload] = {
                         batch_seqs=100),
     "mismatch": Workload("mismatch", 26, 8, 96, 40, 4, 128, 200, 4096, "mismatch", "scaled", 0.1, "decay"),
 }
+
+# Multi-layer feature (k selected source layers per target layer; the paper's
+# Qwen3 direction uses k = 8 over 500 sequences of 1,024 tokens sampled every
+# fourth token, 128,000 calibration rows).
+WORKLOADS["tiny_k3"] = Workload("tiny_k3", 4, 2, 128, 3, 2, 128, 3, 200, "window", "gauss", 0.05, "lognormal",
+                                k=3, sample_stride=4)
+WORKLOADS["qwen_k8"] = Workload("qwen_k8", 40, 8, 128, 64, 8, 128, 500, 1024, "window", "scaled", 0.1, "colmass",
+                                batch_seqs=100, k=8, sample_stride=4)
 
 # Online application workload: maps from the qwen shapes, sender 8 x 32768.
 APPLY = Workload("apply", 40, 8, 128, 64, 8, 128, 8, 32768, "qwen", "scaled", 0.1, "colmass")
@@ -142,6 +158,33 @@ def head_map(wl: Workload) -> Dict[str, np.ndarray]:
                 rows["kv"].append(z)
                 rows["src_layer"].append(sl)
                 rows["src_head"].append(sh)
+                rows["weight_row"].append(l * wl.H_t + h)
+    return {k: np.asarray(v, dtype=np.int32) for k, v in rows.items()}
+
+
+def layer_window(wl: Workload, l: int):
+    """S_l of the ``window`` head maps: the k consecutive source layers centred on
+    round(l (L_s - 1) / (L_t - 1)), clipped to the source model, ascending."""
+    c = _round_ratio(l, wl.L_s - 1, wl.L_t - 1) if wl.L_t > 1 else 0
+    start = min(max(c - wl.k // 2, 0), wl.L_s - wl.k)
+    return list(range(start, start + wl.k))
+
+
+def head_map_multi(wl: Workload) -> Dict[str, np.ndarray]:
+    """Multi-layer head map: per map (tgt_layer, tgt_head, kv, src_layers [k],
+    src_head, weight_row), int32; S_l from :func:`layer_window`, same head index."""
+    if wl.head_map_kind != "window":
+        raise ValueError(wl.head_map_kind)
+    rows = {k: [] for k in ("tgt_layer", "tgt_head", "kv", "src_layers", "src_head", "weight_row")}
+    for l in range(wl.L_t):
+        S = layer_window(wl, l)
+        for z in range(2):
+            for h in range(wl.H_t):
+                rows["tgt_layer"].append(l)
+                rows["tgt_head"].append(h)
+                rows["kv"].append(z)
+                rows["src_layers"].append(S)
+                rows["src_head"].append(h)
                 rows["weight_row"].append(l * wl.H_t + h)
     return {k: np.asarray(v, dtype=np.int32) for k, v in rows.items()}
 
@@ -207,14 +250,15 @@ def gen_source(wl: Workload, seq0: int = 0, n_seqs: Optional[int] = None, seq_le
 
 
 def planted_maps(wl: Workload, device="cpu") -> torch.Tensor:
-    """Planted affine maps [n_maps][P][d_t] fp32: rows 0..d_s-1 ~ N(0, 1/d_s), row d_s ~ N(0,1)."""
-    hm = head_map(wl)
+    """Planted affine maps [n_maps][P][d_t] fp32: rows 0..P-2 ~ N(0, 1/(P-1)), row P-1 ~ N(0,1)."""
+    hm = head_map(wl) if wl.head_map_kind != "window" else head_map_multi(wl)
     n = hm["kv"].shape[0]
+    p = wl.P - 1
     W = torch.empty((n, wl.P, wl.d_t), dtype=torch.float32, device=device)
     for m in range(n):
         gen = _gen(device, wl.name, "map", int(hm["tgt_layer"][m]), int(hm["kv"][m]), int(hm["tgt_head"][m]))
-        W[m, : wl.d_s] = torch.randn((wl.d_s, wl.d_t), generator=gen, device=device) / math.sqrt(wl.d_s)
-        W[m, wl.d_s] = torch.randn((wl.d_t,), generator=gen, device=device)
+        W[m, :p] = torch.randn((p, wl.d_t), generator=gen, device=device) / math.sqrt(p)
+        W[m, p] = torch.randn((wl.d_t,), generator=gen, device=device)
     return W
 
 
@@ -225,15 +269,18 @@ def gen_target(wl: Workload, src: torch.Tensor, seq0: int = 0, device="cpu",
     B, T = src.shape[2], src.shape[4]
     if out is None:
         out = torch.empty((wl.L_t, 2, B, wl.H_t, T, wl.d_t), dtype=torch.bfloat16, device=device)
-    hm = head_map(wl)
+    multi = wl.head_map_kind == "window"
+    hm = head_map_multi(wl) if multi else head_map(wl)
     W = planted_maps(wl, device=device)
+    p = wl.P - 1
     for m in range(hm["kv"].shape[0]):
         l, z, h = int(hm["tgt_layer"][m]), int(hm["kv"][m]), int(hm["tgt_head"][m])
-        sl, sh = int(hm["src_layer"][m]), int(hm["src_head"][m])
-        x = src[sl, z, :, sh].reshape(B * T, wl.d_s).to(torch.float32)
+        sh = int(hm["src_head"][m])
+        layers = [int(j) for j in hm["src_layers"][m]] if multi else [int(hm["src_layer"][m])]
+        x = torch.cat([src[j, z, :, sh].reshape(B * T, wl.d_s) for j in layers], dim=1).to(torch.float32)
         gen = _gen(device, wl.name, "noise", l, z, h, seq0, B, T)
         e = torch.randn((B * T, wl.d_t), generator=gen, device=device, dtype=torch.float32)
-        y = torch.addmm(W[m, wl.d_s].unsqueeze(0), x, W[m, : wl.d_s]).add_(e, alpha=wl.noise)
+        y = torch.addmm(W[m, p].unsqueeze(0), x, W[m, :p]).add_(e, alpha=wl.noise)
         out[l, z, :, h] = y.reshape(B, T, wl.d_t).to(torch.bfloat16)
     return out
 

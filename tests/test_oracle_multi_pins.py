@@ -1,0 +1,244 @@
+"""Pins for the multi-layer oracle functions (Sec. 3.2, Eq. localfeature with k
+selected source layers; calibration rows every ``sample_stride``-th token, Sec. 4.1).
+
+What pins what:
+
+* stats_multi  -- the explicit feature matrix X~ = [x_0 .. x_{k-1} 1] gathered by
+                  numpy slicing (``[::stride]``) and multiplied by numpy; exact
+                  small-integer brute force in Python integers; the diagonal
+                  blocks equal the (separately pinned) single-layer moments;
+                  reordering S_l permutes the blocks; sampling equals zero
+                  weights off the sampling grid.
+* solve at P = k d_s + 1 -- exact recovery of a planted integer multi-layer map.
+* apply_multi  -- a map that selects one layer copies its rows bit for bit; a
+                  pure bias gives RNE(b); numpy fp64 products rounded once.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+
+
+def to_bf16_bits(a) -> np.ndarray:
+    t = torch.as_tensor(np.asarray(a, dtype=np.float32)).to(torch.bfloat16)
+    return t.view(torch.int16).numpy().view(np.uint16)
+
+
+def relF(a, b):
+    return np.linalg.norm(np.asarray(a) - np.asarray(b)) / max(np.linalg.norm(np.asarray(b)), 1e-300)
+
+
+class MultiProblem:
+    """Small explicit multi-layer problem in the canonical cache layout."""
+
+    def __init__(self, rng, k=3, L_s=5, H_s=2, d_s=8, L_t=2, H_t=2, d_t=5, B=3, T=19, values="gauss"):
+        self.k, self.L_s, self.H_s, self.d_s, self.L_t, self.H_t, self.d_t, self.B, self.T = \
+            k, L_s, H_s, d_s, L_t, H_t, d_t, B, T
+        if values == "gauss":
+            xs = rng.standard_normal((L_s, 2, B, H_s, T, d_s)) * (1 + np.arange(L_s))[:, None, None, None, None, None]
+            ys = rng.standard_normal((L_t, 2, B, H_t, T, d_t)) + 2.0
+            w = np.exp(rng.standard_normal((L_t * H_t, B * T)))
+        else:
+            xs = rng.integers(-4, 5, size=(L_s, 2, B, H_s, T, d_s))
+            ys = rng.integers(-4, 5, size=(L_t, 2, B, H_t, T, d_t))
+            w = rng.integers(0, 4, size=(L_t * H_t, B * T))
+        self.src, self.tgt = to_bf16_bits(xs), to_bf16_bits(ys)
+        self.X, self.Y = oracle.bf16_to_double(self.src), oracle.bf16_to_double(self.tgt)
+        self.w = w.astype(np.float32)
+        hm = {f: [] for f in oracle.MULTI_MAP_FIELDS}
+        for l in range(L_t):
+            S = list(rng.permutation(L_s)[:k])             # distinct layers in an arbitrary order
+            for z in range(2):
+                for h in range(H_t):
+                    for f, v in zip(oracle.MULTI_MAP_FIELDS, (l, h, z, S, (h + 1) % H_s, l * H_t + h)):
+                        hm[f].append(v)
+        self.hm = {f: np.asarray(v, np.int32) for f, v in hm.items()}
+        self.ss = synth.cache_strides(L_s, H_s, B, T, d_s)
+        self.ts = synth.cache_strides(L_t, H_t, B, T, d_t)
+
+    @property
+    def n_maps(self):
+        return self.hm["kv"].shape[0]
+
+    def stats(self, stride, w=None, hm=None):
+        return oracle.stats_multi(self.hm if hm is None else hm, self.src, self.ss, self.d_s, self.tgt, self.ts,
+                                  self.d_t, self.w if w is None else w, self.B * self.T, self.B, self.T, stride)
+
+    def design(self, m, stride):
+        """X~ (n x P), Y (n x d_t), w (n) of map m on the sampled tokens, by numpy slicing."""
+        hm = self.hm
+        z, a = hm["kv"][m], hm["src_head"][m]
+        xs = [self.X[j, z, :, a, ::stride].reshape(-1, self.d_s) for j in hm["src_layers"][m]]
+        x = np.concatenate(xs + [np.ones((xs[0].shape[0], 1))], axis=1)
+        y = self.Y[hm["tgt_layer"][m], z, :, hm["tgt_head"][m], ::stride].reshape(-1, self.d_t)
+        w = self.w[hm["weight_row"][m]].reshape(self.B, self.T)[:, ::stride].reshape(-1).astype(np.float64)
+        return x, y, w
+
+
+@pytest.mark.parametrize("stride", [1, 3, 4])
+def test_multi_stats_equal_explicit_feature_matrix(stride):
+    p = MultiProblem(np.random.default_rng(101 + stride))
+    G, C = p.stats(stride)
+    P = p.k * p.d_s + 1
+    assert G.shape == (p.n_maps, P, P) and C.shape == (p.n_maps, P, p.d_t)
+    for m in range(p.n_maps):
+        x, y, w = p.design(m, stride)
+        assert relF(G[m], x.T @ (w[:, None] * x)) < 1e-13
+        assert relF(C[m], x.T @ (w[:, None] * y)) < 1e-13
+        assert G[m, P - 1, P - 1] == pytest.approx(w.sum(), rel=1e-14)
+
+
+def test_multi_stats_exact_integer_brute_force():
+    p = MultiProblem(np.random.default_rng(7), k=3, L_s=4, d_s=4, d_t=3, B=2, T=7, values="int")
+    stride = 2
+    G, C = p.stats(stride)
+    hm = p.hm
+    Xi = p.X.astype(np.int64)
+    Yi = p.Y.astype(np.int64)
+    wi = p.w.astype(np.int64)
+    for m in range(p.n_maps):
+        P = p.k * p.d_s + 1
+        Gb = [[0] * P for _ in range(P)]
+        Cb = [[0] * p.d_t for _ in range(P)]
+        z, a = int(hm["kv"][m]), int(hm["src_head"][m])
+        for b in range(p.B):
+            for t in range(0, p.T, stride):
+                xt = []
+                for j in hm["src_layers"][m]:
+                    xt += [int(v) for v in Xi[j, z, b, a, t]]
+                xt.append(1)
+                yv = [int(v) for v in Yi[hm["tgt_layer"][m], z, b, hm["tgt_head"][m], t]]
+                wv = int(wi[hm["weight_row"][m], b * p.T + t])
+                for r in range(P):
+                    for c in range(P):
+                        Gb[r][c] += wv * xt[r] * xt[c]
+                    for c in range(p.d_t):
+                        Cb[r][c] += wv * xt[r] * yv[c]
+        assert np.array_equal(G[m], np.asarray(Gb, np.float64))
+        assert np.array_equal(C[m], np.asarray(Cb, np.float64))
+
+
+def test_multi_stats_sampling_equals_zero_weights_off_the_grid():
+    p = MultiProblem(np.random.default_rng(3), T=21)
+    stride = 4
+    w0 = p.w.copy().reshape(-1, p.B, p.T)
+    w0[:, :, np.arange(p.T) % stride != 0] = 0.0
+    G1, C1 = p.stats(stride)
+    G2, C2 = p.stats(1, w=w0.reshape(p.w.shape))
+    assert np.array_equal(G1, G2) and np.array_equal(C1, C2)
+
+
+def test_multi_stats_diagonal_blocks_are_single_layer_moments():
+    p = MultiProblem(np.random.default_rng(5))
+    stride = 3
+    G, C = p.stats(stride)
+    ds, P = p.d_s, p.k * p.d_s + 1
+    w0 = p.w.copy().reshape(-1, p.B, p.T)
+    w0[:, :, np.arange(p.T) % stride != 0] = 0.0
+    for i in range(p.k):
+        hm1 = {f: p.hm[f] for f in ("tgt_layer", "tgt_head", "kv", "src_head", "weight_row")}
+        hm1["src_layer"] = p.hm["src_layers"][:, i]
+        G1, C1 = oracle.stats(hm1, p.src, p.ss, ds, p.tgt, p.ts, p.d_t, w0.reshape(p.w.shape), p.B * p.T, p.B, p.T)
+        blk = slice(i * ds, (i + 1) * ds)
+        np.testing.assert_allclose(G[:, blk, blk], G1[:, :ds, :ds], rtol=1e-13, atol=1e-12)
+        np.testing.assert_allclose(G[:, blk, P - 1], G1[:, :ds, ds], rtol=1e-13, atol=1e-12)
+        np.testing.assert_allclose(C[:, blk, :], C1[:, :ds, :], rtol=1e-13, atol=1e-12)
+        np.testing.assert_allclose(C[:, P - 1, :], C1[:, ds, :], rtol=1e-13, atol=1e-12)
+
+
+def test_multi_stats_layer_order_permutes_blocks():
+    p = MultiProblem(np.random.default_rng(9))
+    G, C = p.stats(2)
+    perm = [2, 0, 1]
+    hm2 = dict(p.hm)
+    hm2["src_layers"] = p.hm["src_layers"][:, perm]
+    G2, C2 = p.stats(2, hm=hm2)
+    ds = p.d_s
+    idx = np.concatenate([np.arange(i * ds, (i + 1) * ds) for i in perm] + [np.asarray([p.k * ds])])
+    assert np.array_equal(G2, G[:, idx][:, :, idx])
+    assert np.array_equal(C2, C[:, idx])
+
+
+def test_multi_solve_recovers_planted_integer_map():
+    rng = np.random.default_rng(17)
+    k, d_s, d_t, L_s, B, T, stride = 3, 4, 3, 4, 4, 64, 2
+    x = rng.integers(-4, 5, size=(L_s, 2, B, 1, T, d_s)).astype(np.float64)
+    S = [3, 0, 2]
+    Wstar = rng.integers(-2, 3, size=(k * d_s + 1, d_t)).astype(np.float64)
+    feat = np.concatenate([x[j, 0, :, 0].reshape(-1, d_s) for j in S] + [np.ones((B * T, 1))], axis=1)
+    y = (feat @ Wstar).reshape(1, 1, B, 1, T, d_t)                # integers below 256: exact in bf16
+    y = np.concatenate([y, y], axis=1)
+    hm = {"tgt_layer": [0], "tgt_head": [0], "kv": [0], "src_layers": [S], "src_head": [0], "weight_row": [0]}
+    w = np.exp(rng.standard_normal((1, B * T))).astype(np.float32)
+    G, C = oracle.stats_multi(hm, to_bf16_bits(x), synth.cache_strides(L_s, 1, B, T, d_s), d_s, to_bf16_bits(y),
+                              synth.cache_strides(1, 1, B, T, d_t), d_t, w, B * T, B, T, stride)
+    for unpen in (False, True):
+        W, info = oracle.ridge_solve(G, C, 1e-13, relative=True, bias_unpenalized=unpen)
+        assert info[0] == 0
+        np.testing.assert_allclose(W[0], Wstar, rtol=0, atol=1e-8)
+
+
+def _apply_setup(rng, k=3, L_s=4, d_s=8, d_t=8, B=2, T=9):
+    x = rng.standard_normal((L_s, 2, B, 1, T, d_s)) * 3.0
+    src = to_bf16_bits(x)
+    hm = {"tgt_layer": [0, 0], "tgt_head": [0, 0], "kv": [0, 1], "src_layers": [[1, 3, 0], [2, 0, 1]],
+          "src_head": [0, 0], "weight_row": [0, 0]}
+    hm = {f: np.asarray(v, np.int32) for f, v in hm.items()}
+    return src, hm, synth.cache_strides(L_s, 1, B, T, d_s), synth.cache_strides(1, 1, B, T, d_t)
+
+
+def test_multi_apply_layer_selector_copies_bits_and_bias_rounds():
+    rng = np.random.default_rng(21)
+    k, d = 3, 8
+    src, hm, ss, os_ = _apply_setup(rng)
+    P = k * d + 1
+    for sel in range(k):
+        W = np.zeros((2, P, d))
+        W[:, sel * d:(sel + 1) * d] = np.eye(d)
+        out = np.zeros((1, 2, 2, 1, 9, d), np.uint16)
+        oracle.apply_multi(hm, W, src, ss, d, out, os_, d, 2, 9)
+        for m in range(2):
+            j = hm["src_layers"][m][sel]
+            assert np.array_equal(out[0, hm["kv"][m], :, 0], src[j, hm["kv"][m], :, 0])
+    W = np.zeros((2, P, d))
+    b = rng.standard_normal((2, d)) * 10
+    W[:, P - 1] = b
+    out = np.zeros((1, 2, 2, 1, 9, d), np.uint16)
+    oracle.apply_multi(hm, W, src, ss, d, out, os_, d, 2, 9)
+    for m in range(2):
+        assert np.array_equal(out[0, m], np.broadcast_to(oracle.double_to_bf16(b[m]), (2, 1, 9, d)))
+
+
+def test_multi_apply_matches_fp64_products():
+    rng = np.random.default_rng(23)
+    k, d = 3, 8
+    src, hm, ss, os_ = _apply_setup(rng)
+    X = oracle.bf16_to_double(src)
+    W = rng.standard_normal((2, k * d + 1, d))
+    out = np.zeros((1, 2, 2, 1, 9, d), np.uint16)
+    oracle.apply_multi(hm, W, src, ss, d, out, os_, d, 2, 9)
+    for m in range(2):
+        z = hm["kv"][m]
+        feat = np.concatenate([X[j, z, :, 0].reshape(-1, d) for j in hm["src_layers"][m]] +
+                              [np.ones((18, 1))], axis=1)
+        ref = oracle.double_to_bf16(feat @ W[m]).reshape(2, 1, 9, d)
+        got = out[0, z]
+        same = np.mean(got == ref)
+        assert same >= 0.995
+        ulp = np.abs(oracle.bf16_to_double(got) - oracle.bf16_to_double(ref))
+        assert np.all(ulp <= np.abs(oracle.bf16_to_double(ref)) * 2.0 ** -7 + 1e-30)
+
+
+def test_qwen_k8_workload_shape_and_windows():
+    wl = synth.WORKLOADS["qwen_k8"]
+    hm = synth.head_map_multi(wl)
+    assert wl.P == 1025 and hm["src_layers"].shape == (1024, 8)
+    assert wl.n_seqs * (wl.seq_len // wl.sample_stride) == 128_000       # Sec. 4.1: 500 x 1,024 / 4
+    for S in hm["src_layers"]:
+        assert len(set(S.tolist())) == 8 and S.min() >= 0 and S.max() < wl.L_s
+    # the window is centred on round(l * 39 / 63)
+    for l in range(wl.L_t):
+        S = synth.layer_window(wl, l)
+        assert S[0] <= (2 * l * 39 + 63) // 126 <= S[-1]
