@@ -33,6 +33,10 @@
  *
  *   cb_rope_table, cb_rope
  *
+ * and the multi-layer feature of Sec. 3.2 (k selected source layers per map):
+ *
+ *   cb_plan_create_multi, cb_plan_feature_width, cb_ridge_solve_ws
+ *
  * Conventions shared by every call
  * --------------------------------
  * - Row vectors: a map is W~ = [W ; b^T], a P x d_t fp32 matrix with
@@ -195,7 +199,8 @@ cb_status cb_stats_accumulate(cb_plan *plan, const cb_cache *src, const cb_cache
  * definite G + lambda_m D its pivots are the squared diagonal of the Cholesky
  * factor.  info[m] = 0 on success, else the 1-based index of the first pivot
  * that is not positive and finite (the column where Cholesky would stop), and
- * maps[m] is zero-filled.  P in {65, 97, 129}, d_t in {64, 96, 128}.
+ * maps[m] is zero-filled.  P in {65, 97, 129}, d_t in {64, 96, 128}; wider
+ * systems return CB_ERR_UNSUPPORTED (use cb_ridge_solve_ws).
  */
 cb_status cb_ridge_solve(int32_t n_maps, int32_t P, int32_t d_t, const float *G, const float *C,
                          float lambda, uint32_t flags, float *maps, int32_t *info, void *stream);
@@ -387,6 +392,70 @@ cb_status cb_rope(const cb_cache *in, const cb_cache *out, const float *table, i
  */
 cb_status cb_apply(cb_plan *plan, const float *maps, const cb_cache *src, const cb_cache *tgt_out,
                    void *stream);
+
+/*
+ * Multi-layer mapper support (Sec. 3.2, Eq. localfeature with k selected
+ * source layers S_l, chosen for instance by cb_select_layers): map m predicts
+ * target (tgt_layer[m], tgt_head[m], kv[m]) from the source rows of layers
+ * src_layers[m*k + 0], ..., src_layers[m*k + k-1] (distinct, in that order)
+ * at head src_head[m] and the same component, concatenated:
+ *   x~ = [ x_0 ; x_1 ; ... ; x_{k-1} ; 1 ]      (P = k d_s + 1)
+ * maps[m] is then a P x d_t fp32 matrix whose rows i d_s .. (i+1) d_s - 1 act
+ * on x_i and whose last row is the bias.  Host arrays, read by
+ * cb_plan_create_multi only.
+ */
+typedef struct {
+    int32_t n_maps;
+    int32_t k;
+    const int32_t *tgt_layer;
+    const int32_t *tgt_head;
+    const int32_t *kv;
+    const int32_t *src_layers;  /* [n_maps][k] */
+    const int32_t *src_head;
+    const int32_t *weight_row;
+} cb_head_map_multi;
+
+/*
+ * Plan for multi-layer maps (1 <= k <= 32, d_s = d_t = 128).  The calibration
+ * rows of every cb_stats_accumulate call on this plan are the tokens tok with
+ * tok mod sample_stride == 0 of every sequence (Sec. 4.1 samples every fourth
+ * token); other tokens are never read.  With such a plan, cb_stats_zero and
+ * cb_stats_accumulate compute G [n_maps][P][P] and C [n_maps][P][d_t] for the
+ * multi-layer feature, with the arguments, accuracy and symmetry of the
+ * single-layer calls and no token limit; the products run on the matrix cores
+ * (the work grows as P^2 per row).  G and C must not overlap other buffers of
+ * the call.  Solve with cb_ridge_solve_ws.  The centered calls and cb_apply
+ * return CB_ERR_UNSUPPORTED for such a plan.  Errors as in cb_plan_create,
+ * plus CB_ERR_INVALID_ARGUMENT for a source layer selected twice by one map.
+ */
+cb_status cb_plan_create_multi(const cb_head_map_multi *map, const cb_cache *src_geom, const cb_cache *tgt_geom,
+                               int32_t sample_stride, cb_plan **out);
+
+/*
+ * Batched ridge solve for any feature width (Sec. 3.1, Eq. closedform; the
+ * multi-layer feature of Sec. 3.2 gives P = k d_s + 1):  maps[m] =
+ * (G[m] + lambda_m D)^{-1} C[m], with the arrays, flags, lambda_m and info of
+ * cb_ridge_solve (G symmetric).  P <= 129 runs cb_ridge_solve and ignores the
+ * workspace.  Otherwise (P <= 4097, d_t in {64, 96, 128}) each system is
+ * factored in fp64 in `workspace` (device memory owned by the caller, 8-byte
+ * aligned, at least cb_ridge_solve_workspace_bytes(P, d_t, 1) bytes): a
+ * left-looking blocked Cholesky M = L L^T in 32-column panels, then the
+ * forward and back substitutions for the d_t right-hand sides, one workgroup
+ * of 256 threads per system; the systems are processed in batches of
+ * workspace_bytes / cb_ridge_solve_workspace_bytes(P, d_t, 1).  info[m] = 0, or
+ * the 1-based column of the first pivot that is not positive and finite
+ * (maps[m] zero-filled).  Errors: CB_ERR_SHAPE (workspace too small), else as
+ * cb_ridge_solve.
+ */
+cb_status cb_ridge_solve_ws(int32_t n_maps, int32_t P, int32_t d_t, const float *G, const float *C, float lambda,
+                            uint32_t flags, void *workspace, int64_t workspace_bytes, float *maps, int32_t *info,
+                            void *stream);
+
+/* Workspace bytes cb_ridge_solve_ws needs to solve n_systems systems at once (0 for P <= 129). */
+int64_t cb_ridge_solve_workspace_bytes(int32_t P, int32_t d_t, int32_t n_systems);
+
+/* Feature width P of a plan's maps (d_s + 1, or k d_s + 1) and its k. */
+cb_status cb_plan_feature_width(const cb_plan *plan, int32_t *P, int32_t *k);
 
 /* Static name of a status code. */
 const char *cb_status_string(cb_status status);

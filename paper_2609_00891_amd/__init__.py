@@ -21,6 +21,9 @@ current HIP stream.  The functions keep the C names:
   ESS-floor shrinkage (Sec. 3.3)
 * :func:`cb_rope_table`, :func:`cb_rope` -- rotary position transform of cached
   keys (RoPE removed before fitting, restored after mapping; Sec. 2.1, 3.1)
+* :func:`cb_plan_create_multi`, :func:`cb_ridge_solve_ws` -- maps over the
+  multi-layer feature of k selected source layers (Sec. 3.2, Eq. localfeature)
+  and the blocked solve of their P = k d_s + 1 systems
 
 Caches are bfloat16 tensors indexed ``[layer][kv][seq][head][tok][dim]`` (any
 strides with a unit channel stride).  Importing this package fails if the
@@ -69,6 +72,13 @@ class CbHeadMap(ctypes.Structure):
     _fields_ = [("n_maps", ctypes.c_int32)] + [(f, _i32p) for f in HEAD_MAP_FIELDS]
 
 
+MULTI_MAP_FIELDS = ("tgt_layer", "tgt_head", "kv", "src_layers", "src_head", "weight_row")
+
+
+class CbHeadMapMulti(ctypes.Structure):
+    _fields_ = [("n_maps", ctypes.c_int32), ("k", ctypes.c_int32)] + [(f, _i32p) for f in MULTI_MAP_FIELDS]
+
+
 class CacheBridgeError(RuntimeError):
     def __init__(self, status: int, message: str):
         self.status = status
@@ -85,6 +95,11 @@ _lib.cb_plan_create.argtypes = [ctypes.POINTER(CbHeadMap), ctypes.POINTER(CbCach
                                 ctypes.c_int64, ctypes.POINTER(_vp)]
 _lib.cb_plan_destroy.restype = ctypes.c_int
 _lib.cb_plan_destroy.argtypes = [_vp]
+_lib.cb_plan_create_multi.restype = ctypes.c_int
+_lib.cb_plan_create_multi.argtypes = [ctypes.POINTER(CbHeadMapMulti), ctypes.POINTER(CbCache),
+                                      ctypes.POINTER(CbCache), ctypes.c_int32, ctypes.POINTER(_vp)]
+_lib.cb_plan_feature_width.restype = ctypes.c_int
+_lib.cb_plan_feature_width.argtypes = [_vp, _i32p, _i32p]
 _lib.cb_plan_shape.restype = ctypes.c_int
 _lib.cb_plan_shape.argtypes = [_vp, _i32p, _i32p, _i32p]
 _lib.cb_stats_zero.restype = ctypes.c_int
@@ -95,6 +110,11 @@ _lib.cb_stats_accumulate.argtypes = [_vp, ctypes.POINTER(CbCache), ctypes.POINTE
 _lib.cb_ridge_solve.restype = ctypes.c_int
 _lib.cb_ridge_solve.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp, _vp, ctypes.c_float,
                                 ctypes.c_uint32, _vp, _vp, _vp]
+_lib.cb_ridge_solve_ws.restype = ctypes.c_int
+_lib.cb_ridge_solve_ws.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp, _vp, ctypes.c_float,
+                                   ctypes.c_uint32, _vp, ctypes.c_int64, _vp, _vp, _vp]
+_lib.cb_ridge_solve_workspace_bytes.restype = ctypes.c_int64
+_lib.cb_ridge_solve_workspace_bytes.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]
 _lib.cb_stats_zero_centered.restype = ctypes.c_int
 _lib.cb_stats_zero_centered.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp]
 _lib.cb_stats_means.restype = ctypes.c_int
@@ -180,10 +200,11 @@ def cache_view(t: Optional[torch.Tensor], n_layers=None, n_heads=None, head_dim=
 class Plan:
     """Owning handle of a cb_plan (validated head map, gather schedule, workspace)."""
 
-    def __init__(self, handle: int, n_maps: int, d_s: int, d_t: int, keep):
+    def __init__(self, handle: int, n_maps: int, d_s: int, d_t: int, keep, P: Optional[int] = None, k: int = 1):
         self.handle = handle
         self.n_maps, self.d_s, self.d_t = n_maps, d_s, d_t
-        self.P = d_s + 1
+        self.P = d_s + 1 if P is None else P
+        self.k = k
         self._keep = keep
 
     def close(self):
@@ -224,6 +245,38 @@ def cb_plan_create(head_map: Mapping[str, object], src_geom, tgt_geom, max_token
     return Plan(out.value, nm.value, ds.value, dt.value, arrays)
 
 
+def cb_plan_create_multi(head_map: Mapping[str, object], src_geom, tgt_geom, sample_stride: int = 1) -> Plan:
+    """Compile a multi-layer head map (``src_layers`` is [n_maps][k]; the other
+    five fields as in :func:`cb_plan_create`).  Calibration rows are the tokens
+    ``tok % sample_stride == 0``."""
+    import numpy as np  # noqa: PLC0415
+
+    arrays = [np.ascontiguousarray(np.asarray(head_map[f], dtype=np.int32)) for f in MULTI_MAP_FIELDS]
+    n = arrays[0].shape[0]
+    S = arrays[MULTI_MAP_FIELDS.index("src_layers")]
+    if S.ndim != 2 or S.shape[0] != n:
+        raise ValueError("src_layers must be [n_maps][k]")
+    hm = CbHeadMapMulti()
+    hm.n_maps, hm.k = n, S.shape[1]
+    for f, a in zip(MULTI_MAP_FIELDS, arrays):
+        setattr(hm, f, a.ctypes.data_as(_i32p))
+
+    def geom(g):
+        if isinstance(g, torch.Tensor):
+            return cache_view(g)
+        return cache_view(None, *g)
+
+    sg, tg = geom(src_geom), geom(tgt_geom)
+    out = _vp()
+    _check(_lib.cb_plan_create_multi(ctypes.byref(hm), ctypes.byref(sg), ctypes.byref(tg), int(sample_stride),
+                                     ctypes.byref(out)))
+    nm, ds, dt = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    _check(_lib.cb_plan_shape(out.value, ctypes.byref(nm), ctypes.byref(ds), ctypes.byref(dt)))
+    P, k = ctypes.c_int32(), ctypes.c_int32()
+    _check(_lib.cb_plan_feature_width(out.value, ctypes.byref(P), ctypes.byref(k)))
+    return Plan(out.value, nm.value, ds.value, dt.value, arrays, P=P.value, k=k.value)
+
+
 def cb_plan_destroy(plan: Plan):
     plan.close()
 
@@ -254,6 +307,25 @@ def cb_ridge_solve(G: torch.Tensor, C: torch.Tensor, lam: float, flags: int, map
         raise ValueError("info is int32")
     _check(_lib.cb_ridge_solve(n, P, C.shape[2], _ptr(G), _ptr(C), float(lam), int(flags), _ptr(maps), _ptr(info),
                                _stream(stream)))
+
+
+def cb_ridge_solve_workspace_bytes(P: int, d_t: int, n_systems: int) -> int:
+    """Workspace bytes :func:`cb_ridge_solve_ws` needs for n_systems systems at once (0 if P <= 129)."""
+    return int(_lib.cb_ridge_solve_workspace_bytes(int(P), int(d_t), int(n_systems)))
+
+
+def cb_ridge_solve_ws(G: torch.Tensor, C: torch.Tensor, lam: float, flags: int, maps: torch.Tensor,
+                      info: torch.Tensor, workspace: Optional[torch.Tensor], stream=None):
+    """maps[m] = (G[m] + lambda_m D)^-1 C[m] for any P; the blocked fp64 solve (P > 129)
+    factors in ``workspace`` (a device tensor of at least cb_ridge_solve_workspace_bytes(P, d_t, 1) bytes)."""
+    n, P, P2 = G.shape
+    if P != P2 or C.shape[:2] != (n, P) or maps.shape != C.shape or info.shape != (n,):
+        raise ValueError("G [n][P][P], C/maps [n][P][d_t], info [n]")
+    if info.dtype != torch.int32:
+        raise ValueError("info is int32")
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(_lib.cb_ridge_solve_ws(n, P, C.shape[2], _ptr(G), _ptr(C), float(lam), int(flags), _ptr(workspace),
+                                  int(ws_bytes), _ptr(maps), _ptr(info), _stream(stream)))
 
 
 def _row_stride(weights: torch.Tensor, w_row_stride: Optional[int]) -> int:

@@ -26,6 +26,11 @@ struct cb_plan {
     int32_t n_maps = 0, L_s = 0, H_s = 0, d_s = 0, L_t = 0, H_t = 0, d_t = 0;
     int64_t max_tokens = 0;
     bool duplicate_targets = false;   // some target (layer, kv, head) has several maps (probes)
+    // multi-layer feature (cb_plan_create_multi): k source layers per map
+    bool multi = false;
+    int32_t k = 1, P = 0, sample_stride = 1;
+    int32_t n_tasks = 0;
+    cb::MultiTask *d_tasks = nullptr;
     // statistics schedule
     int32_t n_items = 0;
     int32_t max_chunks = 1;
@@ -156,6 +161,63 @@ cb_status prepare_stats(const cb_plan *p, const cb_cache *src, const cb_cache *t
     return CB_OK;
 }
 
+cb_status single_layer_only(const cb_plan *p, const char *call) {
+    if (p->multi)
+        return fail(CB_ERR_UNSUPPORTED, "%s takes plans of single-layer maps (cb_plan_create), not multi-layer ones", call);
+    return CB_OK;
+}
+
+// Validation and launch arguments of a multi-layer statistics call.
+cb_status prepare_multi(const cb_plan *p, const cb_cache *src, const cb_cache *tgt, const float *weights,
+                        int64_t w_row_stride, cb::MultiArgs &a, bool &empty) {
+    if (cb_status s = check_cache("src", src, p->L_s, p->H_s, p->d_s)) return s;
+    if (cb_status s = check_cache("tgt", tgt, p->L_t, p->H_t, p->d_t)) return s;
+    if (src->n_seqs != tgt->n_seqs || src->seq_len != tgt->seq_len)
+        return fail(CB_ERR_SHAPE, "src and tgt disagree on n_seqs / seq_len");
+    const int64_t N = (int64_t)src->n_seqs * src->seq_len;
+    empty = N == 0;
+    if (empty) return CB_OK;
+    if (!weights) return fail(CB_ERR_INVALID_ARGUMENT, "weights is NULL");
+    if (w_row_stride < N) return fail(CB_ERR_SHAPE, "w_row_stride (%lld) < tokens in the call (%lld)",
+                                      (long long)w_row_stride, (long long)N);
+    if (((uintptr_t)weights) % 4) return fail(CB_ERR_MISALIGNED, "weights must be 4-byte aligned");
+    if (cb_status s = check_device(p)) return s;
+    const int64_t KT = cb::kMultiTileRows;
+    const int64_t rows = (src->seq_len + p->sample_stride - 1) / p->sample_stride;
+    const int64_t tps = (rows + KT - 1) / KT;
+    const int64_t tiles = (int64_t)src->n_seqs * tps;
+    if (tiles > INT32_MAX - 2) return fail(CB_ERR_UNSUPPORTED, "too many row tiles in one call");
+    const int64_t step = (int64_t)p->sample_stride * 2 * KT;
+    if (src->s_tok * step >= (1LL << 31) || tgt->s_tok * step >= (1LL << 31))
+        return fail(CB_ERR_UNSUPPORTED, "token stride x sample_stride too large (16 rows must span < 2 GiB)");
+    a.src = (const uint16_t *)src->data;
+    a.tgt = (const uint16_t *)tgt->data;
+    a.w = weights;
+    a.ss = strides_of(src);
+    a.ts = strides_of(tgt);
+    a.w_row_stride = w_row_stride;
+    a.seq_len = (uint32_t)src->seq_len;
+    a.stride = (uint32_t)p->sample_stride;
+    a.rows_per_seq = (uint32_t)rows;
+    a.TPS = cb::make_fastdiv((uint32_t)tps);
+    a.n_tiles = (int32_t)tiles;
+    {   // flush at most every kMultiFlushTiles tiles, at an even tile count
+        const int64_t iters = (tiles + 1) & ~1LL;
+        const int64_t nf = (iters + cb::kMultiFlushTiles - 1) / cb::kMultiFlushTiles;
+        int64_t ct = (iters + nf - 1) / nf;
+        ct = (ct + 1) & ~1LL;
+        a.chunk_tiles = (int32_t)ct;
+    }
+    a.n_tasks = p->n_tasks;
+    a.per_xcd = (p->n_tasks + 7) / 8;
+    a.k = p->k;
+    a.P = p->P;
+    a.d_t = p->d_t;
+    a.tasks = p->d_tasks;
+    a.zero = p->d_zero;
+    return CB_OK;
+}
+
 cb::ReduceArgs reduce_args(const cb_plan *p, const cb::StatsArgs &a) {
     cb::ReduceArgs r = {};
     r.partials = p->d_partials;
@@ -198,6 +260,7 @@ cb_status cb_plan_destroy(cb_plan *p) {
     hipFree(p->d_whi);
     hipFree(p->d_wlo);
     hipFree(p->d_bias);
+    hipFree(p->d_tasks);
     delete p;
     return ok();
 }
@@ -247,6 +310,7 @@ cb_status cb_plan_create(const cb_head_map *map, const cb_cache *src_geom, const
     p->L_t = L_t; p->H_t = H_t; p->d_t = d_t;
     p->max_tokens = max_tokens_per_call;
     p->duplicate_targets = duplicate;
+    p->P = d_s + 1;
 
     // ---- group maps by source block, in order of first appearance
     std::map<std::tuple<int, int, int>, int> gid;
@@ -359,6 +423,137 @@ cb_status cb_plan_create(const cb_head_map *map, const cb_cache *src_geom, const
     return ok();
 }
 
+cb_status cb_plan_create_multi(const cb_head_map_multi *map, const cb_cache *src_geom, const cb_cache *tgt_geom,
+                               int32_t sample_stride, cb_plan **out) {
+    if (!out) return fail(CB_ERR_INVALID_ARGUMENT, "out is NULL");
+    *out = nullptr;
+    if (!map || !src_geom || !tgt_geom) return fail(CB_ERR_INVALID_ARGUMENT, "map, src_geom and tgt_geom must be non-NULL");
+    if (map->n_maps <= 0) return fail(CB_ERR_INVALID_ARGUMENT, "n_maps must be positive (got %d)", map->n_maps);
+    if (map->k < 1 || map->k > 32) return fail(CB_ERR_UNSUPPORTED, "k must be in 1..32 (got %d)", map->k);
+    if (!map->tgt_layer || !map->tgt_head || !map->kv || !map->src_layers || !map->src_head || !map->weight_row)
+        return fail(CB_ERR_INVALID_ARGUMENT, "every head map array must be non-NULL");
+    if (sample_stride < 1) return fail(CB_ERR_INVALID_ARGUMENT, "sample_stride must be >= 1 (got %d)", sample_stride);
+    const int L_s = src_geom->n_layers, H_s = src_geom->n_heads, d_s = src_geom->head_dim;
+    const int L_t = tgt_geom->n_layers, H_t = tgt_geom->n_heads, d_t = tgt_geom->head_dim;
+    if (L_s <= 0 || H_s <= 0 || L_t <= 0 || H_t <= 0) return fail(CB_ERR_SHAPE, "layer and head counts must be positive");
+    if (d_s != 128 || d_t != 128)
+        return fail(CB_ERR_UNSUPPORTED, "multi-layer maps need d_s = d_t = 128 (got d_s=%d, d_t=%d)", d_s, d_t);
+    const int n = map->n_maps, k = map->k;
+    std::set<std::tuple<int, int, int>> targets;
+    bool duplicate = false;
+    for (int m = 0; m < n; ++m) {
+        const int tl = map->tgt_layer[m], th = map->tgt_head[m], z = map->kv[m];
+        const int sh = map->src_head[m], wr = map->weight_row[m];
+        if (tl < 0 || tl >= L_t || th < 0 || th >= H_t)
+            return fail(CB_ERR_INVALID_ARGUMENT, "map %d: target (%d, %d) outside %d x %d", m, tl, th, L_t, H_t);
+        if (sh < 0 || sh >= H_s) return fail(CB_ERR_INVALID_ARGUMENT, "map %d: source head %d outside %d", m, sh, H_s);
+        if (z != 0 && z != 1) return fail(CB_ERR_INVALID_ARGUMENT, "map %d: kv must be 0 or 1 (got %d)", m, z);
+        if (wr < 0) return fail(CB_ERR_INVALID_ARGUMENT, "map %d: negative weight row", m);
+        std::set<int> seen;
+        for (int i = 0; i < k; ++i) {
+            const int sl = map->src_layers[(int64_t)m * k + i];
+            if (sl < 0 || sl >= L_s) return fail(CB_ERR_INVALID_ARGUMENT, "map %d: source layer %d outside %d", m, sl, L_s);
+            if (!seen.insert(sl).second)
+                return fail(CB_ERR_INVALID_ARGUMENT, "map %d: source layer %d selected twice", m, sl);
+        }
+        if (!targets.insert(std::make_tuple(tl, z, th)).second) duplicate = true;
+    }
+
+    cb_plan *p = new cb_plan();
+    if (hipGetDevice(&p->device) != hipSuccess) {
+        delete p;
+        return fail(CB_ERR_DEVICE, "hipGetDevice failed (no HIP device?)");
+    }
+    int ncu = 0;
+    if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, p->device) == hipSuccess && ncu > 0)
+        p->n_cu = ncu;
+    p->n_maps = n;
+    p->L_s = L_s; p->H_s = H_s; p->d_s = d_s;
+    p->L_t = L_t; p->H_t = H_t; p->d_t = d_t;
+    p->max_tokens = INT64_MAX;
+    p->duplicate_targets = duplicate;
+    p->multi = true;
+    p->k = k;
+    p->P = k * d_s + 1;
+    p->sample_stride = sample_stride;
+
+    // ---- statistics tasks.  Maps are visited by (kv, source head, target
+    // layer, target head): neighbouring maps then read mostly the same source
+    // blocks, and the kernel hands each XCD a contiguous run of tasks.  Row
+    // block i of a map pairs with column blocks i..k-1 and the target block k,
+    // cut into parts of at most four blocks of near-equal size.
+    std::vector<int> order(n);
+    for (int m = 0; m < n; ++m) order[m] = m;
+    std::stable_sort(order.begin(), order.end(), [&](int a, int b) {
+        return std::make_tuple(map->kv[a], map->src_head[a], map->tgt_layer[a], map->tgt_head[a]) <
+               std::make_tuple(map->kv[b], map->src_head[b], map->tgt_layer[b], map->tgt_head[b]);
+    });
+    std::vector<cb::MultiTask> tasks;
+    for (int m : order) {
+        const int32_t *S = map->src_layers + (int64_t)m * k;
+        for (int i = 0; i < k; ++i) {
+            const int ncol = k - i + 1;
+            const int parts = (ncol + 3) / 4;
+            int col = i;
+            for (int pt = 0; pt < parts; ++pt) {
+                const int sz = ncol / parts + (pt < ncol % parts ? 1 : 0);
+                cb::MultiTask t = {};
+                t.map = m;
+                t.row_blk = i;
+                t.n_cols = sz;
+                t.wrow = map->weight_row[m];
+                t.kv = map->kv[m];
+                t.tgt_layer = map->tgt_layer[m];
+                t.tgt_head = map->tgt_head[m];
+                t.src_head = map->src_head[m];
+                t.slot_layer[0] = S[i];
+                t.n_lds = 1;
+                for (int b = 0; b < 4; ++b) {
+                    t.col_blk[b] = i;
+                    t.col_slot[b] = 0;
+                }
+                for (int b = 0; b < sz; ++b, ++col) {
+                    t.col_blk[b] = col;
+                    if (col == i) {
+                        t.col_slot[b] = 0;
+                        t.flags |= 1;
+                        if (i == 0) t.flags |= 4;
+                    } else {
+                        t.col_slot[b] = t.n_lds;
+                        t.slot_layer[t.n_lds++] = col < k ? S[col] : -1;
+                    }
+                    if (col == k && i == 0) t.flags |= 2;   // one owner of sum w y per map
+                }
+                for (int s = t.n_lds; s < 5; ++s) t.slot_layer[s] = S[i];
+                tasks.push_back(t);
+            }
+        }
+    }
+    p->n_tasks = (int32_t)tasks.size();
+
+    bool okm = hipMalloc(&p->d_tasks, sizeof(cb::MultiTask) * tasks.size()) == hipSuccess &&
+               hipMalloc(&p->d_zero, 256) == hipSuccess;
+    if (!okm) {
+        (void)hipGetLastError();
+        cb_plan_destroy(p);
+        return fail(CB_ERR_OUT_OF_MEMORY, "plan allocation failed");
+    }
+    if (hipMemset(p->d_zero, 0, 256) != hipSuccess ||
+        hipMemcpy(p->d_tasks, tasks.data(), sizeof(cb::MultiTask) * tasks.size(), hipMemcpyHostToDevice) != hipSuccess) {
+        cb_plan_destroy(p);
+        return fail(CB_ERR_DEVICE, "copying the schedule to the device failed");
+    }
+    *out = p;
+    return ok();
+}
+
+cb_status cb_plan_feature_width(const cb_plan *p, int32_t *P, int32_t *k) {
+    if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
+    if (P) *P = p->P;
+    if (k) *k = p->k;
+    return ok();
+}
+
 cb_status cb_plan_shape(const cb_plan *p, int32_t *n_maps, int32_t *d_s, int32_t *d_t) {
     if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
     if (n_maps) *n_maps = p->n_maps;
@@ -370,7 +565,7 @@ cb_status cb_plan_shape(const cb_plan *p, int32_t *n_maps, int32_t *d_s, int32_t
 cb_status cb_stats_zero(const cb_plan *p, float *G, float *C, void *stream) {
     if (!p || !G || !C) return fail(CB_ERR_INVALID_ARGUMENT, "plan, G and C must be non-NULL");
     if (cb_status s = check_device(p)) return s;
-    const int P = p->d_s + 1;
+    const int64_t P = p->P;
     hipStream_t st = (hipStream_t)stream;
     if (cb::launch_fill_zero(G, (int64_t)p->n_maps * P * P, st) != hipSuccess ||
         cb::launch_fill_zero(C, (int64_t)p->n_maps * P * p->d_t, st) != hipSuccess)
@@ -383,6 +578,17 @@ cb_status cb_stats_accumulate(cb_plan *p, const cb_cache *src, const cb_cache *t
     if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
     if (!G || !C) return fail(CB_ERR_INVALID_ARGUMENT, "G and C must be non-NULL");
     if (((uintptr_t)G) % 4 || ((uintptr_t)C) % 4) return fail(CB_ERR_MISALIGNED, "G and C must be 4-byte aligned");
+    if (p->multi) {
+        cb::MultiArgs ma = {};
+        bool empty = false;
+        if (cb_status s = prepare_multi(p, src, tgt, weights, w_row_stride, ma, empty)) return s;
+        if (empty) return ok();
+        ma.G = G;
+        ma.C = C;
+        if (cb::launch_stats_multi(ma, (hipStream_t)stream) != hipSuccess)
+            return fail(CB_ERR_DEVICE, "multi-layer statistics kernel launch failed");
+        return ok();
+    }
     cb::StatsArgs a = {};
     bool empty = false;
     if (cb_status s = prepare_stats(p, src, tgt, weights, w_row_stride, a, empty)) return s;
@@ -400,6 +606,7 @@ cb_status cb_stats_accumulate(cb_plan *p, const cb_cache *src, const cb_cache *t
 
 cb_status cb_stats_zero_centered(const cb_plan *p, double *sums, double *sq, float *A, float *B, void *stream) {
     if (!p || !sums || !A || !B) return fail(CB_ERR_INVALID_ARGUMENT, "plan, sums, A and B must be non-NULL");
+    if (cb_status s = single_layer_only(p, "cb_stats_zero_centered")) return s;
     if (cb_status s = check_device(p)) return s;
     const int64_t n = p->n_maps, ds = p->d_s, dt = p->d_t;
     hipStream_t st = (hipStream_t)stream;
@@ -414,6 +621,7 @@ cb_status cb_stats_means(cb_plan *p, const cb_cache *src, const cb_cache *tgt, c
                          int64_t w_row_stride, double *sums, double *sq, void *stream) {
     if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
     if (!sums) return fail(CB_ERR_INVALID_ARGUMENT, "sums must be non-NULL");
+    if (cb_status s = single_layer_only(p, "cb_stats_means")) return s;
     if (((uintptr_t)sums) % 8 || ((uintptr_t)sq) % 8) return fail(CB_ERR_MISALIGNED, "sums and sq must be 8-byte aligned");
     cb::StatsArgs a = {};
     bool empty = false;
@@ -442,6 +650,7 @@ cb_status cb_stats_accumulate_centered(cb_plan *p, const cb_cache *src, const cb
                                        int64_t w_row_stride, const double *sums, float *A, float *B, void *stream) {
     if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
     if (!sums || !A || !B) return fail(CB_ERR_INVALID_ARGUMENT, "sums, A and B must be non-NULL");
+    if (cb_status s = single_layer_only(p, "cb_stats_accumulate_centered")) return s;
     if (((uintptr_t)sums) % 8 || ((uintptr_t)A) % 4 || ((uintptr_t)B) % 4)
         return fail(CB_ERR_MISALIGNED, "sums must be 8-byte and A, B 4-byte aligned");
     cb::StatsArgs a = {};
@@ -464,6 +673,8 @@ cb_status cb_stats_accumulate_centered(cb_plan *p, const cb_cache *src, const cb
 cb_status cb_ridge_solve(int32_t n_maps, int32_t P, int32_t d_t, const float *G, const float *C, float lambda,
                          uint32_t flags, float *maps, int32_t *info, void *stream) {
     if (n_maps < 0) return fail(CB_ERR_INVALID_ARGUMENT, "n_maps is negative");
+    if (P > 129 && supported_width(d_t))
+        return fail(CB_ERR_UNSUPPORTED, "P = %d: systems wider than 129 are solved by cb_ridge_solve_ws", P);
     if (!supported_width(P - 1) || !supported_width(d_t))
         return fail(CB_ERR_UNSUPPORTED, "P must be 65, 97 or 129 and d_t 64, 96 or 128 (got P=%d, d_t=%d)", P, d_t);
     if (flags & ~(uint32_t)(CB_LAMBDA_RELATIVE | CB_RIDGE_BIAS_UNPENALIZED))
@@ -475,6 +686,37 @@ cb_status cb_ridge_solve(int32_t n_maps, int32_t P, int32_t d_t, const float *G,
         return fail(CB_ERR_MISALIGNED, "G, C, maps and info must be 4-byte aligned");
     if (cb::launch_solve(n_maps, P, d_t, G, C, lambda, flags, maps, info, (hipStream_t)stream) != hipSuccess)
         return fail(CB_ERR_DEVICE, "ridge solve launch failed");
+    return ok();
+}
+
+int64_t cb_ridge_solve_workspace_bytes(int32_t P, int32_t d_t, int32_t n_systems) {
+    if (P <= 129 || d_t < 1 || n_systems < 1) return 0;
+    return cb::solve_blocked_bytes_per_system(P, d_t) * (int64_t)n_systems;
+}
+
+cb_status cb_ridge_solve_ws(int32_t n_maps, int32_t P, int32_t d_t, const float *G, const float *C, float lambda,
+                            uint32_t flags, void *workspace, int64_t workspace_bytes, float *maps, int32_t *info,
+                            void *stream) {
+    if (P <= 129) return cb_ridge_solve(n_maps, P, d_t, G, C, lambda, flags, maps, info, stream);
+    if (n_maps < 0) return fail(CB_ERR_INVALID_ARGUMENT, "n_maps is negative");
+    if (P > 4097 || !supported_width(d_t))
+        return fail(CB_ERR_UNSUPPORTED, "need P <= 4097 and d_t in {64, 96, 128} (got P=%d, d_t=%d)", P, d_t);
+    if (flags & ~(uint32_t)(CB_LAMBDA_RELATIVE | CB_RIDGE_BIAS_UNPENALIZED))
+        return fail(CB_ERR_INVALID_ARGUMENT, "unknown flag bits 0x%x", flags);
+    if (!std::isfinite(lambda) || lambda < 0.f) return fail(CB_ERR_INVALID_ARGUMENT, "lambda must be finite and >= 0");
+    if (n_maps == 0) return ok();
+    if (!G || !C || !maps || !info || !workspace)
+        return fail(CB_ERR_INVALID_ARGUMENT, "G, C, maps, info and workspace must be non-NULL");
+    if (((uintptr_t)G) % 4 || ((uintptr_t)C) % 4 || ((uintptr_t)maps) % 4 || ((uintptr_t)info) % 4 ||
+        ((uintptr_t)workspace) % 8)
+        return fail(CB_ERR_MISALIGNED, "G, C, maps, info must be 4-byte and workspace 8-byte aligned");
+    const int64_t need = cb::solve_blocked_bytes_per_system(P, d_t);
+    if (workspace_bytes < need)
+        return fail(CB_ERR_SHAPE, "workspace of %lld bytes is below one system's %lld bytes", (long long)workspace_bytes,
+                    (long long)need);
+    if (cb::launch_solve_blocked(n_maps, P, d_t, G, C, lambda, flags, workspace, workspace_bytes, maps, info,
+                                 (hipStream_t)stream) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "blocked ridge solve launch failed");
     return ok();
 }
 
@@ -676,6 +918,7 @@ cb_status cb_rope(const cb_cache *in, const cb_cache *out, const float *table, i
 
 cb_status cb_apply(cb_plan *p, const float *maps, const cb_cache *src, const cb_cache *tgt_out, void *stream) {
     if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
+    if (p->multi) return fail(CB_ERR_UNSUPPORTED, "cb_apply of multi-layer maps is not available");
     if (p->duplicate_targets)
         return fail(CB_ERR_INVALID_ARGUMENT, "the plan maps some target (layer, kv, head) more than once; "
                                              "cb_apply needs one map per target");

@@ -114,6 +114,41 @@ struct RopeLaunch {
     int32_t n_layers, n_heads, n_seqs, seq_len, d, style, pos_offset, inverse, copy_v;
 };
 
+// One workgroup task of the multi-layer statistics (feature x~ = [x_0; ...;
+// x_{k-1}; 1], blocks of 128 channels): for map `map`, the products of the
+// folded rows of feature block `row_blk` with the exact columns of up to four
+// column blocks (a source block j >= row_blk, or the target block, numbered
+// k), over every calibration row of a call.  The blocks the task reads are
+// staged in LDS slots: slot 0 holds the row block, and a column block that is
+// the row block itself (the diagonal block) reads slot 0 too.
+struct MultiTask {
+    int32_t map, row_blk, n_cols, n_lds;
+    int32_t flags;            // 1: owns sum w x of the row block, 2: sum w y, 4: sum w
+    int32_t wrow, kv, tgt_layer, tgt_head, src_head;
+    int32_t col_blk[4];       // feature block of each column block (k: the target)
+    int32_t col_slot[4];      // LDS slot each column block reads
+    int32_t slot_layer[5];    // source layer staged in each slot, -1: the target block
+};
+
+struct MultiArgs {
+    const uint16_t *src;
+    const uint16_t *tgt;
+    const float *w;
+    Strides ss, ts;
+    int64_t w_row_stride;
+    uint32_t seq_len;         // tokens per sequence
+    uint32_t stride;          // calibration rows: tokens tok = r * stride
+    uint32_t rows_per_seq;    // ceil(seq_len / stride)
+    FastDiv TPS;              // row tiles per sequence (the last one may be partial)
+    int32_t n_tiles;          // row tiles in this call
+    int32_t chunk_tiles;      // tiles between two flushes into G, C
+    int32_t n_tasks, per_xcd; // tasks; ceil(n_tasks / 8)
+    int32_t k, P, d_t;
+    const MultiTask *tasks;
+    const void *zero;         // >= 256 zero bytes
+    float *G, *C;
+};
+
 // Launchers (return hipError_t of the launch).
 hipError_t launch_rope_table(int32_t d, int32_t n_pos, double theta, float *table, hipStream_t s);
 hipError_t launch_rope(const RopeLaunch &L, hipStream_t s);
@@ -133,6 +168,13 @@ hipError_t launch_solve_centered(int32_t n_maps, int32_t d_s, int32_t d_t, const
                                  const float *B, float lambda, uint32_t flags, float *maps, int32_t *info,
                                  hipStream_t s);
 hipError_t launch_fill_zero(float *p, int64_t n, hipStream_t s);
+hipError_t launch_stats_multi(const MultiArgs &a, hipStream_t s);
+int64_t solve_blocked_bytes_per_system(int32_t P, int32_t d_t);
+hipError_t launch_solve_blocked(int32_t n_maps, int32_t P, int32_t d_t, const float *G, const float *C, float lambda,
+                                uint32_t flags, void *ws, int64_t ws_bytes, float *maps, int32_t *info,
+                                hipStream_t s);
+constexpr int kMultiTileRows = 16;      // calibration rows per multi-layer tile
+constexpr int kMultiFlushTiles = 1024;  // at most 16,384 rows summed in fp32 before a flush
 hipError_t launch_solve(int32_t n_maps, int32_t P, int32_t d_t, const float *G, const float *C,
                         float lambda, uint32_t flags, float *maps, int32_t *info, hipStream_t s);
 hipError_t launch_split_maps(int32_t n_maps, int32_t d_s, int32_t d_t, const float *maps,

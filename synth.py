@@ -23,8 +23,8 @@ Workloads (``WORKLOADS``):
   src_layer = round(l*25/39); 200 seqs x 4096 tokens; w = exp(2z)/sqrt(t+1)
   mean-one.
 * ``tiny_k3`` -- multi-layer feature, k = 3: src 4x2x128, tgt 3x2x128,
-  S_l = 3 consecutive source layers (``window``), 3 seqs x 200 tokens, every
-  fourth token a calibration row (ragged tiles), P = 385.
+  S_l = 3 consecutive source layers (``window``), 4 seqs x 520 tokens, every
+  fourth token a calibration row (520 rows > P = 385; ragged tiles).
 * ``qwen_k8`` -- the paper's Qwen3-14B->32B construction shape: k = 8
   (P = 1025), 500 seqs x 1024 tokens, every fourth token (128,000 rows),
   streamed as 5 batches of 100; sources and weights as ``qwen50``.
@@ -104,7 +104,7 @@ WORKLOADS: Dict[str, Workload] = {
 # Multi-layer feature (k selected source layers per target layer; the paper's
 # Qwen3 direction uses k = 8 over 500 sequences of 1,024 tokens sampled every
 # fourth token, 128,000 calibration rows).
-WORKLOADS["tiny_k3"] = Workload("tiny_k3", 4, 2, 128, 3, 2, 128, 3, 200, "window", "gauss", 0.05, "lognormal",
+WORKLOADS["tiny_k3"] = Workload("tiny_k3", 4, 2, 128, 3, 2, 128, 4, 520, "window", "gauss", 0.05, "lognormal",
                                 k=3, sample_stride=4)
 WORKLOADS["qwen_k8"] = Workload("qwen_k8", 40, 8, 128, 64, 8, 128, 500, 1024, "window", "scaled", 0.1, "colmass",
                                 batch_seqs=100, k=8, sample_stride=4)

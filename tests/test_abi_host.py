@@ -181,3 +181,38 @@ def test_rope_entry_points_reject_bad_arguments_on_the_host():
     assert call(style=2) == 1
     assert call(n_pos=6) == 2                            # positions 0..7 need 8 table rows
     assert call(off=60) == 2
+
+
+def test_multi_layer_entry_points_reject_bad_arguments_on_the_host():
+    import paper_2609_00891_amd as cb
+    lib = cb.library()
+    hm = {"tgt_layer": [0, 1], "tgt_head": [0, 0], "kv": [0, 1], "src_layers": [[0, 1], [1, 2]],
+          "src_head": [0, 0], "weight_row": [0, 1]}
+
+    def create(h=hm, src=(3, 1, 128), tgt=(2, 1, 128), stride=1):
+        return cb.cb_plan_create_multi(h, src, tgt, stride)
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_UNSUPPORTED"):
+        create(src=(3, 1, 64))                                       # multi-layer maps need d = 128
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_INVALID_ARGUMENT"):
+        create(stride=0)
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_INVALID_ARGUMENT"):
+        create(dict(hm, src_layers=[[0, 0], [1, 2]]))                # a layer selected twice
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_INVALID_ARGUMENT"):
+        create(dict(hm, src_layers=[[0, 1], [1, 3]]))                # layer outside the source model
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_UNSUPPORTED"):
+        create(dict(hm, src_layers=[list(range(33))] * 2), src=(40, 1, 128))   # k > 32
+    assert lib.cb_plan_create_multi(None, None, None, 1, None) == 1
+    f = ctypes.c_float
+    ws = lib.cb_ridge_solve_ws
+    assert ws(4, 1025, 128, None, None, f(0.1), 0, None, 0, None, None, None) == 1       # NULL pointers
+    assert ws(4, 1025, 100, None, None, f(0.1), 0, None, 0, None, None, None) == 6       # d_t
+    assert ws(4, 5000, 128, None, None, f(0.1), 0, None, 0, None, None, None) == 6       # P too wide
+    assert ws(4, 1025, 128, None, None, f(0.1), 8, None, 0, None, None, None) == 1       # unknown flag
+    assert ws(0, 1025, 128, None, None, f(0.1), 1, None, 0, None, None, None) == 0
+    fake = ctypes.c_void_p(256)
+    assert ws(4, 1025, 128, fake, fake, f(0.1), 1, fake, 1024, fake, fake, None) == 2    # workspace too small
+    assert lib.cb_ridge_solve(4, 1025, 128, fake, fake, f(0.1), 1, fake, fake, None) == 6
+    per = cb.cb_ridge_solve_workspace_bytes(1025, 128, 1)
+    assert per == (1025 * 1025 + 1025 * 128) * 8
+    assert cb.cb_ridge_solve_workspace_bytes(1025, 128, 3) == 3 * per
+    assert cb.cb_ridge_solve_workspace_bytes(129, 128, 3) == 0

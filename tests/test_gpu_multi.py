@@ -1,0 +1,299 @@
+"""GPU parity of the multi-layer path (Sec. 3.2, Eq. localfeature with k selected
+source layers; P = k d_s + 1) against the fp64 oracle, through the C ABI.
+
+Statistics from cb_stats_accumulate on a cb_plan_create_multi plan, solved by
+cb_ridge_solve_ws (blocked fp64 Cholesky), compared with oracle.stats_multi and
+oracle.ridge_solve on the exact bits the GPU consumed.  Bars (relative
+Frobenius error per map): G and C 1e-4, maps 1e-3; the solver alone (same fp32
+moments on both sides, maps rounded to fp32) 1e-6; G exactly symmetric.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+TOL_STATS = 1e-4
+TOL_MAPS = 1e-3
+TOL_SOLVER = 1e-6
+NTHREADS = min(16, os.cpu_count() or 1)
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def cb():
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    import paper_2609_00891_amd as cbmod
+    return cbmod
+
+
+@pytest.fixture(autouse=True)
+def _free_memory():
+    yield
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def relF(a, b):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
+
+
+def bits(t):
+    return synth.bf16_bits(t)
+
+
+def random_multi_map(rng, k, L_s, H_s, L_t, H_t):
+    hm = {f: [] for f in oracle.MULTI_MAP_FIELDS}
+    for l in range(L_t):
+        S = [int(v) for v in rng.permutation(L_s)[:k]]
+        for z in range(2):
+            for h in range(H_t):
+                for f, v in zip(oracle.MULTI_MAP_FIELDS, (l, h, z, S, int(rng.integers(H_s)), l * H_t + h)):
+                    hm[f].append(v)
+    return {f: np.asarray(v, np.int32) for f, v in hm.items()}
+
+
+def small_inputs(rng, L_s, H_s, L_t, H_t, B, T, d=128, device="cuda"):
+    g = torch.Generator(device="cpu")
+    g.manual_seed(int(rng.integers(1 << 31)))
+    scale = torch.exp(torch.randn((L_s, 2, 1, H_s, 1, d), generator=g))
+    src = (torch.randn((L_s, 2, B, H_s, T, d), generator=g) * scale).to(torch.bfloat16)
+    tgt = (torch.randn((L_t, 2, B, H_t, T, d), generator=g) * 2.0 + 1.0).to(torch.bfloat16)
+    w = torch.exp(torch.randn((L_t * H_t, B * T), generator=g))
+    return src.to(device), tgt.to(device), w.to(device)
+
+
+def gpu_stats(cb, plan, batches, G=None, C=None):
+    n, P, dt = plan.n_maps, plan.P, plan.d_t
+    if G is None:
+        G = torch.empty((n, P, P), dtype=torch.float32, device="cuda")
+        C = torch.empty((n, P, dt), dtype=torch.float32, device="cuda")
+        cb.cb_stats_zero(plan, G, C)
+    for src, tgt, w in batches:
+        cb.cb_stats_accumulate(plan, src, tgt, w, G, C)
+    torch.cuda.synchronize()
+    return G, C
+
+
+def oracle_stats_full(hm, src, tgt, w, stride, sel=None):
+    """Oracle moments of the maps `sel` (all by default) on host copies of the caches."""
+    if sel is not None:
+        hm = {f: v[sel] for f, v in hm.items()}
+    sb, tb = bits(src), bits(tgt)
+    L_s, _, B, H_s, T, d_s = src.shape
+    L_t, _, _, H_t, _, d_t = tgt.shape
+    return oracle.stats_multi(hm, sb, synth.cache_strides(L_s, H_s, B, T, d_s), d_s, tb,
+                              synth.cache_strides(L_t, H_t, B, T, d_t), d_t, w.cpu().numpy(), B * T, B, T, stride,
+                              n_threads=NTHREADS)
+
+
+def compact_multi(hm, sel, src, tgt, w, stride):
+    """Host copies of only the sampled rows that the maps `sel` read (sliced on the
+    device), with a head map onto them; the oracle then runs with stride 1."""
+    k = hm["src_layers"].shape[1]
+    B, T = src.shape[2], src.shape[4]
+    xs, ys, ws = [], [], []
+    for m in sel:
+        z, a = int(hm["kv"][m]), int(hm["src_head"][m])
+        for j in hm["src_layers"][m]:
+            xs.append(src[int(j), z, :, a, ::stride])
+        ys.append(tgt[int(hm["tgt_layer"][m]), z, :, int(hm["tgt_head"][m]), ::stride])
+        ws.append(w[int(hm["weight_row"][m])].reshape(B, T)[:, ::stride].reshape(-1))
+    n, Ts = len(sel), xs[0].shape[1]
+    d_s, d_t = xs[0].shape[-1], ys[0].shape[-1]
+    xb = bits(torch.stack(xs)).reshape(n * k, 1, B, 1, Ts, d_s)
+    yb = bits(torch.stack(ys)).reshape(n, 1, B, 1, Ts, d_t)
+    wb = torch.stack(ws).cpu().numpy()
+    chm = {"tgt_layer": np.arange(n, dtype=np.int32), "tgt_head": np.zeros(n, np.int32),
+           "kv": np.zeros(n, np.int32), "src_layers": np.arange(n * k, dtype=np.int32).reshape(n, k),
+           "src_head": np.zeros(n, np.int32), "weight_row": np.arange(n, dtype=np.int32)}
+    ss = (B * Ts * d_s, 0, Ts * d_s, 0, d_s)          # [layer][1][seq][1][tok][dim]: one component
+    ts = (B * Ts * d_t, 0, Ts * d_t, 0, d_t)
+    return oracle.stats_multi(chm, xb, ss, d_s, yb, ts, d_t, np.ascontiguousarray(wb), B * Ts, B, Ts, 1,
+                              n_threads=NTHREADS)
+
+
+def check_stats(G, C, Go, Co, sel, tol=TOL_STATS):
+    idx = torch.as_tensor(np.asarray(sel), device=G.device)
+    Gg = G[idx].double().cpu().numpy()
+    Cg = C[idx].double().cpu().numpy()
+    eg = max(relF(Gg[i], Go[i]) for i in range(len(sel)))
+    ec = max(relF(Cg[i], Co[i]) for i in range(len(sel)))
+    say(f"  stats parity: max relF G {eg:.3e}, C {ec:.3e}")
+    assert eg <= tol and ec <= tol
+    assert np.array_equal(Gg, np.transpose(Gg, (0, 2, 1))), "G must be exactly symmetric"
+    return eg, ec
+
+
+def gpu_solve_ws(cb, G, C, lam=1e-2, flags=None):
+    if flags is None:
+        flags = cb.CB_LAMBDA_RELATIVE
+    n, P, _ = G.shape
+    d_t = C.shape[2]
+    maps = torch.empty_like(C)
+    info = torch.empty((n,), dtype=torch.int32, device="cuda")
+    per = cb.cb_ridge_solve_workspace_bytes(P, d_t, 1)
+    nsys = max(1, min(n, (8 << 30) // max(per, 1)))
+    ws = torch.empty((max(per * nsys, 8),), dtype=torch.uint8, device="cuda")
+    cb.cb_ridge_solve_ws(G, C, lam, flags, maps, info, ws)
+    torch.cuda.synchronize()
+    return maps, info
+
+
+def check_solve(cb, G, C, maps, info, Go, Co, sel, unpen, label=""):
+    """End to end (oracle solve of oracle moments) and the solver alone (oracle
+    solve of the GPU's own fp32 moments)."""
+    idx = torch.as_tensor(np.asarray(sel), device=G.device)
+    Wo, io = oracle.ridge_solve(Go, Co, 1e-2, relative=True, bias_unpenalized=unpen, n_threads=NTHREADS)
+    Wg = maps[idx].double().cpu().numpy()
+    Ws, _ = oracle.ridge_solve(G[idx].double().cpu().numpy(), C[idx].double().cpu().numpy(), 1e-2, relative=True,
+                               bias_unpenalized=unpen, n_threads=NTHREADS)
+    e2e = max(relF(Wg[i], Wo[i]) for i in range(len(sel)))
+    alone = max(relF(Wg[i], Ws[i]) for i in range(len(sel)))
+    say(f"  solve{label}: maps relF end-to-end {e2e:.3e}, solver alone {alone:.3e}")
+    assert (info[idx].cpu().numpy() == 0).all() and (io == 0).all()
+    assert e2e <= TOL_MAPS and alone <= TOL_SOLVER
+    return e2e, alone
+
+
+# ----------------------------------------------------------------------------- small, all maps
+
+def test_multi_tiny_k3_end_to_end(cb):
+    wl = synth.WORKLOADS["tiny_k3"]
+    say(f"multi tiny_k3: P={wl.P}, {wl.n_seqs} x {wl.seq_len} tokens, stride {wl.sample_stride}")
+    src = synth.gen_source(wl, device="cuda")
+    tgt = synth.gen_target(wl, src, device="cuda")
+    w = synth.gen_weights(wl, device="cuda")
+    hm = synth.head_map_multi(wl)
+    plan = cb.cb_plan_create_multi(hm, src, tgt, wl.sample_stride)
+    assert plan.P == wl.P and plan.k == wl.k
+    G, C = gpu_stats(cb, plan, [(src, tgt, w)])
+    Go, Co = oracle_stats_full(hm, src, tgt, w, wl.sample_stride)
+    sel = list(range(plan.n_maps))
+    check_stats(G, C, Go, Co, sel)
+    for unpen in (False, True):
+        flags = cb.CB_LAMBDA_RELATIVE | (cb.CB_RIDGE_BIAS_UNPENALIZED if unpen else 0)
+        maps, info = gpu_solve_ws(cb, G, C, 1e-2, flags)
+        check_solve(cb, G, C, maps, info, Go, Co, sel, unpen, " (bias unpenalized)" if unpen else "")
+    plan.close()
+
+
+# T gives at least 2P calibration rows over the 3 sequences (a well-posed fit,
+# so the maps bar measures the arithmetic, not the conditioning of a rank-
+# deficient problem), with a partial last tile in every sequence.
+@pytest.mark.parametrize("k,stride,T", [(1, 1, 100), (2, 3, 520), (3, 4, 1030), (5, 2, 858)])
+def test_multi_widths_strides_ragged_tiles_and_batches(cb, k, stride, T):
+    rng = np.random.default_rng(1000 + 10 * k + stride)
+    L_s, H_s, L_t, H_t, B = 6, 2, 2, 2, 3
+    say(f"multi k={k} stride={stride} T={T}")
+    src, tgt, w = small_inputs(rng, L_s, H_s, L_t, H_t, B, T)
+    hm = random_multi_map(rng, k, L_s, H_s, L_t, H_t)
+    plan = cb.cb_plan_create_multi(hm, src, tgt, stride)
+    # three uneven batches of sequences, accumulated across calls
+    cuts = [(0, 1), (1, 1), (1, 3)]
+    batches = [(src[:, :, a:b], tgt[:, :, a:b], w.reshape(-1, B, T)[:, a:b].reshape(w.shape[0], -1))
+               for a, b in cuts]
+    G, C = gpu_stats(cb, plan, batches)
+    Go, Co = oracle_stats_full(hm, src, tgt, w, stride)
+    sel = list(range(plan.n_maps))
+    check_stats(G, C, Go, Co, sel)
+    maps, info = gpu_solve_ws(cb, G, C)
+    check_solve(cb, G, C, maps, info, Go, Co, sel, False)
+    plan.close()
+
+
+def test_multi_determinism_scaling_and_zero_weights(cb):
+    rng = np.random.default_rng(77)
+    L_s, H_s, L_t, H_t, B, T, k, stride = 5, 2, 2, 2, 2, 150, 3, 4
+    src, tgt, w = small_inputs(rng, L_s, H_s, L_t, H_t, B, T)
+    hm = random_multi_map(rng, k, L_s, H_s, L_t, H_t)
+    plan = cb.cb_plan_create_multi(hm, src, tgt, stride)
+    G1, C1 = gpu_stats(cb, plan, [(src, tgt, w)])
+    G2, C2 = gpu_stats(cb, plan, [(src, tgt, w)])
+    assert torch.equal(G1, G2) and torch.equal(C1, C2), "results must be bitwise reproducible"
+    G4, C4 = gpu_stats(cb, plan, [(src, tgt, 4.0 * w)])
+    assert torch.equal(G4, 4.0 * G1) and torch.equal(C4, 4.0 * C1), "power-of-two weight scaling must be exact"
+    # an empty call adds nothing
+    cb.cb_stats_accumulate(plan, src[:, :, :0], tgt[:, :, :0], w, G1, C1)
+    torch.cuda.synchronize()
+    assert torch.equal(G1, G2)
+    # weight rows of zero: zero moments, relative lambda 0, first pivot fails
+    wz = w.clone()
+    wz[0] = 0.0
+    Gz, Cz = gpu_stats(cb, plan, [(src, tgt, wz)])
+    zero_maps = [m for m in range(plan.n_maps) if hm["weight_row"][m] == 0]
+    assert zero_maps and all(float(Gz[m].abs().max()) == 0.0 and float(Cz[m].abs().max()) == 0.0
+                             for m in zero_maps)
+    maps, info = gpu_solve_ws(cb, Gz, Cz)
+    inf = info.cpu().numpy()
+    for m in range(plan.n_maps):
+        if m in zero_maps:
+            assert inf[m] == 1 and float(maps[m].abs().max()) == 0.0
+        else:
+            assert inf[m] == 0
+    plan.close()
+
+
+def test_multi_device_side_argument_errors(cb):
+    rng = np.random.default_rng(5)
+    src, tgt, w = small_inputs(rng, 4, 2, 2, 2, 1, 32)
+    hm = random_multi_map(rng, 2, 4, 2, 2, 2)
+    plan = cb.cb_plan_create_multi(hm, src, tgt, 2)
+    n, P = plan.n_maps, plan.P
+    G = torch.zeros((n, P, P), dtype=torch.float32, device="cuda")
+    C = torch.zeros((n, P, 128), dtype=torch.float32, device="cuda")
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_SHAPE"):
+        cb.cb_stats_accumulate(plan, src[:2], tgt, w, G, C)              # wrong source layer count
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_UNSUPPORTED"):
+        cb.cb_apply(plan, C, src, tgt)
+    sums = torch.zeros((n, 257), dtype=torch.float64, device="cuda")
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_UNSUPPORTED"):
+        cb.cb_stats_means(plan, src, tgt, w, sums)
+    maps = torch.empty_like(C)
+    info = torch.empty((n,), dtype=torch.int32, device="cuda")
+    small = torch.empty((1024,), dtype=torch.uint8, device="cuda")
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_SHAPE"):
+        cb.cb_ridge_solve_ws(G, C, 1e-2, cb.CB_LAMBDA_RELATIVE, maps, info, small)
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_UNSUPPORTED"):
+        cb.cb_ridge_solve(G, C, 1e-2, cb.CB_LAMBDA_RELATIVE, maps, info)
+    plan.close()
+
+
+# ----------------------------------------------------------------------------- full size
+
+def test_multi_qwen_k8_batch_full_size_sampled_maps(cb):
+    """The resident 100-sequence batch of the k = 8 construction (40 -> 64 layers x
+    8 heads x 128, 1,024 tokens per sequence, every fourth token: 25,600 rows per
+    call), launched as the benchmark launches it; eight sampled maps against the
+    oracle, all 1,024 systems solved."""
+    wl = synth.WORKLOADS["qwen_k8"]
+    bw = wl.with_(n_seqs=wl.batch_seqs)
+    say(f"multi qwen_k8 batch: {bw.n_seqs} x {bw.seq_len} tokens, stride {bw.sample_stride}, P={bw.P}")
+    src = synth.gen_source(bw, device="cuda")
+    tgt = synth.gen_target(bw, src, device="cuda")
+    w = synth.gen_weights(bw, device="cuda", chunk=50)
+    hm = synth.head_map_multi(wl)
+    plan = cb.cb_plan_create_multi(hm, src, tgt, wl.sample_stride)
+    G, C = gpu_stats(cb, plan, [(src, tgt, w)])
+    sel = [0, 1, 135, 511, 512, 777, 1022, 1023]
+    say("  oracle on the sampled maps ...")
+    Go, Co = compact_multi(hm, sel, src, tgt, w, wl.sample_stride)
+    check_stats(G, C, Go, Co, sel)
+    del src, tgt
+    torch.cuda.empty_cache()
+    maps, info = gpu_solve_ws(cb, G, C, 1e-2, cb.CB_LAMBDA_RELATIVE | cb.CB_RIDGE_BIAS_UNPENALIZED)
+    assert int((info != 0).sum()) == 0
+    check_solve(cb, G, C, maps, info, Go, Co, sel, True)
+    plan.close()
