@@ -186,7 +186,7 @@ cb_status prepare_multi(const cb_plan *p, const cb_cache *src, const cb_cache *t
     const int64_t rows = (src->seq_len + p->sample_stride - 1) / p->sample_stride;
     const int64_t tps = (rows + KT - 1) / KT;
     const int64_t tiles = (int64_t)src->n_seqs * tps;
-    if (tiles > INT32_MAX - 2) return fail(CB_ERR_UNSUPPORTED, "too many row tiles in one call");
+    if (tiles > INT32_MAX - 16) return fail(CB_ERR_UNSUPPORTED, "too many row tiles in one call");
     const int64_t step = (int64_t)p->sample_stride * 2 * KT;
     if (src->s_tok * step >= (1LL << 31) || tgt->s_tok * step >= (1LL << 31))
         return fail(CB_ERR_UNSUPPORTED, "token stride x sample_stride too large (16 rows must span < 2 GiB)");
@@ -201,11 +201,11 @@ cb_status prepare_multi(const cb_plan *p, const cb_cache *src, const cb_cache *t
     a.rows_per_seq = (uint32_t)rows;
     a.TPS = cb::make_fastdiv((uint32_t)tps);
     a.n_tiles = (int32_t)tiles;
-    {   // flush at most every kMultiFlushTiles tiles, at an even tile count
-        const int64_t iters = (tiles + 1) & ~1LL;
+    {   // flush at most every kMultiFlushTiles tiles, at a multiple of six tiles (one loop trip)
+        const int64_t iters = (tiles + 5) / 6 * 6;
         const int64_t nf = (iters + cb::kMultiFlushTiles - 1) / cb::kMultiFlushTiles;
         int64_t ct = (iters + nf - 1) / nf;
-        ct = (ct + 1) & ~1LL;
+        ct = (ct + 5) / 6 * 6;
         a.chunk_tiles = (int32_t)ct;
     }
     a.n_tasks = p->n_tasks;
@@ -522,7 +522,7 @@ cb_status cb_plan_create_multi(const cb_head_map_multi *map, const cb_cache *src
                         t.col_slot[b] = t.n_lds;
                         t.slot_layer[t.n_lds++] = col < k ? S[col] : -1;
                     }
-                    if (col == k && i == 0) t.flags |= 2;   // one owner of sum w y per map
+                    if (col == k && i == 0) t.flags |= 2;   // one owner of sum w y per map (its last block)
                 }
                 for (int s = t.n_lds; s < 5; ++s) t.slot_layer[s] = S[i];
                 tasks.push_back(t);

@@ -27,12 +27,12 @@
 //
 // Staging.  A tile is 16 calibration rows of one sequence.  Its blocks (the
 // row block and the column blocks other than the diagonal one) move HBM -> LDS
-// by global_load_lds_dwordx4 through a six-stage ring, five tiles ahead; each
+// by global_load_lds_dwordx4 through a six-stage ring, six tiles ahead; each
 // 16-byte chunk c of row t sits at chunk c ^ 4(t mod 4) so the transposed
 // operand reads (ds_read_b64_tr_b16) are conflict free.  Rows past the end of
 // a sequence repeat its last row with weight zero.
 //
-// Flush.  Every at most 1,024 tiles (16,384 rows) and at the end of the call
+// Flush.  Every at most 1,020 tiles (16,320 rows) and at the end of the call
 // each wave adds its tiles into G (and C): a tile above the diagonal goes to
 // its block and, transposed through LDS, to the mirrored block; a tile on the
 // diagonal contributes its upper triangle to both triangles; tiles below the
@@ -50,7 +50,6 @@ struct MCfg {
     static constexpr int OFF_W = MAXS * BLK;       // weights of the tile: [KT] fp32
     static constexpr int STAGE = OFF_W + KT * 4;
     static constexpr int NST = 6;                  // ring stages
-    static constexpr int AHEAD = NST - 1;          // tiles in flight ahead of the computed one
     static constexpr int TRS = 33;                 // row stride (floats) of the transpose scratch
     static constexpr int OFF_T = NST * STAGE;
     static constexpr int LDS = OFF_T + 4 * 32 * TRS * 4;
@@ -84,7 +83,9 @@ __device__ __forceinline__ void flush_rows(const float *tr, int lane, int mode, 
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 }
 
-template <int N>
+// N: column blocks of the task.  YS: the task owns sum w y of its map (its
+// last column block is the target block), so it also sums w y on the VALU.
+template <int N, bool YS>
 __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &tk, const MultiCtx &c,
                                            lds_char_t *lds, int wave, int lane) {
     using K = MCfg;
@@ -151,9 +152,10 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
         ecol_y[e] = tk.col_blk[b] == a.k;
     }
     const uint32_t lw = K::OFF_W + (lane >> 5) * 32;
-    const bool do_sumx = (tk.flags & 1) && q == 0;
-    const bool do_sumw = (tk.flags & 4) && wave == 0;
-    const bool do_sumy = (tk.flags & 2) && p == 0;
+    const bool own_sumx = (tk.flags & 1) && q == 0;
+    const bool own_sumw = (tk.flags & 4) && wave == 0;
+    // entries of this wave that read the target block when it is the task's last column block
+    auto ycol = [&](int e) { return YS && q * E + e >= 4 * (N - 1); };
 
     struct Ops {
         bf16x8_t xr[2], cf[E];
@@ -185,45 +187,51 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
         o.w[0] = w0[0]; o.w[1] = w0[1]; o.w[2] = w0[2]; o.w[3] = w0[3];
         o.w[4] = w1[0]; o.w[5] = w1[1]; o.w[6] = w1[2]; o.w[7] = w1[3];
     };
-    // a = w x for the lane's 8 rows of one channel, split into hi + lo; the
-    // bias sums of the tile on the side.
+    // a = w x for the lane's 8 rows of one channel of row block r, split into
+    // hi + lo; sum w x on the side (kept by every wave: it is branch free and
+    // written only by the owner).
+    auto fold_row = [&](Folded &f, const Ops &o, int r) {
+        const uint4 ax = __builtin_bit_cast(uint4, o.xr[r]);
+        const uint32_t xv[4] = {ax.x, ax.y, ax.z, ax.w};
+        float av[8];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            av[2 * e] = o.w[2 * e] * bf_lo(xv[e]);
+            av[2 * e + 1] = o.w[2 * e + 1] * bf_hi(xv[e]);
+        }
+        uint32_t hv[4], lv[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            hv[e] = pack_bf16(av[2 * e], av[2 * e + 1]);
+            lv[e] = pack_bf16(av[2 * e] - bf_lo(hv[e]), av[2 * e + 1] - bf_hi(hv[e]));
+        }
+        sumx[r] += ((av[0] + av[1]) + (av[2] + av[3])) + ((av[4] + av[5]) + (av[6] + av[7]));
+        f.hi[r] = __builtin_bit_cast(bf16x8_t, make_uint4(hv[0], hv[1], hv[2], hv[3]));
+        f.lo[r] = __builtin_bit_cast(bf16x8_t, make_uint4(lv[0], lv[1], lv[2], lv[3]));
+    };
+    auto sum_w = [&](const Ops &o) {
+        sumw += ((o.w[0] + o.w[1]) + (o.w[2] + o.w[3])) + ((o.w[4] + o.w[5]) + (o.w[6] + o.w[7]));
+    };
+    auto sum_y = [&](const Ops &o) {
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            if (!ycol(e)) continue;
+            const uint4 yv = __builtin_bit_cast(uint4, o.cf[e]);
+            const uint32_t yy[4] = {yv.x, yv.y, yv.z, yv.w};
+            float py[8];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                py[2 * i] = o.w[2 * i] * bf_lo(yy[i]);
+                py[2 * i + 1] = o.w[2 * i + 1] * bf_hi(yy[i]);
+            }
+            sumy[e] += ((py[0] + py[1]) + (py[2] + py[3])) + ((py[4] + py[5]) + (py[6] + py[7]));
+        }
+    };
     auto fold = [&](Folded &f, const Ops &o) {
-#pragma unroll
-        for (int r = 0; r < 2; ++r) {
-            const uint4 ax = __builtin_bit_cast(uint4, o.xr[r]);
-            const uint32_t xv[4] = {ax.x, ax.y, ax.z, ax.w};
-            float av[8];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                av[2 * e] = o.w[2 * e] * bf_lo(xv[e]);
-                av[2 * e + 1] = o.w[2 * e + 1] * bf_hi(xv[e]);
-            }
-            uint32_t hv[4], lv[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                hv[e] = pack_bf16(av[2 * e], av[2 * e + 1]);
-                lv[e] = pack_bf16(av[2 * e] - bf_lo(hv[e]), av[2 * e + 1] - bf_hi(hv[e]));
-            }
-            if (do_sumx) sumx[r] += ((av[0] + av[1]) + (av[2] + av[3])) + ((av[4] + av[5]) + (av[6] + av[7]));
-            f.hi[r] = __builtin_bit_cast(bf16x8_t, make_uint4(hv[0], hv[1], hv[2], hv[3]));
-            f.lo[r] = __builtin_bit_cast(bf16x8_t, make_uint4(lv[0], lv[1], lv[2], lv[3]));
-        }
-        if (do_sumw) sumw += ((o.w[0] + o.w[1]) + (o.w[2] + o.w[3])) + ((o.w[4] + o.w[5]) + (o.w[6] + o.w[7]));
-        if (do_sumy) {
-#pragma unroll
-            for (int e = 0; e < E; ++e) {
-                if (!ecol_y[e]) continue;
-                const uint4 yv = __builtin_bit_cast(uint4, o.cf[e]);
-                const uint32_t yy[4] = {yv.x, yv.y, yv.z, yv.w};
-                float py[8];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    py[2 * i] = o.w[2 * i] * bf_lo(yy[i]);
-                    py[2 * i + 1] = o.w[2 * i + 1] * bf_hi(yy[i]);
-                }
-                sumy[e] += ((py[0] + py[1]) + (py[2] + py[3])) + ((py[4] + py[5]) + (py[6] + py[7]));
-            }
-        }
+        fold_row(f, o, 0);
+        fold_row(f, o, 1);
+        sum_w(o);
+        sum_y(o);
     };
     auto mma_hi = [&](const Folded &f, const Ops &o) {
 #pragma unroll
@@ -272,7 +280,7 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
             }
         }
         // bias row / column: lanes l and l + 32 hold the two halves of each K step
-        if (do_sumx) {
+        if (own_sumx) {
 #pragma unroll
             for (int r = 0; r < 2; ++r) {
                 const float s = sumx[r] + __shfl_xor(sumx[r], 32);
@@ -281,54 +289,107 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
                     Gm[(int64_t)ch * P + P - 1] += s;
                     Gm[(int64_t)(P - 1) * P + ch] += s;
                 }
-                sumx[r] = 0.f;
             }
         }
-        if (do_sumy) {
+        sumx[0] = sumx[1] = 0.f;
+        if (YS && p == 0) {
 #pragma unroll
             for (int e = 0; e < E; ++e) {
-                if (!ecol_y[e]) continue;
+                if (!ycol(e)) continue;
                 const float s = sumy[e] + __shfl_xor(sumy[e], 32);
                 const int win = (q * E + e) & 3;
                 if (lane < 32) Cm[(int64_t)(P - 1) * a.d_t + 32 * win + lane] += s;
-                sumy[e] = 0.f;
             }
         }
-        if (do_sumw) {
+#pragma unroll
+        for (int e = 0; e < E; ++e) sumy[e] = 0.f;
+        if (own_sumw) {
             const float s = sumw + __shfl_xor(sumw, 32);
             if (lane == 0) Gm[(int64_t)(P - 1) * P + P - 1] += s;
-            sumw = 0.f;
         }
+        sumw = 0.f;
         zero_acc();
     };
 
-    // ---- pipeline: tiles 0 .. AHEAD-1 fill the ring
+    // ---- pipeline.  Tile t's operands are read from LDS two iterations ahead
+    // (iteration t-2), folded one iteration ahead (t-1) and multiplied in
+    // iteration t, so no LDS latency sits in front of a fold and no fold in
+    // front of an MFMA.  Iteration t: tile t+2 has landed (wait + barrier);
+    // tile t+6 is issued into the stage of tile t, whose reads finished two
+    // iterations ago; the hi MFMAs of tile t run with the fold of row block 0
+    // of tile t+1 and half of the reads of tile t+2, the lo MFMAs with the
+    // rest (an MFMA keeps the matrix core busy for about as long as the wave
+    // needs to issue five other instructions).  Operand sets rotate with
+    // period 3, folded sets with period 2: six iterations per loop trip.
 #pragma unroll
-    for (int u = 0; u < K::AHEAD; ++u) issue(u, u);
-    const int n_iter = (a.n_tiles + 1) & ~1;                   // an odd count ends with a zero-weight tile
-    wait_vm_rt((K::AHEAD - 1) * per_tile);                   // tile 0 has landed
+    for (int u = 0; u < K::NST; ++u) issue(u, u);
+    const int n_iter = (a.n_tiles + 5) / 6 * 6;              // padded with zero-weight tiles
+    Ops o0, o1, o2;
+    Folded f0, f1;
+    wait_vm_rt((K::NST - 1) * per_tile);                     // tile 0 has landed
     lds_barrier();
-    Ops oa, ob;
-    Folded fa, fb;
-    read_ops(oa, 0);
-    fold(fa, oa);
-    // Iteration t: tile t+1 has landed (wait + barrier), tile t+AHEAD is issued
-    // into the stage of tile t-1, tile t+1 is read and folded while the
-    // MFMAs of tile t run.
-    auto iteration = [&](int t, const Ops &oc, const Folded &fc, Ops &on, Folded &fn) {
-        wait_vm_rt((K::AHEAD - 2) * per_tile);
+    read_ops(o0, 0);
+    wait_vm_rt((K::NST - 2) * per_tile);                     // tile 1 has landed
+    lds_barrier();
+    read_ops(o1, 1);
+    fold(f0, o0);
+    auto pin = [&](const Folded &f) {
+#pragma unroll
+        for (int r = 0; r < 2; ++r) asm volatile("" ::"v"(f.hi[r]), "v"(f.lo[r]));
+        asm volatile("" ::"v"(sumx[0]), "v"(sumx[1]), "v"(sumw));
+    };
+    auto read_half = [&](Ops &o, int st, int half) {
+        const lds_char_t *S = lds + st * K::STAGE;
+        if (half == 0) {
+#pragma unroll
+            for (int r = 0; r < 2; ++r) o.xr[r] = tr_read8(S + xoff[r], S + xoff[r] + 4 * K::ROW);
+            const f32x4_t w0 = *(const lds_f32x4_t *)(S + lw);
+            const f32x4_t w1 = *(const lds_f32x4_t *)(S + lw + 16);
+            o.w[0] = w0[0]; o.w[1] = w0[1]; o.w[2] = w0[2]; o.w[3] = w0[3];
+            o.w[4] = w1[0]; o.w[5] = w1[1]; o.w[6] = w1[2]; o.w[7] = w1[3];
+        }
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+            if ((e < E / 2) == (half == 0)) o.cf[e] = tr_read8(S + coff[e], S + coff[e] + 4 * K::ROW);
+    };
+    auto iteration = [&](int t, const Ops &oa, const Folded &fa, const Ops &ob, Folded &fb, Ops &oc) {
+        wait_vm_rt((K::NST - 3) * per_tile);                 // tile t+2 has landed
         lds_barrier();
-        issue(t + K::AHEAD, (t + K::AHEAD) % K::NST);
-        read_ops(on, (t + 1) % K::NST);
-        mma_hi(fc, oc);
-        fold(fn, on);
-        mma_lo(fc, oc);
+        issue(t + K::NST, t % K::NST);
+        __builtin_amdgcn_sched_barrier(0);
+        read_half(oc, (t + 2) % K::NST, 0);
+        mma_hi(fa, oa);
+        fold_row(fb, ob, 0);
+#pragma unroll
+        for (int i = 0; i < 2 * E; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);            // one MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);            // one LDS read
+            __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);            // three VALU
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        read_half(oc, (t + 2) % K::NST, 1);
+        fold_row(fb, ob, 1);
+        sum_w(ob);
+        mma_lo(fa, oa);
+        pin(fb);
+#pragma unroll
+        for (int i = 0; i < 2 * E; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (YS) sum_y(ob);
     };
     for (int c0 = 0; c0 < n_iter; c0 += a.chunk_tiles) {
         const int c1 = min(c0 + a.chunk_tiles, n_iter);
-        for (int t = c0; t < c1; t += 2) {
-            iteration(t, oa, fa, ob, fb);
-            iteration(t + 1, ob, fb, oa, fa);
+        for (int t = c0; t < c1; t += 6) {
+            iteration(t + 0, o0, f0, o1, f1, o2);
+            iteration(t + 1, o1, f1, o2, f0, o0);
+            iteration(t + 2, o2, f0, o0, f1, o1);
+            iteration(t + 3, o0, f1, o1, f0, o2);
+            iteration(t + 4, o1, f0, o2, f1, o0);
+            iteration(t + 5, o2, f1, o0, f0, o1);
         }
         flush();
     }
@@ -363,11 +424,16 @@ void stats_multi_kernel(MultiArgs a) {
             c.slot_stok[s] = a.ss.tok;
         }
     }
-    switch (tk.n_cols) {
-        case 1: multi_wave<1>(a, tk, c, lds, wave, lane); break;
-        case 2: multi_wave<2>(a, tk, c, lds, wave, lane); break;
-        case 3: multi_wave<3>(a, tk, c, lds, wave, lane); break;
-        default: multi_wave<4>(a, tk, c, lds, wave, lane); break;
+    const bool ys = (tk.flags & 2) != 0;
+    switch (tk.n_cols * 2 + (ys ? 1 : 0)) {
+        case 2: multi_wave<1, false>(a, tk, c, lds, wave, lane); break;
+        case 3: multi_wave<1, true>(a, tk, c, lds, wave, lane); break;
+        case 4: multi_wave<2, false>(a, tk, c, lds, wave, lane); break;
+        case 5: multi_wave<2, true>(a, tk, c, lds, wave, lane); break;
+        case 6: multi_wave<3, false>(a, tk, c, lds, wave, lane); break;
+        case 7: multi_wave<3, true>(a, tk, c, lds, wave, lane); break;
+        case 8: multi_wave<4, false>(a, tk, c, lds, wave, lane); break;
+        default: multi_wave<4, true>(a, tk, c, lds, wave, lane); break;
     }
 }
 
