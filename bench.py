@@ -279,6 +279,69 @@ def rope_leg(cb, cache, steps):
     return {"ms": ms, "GBps": bytes_ / (ms / 1e3) / 1e9, "bytes_per_pass": bytes_}
 
 
+def multi_leg(cb, synth, steps):
+    """The paper's own construction shape (Sec. 4.1): multi-layer maps with k = 8
+    selected source layers per target layer (P = 1,025), 500 sequences of 1,024
+    tokens sampled every fourth token (128,000 calibration rows), streamed as 5
+    calls of one resident 100-sequence batch, then the 1,024-system blocked
+    fp64 ridge solve.  Timed with events on the launch stream after one warm-up
+    build."""
+    import torch
+    wl = synth.WORKLOADS["qwen_k8"]
+    B = wl.batch_seqs
+    n_calls = wl.n_seqs // B
+    bw = wl.with_(n_seqs=B)
+    log(f"generating the k = {wl.k} batch: {B} x {wl.seq_len} tokens")
+    src = synth.gen_source(bw, 0, device="cuda")
+    tgt = synth.gen_target(bw, src, 0, device="cuda")
+    w = synth.gen_weights(bw, 0, device="cuda", chunk=50)
+    hm = synth.head_map_multi(wl)
+    plan = cb.cb_plan_create_multi(hm, src, tgt, wl.sample_stride)
+    n, P, d_t = plan.n_maps, plan.P, plan.d_t
+    G = torch.empty((n, P, P), dtype=torch.float32, device="cuda")
+    C = torch.empty((n, P, d_t), dtype=torch.float32, device="cuda")
+    maps = torch.empty_like(C)
+    info = torch.empty((n,), dtype=torch.int32, device="cuda")
+    ws = torch.empty((cb.cb_ridge_solve_workspace_bytes(P, d_t, n),), dtype=torch.uint8, device="cuda")
+    flags = cb.CB_LAMBDA_RELATIVE | cb.CB_RIDGE_BIAS_UNPENALIZED
+    stream = torch.cuda.current_stream()
+    recs = []
+    for it in range(steps + 1):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(n_calls + 3)]
+        e[0].record(stream)
+        cb.cb_stats_zero(plan, G, C)
+        e[1].record(stream)
+        for i in range(n_calls):
+            cb.cb_stats_accumulate(plan, src, tgt, w, G, C)
+            e[2 + i].record(stream)
+        cb.cb_ridge_solve_ws(G, C, wl.lam_rel, flags, maps, info, ws)
+        e[n_calls + 2].record(stream)
+        if it > 0:
+            recs.append(e)
+    torch.cuda.synchronize()
+    mean = lambda v: sum(v) / len(v)  # noqa: E731
+    call_ms = mean([e[1 + i].elapsed_time(e[2 + i]) for e in recs for i in range(n_calls)])
+    solve_ms = mean([e[n_calls + 1].elapsed_time(e[n_calls + 2]) for e in recs])
+    build_ms = mean([e[0].elapsed_time(e[n_calls + 2]) for e in recs])
+    rows_per_call = B * ((wl.seq_len + wl.sample_stride - 1) // wl.sample_stride)
+    flop_per_row = 2 * n * (P * P + P * d_t)                  # dense P x P Gram, algorithmic
+    tflops = flop_per_row * rows_per_call / (call_ms / 1e3) / 1e12
+    bad = int((info != 0).sum().item())
+    plan.close()
+    return {
+        "workload": f"qwen3-14b->32b-shaped k={wl.k} build (P={P}, {n} maps): {wl.n_seqs} seqs x {wl.seq_len} tok, "
+                    f"every {wl.sample_stride}th token ({wl.n_seqs * rows_per_call // B} rows), "
+                    f"{n_calls} x {B}-seq resident batch, + {n}-system blocked fp64 solve",
+        "s_per_500seq_build": build_ms / 1e3,
+        "calib_rows_per_s": wl.n_seqs * rows_per_call // B / (build_ms / 1e3),
+        "legs_ms": {"stats_call": call_ms, "solve": solve_ms},
+        "roofline": {"bound": "mfma", "kernel": "stats_multi_kernel per 100-seq call", "achieved": tflops,
+                     "peak": 2500.0, "unit": "TFLOP/s", "frac": tflops / 2500.0,
+                     "algorithmic_flops_per_launch": flop_per_row * rows_per_call},
+        "nonpositive_pivots": bad,
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -295,6 +358,8 @@ def main():
                     help="timed attention-aligned weight passes over the resident batch (0: skip)")
     ap.add_argument("--rope-steps", type=int, default=3,
                     help="timed in-place RoPE passes over the applied target cache (0: skip)")
+    ap.add_argument("--multi-steps", type=int, default=2,
+                    help="timed k = 8 multi-layer builds (P = 1025), after the other legs (0: skip)")
     ap.add_argument("--hbm-copy-probe", type=float, default=None, metavar="GIB",
                     help="only time a plain copy of GIB GiB (counter calibration)")
     args = ap.parse_args()
@@ -445,6 +510,11 @@ def main():
         res["attn_weights"] = attn_leg(cb, synth, bw, tgt, args.attn_steps)
     if args.rope_steps > 0 and aout is not None:
         res["rope"] = rope_leg(cb, aout, args.rope_steps)
+    if args.multi_steps > 0:
+        asrc = aout = None
+        torch.cuda.empty_cache()
+        res["multi_layer_k8"] = multi_leg(cb, synth, args.multi_steps)
+        torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         n_threads = int(os.environ.get("OMP_NUM_THREADS", str(os.cpu_count() or 1)))
         log(f"cpu baseline on {n_threads} threads")

@@ -479,54 +479,92 @@ cb_status cb_plan_create_multi(const cb_head_map_multi *map, const cb_cache *src
 
     // ---- statistics tasks.  Maps are visited by (kv, source head, target
     // layer, target head): neighbouring maps then read mostly the same source
-    // blocks, and the kernel hands each XCD a contiguous run of tasks.  Row
-    // block i of a map pairs with column blocks i..k-1 and the target block k,
-    // cut into parts of at most four blocks of near-equal size.
+    // blocks, and the kernel hands each XCD a contiguous run of tasks.  The
+    // cells of a map (every unordered pair {i, j} of source blocks, the k
+    // diagonal blocks and the k (i, target) cells) are packed into equal
+    // rectangles {r0, r1} x {c0, c1}; a pair may be computed in either
+    // orientation because G is mirrored:
+    //   couple (a, b) = (2m, 2m+1):   {a, b} x {a, y}   -> (a,a) {a,b} (a,y) (b,y)
+    //   couples m < m':               {a, b} x {a', b'} -> four pairs
+    //   the diagonals (b, b) left by the couples, two at a time:
+    //                                 {b, b'} x {b, b'} -> (b,b) (b',b') (the pair is already done)
+    //   an unpaired last block c:     {c, c} x {c, y}, then its pairs with
+    //                                 the couples, {c, c} x {a, b} (half used)
+    // At k = 8 that is 12 tasks for 44 cells.
     std::vector<int> order(n);
     for (int m = 0; m < n; ++m) order[m] = m;
     std::stable_sort(order.begin(), order.end(), [&](int a, int b) {
         return std::make_tuple(map->kv[a], map->src_head[a], map->tgt_layer[a], map->tgt_head[a]) <
                std::make_tuple(map->kv[b], map->src_head[b], map->tgt_layer[b], map->tgt_head[b]);
     });
+    struct Rect { int r0, r1, c0, c1, mask; };
+    std::vector<Rect> rects;
+    const int Y = k;
+    const int nc = k / 2;
+    for (int m = 0; m < nc; ++m) rects.push_back({2 * m, 2 * m + 1, 2 * m, Y, 0xF});
+    for (int m = 0; m < nc; ++m)
+        for (int m2 = m + 1; m2 < nc; ++m2) rects.push_back({2 * m, 2 * m + 1, 2 * m2, 2 * m2 + 1, 0xF});
+    for (int m = 0; m < nc; m += 2) {
+        const int b = 2 * m + 1;
+        if (m + 1 < nc) {
+            const int b2 = 2 * m + 3;
+            rects.push_back({b, b2, b, b2, 0x9});            // cells (b, b) and (b2, b2)
+        } else {
+            rects.push_back({b, b, b, b, 0x1});              // a lone leftover diagonal
+        }
+    }
+    if (k % 2) {
+        const int c = k - 1;
+        rects.push_back({c, c, c, Y, 0x3});                  // (c, c) and (c, y)
+        for (int m = 0; m < nc; ++m) rects.push_back({c, c, 2 * m, 2 * m + 1, 0x3});
+    }
     std::vector<cb::MultiTask> tasks;
     for (int m : order) {
         const int32_t *S = map->src_layers + (int64_t)m * k;
-        for (int i = 0; i < k; ++i) {
-            const int ncol = k - i + 1;
-            const int parts = (ncol + 3) / 4;
-            int col = i;
-            for (int pt = 0; pt < parts; ++pt) {
-                const int sz = ncol / parts + (pt < ncol % parts ? 1 : 0);
-                cb::MultiTask t = {};
-                t.map = m;
-                t.row_blk = i;
-                t.n_cols = sz;
-                t.wrow = map->weight_row[m];
-                t.kv = map->kv[m];
-                t.tgt_layer = map->tgt_layer[m];
-                t.tgt_head = map->tgt_head[m];
-                t.src_head = map->src_head[m];
-                t.slot_layer[0] = S[i];
-                t.n_lds = 1;
-                for (int b = 0; b < 4; ++b) {
-                    t.col_blk[b] = i;
-                    t.col_slot[b] = 0;
+        std::vector<char> own_x(k, 0);
+        bool own_w = false, own_y = false;
+        for (const Rect &rc : rects) {
+            cb::MultiTask t = {};
+            t.map = m;
+            t.wrow = map->weight_row[m];
+            t.kv = map->kv[m];
+            t.tgt_layer = map->tgt_layer[m];
+            t.tgt_head = map->tgt_head[m];
+            t.src_head = map->src_head[m];
+            t.rows[0] = rc.r0; t.rows[1] = rc.r1;
+            t.cols[0] = rc.c0; t.cols[1] = rc.c1;
+            t.cell_mask = rc.mask;
+            int blk[4];
+            t.n_lds = 0;
+            auto slot_of = [&](int b) {
+                for (int s2 = 0; s2 < t.n_lds; ++s2)
+                    if (blk[s2] == b) return s2;
+                blk[t.n_lds] = b;
+                t.slot_layer[t.n_lds] = b < k ? S[b] : -1;
+                return t.n_lds++;
+            };
+            t.row_slot[0] = slot_of(rc.r0);
+            t.row_slot[1] = slot_of(rc.r1);
+            t.col_slot[0] = slot_of(rc.c0);
+            t.col_slot[1] = slot_of(rc.c1);
+            for (int s2 = t.n_lds; s2 < 4; ++s2) t.slot_layer[s2] = t.slot_layer[0];
+            for (int a2 = 0; a2 < 2; ++a2) {
+                const int r = a2 == 0 ? rc.r0 : rc.r1;
+                const bool used = ((rc.mask >> (2 * a2)) & 3) != 0;
+                if (used && !own_x[r] && !(a2 == 1 && rc.r1 == rc.r0)) {
+                    own_x[r] = 1;
+                    t.flags |= 1 << a2;
                 }
-                for (int b = 0; b < sz; ++b, ++col) {
-                    t.col_blk[b] = col;
-                    if (col == i) {
-                        t.col_slot[b] = 0;
-                        t.flags |= 1;
-                        if (i == 0) t.flags |= 4;
-                    } else {
-                        t.col_slot[b] = t.n_lds;
-                        t.slot_layer[t.n_lds++] = col < k ? S[col] : -1;
-                    }
-                    if (col == k && i == 0) t.flags |= 2;   // one owner of sum w y per map (its last block)
-                }
-                for (int s = t.n_lds; s < 5; ++s) t.slot_layer[s] = S[i];
-                tasks.push_back(t);
             }
+            if (!own_w && (t.flags & 1) && rc.r0 == 0) {
+                own_w = true;
+                t.flags |= 4;
+            }
+            if (!own_y && rc.c1 == Y) {
+                own_y = true;
+                t.flags |= 8;
+            }
+            tasks.push_back(t);
         }
     }
     p->n_tasks = (int32_t)tasks.size();

@@ -116,18 +116,19 @@ struct RopeLaunch {
 
 // One workgroup task of the multi-layer statistics (feature x~ = [x_0; ...;
 // x_{k-1}; 1], blocks of 128 channels): for map `map`, the products of the
-// folded rows of feature block `row_blk` with the exact columns of up to four
-// column blocks (a source block j >= row_blk, or the target block, numbered
-// k), over every calibration row of a call.  The blocks the task reads are
-// staged in LDS slots: slot 0 holds the row block, and a column block that is
-// the row block itself (the diagonal block) reads slot 0 too.
+// folded rows of feature blocks rows[0], rows[1] with the exact columns of
+// feature blocks cols[0], cols[1] (block k is the target block; it is only
+// ever cols[1]), over every calibration row of a call.  Cell (rows[a],
+// cols[b]) is written when bit 2a + b of cell_mask is set.  The distinct
+// blocks of the task are staged in LDS slots 0..n_lds-1.
 struct MultiTask {
-    int32_t map, row_blk, n_cols, n_lds;
-    int32_t flags;            // 1: owns sum w x of the row block, 2: sum w y, 4: sum w
+    int32_t map, n_lds;
+    int32_t flags;            // 1, 2: owns sum w x of rows[0], rows[1]; 4: owns sum w; 8: owns sum w y
     int32_t wrow, kv, tgt_layer, tgt_head, src_head;
-    int32_t col_blk[4];       // feature block of each column block (k: the target)
-    int32_t col_slot[4];      // LDS slot each column block reads
-    int32_t slot_layer[5];    // source layer staged in each slot, -1: the target block
+    int32_t rows[2], cols[2];
+    int32_t row_slot[2], col_slot[2];
+    int32_t cell_mask;
+    int32_t slot_layer[4];    // source layer staged in each slot, -1: the target block
 };
 
 struct MultiArgs {

@@ -11,22 +11,26 @@
 // the work is a dense contraction over rows and runs on the matrix cores.
 //
 // Decomposition.  The feature splits into blocks of 128 channels: source
-// blocks 0..k-1 and the target block k.  A task is (map, row block i, up to
-// four column blocks j >= i, the target block included); the tasks of a map
-// cover the upper block triangle of G and the cross block of C once.  One
-// workgroup runs one task over every calibration row of the call and adds its
-// fp32 sums into G and C itself (it is the only writer of those elements), so
-// there are no partial sums, no reduction pass and no atomics.
+// blocks 0..k-1 and the target block k.  The work of a map is the set of
+// cells (i, j) of the block matrix with i, j < k (each unordered pair once:
+// G is symmetric, so a cell may be computed as (i, j) or as (j, i)) and the
+// cells (i, k) of C.  A task is a rectangle: two row blocks times two column
+// blocks, four cells (some marked unused when the cells do not pack evenly).
+// Every task does the same work, so the tasks of a map, launched together on
+// one XCD, move through the rows in step and read each staged row while it
+// is still in L2.  One workgroup runs one task over every calibration row of
+// the call and adds its fp32 sums into G and C itself (it is the only writer
+// of those elements): no partial sums, no reduction pass, no atomics.
 //
-// Per workgroup: four waves, one per SIMD.  Wave (p, q) owns rows 64p..64p+63
-// of the row block (two 32-row MFMA blocks) and half q of the task's column
-// blocks (2N 32-column blocks for N column blocks): 4N 32x32 accumulator
-// tiles.  Per 16-row K step it folds the fp32 weight into its two x
-// fragments, splits w x into hi = RNE_bf16(w x) and lo = RNE_bf16(w x - hi),
-// and issues 8N v_mfma_f32_32x32x16_bf16 against the exact bf16 columns.
+// Per workgroup: four waves, one per SIMD.  Wave w owns 64 rows of row block
+// rows[w / 2] (two 32-row MFMA blocks) and all eight 32-column blocks of the
+// two column blocks: 16 accumulator tiles, 32 v_mfma_f32_32x32x16_bf16 per
+// 16-row K step.  It folds the fp32 weight into its two x fragments and
+// splits w x into hi = RNE_bf16(w x) and lo = RNE_bf16(w x - hi); the
+// column operands are the exact bf16 rows.
 //
 // Staging.  A tile is 16 calibration rows of one sequence.  Its blocks (the
-// row block and the column blocks other than the diagonal one) move HBM -> LDS
+// distinct blocks among its two row and two column blocks) move HBM -> LDS
 // by global_load_lds_dwordx4 through a six-stage ring, six tiles ahead; each
 // 16-byte chunk c of row t sits at chunk c ^ 4(t mod 4) so the transposed
 // operand reads (ds_read_b64_tr_b16) are conflict free.  Rows past the end of
@@ -46,10 +50,10 @@ struct MCfg {
     static constexpr int KT = kMultiTileRows;      // 16 rows per tile: one K step
     static constexpr int ROW = 256;                // bytes per 128-channel row
     static constexpr int BLK = KT * ROW;           // 4096 bytes per block and stage
-    static constexpr int MAXS = 5;                 // LDS slots (row block + 4 column blocks)
+    static constexpr int MAXS = 4;                 // LDS slots (two row and two column blocks)
     static constexpr int OFF_W = MAXS * BLK;       // weights of the tile: [KT] fp32
     static constexpr int STAGE = OFF_W + KT * 4;
-    static constexpr int NST = 6;                  // ring stages
+    static constexpr int NST = 6;                  // ring stages (one per iteration of a loop trip)
     static constexpr int TRS = 33;                 // row stride (floats) of the transpose scratch
     static constexpr int OFF_T = NST * STAGE;
     static constexpr int LDS = OFF_T + 4 * 32 * TRS * 4;
@@ -60,8 +64,64 @@ struct MCfg {
 // Per-workgroup state that is uniform across the wave.
 struct MultiCtx {
     const uint16_t *slot_base[MCfg::MAXS];   // (layer, kv, head) base of each staged block
-    int64_t slot_sseq[MCfg::MAXS], slot_stok[MCfg::MAXS];
 };
+
+// All copies of one tile by one wave, under one save of M0 (and EXEC): NL
+// 16-byte copies into consecutive 4 KiB LDS slots starting at m0, then a
+// dword copy of the weights by lanes 0..3 into wm0 + 4 lane.  M0 and EXEC are
+// restored before the statement ends, so the compiler's use of them is
+// unaffected.
+template <int NL>
+__device__ __forceinline__ void dma_tile(const uint32_t (&voff)[NL], const void *const (&base)[NL], uint32_t m0,
+                                         const void *wg, uint32_t wm0) {
+    uint32_t keep_m0;
+    uint64_t keep_exec;
+#define CB_CP(i) "global_load_lds_dwordx4 %" #i "_v, %" #i "_s\n\t"
+    if constexpr (NL == 1) {
+        asm volatile("s_mov_b32 %[km], m0\n\ts_mov_b32 m0, %[m0]\n\t"
+                     "global_load_lds_dwordx4 %[v0], %[s0]\n\t"
+                     "s_mov_b32 m0, %[wm]\n\ts_mov_b64 %[ke], exec\n\ts_mov_b64 exec, 15\n\t"
+                     "global_load_lds_dword %[wg], off\n\ts_mov_b64 exec, %[ke]\n\ts_mov_b32 m0, %[km]"
+                     : [km] "=&s"(keep_m0), [ke] "=&s"(keep_exec)
+                     : [m0] "s"(m0), [v0] "v"(voff[0]), [s0] "s"(base[0]), [wm] "s"(wm0), [wg] "v"(wg)
+                     : "memory");
+    } else if constexpr (NL == 2) {
+        asm volatile("s_mov_b32 %[km], m0\n\ts_mov_b32 m0, %[m0]\n\t"
+                     "global_load_lds_dwordx4 %[v0], %[s0]\n\ts_add_u32 m0, m0, 0x1000\n\t"
+                     "global_load_lds_dwordx4 %[v1], %[s1]\n\t"
+                     "s_mov_b32 m0, %[wm]\n\ts_mov_b64 %[ke], exec\n\ts_mov_b64 exec, 15\n\t"
+                     "global_load_lds_dword %[wg], off\n\ts_mov_b64 exec, %[ke]\n\ts_mov_b32 m0, %[km]"
+                     : [km] "=&s"(keep_m0), [ke] "=&s"(keep_exec)
+                     : [m0] "s"(m0), [v0] "v"(voff[0]), [s0] "s"(base[0]), [v1] "v"(voff[1]), [s1] "s"(base[1]),
+                       [wm] "s"(wm0), [wg] "v"(wg)
+                     : "memory", "scc");
+    } else if constexpr (NL == 3) {
+        asm volatile("s_mov_b32 %[km], m0\n\ts_mov_b32 m0, %[m0]\n\t"
+                     "global_load_lds_dwordx4 %[v0], %[s0]\n\ts_add_u32 m0, m0, 0x1000\n\t"
+                     "global_load_lds_dwordx4 %[v1], %[s1]\n\ts_add_u32 m0, m0, 0x1000\n\t"
+                     "global_load_lds_dwordx4 %[v2], %[s2]\n\t"
+                     "s_mov_b32 m0, %[wm]\n\ts_mov_b64 %[ke], exec\n\ts_mov_b64 exec, 15\n\t"
+                     "global_load_lds_dword %[wg], off\n\ts_mov_b64 exec, %[ke]\n\ts_mov_b32 m0, %[km]"
+                     : [km] "=&s"(keep_m0), [ke] "=&s"(keep_exec)
+                     : [m0] "s"(m0), [v0] "v"(voff[0]), [s0] "s"(base[0]), [v1] "v"(voff[1]), [s1] "s"(base[1]),
+                       [v2] "v"(voff[2]), [s2] "s"(base[2]), [wm] "s"(wm0), [wg] "v"(wg)
+                     : "memory", "scc");
+    } else {
+        asm volatile("s_mov_b32 %[km], m0\n\ts_mov_b32 m0, %[m0]\n\t"
+                     "global_load_lds_dwordx4 %[v0], %[s0]\n\ts_add_u32 m0, m0, 0x1000\n\t"
+                     "global_load_lds_dwordx4 %[v1], %[s1]\n\ts_add_u32 m0, m0, 0x1000\n\t"
+                     "global_load_lds_dwordx4 %[v2], %[s2]\n\ts_add_u32 m0, m0, 0x1000\n\t"
+                     "global_load_lds_dwordx4 %[v3], %[s3]\n\t"
+                     "s_mov_b32 m0, %[wm]\n\ts_mov_b64 %[ke], exec\n\ts_mov_b64 exec, 15\n\t"
+                     "global_load_lds_dword %[wg], off\n\ts_mov_b64 exec, %[ke]\n\ts_mov_b32 m0, %[km]"
+                     : [km] "=&s"(keep_m0), [ke] "=&s"(keep_exec)
+                     : [m0] "s"(m0), [v0] "v"(voff[0]), [s0] "s"(base[0]), [v1] "v"(voff[1]), [s1] "s"(base[1]),
+                       [v2] "v"(voff[2]), [s2] "s"(base[2]), [v3] "v"(voff[3]), [s3] "s"(base[3]),
+                       [wm] "s"(wm0), [wg] "v"(wg)
+                     : "memory", "scc");
+    }
+#undef CB_CP
+}
 
 // Adds the 32 x 32 tile held in the wave's transpose scratch `tr` (row i at
 // tr + 33 i) into global memory, two rows per step: mode 0 and 2 add it at
@@ -83,57 +143,70 @@ __device__ __forceinline__ void flush_rows(const float *tr, int lane, int mode, 
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 }
 
-// N: column blocks of the task.  YS: the task owns sum w y of its map (its
-// last column block is the target block), so it also sums w y on the VALU.
-template <int N, bool YS>
+// NL: blocks staged per tile (distinct blocks of the task).  HASY: the last
+// of them is the target block (it is only ever the second column block).
+// YS: the task also owns sum w y of its map: wave w sums w y over 32 of the
+// target's channels.
+template <int NL, bool HASY, bool YS>
 __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &tk, const MultiCtx &c,
                                            lds_char_t *lds, int wave, int lane) {
     using K = MCfg;
-    constexpr int E = 2 * N;                    // 32-column blocks of this wave
-    const int p = wave & 1, q = wave >> 1;
+    constexpr int E = 8;                        // 32-column blocks of every wave
+    constexpr int PER_TILE = NL + 1;            // copy instructions per tile and wave
+    const int rs = wave >> 1, half = wave & 1;  // row slot (0: rows[0], 1: rows[1]), 64-row half
     const uint32_t lds_base = (uint32_t)(uintptr_t)lds;
-    const int n_lds = tk.n_lds;
 
-    // ---- copy descriptors: wave w copies rows 4w..4w+3 of every staged block
+    // ---- copy descriptors: wave w copies rows 4w..4w+3 of every staged block.
+    // A cursor walks the call's tiles in order (16 rows on, or on to the next
+    // sequence); tiles past the end repeat the last one with zero weights.
     const int crow = 4 * wave + (lane >> 4);
     const uint32_t cchunk = (uint32_t)((lane & 15) ^ (4 * (crow & 3))) * 16u;
-    uint32_t cstep[K::MAXS];                    // bytes between consecutive calibration rows
+    const uint32_t sstep = (uint32_t)(a.ss.tok * 2 * (int64_t)a.stride);   // bytes between calibration rows
+    const uint32_t tstep = (uint32_t)(a.ts.tok * 2 * (int64_t)a.stride);
+    uint32_t voff_full[NL];                     // lane offsets of a full tile
+    auto slot_y = [](int s) { return HASY && s == NL - 1; };
 #pragma unroll
-    for (int s = 0; s < K::MAXS; ++s) cstep[s] = (uint32_t)(c.slot_stok[s] * 2 * (int64_t)a.stride);
+    for (int s = 0; s < NL; ++s) voff_full[s] = (uint32_t)crow * (slot_y(s) ? tstep : sstep) + cchunk;
     const float *wrow = a.w + (int64_t)tk.wrow * a.w_row_stride;
-    const int per_tile = n_lds + 1;             // copy instructions per tile and wave
-
-    struct TilePos {
-        uint32_t seq, r0, tmax;                 // sequence, first row, last valid row offset
-        bool live;
-    };
-    auto tile_at = [&](int u) {
-        TilePos t;
-        t.live = u < a.n_tiles;
-        const uint32_t v = (uint32_t)(t.live ? u : a.n_tiles - 1);
-        t.seq = fastdiv(v, a.TPS);
-        t.r0 = (v - t.seq * a.TPS.d) * K::KT;
-        t.tmax = min((uint32_t)K::KT - 1, a.rows_per_seq - 1 - t.r0);
-        return t;
-    };
-    auto issue = [&](int u, int st) {
-        const TilePos t = tile_at(u);
+    const uint32_t wr = 4 * wave + (lane & 3);  // the weight row this lane copies (lanes 0..3)
+    struct Cursor {
+        int u;                                  // tile index
+        uint32_t seq, r0;                       // sequence, first row of the tile
+        int64_t soff, toff;                     // element offsets of the tile in the source / target blocks
+        const float *wp;                        // weight of the tile's first row
+    } cur = {0, 0u, 0u, 0, 0, wrow};
+    const int64_t sadv = (int64_t)K::KT * a.stride * a.ss.tok, tadv = (int64_t)K::KT * a.stride * a.ts.tok;
+    auto issue = [&](int st) {
+        const bool live = cur.u < a.n_tiles;
+        const uint32_t tmax = min((uint32_t)K::KT - 1, a.rows_per_seq - 1 - cur.r0);
         const uint32_t stage = lds_base + st * K::STAGE;
-        const uint32_t row = min((uint32_t)crow, t.tmax);
-        const int64_t tok0 = (int64_t)t.r0 * a.stride;
+        const uint32_t row = min((uint32_t)crow, tmax);
+        uint32_t voff[NL];
+        const void *base[NL];
 #pragma unroll
-        for (int s = 0; s < K::MAXS; ++s) {
-            if (s < n_lds) {
-                const void *base = uniform_ptr(c.slot_base[s] + t.seq * c.slot_sseq[s] + tok0 * c.slot_stok[s]);
-                dma16_sbase(row * cstep[s] + cchunk, base,
-                            __builtin_amdgcn_readfirstlane(stage + s * K::BLK + wave * 1024));
+        for (int s = 0; s < NL; ++s) {
+            voff[s] = tmax == K::KT - 1 ? voff_full[s] : row * (slot_y(s) ? tstep : sstep) + cchunk;
+            base[s] = uniform_ptr(c.slot_base[s] + (slot_y(s) ? cur.toff : cur.soff));
+        }
+        const bool ok = live && wr <= tmax;
+        const void *g = ok ? (const void *)(cur.wp + (int64_t)wr * a.stride) : a.zero;
+        dma_tile<NL>(voff, base, __builtin_amdgcn_readfirstlane(stage + wave * 1024), g,
+                     __builtin_amdgcn_readfirstlane(stage + K::OFF_W + 16 * wave));
+        if (cur.u + 1 < a.n_tiles) {
+            cur.r0 += K::KT;
+            if (cur.r0 >= a.rows_per_seq) {
+                cur.r0 = 0;
+                cur.seq += 1;
+                cur.soff = (int64_t)cur.seq * a.ss.seq;
+                cur.toff = (int64_t)cur.seq * a.ts.seq;
+                cur.wp = wrow + (int64_t)cur.seq * a.seq_len;
+            } else {
+                cur.soff += sadv;
+                cur.toff += tadv;
+                cur.wp += K::KT * a.stride;
             }
         }
-        const uint32_t wr = 4 * wave + (lane & 3);
-        const bool ok = t.live && wr <= t.tmax;
-        const void *g = ok ? (const void *)(wrow + (int64_t)t.seq * a.seq_len + (int64_t)(t.r0 + wr) * a.stride)
-                           : a.zero;
-        dma4_lanes(g, __builtin_amdgcn_readfirstlane(stage + K::OFF_W + 16 * wave), 0xFull);
+        cur.u += 1;
     };
 
     // ---- operand geometry (transposed reads; see cb_stats_kernel.h)
@@ -142,20 +215,17 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
     const int cl = 2 * (g16 & 1) + (aa >> 1);
     const uint32_t lrow = tok_l * K::ROW + cl * 16 + (aa & 1) * 8;
     uint32_t xoff[2], coff[E];
+    const uint32_t xslot = (uint32_t)tk.row_slot[rs] * K::BLK;
 #pragma unroll
-    for (int r = 0; r < 2; ++r) xoff[r] = lrow + 64u * ((uint32_t)(2 * p + r) ^ (uint32_t)kk);
-    bool ecol_y[E];
+    for (int r = 0; r < 2; ++r) xoff[r] = xslot + lrow + 64u * ((uint32_t)(2 * half + r) ^ (uint32_t)kk);
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-        const int gi = q * E + e, b = gi >> 2, win = gi & 3;
-        coff[e] = (uint32_t)tk.col_slot[b] * K::BLK + lrow + 64u * ((uint32_t)win ^ (uint32_t)kk);
-        ecol_y[e] = tk.col_blk[b] == a.k;
-    }
+    for (int e = 0; e < E; ++e)
+        coff[e] = (uint32_t)tk.col_slot[e >> 2] * K::BLK + lrow + 64u * ((uint32_t)(e & 3) ^ (uint32_t)kk);
     const uint32_t lw = K::OFF_W + (lane >> 5) * 32;
-    const bool own_sumx = (tk.flags & 1) && q == 0;
+    const bool own_sumx = (tk.flags >> rs) & 1;
     const bool own_sumw = (tk.flags & 4) && wave == 0;
-    // entries of this wave that read the target block when it is the task's last column block
-    auto ycol = [&](int e) { return YS && q * E + e >= 4 * (N - 1); };
+    // the target block is column block 1 of a YS task: wave w sums w y over its window w
+    auto ycol = [&](int e) { return YS && e == 4 + wave; };
 
     struct Ops {
         bf16x8_t xr[2], cf[E];
@@ -165,9 +235,7 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
         bf16x8_t hi[2], lo[2];
     };
     f32x16_t acc[2 * E];
-    float sumx[2] = {0.f, 0.f}, sumy[E], sumw = 0.f;
-#pragma unroll
-    for (int e = 0; e < E; ++e) sumy[e] = 0.f;
+    float sumx[2] = {0.f, 0.f}, sumy = 0.f, sumw = 0.f;
     auto zero_acc = [&]() {
 #pragma unroll
         for (int t = 0; t < 2 * E; ++t)
@@ -213,10 +281,10 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
         sumw += ((o.w[0] + o.w[1]) + (o.w[2] + o.w[3])) + ((o.w[4] + o.w[5]) + (o.w[6] + o.w[7]));
     };
     auto sum_y = [&](const Ops &o) {
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-            if (!ycol(e)) continue;
-            const uint4 yv = __builtin_bit_cast(uint4, o.cf[e]);
+        // entry 4 + wave: selected with a uniform switch-free blend of the four candidates
+        if constexpr (YS) {
+            const bf16x8_t yf = wave == 0 ? o.cf[4] : wave == 1 ? o.cf[5] : wave == 2 ? o.cf[6] : o.cf[7];
+            const uint4 yv = __builtin_bit_cast(uint4, yf);
             const uint32_t yy[4] = {yv.x, yv.y, yv.z, yv.w};
             float py[8];
 #pragma unroll
@@ -224,7 +292,7 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
                 py[2 * i] = o.w[2 * i] * bf_lo(yy[i]);
                 py[2 * i + 1] = o.w[2 * i + 1] * bf_hi(yy[i]);
             }
-            sumy[e] += ((py[0] + py[1]) + (py[2] + py[3])) + ((py[4] + py[5]) + (py[6] + py[7]));
+            sumy += ((py[0] + py[1]) + (py[2] + py[3])) + ((py[4] + py[5]) + (py[6] + py[7]));
         }
     };
     auto fold = [&](Folded &f, const Ops &o) {
@@ -254,15 +322,18 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
     float *Cm = a.C + (int64_t)tk.map * a.P * a.d_t;
     const int P = a.P;
     auto flush = [&]() {
+        const int rb = tk.rows[rs];                          // feature block of this wave's rows
 #pragma unroll
         for (int r = 0; r < 2; ++r) {
-            const int R = 4 * tk.row_blk + 2 * p + r;            // 32-row block of G
+            const int R = 4 * rb + 2 * half + r;             // 32-row block of G
 #pragma unroll
             for (int e = 0; e < E; ++e) {
-                const int gi = q * E + e, b = gi >> 2, win = gi & 3;
-                const bool is_y = ecol_y[e];
-                const int Cc = 4 * tk.col_blk[b] + win;          // 32-column block (of G, or of C if is_y)
-                if (!is_y && Cc < R) continue;                   // below the diagonal: dropped
+                const int cb = e >> 2, win = e & 3;
+                if (!((tk.cell_mask >> (2 * rs + cb)) & 1)) continue;      // an unused cell
+                const int col = tk.cols[cb];
+                const bool is_y = col == a.k;
+                const int Cc = 4 * col + win;                // 32-column block (of G, or of C if is_y)
+                if (!is_y && col == rb && Cc < R) continue;  // below the diagonal of a diagonal block
                 const f32x16_t &t = acc[r * E + e];
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {
@@ -270,7 +341,7 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
                     tr[i * K::TRS + (lane & 31)] = t[v];
                 }
                 asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-                // mode 0: cross tile of C; 1: diagonal tile of G; 2: tile above the diagonal (+ mirror)
+                // mode 0: cross tile of C; 1: diagonal tile of G; 2: any other tile of G (+ its mirror)
                 const int mode = is_y ? 0 : (Cc == R ? 1 : 2);
                 float *dst = is_y ? Cm + (int64_t)(32 * R) * a.d_t + 32 * win
                                   : Gm + (int64_t)(32 * R) * P + 32 * Cc;
@@ -283,29 +354,23 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
         if (own_sumx) {
 #pragma unroll
             for (int r = 0; r < 2; ++r) {
-                const float s = sumx[r] + __shfl_xor(sumx[r], 32);
+                const float sx = sumx[r] + __shfl_xor(sumx[r], 32);
                 if (lane < 32) {
-                    const int ch = 128 * tk.row_blk + 64 * p + 32 * r + lane;
-                    Gm[(int64_t)ch * P + P - 1] += s;
-                    Gm[(int64_t)(P - 1) * P + ch] += s;
+                    const int ch = 128 * rb + 64 * half + 32 * r + lane;
+                    Gm[(int64_t)ch * P + P - 1] += sx;
+                    Gm[(int64_t)(P - 1) * P + ch] += sx;
                 }
             }
         }
         sumx[0] = sumx[1] = 0.f;
-        if (YS && p == 0) {
-#pragma unroll
-            for (int e = 0; e < E; ++e) {
-                if (!ycol(e)) continue;
-                const float s = sumy[e] + __shfl_xor(sumy[e], 32);
-                const int win = (q * E + e) & 3;
-                if (lane < 32) Cm[(int64_t)(P - 1) * a.d_t + 32 * win + lane] += s;
-            }
+        if (YS) {
+            const float sy = sumy + __shfl_xor(sumy, 32);
+            if (lane < 32) Cm[(int64_t)(P - 1) * a.d_t + 32 * wave + lane] += sy;
         }
-#pragma unroll
-        for (int e = 0; e < E; ++e) sumy[e] = 0.f;
+        sumy = 0.f;
         if (own_sumw) {
-            const float s = sumw + __shfl_xor(sumw, 32);
-            if (lane == 0) Gm[(int64_t)(P - 1) * P + P - 1] += s;
+            const float sw = sumw + __shfl_xor(sumw, 32);
+            if (lane == 0) Gm[(int64_t)(P - 1) * P + P - 1] += sw;
         }
         sumw = 0.f;
         zero_acc();
@@ -322,14 +387,14 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
     // needs to issue five other instructions).  Operand sets rotate with
     // period 3, folded sets with period 2: six iterations per loop trip.
 #pragma unroll
-    for (int u = 0; u < K::NST; ++u) issue(u, u);
+    for (int u = 0; u < K::NST; ++u) issue(u);                // tiles 0 .. NST-1 into stages 0 .. NST-1
     const int n_iter = (a.n_tiles + 5) / 6 * 6;              // padded with zero-weight tiles
     Ops o0, o1, o2;
     Folded f0, f1;
-    wait_vm_rt((K::NST - 1) * per_tile);                     // tile 0 has landed
+    wait_vm<(K::NST - 1) * PER_TILE>();                      // tile 0 has landed
     lds_barrier();
     read_ops(o0, 0);
-    wait_vm_rt((K::NST - 2) * per_tile);                     // tile 1 has landed
+    wait_vm<(K::NST - 2) * PER_TILE>();                      // tile 1 has landed
     lds_barrier();
     read_ops(o1, 1);
     fold(f0, o0);
@@ -352,12 +417,12 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
         for (int e = 0; e < E; ++e)
             if ((e < E / 2) == (half == 0)) o.cf[e] = tr_read8(S + coff[e], S + coff[e] + 4 * K::ROW);
     };
-    auto iteration = [&](int t, const Ops &oa, const Folded &fa, const Ops &ob, Folded &fb, Ops &oc) {
-        wait_vm_rt((K::NST - 3) * per_tile);                 // tile t+2 has landed
+    auto iteration = [&](const int i, const Ops &oa, const Folded &fa, const Ops &ob, Folded &fb, Ops &oc) {
+        wait_vm<(K::NST - 3) * PER_TILE>();                  // tile t+2 has landed
         lds_barrier();
-        issue(t + K::NST, t % K::NST);
+        issue(i);                                            // tile t + NST into the stage of tile t
         __builtin_amdgcn_sched_barrier(0);
-        read_half(oc, (t + 2) % K::NST, 0);
+        read_half(oc, (i + 2) % K::NST, 0);
         mma_hi(fa, oa);
         fold_row(fb, ob, 0);
 #pragma unroll
@@ -367,7 +432,7 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
             __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);            // three VALU
         }
         __builtin_amdgcn_sched_barrier(0);
-        read_half(oc, (t + 2) % K::NST, 1);
+        read_half(oc, (i + 2) % K::NST, 1);
         fold_row(fb, ob, 1);
         sum_w(ob);
         mma_lo(fa, oa);
@@ -381,15 +446,16 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
         __builtin_amdgcn_sched_barrier(0);
         if constexpr (YS) sum_y(ob);
     };
+    // t = 6 j + i: the stage of tile t is i, a constant in each unrolled iteration
     for (int c0 = 0; c0 < n_iter; c0 += a.chunk_tiles) {
         const int c1 = min(c0 + a.chunk_tiles, n_iter);
         for (int t = c0; t < c1; t += 6) {
-            iteration(t + 0, o0, f0, o1, f1, o2);
-            iteration(t + 1, o1, f1, o2, f0, o0);
-            iteration(t + 2, o2, f0, o0, f1, o1);
-            iteration(t + 3, o0, f1, o1, f0, o2);
-            iteration(t + 4, o1, f0, o2, f1, o0);
-            iteration(t + 5, o2, f1, o0, f0, o1);
+            iteration(0, o0, f0, o1, f1, o2);
+            iteration(1, o1, f1, o2, f0, o0);
+            iteration(2, o2, f0, o0, f1, o1);
+            iteration(3, o0, f1, o1, f0, o2);
+            iteration(4, o1, f0, o2, f1, o0);
+            iteration(5, o2, f1, o0, f0, o1);
         }
         flush();
     }
@@ -413,27 +479,21 @@ void stats_multi_kernel(MultiArgs a) {
     MultiCtx c;
 #pragma unroll
     for (int s = 0; s < K::MAXS; ++s) {
-        const int L = s < tk.n_lds ? tk.slot_layer[s] : tk.slot_layer[0];
-        if (L < 0) {
-            c.slot_base[s] = a.tgt + tk.tgt_layer * a.ts.layer + tk.kv * a.ts.kv + tk.tgt_head * a.ts.head;
-            c.slot_sseq[s] = a.ts.seq;
-            c.slot_stok[s] = a.ts.tok;
-        } else {
-            c.slot_base[s] = a.src + L * a.ss.layer + tk.kv * a.ss.kv + tk.src_head * a.ss.head;
-            c.slot_sseq[s] = a.ss.seq;
-            c.slot_stok[s] = a.ss.tok;
-        }
+        const int L = tk.slot_layer[s];
+        c.slot_base[s] = L < 0 ? a.tgt + tk.tgt_layer * a.ts.layer + tk.kv * a.ts.kv + tk.tgt_head * a.ts.head
+                               : a.src + L * a.ss.layer + tk.kv * a.ss.kv + tk.src_head * a.ss.head;
     }
-    const bool ys = (tk.flags & 2) != 0;
-    switch (tk.n_cols * 2 + (ys ? 1 : 0)) {
-        case 2: multi_wave<1, false>(a, tk, c, lds, wave, lane); break;
-        case 3: multi_wave<1, true>(a, tk, c, lds, wave, lane); break;
-        case 4: multi_wave<2, false>(a, tk, c, lds, wave, lane); break;
-        case 5: multi_wave<2, true>(a, tk, c, lds, wave, lane); break;
-        case 6: multi_wave<3, false>(a, tk, c, lds, wave, lane); break;
-        case 7: multi_wave<3, true>(a, tk, c, lds, wave, lane); break;
-        case 8: multi_wave<4, false>(a, tk, c, lds, wave, lane); break;
-        default: multi_wave<4, true>(a, tk, c, lds, wave, lane); break;
+    // variant: staged blocks (1..4), target block staged (HASY), sum w y owned (YS)
+    const bool hasy = tk.slot_layer[tk.n_lds - 1] < 0;
+    const int var = (tk.n_lds - 1) * 3 + (hasy ? ((tk.flags & 8) ? 2 : 1) : 0);
+    switch (var) {
+#define CB_V(NL_)                                                                   \
+        case (NL_ - 1) * 3 + 0: multi_wave<NL_, false, false>(a, tk, c, lds, wave, lane); break; \
+        case (NL_ - 1) * 3 + 1: multi_wave<NL_, true, false>(a, tk, c, lds, wave, lane); break;  \
+        case (NL_ - 1) * 3 + 2: multi_wave<NL_, true, true>(a, tk, c, lds, wave, lane); break;
+        CB_V(1) CB_V(2) CB_V(3) CB_V(4)
+#undef CB_V
+        default: break;
     }
 }
 
