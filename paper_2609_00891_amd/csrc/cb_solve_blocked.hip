@@ -8,16 +8,23 @@
 //   M = G + lambda_m D  (lambda_m = lambda, or lambda tr(G) / P; D = I, or
 //                        diag(1, .., 1, 0) with CB_RIDGE_BIAS_UNPENALIZED)
 //   1. left-looking blocked Cholesky M = L L^T in panels of 32 columns:
-//      panel = M[c0:, c0:c0+32] - L[c0:, :c0] L[c0:c0+32, :c0]^T (LDS-tiled),
-//      the 32 x 32 diagonal block factored in LDS, the rows below solved
-//      against it (one thread per row);
-//   2. forward substitution L Z = C by 32-row panels;
+//      panel = M[c0:, c0:c0+32] - L[c0:, :c0] L[c0:c0+32, :c0]^T as a
+//      register-blocked GEMM (8 x 4 outputs per thread, 16-wide chunks of the
+//      inner dimension double-buffered through LDS so the next chunk's global
+//      loads overlap this chunk's FMAs); the 32 x 32 diagonal block factored
+//      by one wave in LDS, which also forms its inverse by forward
+//      elimination and stores it, transposed, in the block's unused upper
+//      half; the rows below solved against it, one row per thread;
+//   2. forward substitution L Z = C by 32-row panels: the panel GEMM, then
+//      the panel's rows times the inverse of its diagonal block (formed and
+//      kept by the factorization), both 4 x 4 outputs per thread;
 //   3. back substitution L^T W~ = Z by 32-row panels, in place of Z;
 //   4. maps = (float) W~.
 // A pivot that is not positive and finite stops the system: info = its
 // 1-based column, maps zero-filled (the report of the register solver).
 //
-// Workspace per system: L (P x P fp64, lower triangle used) and Z (P x d_t
+// Workspace per system: L (P x P fp64: the lower triangle, plus the inverse
+// diagonal blocks in the upper halves of the diagonal blocks) and Z (P x d_t
 // fp64).  Systems are solved in batches that fit the workspace.
 #include <algorithm>
 
@@ -26,28 +33,42 @@
 namespace cb {
 namespace {
 
-constexpr int NB = 32;          // panel width
-constexpr int TRW = 64;         // rows per GEMM tile of the factorization
-constexpr int KC = 32;          // inner-dimension chunk
 constexpr int NT = 256;
-constexpr int LP = 33;          // padded LDS row (doubles)
+constexpr int NB = 32;          // panel width
+constexpr int KC = 16;          // inner-dimension chunk
+constexpr int KP = KC + 1;      // padded LDS row of a chunk (doubles)
+constexpr int TR = 256;         // rows per GEMM pass of the factorization
+constexpr int DP = NB + 1;      // padded row of the diagonal block
 constexpr int DTMAX = 128;
-constexpr int ZP = DTMAX + 1;
+constexpr int ZP = DTMAX + 1;   // padded row of a right-hand-side chunk
+
+// LDS (doubles): factorization: A chunks [2][TR][KP], B chunks [2][NB][KP];
+// substitutions: L chunks [2][NB][KP], Z chunks [2][KC][ZP], panel rhs [NB][ZP].
+constexpr int OFF_A = 0;
+constexpr int OFF_B = OFF_A + 2 * TR * KP;
+constexpr int OFF_L = 0;
+constexpr int OFF_Z = OFF_L + 2 * NB * KP;
+constexpr int OFF_R = OFF_Z + 2 * KC * ZP;
+constexpr int SH_WORK = std::max(OFF_B + 2 * NB * KP, OFF_R + NB * ZP);
+
+__device__ __forceinline__ void wave_sync_lds() {
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_wave_barrier();
+}
 
 __global__ __launch_bounds__(NT) void chol_solve_kernel(int32_t P, int32_t d_t, const float *__restrict__ G,
                                                         const float *__restrict__ C, float lambda, uint32_t flags,
                                                         double *__restrict__ ws, int64_t ws_stride, int32_t m0,
                                                         float *__restrict__ maps, int32_t *__restrict__ info) {
-    __shared__ double sA[TRW * LP];        // row tile chunk (factorization) / L panel chunk (solves)
-    __shared__ double sB[KC * ZP];         // panel rows chunk (factorization) / Z rows chunk (solves)
-    __shared__ double sD[NB * LP];         // the factored diagonal block
-    __shared__ double sR[NB * ZP];         // right-hand sides of one panel (solves)
-    __shared__ double sInv[NB];
+    __shared__ double sh[SH_WORK];
+    __shared__ double sD[NB * DP];         // the diagonal block of the current panel
+    __shared__ double sInv[NB];            // reciprocals of its diagonal
+    __shared__ double sV[NB * DP];         // the inverse of the diagonal block
     __shared__ double red[NT / 64];
     __shared__ int s_bad;
 
     const int m = m0 + blockIdx.x;
-    const int tid = threadIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     double *L = ws + (int64_t)blockIdx.x * ws_stride;
     double *Z = L + (int64_t)P * P;
     const float *Gm = G + (int64_t)m * P * P;
@@ -58,101 +79,162 @@ __global__ __launch_bounds__(NT) void chol_solve_kernel(int32_t P, int32_t d_t, 
     double tr = 0.0;
     for (int i = tid; i < P; i += NT) tr += (double)Gm[(int64_t)i * P + i];
     for (int o = 32; o > 0; o >>= 1) tr += __shfl_xor(tr, o);
-    if ((tid & 63) == 0) red[tid >> 6] = tr;
+    if (lane == 0) red[wave] = tr;
     if (tid == 0) s_bad = 0;
     __syncthreads();
     const double trace = (red[0] + red[1]) + (red[2] + red[3]);
     const double lam = (flags & CB_LAMBDA_RELATIVE) ? (double)lambda * trace / (double)P : (double)lambda;
     const int lam_last = (flags & CB_RIDGE_BIAS_UNPENALIZED) ? P - 1 : P;   // diagonal entries < lam_last get lambda
 
+    // Loads the inverse V of the 32 x 32 diagonal block at (c0, c0) into sV
+    // (lower triangular, zero outside the nb x nb block): its diagonal is
+    // 1 / L[c0+i][c0+i], its strictly lower part was stored transposed in the
+    // (otherwise unused) strictly upper part of the block by the factorization.
+    auto load_inv = [&](int c0, int nb) {
+        for (int e = tid; e < NB * NB; e += NT) {
+            const int i = e / NB, c = e % NB;
+            double v = 0.0;
+            if (i < nb && c < nb) {
+                if (c == i) v = 1.0 / L[(int64_t)(c0 + i) * P + c0 + i];
+                else if (c < i) v = L[(int64_t)(c0 + c) * P + c0 + i];
+            }
+            sV[i * DP + c] = v;
+        }
+    };
+
     // ================= 1. blocked Cholesky
+    double *sA = sh + OFF_A, *sB = sh + OFF_B;
+    const int cg = tid & 7, rg = tid >> 3;             // GEMM: columns 4cg..4cg+3, rows rg + 32 i
     for (int c0 = 0; c0 < P; c0 += NB) {
         const int nb = min(NB, P - c0);
-        // panel = M[c0:, c0:c0+nb] - L[c0:, :c0] L[c0:c0+nb, :c0]^T, into L
-        const int i0 = tid >> 3, j0 = (tid & 7) * 4;
-        for (int rt = c0; rt < P; rt += TRW) {
-            double acc[2][4] = {{0, 0, 0, 0}, {0, 0, 0, 0}};
-            for (int k0 = 0; k0 < c0; k0 += KC) {
-                for (int e = tid; e < TRW * KC; e += NT) {
-                    const int i = e / KC, kk = e % KC;
-                    sA[i * LP + kk] = rt + i < P ? L[(int64_t)(rt + i) * P + k0 + kk] : 0.0;
-                }
-                for (int e = tid; e < NB * KC; e += NT) {
-                    const int j = e / KC, kk = e % KC;
-                    sB[j * LP + kk] = j < nb ? L[(int64_t)(c0 + j) * P + k0 + kk] : 0.0;
-                }
-                __syncthreads();
-#pragma unroll 8
-                for (int kk = 0; kk < KC; ++kk) {
-                    const double a0 = sA[i0 * LP + kk], a1 = sA[(i0 + 32) * LP + kk];
+        const int nch = c0 / KC;                        // c0 is a multiple of 32
+        for (int rt = c0; rt < P; rt += TR) {
+            double acc[8][4];
 #pragma unroll
-                    for (int b = 0; b < 4; ++b) {
-                        const double bv = sB[(j0 + b) * LP + kk];
-                        acc[0][b] = fma(a0, bv, acc[0][b]);
-                        acc[1][b] = fma(a1, bv, acc[1][b]);
-                    }
+            for (int i = 0; i < 8; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
+            double pa[16], pb[2];
+            auto fetch = [&](int ch) {                  // chunk ch of L[rt:rt+256, :] and L[c0:c0+32, :]
+                const int k0 = ch * KC, kk = tid & 15;
+#pragma unroll
+                for (int q = 0; q < 16; ++q) {
+                    const int r = rt + (tid >> 4) + 16 * q;
+                    pa[q] = r < P ? L[(int64_t)r * P + k0 + kk] : 0.0;
                 }
+#pragma unroll
+                for (int q = 0; q < 2; ++q) {
+                    const int j = (tid >> 4) + 16 * q;
+                    pb[q] = j < nb ? L[(int64_t)(c0 + j) * P + k0 + kk] : 0.0;
+                }
+            };
+            auto stash = [&](int buf) {
+                const int kk = tid & 15;
+#pragma unroll
+                for (int q = 0; q < 16; ++q) sA[buf * TR * KP + ((tid >> 4) + 16 * q) * KP + kk] = pa[q];
+#pragma unroll
+                for (int q = 0; q < 2; ++q) sB[buf * NB * KP + ((tid >> 4) + 16 * q) * KP + kk] = pb[q];
+            };
+            if (nch > 0) fetch(0);
+            for (int ch = 0; ch < nch; ++ch) {
+                stash(ch & 1);
                 __syncthreads();
+                if (ch + 1 < nch) fetch(ch + 1);
+                const double *a = sA + (ch & 1) * TR * KP, *b = sB + (ch & 1) * NB * KP;
+#pragma unroll 4
+                for (int kk = 0; kk < KC; ++kk) {
+                    double av[8], bv[4];
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) av[i] = a[(rg + 32 * i) * KP + kk];
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) bv[j] = b[(4 * cg + j) * KP + kk];
+#pragma unroll
+                    for (int i = 0; i < 8; ++i)
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) acc[i][j] = fma(av[i], bv[j], acc[i][j]);
+                }
             }
 #pragma unroll
-            for (int a = 0; a < 2; ++a) {
-                const int r = rt + i0 + 32 * a;
+            for (int i = 0; i < 8; ++i) {
+                const int r = rt + rg + 32 * i;
                 if (r >= P) continue;
 #pragma unroll
-                for (int b = 0; b < 4; ++b) {
-                    const int c = c0 + j0 + b;
-                    if (j0 + b >= nb) continue;
+                for (int j = 0; j < 4; ++j) {
+                    const int c = c0 + 4 * cg + j;
+                    if (4 * cg + j >= nb) continue;
                     double v = (double)Gm[(int64_t)r * P + c];
                     if (r == c && c < lam_last) v += lam;
-                    L[(int64_t)r * P + c] = v - acc[a][b];
+                    L[(int64_t)r * P + c] = v - acc[i][j];
                 }
             }
+            __syncthreads();
         }
-        __syncthreads();
-        // factor the diagonal block in LDS
-        for (int e = tid; e < NB * NB; e += NT) {
-            const int i = e / NB, j = e % NB;
-            sD[i * LP + j] = (i < nb && j < nb && j <= i) ? L[(int64_t)(c0 + i) * P + c0 + j] : 0.0;
-        }
-        __syncthreads();
-        for (int j = 0; j < nb; ++j) {
-            if (tid == 0) {
-                const double d = sD[j * LP + j];
+        // factor the diagonal block: one wave, right-looking, in LDS
+        if (wave == 0) {
+            for (int e = lane; e < NB * NB; e += 64) {
+                const int i = e / NB, j = e % NB;
+                sD[i * DP + j] = (i < nb && j <= i) ? L[(int64_t)(c0 + i) * P + c0 + j] : 0.0;
+            }
+            wave_sync_lds();
+            int bad = 0;
+            for (int j = 0; j < nb; ++j) {
+                const double d = sD[j * DP + j];
                 if (!(d > 0.0) || !isfinite(d)) {
-                    s_bad = c0 + j + 1;
-                } else {
-                    const double s = sqrt(d);
-                    sD[j * LP + j] = s;
-                    sInv[j] = 1.0 / s;
+                    bad = c0 + j + 1;
+                    break;
+                }
+                const double s = sqrt(d), inv = 1.0 / s;
+                wave_sync_lds();
+                if (lane == 0) {
+                    sD[j * DP + j] = s;
+                    sInv[j] = inv;
+                }
+                if (lane > j && lane < nb) sD[lane * DP + j] *= inv;
+                wave_sync_lds();
+                for (int e = lane; e < NB * NB; e += 64) {
+                    const int i = e / NB, l = e % NB;
+                    if (i > j && l > j && l <= i && i < nb) sD[i * DP + l] -= sD[i * DP + j] * sD[l * DP + j];
+                }
+                wave_sync_lds();
+            }
+            if (lane == 0) s_bad = bad;
+            if (!bad) {
+                // V = L_dd^-1 by forward elimination on the identity, one row of V per step
+                for (int e = lane; e < NB * NB; e += 64) {
+                    const int i = e / NB, c = e % NB;
+                    sV[i * DP + c] = i == c ? 1.0 : 0.0;
+                }
+                wave_sync_lds();
+                for (int j = 0; j < nb; ++j) {
+                    if (lane < NB) sV[j * DP + lane] *= sInv[j];
+                    wave_sync_lds();
+                    for (int e = lane; e < (nb - 1 - j) * NB; e += 64) {
+                        const int i = j + 1 + e / NB, c = e % NB;
+                        sV[i * DP + c] -= sD[i * DP + j] * sV[j * DP + c];
+                    }
+                    wave_sync_lds();
                 }
             }
-            __syncthreads();
-            if (s_bad) break;
-            if (tid > j && tid < nb) sD[tid * LP + j] *= sInv[j];
-            __syncthreads();
-            for (int e = tid; e < NB * NB; e += NT) {
-                const int i = e / NB, l = e % NB;
-                if (i > j && l > j && l <= i && i < nb) sD[i * LP + l] -= sD[i * LP + j] * sD[l * LP + j];
-            }
-            __syncthreads();
         }
+        __syncthreads();
         if (s_bad) break;
         for (int e = tid; e < NB * NB; e += NT) {
             const int i = e / NB, j = e % NB;
-            if (i < nb && j <= i) L[(int64_t)(c0 + i) * P + c0 + j] = sD[i * LP + j];
+            if (i < nb && j <= i) L[(int64_t)(c0 + i) * P + c0 + j] = sD[i * DP + j];
+            if (i < nb && j < i) L[(int64_t)(c0 + j) * P + c0 + i] = sV[i * DP + j];   // V, transposed, above
         }
-        // rows below: L[r][c0:c0+32] = panel row solved against the diagonal block
+        // rows below: x L_dd^T = panel row, column by column
         for (int r = c0 + NB + tid; r < P; r += NT) {
-            asm volatile("" ::: "memory");              // keeps the block's LDS reads inside the row loop
+            const double *dd = sD, *iv = sInv;          // opaque: one base register, immediate offsets
+            asm volatile("" : "+v"(dd), "+v"(iv));
             double x[NB];
 #pragma unroll
             for (int j = 0; j < NB; ++j) x[j] = L[(int64_t)r * P + c0 + j];
 #pragma unroll
             for (int j = 0; j < NB; ++j) {
-                double s = x[j];
+                x[j] *= iv[j];
 #pragma unroll
-                for (int i = 0; i < j; ++i) s -= x[i] * sD[j * LP + i];
-                x[j] = s * sInv[j];
+                for (int i = j + 1; i < NB; ++i) x[i] = fma(-x[j], dd[i * DP + j], x[i]);
             }
 #pragma unroll
             for (int j = 0; j < NB; ++j) L[(int64_t)r * P + c0 + j] = x[j];
@@ -165,122 +247,134 @@ __global__ __launch_bounds__(NT) void chol_solve_kernel(int32_t P, int32_t d_t, 
         return;
     }
 
-    // ================= 2. forward substitution L Z = C
-    const int ri = tid >> 4, cj = (tid & 15) * 8;          // GEMM outputs: rows ri, ri+16; cols cj..cj+7
-    for (int c0 = 0; c0 < P; c0 += NB) {
-        const int nb = min(NB, P - c0);
-        double acc[2][8];
+    // ================= 2., 3. substitutions (Z then W~ in Z)
+    double *sL = sh + OFF_L, *sZ = sh + OFF_Z, *sR = sh + OFF_R;
+    const int ri = tid >> 5, cj = tid & 31;            // GEMM: rows ri + 8 q, columns cj + 32 n
+    // acc[q][n] = sum over k in [k_lo, k_hi) of Lop(i, k) Z[k][c], i = ri + 8 q, c = cj + 32 n, where
+    // Lop(i, k) = L[c0 + i][k] (forward) or L[k][c0 + i] (backward).
+    auto panel_gemm = [&](double (&acc)[4][4], int c0, int nb, int k_lo, int k_hi, bool backward) {
 #pragma unroll
-        for (int a = 0; a < 2; ++a)
+        for (int q = 0; q < 4; ++q)
 #pragma unroll
-            for (int b = 0; b < 8; ++b) acc[a][b] = 0.0;
-        for (int k0 = 0; k0 < c0; k0 += KC) {
-            for (int e = tid; e < NB * KC; e += NT) {
-                const int i = e / KC, kk = e % KC;
-                sA[i * LP + kk] = i < nb ? L[(int64_t)(c0 + i) * P + k0 + kk] : 0.0;
+            for (int n = 0; n < 4; ++n) acc[q][n] = 0.0;
+        const int nch = (k_hi - k_lo + KC - 1) / KC;
+        double pl[2], pz[8];
+        auto fetch = [&](int ch) {
+            const int k0 = k_lo + ch * KC;
+#pragma unroll
+            for (int q = 0; q < 2; ++q) {               // 32 x 16 operand: (i, kk)
+                const int e = tid + NT * q;
+                int i, kk;
+                if (backward) { kk = e / NB; i = e % NB; } else { i = e / KC; kk = e % KC; }
+                const int k = k0 + kk;
+                pl[q] = (i < nb && k < k_hi) ? (backward ? L[(int64_t)k * P + c0 + i] : L[(int64_t)(c0 + i) * P + k])
+                                             : 0.0;
             }
-            for (int e = tid; e < KC * DTMAX; e += NT) {
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {               // 16 x 128 operand: (kk, c)
+                const int e = tid + NT * q;
                 const int kk = e / DTMAX, c = e % DTMAX;
-                sB[kk * ZP + c] = c < d_t ? Z[(int64_t)(k0 + kk) * d_t + c] : 0.0;
+                const int k = k0 + kk;
+                pz[q] = (k < k_hi && c < d_t) ? Z[(int64_t)k * d_t + c] : 0.0;
             }
+        };
+        auto stash = [&](int buf) {
+#pragma unroll
+            for (int q = 0; q < 2; ++q) {
+                const int e = tid + NT * q;
+                int i, kk;
+                if (backward) { kk = e / NB; i = e % NB; } else { i = e / KC; kk = e % KC; }
+                sL[buf * NB * KP + i * KP + kk] = pl[q];
+            }
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const int e = tid + NT * q;
+                sZ[buf * KC * ZP + (e / DTMAX) * ZP + e % DTMAX] = pz[q];
+            }
+        };
+        if (nch > 0) fetch(0);
+        for (int ch = 0; ch < nch; ++ch) {
+            stash(ch & 1);
             __syncthreads();
+            if (ch + 1 < nch) fetch(ch + 1);
+            const double *a = sL + (ch & 1) * NB * KP, *b = sZ + (ch & 1) * KC * ZP;
 #pragma unroll 4
             for (int kk = 0; kk < KC; ++kk) {
-                const double a0 = sA[ri * LP + kk], a1 = sA[(ri + 16) * LP + kk];
+                double av[4], bv[4];
 #pragma unroll
-                for (int b = 0; b < 8; ++b) {
-                    const double zv = sB[kk * ZP + cj + b];
-                    acc[0][b] = fma(a0, zv, acc[0][b]);
-                    acc[1][b] = fma(a1, zv, acc[1][b]);
-                }
+                for (int q = 0; q < 4; ++q) av[q] = a[(ri + 8 * q) * KP + kk];
+#pragma unroll
+                for (int n = 0; n < 4; ++n) bv[n] = b[kk * ZP + cj + 32 * n];
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+#pragma unroll
+                    for (int n = 0; n < 4; ++n) acc[q][n] = fma(av[q], bv[n], acc[q][n]);
             }
-            __syncthreads();
+        }
+    };
+
+    // Z[c0 + i][c] = sum_k V[i][k] R[k][c]  (forward, V = L_dd^-1), or
+    //               sum_k V[k][i] R[k][c]  (backward, V^T = L_dd^-T), R the panel
+    // right-hand sides in sR; 4 x 4 outputs per thread.
+    auto apply_inv = [&](int c0, int nb, bool transposed) {
+        double acc[4][4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int n = 0; n < 4; ++n) acc[q][n] = 0.0;
+#pragma unroll 4
+        for (int k = 0; k < NB; ++k) {
+            double av[4], bv[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) av[q] = transposed ? sV[k * DP + ri + 8 * q] : sV[(ri + 8 * q) * DP + k];
+#pragma unroll
+            for (int n = 0; n < 4; ++n) bv[n] = sR[k * ZP + cj + 32 * n];
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+                for (int n = 0; n < 4; ++n) acc[q][n] = fma(av[q], bv[n], acc[q][n]);
         }
 #pragma unroll
-        for (int a = 0; a < 2; ++a)
+        for (int q = 0; q < 4; ++q)
 #pragma unroll
-            for (int b = 0; b < 8; ++b) {
-                const int i = ri + 16 * a, c = cj + b;
-                sR[i * ZP + c] = (i < nb && c < d_t) ? (double)Cm[(int64_t)(c0 + i) * d_t + c] - acc[a][b] : 0.0;
+            for (int n = 0; n < 4; ++n) {
+                const int i = ri + 8 * q, c = cj + 32 * n;
+                if (i < nb && c < d_t) Z[(int64_t)(c0 + i) * d_t + c] = acc[q][n];
             }
-        for (int e = tid; e < NB * NB; e += NT) {
-            const int i = e / NB, j = e % NB;
-            sD[i * LP + j] = (i < nb && j <= i) ? L[(int64_t)(c0 + i) * P + c0 + j] : 0.0;
-        }
+    };
+    // forward: Z[c0:c1] = L_dd^-1 (C[c0:c1] - L[c0:c1, :c0] Z[:c0])
+    for (int c0 = 0; c0 < P; c0 += NB) {
+        const int nb = min(NB, P - c0);
+        double acc[4][4];
+        panel_gemm(acc, c0, nb, 0, c0, false);
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int n = 0; n < 4; ++n) {
+                const int i = ri + 8 * q, c = cj + 32 * n;
+                sR[i * ZP + c] = (i < nb && c < d_t) ? (double)Cm[(int64_t)(c0 + i) * d_t + c] - acc[q][n] : 0.0;
+            }
+        load_inv(c0, nb);
         __syncthreads();
-        if (tid < d_t) {
-            double z[NB];
-#pragma unroll
-            for (int i = 0; i < NB; ++i) {
-                double s = sR[i * ZP + tid];
-#pragma unroll
-                for (int l = 0; l < i; ++l) s -= sD[i * LP + l] * z[l];
-                z[i] = i < nb ? s / sD[i * LP + i] : 0.0;
-            }
-#pragma unroll
-            for (int i = 0; i < NB; ++i)
-                if (i < nb) Z[(int64_t)(c0 + i) * d_t + tid] = z[i];
-        }
+        apply_inv(c0, nb, false);
         __syncthreads();
     }
-
-    // ================= 3. back substitution L^T W~ = Z (W~ overwrites Z)
+    // backward: W[c0:c1] = L_dd^-T (Z[c0:c1] - L[c1:, c0:c1]^T W[c1:])
     const int last = ((P - 1) / NB) * NB;
     for (int c0 = last; c0 >= 0; c0 -= NB) {
         const int nb = min(NB, P - c0), c1 = c0 + nb;
-        double acc[2][8];
+        double acc[4][4];
+        panel_gemm(acc, c0, nb, c1, P, true);
 #pragma unroll
-        for (int a = 0; a < 2; ++a)
+        for (int q = 0; q < 4; ++q)
 #pragma unroll
-            for (int b = 0; b < 8; ++b) acc[a][b] = 0.0;
-        for (int k0 = c1; k0 < P; k0 += KC) {
-            // L[k][c0 + i] for k in the chunk, stored as sA[i][kk]
-            for (int e = tid; e < KC * NB; e += NT) {
-                const int kk = e / NB, i = e % NB;
-                sA[i * LP + kk] = (k0 + kk < P) ? L[(int64_t)(k0 + kk) * P + c0 + i] : 0.0;
+            for (int n = 0; n < 4; ++n) {
+                const int i = ri + 8 * q, c = cj + 32 * n;
+                sR[i * ZP + c] = (i < nb && c < d_t) ? Z[(int64_t)(c0 + i) * d_t + c] - acc[q][n] : 0.0;
             }
-            for (int e = tid; e < KC * DTMAX; e += NT) {
-                const int kk = e / DTMAX, c = e % DTMAX;
-                sB[kk * ZP + c] = (k0 + kk < P && c < d_t) ? Z[(int64_t)(k0 + kk) * d_t + c] : 0.0;
-            }
-            __syncthreads();
-#pragma unroll 4
-            for (int kk = 0; kk < KC; ++kk) {
-                const double a0 = sA[ri * LP + kk], a1 = sA[(ri + 16) * LP + kk];
-#pragma unroll
-                for (int b = 0; b < 8; ++b) {
-                    const double zv = sB[kk * ZP + cj + b];
-                    acc[0][b] = fma(a0, zv, acc[0][b]);
-                    acc[1][b] = fma(a1, zv, acc[1][b]);
-                }
-            }
-            __syncthreads();
-        }
-#pragma unroll
-        for (int a = 0; a < 2; ++a)
-#pragma unroll
-            for (int b = 0; b < 8; ++b) {
-                const int i = ri + 16 * a, c = cj + b;
-                sR[i * ZP + c] = (i < nb && c < d_t) ? Z[(int64_t)(c0 + i) * d_t + c] - acc[a][b] : 0.0;
-            }
-        for (int e = tid; e < NB * NB; e += NT) {
-            const int i = e / NB, j = e % NB;
-            sD[i * LP + j] = (i < nb && j <= i) ? L[(int64_t)(c0 + i) * P + c0 + j] : 0.0;
-        }
+        load_inv(c0, nb);
         __syncthreads();
-        if (tid < d_t) {
-            double w[NB];
-#pragma unroll
-            for (int i = NB - 1; i >= 0; --i) {
-                double s = sR[i * ZP + tid];
-#pragma unroll
-                for (int l = i + 1; l < NB; ++l) s -= sD[l * LP + i] * w[l];
-                w[i] = i < nb ? s / sD[i * LP + i] : 0.0;
-            }
-#pragma unroll
-            for (int i = 0; i < NB; ++i)
-                if (i < nb) Z[(int64_t)(c0 + i) * d_t + tid] = w[i];
-        }
+        apply_inv(c0, nb, true);
         __syncthreads();
     }
 
