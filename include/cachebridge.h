@@ -424,9 +424,12 @@ typedef struct {
  * multi-layer feature, with the arguments, accuracy and symmetry of the
  * single-layer calls and no token limit; the products run on the matrix cores
  * (the work grows as P^2 per row).  G and C must not overlap other buffers of
- * the call.  Solve with cb_ridge_solve_ws.  The centered calls and cb_apply
- * return CB_ERR_UNSUPPORTED for such a plan.  Errors as in cb_plan_create,
- * plus CB_ERR_INVALID_ARGUMENT for a source layer selected twice by one map.
+ * the call.  Solve with cb_ridge_solve_ws.  cb_apply maps a sender cache with
+ * the P x d_t maps, every token: out = RNE_bf16([x_0, ..., x_{k-1}, 1] maps[m])
+ * (coefficients as two bf16 terms, fp32 sums and bias, one rounding).  The
+ * centered and means calls return CB_ERR_UNSUPPORTED for such a plan.  Errors
+ * as in cb_plan_create, plus CB_ERR_INVALID_ARGUMENT for a source layer
+ * selected twice by one map.
  */
 cb_status cb_plan_create_multi(const cb_head_map_multi *map, const cb_cache *src_geom, const cb_cache *tgt_geom,
                                int32_t sample_stride, cb_plan **out);

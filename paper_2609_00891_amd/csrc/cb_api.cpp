@@ -31,6 +31,9 @@ struct cb_plan {
     int32_t k = 1, P = 0, sample_stride = 1;
     int32_t n_tasks = 0;
     cb::MultiTask *d_tasks = nullptr;
+    cb::ApplyMultiMap *d_amaps = nullptr;   // multi-layer application: map records, visiting order, layers
+    int32_t *d_aorder = nullptr;
+    int32_t *d_alayers = nullptr;
     // statistics schedule
     int32_t n_items = 0;
     int32_t max_chunks = 1;
@@ -261,6 +264,9 @@ cb_status cb_plan_destroy(cb_plan *p) {
     hipFree(p->d_wlo);
     hipFree(p->d_bias);
     hipFree(p->d_tasks);
+    hipFree(p->d_amaps);
+    hipFree(p->d_aorder);
+    hipFree(p->d_alayers);
     delete p;
     return ok();
 }
@@ -569,15 +575,26 @@ cb_status cb_plan_create_multi(const cb_head_map_multi *map, const cb_cache *src
     }
     p->n_tasks = (int32_t)tasks.size();
 
+    std::vector<cb::ApplyMultiMap> amaps(n);
+    for (int m = 0; m < n; ++m) amaps[m] = {map->tgt_layer[m], map->tgt_head[m], map->kv[m], map->src_head[m]};
+    const size_t wsplit = (size_t)n * d_t * (size_t)(k * d_s) * sizeof(uint16_t);
     bool okm = hipMalloc(&p->d_tasks, sizeof(cb::MultiTask) * tasks.size()) == hipSuccess &&
-               hipMalloc(&p->d_zero, 256) == hipSuccess;
+               hipMalloc(&p->d_zero, 256) == hipSuccess &&
+               hipMalloc(&p->d_amaps, sizeof(cb::ApplyMultiMap) * n) == hipSuccess &&
+               hipMalloc(&p->d_aorder, sizeof(int32_t) * n) == hipSuccess &&
+               hipMalloc(&p->d_alayers, sizeof(int32_t) * (size_t)n * k) == hipSuccess &&
+               hipMalloc(&p->d_whi, wsplit) == hipSuccess && hipMalloc(&p->d_wlo, wsplit) == hipSuccess &&
+               hipMalloc(&p->d_bias, sizeof(float) * n * d_t) == hipSuccess;
     if (!okm) {
         (void)hipGetLastError();
         cb_plan_destroy(p);
         return fail(CB_ERR_OUT_OF_MEMORY, "plan allocation failed");
     }
     if (hipMemset(p->d_zero, 0, 256) != hipSuccess ||
-        hipMemcpy(p->d_tasks, tasks.data(), sizeof(cb::MultiTask) * tasks.size(), hipMemcpyHostToDevice) != hipSuccess) {
+        hipMemcpy(p->d_tasks, tasks.data(), sizeof(cb::MultiTask) * tasks.size(), hipMemcpyHostToDevice) != hipSuccess ||
+        hipMemcpy(p->d_amaps, amaps.data(), sizeof(cb::ApplyMultiMap) * n, hipMemcpyHostToDevice) != hipSuccess ||
+        hipMemcpy(p->d_aorder, order.data(), sizeof(int32_t) * n, hipMemcpyHostToDevice) != hipSuccess ||
+        hipMemcpy(p->d_alayers, map->src_layers, sizeof(int32_t) * (size_t)n * k, hipMemcpyHostToDevice) != hipSuccess) {
         cb_plan_destroy(p);
         return fail(CB_ERR_DEVICE, "copying the schedule to the device failed");
     }
@@ -956,7 +973,51 @@ cb_status cb_rope(const cb_cache *in, const cb_cache *out, const float *table, i
 
 cb_status cb_apply(cb_plan *p, const float *maps, const cb_cache *src, const cb_cache *tgt_out, void *stream) {
     if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
-    if (p->multi) return fail(CB_ERR_UNSUPPORTED, "cb_apply of multi-layer maps is not available");
+    if (p->multi) {
+        if (p->duplicate_targets)
+            return fail(CB_ERR_INVALID_ARGUMENT, "the plan maps some target (layer, kv, head) more than once; "
+                                                 "cb_apply needs one map per target");
+        if (!maps) return fail(CB_ERR_INVALID_ARGUMENT, "maps is NULL");
+        if (cb_status s = check_cache("src", src, p->L_s, p->H_s, p->d_s)) return s;
+        if (cb_status s = check_cache("tgt_out", tgt_out, p->L_t, p->H_t, p->d_t)) return s;
+        if (src->n_seqs != tgt_out->n_seqs || src->seq_len != tgt_out->seq_len)
+            return fail(CB_ERR_SHAPE, "src and tgt_out disagree on n_seqs / seq_len");
+        if (((uintptr_t)maps) % 4) return fail(CB_ERR_MISALIGNED, "maps must be 4-byte aligned");
+        const int64_t N = (int64_t)src->n_seqs * src->seq_len;
+        if (N > (int64_t)INT32_MAX - 4096) return fail(CB_ERR_UNSUPPORTED, "too many tokens in one call");
+        if (cb_status s = check_device(p)) return s;
+        hipStream_t st = (hipStream_t)stream;
+        const int Pm1 = p->P - 1;
+        if (cb::launch_split_maps(p->n_maps, Pm1, p->d_t, maps, p->d_whi, p->d_wlo, p->d_bias, st) != hipSuccess)
+            return fail(CB_ERR_DEVICE, "map split launch failed");
+        if (N == 0) return ok();
+        cb::ApplyMultiArgs a = {};
+        a.src = (const uint16_t *)src->data;
+        a.out = (uint16_t *)tgt_out->data;
+        a.ss = strides_of(src);
+        a.os = strides_of(tgt_out);
+        a.T = cb::make_fastdiv((uint32_t)src->seq_len);
+        a.N = N;
+        a.k = p->k;
+        a.d_t = p->d_t;
+        a.n_maps = p->n_maps;
+        a.n_tiles = (int32_t)((N + 255) / 256);
+        a.group = 4;
+        const int64_t n_groups = (p->n_maps + a.group - 1) / a.group;
+        const int64_t n_tasks = n_groups * a.n_tiles * a.group;
+        if (n_tasks > (int64_t)INT32_MAX - 8) return fail(CB_ERR_UNSUPPORTED, "too many application workgroups");
+        a.n_tasks = (int32_t)n_tasks;
+        a.per_xcd = (a.n_tasks + 7) / 8;
+        a.maps = p->d_amaps;
+        a.order = p->d_aorder;
+        a.src_layers = p->d_alayers;
+        a.w_hi = p->d_whi;
+        a.w_lo = p->d_wlo;
+        a.bias = p->d_bias;
+        if (cb::launch_apply_multi(a, st) != hipSuccess)
+            return fail(CB_ERR_DEVICE, "multi-layer application kernel launch failed");
+        return ok();
+    }
     if (p->duplicate_targets)
         return fail(CB_ERR_INVALID_ARGUMENT, "the plan maps some target (layer, kv, head) more than once; "
                                              "cb_apply needs one map per target");

@@ -150,6 +150,29 @@ struct MultiArgs {
     float *G, *C;
 };
 
+// One map of the multi-layer application.
+struct ApplyMultiMap {
+    int32_t tgt_layer, tgt_head, kv, src_head;
+};
+
+struct ApplyMultiArgs {
+    const uint16_t *src;
+    uint16_t *out;
+    Strides ss, os;
+    FastDiv T;                // tokens per sequence
+    int64_t N;                // tokens (n_seqs * seq_len)
+    int32_t k, d_t, n_maps;
+    int32_t n_tiles;          // 256-token tiles per map
+    int32_t group;            // maps per group (visited token-tile first)
+    int32_t n_tasks, per_xcd;
+    const ApplyMultiMap *maps;
+    const int32_t *order;     // [n_maps] maps in visiting order
+    const int32_t *src_layers;// [n_maps][k]
+    const uint16_t *w_hi;     // [n_maps][d_t][k * 128] bf16, transposed maps
+    const uint16_t *w_lo;
+    const float *bias;        // [n_maps][d_t]
+};
+
 // Launchers (return hipError_t of the launch).
 hipError_t launch_rope_table(int32_t d, int32_t n_pos, double theta, float *table, hipStream_t s);
 hipError_t launch_rope(const RopeLaunch &L, hipStream_t s);
@@ -170,6 +193,7 @@ hipError_t launch_solve_centered(int32_t n_maps, int32_t d_s, int32_t d_t, const
                                  hipStream_t s);
 hipError_t launch_fill_zero(float *p, int64_t n, hipStream_t s);
 hipError_t launch_stats_multi(const MultiArgs &a, hipStream_t s);
+hipError_t launch_apply_multi(const ApplyMultiArgs &a, hipStream_t s);
 int64_t solve_blocked_bytes_per_system(int32_t P, int32_t d_t);
 hipError_t launch_solve_blocked(int32_t n_maps, int32_t P, int32_t d_t, const float *G, const float *C, float lambda,
                                 uint32_t flags, void *ws, int64_t ws_bytes, float *maps, int32_t *info,

@@ -3,9 +3,12 @@ source layers; P = k d_s + 1) against the fp64 oracle, through the C ABI.
 
 Statistics from cb_stats_accumulate on a cb_plan_create_multi plan, solved by
 cb_ridge_solve_ws (blocked fp64 Cholesky), compared with oracle.stats_multi and
-oracle.ridge_solve on the exact bits the GPU consumed.  Bars (relative
-Frobenius error per map): G and C 1e-4, maps 1e-3; the solver alone (same fp32
-moments on both sides, maps rounded to fp32) 1e-6; G exactly symmetric.
+oracle.ridge_solve on the exact bits the GPU consumed; cb_apply of the maps
+compared with oracle.apply_multi on the same fp32 maps.  Bars (relative
+Frobenius error per map): G and C 1e-4, maps 1e-3, applied caches 1e-3 with
+every element within one bf16 ulp plus 1e-4 of its map's RMS output; the solver
+alone (same fp32 moments on both sides, maps rounded to fp32) 1e-6; G exactly
+symmetric.
 """
 import os
 import sys
@@ -256,8 +259,10 @@ def test_multi_device_side_argument_errors(cb):
     C = torch.zeros((n, P, 128), dtype=torch.float32, device="cuda")
     with pytest.raises(cb.CacheBridgeError, match="CB_ERR_SHAPE"):
         cb.cb_stats_accumulate(plan, src[:2], tgt, w, G, C)              # wrong source layer count
-    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_UNSUPPORTED"):
-        cb.cb_apply(plan, C, src, tgt)
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_SHAPE"):
+        cb.cb_apply(plan, C, src, tgt[:1])                               # wrong target layer count
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_SHAPE"):
+        cb.cb_apply(plan, C, src[:, :, :, :, :16], tgt)                  # token counts disagree
     sums = torch.zeros((n, 257), dtype=torch.float64, device="cuda")
     with pytest.raises(cb.CacheBridgeError, match="CB_ERR_UNSUPPORTED"):
         cb.cb_stats_means(plan, src, tgt, w, sums)
@@ -296,4 +301,150 @@ def test_multi_qwen_k8_batch_full_size_sampled_maps(cb):
     maps, info = gpu_solve_ws(cb, G, C, 1e-2, cb.CB_LAMBDA_RELATIVE | cb.CB_RIDGE_BIAS_UNPENALIZED)
     assert int((info != 0).sum()) == 0
     check_solve(cb, G, C, maps, info, Go, Co, sel, True)
+    plan.close()
+
+
+# ----------------------------------------------------------------------------- application
+
+TOL_APPLY = 1e-3
+
+
+def gpu_apply(cb, plan, maps, src, L_t, H_t, out=None):
+    if out is None:
+        B, T = src.shape[2], src.shape[4]
+        out = torch.zeros((L_t, 2, B, H_t, T, plan.d_t), dtype=torch.bfloat16, device="cuda")
+    cb.cb_apply(plan, maps, src, out)
+    torch.cuda.synchronize()
+    return out
+
+
+def oracle_apply_multi(hm, maps, src, L_t, H_t, d_t, sel=None):
+    """Oracle application of the maps `sel` (all by default) with the fp32 maps the
+    GPU used, on a host copy of the sender cache."""
+    if sel is not None:
+        hm = {f: v[sel] for f, v in hm.items()}
+        maps = maps[torch.as_tensor(sel, device=maps.device)]
+    L_s, _, B, H_s, T, d_s = src.shape
+    ref = np.zeros((L_t, 2, B, H_t, T, d_t), dtype=np.uint16)
+    oracle.apply_multi(hm, maps.double().cpu().numpy(), bits(src), synth.cache_strides(L_s, H_s, B, T, d_s), d_s,
+                       ref, synth.cache_strides(L_t, H_t, B, T, d_t), d_t, B, T, n_threads=NTHREADS)
+    return ref
+
+
+def check_apply_multi(ob, ref, hm, sel, label=""):
+    """Per map in `sel`: relF within the bar and every element within one bf16 ulp
+    of the oracle's value plus 1e-4 of the map's RMS output (near-zero outputs see
+    the ~2^-17 relative error of the split coefficients as several ulps)."""
+    worst_e, worst_b, same, cnt = 0.0, 0.0, 0, 0
+    for m in sel:
+        l, z, h = int(hm["tgt_layer"][m]), int(hm["kv"][m]), int(hm["tgt_head"][m])
+        og, orf = ob[l, z, :, h], ref[l, z, :, h]
+        g = oracle.bf16_to_double(og)
+        r = oracle.bf16_to_double(orf)
+        worst_e = max(worst_e, relF(g, r))
+        rms = np.sqrt((r * r).mean())
+        ulp = np.spacing(np.abs(r).astype(np.float32)).astype(np.float64) * 65536.0
+        worst_b = max(worst_b, float((np.abs(g - r) / (ulp + 1e-4 * rms)).max()))
+        same += int((og == orf).sum())
+        cnt += og.size
+    say(f"  multi apply parity{label}: worst per-map relF {worst_e:.3e}, bitwise-equal {same / cnt:.6f}, "
+        f"worst err/bound {worst_b:.3f}")
+    assert worst_e <= TOL_APPLY and worst_b <= 1.0
+
+
+def random_maps(rng, n, P, d_t):
+    g = torch.Generator(device="cpu")
+    g.manual_seed(int(rng.integers(1 << 31)))
+    W = torch.randn((n, P, d_t), generator=g) / np.sqrt(P - 1)
+    W[:, P - 1] = torch.randn((n, d_t), generator=g)
+    return W.to("cuda")
+
+
+def test_multi_apply_tiny_k3_fitted_maps(cb):
+    # the maps fitted on tiny_k3 applied to the same sender: 4 x 520 tokens
+    # (eight full 256-token tiles and a 32-token tail)
+    wl = synth.WORKLOADS["tiny_k3"]
+    src = synth.gen_source(wl, device="cuda")
+    tgt = synth.gen_target(wl, src, device="cuda")
+    w = synth.gen_weights(wl, device="cuda")
+    hm = synth.head_map_multi(wl)
+    plan = cb.cb_plan_create_multi(hm, src, tgt, wl.sample_stride)
+    G, C = gpu_stats(cb, plan, [(src, tgt, w)])
+    maps, info = gpu_solve_ws(cb, G, C, 1e-2, cb.CB_LAMBDA_RELATIVE | cb.CB_RIDGE_BIAS_UNPENALIZED)
+    assert int((info != 0).sum()) == 0
+    out = gpu_apply(cb, plan, maps, src, wl.L_t, wl.H_t)
+    ref = oracle_apply_multi(hm, maps, src, wl.L_t, wl.H_t, wl.d_t)
+    check_apply_multi(bits(out), ref, hm, range(plan.n_maps), " (tiny_k3)")
+    plan.close()
+
+
+@pytest.mark.parametrize("k,B,T", [(1, 1, 37), (2, 3, 100), (4, 2, 300), (5, 1, 256), (8, 2, 129)])
+def test_multi_apply_random_maps_ragged_tokens(cb, k, B, T):
+    rng = np.random.default_rng(100 + k)
+    L_s, H_s, L_t, H_t = max(k, 3) + 1, 2, 3, 2
+    src, tgt, _ = small_inputs(rng, L_s, H_s, L_t, H_t, B, T)
+    hm = random_multi_map(rng, k, L_s, H_s, L_t, H_t)
+    plan = cb.cb_plan_create_multi(hm, src, tgt, 1)
+    maps = random_maps(rng, plan.n_maps, plan.P, plan.d_t)
+    say(f"multi apply k={k}: {B} x {T} tokens, {plan.n_maps} maps")
+    out = gpu_apply(cb, plan, maps, src, L_t, H_t)
+    ref = oracle_apply_multi(hm, maps, src, L_t, H_t, 128)
+    check_apply_multi(bits(out), ref, hm, range(plan.n_maps), f" (k={k}, N={B * T})")
+    plan.close()
+
+
+def test_multi_apply_selector_maps_copy_bits_strided_output(cb):
+    # map m copies source layer j_m of its window (identity block, zero bias): the
+    # output bits equal the sender's bits.  The target is a view with room for
+    # more tokens (sequence stride larger than the written rows), and the rows
+    # past the written ones must stay untouched.
+    rng = np.random.default_rng(9)
+    k, L_s, H_s, L_t, H_t, B, T = 3, 5, 2, 4, 2, 3, 300
+    src, tgt, _ = small_inputs(rng, L_s, H_s, L_t, H_t, B, T)
+    hm = random_multi_map(rng, k, L_s, H_s, L_t, H_t)
+    plan = cb.cb_plan_create_multi(hm, src, tgt, 1)
+    n, P = plan.n_maps, plan.P
+    maps = torch.zeros((n, P, 128), dtype=torch.float32)
+    pick = rng.integers(k, size=n)
+    for m in range(n):
+        maps[m, 128 * pick[m]:128 * pick[m] + 128] = torch.eye(128)
+    maps = maps.to("cuda")
+    big = torch.full((L_t, 2, B, H_t, T + 64, 128), 7.0, dtype=torch.bfloat16, device="cuda")
+    out = gpu_apply(cb, plan, maps, src, L_t, H_t, out=big[:, :, :, :, :T])
+    ob, sb = bits(big), bits(src)
+    for m in range(n):
+        l, z, h = int(hm["tgt_layer"][m]), int(hm["kv"][m]), int(hm["tgt_head"][m])
+        j, a = int(hm["src_layers"][m][pick[m]]), int(hm["src_head"][m])
+        assert np.array_equal(ob[l, z, :, h, :T], sb[j, z, :, a]), f"map {m} must copy source layer {j}"
+    assert (big[:, :, :, :, T:] == 7.0).all(), "rows past the written tokens must stay untouched"
+    # an empty call writes nothing
+    before = big.clone()
+    cb.cb_apply(plan, maps * 2.0, src[:, :, :0], big[:, :, :0, :, :T])
+    torch.cuda.synchronize()
+    assert torch.equal(big, before)
+    plan.close()
+
+
+def test_multi_apply_qwen_k8_batch_sampled(cb):
+    """The k = 8 construction's maps (40 -> 64 layers x 8 heads, 1,024 maps, P =
+    1,025) applied to a 100-sequence x 1,024-token sender batch, as the benchmark
+    launches it; eight sampled maps on the first and last 512 tokens of two
+    sequences against the oracle."""
+    wl = synth.WORKLOADS["qwen_k8"]
+    bw = wl.with_(n_seqs=wl.batch_seqs)
+    rng = np.random.default_rng(8)
+    src = synth.gen_source(bw, device="cuda")
+    hm = synth.head_map_multi(wl)
+    plan = cb.cb_plan_create_multi(hm, src, (wl.L_t, wl.H_t, wl.d_t), wl.sample_stride)
+    maps = random_maps(rng, plan.n_maps, plan.P, plan.d_t)
+    say(f"multi apply qwen_k8: {bw.n_seqs} x {bw.seq_len} tokens, {plan.n_maps} maps")
+    out = gpu_apply(cb, plan, maps, src, wl.L_t, wl.H_t)
+    sel = [0, 1, 135, 511, 512, 777, 1022, 1023]
+    hs = {f: v[sel] for f, v in hm.items()}
+    ms = maps[torch.as_tensor(sel, device=maps.device)]
+    for b, t0, t1 in ((0, 0, 512), (bw.n_seqs - 1, bw.seq_len - 512, bw.seq_len)):
+        s_sub = src[:, :, b:b + 1, :, t0:t1].contiguous()
+        ref = oracle_apply_multi(hs, ms, s_sub, wl.L_t, wl.H_t, wl.d_t)
+        ob = bits(out[:, :, b:b + 1, :, t0:t1].contiguous())
+        check_apply_multi(ob, ref, hs, range(len(sel)), f" (seq {b}, tokens {t0}..{t1})")
     plan.close()
