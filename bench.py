@@ -61,6 +61,47 @@ def measured_traffic():
     return t.get("bytes_per_launch")
 
 
+def _pmc_means(folder, counter, name_filter):
+    """Mean per dispatch of `counter` (summed over the dispatch's rows) for each
+    kernel whose name passes `name_filter`, from a rocprofv3 --pmc CSV folder."""
+    import csv
+    import glob
+    per = {}
+    for f in glob.glob(os.path.join(folder, "**", "*counter_collection.csv"), recursive=True):
+        for row in csv.DictReader(open(f)):
+            if row["Counter_Name"] != counter or not name_filter(row["Kernel_Name"]):
+                continue
+            key = (row["Kernel_Name"], row.get("Dispatch_Id", ""))
+            per[key] = per.get(key, 0.0) + float(row["Counter_Value"])
+    by_kernel = {}
+    for (k, _), v in per.items():
+        by_kernel.setdefault(k, []).append(v)
+    return {k: sum(v) / len(v) for k, v in by_kernel.items()}
+
+
+def write_traffic(fetch_dir, write_dir, cfetch_dir, cwrite_dir, copy_gib):
+    """Turn four rocprofv3 --pmc runs into the traffic file: FETCH_SIZE and
+    WRITE_SIZE (KiB per dispatch) of one statistics call (the statistics kernel
+    and its reduction), each scaled by what the same counter reads for the
+    plain device copy of `copy_gib` GiB (--hbm-copy-probe)."""
+    n = copy_gib * (1 << 30)
+    main = lambda k: "::stats_kernel<128, 128, false, false>" in k or \
+        "::reduce_kernel<128, 128, false>" in k  # noqa: E731
+    f = _pmc_means(fetch_dir, "FETCH_SIZE", main)
+    w = _pmc_means(write_dir, "WRITE_SIZE", main)
+    cf = max(_pmc_means(cfetch_dir, "FETCH_SIZE", lambda k: True).values())
+    cw = max(_pmc_means(cwrite_dir, "WRITE_SIZE", lambda k: True).values())
+    ff, wf = n / (cf * 1024.0), n / (cw * 1024.0)
+    fetch = sum(f.values()) * 1024.0 * ff
+    write = sum(w.values()) * 1024.0 * wf
+    rec = {"kernel_sha": stats_kernel_sha(), "bytes_per_launch": fetch + write, "fetch_bytes": fetch,
+           "write_bytes": write, "fetch_factor": ff, "write_factor": wf,
+           "kernels": sorted(f), "source": "profiles/stats_kernel_qwen500_batch100.md"}
+    with open(TRAFFIC_FILE, "w") as fh:
+        json.dump(rec, fh, indent=1)
+    print(json.dumps(rec), flush=True)
+
+
 def cpu_baseline(wl, src, tgt, w, hm, n_threads):
     """The fp64 oracle, as it stands, on a bounded sample of the resident batch:
     every map over the first `CB_CPU_SAMPLE_SEQS` full sequences."""
@@ -284,8 +325,8 @@ def multi_leg(cb, synth, steps):
     selected source layers per target layer (P = 1,025), 500 sequences of 1,024
     tokens sampled every fourth token (128,000 calibration rows), streamed as 5
     calls of one resident 100-sequence batch, then the 1,024-system blocked
-    fp64 ridge solve.  Timed with events on the launch stream after one warm-up
-    build."""
+    fp64 ridge solve; then the maps applied to the batch's 102,400 sender
+    tokens.  Timed with events on the launch stream after one warm-up run."""
     import torch
     wl = synth.WORKLOADS["qwen_k8"]
     B = wl.batch_seqs
@@ -327,6 +368,20 @@ def multi_leg(cb, synth, steps):
     flop_per_row = 2 * n * (P * P + P * d_t)                  # dense P x P Gram, algorithmic
     tflops = flop_per_row * rows_per_call / (call_ms / 1e3) / 1e12
     bad = int((info != 0).sum().item())
+    # online application of the fitted maps to the resident sender batch
+    del tgt, w, G, C, ws
+    torch.cuda.empty_cache()
+    out = torch.empty((wl.L_t, 2, B, wl.H_t, wl.seq_len, d_t), dtype=torch.bfloat16, device="cuda")
+    ea = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 2)]
+    for it in range(steps + 1):
+        if it > 0:
+            ea[it].record(stream)
+        cb.cb_apply(plan, maps, src, out)
+    ea[steps + 1].record(stream)
+    torch.cuda.synchronize()
+    apply_ms = ea[1].elapsed_time(ea[steps + 1]) / steps
+    apply_flop = 2.0 * n * B * wl.seq_len * P * d_t
+    del out
     plan.close()
     return {
         "workload": f"qwen3-14b->32b-shaped k={wl.k} build (P={P}, {n} maps): {wl.n_seqs} seqs x {wl.seq_len} tok, "
@@ -334,7 +389,11 @@ def multi_leg(cb, synth, steps):
                     f"{n_calls} x {B}-seq resident batch, + {n}-system blocked fp64 solve",
         "s_per_500seq_build": build_ms / 1e3,
         "calib_rows_per_s": wl.n_seqs * rows_per_call // B / (build_ms / 1e3),
-        "legs_ms": {"stats_call": call_ms, "solve": solve_ms},
+        "legs_ms": {"stats_call": call_ms, "solve": solve_ms, "apply_100seq": apply_ms},
+        "apply_tokens_per_s": B * wl.seq_len / (apply_ms / 1e3),
+        "apply_roofline": {"bound": "mfma", "kernel": "split_maps_kernel + apply_multi_kernel per 100-seq call",
+                           "achieved": apply_flop / (apply_ms / 1e3) / 1e12, "peak": 2500.0, "unit": "TFLOP/s",
+                           "frac": apply_flop / (apply_ms / 1e3) / 1e12 / 2500.0},
         "roofline": {"bound": "mfma", "kernel": "stats_multi_kernel per 100-seq call", "achieved": tflops,
                      "peak": 2500.0, "unit": "TFLOP/s", "frac": tflops / 2500.0,
                      "algorithmic_flops_per_launch": flop_per_row * rows_per_call},
@@ -362,7 +421,14 @@ def main():
                     help="timed k = 8 multi-layer builds (P = 1025), after the other legs (0: skip)")
     ap.add_argument("--hbm-copy-probe", type=float, default=None, metavar="GIB",
                     help="only time a plain copy of GIB GiB (counter calibration)")
+    ap.add_argument("--write-traffic", nargs=5, default=None,
+                    metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR", "COPY_GIB"),
+                    help="only write the traffic file from rocprofv3 --pmc CSV folders (no GPU)")
     args = ap.parse_args()
+    if args.write_traffic:
+        a = args.write_traffic
+        write_traffic(a[0], a[1], a[2], a[3], float(a[4]))
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); "
               "the path is single-GPU by design (see DESIGN.md, 'Sharding').", file=sys.stderr)
