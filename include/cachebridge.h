@@ -426,8 +426,11 @@ typedef struct {
  * (the work grows as P^2 per row).  G and C must not overlap other buffers of
  * the call.  Solve with cb_ridge_solve_ws.  cb_apply maps a sender cache with
  * the P x d_t maps, every token: out = RNE_bf16([x_0, ..., x_{k-1}, 1] maps[m])
- * (coefficients as two bf16 terms, fp32 sums and bias, one rounding).  The
- * centered and means calls return CB_ERR_UNSUPPORTED for such a plan.  Errors
+ * (coefficients as two bf16 terms, fp32 sums and bias, one rounding); the
+ * rows of one source (layer, kv, head) must span fewer than 2^32 elements
+ * ((n_seqs - 1) s_seq + (seq_len - 1) s_tok + 128), else CB_ERR_UNSUPPORTED
+ * (apply in smaller batches).  The centered and means calls return
+ * CB_ERR_UNSUPPORTED for such a plan.  Errors
  * as in cb_plan_create, plus CB_ERR_INVALID_ARGUMENT for a source layer
  * selected twice by one map.
  */

@@ -583,7 +583,7 @@ cb_status cb_plan_create_multi(const cb_head_map_multi *map, const cb_cache *src
                hipMalloc(&p->d_amaps, sizeof(cb::ApplyMultiMap) * n) == hipSuccess &&
                hipMalloc(&p->d_aorder, sizeof(int32_t) * n) == hipSuccess &&
                hipMalloc(&p->d_alayers, sizeof(int32_t) * (size_t)n * k) == hipSuccess &&
-               hipMalloc(&p->d_whi, wsplit) == hipSuccess && hipMalloc(&p->d_wlo, wsplit) == hipSuccess &&
+               hipMalloc(&p->d_whi, 2 * wsplit) == hipSuccess &&   // hi and lo fragment planes
                hipMalloc(&p->d_bias, sizeof(float) * n * d_t) == hipSuccess;
     if (!okm) {
         (void)hipGetLastError();
@@ -985,10 +985,13 @@ cb_status cb_apply(cb_plan *p, const float *maps, const cb_cache *src, const cb_
         if (((uintptr_t)maps) % 4) return fail(CB_ERR_MISALIGNED, "maps must be 4-byte aligned");
         const int64_t N = (int64_t)src->n_seqs * src->seq_len;
         if (N > (int64_t)INT32_MAX - 4096) return fail(CB_ERR_UNSUPPORTED, "too many tokens in one call");
+        if (N > 0 && (int64_t)(src->n_seqs - 1) * src->s_seq + (int64_t)(src->seq_len - 1) * src->s_tok + 128 >
+                         (int64_t)UINT32_MAX)
+            return fail(CB_ERR_UNSUPPORTED, "src rows of one (layer, kv, head) span more than 2^32 elements; "
+                                            "apply in smaller batches");
         if (cb_status s = check_device(p)) return s;
         hipStream_t st = (hipStream_t)stream;
-        const int Pm1 = p->P - 1;
-        if (cb::launch_split_maps(p->n_maps, Pm1, p->d_t, maps, p->d_whi, p->d_wlo, p->d_bias, st) != hipSuccess)
+        if (cb::launch_split_maps_frag(p->n_maps, p->k, maps, p->d_whi, p->d_bias, st) != hipSuccess)
             return fail(CB_ERR_DEVICE, "map split launch failed");
         if (N == 0) return ok();
         cb::ApplyMultiArgs a = {};
@@ -999,22 +1002,18 @@ cb_status cb_apply(cb_plan *p, const float *maps, const cb_cache *src, const cb_
         a.T = cb::make_fastdiv((uint32_t)src->seq_len);
         a.N = N;
         a.k = p->k;
-        a.d_t = p->d_t;
         a.n_maps = p->n_maps;
         a.n_tiles = (int32_t)((N + 255) / 256);
-        a.group = 4;
-        const int64_t n_groups = (p->n_maps + a.group - 1) / a.group;
-        const int64_t n_tasks = n_groups * a.n_tiles * a.group;
-        if (n_tasks > (int64_t)INT32_MAX - 8) return fail(CB_ERR_UNSUPPORTED, "too many application workgroups");
+        const int64_t n_tasks = (int64_t)p->n_maps * a.n_tiles;
+        if (n_tasks > (int64_t)INT32_MAX - 8) return fail(CB_ERR_UNSUPPORTED, "too many application tasks");
         a.n_tasks = (int32_t)n_tasks;
         a.per_xcd = (a.n_tasks + 7) / 8;
         a.maps = p->d_amaps;
         a.order = p->d_aorder;
         a.src_layers = p->d_alayers;
-        a.w_hi = p->d_whi;
-        a.w_lo = p->d_wlo;
+        a.wfrag = p->d_whi;
         a.bias = p->d_bias;
-        if (cb::launch_apply_multi(a, st) != hipSuccess)
+        if (cb::launch_apply_multi(a, p->n_cu, st) != hipSuccess)
             return fail(CB_ERR_DEVICE, "multi-layer application kernel launch failed");
         return ok();
     }

@@ -3,24 +3,36 @@
 // CacheBridge Sec. 1 (online handoff) with the multi-layer feature of Sec. 3.2:
 // map m reads the sender's rows of its k selected source layers and writes
 //     out[t, :] = RNE_bf16( sum_i x_{i,t} W_{m,i} + b_m )
-// where W_{m,i} is rows 128 i .. 128 i + 127 of the map.  The maps arrive
-// split as W^T in two bf16 planes (hi = RNE(W), lo = RNE(W - hi)) and an fp32
-// bias, as for the single-layer apply.
+// where W_{m,i} is rows 128 i .. 128 i + 127 of the map.  At k = 8 that is
+// 262 kFLOP per token and map against 256 bytes written: a dense contraction,
+// run on the matrix cores.
 //
-// One workgroup per (map, tile of 256 tokens), four waves; wave w owns output
-// channels 32 w .. 32 w + 31.  For each of the k source blocks the tile's 256
-// rows are copied HBM -> LDS (direct-to-LDS, 16-byte chunk c of token row t at
-// position c ^ (t mod 16), double buffered: block i+1 streams in while block i
-// is multiplied), the wave loads its W^T hi/lo fragments for the block from
-// global memory, and accumulates D = W^T x^T (channels x tokens, K = the
-// block's 128 channels) with v_mfma_f32_32x32x16_bf16, hi and lo products into
-// the same fp32 accumulators.  Then the bias is added, the sum rounded once to
-// bf16 and stored as 16-byte chunks of target rows.
+// split_maps_frag_kernel: W (fp32) -> W^T as bf16 MFMA fragments, hi =
+//   RNE(W) and lo = RNE(W - hi) (together ~16 significant bits), laid out
+//   [map][block i][K step ks][wave w][plane][lane][8]: lane l of wave w holds
+//   output channel 32 w + (l mod 32), inputs 128 i + 16 ks + 8 (l / 32) .. + 7.
+//   One fragment load is 1 KiB contiguous.  The fp32 bias is kept apart.
 //
-// Workgroup order: maps in groups of four neighbouring target layers (same K/V
-// component and head); within a group the tiles are visited token-tile first,
-// so the four maps' W^T stays in L2 and their overlapping source windows
-// share the staged rows.
+// apply_multi_kernel: a task is (map, tile of 256 tokens).  The grid is
+//   persistent, one workgroup of four waves per compute unit; the workgroups
+//   of one XCD walk a contiguous run of tasks (maps in groups of four
+//   neighbouring target layers, token tile first within a group, so the
+//   group's W^T and the overlapping source windows stay in that XCD's L2).
+//   Wave w owns output channels 32 w .. 32 w + 31 of all 256 tokens: eight
+//   32 x 32 fp32 accumulator tiles, D = W^T x^T with
+//   v_mfma_f32_32x32x16_bf16 (K = source channels), hi and lo products into
+//   the same accumulators.
+//
+//   The work is one stream of source blocks (task, i), eight K steps each,
+//   software-pipelined across blocks and tasks:
+//     * the 256 x 128 rows of block b+1 are loaded into registers while block
+//       b is multiplied, written to the other LDS buffer (16-byte chunk c of
+//       token row t at c ^ (t mod 16)) at its last step, then one barrier;
+//     * the x fragments of step s+1 are read from LDS during step s;
+//     * the W^T fragments are loaded one block ahead, each into the registers
+//       its step has just consumed.
+//   At the end of a task the bias is added, the sum rounded once to bf16 and
+//   stored as 16-byte chunks of target rows.
 #include "cb_internal.h"
 
 namespace cb {
@@ -30,11 +42,14 @@ typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
 typedef __attribute__((ext_vector_type(16))) float f32x16_t;
 typedef __attribute__((ext_vector_type(2))) float f32x2_t;
 typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
 
-constexpr int TT = 256;                 // tokens per workgroup
+constexpr int TT = 256;                 // tokens per task
 constexpr int ROWB = 256;               // bytes per 128-channel row
 constexpr int BUFB = TT * ROWB;         // one staged source block (64 KiB)
-constexpr int CPW = BUFB / 1024 / 4;    // copy instructions per wave and block (16)
+constexpr int CPW = BUFB / 1024 / 4;    // 16-byte row chunks per lane and block (16)
+constexpr int FRAG = 512;               // bf16 elements of one wave fragment (64 lanes x 8)
+constexpr int64_t WBLK = 8 * 4 * 2 * FRAG;  // fragment elements per (map, block)
 
 __device__ __forceinline__ uint32_t fastdiv_u(uint32_t n, const FastDiv &f) {
     const uint32_t t = __umulhi(n, f.m);
@@ -47,162 +62,286 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
     return __builtin_bit_cast(uint32_t, p);
 }
 
-// HBM -> LDS copy of 16 bytes per lane to M0 + 16 lane; M0 restored inside.
-__device__ __forceinline__ void dma16(const void *gaddr, uint32_t m0) {
-    uint32_t keep;
-    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
-                 : "=&s"(keep)
-                 : "v"(gaddr), "s"(m0)
-                 : "memory");
+// This wave's LDS reads and writes have completed, then the workgroup barrier;
+// the empty asm keeps the compiler from moving memory operations across it.
+__device__ __forceinline__ void lds_sync() {
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0); vmcnt, expcnt untouched
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+__global__ __launch_bounds__(256) void split_maps_frag_kernel(int n_maps, int k, const float *__restrict__ maps,
+                                                              uint16_t *__restrict__ wfrag, float *__restrict__ bias) {
+    const int P = 128 * k + 1;
+    const int64_t total = (int64_t)n_maps * k * 8 * 4 * 64;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+         e += (int64_t)gridDim.x * blockDim.x) {
+        const int lane = (int)(e & 63), w = (int)((e >> 6) & 3), ks = (int)((e >> 8) & 7);
+        const int64_t mi = e >> 11;                       // map * k + block
+        const int64_t m = mi / k;
+        const int i = (int)(mi - m * k);
+        const int c = 32 * w + (lane & 31);
+        const int K0 = 128 * i + 16 * ks + 8 * (lane >> 5);
+        const float *src = maps + (m * P + K0) * 128 + c;
+        uint32_t hi[4], lo[4];
+#pragma unroll
+        for (int j = 0; j < 8; j += 2) {
+            const float v0 = src[j * 128], v1 = src[(j + 1) * 128];
+            const uint32_t p = pack_bf16(v0, v1);
+            const float h0 = __uint_as_float(p << 16), h1 = __uint_as_float(p & 0xffff0000u);
+            hi[j / 2] = p;
+            lo[j / 2] = pack_bf16(v0 - h0, v1 - h1);
+        }
+        uint16_t *dst = wfrag + ((mi * 8 + ks) * 4 + w) * (2 * FRAG) + lane * 8;
+        *reinterpret_cast<uint4 *>(dst) = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+        *reinterpret_cast<uint4 *>(dst + FRAG) = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+        if (i == 0 && ks == 0 && lane < 32) bias[m * 128 + c] = maps[(m * P + P - 1) * 128 + c];
+    }
+}
+
+// Uniform description of one task.
+struct Task {
+    int32_t m;          // map index
+    int64_t tok0;       // first token of the tile
+    const uint16_t *x;  // source base of the map's (kv, head), layer 0
+    const int32_t *layers;
+};
+
+__device__ __forceinline__ Task task_of(const ApplyMultiArgs &a, int task) {
+    // maps in groups of four (the last group may be smaller), tile-major inside a group
+    const int full = a.n_maps & ~3;
+    const int64_t in_full = (int64_t)full * a.n_tiles;
+    int tile, gm;
+    if (task < in_full) {
+        const int per = 4 * a.n_tiles;
+        const int g = task / per, r = task - g * per;
+        tile = r >> 2;
+        gm = 4 * g + (r & 3);
+    } else {
+        const int rem = a.n_maps - full;
+        const int r = task - (int)in_full;
+        tile = r / rem;
+        gm = full + (r - tile * rem);
+    }
+    Task t;
+    t.m = __builtin_amdgcn_readfirstlane(a.order[gm]);
+    t.tok0 = (int64_t)tile * TT;
+    const ApplyMultiMap mp = a.maps[t.m];
+    t.x = a.src + mp.kv * a.ss.kv + mp.src_head * a.ss.head;
+    t.layers = a.src_layers + (int64_t)t.m * a.k;
+    return t;
 }
 
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
 void apply_multi_kernel(ApplyMultiArgs a) {
     __shared__ __attribute__((aligned(16))) char lds[2 * BUFB];
-    const int b = blockIdx.x;
-    const int task = (b & 7) * a.per_xcd + (b >> 3);       // a contiguous run of tasks per XCD
-    if (task >= a.n_tasks) return;
+    const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+    const int per_wg = gridDim.x >> 3;                    // workgroups per XCD (the grid is a multiple of 8)
+    const int t_end = min(xcd * a.per_xcd + a.per_xcd, a.n_tasks);
+    int task = xcd * a.per_xcd + slot;
+    if (task >= t_end) return;
+
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    // task -> (group of maps, token tile, map in group)
-    const int per_group = a.n_tiles * a.group;
-    const int grp = task / per_group, rem = task - grp * per_group;
-    const int tile = rem / a.group;
-    const int gm = grp * a.group + rem % a.group;
-    if (gm >= a.n_maps) return;
-    const int m = a.order[gm];
-    const ApplyMultiMap &mp = a.maps[m];
-    const int k = a.k, Pm1 = 128 * k;
-    const int64_t tok0 = (int64_t)tile * TT;
-
-    // ---- copy geometry: instruction j of this wave covers token rows 4 c .. 4 c + 3, c = wave + 4 j
-    const int ch = lane & 15;
-    int64_t rowoff[CPW];                                  // element offset of the lane's token row in a block
-    uint32_t cpos[CPW];                                   // source chunk of the lane (swizzled position ch)
-#pragma unroll
-    for (int j = 0; j < CPW; ++j) {
-        const int t = 4 * (wave + 4 * j) + (lane >> 4);
-        int64_t n = tok0 + t;
-        if (n >= a.N) n = a.N - 1;                        // rows past the end repeat the last token
-        const uint32_t seq = fastdiv_u((uint32_t)n, a.T);
-        const uint32_t tk = (uint32_t)n - seq * a.T.d;
-        rowoff[j] = (int64_t)seq * a.ss.seq + (int64_t)tk * a.ss.tok;
-        cpos[j] = (uint32_t)(ch ^ (t & 15)) * 8u;         // elements
-    }
-    const uint32_t lds_base = (uint32_t)(uintptr_t)lds;
-    auto issue = [&](int i, int buf) {
-        const int L = a.src_layers[(int64_t)m * k + i];
-        const uint16_t *blk = a.src + L * a.ss.layer + mp.kv * a.ss.kv + mp.src_head * a.ss.head;
-#pragma unroll
-        for (int j = 0; j < CPW; ++j)
-            dma16(blk + rowoff[j] + cpos[j],
-                  __builtin_amdgcn_readfirstlane(lds_base + buf * BUFB + (wave + 4 * j) * 1024));
-    };
-
-    // ---- W^T fragments of this wave for block i: 8 K steps x (hi, lo)
-    const int c = 32 * wave + (lane & 31);                // output channel of the A operand row
-    const uint16_t *whi = a.w_hi + ((int64_t)m * a.d_t + c) * Pm1 + 8 * (lane >> 5);
-    const uint16_t *wlo = a.w_lo + ((int64_t)m * a.d_t + c) * Pm1 + 8 * (lane >> 5);
-    struct WF {
-        bf16x8_t hi[8], lo[8];
-    };
-    auto load_w = [&](WF &f, int i) {
-#pragma unroll
-        for (int ks = 0; ks < 8; ++ks) {
-            f.hi[ks] = *reinterpret_cast<const bf16x8_t *>(whi + 128 * i + 16 * ks);
-            f.lo[ks] = *reinterpret_cast<const bf16x8_t *>(wlo + 128 * i + 16 * ks);
-        }
-    };
-
-    f32x16_t acc[TT / 32];
-#pragma unroll
-    for (int s = 0; s < TT / 32; ++s)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) acc[s][v] = 0.f;
-    // B operand (x^T): lane holds token row 32 s + (lane & 31), channels 16 ks + 8 (lane >> 5) .. + 7
+    const int k = a.k;
     const uint32_t lrow = lane & 31, lhalf = lane >> 5;
-    auto compute = [&](const WF &f, int buf) {
-        const char *B = lds + buf * BUFB;
-#pragma unroll
-        for (int ks = 0; ks < 8; ++ks) {
-            bf16x8_t x[TT / 32];
-#pragma unroll
-            for (int s = 0; s < TT / 32; ++s) {
-                const uint32_t t = 32 * s + lrow;
-                x[s] = *reinterpret_cast<const bf16x8_t *>(B + t * ROWB + (((2 * ks + lhalf) ^ (t & 15)) * 16));
-            }
-#pragma unroll
-            for (int s = 0; s < TT / 32; ++s) acc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.hi[ks], x[s], acc[s], 0, 0, 0);
-#pragma unroll
-            for (int s = 0; s < TT / 32; ++s) acc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.lo[ks], x[s], acc[s], 0, 0, 0);
-        }
-    };
 
-    // ---- blocks: i+1 streams in (copies and W fragments) while i is multiplied
-    WF wa, wb;
-    load_w(wa, 0);
-    issue(0, 0);
-    for (int i = 0; i < k; i += 2) {
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // block i (and its W) has landed
-        __syncthreads();
-        if (i + 1 < k) {
-            load_w(wb, i + 1);
-            issue(i + 1, 1);
-        }
-        compute(wa, 0);
-        if (i + 1 < k) {
-            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-            __syncthreads();
-            if (i + 2 < k) {
-                load_w(wa, i + 2);
-                issue(i + 2, 0);
-            }
-            compute(wb, 1);
-        }
-    }
-
-    // ---- bias, one rounding, 16-byte stores of target rows
-    // D[i][t]: t = lane & 31, channel 32 wave + 8 (v / 4) + 4 (lane / 32) + (v & 3)
-    float bias[16];
+    // ---- staging geometry: chunk j of this lane is token row 16 j + 4 wave + lane / 16, chunk lane mod 16,
+    // written at LDS chunk position (lane mod 16) ^ (row mod 16), row mod 16 = 4 wave + lane / 16
+    const int rsub = 4 * wave + (lane >> 4);
+    const uint32_t sdst = (uint32_t)rsub * ROWB + (uint32_t)((lane & 15) ^ rsub) * 16u;
+    // element offset of the lane's chunk inside a (layer, kv, head) block (below 2^32: checked on the host)
+    uint32_t rowoff[CPW];
+    auto set_rows = [&](int64_t tok0) {
 #pragma unroll
-    for (int v = 0; v < 16; ++v) bias[v] = a.bias[(int64_t)m * a.d_t + 32 * wave + 8 * (v >> 2) + 4 * lhalf + (v & 3)];
-    uint16_t *obase = a.out + mp.tgt_layer * a.os.layer + mp.kv * a.os.kv + mp.tgt_head * a.os.head + 32 * wave;
-#pragma unroll
-    for (int s = 0; s < TT / 32; ++s) {
-        uint32_t pk[8];
-#pragma unroll
-        for (int gq = 0; gq < 4; ++gq) {
-            pk[2 * gq] = pack_bf16(acc[s][4 * gq + 0] + bias[4 * gq + 0], acc[s][4 * gq + 1] + bias[4 * gq + 1]);
-            pk[2 * gq + 1] = pack_bf16(acc[s][4 * gq + 2] + bias[4 * gq + 2], acc[s][4 * gq + 3] + bias[4 * gq + 3]);
-        }
-        // exchange with lane ^ 32 so that each lane owns 8 consecutive channels:
-        // lanes < 32 get channels 0-7 and 16-23, lanes >= 32 get 8-15 and 24-31
-        uint4 o[2];
-#pragma unroll
-        for (int p = 0; p < 2; ++p) {
-            const uint32_t s0 = lhalf ? pk[4 * p + 0] : pk[4 * p + 2];
-            const uint32_t s1 = lhalf ? pk[4 * p + 1] : pk[4 * p + 3];
-            const uint32_t r0 = (uint32_t)__shfl_xor((int)s0, 32);
-            const uint32_t r1 = (uint32_t)__shfl_xor((int)s1, 32);
-            o[p] = lhalf ? make_uint4(r0, r1, pk[4 * p + 2], pk[4 * p + 3])
-                         : make_uint4(pk[4 * p + 0], pk[4 * p + 1], r0, r1);
-        }
-        const int64_t n = tok0 + 32 * s + (int64_t)lrow;
-        if (n < a.N) {
+        for (int j = 0; j < CPW; ++j) {
+            int64_t n = tok0 + 16 * j + rsub;
+            if (n >= a.N) n = a.N - 1;                    // rows past the end repeat the last token
             const uint32_t seq = fastdiv_u((uint32_t)n, a.T);
             const uint32_t tk = (uint32_t)n - seq * a.T.d;
-            uint16_t *orow = obase + (int64_t)seq * a.os.seq + (int64_t)tk * a.os.tok + 8 * lhalf;
-            *reinterpret_cast<uint4 *>(orow) = o[0];
-            *reinterpret_cast<uint4 *>(orow + 16) = o[1];
+            rowoff[j] = (uint32_t)(seq * a.ss.seq + tk * a.ss.tok) + (lane & 15) * 8;
         }
+    };
+    // half h of a block: chunks 8 h .. 8 h + 7 of the lane
+    constexpr int HC = CPW / 2;
+    auto load_half = [&](u32x4_t (&st)[HC], const uint16_t *xb, int h) {
+#pragma unroll
+        for (int j = 0; j < HC; ++j) st[j] = *reinterpret_cast<const u32x4_t *>(xb + rowoff[HC * h + j]);
+    };
+    // a quarter q of the block: chunks 4 q .. 4 q + 3, into st0 (q < 2) or st1
+    auto load_quarter = [&](u32x4_t (&st)[HC], const uint16_t *xb, int q) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            st[4 * (q & 1) + j] = *reinterpret_cast<const u32x4_t *>(xb + rowoff[4 * q + j]);
+    };
+    auto store_half = [&](const u32x4_t (&st)[HC], int buf, int h) {
+#pragma unroll
+        for (int j = 0; j < HC; ++j)
+            *reinterpret_cast<u32x4_t *>(lds + buf * BUFB + (HC * h + j) * 4096 + sdst) = st[j];
+    };
+    // x fragments of step ks: token row 32 s + lane mod 32, channels 16 ks + 8 (lane / 32) .. + 7
+    bf16x8_t xr[2][8];
+    auto read_x = [&](bf16x8_t (&x)[8], int buf, int ks) {
+        const char *B = lds + buf * BUFB + lrow * ROWB + (((2 * ks + lhalf) ^ (lrow & 15)) * 16);
+#pragma unroll
+        for (int s = 0; s < 8; ++s) x[s] = *reinterpret_cast<const bf16x8_t *>(B + s * 32 * ROWB);
+    };
+    // W^T fragments of the eight steps of a block; step ks's registers are refilled with the next block's
+    // fragments right after its MFMAs, so every fragment is loaded one block ahead
+    bf16x8_t wh[8], wl[8];
+    const int64_t wlane = (int64_t)wave * (2 * FRAG) + lane * 8;
+    auto wptr = [&](int m, int i) { return a.wfrag + ((int64_t)m * k + i) * WBLK + wlane; };
+    auto load_w = [&](int r, const uint16_t *p) {
+        wh[r] = *reinterpret_cast<const bf16x8_t *>(p);
+        wl[r] = *reinterpret_cast<const bf16x8_t *>(p + FRAG);
+    };
+
+    f32x16_t acc[8];
+#pragma unroll
+    for (int s = 0; s < 8; ++s)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[s][v] = 0.f;
+
+    // ---- prologue: block 0 of the first task in LDS buffer 0, its W fragments, x of step 0
+    Task cur = task_of(a, task);
+    set_rows(cur.tok0);
+    {
+        const uint16_t *xb = cur.x + cur.layers[0] * a.ss.layer;
+        u32x4_t st0[HC], st1[HC];
+        load_half(st0, xb, 0);
+        load_half(st1, xb, 1);
+        const uint16_t *w0 = wptr(cur.m, 0);
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) load_w(ks, w0 + ks * 8 * FRAG);
+        store_half(st0, 0, 0);
+        store_half(st1, 0, 1);
+    }
+    lds_sync();
+    read_x(xr[0], 0, 0);
+    int buf = 0;
+
+    while (true) {
+        Task nxt = cur;
+        int next_task = task;
+        bool more = true;                                  // is there a block after the current one
+        for (int i = 0; i < k; ++i) {
+            // ---- the block after (cur, i): (cur, i + 1) or block 0 of the next task
+            int ni = i + 1;
+            if (ni == k) {
+                next_task = task + per_wg;
+                more = next_task < t_end;
+                if (more) {
+                    nxt = task_of(a, next_task);
+                    set_rows(nxt.tok0);
+                }
+                ni = 0;
+            }
+            const uint16_t *nw = more ? wptr(nxt.m, ni) : wptr(cur.m, i);  // past the end: reload valid fragments
+            // past the end of the stream the current block is loaded again (and never read)
+            const uint16_t *nxb = more ? nxt.x + nxt.layers[ni] * a.ss.layer : cur.x + cur.layers[i] * a.ss.layer;
+            u32x4_t st0[HC], st1[HC];
+#pragma unroll
+            for (int ks = 0; ks < 8; ++ks) {
+                // one step: the next block's rows requested (first step) or published (last two steps), the 16
+                // MFMAs with the x reads of the following step interleaved, then the next block's W fragments of
+                // this step into the registers just consumed.  In-order completion: a W fragment is waited for
+                // one block after its request, and the only slower requests ahead of it (the x rows of its own
+                // block) are complete by then.
+                __builtin_amdgcn_sched_barrier(0);
+                if (ks == 7) {
+                    store_half(st1, buf ^ 1, 1);
+                    lds_sync();
+                }
+                if (ks < 4) {
+                    if (ks < 2) load_quarter(st0, nxb, ks);
+                    else load_quarter(st1, nxb, ks);
+                }
+                if (ks == 6) store_half(st0, buf ^ 1, 0);
+                // at the end of the stream the last read is of a buffer nobody uses any more
+                read_x(xr[(ks + 1) & 1], ks < 7 ? buf : buf ^ 1, (ks + 1) & 7);
+                const bf16x8_t *x = xr[ks & 1];
+#pragma unroll
+                for (int s = 0; s < 8; ++s) acc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wh[ks], x[s], acc[s], 0, 0, 0);
+#pragma unroll
+                for (int s = 0; s < 8; ++s) acc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wl[ks], x[s], acc[s], 0, 0, 0);
+                load_w(ks, nw + ks * 8 * FRAG);
+                if (ks < 4) __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);     // x rows of the next block
+                if (ks == 6) __builtin_amdgcn_sched_group_barrier(0x200, 8, 0);
+#pragma unroll
+                for (int r = 0; r < 8; ++r) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+                __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);                 // W of the next block
+            }
+            buf ^= 1;
+        }
+
+        // ---- epilogue of the task: bias, one rounding, 16-byte stores of target rows
+        // D[i][t]: t = lane & 31, channel 32 wave + 8 (v / 4) + 4 (lane / 32) + (v & 3)
+        {
+            const ApplyMultiMap mp = a.maps[cur.m];
+            float bias[16];
+#pragma unroll
+            for (int v = 0; v < 16; ++v) bias[v] = a.bias[(int64_t)cur.m * 128 + 32 * wave + 8 * (v >> 2) + 4 * lhalf + (v & 3)];
+            uint16_t *obase = a.out + mp.tgt_layer * a.os.layer + mp.kv * a.os.kv + mp.tgt_head * a.os.head + 32 * wave;
+#pragma unroll
+            for (int s = 0; s < 8; ++s) {
+                uint32_t pk[8];
+#pragma unroll
+                for (int gq = 0; gq < 4; ++gq) {
+                    pk[2 * gq] = pack_bf16(acc[s][4 * gq + 0] + bias[4 * gq + 0], acc[s][4 * gq + 1] + bias[4 * gq + 1]);
+                    pk[2 * gq + 1] = pack_bf16(acc[s][4 * gq + 2] + bias[4 * gq + 2], acc[s][4 * gq + 3] + bias[4 * gq + 3]);
+                }
+                // exchange with lane ^ 32 so that each lane owns 8 consecutive channels:
+                // lanes < 32 get channels 0-7 and 16-23, lanes >= 32 get 8-15 and 24-31
+                uint4 o[2];
+#pragma unroll
+                for (int p = 0; p < 2; ++p) {
+                    const uint32_t s0 = lhalf ? pk[4 * p + 0] : pk[4 * p + 2];
+                    const uint32_t s1 = lhalf ? pk[4 * p + 1] : pk[4 * p + 3];
+                    const uint32_t r0 = (uint32_t)__shfl_xor((int)s0, 32);
+                    const uint32_t r1 = (uint32_t)__shfl_xor((int)s1, 32);
+                    o[p] = lhalf ? make_uint4(r0, r1, pk[4 * p + 2], pk[4 * p + 3])
+                                 : make_uint4(pk[4 * p + 0], pk[4 * p + 1], r0, r1);
+                }
+                const int64_t n = cur.tok0 + 32 * s + (int64_t)lrow;
+                if (n < a.N) {
+                    const uint32_t seq = fastdiv_u((uint32_t)n, a.T);
+                    const uint32_t tk = (uint32_t)n - seq * a.T.d;
+                    uint16_t *orow = obase + (int64_t)seq * a.os.seq + (int64_t)tk * a.os.tok + 8 * lhalf;
+                    *reinterpret_cast<uint4 *>(orow) = o[0];
+                    *reinterpret_cast<uint4 *>(orow + 16) = o[1];
+                }
+#pragma unroll
+                for (int v = 0; v < 16; ++v) acc[s][v] = 0.f;
+            }
+        }
+        if (!more) break;
+        cur = nxt;
+        task = next_task;
     }
 }
 
 }  // namespace
 
-hipError_t launch_apply_multi(const ApplyMultiArgs &a, hipStream_t s) {
+hipError_t launch_split_maps_frag(int32_t n_maps, int32_t k, const float *maps, uint16_t *wfrag, float *bias,
+                                  hipStream_t s) {
+    const int64_t n = (int64_t)n_maps * k * 8 * 4 * 64;
+    if (n == 0) return hipSuccess;
+    int64_t blocks = (n + 255) / 256;
+    if (blocks > 16384) blocks = 16384;
+    hipLaunchKernelGGL(split_maps_frag_kernel, dim3((unsigned)blocks), dim3(256), 0, s, n_maps, k, maps, wfrag, bias);
+    return hipGetLastError();
+}
+
+hipError_t launch_apply_multi(const ApplyMultiArgs &a, int32_t n_cu, hipStream_t s) {
     if (a.n_tasks == 0) return hipSuccess;
-    hipLaunchKernelGGL(apply_multi_kernel, dim3(8 * a.per_xcd), dim3(256), 0, s, a);
+    // one workgroup per compute unit, a multiple of 8 so every XCD gets the same count
+    int per_xcd_wg = n_cu / 8 > 0 ? n_cu / 8 : 1;
+    if (per_xcd_wg > a.per_xcd) per_xcd_wg = a.per_xcd;
+    hipLaunchKernelGGL(apply_multi_kernel, dim3(8 * per_xcd_wg), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 

@@ -161,16 +161,15 @@ struct ApplyMultiArgs {
     Strides ss, os;
     FastDiv T;                // tokens per sequence
     int64_t N;                // tokens (n_seqs * seq_len)
-    int32_t k, d_t, n_maps;
+    int32_t k, n_maps;
     int32_t n_tiles;          // 256-token tiles per map
-    int32_t group;            // maps per group (visited token-tile first)
-    int32_t n_tasks, per_xcd;
+    int32_t n_tasks;          // n_maps * n_tiles (map, tile) tasks
+    int32_t per_xcd;          // tasks per XCD (a contiguous run)
     const ApplyMultiMap *maps;
     const int32_t *order;     // [n_maps] maps in visiting order
     const int32_t *src_layers;// [n_maps][k]
-    const uint16_t *w_hi;     // [n_maps][d_t][k * 128] bf16, transposed maps
-    const uint16_t *w_lo;
-    const float *bias;        // [n_maps][d_t]
+    const uint16_t *wfrag;    // W^T as MFMA fragments, [n_maps][k][8][4][2][64][8] bf16 (hi, lo planes)
+    const float *bias;        // [n_maps][128]
 };
 
 // Launchers (return hipError_t of the launch).
@@ -193,7 +192,9 @@ hipError_t launch_solve_centered(int32_t n_maps, int32_t d_s, int32_t d_t, const
                                  hipStream_t s);
 hipError_t launch_fill_zero(float *p, int64_t n, hipStream_t s);
 hipError_t launch_stats_multi(const MultiArgs &a, hipStream_t s);
-hipError_t launch_apply_multi(const ApplyMultiArgs &a, hipStream_t s);
+hipError_t launch_split_maps_frag(int32_t n_maps, int32_t k, const float *maps, uint16_t *wfrag, float *bias,
+                                  hipStream_t s);
+hipError_t launch_apply_multi(const ApplyMultiArgs &a, int32_t n_cu, hipStream_t s);
 int64_t solve_blocked_bytes_per_system(int32_t P, int32_t d_t);
 hipError_t launch_solve_blocked(int32_t n_maps, int32_t P, int32_t d_t, const float *G, const float *C, float lambda,
                                 uint32_t flags, void *ws, int64_t ws_bytes, float *maps, int32_t *info,
