@@ -147,10 +147,11 @@ template <> struct Own<2, 1> {
 // does not add its own conservative waits between them and the LDS reads of
 // other ring stages; completion is tracked with explicit vmcnt waits below.
 // M0 (and EXEC, where a copy is limited to some lanes) is saved and restored
-// inside the statement, so the compiler's own use of them is unaffected.
+// inside the statement, so the compiler's own use of them is unaffected.  The
+// row copies carry the non-temporal hint: every row is read once per call.
 __device__ __forceinline__ void dma16_sbase(uint32_t voff, const void *sbase, uint32_t m0) {
     uint32_t keep;
-    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\tglobal_load_lds_dwordx4 %1, %2\n\ts_mov_b32 m0, %0"
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\tglobal_load_lds_dwordx4 %1, %2 nt\n\ts_mov_b32 m0, %0"
                  : "=&s"(keep)
                  : "v"(voff), "s"(sbase), "s"(m0)
                  : "memory");
@@ -158,8 +159,8 @@ __device__ __forceinline__ void dma16_sbase(uint32_t voff, const void *sbase, ui
 // Two copies into LDS destinations m0 and m0 + 4096 under one M0 save/restore.
 __device__ __forceinline__ void dma16_pair(uint32_t va, const void *sa, uint32_t vb, const void *sb, uint32_t m0) {
     uint32_t keep;
-    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %5\n\tglobal_load_lds_dwordx4 %1, %2\n\t"
-                 "s_add_u32 m0, m0, 0x1000\n\tglobal_load_lds_dwordx4 %3, %4\n\ts_mov_b32 m0, %0"
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %5\n\tglobal_load_lds_dwordx4 %1, %2 nt\n\t"
+                 "s_add_u32 m0, m0, 0x1000\n\tglobal_load_lds_dwordx4 %3, %4 nt\n\ts_mov_b32 m0, %0"
                  : "=&s"(keep)
                  : "v"(va), "s"(sa), "v"(vb), "s"(sb), "s"(m0)
                  : "memory", "scc");
