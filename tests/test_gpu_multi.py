@@ -217,6 +217,49 @@ def test_multi_widths_strides_ragged_tiles_and_batches(cb, k, stride, T):
     plan.close()
 
 
+def test_multi_max_width_k32_stats_and_apply(cb):
+    # the widest feature a plan takes: k = 32 source layers, P = 4,097 (two maps,
+    # 640 rows in two sequences with ragged tiles): moments and application
+    rng = np.random.default_rng(32)
+    k, L_s, H_s, L_t, H_t, B, T = 32, 33, 1, 1, 1, 2, 320
+    src, tgt, w = small_inputs(rng, L_s, H_s, L_t, H_t, B, T)
+    hm = random_multi_map(rng, k, L_s, H_s, L_t, H_t)
+    plan = cb.cb_plan_create_multi(hm, src, tgt, 1)
+    assert plan.P == 4097 and plan.n_maps == 2
+    say(f"multi k=32: P={plan.P}, {B} x {T} tokens")
+    G, C = gpu_stats(cb, plan, [(src, tgt, w)])
+    Go, Co = oracle_stats_full(hm, src, tgt, w, 1)
+    check_stats(G, C, Go, Co, [0, 1])
+    maps = random_maps(rng, plan.n_maps, plan.P, plan.d_t)
+    out = gpu_apply(cb, plan, maps, src, L_t, H_t)
+    ref = oracle_apply_multi(hm, maps, src, L_t, H_t, 128)
+    check_apply_multi(bits(out), ref, hm, range(2), " (k=32)")
+    plan.close()
+
+
+def test_multi_wide_solve_p2049_solver_alone(cb):
+    # the blocked fp64 solve at P = 2,049 (k = 16) on the GPU's own moments of
+    # 1,200 rows (fewer rows than P: only the relative ridge makes it definite),
+    # against the oracle's solve of the same fp32 moments; both ridge modes
+    rng = np.random.default_rng(16)
+    k, L_s, H_s, L_t, H_t, B, T = 16, 17, 1, 1, 1, 3, 400
+    src, tgt, w = small_inputs(rng, L_s, H_s, L_t, H_t, B, T)
+    hm = random_multi_map(rng, k, L_s, H_s, L_t, H_t)
+    plan = cb.cb_plan_create_multi(hm, src, tgt, 1)
+    G, C = gpu_stats(cb, plan, [(src, tgt, w)])
+    for unpen in (False, True):
+        flags = cb.CB_LAMBDA_RELATIVE | (cb.CB_RIDGE_BIAS_UNPENALIZED if unpen else 0)
+        maps, info = gpu_solve_ws(cb, G, C, 1e-2, flags)
+        assert (info.cpu().numpy() == 0).all()
+        Ws, io = oracle.ridge_solve(G.double().cpu().numpy(), C.double().cpu().numpy(), 1e-2, relative=True,
+                                    bias_unpenalized=unpen, n_threads=NTHREADS)
+        assert (io == 0).all()
+        e = max(relF(maps[i].double().cpu().numpy(), Ws[i]) for i in range(plan.n_maps))
+        say(f"  P=2049 solver alone (bias unpenalized={unpen}): {e:.3e}")
+        assert e <= TOL_SOLVER
+    plan.close()
+
+
 def test_multi_determinism_scaling_and_zero_weights(cb):
     rng = np.random.default_rng(77)
     L_s, H_s, L_t, H_t, B, T, k, stride = 5, 2, 2, 2, 2, 150, 3, 4
