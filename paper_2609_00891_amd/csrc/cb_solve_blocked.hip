@@ -9,13 +9,14 @@
 //                        diag(1, .., 1, 0) with CB_RIDGE_BIAS_UNPENALIZED)
 //   1. left-looking blocked Cholesky M = L L^T in panels of 32 columns:
 //      panel = M[c0:, c0:c0+32] - L[c0:, :c0] L[c0:c0+32, :c0]^T as a
-//      register-blocked GEMM (8 x 4 outputs per thread, 16-wide chunks of the
+//      register-blocked GEMM (up to 6 x 4 outputs per thread, 16-wide chunks of the
 //      inner dimension double-buffered through LDS so the next chunk's global
 //      loads overlap this chunk's FMAs); the 32 x 32 diagonal block factored
 //      by one wave in LDS, which also forms its inverse by forward
 //      elimination and stores it, transposed, in the block's unused upper
 //      half; the rows below solved against it, one row per thread;
-//   2. forward substitution L Z = C by 32-row panels: the panel GEMM, then
+//   2. forward substitution L Z = C by 32-row panels: the panel GEMM (8-wide
+//      chunks of the inner dimension through LDS), then
 //      the panel's rows times the inverse of its diagonal block (formed and
 //      kept by the factorization), both 4 x 4 outputs per thread;
 //   3. back substitution L^T W~ = Z by 32-row panels, in place of Z;
@@ -27,6 +28,7 @@
 // diagonal blocks in the upper halves of the diagonal blocks) and Z (P x d_t
 // fp64).  Systems are solved in batches that fit the workspace.
 #include <algorithm>
+#include <type_traits>
 
 #include "cb_internal.h"
 
@@ -37,18 +39,24 @@ constexpr int NT = 256;
 constexpr int NB = 32;          // panel width
 constexpr int KC = 16;          // inner-dimension chunk
 constexpr int KP = KC + 1;      // padded LDS row of a chunk (doubles)
-constexpr int TR = 256;         // rows per GEMM pass of the factorization
+constexpr int TR = 192;         // rows per GEMM pass of the factorization
+static_assert(TR == 6 * 32, "the pass dispatch below covers 1 .. 6 groups of 32 rows");
+constexpr int KS = 8;           // inner-dimension chunk of the substitutions
+constexpr int KSP = KS + 1;
 constexpr int DP = NB + 1;      // padded row of the diagonal block
 constexpr int DTMAX = 128;
 constexpr int ZP = DTMAX + 1;   // padded row of a right-hand-side chunk
 
 // LDS (doubles): factorization: A chunks [2][TR][KP], B chunks [2][NB][KP];
-// substitutions: L chunks [2][NB][KP], Z chunks [2][KC][ZP], panel rhs [NB][ZP].
+// substitutions: L chunks [2][NB][KSP], Z chunks [2][KS][ZP], panel rhs [NB][ZP].
+// About 78 KB in all, so two systems share a compute unit.
 constexpr int OFF_A = 0;
 constexpr int OFF_B = OFF_A + 2 * TR * KP;
 constexpr int OFF_L = 0;
-constexpr int OFF_Z = OFF_L + 2 * NB * KP;
-constexpr int OFF_R = OFF_Z + 2 * KC * ZP;
+constexpr int OFF_Z = OFF_L + 2 * NB * KSP;
+constexpr int OFF_R = OFF_Z + 2 * KS * ZP;
+constexpr int LQ = NB * KS / NT, ZQ = KS * DTMAX / NT;   // operand elements per thread and chunk
+static_assert(LQ * NT == NB * KS && ZQ * NT == KS * DTMAX, "substitution chunks split evenly over the threads");
 constexpr int SH_WORK = std::max(OFF_B + 2 * NB * KP, OFF_R + NB * ZP);
 
 __device__ __forceinline__ void wave_sync_lds() {
@@ -108,17 +116,21 @@ __global__ __launch_bounds__(NT) void chol_solve_kernel(int32_t P, int32_t d_t, 
     for (int c0 = 0; c0 < P; c0 += NB) {
         const int nb = min(NB, P - c0);
         const int nch = c0 / KC;                        // c0 is a multiple of 32
-        for (int rt = c0; rt < P; rt += TR) {
-            double acc[8][4];
+        // rows c0 .. P-1 in passes of up to TR rows; a pass of NI 32-row groups
+        // (the last one may be shorter) is compiled for its NI so that no FMA is
+        // spent on rows past P
+        auto gemm_pass = [&](auto NIc, int rt) {
+            constexpr int NI = decltype(NIc)::value;
+            double acc[NI][4];
 #pragma unroll
-            for (int i = 0; i < 8; ++i)
+            for (int i = 0; i < NI; ++i)
 #pragma unroll
                 for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
-            double pa[16], pb[2];
-            auto fetch = [&](int ch) {                  // chunk ch of L[rt:rt+256, :] and L[c0:c0+32, :]
+            double pa[2 * NI], pb[2];
+            auto fetch = [&](int ch) {                  // chunk ch of L[rt:rt+32NI, :] and L[c0:c0+32, :]
                 const int k0 = ch * KC, kk = tid & 15;
 #pragma unroll
-                for (int q = 0; q < 16; ++q) {
+                for (int q = 0; q < 2 * NI; ++q) {
                     const int r = rt + (tid >> 4) + 16 * q;
                     pa[q] = r < P ? L[(int64_t)r * P + k0 + kk] : 0.0;
                 }
@@ -131,7 +143,7 @@ __global__ __launch_bounds__(NT) void chol_solve_kernel(int32_t P, int32_t d_t, 
             auto stash = [&](int buf) {
                 const int kk = tid & 15;
 #pragma unroll
-                for (int q = 0; q < 16; ++q) sA[buf * TR * KP + ((tid >> 4) + 16 * q) * KP + kk] = pa[q];
+                for (int q = 0; q < 2 * NI; ++q) sA[buf * TR * KP + ((tid >> 4) + 16 * q) * KP + kk] = pa[q];
 #pragma unroll
                 for (int q = 0; q < 2; ++q) sB[buf * NB * KP + ((tid >> 4) + 16 * q) * KP + kk] = pb[q];
             };
@@ -143,19 +155,19 @@ __global__ __launch_bounds__(NT) void chol_solve_kernel(int32_t P, int32_t d_t, 
                 const double *a = sA + (ch & 1) * TR * KP, *b = sB + (ch & 1) * NB * KP;
 #pragma unroll 4
                 for (int kk = 0; kk < KC; ++kk) {
-                    double av[8], bv[4];
+                    double av[NI], bv[4];
 #pragma unroll
-                    for (int i = 0; i < 8; ++i) av[i] = a[(rg + 32 * i) * KP + kk];
+                    for (int i = 0; i < NI; ++i) av[i] = a[(rg + 32 * i) * KP + kk];
 #pragma unroll
                     for (int j = 0; j < 4; ++j) bv[j] = b[(4 * cg + j) * KP + kk];
 #pragma unroll
-                    for (int i = 0; i < 8; ++i)
+                    for (int i = 0; i < NI; ++i)
 #pragma unroll
                         for (int j = 0; j < 4; ++j) acc[i][j] = fma(av[i], bv[j], acc[i][j]);
                 }
             }
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
+            for (int i = 0; i < NI; ++i) {
                 const int r = rt + rg + 32 * i;
                 if (r >= P) continue;
 #pragma unroll
@@ -168,6 +180,16 @@ __global__ __launch_bounds__(NT) void chol_solve_kernel(int32_t P, int32_t d_t, 
                 }
             }
             __syncthreads();
+        };
+        for (int rt = c0; rt < P; rt += TR) {
+            switch (min((P - rt + 31) / 32, TR / 32)) {
+                case 1: gemm_pass(std::integral_constant<int, 1>(), rt); break;
+                case 2: gemm_pass(std::integral_constant<int, 2>(), rt); break;
+                case 3: gemm_pass(std::integral_constant<int, 3>(), rt); break;
+                case 4: gemm_pass(std::integral_constant<int, 4>(), rt); break;
+                case 5: gemm_pass(std::integral_constant<int, 5>(), rt); break;
+                default: gemm_pass(std::integral_constant<int, TR / 32>(), rt); break;
+            }
         }
         // factor the diagonal block: one wave, right-looking, in LDS
         if (wave == 0) {
@@ -257,21 +279,21 @@ __global__ __launch_bounds__(NT) void chol_solve_kernel(int32_t P, int32_t d_t, 
         for (int q = 0; q < 4; ++q)
 #pragma unroll
             for (int n = 0; n < 4; ++n) acc[q][n] = 0.0;
-        const int nch = (k_hi - k_lo + KC - 1) / KC;
-        double pl[2], pz[8];
+        const int nch = (k_hi - k_lo + KS - 1) / KS;
+        double pl[LQ], pz[ZQ];
         auto fetch = [&](int ch) {
-            const int k0 = k_lo + ch * KC;
+            const int k0 = k_lo + ch * KS;
 #pragma unroll
-            for (int q = 0; q < 2; ++q) {               // 32 x 16 operand: (i, kk)
+            for (int q = 0; q < LQ; ++q) {              // 32 x KS operand: (i, kk)
                 const int e = tid + NT * q;
                 int i, kk;
-                if (backward) { kk = e / NB; i = e % NB; } else { i = e / KC; kk = e % KC; }
+                if (backward) { kk = e / NB; i = e % NB; } else { i = e / KS; kk = e % KS; }
                 const int k = k0 + kk;
                 pl[q] = (i < nb && k < k_hi) ? (backward ? L[(int64_t)k * P + c0 + i] : L[(int64_t)(c0 + i) * P + k])
                                              : 0.0;
             }
 #pragma unroll
-            for (int q = 0; q < 8; ++q) {               // 16 x 128 operand: (kk, c)
+            for (int q = 0; q < ZQ; ++q) {              // KS x 128 operand: (kk, c)
                 const int e = tid + NT * q;
                 const int kk = e / DTMAX, c = e % DTMAX;
                 const int k = k0 + kk;
@@ -280,16 +302,16 @@ __global__ __launch_bounds__(NT) void chol_solve_kernel(int32_t P, int32_t d_t, 
         };
         auto stash = [&](int buf) {
 #pragma unroll
-            for (int q = 0; q < 2; ++q) {
+            for (int q = 0; q < LQ; ++q) {
                 const int e = tid + NT * q;
                 int i, kk;
-                if (backward) { kk = e / NB; i = e % NB; } else { i = e / KC; kk = e % KC; }
-                sL[buf * NB * KP + i * KP + kk] = pl[q];
+                if (backward) { kk = e / NB; i = e % NB; } else { i = e / KS; kk = e % KS; }
+                sL[buf * NB * KSP + i * KSP + kk] = pl[q];
             }
 #pragma unroll
-            for (int q = 0; q < 8; ++q) {
+            for (int q = 0; q < ZQ; ++q) {
                 const int e = tid + NT * q;
-                sZ[buf * KC * ZP + (e / DTMAX) * ZP + e % DTMAX] = pz[q];
+                sZ[buf * KS * ZP + (e / DTMAX) * ZP + e % DTMAX] = pz[q];
             }
         };
         if (nch > 0) fetch(0);
@@ -297,12 +319,12 @@ __global__ __launch_bounds__(NT) void chol_solve_kernel(int32_t P, int32_t d_t, 
             stash(ch & 1);
             __syncthreads();
             if (ch + 1 < nch) fetch(ch + 1);
-            const double *a = sL + (ch & 1) * NB * KP, *b = sZ + (ch & 1) * KC * ZP;
+            const double *a = sL + (ch & 1) * NB * KSP, *b = sZ + (ch & 1) * KS * ZP;
 #pragma unroll 4
-            for (int kk = 0; kk < KC; ++kk) {
+            for (int kk = 0; kk < KS; ++kk) {
                 double av[4], bv[4];
 #pragma unroll
-                for (int q = 0; q < 4; ++q) av[q] = a[(ri + 8 * q) * KP + kk];
+                for (int q = 0; q < 4; ++q) av[q] = a[(ri + 8 * q) * KSP + kk];
 #pragma unroll
                 for (int n = 0; n < 4; ++n) bv[n] = b[kk * ZP + cj + 32 * n];
 #pragma unroll
