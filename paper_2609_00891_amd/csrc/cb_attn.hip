@@ -21,12 +21,12 @@
 // and a long key range share each SIMD).  Key tiles of 32 rows of K and V are
 // streamed into a double-buffered LDS ring (16-byte chunks XOR-swizzled by
 // key) by all 512 threads, which also form |v_i|^2; the waves then sweep the
-// keys four times:
+// keys three times:
 //   A  S^T = K Q^T (v_mfma_f32_32x32x16_bf16, one lane per query): the
-//      online softmax maximum m and normalizer l of every query;
-//   B1 with the final m and l, a = exp(s - m) / l directly: o = sum a v (a
-//      split into two bf16 terms, V^T read with ds_read_b64_tr_b16 in the key
-//      order of the accumulator layout);
+//      online softmax maximum m and normalizer l of every query, and with
+//      them o = sum exp(s - m) v / l (the partial o rescaled whenever m
+//      grows; exp(s - m) split into two bf16 terms, V^T read with
+//      ds_read_b64_tr_b16 in the key order of the accumulator layout);
 //   B2 sum a^2 v, sum a^2 and sum a^2 |v|^2 over the eligible keys, then the
 //      unit masses of every boundary for both components (the K mass is
 //      sum a^2 (|v|^2 - 2 o.v + |o|^2) |q|^2 / d, expanded);
@@ -34,7 +34,7 @@
 //      key): every eligible (query, key) term, summed over the wave's queries
 //      in registers; the eight waves' sums are added in a fixed order.
 // Separate sweeps keep one set of accumulators live at a time (two waves per
-// SIMD leave 256 registers per lane) and make B1 and B2 free of rescaling.
+// SIMD leave 256 registers per lane) and make B2 free of rescaling.
 #include "cb_internal.h"
 
 namespace cb {
@@ -211,31 +211,8 @@ void attn_sens_kernel(AttnArgs a) {
     const int ntAll = (cmax + kKT) / kKT;
     const int ntAllC = cmax > 0 ? (cmax + kKT - 1) / kKT : 0;
 
-    // ---- sweep A: softmax maximum and normalizer (log2 units)
-    float m = -HUGE_VALF, lsum = 0.f;
-    sweep(ntAll, [&](int kt, int st) {
-        if (kt >= ntAB) return;
-        const f32x16_t S = s_tile(st, true);
-        float x[16], tmax = -HUGE_VALF;
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            const int key = kt * kKT + acc_row(v, hh);
-            x[v] = key <= c ? S[v] * a.scale_log2 : -HUGE_VALF;
-            tmax = fmaxf(tmax, x[v]);
-        }
-        tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-        if (tmax > -HUGE_VALF) {
-            const float mn = fmaxf(m, tmax);
-            float ts = 0.f;
-#pragma unroll
-            for (int v = 0; v < 16; ++v) ts += exp2f(x[v] - mn);
-            ts += __shfl_xor(ts, 32);
-            lsum = lsum * exp2f(m - mn) + ts;
-            m = mn;
-        }
-    });
-    const float inv_l = lsum > 0.f ? 1.f / lsum : 0.f;
 
+    float m = -HUGE_VALF, lsum = 0.f, inv_l = 0.f;             // per query row, log2 units
     // V^T operand of key step kk of 32-d tile t: d row 32 t + (lane & 31), keys
     // 16 kk + {0..3, 8..11} + 4 hh (the key order of the accumulator layout)
     auto vtfrag = [&](const char *Vs, int kk, int t) {
@@ -262,20 +239,45 @@ void attn_sens_kernel(AttnArgs a) {
         }
     };
 
-    // ---- sweep B1: o = sum a v
+    // ---- sweep A: the softmax maximum m and normalizer l (log2 units) and,
+    // online, o = sum_i exp(s_i - m) v_i / l: whenever a tile raises a row's
+    // maximum its partial o is rescaled by exp(m_old - m_new), and o is divided
+    // by l once every key has been seen.  p = exp(s - m) <= 1 enters the MFMA
+    // as two bf16 terms.
     f32x16_t OT[NDT];
 #pragma unroll
     for (int t = 0; t < NDT; ++t) OT[t] = f32x16_t{};
     sweep(ntAll, [&](int kt, int st) {
         if (kt >= ntAB) return;
         const f32x16_t S = s_tile(st, true);
+        float x[16], tmax = -HUGE_VALF;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int key = kt * kKT + acc_row(v, hh);
+            x[v] = key <= c ? S[v] * a.scale_log2 : -HUGE_VALF;
+            tmax = fmaxf(tmax, x[v]);
+        }
+        tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+        const float mn = fmaxf(m, tmax);                     // -inf only while the row has no key yet
+        const float alpha = m > -HUGE_VALF ? exp2f(m - mn) : 0.f;
+        float pv[16], ts = 0.f;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            pv[v] = x[v] > -HUGE_VALF ? exp2f(x[v] - mn) : 0.f;
+            ts += pv[v];
+        }
+        ts += __shfl_xor(ts, 32);
+        lsum = lsum * alpha + ts;
+        m = mn;
+#pragma unroll
+        for (int t = 0; t < NDT; ++t)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) OT[t][v] *= alpha;
         const char *Vs = kst(st) + TB;
 #pragma unroll
         for (int kk = 0; kk < 2; ++kk) {
-            float av[8];
-            probs(S, kt, kk, false, av);
             bf16x8_t ph, pl;
-            split8(av, ph, pl);
+            split8(pv + 8 * kk, ph, pl);
 #pragma unroll
             for (int t = 0; t < NDT; ++t) {
                 const bf16x8_t vf = vtfrag(Vs, kk, t);
@@ -284,6 +286,11 @@ void attn_sens_kernel(AttnArgs a) {
             }
         }
     });
+    inv_l = lsum > 0.f ? 1.f / lsum : 0.f;
+#pragma unroll
+    for (int t = 0; t < NDT; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) OT[t][v] *= inv_l;
     float oo = 0.f;
     bf16x8_t oh[NDT][2], ol[NDT][2];                          // o as two bf16 terms (the A operand of o V^T)
 #pragma unroll
