@@ -40,6 +40,7 @@ struct cb_plan {
     cb::StatsItem *d_items = nullptr;
     int32_t *d_map_item = nullptr;
     int32_t *d_map_slot = nullptr;
+    int32_t *d_map_yown = nullptr;
     float *d_partials = nullptr;
     void *d_zero = nullptr;        // zero bytes: source of copies for absent tokens
     // application schedule and split coefficients
@@ -226,6 +227,7 @@ cb::ReduceArgs reduce_args(const cb_plan *p, const cb::StatsArgs &a) {
     r.partials = p->d_partials;
     r.map_item = p->d_map_item;
     r.map_slot = p->d_map_slot;
+    r.map_yown = p->d_map_yown;
     r.n_items = p->n_items;
     r.n_chunks = a.n_chunks;
     r.n_maps = p->n_maps;
@@ -257,6 +259,7 @@ cb_status cb_plan_destroy(cb_plan *p) {
     hipFree(p->d_items);
     hipFree(p->d_map_item);
     hipFree(p->d_map_slot);
+    hipFree(p->d_map_yown);
     hipFree(p->d_partials);
     hipFree(p->d_zero);
     hipFree(p->d_groups);
@@ -332,8 +335,22 @@ cb_status cb_plan_create(const cb_head_map *map, const cb_cache *src_geom, const
         }
     }
 
+    // Target sums (sum w y, sum w y^2) depend only on the target block and the
+    // weight row: the first map of each such pair carries them for all of its
+    // maps, so the means pass reads every target row once per call.
+    std::vector<int32_t> yown(n);
+    {
+        std::map<std::tuple<int, int, int, int>, int> first;
+        for (int m = 0; m < n; ++m) {
+            const auto key = std::make_tuple(map->tgt_layer[m], map->kv[m], map->tgt_head[m], map->weight_row[m]);
+            auto f = first.find(key);
+            if (f == first.end()) f = first.emplace(key, m).first;
+            yown[m] = f->second;
+        }
+    }
     auto fill_slot = [&](cb::StatsItem &it, int s, int m) {
         it.map[s] = m;
+        it.own_y[s] = yown[m] == m;
         it.src_layer[s] = map->src_layer[m];
         it.src_head[s] = map->src_head[m];
         it.kv[s] = map->kv[m];
@@ -406,6 +423,7 @@ cb_status cb_plan_create(const cb_head_map *map, const cb_cache *src_geom, const
     bool okm = hipMalloc(&p->d_items, sizeof(cb::StatsItem) * items.size()) == hipSuccess &&
                hipMalloc(&p->d_map_item, sizeof(int32_t) * n) == hipSuccess &&
                hipMalloc(&p->d_map_slot, sizeof(int32_t) * n) == hipSuccess &&
+               hipMalloc(&p->d_map_yown, sizeof(int32_t) * n) == hipSuccess &&
                hipMalloc(&p->d_partials, partial_bytes) == hipSuccess &&
                hipMalloc(&p->d_zero, 256) == hipSuccess &&
                hipMalloc(&p->d_groups, sizeof(cb::ApplyGroup) * agroups.size()) == hipSuccess &&
@@ -420,6 +438,7 @@ cb_status cb_plan_create(const cb_head_map *map, const cb_cache *src_geom, const
                hipMemcpy(p->d_items, items.data(), sizeof(cb::StatsItem) * items.size(), hipMemcpyHostToDevice) == hipSuccess &&
                hipMemcpy(p->d_map_item, map_item.data(), sizeof(int32_t) * n, hipMemcpyHostToDevice) == hipSuccess &&
                hipMemcpy(p->d_map_slot, map_slot.data(), sizeof(int32_t) * n, hipMemcpyHostToDevice) == hipSuccess &&
+               hipMemcpy(p->d_map_yown, yown.data(), sizeof(int32_t) * n, hipMemcpyHostToDevice) == hipSuccess &&
                hipMemcpy(p->d_groups, agroups.data(), sizeof(cb::ApplyGroup) * agroups.size(), hipMemcpyHostToDevice) == hipSuccess;
     if (!okc) {
         cb_plan_destroy(p);

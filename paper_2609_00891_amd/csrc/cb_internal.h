@@ -18,6 +18,7 @@ struct StatsItem {
     int32_t map[2];
     int32_t src_layer[2], src_head[2], kv[2];
     int32_t tgt_layer[2], tgt_head[2], wrow[2];
+    int32_t own_y[2];     // this slot's map carries the target sums of its (target block, weight row)
 };
 
 // One source block (src_layer, kv, src_head) and up to two target maps that
@@ -73,6 +74,7 @@ struct ReduceArgs {
     const float *partials;
     const int32_t *map_item;  // [n_maps]
     const int32_t *map_slot;  // [n_maps]
+    const int32_t *map_yown;  // [n_maps]: the map whose means partial holds this map's target sums
     int32_t n_items, n_chunks, n_maps;
     float *G, *C;         // plain: G [n][P][P], C [n][P][d_t]; centered: A [n][d_s][d_s], B [n][d_s][d_t]
     double *sums;         // centered: read; means: added to.  [n_maps][1 + d_s + d_t] = (sum w, sum w x, sum w y)

@@ -72,6 +72,7 @@ __device__ __forceinline__ void means_unit(const StatsArgs &a, const StatsItem *
                                : a.tgt + it->tgt_layer[slot] * st.layer + it->kv[slot] * st.kv + it->tgt_head[slot] * st.head;
     base += 8 * cc + (int64_t)row * st.tok;
     const float *wp = a.w + (int64_t)it->wrow[slot] * a.w_row_stride + row;
+    const bool load = isx || it->own_y[slot];                   // target rows: the owner map's item only
     const int64_t jstep = (int64_t)R * st.tok;                  // elements between a thread's tokens
 
     double acc[8], acq[8], sw = 0.0;
@@ -91,7 +92,7 @@ __device__ __forceinline__ void means_unit(const StatsArgs &a, const StatsItem *
             v[j] = make_uint4(0u, 0u, 0u, 0u);
             wa[j] = 0.f;
             if (row + j * R < nvalid) {
-                v[j] = *(const uint4 *)(p + j * jstep);
+                if (load) v[j] = *(const uint4 *)(p + j * jstep);
                 wa[j] = wp[w0 + j * R];
             }
         }
@@ -161,11 +162,15 @@ __global__ __launch_bounds__(256) void means_reduce_kernel(ReduceArgs a) {
     using M = MCfg<DS, DT, SQ>;
     const int m = blockIdx.x;
     const int item = a.map_item[m], slot = a.map_slot[m];
+    const int o = a.map_yown[m];                               // carries the target sums
     const double *part = (const double *)a.partials + ((int64_t)item * 2 + slot) * M::NE;
+    const double *opart = (const double *)a.partials + ((int64_t)a.map_item[o] * 2 + a.map_slot[o]) * M::NE;
     const int64_t chunk_stride = (int64_t)a.n_items * 2 * M::NE;
     for (int e = threadIdx.x; e < M::NE; e += 256) {
+        const bool ysum = (e >= 1 + DS && e < M::NS) || e >= M::NS + DS;
+        const double *src = ysum ? opart : part;
         double s = 0.0;
-        for (int ch = 0; ch < a.n_chunks; ++ch) s += part[ch * chunk_stride + e];
+        for (int ch = 0; ch < a.n_chunks; ++ch) s += src[ch * chunk_stride + e];
         if (e < M::NS) a.sums[(int64_t)m * M::NS + e] += s;
         else a.sq[(int64_t)m * M::NQ + (e - M::NS)] += s;
     }
