@@ -568,6 +568,10 @@ def main():
     }
     if args.centered_steps > 0:
         res["centered"] = centered_leg(cb, plan, wl, src, tgt, w, n_calls, maps, bytes_per_call, args.centered_steps)
+        # context: the weighted-means pass streams exactly the statistics call's bytes with no matrix work;
+        # its rate is the read rate this workload reaches on this board (the fraction above stays vs 8 TB/s)
+        res["roofline"]["measured_read_ceiling_GBps"] = res["centered"]["means_GBps"]
+        res["roofline"]["frac_of_measured_read_ceiling"] = achieved / res["centered"]["means_GBps"]
     if args.probe_steps > 0 or args.attn_steps > 0:
         del G, C
     if args.probe_steps > 0:
