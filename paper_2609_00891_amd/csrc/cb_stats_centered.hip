@@ -35,13 +35,14 @@ struct MCfg {
 };
 
 // Geometry of pass 1 for an item of NSL maps: NCOL 16-byte chunks per token
-// (x0 y0, or x0 y0 x1 y1), R token rows per workgroup pass, J loads per thread
-// per 32-token tile.
-template <int DS, int DT, int NSL>
+// (x0 y0, or x0 y0 x1 y1; x0, or x0 x1, when YS is false because none of the
+// item's maps carries target sums), R token rows per workgroup pass (at most
+// the rows of the reduction buffer), J loads per thread per 32-token tile.
+template <int DS, int DT, int NSL, bool YS>
 struct MGeo {
     static constexpr int NCBX = DS / 8, NCBY = DT / 8;
-    static constexpr int NCOL = NSL * (NCBX + NCBY);
-    static constexpr int R = 256 / NCOL;
+    static constexpr int NCOL = NSL * (YS ? NCBX + NCBY : NCBX);
+    static constexpr int R = 256 / NCOL < 256 / (NCBX + NCBY) ? 256 / NCOL : 256 / (NCBX + NCBY);
     static constexpr int J = (kStatsTileTokens + R - 1) / R;
 };
 
@@ -52,19 +53,20 @@ struct MGeo {
 // repeated lines do not reach HBM twice.  Tiles are whole 32-token runs of
 // one sequence, so their position is computed once per tile (the same in
 // every thread).
-template <int DS, int DT, bool SQ, int NSL>
+template <int DS, int DT, bool SQ, int NSL, bool YS>
 __device__ __forceinline__ void means_unit(const StatsArgs &a, const StatsItem *it, int tile_begin, int n_tiles,
                                            double (*red)[2 * MCfg<DS, DT, SQ>::NE]) {
     using M = MCfg<DS, DT, SQ>;
-    using Gm = MGeo<DS, DT, NSL>;
+    using Gm = MGeo<DS, DT, NSL, YS>;
     constexpr int NCBX = M::NCBX, NCBY = M::NCBY, NS = M::NS, NE = M::NE, R = Gm::R, J = Gm::J;
     const int tid = threadIdx.x;
     const int col = tid % Gm::NCOL, row = tid / Gm::NCOL;
     if (row >= R) return;
 
     // column -> map slot, x or y row, and chunk within the row
-    const int slot = col / (NCBX + NCBY);
-    const int cs = col - slot * (NCBX + NCBY);
+    constexpr int NPS = YS ? NCBX + NCBY : NCBX;                 // columns per slot
+    const int slot = col / NPS;
+    const int cs = col - slot * NPS;
     const bool isx = cs < NCBX;
     const int cc = isx ? cs : cs - NCBX;
     const Strides st = isx ? a.ss : a.ts;
@@ -145,8 +147,14 @@ void means_kernel(StatsArgs a) {
     const int n_tiles = min(a.n_tiles, tile_begin + a.chunk_tiles) - tile_begin;
     if (n_tiles <= 0) return;                                  // the same in every thread
     int R;
-    if (n_slots == 1) { means_unit<DS, DT, SQ, 1>(a, it, tile_begin, n_tiles, red); R = MGeo<DS, DT, 1>::R; }
-    else { means_unit<DS, DT, SQ, 2>(a, it, tile_begin, n_tiles, red); R = MGeo<DS, DT, 2>::R; }
+    const bool ys = it->own_y[0] || (n_slots == 2 && it->own_y[1]);   // the same in every thread
+    if (n_slots == 1) {
+        if (ys) { means_unit<DS, DT, SQ, 1, true>(a, it, tile_begin, n_tiles, red); R = MGeo<DS, DT, 1, true>::R; }
+        else { means_unit<DS, DT, SQ, 1, false>(a, it, tile_begin, n_tiles, red); R = MGeo<DS, DT, 1, false>::R; }
+    } else {
+        if (ys) { means_unit<DS, DT, SQ, 2, true>(a, it, tile_begin, n_tiles, red); R = MGeo<DS, DT, 2, true>::R; }
+        else { means_unit<DS, DT, SQ, 2, false>(a, it, tile_begin, n_tiles, red); R = MGeo<DS, DT, 2, false>::R; }
+    }
     __syncthreads();
     double *dst = (double *)a.partials + (int64_t)unit * 2 * NE;
     for (int idx = threadIdx.x; idx < n_slots * NE; idx += 256) {
@@ -167,7 +175,8 @@ __global__ __launch_bounds__(256) void means_reduce_kernel(ReduceArgs a) {
     const double *opart = (const double *)a.partials + ((int64_t)a.map_item[o] * 2 + a.map_slot[o]) * M::NE;
     const int64_t chunk_stride = (int64_t)a.n_items * 2 * M::NE;
     for (int e = threadIdx.x; e < M::NE; e += 256) {
-        const bool ysum = (e >= 1 + DS && e < M::NS) || e >= M::NS + DS;
+        // sum w and the target sums come from the map that carries them (same weight row and target)
+        const bool ysum = e == 0 || (e >= 1 + DS && e < M::NS) || e >= M::NS + DS;
         const double *src = ysum ? opart : part;
         double s = 0.0;
         for (int ch = 0; ch < a.n_chunks; ++ch) s += src[ch * chunk_stride + e];

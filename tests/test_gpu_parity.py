@@ -669,6 +669,8 @@ def test_probe_r2_and_layer_selection(cb, d_s, d_t):
     sqo = oracle.weighted_squares(chm, xb, ss, d_s, yb, ts, d_t, ws, Bn * T, Bn, T, n_threads=NTHREADS)
     esq = max(relF(sq[m].cpu().numpy(), sqo[m]) for m in sel)
     so, Ao, Bo = oracle.stats_centered(chm, xb, ss, d_s, yb, ts, d_t, ws, Bn * T, Bn, T, n_threads=NTHREADS)
+    # every map's (sum w, sum w x, sum w y), including the maps whose target sums another map carries
+    esum = max(relF(sums[m].cpu().numpy(), so[m]) for m in sel)
     Wo, io = oracle.ridge_solve_centered(so, Ao, Bo, 0.0, relative=False, n_threads=NTHREADS)
     assert (io == 0).all()
     r2o = oracle.probe_r2(chm, Wo, xb, ss, d_s, yb, ts, d_t, ws, Bn * T, Bn, T, n_threads=NTHREADS)
@@ -677,8 +679,9 @@ def test_probe_r2_and_layer_selection(cb, d_s, d_t):
                           n_threads=NTHREADS)
     g = r2.cpu().numpy()
     e_end, e_alone = float(np.abs(g - r2o).max()), float(np.abs(g - r2s).max())
-    say(f"  probes: sq relF {esq:.3e}; R^2 max |diff| end-to-end {e_end:.3e}, kernel alone {e_alone:.3e}")
-    assert esq <= TOL_SUMS and e_end <= TOL_R2 and e_alone <= TOL_R2
+    say(f"  probes: sums relF {esum:.3e}, sq relF {esq:.3e}; R^2 max |diff| end-to-end {e_end:.3e}, "
+        f"kernel alone {e_alone:.3e}")
+    assert esum <= TOL_SUMS and esq <= TOL_SUMS and e_end <= TOL_R2 and e_alone <= TOL_R2
     # selection: the planted layer first on both sides; the full order agrees
     # wherever the oracle's scores are separated by more than the R^2 bar
     selg, scg = cb.cb_select_layers(hm, g, L_t, L_s, L_s)
