@@ -256,20 +256,20 @@ const char *cb_last_error(void) { return g_last_error.c_str(); }
 cb_status cb_plan_destroy(cb_plan *p) {
     if (!p) return ok();
     (void)hipDeviceSynchronize();
-    hipFree(p->d_items);
-    hipFree(p->d_map_item);
-    hipFree(p->d_map_slot);
-    hipFree(p->d_map_yown);
-    hipFree(p->d_partials);
-    hipFree(p->d_zero);
-    hipFree(p->d_groups);
-    hipFree(p->d_whi);
-    hipFree(p->d_wlo);
-    hipFree(p->d_bias);
-    hipFree(p->d_tasks);
-    hipFree(p->d_amaps);
-    hipFree(p->d_aorder);
-    hipFree(p->d_alayers);
+    (void)hipFree(p->d_items);
+    (void)hipFree(p->d_map_item);
+    (void)hipFree(p->d_map_slot);
+    (void)hipFree(p->d_map_yown);
+    (void)hipFree(p->d_partials);
+    (void)hipFree(p->d_zero);
+    (void)hipFree(p->d_groups);
+    (void)hipFree(p->d_whi);
+    (void)hipFree(p->d_wlo);
+    (void)hipFree(p->d_bias);
+    (void)hipFree(p->d_tasks);
+    (void)hipFree(p->d_amaps);
+    (void)hipFree(p->d_aorder);
+    (void)hipFree(p->d_alayers);
     delete p;
     return ok();
 }

@@ -134,7 +134,7 @@ __device__ __forceinline__ void means_unit(const StatsArgs &a, const StatsItem *
 // One workgroup per (item, chunk) unit: the unit's rows are combined through
 // LDS in a fixed order and written as an fp64 partial [unit][2][NE].
 template <int DS, int DT, bool SQ>
-__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(4)))
+__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(SQ ? 2 : 4)))
 void means_kernel(StatsArgs a) {
     using M = MCfg<DS, DT, SQ>;
     constexpr int NE = M::NE;
