@@ -699,6 +699,44 @@ def test_probe_r2_and_layer_selection(cb, d_s, d_t):
     plan.close()
 
 
+def test_means_shared_and_distinct_target_sums(cb):
+    """Maps that read one target block under one weight row share a single set of
+    target sums (and sum w) in the means pass; maps that read it under different
+    weight rows do not.  Every map's sums and sums of squares against the oracle."""
+    L_s, L_t, H = 3, 2, 2
+    wl = synth.Workload("probe", L_s, H, 64, L_t, H, 96, 3, 200, "qwen", "offset", 0.3, "lognormal")
+    src, tgt, _ = make_inputs(wl)
+    hm = probe_head_map(L_t, L_s, H)
+    n = len(hm["kv"])
+    base = L_t * H
+    wr = hm["weight_row"].copy()
+    for m in range(n):                      # odd source layers: a weight row of their own per target
+        if hm["src_layer"][m] % 2 == 1:
+            wr[m] = base + hm["tgt_layer"][m] * H + hm["tgt_head"][m]
+    hm["weight_row"] = wr
+    N = wl.n_seqs * wl.seq_len
+    g = torch.Generator(device="cuda")
+    g.manual_seed(5)
+    w = torch.exp(torch.randn((2 * base, N), generator=g, device="cuda"))
+    plan = cb.cb_plan_create(hm, src, tgt, N)
+    sums = torch.empty((n, 1 + 64 + 96), dtype=torch.float64, device="cuda")
+    sq = torch.empty((n, 64 + 96), dtype=torch.float64, device="cuda")
+    A = torch.empty((n, 64, 64), dtype=torch.float32, device="cuda")
+    B = torch.empty((n, 64, 96), dtype=torch.float32, device="cuda")
+    cb.cb_stats_zero_centered(plan, sums, A, B, sq=sq)
+    cb.cb_stats_means(plan, src, tgt, w, sums, sq=sq)
+    torch.cuda.synchronize()
+    sel = list(range(n))
+    chm, xb, ss, yb, ts, ws, Bn, T = compact(hm, sel, src, tgt, w)
+    so, _, _ = oracle.stats_centered(chm, xb, ss, 64, yb, ts, 96, ws, Bn * T, Bn, T, n_threads=NTHREADS)
+    sqo = oracle.weighted_squares(chm, xb, ss, 64, yb, ts, 96, ws, Bn * T, Bn, T, n_threads=NTHREADS)
+    esum = max(relF(sums[m].cpu().numpy(), so[m]) for m in sel)
+    esq = max(relF(sq[m].cpu().numpy(), sqo[m]) for m in sel)
+    say(f"  shared / distinct target sums: sums relF {esum:.3e}, sq relF {esq:.3e}")
+    assert esum <= TOL_SUMS and esq <= TOL_SUMS
+    plan.close()
+
+
 def test_probe_qwen_shape_all_layer_pairs_sampled_maps(cb):
     # the selector's real size: 64 target layers x 40 source layers x 8 heads x
     # K/V = 40,960 probes over a 2 x 1024-token calibration slice
