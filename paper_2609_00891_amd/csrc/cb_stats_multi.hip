@@ -429,7 +429,7 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
         for (int i = 0; i < 2 * E; ++i) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);            // one MFMA
             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);            // one LDS read
-            __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);            // three VALU
+            __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);            // up to five VALU
         }
         __builtin_amdgcn_sched_barrier(0);
         read_half(oc, (i + 2) % K::NST, 1);
@@ -441,7 +441,7 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
         for (int i = 0; i < 2 * E; ++i) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);            // up to five VALU
         }
         __builtin_amdgcn_sched_barrier(0);
         if constexpr (YS) sum_y(ob);
