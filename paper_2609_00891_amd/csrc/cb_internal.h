@@ -202,7 +202,7 @@ hipError_t launch_solve_blocked(int32_t n_maps, int32_t P, int32_t d_t, const fl
                                 uint32_t flags, void *ws, int64_t ws_bytes, float *maps, int32_t *info,
                                 hipStream_t s);
 constexpr int kMultiTileRows = 16;      // calibration rows per multi-layer tile
-constexpr int kMultiFlushTiles = 1020;  // at most 16,320 rows summed in fp32 before a flush (a multiple of 6)
+constexpr int kMultiFlushTiles = 2046;  // at most 32,736 rows summed in fp32 before a flush (a multiple of 6)
 hipError_t launch_solve(int32_t n_maps, int32_t P, int32_t d_t, const float *G, const float *C,
                         float lambda, uint32_t flags, float *maps, int32_t *info, hipStream_t s);
 hipError_t launch_split_maps(int32_t n_maps, int32_t d_s, int32_t d_t, const float *maps,

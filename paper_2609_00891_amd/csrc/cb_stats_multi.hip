@@ -36,7 +36,7 @@
 // operand reads (ds_read_b64_tr_b16) are conflict free.  Rows past the end of
 // a sequence repeat its last row with weight zero.
 //
-// Flush.  Every at most 1,020 tiles (16,320 rows) and at the end of the call
+// Flush.  Every at most 2,046 tiles (32,736 rows) and at the end of the call
 // each wave adds its tiles into G (and C): a tile above the diagonal goes to
 // its block and, transposed through LDS, to the mirrored block; a tile on the
 // diagonal contributes its upper triangle to both triangles; tiles below the
