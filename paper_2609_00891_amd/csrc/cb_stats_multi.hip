@@ -124,20 +124,30 @@ __device__ __forceinline__ void dma_tile(const uint32_t (&voff)[NL], const void 
 }
 
 // Adds the 32 x 32 tile held in the wave's transpose scratch `tr` (row i at
-// tr + 33 i) into global memory, two rows per step: mode 0 and 2 add it at
-// dst (leading dimension ld), mode 2 also adds its transpose at mir, and mode
-// 1 (a diagonal tile of G) adds its upper triangle to both triangles.
+// tr + 33 i) into global memory, two rows per lane group: mode 0 and 2 add it
+// at dst (leading dimension ld), mode 2 also adds its transpose at mir, and
+// mode 1 (a diagonal tile of G) adds its upper triangle to both triangles.
+// The loads of two row pairs are issued before their adds, so the global
+// latency is paid 8 times per tile, not 16 (the loop's operand pipeline stays
+// live across a flush, which leaves no registers for more).
 __device__ __forceinline__ void flush_rows(const float *tr, int lane, int mode, float *dst, float *mir, int64_t ld) {
+    constexpr int FB = 2;
     const int jj = lane & 31;
 #pragma unroll 1
-    for (int it = 0; it < 16; ++it) {
-        const int ii = 2 * it + (lane >> 5);
-        const float up = tr[ii * MCfg::TRS + jj], dn = tr[jj * MCfg::TRS + ii];
-        float *d = dst + (int64_t)ii * ld + jj;
-        *d += mode == 1 && ii > jj ? dn : up;
-        if (mode == 2) {
-            float *dm = mir + (int64_t)ii * ld + jj;
-            *dm += dn;
+    for (int i0 = 0; i0 < 16; i0 += FB) {
+        float cur[FB], curm[FB];
+#pragma unroll
+        for (int it = 0; it < FB; ++it) {
+            const int ii = 2 * (i0 + it) + (lane >> 5);
+            cur[it] = dst[(int64_t)ii * ld + jj];
+            curm[it] = mode == 2 ? mir[(int64_t)ii * ld + jj] : 0.f;
+        }
+#pragma unroll
+        for (int it = 0; it < FB; ++it) {
+            const int ii = 2 * (i0 + it) + (lane >> 5);
+            const float up = tr[ii * MCfg::TRS + jj], dn = tr[jj * MCfg::TRS + ii];
+            dst[(int64_t)ii * ld + jj] = cur[it] + (mode == 1 && ii > jj ? dn : up);
+            if (mode == 2) mir[(int64_t)ii * ld + jj] = curm[it] + dn;
         }
     }
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
