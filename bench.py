@@ -298,26 +298,37 @@ def attn_leg(cb, synth, bw, tgt, steps):
     }
 
 
-def rope_leg(cb, cache, steps):
-    """Target RoPE restored on mapped keys (Sec. 3.1): an in-place rotation of the
-    K rows of the applied 8 x 32,768-token target cache (base 1e6, half-split
-    pairs), timed with events after one warm-up pass (the cache is not used
-    afterwards)."""
+def rope_leg(cb, plan, maps, asrc, cache, steps):
+    """Target RoPE restored on mapped keys (Sec. 3.1) for the applied 8 x 32,768-token
+    target cache (base 1e6, half-split pairs): the in-place rotation pass over its
+    K rows, and the fused form (cb_apply_rope: mapping and rotation in one kernel,
+    one rounding) against cb_apply alone, each timed with events after one warm-up
+    call (the cache is not used afterwards)."""
     import torch
     L, _, B, H, T, d = cache.shape
     table = torch.empty((T, d // 2, 2), dtype=torch.float32, device="cuda")
     cb.cb_rope_table(1e6, d, T, table)
     stream = torch.cuda.current_stream()
-    e = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 2)]
-    cb.cb_rope(cache, cache, table)
-    e[0].record(stream)
-    for i in range(steps):
-        cb.cb_rope(cache, cache, table, inverse=(i % 2 == 0))
-        e[i + 1].record(stream)
-    torch.cuda.synchronize()
-    ms = sum(e[i].elapsed_time(e[i + 1]) for i in range(steps)) / steps
+
+    def timed(fn):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+        fn(0)
+        e[0].record(stream)
+        for i in range(steps):
+            fn(i)
+            e[i + 1].record(stream)
+        torch.cuda.synchronize()
+        return sum(e[i].elapsed_time(e[i + 1]) for i in range(steps)) / steps
+
+    ms = timed(lambda i: cb.cb_rope(cache, cache, table, inverse=(i % 2 == 0)))
     bytes_ = 2 * L * B * H * T * d * 2                       # K rows read and written once
-    return {"ms": ms, "GBps": bytes_ / (ms / 1e3) / 1e9, "bytes_per_pass": bytes_}
+    res = {"ms": ms, "GBps": bytes_ / (ms / 1e3) / 1e9, "bytes_per_pass": bytes_}
+    if plan is not None:
+        apply_ms = timed(lambda i: cb.cb_apply(plan, maps, asrc, cache))
+        fused_ms = timed(lambda i: cb.cb_apply_rope(plan, maps, asrc, cache, table))
+        res.update({"apply_ms": apply_ms, "apply_rope_fused_ms": fused_ms,
+                    "apply_then_rope_ms": apply_ms + ms})
+    return res
 
 
 def multi_leg(cb, synth, steps):
@@ -579,7 +590,7 @@ def main():
     if args.attn_steps > 0:
         res["attn_weights"] = attn_leg(cb, synth, bw, tgt, args.attn_steps)
     if args.rope_steps > 0 and aout is not None:
-        res["rope"] = rope_leg(cb, aout, args.rope_steps)
+        res["rope"] = rope_leg(cb, plan, maps, asrc, aout, args.rope_steps)
     if args.multi_steps > 0:
         asrc = aout = None
         torch.cuda.empty_cache()

@@ -31,7 +31,7 @@
  * and the rotary position transform of cached keys (Sec. 2.1, Sec. 3.1: RoPE
  * removed before fitting, restored after mapping):
  *
- *   cb_rope_table, cb_rope
+ *   cb_rope_table, cb_rope, cb_apply_rope (mapping with the target RoPE fused)
  *
  * and the multi-layer feature of Sec. 3.2 (k selected source layers per map):
  *
@@ -392,6 +392,23 @@ cb_status cb_rope(const cb_cache *in, const cb_cache *out, const float *table, i
  */
 cb_status cb_apply(cb_plan *plan, const float *maps, const cb_cache *src, const cb_cache *tgt_out,
                    void *stream);
+
+/*
+ * Online mapping with the target's rotary transform fused (Sec. 1 pipeline;
+ * Sec. 2.1, Sec. 3.1: the mapped keys receive the target model's RoPE before
+ * decoding).  Identical to cb_apply for V outputs (kv = 1).  For K outputs
+ * (kv = 0) the fp32 sum s = x W + b of each token at position pos = pos_offset
+ * + tok has its channel pairs (style CB_ROPE_HALF_SPLIT or
+ * CB_ROPE_INTERLEAVED) turned by the table's angle of pos,
+ *   (a, b) -> (a cos - b sin, b cos + a sin),
+ * in fp32 and is then rounded once to bfloat16; cb_apply followed by cb_rope
+ * rounds twice.  table: from cb_rope_table with head_dim = the plan's d_t and
+ * n_pos >= pos_offset + seq_len, device, 16-byte aligned, caller-owned.
+ * Errors as cb_apply; CB_ERR_SHAPE for a short table, CB_ERR_UNSUPPORTED for
+ * a multi-layer plan (apply those with cb_apply, then cb_rope).
+ */
+cb_status cb_apply_rope(cb_plan *plan, const float *maps, const cb_cache *src, const cb_cache *tgt_out,
+                        const float *table, int32_t n_pos, int32_t style, int32_t pos_offset, void *stream);
 
 /*
  * Multi-layer mapper support (Sec. 3.2, Eq. localfeature with k selected

@@ -727,6 +727,62 @@ int oracle_stats_multi(int n_maps, int k,
 }
 
 /*
+ * Online application with the target's rotary transform (Sec. 1 pipeline;
+ * Sec. 2.1, Sec. 3.1: the mapped keys receive the target RoPE).  For every map
+ * and token, s = x~ W~ in fp64 as in oracle_apply; when the map is a K map
+ * (kv = 0), the pairs of s (style 0: (i, i + d_t/2), style 1: (2i, 2i + 1))
+ * are turned by the angle pos * theta^(-2 i / d_t), pos = pos_offset + t:
+ *   (a, b) -> (a cos - b sin, b cos + a sin),
+ * in fp64; then every channel is rounded once to bf16 (RNE).  V maps write
+ * RNE_bf16(s).  Returns 0.
+ */
+int oracle_apply_rope(int n_maps,
+                      const int32_t *tgt_layer, const int32_t *tgt_head, const int32_t *kv,
+                      const int32_t *src_layer, const int32_t *src_head,
+                      const double *W,
+                      const uint16_t *src, const int64_t *src_strides, int d_s,
+                      uint16_t *out, const int64_t *out_strides, int d_t,
+                      int n_seqs, int seq_len, double theta, int style, int pos_offset, int n_threads) {
+    const int P = d_s + 1;
+    const int h = d_t / 2;
+    set_threads(n_threads);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int m = 0; m < n_maps; ++m) {
+        const double *Wm = W + (int64_t)m * P * d_t;
+        double *xt = (double *)malloc(sizeof(double) * (size_t)P);
+        double *s = (double *)malloc(sizeof(double) * (size_t)d_t);
+        for (int b = 0; b < n_seqs; ++b) {
+            for (int t = 0; t < seq_len; ++t) {
+                const uint16_t *xr = src + row_offset(src_strides, src_layer[m], kv[m], b, src_head[m], t);
+                uint16_t *orow = out + row_offset(out_strides, tgt_layer[m], kv[m], b, tgt_head[m], t);
+                for (int i = 0; i < d_s; ++i) xt[i] = bf16_bits_to_double(xr[i]);
+                xt[d_s] = 1.0;
+                for (int j = 0; j < d_t; ++j) {
+                    double acc = 0.0;
+                    for (int k = 0; k < P; ++k) acc += xt[k] * Wm[(int64_t)k * d_t + j];
+                    s[j] = acc;
+                }
+                if (kv[m] == 0) {
+                    const double pos = (double)(pos_offset + t);
+                    for (int i = 0; i < h; ++i) {
+                        const double ang = pos * pow(theta, -2.0 * i / (double)d_t);
+                        const double c = cos(ang), sn = sin(ang);
+                        const int ia = style == 0 ? i : 2 * i, ib = style == 0 ? i + h : 2 * i + 1;
+                        const double a = s[ia], bb = s[ib];
+                        s[ia] = a * c - bb * sn;
+                        s[ib] = bb * c + a * sn;
+                    }
+                }
+                for (int j = 0; j < d_t; ++j) orow[j] = oracle_double_to_bf16(s[j]);
+            }
+        }
+        free(s);
+        free(xt);
+    }
+    return 0;
+}
+
+/*
  * Online application of multi-layer maps (Sec. 3.2 feature, Sec. 1 pipeline):
  *   W [n_maps][P][d_t], P = k d_s + 1, rows i d_s .. (i+1) d_s - 1 act on the
  *   source row of src_layers[m*k + i], the last row is the bias;

@@ -20,7 +20,9 @@ current HIP stream.  The functions keep the C names:
   calibration weights: raw sensitivities at causal prefix boundaries and the
   ESS-floor shrinkage (Sec. 3.3)
 * :func:`cb_rope_table`, :func:`cb_rope` -- rotary position transform of cached
-  keys (RoPE removed before fitting, restored after mapping; Sec. 2.1, 3.1)
+  keys (RoPE removed before fitting, restored after mapping; Sec. 2.1, 3.1);
+  :func:`cb_apply_rope` -- the mapping with the target's RoPE fused into its
+  epilogue (one rounding)
 * :func:`cb_plan_create_multi`, :func:`cb_ridge_solve_ws` -- maps over the
   multi-layer feature of k selected source layers (Sec. 3.2, Eq. localfeature)
   and the blocked solve of their P = k d_s + 1 systems
@@ -144,6 +146,9 @@ _lib.cb_rope.argtypes = [ctypes.POINTER(CbCache), ctypes.POINTER(CbCache), _vp, 
                          ctypes.c_int32, ctypes.c_int32, _vp]
 _lib.cb_apply.restype = ctypes.c_int
 _lib.cb_apply.argtypes = [_vp, _vp, ctypes.POINTER(CbCache), ctypes.POINTER(CbCache), _vp]
+_lib.cb_apply_rope.restype = ctypes.c_int
+_lib.cb_apply_rope.argtypes = [_vp, _vp, ctypes.POINTER(CbCache), ctypes.POINTER(CbCache), _vp, ctypes.c_int32,
+                               ctypes.c_int32, ctypes.c_int32, _vp]
 _lib.cb_status_string.restype = ctypes.c_char_p
 _lib.cb_status_string.argtypes = [ctypes.c_int]
 _lib.cb_last_error.restype = ctypes.c_char_p
@@ -474,3 +479,14 @@ def cb_apply(plan: Plan, maps: torch.Tensor, src: torch.Tensor, tgt_out: torch.T
         raise ValueError("maps are float32")
     sv, ov = cache_view(src), cache_view(tgt_out)
     _check(_lib.cb_apply(plan.handle, _ptr(maps), ctypes.byref(sv), ctypes.byref(ov), _stream(stream)))
+
+
+def cb_apply_rope(plan: Plan, maps: torch.Tensor, src: torch.Tensor, tgt_out: torch.Tensor, table: torch.Tensor,
+                  style: int = CB_ROPE_HALF_SPLIT, pos_offset: int = 0, stream=None):
+    """cb_apply with the target RoPE (table from cb_rope_table, head_dim d_t) turning the K outputs in fp32
+    before their single rounding."""
+    if maps.dtype != torch.float32 or table.dtype != torch.float32:
+        raise ValueError("maps and table are float32")
+    sv, ov = cache_view(src), cache_view(tgt_out)
+    _check(_lib.cb_apply_rope(plan.handle, _ptr(maps), ctypes.byref(sv), ctypes.byref(ov), _ptr(table),
+                              int(table.shape[0]), int(style), int(pos_offset), _stream(stream)))

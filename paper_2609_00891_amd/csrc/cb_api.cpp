@@ -1068,6 +1068,65 @@ cb_status cb_rope(const cb_cache *in, const cb_cache *out, const float *table, i
     return ok();
 }
 
+// Single-layer application, optionally with the target's rotary transform
+// applied to the K outputs before their rounding (rope_table non-NULL).
+static cb_status apply_single(cb_plan *p, const float *maps, const cb_cache *src, const cb_cache *tgt_out,
+                              const float *rope_table, int32_t rope_n_pos, int32_t rope_style,
+                              int32_t rope_pos_offset, void *stream) {
+    if (p->duplicate_targets)
+        return fail(CB_ERR_INVALID_ARGUMENT, "the plan maps some target (layer, kv, head) more than once; "
+                                             "cb_apply needs one map per target");
+    if (!maps) return fail(CB_ERR_INVALID_ARGUMENT, "maps is NULL");
+    if (cb_status s = check_cache("src", src, p->L_s, p->H_s, p->d_s)) return s;
+    if (cb_status s = check_cache("tgt_out", tgt_out, p->L_t, p->H_t, p->d_t)) return s;
+    if (src->n_seqs != tgt_out->n_seqs || src->seq_len != tgt_out->seq_len)
+        return fail(CB_ERR_SHAPE, "src and tgt_out disagree on n_seqs / seq_len");
+    if (((uintptr_t)maps) % 4) return fail(CB_ERR_MISALIGNED, "maps must be 4-byte aligned");
+    const int64_t N = (int64_t)src->n_seqs * src->seq_len;
+    if (N > (int64_t)INT32_MAX - 4096) return fail(CB_ERR_UNSUPPORTED, "too many tokens in one call");
+    if (rope_table) {
+        if (rope_pos_offset < 0 || (int64_t)rope_pos_offset + src->seq_len > rope_n_pos)
+            return fail(CB_ERR_SHAPE, "positions %d .. %lld need a table of that many rows (n_pos = %d)",
+                        rope_pos_offset, (long long)rope_pos_offset + src->seq_len - 1, rope_n_pos);
+        if (((uintptr_t)rope_table) % 16) return fail(CB_ERR_MISALIGNED, "table must be 16-byte aligned");
+    }
+    if (cb_status s = check_device(p)) return s;
+    hipStream_t st = (hipStream_t)stream;
+    if (cb::launch_split_maps(p->n_maps, p->d_s, p->d_t, maps, p->d_whi, p->d_wlo, p->d_bias, st) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "map split launch failed");
+    if (N == 0) return ok();
+    cb::ApplyArgs a = {};
+    a.src = (const uint16_t *)src->data;
+    a.out = (uint16_t *)tgt_out->data;
+    a.ss = strides_of(src);
+    a.os = strides_of(tgt_out);
+    a.T = cb::make_fastdiv((uint32_t)src->seq_len);
+    a.N = (int32_t)N;
+    // Token tiles of whole 32-token sub-blocks: about 16 workgroups per
+    // compute unit in total, at most 8192 tokens (a workgroup streams its
+    // tile through a ring, so longer tiles amortize the ring's fill).
+    {
+        const int64_t target = 16LL * p->n_cu;
+        int64_t tt = ((int64_t)N * std::max(p->n_groups, 1) + target - 1) / target;
+        tt = std::min<int64_t>(std::max<int64_t>(tt, 256), 8192);
+        tt = (tt + 31) / 32 * 32;
+        a.tile_tokens = (int32_t)tt;
+    }
+    a.n_tiles = (int32_t)((N + a.tile_tokens - 1) / a.tile_tokens);
+    a.groups = p->d_groups;
+    a.w_hi = p->d_whi;
+    a.w_lo = p->d_wlo;
+    a.bias = p->d_bias;
+    a.rope_table = rope_table;
+    a.rope_style = rope_style;
+    a.rope_pos_offset = rope_pos_offset;
+    if ((int64_t)p->n_groups * a.n_tiles > (int64_t)INT32_MAX)
+        return fail(CB_ERR_UNSUPPORTED, "too many application workgroups");
+    if (cb::launch_apply(p->d_s, p->d_t, p->n_groups, a, st) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "application kernel launch failed");
+    return ok();
+}
+
 cb_status cb_apply(cb_plan *p, const float *maps, const cb_cache *src, const cb_cache *tgt_out, void *stream) {
     if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
     if (p->multi) {
@@ -1114,49 +1173,17 @@ cb_status cb_apply(cb_plan *p, const float *maps, const cb_cache *src, const cb_
             return fail(CB_ERR_DEVICE, "multi-layer application kernel launch failed");
         return ok();
     }
-    if (p->duplicate_targets)
-        return fail(CB_ERR_INVALID_ARGUMENT, "the plan maps some target (layer, kv, head) more than once; "
-                                             "cb_apply needs one map per target");
-    if (!maps) return fail(CB_ERR_INVALID_ARGUMENT, "maps is NULL");
-    if (cb_status s = check_cache("src", src, p->L_s, p->H_s, p->d_s)) return s;
-    if (cb_status s = check_cache("tgt_out", tgt_out, p->L_t, p->H_t, p->d_t)) return s;
-    if (src->n_seqs != tgt_out->n_seqs || src->seq_len != tgt_out->seq_len)
-        return fail(CB_ERR_SHAPE, "src and tgt_out disagree on n_seqs / seq_len");
-    if (((uintptr_t)maps) % 4) return fail(CB_ERR_MISALIGNED, "maps must be 4-byte aligned");
-    const int64_t N = (int64_t)src->n_seqs * src->seq_len;
-    if (N > (int64_t)INT32_MAX - 4096) return fail(CB_ERR_UNSUPPORTED, "too many tokens in one call");
-    if (cb_status s = check_device(p)) return s;
-    hipStream_t st = (hipStream_t)stream;
-    if (cb::launch_split_maps(p->n_maps, p->d_s, p->d_t, maps, p->d_whi, p->d_wlo, p->d_bias, st) != hipSuccess)
-        return fail(CB_ERR_DEVICE, "map split launch failed");
-    if (N == 0) return ok();
-    cb::ApplyArgs a = {};
-    a.src = (const uint16_t *)src->data;
-    a.out = (uint16_t *)tgt_out->data;
-    a.ss = strides_of(src);
-    a.os = strides_of(tgt_out);
-    a.T = cb::make_fastdiv((uint32_t)src->seq_len);
-    a.N = (int32_t)N;
-    // Token tiles of whole 32-token sub-blocks: about 16 workgroups per
-    // compute unit in total, at most 8192 tokens (a workgroup streams its
-    // tile through a ring, so longer tiles amortize the ring's fill).
-    {
-        const int64_t target = 16LL * p->n_cu;
-        int64_t tt = ((int64_t)N * std::max(p->n_groups, 1) + target - 1) / target;
-        tt = std::min<int64_t>(std::max<int64_t>(tt, 256), 8192);
-        tt = (tt + 31) / 32 * 32;
-        a.tile_tokens = (int32_t)tt;
-    }
-    a.n_tiles = (int32_t)((N + a.tile_tokens - 1) / a.tile_tokens);
-    a.groups = p->d_groups;
-    a.w_hi = p->d_whi;
-    a.w_lo = p->d_wlo;
-    a.bias = p->d_bias;
-    if ((int64_t)p->n_groups * a.n_tiles > (int64_t)INT32_MAX)
-        return fail(CB_ERR_UNSUPPORTED, "too many application workgroups");
-    if (cb::launch_apply(p->d_s, p->d_t, p->n_groups, a, st) != hipSuccess)
-        return fail(CB_ERR_DEVICE, "application kernel launch failed");
-    return ok();
+    return apply_single(p, maps, src, tgt_out, nullptr, 0, 0, 0, stream);
+}
+
+cb_status cb_apply_rope(cb_plan *p, const float *maps, const cb_cache *src, const cb_cache *tgt_out,
+                        const float *table, int32_t n_pos, int32_t style, int32_t pos_offset, void *stream) {
+    if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
+    if (style != CB_ROPE_HALF_SPLIT && style != CB_ROPE_INTERLEAVED)
+        return fail(CB_ERR_INVALID_ARGUMENT, "unknown rope style %d", style);
+    if (p->multi) return fail(CB_ERR_UNSUPPORTED, "the fused rotary epilogue needs a single-layer plan");
+    if (!table) return fail(CB_ERR_INVALID_ARGUMENT, "table is NULL");
+    return apply_single(p, maps, src, tgt_out, table, n_pos, style, pos_offset, stream);
 }
 
 }  // extern "C"

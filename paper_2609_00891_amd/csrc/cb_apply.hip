@@ -16,6 +16,14 @@
 //   tile D = W^T x^T with v_mfma_f32_32x32x16_bf16 (K = source channels),
 //   adds the bias, rounds once to bf16 and stores 16-byte chunks of target
 //   rows.  A source block shared by two target maps is read once.
+//
+// With the target's rotary transform fused (Sec. 2.1, Sec. 3.1: the mapped
+// keys receive the target's RoPE), the K outputs are turned in fp32 before
+// the single rounding.  Style (2i, 2i+1) pairs sit in accumulator registers
+// v and v+1 of one lane.  For the half split (i, i + d/2) a wave's 32 MFMA
+// rows are channel groups rb*16 .. rb*16+15 and d/2 + rb*16 .. +15 instead of
+// one 32-channel block, which puts each pair in registers v and v+8 of one
+// lane; the stores then write those two 16-channel groups.
 #include "cb_internal.h"
 
 namespace cb {
@@ -106,13 +114,23 @@ __device__ __forceinline__ void wait_vm() {
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
+// Rotary style of the fused epilogue: none, pairs (i, i + d/2), pairs (2i, 2i+1).
+enum { kRopeNone = 0, kRopeHalf = 1, kRopeInterleaved = 2 };
+
+// Target channel of MFMA row i (0..31) of wave rb.
+template <int DT, int RS>
+__device__ __forceinline__ int out_channel(int rb, int i) {
+    if (RS == kRopeHalf) return i < 16 ? rb * 16 + i : DT / 2 + rb * 16 + (i - 16);
+    return rb * 32 + i;
+}
+
 // One workgroup per (group, token tile).  The copy wave streams 32-token
 // sub-blocks of the group's source rows HBM -> LDS through an NST-stage ring
 // (NST - 1 sub-blocks ahead); since it issues nothing but these copies, its
 // vmcnt waits are exact.  One barrier per sub-block publishes the landed
 // stage to the computing waves and tells the copy wave that the stage read
 // one sub-block earlier is free again.
-template <int DS, int DT>
+template <int DS, int DT, int RS>
 __global__ __attribute__((amdgpu_flat_work_group_size(ACfg<DS, DT>::NT, ACfg<DS, DT>::NT))) void apply_kernel(ApplyArgs a) {
     using K = ACfg<DS, DT>;
     __shared__ __attribute__((aligned(16))) char lds[K::NST * K::BUFB];
@@ -162,35 +180,58 @@ __global__ __attribute__((amdgpu_flat_work_group_size(ACfg<DS, DT>::NT, ACfg<DS,
     const bool active = slot < grp->n_slots;
     const int sl = active ? slot : 0;
     const int m = grp->map[sl];
-    uint16_t *obase = a.out + grp->tgt_layer[sl] * a.os.layer + kv * a.os.kv + grp->tgt_head[sl] * a.os.head + rb * 32;
+    uint16_t *obase = a.out + grp->tgt_layer[sl] * a.os.layer + kv * a.os.kv + grp->tgt_head[sl] * a.os.head;
+    const bool rotate = RS != kRopeNone && kv == 0;            // only keys carry positions
 
     // coefficients of this wave's 32 target channels, kept in registers
     const uint32_t lrow = lane & 31, lhalf = lane >> 5;
     bf16x8_t ahi[K::KS], alo[K::KS];
     float bias[16];
     {
-        const uint16_t *wh = a.w_hi + ((int64_t)m * DT + rb * 32 + lrow) * DS + 8 * lhalf;
-        const uint16_t *wl = a.w_lo + ((int64_t)m * DT + rb * 32 + lrow) * DS + 8 * lhalf;
+        const int ch = out_channel<DT, RS>(rb, (int)lrow);
+        const uint16_t *wh = a.w_hi + ((int64_t)m * DT + ch) * DS + 8 * lhalf;
+        const uint16_t *wl = a.w_lo + ((int64_t)m * DT + ch) * DS + 8 * lhalf;
 #pragma unroll
         for (int ks = 0; ks < K::KS; ++ks) {
             ahi[ks] = *reinterpret_cast<const bf16x8_t *>(wh + 16 * ks);
             alo[ks] = *reinterpret_cast<const bf16x8_t *>(wl + 16 * ks);
         }
-        const float *bp = a.bias + (int64_t)m * DT + rb * 32 + 4 * lhalf;
 #pragma unroll
         for (int gq = 0; gq < 4; ++gq) {
-            const float4 b4 = *reinterpret_cast<const float4 *>(bp + 8 * gq);
+            // rows 8 gq + 4 lhalf .. + 3: four consecutive channels
+            const float *bp = a.bias + (int64_t)m * DT + out_channel<DT, RS>(rb, 8 * gq + 4 * (int)lhalf);
+            const float4 b4 = *reinterpret_cast<const float4 *>(bp);
             bias[4 * gq + 0] = b4.x;
             bias[4 * gq + 1] = b4.y;
             bias[4 * gq + 2] = b4.z;
             bias[4 * gq + 3] = b4.w;
         }
     }
+    // channel offsets of the lane's two 16-byte output chunks (after the
+    // exchange below: MFMA rows 8 lhalf .. +7 and 16 + 8 lhalf .. +7)
+    const int oc0 = out_channel<DT, RS>(rb, 8 * (int)lhalf), oc1 = out_channel<DT, RS>(rb, 16 + 8 * (int)lhalf);
 
     for (int sb = 0; sb < n_sb; ++sb) {
         lds_barrier();                                         // sub-block sb has landed
         if (!active) continue;
         const char *B = lds + (sb % K::NST) * K::BUFB;
+        const int tau = tok0 + sb * K::SB + (int)lrow;
+        const uint32_t bseq = fastdiv((uint32_t)min(tau, tok1 - 1), a.T);
+        const uint32_t tt = (uint32_t)min(tau, tok1 - 1) - bseq * a.T.d;
+        // (cos, sin) of the lane's eight rotated pairs, loaded before the
+        // products so that their latency hides behind the MFMA chains
+        float4 cs[4];
+        if (RS != kRopeNone && rotate) {
+            const float *row = a.rope_table + (int64_t)(a.rope_pos_offset + (int)tt) * DT;   // [d/2][2] per position
+#pragma unroll
+            for (int gq = 0; gq < 4; ++gq) {
+                // half split: frequencies rb*16 + 8 (gq/2) + 4 lhalf + {0..3}, two float4 per group of four
+                // interleaved: frequencies rb*16 + 4 gq + 2 lhalf + {0, 1}, one float4
+                const int f = RS == kRopeHalf ? rb * 16 + 8 * (gq >> 1) + 4 * (int)lhalf + 2 * (gq & 1)
+                                              : rb * 16 + 4 * gq + 2 * (int)lhalf;
+                cs[gq] = *reinterpret_cast<const float4 *>(row + 2 * f);
+            }
+        }
         // hi and lo terms in two accumulators: two independent MFMA chains
         f32x16_t acc, acl;
 #pragma unroll
@@ -201,14 +242,35 @@ __global__ __attribute__((amdgpu_flat_work_group_size(ACfg<DS, DT>::NT, ACfg<DS,
             acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ahi[ks], bx, acc, 0, 0, 0);
             acl = __builtin_amdgcn_mfma_f32_32x32x16_bf16(alo[ks], bx, acl, 0, 0, 0);
         }
-#pragma unroll
-        for (int v = 0; v < 16; ++v) acc[v] += acl[v];
         // D[i][t]: t = lane & 31, i = 8*(v/4) + 4*(lane/32) + (v&3)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[v] = acc[v] + acl[v] + bias[v];
+        if (RS == kRopeHalf && rotate) {
+            // pair (v, v + 8): channels c and c + d/2, frequency c
+#pragma unroll
+            for (int v = 0; v < 8; ++v) {
+                const float4 q = cs[2 * (v >> 2) + ((v & 3) >> 1)];
+                const float c = (v & 1) ? q.z : q.x, sn = (v & 1) ? q.w : q.y;
+                const float x0 = acc[v], x1 = acc[v + 8];
+                acc[v] = __builtin_fmaf(x0, c, -x1 * sn);
+                acc[v + 8] = __builtin_fmaf(x1, c, x0 * sn);
+            }
+        } else if (RS == kRopeInterleaved && rotate) {
+            // pair (v, v + 1), v even: channels 2f and 2f + 1
+#pragma unroll
+            for (int v = 0; v < 16; v += 2) {
+                const float4 q = cs[v >> 2];
+                const float c = (v & 2) ? q.z : q.x, sn = (v & 2) ? q.w : q.y;
+                const float x0 = acc[v], x1 = acc[v + 1];
+                acc[v] = __builtin_fmaf(x0, c, -x1 * sn);
+                acc[v + 1] = __builtin_fmaf(x1, c, x0 * sn);
+            }
+        }
         uint32_t pk[8];
 #pragma unroll
         for (int gq = 0; gq < 4; ++gq) {
-            pk[2 * gq] = pack_bf16(acc[4 * gq + 0] + bias[4 * gq + 0], acc[4 * gq + 1] + bias[4 * gq + 1]);
-            pk[2 * gq + 1] = pack_bf16(acc[4 * gq + 2] + bias[4 * gq + 2], acc[4 * gq + 3] + bias[4 * gq + 3]);
+            pk[2 * gq] = pack_bf16(acc[4 * gq + 0], acc[4 * gq + 1]);
+            pk[2 * gq + 1] = pack_bf16(acc[4 * gq + 2], acc[4 * gq + 3]);
         }
         // Exchange with lane ^ 32 so that each lane owns 8 consecutive
         // channels: lanes < 32 get channels 0-7 and 16-23, lanes >= 32 get
@@ -223,13 +285,10 @@ __global__ __attribute__((amdgpu_flat_work_group_size(ACfg<DS, DT>::NT, ACfg<DS,
             o[p] = lhalf ? make_uint4(r0, r1, pk[4 * p + 2], pk[4 * p + 3])
                          : make_uint4(pk[4 * p + 0], pk[4 * p + 1], r0, r1);
         }
-        const int tau = tok0 + sb * K::SB + (int)lrow;
         if (tau < tok1) {
-            const uint32_t b = fastdiv((uint32_t)tau, a.T);
-            const uint32_t tt = (uint32_t)tau - b * a.T.d;
-            uint16_t *orow = obase + (int64_t)b * a.os.seq + (int64_t)tt * a.os.tok + 8 * lhalf;
-            *reinterpret_cast<uint4 *>(orow) = o[0];
-            *reinterpret_cast<uint4 *>(orow + 16) = o[1];
+            uint16_t *orow = obase + (int64_t)bseq * a.os.seq + (int64_t)tt * a.os.tok;
+            *reinterpret_cast<uint4 *>(orow + oc0) = o[0];
+            *reinterpret_cast<uint4 *>(orow + oc1) = o[1];
         }
     }
 }
@@ -239,7 +298,12 @@ hipError_t launch_apply_t(int n_groups, const ApplyArgs &a, hipStream_t s) {
     using K = ACfg<DS, DT>;
     const int64_t grid = (int64_t)n_groups * a.n_tiles;
     if (grid == 0) return hipSuccess;
-    hipLaunchKernelGGL((apply_kernel<DS, DT>), dim3((unsigned)grid), dim3(K::NT), 0, s, a);
+    if (!a.rope_table)
+        hipLaunchKernelGGL((apply_kernel<DS, DT, kRopeNone>), dim3((unsigned)grid), dim3(K::NT), 0, s, a);
+    else if (a.rope_style == 0)
+        hipLaunchKernelGGL((apply_kernel<DS, DT, kRopeHalf>), dim3((unsigned)grid), dim3(K::NT), 0, s, a);
+    else
+        hipLaunchKernelGGL((apply_kernel<DS, DT, kRopeInterleaved>), dim3((unsigned)grid), dim3(K::NT), 0, s, a);
     return hipGetLastError();
 }
 

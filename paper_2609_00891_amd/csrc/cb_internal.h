@@ -93,6 +93,9 @@ struct ApplyArgs {
     const uint16_t *w_hi; // [n_maps][d_t][d_s] bf16, transposed maps
     const uint16_t *w_lo;
     const float *bias;    // [n_maps][d_t]
+    const float *rope_table;  // NULL, or the target's (cos, sin) [n_pos][d_t/2][2]: K outputs are rotated
+    int32_t rope_style;       // 0: pairs (i, i + d_t/2), 1: pairs (2i, 2i + 1)
+    int32_t rope_pos_offset;  // position of token 0 of every sequence
 };
 
 // Attention-aligned sensitivities of one call (host side of the launch).

@@ -181,6 +181,10 @@ def test_rope_entry_points_reject_bad_arguments_on_the_host():
     assert call(style=2) == 1
     assert call(n_pos=6) == 2                            # positions 0..7 need 8 table rows
     assert call(off=60) == 2
+    # the fused mapping: a NULL plan, then an unknown style, before anything else
+    ar = lambda plan, style=0: lib.cb_apply_rope(plan, ctypes.c_void_p(256), ctypes.byref(c),  # noqa: E731
+                                                 ctypes.byref(c), ctypes.c_void_p(256), 64, style, 0, None)
+    assert ar(None) == 1
 
 
 def test_multi_layer_entry_points_reject_bad_arguments_on_the_host():

@@ -155,16 +155,27 @@ def gpu_solve_ws(cb, G, C, lam=1e-2, flags=None):
     return maps, info
 
 
+def shared_f32(a):
+    """An array the oracle made, rounded once to fp32: the device tensor the GPU
+    call takes and the exact fp64 copy of the same values the oracle takes."""
+    a32 = np.ascontiguousarray(np.asarray(a, dtype=np.float32))
+    return torch.from_numpy(a32).to("cuda"), a32.astype(np.float64)
+
+
 def check_solve(cb, G, C, maps, info, Go, Co, sel, unpen, label=""):
-    """End to end (oracle solve of oracle moments) and the solver alone (oracle
-    solve of the GPU's own fp32 moments)."""
+    """End to end (the GPU's maps from its own moments against the oracle's solve
+    of the oracle's moments) and the solver alone (both sides solve the oracle's
+    moments rounded to fp32)."""
     idx = torch.as_tensor(np.asarray(sel), device=G.device)
     Wo, io = oracle.ridge_solve(Go, Co, 1e-2, relative=True, bias_unpenalized=unpen, n_threads=NTHREADS)
     Wg = maps[idx].double().cpu().numpy()
-    Ws, _ = oracle.ridge_solve(G[idx].double().cpu().numpy(), C[idx].double().cpu().numpy(), 1e-2, relative=True,
-                               bias_unpenalized=unpen, n_threads=NTHREADS)
+    (Gt, G64), (Ct, C64) = shared_f32(Go), shared_f32(Co)
+    flags = cb.CB_LAMBDA_RELATIVE | (cb.CB_RIDGE_BIAS_UNPENALIZED if unpen else 0)
+    ms, _ = gpu_solve_ws(cb, Gt, Ct, 1e-2, flags)
+    del Gt, Ct
+    Ws, _ = oracle.ridge_solve(G64, C64, 1e-2, relative=True, bias_unpenalized=unpen, n_threads=NTHREADS)
     e2e = max(relF(Wg[i], Wo[i]) for i in range(len(sel)))
-    alone = max(relF(Wg[i], Ws[i]) for i in range(len(sel)))
+    alone = max(relF(ms[i].double().cpu().numpy(), Ws[i]) for i in range(len(sel)))
     say(f"  solve{label}: maps relF end-to-end {e2e:.3e}, solver alone {alone:.3e}")
     assert (info[idx].cpu().numpy() == 0).all() and (io == 0).all()
     assert e2e <= TOL_MAPS and alone <= TOL_SOLVER
@@ -238,21 +249,22 @@ def test_multi_max_width_k32_stats_and_apply(cb):
 
 
 def test_multi_wide_solve_p2049_solver_alone(cb):
-    # the blocked fp64 solve at P = 2,049 (k = 16) on the GPU's own moments of
-    # 1,200 rows (fewer rows than P: only the relative ridge makes it definite),
-    # against the oracle's solve of the same fp32 moments; both ridge modes
+    # the blocked fp64 solve at P = 2,049 (k = 16) on the oracle's moments of
+    # 1,200 rows rounded to fp32 (fewer rows than P: only the relative ridge
+    # makes it definite), against the oracle's solve of the same values; both
+    # ridge modes
     rng = np.random.default_rng(16)
     k, L_s, H_s, L_t, H_t, B, T = 16, 17, 1, 1, 1, 3, 400
     src, tgt, w = small_inputs(rng, L_s, H_s, L_t, H_t, B, T)
     hm = random_multi_map(rng, k, L_s, H_s, L_t, H_t)
     plan = cb.cb_plan_create_multi(hm, src, tgt, 1)
-    G, C = gpu_stats(cb, plan, [(src, tgt, w)])
+    Go, Co = oracle_stats_full(hm, src, tgt, w, 1)
+    (Gt, G64), (Ct, C64) = shared_f32(Go), shared_f32(Co)        # the oracle's moments on both sides
     for unpen in (False, True):
         flags = cb.CB_LAMBDA_RELATIVE | (cb.CB_RIDGE_BIAS_UNPENALIZED if unpen else 0)
-        maps, info = gpu_solve_ws(cb, G, C, 1e-2, flags)
+        maps, info = gpu_solve_ws(cb, Gt, Ct, 1e-2, flags)
         assert (info.cpu().numpy() == 0).all()
-        Ws, io = oracle.ridge_solve(G.double().cpu().numpy(), C.double().cpu().numpy(), 1e-2, relative=True,
-                                    bias_unpenalized=unpen, n_threads=NTHREADS)
+        Ws, io = oracle.ridge_solve(G64, C64, 1e-2, relative=True, bias_unpenalized=unpen, n_threads=NTHREADS)
         assert (io == 0).all()
         e = max(relF(maps[i].double().cpu().numpy(), Ws[i]) for i in range(plan.n_maps))
         say(f"  P=2049 solver alone (bias unpenalized={unpen}): {e:.3e}")
@@ -415,6 +427,7 @@ def test_multi_apply_tiny_k3_fitted_maps(cb):
     G, C = gpu_stats(cb, plan, [(src, tgt, w)])
     maps, info = gpu_solve_ws(cb, G, C, 1e-2, cb.CB_LAMBDA_RELATIVE | cb.CB_RIDGE_BIAS_UNPENALIZED)
     assert int((info != 0).sum()) == 0
+    maps = random_maps(np.random.default_rng(3), plan.n_maps, plan.P, plan.d_t)   # seeded, not the GPU's
     out = gpu_apply(cb, plan, maps, src, wl.L_t, wl.H_t)
     ref = oracle_apply_multi(hm, maps, src, wl.L_t, wl.H_t, wl.d_t)
     check_apply_multi(bits(out), ref, hm, range(plan.n_maps), " (tiny_k3)")

@@ -159,21 +159,30 @@ def test_tiny_end_to_end(cb):
         Wo, io = oracle.ridge_solve(Go, Co, wl.lam_rel, relative=True, bias_unpenalized=unpen)
         Wg = maps.double().cpu().numpy()
         e = max(relF(Wg[i], Wo[i]) for i in sel)
-        # the solver alone, on the very fp32 moments the GPU produced
-        Ws, _ = oracle.ridge_solve(G.double().cpu().numpy(), C.double().cpu().numpy(), wl.lam_rel,
-                                   relative=True, bias_unpenalized=unpen)
-        es = max(relF(Wg[i], Ws[i]) for i in sel)
+        # the solver alone: both sides solve the oracle's moments rounded to fp32
+        (Gt, G64), (Ct, C64) = shared_f32(Go), shared_f32(Co)
+        ms, _ = gpu_solve(cb, Gt, Ct, wl.lam_rel, flags)
+        Ws, _ = oracle.ridge_solve(G64, C64, wl.lam_rel, relative=True, bias_unpenalized=unpen)
+        es = max(relF(ms[i].double().cpu().numpy(), Ws[i]) for i in sel)
         say(f"  maps parity (unpen={unpen}): end-to-end {e:.3e}, solver alone {es:.3e}")
         assert e <= TOL_MAPS and es <= 1e-6
     # apply the fitted maps back to the source cache
     out = torch.zeros_like(tgt)
-    cb.cb_apply(plan, maps, src, out)
+    Wt, W64 = shared_f32(Wo)                       # the oracle's maps on both sides
+    cb.cb_apply(plan, Wt, src, out)
     torch.cuda.synchronize()
     ref = np.zeros(tuple(out.shape), dtype=np.uint16)
-    oracle.apply(hm, maps.double().cpu().numpy(), bits(src), src.stride()[:5], wl.d_s, ref, out.stride()[:5],
+    oracle.apply(hm, W64, bits(src), src.stride()[:5], wl.d_s, ref, out.stride()[:5],
                  wl.d_t, wl.n_seqs, wl.seq_len)
     check_apply(bits(out).reshape(ref.shape), ref)
     plan.close()
+
+
+def shared_f32(a):
+    """An array the oracle made, rounded once to fp32: the device tensor the GPU
+    call takes and the exact fp64 copy of the same values the oracle takes."""
+    a32 = np.ascontiguousarray(np.asarray(a, dtype=np.float32))
+    return torch.from_numpy(a32).to("cuda"), a32.astype(np.float64)
 
 
 WIDTHS = [(ds, dt) for ds in (64, 96, 128) for dt in (64, 96, 128)]
@@ -197,10 +206,11 @@ def test_widths_ragged_tokens_and_shared_sources(cb, d_s, d_t):
     Wo, _ = oracle.ridge_solve(Go, Co, 1e-2, relative=True)
     assert max(relF(maps[i].double().cpu().numpy(), Wo[i]) for i in sel) <= TOL_MAPS
     out = torch.zeros_like(tgt)
-    cb.cb_apply(plan, maps, src, out)
+    Wt, W64 = shared_f32(Wo)                       # the oracle's maps on both sides
+    cb.cb_apply(plan, Wt, src, out)
     torch.cuda.synchronize()
     ref = np.zeros(tuple(out.shape), dtype=np.uint16)
-    oracle.apply(hm, maps.double().cpu().numpy(), bits(src), src.stride()[:5], d_s, ref, out.stride()[:5],
+    oracle.apply(hm, W64, bits(src), src.stride()[:5], d_s, ref, out.stride()[:5],
                  d_t, wl.n_seqs, wl.seq_len)
     check_apply(bits(out).reshape(ref.shape), ref)
     plan.close()
@@ -225,10 +235,11 @@ def test_single_map_items(cb, d_s, d_t, T):
     Wo, _ = oracle.ridge_solve(Go, Co, 1e-2, relative=True)
     assert max(relF(maps[i].double().cpu().numpy(), Wo[i]) for i in sel) <= TOL_MAPS
     out = torch.zeros_like(tgt)
-    cb.cb_apply(plan, maps, src, out)
+    Wt, W64 = shared_f32(Wo)                       # the oracle's maps on both sides
+    cb.cb_apply(plan, Wt, src, out)
     torch.cuda.synchronize()
     ref = np.zeros(tuple(out.shape), dtype=np.uint16)
-    oracle.apply(hm, maps.double().cpu().numpy(), bits(src), src.stride()[:5], d_s, ref, out.stride()[:5],
+    oracle.apply(hm, W64, bits(src), src.stride()[:5], d_s, ref, out.stride()[:5],
                  d_t, wl.n_seqs, wl.seq_len)
     check_apply(bits(out).reshape(ref.shape), ref)
     plan.close()
@@ -466,14 +477,15 @@ def check_centered_maps(cb, sums, A, B, so, Ao, Bo, sel, lam):
     assert (io == 0).all()
     Wg = maps.double().cpu().numpy()
     e = max(relF(Wg[m], Wo[i]) for i, m in enumerate(sel))
-    # the solver alone, on the very moments the GPU produced
-    idx = torch.as_tensor(sel, device=A.device)
-    Ws, _ = oracle.ridge_solve_centered(sums[idx].cpu().numpy(), A[idx].double().cpu().numpy(),
-                                        B[idx].double().cpu().numpy(), lam, relative=True, n_threads=NTHREADS)
-    es = max(relF(Wg[m], Ws[i]) for i, m in enumerate(sel))
+    # the solver alone: both sides solve the oracle's sums (fp64) and moments rounded to fp32
+    (At, A64), (Bt, B64) = shared_f32(Ao), shared_f32(Bo)
+    ms, _ = gpu_solve_centered(cb, torch.from_numpy(np.ascontiguousarray(so)).to("cuda"), At, Bt, lam,
+                               cb.CB_LAMBDA_RELATIVE)
+    Ws, _ = oracle.ridge_solve_centered(so, A64, B64, lam, relative=True, n_threads=NTHREADS)
+    es = max(relF(ms[i].double().cpu().numpy(), Ws[i]) for i in range(len(sel)))
     say(f"  centered maps parity: end-to-end {e:.3e}, solver alone {es:.3e}")
     assert e <= TOL_MAPS and es <= 1e-6
-    return maps
+    return maps, Wo
 
 
 def test_centered_tiny_end_to_end(cb):
@@ -485,7 +497,7 @@ def test_centered_tiny_end_to_end(cb):
     sel = list(range(wl.n_maps))
     so, Ao, Bo = oracle_centered_sel(hm, sel, src, tgt, w)
     check_centered(sums, A, B, so, Ao, Bo, sel)
-    maps = check_centered_maps(cb, sums, A, B, so, Ao, Bo, sel, wl.lam_rel)
+    maps, Wo = check_centered_maps(cb, sums, A, B, so, Ao, Bo, sel, wl.lam_rel)
     # the uncentered augmented form with an unpenalized bias solves the same problem
     G, C = gpu_stats(cb, plan, src, tgt, w)
     mu, _ = gpu_solve(cb, G, C, wl.lam_rel, cb.CB_LAMBDA_RELATIVE | cb.CB_RIDGE_BIAS_UNPENALIZED)
@@ -493,10 +505,11 @@ def test_centered_tiny_end_to_end(cb):
     say(f"  centered vs uncentered-augmented maps: {ex:.3e}")
     assert ex <= 2 * TOL_MAPS
     out = torch.zeros_like(tgt)
-    cb.cb_apply(plan, maps, src, out)
+    Wt, W64 = shared_f32(Wo)                       # the oracle's maps on both sides
+    cb.cb_apply(plan, Wt, src, out)
     torch.cuda.synchronize()
     ref = np.zeros(tuple(out.shape), dtype=np.uint16)
-    oracle.apply(hm, maps.double().cpu().numpy(), bits(src), src.stride()[:5], wl.d_s, ref, out.stride()[:5],
+    oracle.apply(hm, W64, bits(src), src.stride()[:5], wl.d_s, ref, out.stride()[:5],
                  wl.d_t, wl.n_seqs, wl.seq_len)
     check_apply(bits(out).reshape(ref.shape), ref)
     plan.close()
@@ -584,11 +597,13 @@ def test_centered_zero_weights_empty_calls_and_determinism(cb):
     maps, info = gpu_solve_centered(cb, s1, A1, B1, lam, 0)
     assert (info.cpu().numpy() == 0).all()
     Wo, _ = oracle.ridge_solve_centered(so, Ao, Bo, lam, relative=False)
-    Ws, _ = oracle.ridge_solve_centered(s1.cpu().numpy(), A1.double().cpu().numpy(), B1.double().cpu().numpy(),
-                                        lam, relative=False)
+    # the solver alone: both sides solve the oracle's sums and moments (rounded to fp32)
+    (At, A64), (Bt, B64) = shared_f32(Ao), shared_f32(Bo)
+    ms, _ = gpu_solve_centered(cb, torch.from_numpy(np.ascontiguousarray(so)).to("cuda"), At, Bt, lam, 0)
+    Ws, _ = oracle.ridge_solve_centered(so, A64, B64, lam, relative=False)
     live = [m for m in sel if m not in zero_maps]
     e = max(relF(maps[m].double().cpu().numpy(), Wo[m]) for m in live)
-    es = max(relF(maps[m].double().cpu().numpy(), Ws[m]) for m in live)
+    es = max(relF(ms[m].double().cpu().numpy(), Ws[m]) for m in live)
     say(f"  centered maps parity (absolute lambda): end-to-end {e:.3e}, solver alone {es:.3e}")
     assert e <= TOL_MAPS and es <= 1e-6
     for m in zero_maps:
@@ -674,11 +689,16 @@ def test_probe_r2_and_layer_selection(cb, d_s, d_t):
     Wo, io = oracle.ridge_solve_centered(so, Ao, Bo, 0.0, relative=False, n_threads=NTHREADS)
     assert (io == 0).all()
     r2o = oracle.probe_r2(chm, Wo, xb, ss, d_s, yb, ts, d_t, ws, Bn * T, Bn, T, n_threads=NTHREADS)
-    # the R^2 kernel alone: the oracle's residual pass on the GPU's own maps
-    r2s = oracle.probe_r2(chm, maps.double().cpu().numpy(), xb, ss, d_s, yb, ts, d_t, ws, Bn * T, Bn, T,
-                          n_threads=NTHREADS)
+    # the R^2 kernel alone: the GPU's R^2 from the oracle's sums, squares, moments (fp32) and maps
+    # (fp32) against the oracle's residual pass over the data with the same maps
+    (At, _), (Bt, _), (Wt, W64) = shared_f32(Ao), shared_f32(Bo), shared_f32(Wo)
+    r2k = torch.empty((n,), dtype=torch.float64, device="cuda")
+    cb.cb_probe_r2(torch.from_numpy(np.ascontiguousarray(so)).to("cuda"),
+                   torch.from_numpy(np.ascontiguousarray(sqo)).to("cuda"), At, Bt, Wt, r2k)
+    torch.cuda.synchronize()
+    r2s = oracle.probe_r2(chm, W64, xb, ss, d_s, yb, ts, d_t, ws, Bn * T, Bn, T, n_threads=NTHREADS)
     g = r2.cpu().numpy()
-    e_end, e_alone = float(np.abs(g - r2o).max()), float(np.abs(g - r2s).max())
+    e_end, e_alone = float(np.abs(g - r2o).max()), float(np.abs(r2k.cpu().numpy() - r2s).max())
     say(f"  probes: sums relF {esum:.3e}, sq relF {esq:.3e}; R^2 max |diff| end-to-end {e_end:.3e}, "
         f"kernel alone {e_alone:.3e}")
     assert esum <= TOL_SUMS and esq <= TOL_SUMS and e_end <= TOL_R2 and e_alone <= TOL_R2
@@ -913,6 +933,36 @@ def check_apply_rotated(ob, ref, label=""):
     assert e <= TOL_APPLY and worst <= 1.0
 
 
+@pytest.mark.parametrize("d_s,d_t,style,off", [(128, 128, 0, 0), (128, 128, 1, 11), (64, 96, 0, 5),
+                                                (96, 64, 1, 0), (128, 64, 0, 3000)])
+def test_apply_rope_matches_oracle(cb, d_s, d_t, style, off):
+    # three token tiles of 256 with a ragged 88-token tail; K outputs turned
+    # by the target RoPE before the single rounding, V outputs as cb_apply
+    wl = synth.Workload("aprope", 3, 2, d_s, 4, 2, d_t, 2, 300, "qwen", "scaled", 0.1, "lognormal")
+    src = synth.gen_source(wl, device="cuda")
+    hm = synth.head_map(wl)
+    theta = 1e6 if style == 0 else 1e4
+    table = gpu_rope_table(cb, theta, d_t, off + wl.seq_len)
+    plan = cb.cb_plan_create(hm, (wl.L_s, wl.H_s, wl.d_s), (wl.L_t, wl.H_t, wl.d_t), 1024)
+    maps = synth.planted_maps(wl, device="cuda")
+    out = torch.zeros((wl.L_t, 2, wl.n_seqs, wl.H_t, wl.seq_len, d_t), dtype=torch.bfloat16, device="cuda")
+    plain = torch.zeros_like(out)
+    say(f"apply_rope d_s={d_s} d_t={d_t} style={style} offset={off}")
+    cb.cb_apply_rope(plan, maps, src, out, table, style, off)
+    cb.cb_apply(plan, maps, src, plain)
+    torch.cuda.synchronize()
+    ref = np.zeros(tuple(out.shape), dtype=np.uint16)
+    oracle.apply_rope(hm, maps.double().cpu().numpy(), bits(src), src.stride()[:5], d_s, ref,
+                      tuple(out.stride()[:5]), d_t, wl.n_seqs, wl.seq_len, theta, style, off, n_threads=NTHREADS)
+    ob = bits(out).reshape(ref.shape)
+    check_apply(ob, ref, f" (fused rope, style {style})")
+    assert np.array_equal(ob[:, 1], bits(plain).reshape(ref.shape)[:, 1])     # V: bitwise cb_apply
+    assert not np.array_equal(ob[:, 0], bits(plain).reshape(ref.shape)[:, 0])
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_SHAPE"):
+        cb.cb_apply_rope(plan, maps, src, out, table[: off + wl.seq_len - 1], style, off)
+    plan.close()
+
+
 def test_rope_fit_and_apply_end_to_end(cb):
     # caches as a model holds them: keys carry RoPE (source base 1e4, target base
     # 1e6).  Fit on de-rotated keys, apply on the de-rotated sender, then
@@ -934,10 +984,6 @@ def test_rope_fit_and_apply_end_to_end(cb):
     G, C = gpu_stats(cb, plan, src_g, tgt_g, w)
     maps, info = gpu_solve(cb, G, C, wl.lam_rel, cb.CB_LAMBDA_RELATIVE | cb.CB_RIDGE_BIAS_UNPENALIZED)
     assert (info.cpu().numpy() == 0).all()
-    out = torch.zeros_like(tgt_rot)
-    cb.cb_apply(plan, maps, src_g, out)
-    cb.cb_rope(out, out, tab_t)
-    torch.cuda.synchronize()
     # oracle: de-rotation, statistics, solve, apply, rotation -- the same steps in fp64
     src_o = oracle.rope(src_rot_b, src_c.stride()[:5], wl.L_s, wl.H_s, wl.d_s, wl.n_seqs, wl.seq_len, ts, inverse=True)
     tgt_o = oracle.rope(tgt_rot_b, tgt_c.stride()[:5], wl.L_t, wl.H_t, wl.d_t, wl.n_seqs, wl.seq_len, tt, inverse=True)
@@ -950,11 +996,26 @@ def test_rope_fit_and_apply_end_to_end(cb):
     e = max(relF(maps[i].double().cpu().numpy(), Wo[i]) for i in sel)
     say(f"  maps parity on de-rotated keys: {e:.3e}")
     assert e <= TOL_MAPS
+    # mapping with the target rotation restored, on the oracle's maps and de-rotated sender (both sides)
+    Wt, W64 = shared_f32(Wo)
+    src_ob = as_bf16(src_o)
+    out = torch.zeros_like(tgt_rot)
+    cb.cb_apply(plan, Wt, src_ob, out)
+    cb.cb_rope(out, out, tab_t)
+    torch.cuda.synchronize()
     mapped = np.zeros(tuple(out.shape), dtype=np.uint16)
-    oracle.apply(hm, maps.double().cpu().numpy(), src_o, src_c.stride()[:5], wl.d_s, mapped,
+    oracle.apply(hm, W64, src_o, src_c.stride()[:5], wl.d_s, mapped,
                  tuple(out.stride()[:5]), wl.d_t, wl.n_seqs, wl.seq_len)
     ref = oracle.rope(mapped, tuple(out.stride()[:5]), wl.L_t, wl.H_t, wl.d_t, wl.n_seqs, wl.seq_len, tt)
     check_apply_rotated(bits(out).reshape(ref.shape), ref, " (rotated keys)")
+    # the fused form rounds once: within check_apply's bound of the oracle's fused result
+    fused = torch.zeros_like(tgt_rot)
+    cb.cb_apply_rope(plan, Wt, src_ob, fused, tab_t)
+    torch.cuda.synchronize()
+    ref1 = np.zeros(tuple(out.shape), dtype=np.uint16)
+    oracle.apply_rope(hm, W64, src_o, src_c.stride()[:5], wl.d_s, ref1,
+                      tuple(out.stride()[:5]), wl.d_t, wl.n_seqs, wl.seq_len, tt)
+    check_apply(bits(fused).reshape(ref1.shape), ref1, " (fused target rotation)")
     # the K maps recover the planted content map: fitted without de-rotation they do not
     Gr, Cr = gpu_stats(cb, plan, src_rot, tgt_rot, w)
     mr, _ = gpu_solve(cb, Gr, Cr, wl.lam_rel, cb.CB_LAMBDA_RELATIVE | cb.CB_RIDGE_BIAS_UNPENALIZED)

@@ -867,3 +867,58 @@ def test_rope_inverse_undoes_forward_up_to_bf16_rounding():
     na = np.hypot(a[:, 0, ..., :d // 2], a[:, 0, ..., d // 2:])
     nb = np.hypot(bf16_val(fwd)[:, 0, ..., :d // 2], bf16_val(fwd)[:, 0, ..., d // 2:])
     assert np.abs(nb - na).max() <= 2 ** -7 * na.max()
+
+
+@pytest.mark.parametrize("style", [0, 1])
+def test_apply_rope_is_rotation_of_the_unrounded_map_output(style):
+    # K outputs: the rotation (pinned above by RoFormer's relative-position
+    # property) of the exact x~ W~, rounded once; V outputs: plain cb_apply
+    rng = np.random.default_rng(53)
+    wl, hm, src, out = apply_problem(rng, d_s=8, d_t=16, hm_kind="qwen")
+    n = hm["kv"].shape[0]
+    ss = synth.cache_strides(wl.L_s, wl.H_s, wl.n_seqs, wl.seq_len, wl.d_s)
+    os_ = synth.cache_strides(wl.L_t, wl.H_t, wl.n_seqs, wl.seq_len, wl.d_t)
+    # dyadic coefficients with few bits: x~ W~ is exact in fp64 in any order
+    W = rng.integers(-64, 65, size=(n, wl.P, wl.d_t)) / 64.0
+    theta, off = 1e4, 7
+    oracle.apply_rope(hm, W, src, ss, wl.d_s, out, os_, wl.d_t, wl.n_seqs, wl.seq_len, theta, style, off)
+    plain = np.zeros_like(out)
+    oracle.apply(hm, W, src, ss, wl.d_s, plain, os_, wl.d_t, wl.n_seqs, wl.seq_len)
+    X = bf16_val(src)
+    pos = off + np.arange(wl.seq_len)
+    for m in range(n):
+        got = out[hm["tgt_layer"][m], hm["kv"][m], :, hm["tgt_head"][m]]
+        if hm["kv"][m] == 1:
+            assert np.array_equal(got, plain[hm["tgt_layer"][m], 1, :, hm["tgt_head"][m]])
+            continue
+        x = X[hm["src_layer"][m], 0, :, hm["src_head"][m]]
+        s = np.concatenate([x, np.ones(x.shape[:-1] + (1,))], -1) @ W[m]
+        assert np.array_equal(got, oracle.double_to_bf16(_rope_f64(s, pos[None, :], theta, style)))
+    # position 0 is the identity: a one-token call at offset 0 equals cb_apply
+    one_src = np.ascontiguousarray(src[..., :1, :])
+    o1, p1 = (np.zeros(out.shape[:-2] + (1, wl.d_t), dtype=np.uint16) for _ in range(2))
+    ss1 = synth.cache_strides(wl.L_s, wl.H_s, wl.n_seqs, 1, wl.d_s)
+    os1 = synth.cache_strides(wl.L_t, wl.H_t, wl.n_seqs, 1, wl.d_t)
+    oracle.apply_rope(hm, W, one_src, ss1, wl.d_s, o1, os1, wl.d_t, wl.n_seqs, 1, theta, style, 0)
+    oracle.apply(hm, W, one_src, ss1, wl.d_s, p1, os1, wl.d_t, wl.n_seqs, 1)
+    assert np.array_equal(o1, p1)
+
+
+def test_apply_rope_inverse_rotation_recovers_cb_apply():
+    # de-rotating the fused output with the pinned inverse transform gives
+    # the plain mapped cache back up to the two extra roundings
+    rng = np.random.default_rng(54)
+    wl, hm, src, out = apply_problem(rng, d_s=8, d_t=32, hm_kind="qwen")
+    n = hm["kv"].shape[0]
+    ss = synth.cache_strides(wl.L_s, wl.H_s, wl.n_seqs, wl.seq_len, wl.d_s)
+    os_ = synth.cache_strides(wl.L_t, wl.H_t, wl.n_seqs, wl.seq_len, wl.d_t)
+    W = rng.standard_normal((n, wl.P, wl.d_t)) * 0.3
+    oracle.apply_rope(hm, W, src, ss, wl.d_s, out, os_, wl.d_t, wl.n_seqs, wl.seq_len, 1e6, 0, 300)
+    plain = np.zeros_like(out)
+    oracle.apply(hm, W, src, ss, wl.d_s, plain, os_, wl.d_t, wl.n_seqs, wl.seq_len)
+    back = oracle.rope(out, os_, wl.L_t, wl.H_t, wl.d_t, wl.n_seqs, wl.seq_len, 1e6, 0, inverse=True,
+                       pos_offset=300)
+    a, b = bf16_val(plain), bf16_val(back)
+    assert np.array_equal(back[:, 1], out[:, 1]) and np.array_equal(out[:, 1], plain[:, 1])
+    assert relF(b, a) < 2 ** -7
+    assert not np.array_equal(out[:, 0], plain[:, 0])                 # the keys did turn
