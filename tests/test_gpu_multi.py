@@ -504,3 +504,20 @@ def test_multi_apply_qwen_k8_batch_sampled(cb):
         ob = bits(out[:, :, b:b + 1, :, t0:t1].contiguous())
         check_apply_multi(ob, ref, hs, range(len(sel)), f" (seq {b}, tokens {t0}..{t1})")
     plan.close()
+
+
+def test_multi_plan_rejects_fused_rotary_apply(cb):
+    # the fused target rotation is a single-layer epilogue: a multi-layer plan
+    # is refused before anything is enqueued, and the output is untouched
+    rng = np.random.default_rng(41)
+    src, tgt, _ = small_inputs(rng, 4, 1, 1, 1, 1, 32)
+    hm = random_multi_map(rng, 2, 4, 1, 1, 1)
+    plan = cb.cb_plan_create_multi(hm, src, tgt, 1)
+    maps = random_maps(rng, plan.n_maps, plan.P, plan.d_t)
+    table = torch.zeros((32, 64, 2), dtype=torch.float32, device="cuda")
+    out = torch.zeros_like(tgt)
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_UNSUPPORTED"):
+        cb.cb_apply_rope(plan, maps, src, out, table)
+    torch.cuda.synchronize()
+    assert not out.view(torch.int16).any()
+    plan.close()

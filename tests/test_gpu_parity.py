@@ -963,6 +963,33 @@ def test_apply_rope_matches_oracle(cb, d_s, d_t, style, off):
     plan.close()
 
 
+def test_apply_rope_edge_cases(cb):
+    # an empty sender changes nothing; one token at position 0 equals cb_apply;
+    # an unknown style is rejected before anything is enqueued
+    wl = synth.Workload("aprope1", 2, 2, 64, 2, 2, 64, 3, 1, "qwen", "scaled", 0.1, "lognormal")
+    src = synth.gen_source(wl, device="cuda")
+    hm = synth.head_map(wl)
+    plan = cb.cb_plan_create(hm, (wl.L_s, wl.H_s, wl.d_s), (wl.L_t, wl.H_t, wl.d_t), 1024)
+    maps = synth.planted_maps(wl, device="cuda")
+    table = gpu_rope_table(cb, 1e4, wl.d_t, 4)
+    out = torch.full((wl.L_t, 2, wl.n_seqs, wl.H_t, 1, wl.d_t), 7.0, dtype=torch.bfloat16, device="cuda")
+    keep = out.clone()
+    cb.cb_apply_rope(plan, maps, src[:, :, :0], out[:, :, :0], table)
+    torch.cuda.synchronize()
+    assert torch.equal(out, keep)
+    plain = torch.zeros_like(out)
+    for style in (0, 1):
+        cb.cb_apply_rope(plan, maps, src, out, table, style, 0)
+        cb.cb_apply(plan, maps, src, plain)
+        torch.cuda.synchronize()
+        assert torch.equal(out, plain)
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_INVALID_ARGUMENT"):
+        cb.cb_apply_rope(plan, maps, src, out, table, 2, 0)
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_SHAPE"):
+        cb.cb_apply_rope(plan, maps, src, out, table, 0, 4)             # position 4 needs 5 rows
+    plan.close()
+
+
 def test_rope_fit_and_apply_end_to_end(cb):
     # caches as a model holds them: keys carry RoPE (source base 1e4, target base
     # 1e6).  Fit on de-rotated keys, apply on the de-rotated sender, then
