@@ -442,7 +442,8 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); "
-              "the path is single-GPU by design (see DESIGN.md, 'Sharding').", file=sys.stderr)
+              "the path runs on one GPU: the maps are independent, so several GPUs would each take a "
+              "share of the maps (or of the calibration sequences, adding their G and C).", file=sys.stderr)
         sys.exit(2)
 
     if args.hbm_copy_probe:
