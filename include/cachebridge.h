@@ -141,9 +141,10 @@ typedef struct cb_plan cb_plan;
 #define CB_RIDGE_BIAS_UNPENALIZED 2u /* no ridge on the bias row: Eq. closedform    */
 
 /*
- * Compile the head map into a static gather schedule (Sec. 2.3: the support
- * is fixed before fitting and can be compiled into a static gather schedule)
- * and allocate the plan's workspace on the current device.
+ * Turn the head map into the fixed list of work items the statistics kernel
+ * walks (Sec. 2.3: the support of every map is known before any fitting, so
+ * the reads can be planned once) and allocate the plan's workspace on the
+ * current device.
  *   src_geom / tgt_geom: only n_layers, n_heads and head_dim are read.
  *   max_tokens_per_call: upper bound on n_seqs * seq_len of any later
  *     cb_stats_accumulate call (sizes the per-workgroup partial sums).

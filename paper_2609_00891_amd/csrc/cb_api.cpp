@@ -1,11 +1,10 @@
 // cb_api.cpp -- host side of the C ABI declared in include/cachebridge.h.
 //
 // Validation happens here, before anything is enqueued.  cb_plan_create turns
-// the head map into the static gather schedule of the statistics kernel
-// (CacheBridge Sec. 2.3: the support is fixed before fitting and is compiled
-// into a static gather schedule) and into the source-block groups of the
-// application kernel, and allocates the plan's workspace.  No other call
-// allocates.
+// the head map into the work items of the statistics kernel (CacheBridge
+// Sec. 2.3: every map's support is known before fitting, so its reads are
+// planned once) and into the source-block groups of the application kernel,
+// and allocates the plan's workspace.  No other call allocates.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>

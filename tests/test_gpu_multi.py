@@ -374,14 +374,16 @@ def gpu_apply(cb, plan, maps, src, L_t, H_t, out=None):
 
 
 def oracle_apply_multi(hm, maps, src, L_t, H_t, d_t, sel=None):
-    """Oracle application of the maps `sel` (all by default) with the fp32 maps the
-    GPU used, on a host copy of the sender cache."""
+    """Oracle application of the maps `sel` (all by default) on a host copy of the
+    sender cache; `maps` is the device tensor the GPU used or an fp64 array."""
+    if isinstance(maps, torch.Tensor):
+        maps = maps.double().cpu().numpy()
     if sel is not None:
         hm = {f: v[sel] for f, v in hm.items()}
-        maps = maps[torch.as_tensor(sel, device=maps.device)]
+        maps = maps[np.asarray(sel)]
     L_s, _, B, H_s, T, d_s = src.shape
     ref = np.zeros((L_t, 2, B, H_t, T, d_t), dtype=np.uint16)
-    oracle.apply_multi(hm, maps.double().cpu().numpy(), bits(src), synth.cache_strides(L_s, H_s, B, T, d_s), d_s,
+    oracle.apply_multi(hm, np.ascontiguousarray(maps, dtype=np.float64), bits(src), synth.cache_strides(L_s, H_s, B, T, d_s), d_s,
                        ref, synth.cache_strides(L_t, H_t, B, T, d_t), d_t, B, T, n_threads=NTHREADS)
     return ref
 
@@ -416,21 +418,39 @@ def random_maps(rng, n, P, d_t):
 
 
 def test_multi_apply_tiny_k3_fitted_maps(cb):
-    # the maps fitted on tiny_k3 applied to the same sender: 4 x 520 tokens
-    # (eight full 256-token tiles and a 32-token tail)
+    # Maps fitted on tiny_k3 applied to the same sender: 4 x 520 tokens (eight
+    # full 256-token tiles and a 32-token tail).  Two checks:
+    #  * the apply alone: the oracle's fitted maps, rounded once to fp32, on both
+    #    sides (per-element bar);
+    #  * the whole chain: the GPU's statistics -> solve -> apply against the
+    #    oracle's statistics -> solve -> apply (relative Frobenius bar).
     wl = synth.WORKLOADS["tiny_k3"]
     src = synth.gen_source(wl, device="cuda")
     tgt = synth.gen_target(wl, src, device="cuda")
     w = synth.gen_weights(wl, device="cuda")
     hm = synth.head_map_multi(wl)
     plan = cb.cb_plan_create_multi(hm, src, tgt, wl.sample_stride)
+    flags = cb.CB_LAMBDA_RELATIVE | cb.CB_RIDGE_BIAS_UNPENALIZED
     G, C = gpu_stats(cb, plan, [(src, tgt, w)])
-    maps, info = gpu_solve_ws(cb, G, C, 1e-2, cb.CB_LAMBDA_RELATIVE | cb.CB_RIDGE_BIAS_UNPENALIZED)
+    maps_gpu, info = gpu_solve_ws(cb, G, C, 1e-2, flags)
     assert int((info != 0).sum()) == 0
-    maps = random_maps(np.random.default_rng(3), plan.n_maps, plan.P, plan.d_t)   # seeded, not the GPU's
-    out = gpu_apply(cb, plan, maps, src, wl.L_t, wl.H_t)
-    ref = oracle_apply_multi(hm, maps, src, wl.L_t, wl.H_t, wl.d_t)
-    check_apply_multi(bits(out), ref, hm, range(plan.n_maps), " (tiny_k3)")
+    Go, Co = oracle_stats_full(hm, src, tgt, w, wl.sample_stride)
+    Wo, io = oracle.ridge_solve(Go, Co, 1e-2, relative=True, bias_unpenalized=True, n_threads=NTHREADS)
+    assert (io == 0).all()
+    maps_t, maps64 = shared_f32(Wo)
+    out = gpu_apply(cb, plan, maps_t, src, wl.L_t, wl.H_t)
+    ref = oracle_apply_multi(hm, maps64, src, wl.L_t, wl.H_t, wl.d_t)
+    check_apply_multi(bits(out), ref, hm, range(plan.n_maps), " (tiny_k3, oracle's fitted maps)")
+    # chained: the GPU's own fitted maps against the oracle's unrounded fp64 maps
+    out2 = gpu_apply(cb, plan, maps_gpu, src, wl.L_t, wl.H_t)
+    ref2 = oracle_apply_multi(hm, Wo, src, wl.L_t, wl.H_t, wl.d_t)
+    ob2 = bits(out2)
+    worst = 0.0
+    for m in range(plan.n_maps):
+        l, z, h = int(hm["tgt_layer"][m]), int(hm["kv"][m]), int(hm["tgt_head"][m])
+        worst = max(worst, relF(oracle.bf16_to_double(ob2[l, z, :, h]), oracle.bf16_to_double(ref2[l, z, :, h])))
+    say(f"  chained statistics -> solve -> apply (tiny_k3): worst per-map relF {worst:.3e}")
+    assert worst <= TOL_APPLY
     plan.close()
 
 
