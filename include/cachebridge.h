@@ -478,6 +478,28 @@ cb_status cb_ridge_solve_ws(int32_t n_maps, int32_t P, int32_t d_t, const float 
 /* Workspace bytes cb_ridge_solve_ws needs to solve n_systems systems at once (0 for P <= 129). */
 int64_t cb_ridge_solve_workspace_bytes(int32_t P, int32_t d_t, int32_t n_systems);
 
+/*
+ * Allocation-free wide ridge solve, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the solve of cb_ridge_solve_ws -- same arguments minus
+ * the workspace, same arithmetic, identical results -- with the factors in a
+ * fixed device array of cb_ridge_solve_noalloc_max_bytes() bytes (128 MiB)
+ * that every GPU the library runs on holds until the process ends.  The
+ * systems are solved in batches of that size divided by
+ * cb_ridge_solve_workspace_bytes(P, d_t, 1).  No call allocates; the first call
+ * on a device looks up the array's address there (make it before a graph
+ * capture).  The array keeps the last call's contents; calls that overlap on
+ * one GPU (several streams or threads) race on it and must be serialized.
+ * P <= 129 runs cb_ridge_solve (no scratch).  Errors as cb_ridge_solve_ws, and
+ * CB_ERR_UNSUPPORTED when one system needs more than the array holds
+ * ((P^2 + P d_t) * 8 bytes: P > 4032 at d_t = 128).
+ */
+cb_status cb_ridge_solve_noalloc(int32_t n_maps, int32_t P, int32_t d_t, const float *G, const float *C,
+                                 float lambda, uint32_t flags, float *maps, int32_t *info, void *stream);
+
+/* Bytes of the fixed device array of cb_ridge_solve_noalloc. */
+int64_t cb_ridge_solve_noalloc_max_bytes(void);
+
 /* Feature width P of a plan's maps (d_s + 1, or k d_s + 1) and its k. */
 cb_status cb_plan_feature_width(const cb_plan *plan, int32_t *P, int32_t *k);
 

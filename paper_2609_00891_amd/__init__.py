@@ -115,6 +115,11 @@ _lib.cb_ridge_solve.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, 
 _lib.cb_ridge_solve_ws.restype = ctypes.c_int
 _lib.cb_ridge_solve_ws.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp, _vp, ctypes.c_float,
                                    ctypes.c_uint32, _vp, ctypes.c_int64, _vp, _vp, _vp]
+_lib.cb_ridge_solve_noalloc.restype = ctypes.c_int
+_lib.cb_ridge_solve_noalloc.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp, _vp, ctypes.c_float,
+                                        ctypes.c_uint32, _vp, _vp, _vp]
+_lib.cb_ridge_solve_noalloc_max_bytes.restype = ctypes.c_int64
+_lib.cb_ridge_solve_noalloc_max_bytes.argtypes = []
 _lib.cb_ridge_solve_workspace_bytes.restype = ctypes.c_int64
 _lib.cb_ridge_solve_workspace_bytes.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]
 _lib.cb_stats_zero_centered.restype = ctypes.c_int
@@ -331,6 +336,23 @@ def cb_ridge_solve_ws(G: torch.Tensor, C: torch.Tensor, lam: float, flags: int, 
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(_lib.cb_ridge_solve_ws(n, P, C.shape[2], _ptr(G), _ptr(C), float(lam), int(flags), _ptr(workspace),
                                   int(ws_bytes), _ptr(maps), _ptr(info), _stream(stream)))
+
+
+def cb_ridge_solve_noalloc(G: torch.Tensor, C: torch.Tensor, lam: float, flags: int, maps: torch.Tensor,
+                           info: torch.Tensor, stream=None):
+    """cb_ridge_solve_ws without a workspace: the library's fixed device scratch array
+    (cb_ridge_solve_noalloc_max_bytes()) holds the factors; nothing is allocated."""
+    n, P, P2 = G.shape
+    if P != P2 or C.shape[:2] != (n, P) or maps.shape != C.shape or info.shape != (n,):
+        raise ValueError("G [n][P][P], C/maps [n][P][d_t], info [n]")
+    if info.dtype != torch.int32:
+        raise ValueError("info is int32")
+    _check(_lib.cb_ridge_solve_noalloc(n, P, C.shape[2], _ptr(G), _ptr(C), float(lam), int(flags), _ptr(maps),
+                                       _ptr(info), _stream(stream)))
+
+
+def cb_ridge_solve_noalloc_max_bytes() -> int:
+    return int(_lib.cb_ridge_solve_noalloc_max_bytes())
 
 
 def _row_stride(weights: torch.Tensor, w_row_stride: Optional[int]) -> int:

@@ -871,6 +871,33 @@ cb_status cb_ridge_solve_ws(int32_t n_maps, int32_t P, int32_t d_t, const float 
     return ok();
 }
 
+cb_status cb_ridge_solve_noalloc(int32_t n_maps, int32_t P, int32_t d_t, const float *G, const float *C, float lambda,
+                                 uint32_t flags, float *maps, int32_t *info, void *stream) {
+    if (P <= 129) return cb_ridge_solve(n_maps, P, d_t, G, C, lambda, flags, maps, info, stream);
+    if (n_maps < 0) return fail(CB_ERR_INVALID_ARGUMENT, "n_maps is negative");
+    if (P > 4097 || !supported_width(d_t))
+        return fail(CB_ERR_UNSUPPORTED, "need P <= 4097 and d_t in {64, 96, 128} (got P=%d, d_t=%d)", P, d_t);
+    const int64_t need = cb::solve_blocked_bytes_per_system(P, d_t);
+    if (need > cb::kStaticSolveScratchBytes)
+        return fail(CB_ERR_UNSUPPORTED,
+                    "one system of P=%d, d_t=%d needs %lld bytes of scratch; the allocation-free solve holds %lld "
+                    "(use cb_ridge_solve_ws)",
+                    P, d_t, (long long)need, (long long)cb::kStaticSolveScratchBytes);
+    if (flags & ~(uint32_t)(CB_LAMBDA_RELATIVE | CB_RIDGE_BIAS_UNPENALIZED))
+        return fail(CB_ERR_INVALID_ARGUMENT, "unknown flag bits 0x%x", flags);
+    if (!std::isfinite(lambda) || lambda < 0.f) return fail(CB_ERR_INVALID_ARGUMENT, "lambda must be finite and >= 0");
+    if (n_maps == 0) return ok();
+    if (!G || !C || !maps || !info) return fail(CB_ERR_INVALID_ARGUMENT, "G, C, maps and info must be non-NULL");
+    if (((uintptr_t)G) % 4 || ((uintptr_t)C) % 4 || ((uintptr_t)maps) % 4 || ((uintptr_t)info) % 4)
+        return fail(CB_ERR_MISALIGNED, "G, C, maps and info must be 4-byte aligned");
+    if (cb::launch_solve_blocked_static(n_maps, P, d_t, G, C, lambda, flags, maps, info, (hipStream_t)stream) !=
+        hipSuccess)
+        return fail(CB_ERR_DEVICE, "allocation-free blocked ridge solve failed (scratch lookup or launch)");
+    return ok();
+}
+
+int64_t cb_ridge_solve_noalloc_max_bytes(void) { return cb::kStaticSolveScratchBytes; }
+
 cb_status cb_ridge_solve_centered(int32_t n_maps, int32_t d_s, int32_t d_t, const double *sums, const float *A,
                                   const float *B, float lambda, uint32_t flags, float *maps, int32_t *info,
                                   void *stream) {

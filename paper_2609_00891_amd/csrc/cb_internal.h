@@ -206,6 +206,10 @@ hipError_t launch_solve_blocked(int32_t n_maps, int32_t P, int32_t d_t, const fl
                                 hipStream_t s);
 constexpr int kMultiTileRows = 16;      // calibration rows per multi-layer tile
 constexpr int kMultiFlushTiles = 2046;  // at most 32,736 rows summed in fp32 before a flush (a multiple of 6)
+// Size of the fixed device array of the allocation-free blocked solve.
+constexpr int64_t kStaticSolveScratchBytes = 128ll << 20;
+hipError_t launch_solve_blocked_static(int32_t n_maps, int32_t P, int32_t d_t, const float *G, const float *C,
+                                       float lambda, uint32_t flags, float *maps, int32_t *info, hipStream_t s);
 hipError_t launch_solve(int32_t n_maps, int32_t P, int32_t d_t, const float *G, const float *C,
                         float lambda, uint32_t flags, float *maps, int32_t *info, hipStream_t s);
 hipError_t launch_split_maps(int32_t n_maps, int32_t d_s, int32_t d_t, const float *maps,

@@ -28,6 +28,7 @@
 // diagonal blocks in the upper halves of the diagonal blocks) and Z (P x d_t
 // fp64).  Systems are solved in batches that fit the workspace.
 #include <algorithm>
+#include <mutex>
 #include <type_traits>
 
 #include "cb_internal.h"
@@ -428,6 +429,45 @@ hipError_t launch_solve_blocked(int32_t n_maps, int32_t P, int32_t d_t, const fl
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
+}
+
+// Allocation-free variant: the factors live in `scratch`, a fixed device array
+// that the code object carries (every GPU the library runs on holds its own
+// copy until the process ends).  Its device address is looked up once per
+// device, with that device current, on the first call there; host code never
+// passes the array's name itself to a kernel (on the host it only names the
+// variable).  Calls that overlap on one GPU share the array and race.
+static __device__ __align__(256) double scratch[kStaticSolveScratchBytes / sizeof(double)];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t static_solve_scratch(void **out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
+}
+
+hipError_t launch_solve_blocked_static(int32_t n_maps, int32_t P, int32_t d_t, const float *G, const float *C,
+                                       float lambda, uint32_t flags, float *maps, int32_t *info, hipStream_t s) {
+    void *ws = nullptr;
+    const hipError_t e = static_solve_scratch(&ws);
+    if (e != hipSuccess) return e;
+    return launch_solve_blocked(n_maps, P, d_t, G, C, lambda, flags, ws, kStaticSolveScratchBytes, maps, info, s);
 }
 
 }  // namespace cb

@@ -220,3 +220,23 @@ def test_multi_layer_entry_points_reject_bad_arguments_on_the_host():
     assert per == (1025 * 1025 + 1025 * 128) * 8
     assert cb.cb_ridge_solve_workspace_bytes(1025, 128, 3) == 3 * per
     assert cb.cb_ridge_solve_workspace_bytes(129, 128, 3) == 0
+
+
+def test_noalloc_solve_rejects_systems_beyond_its_scratch_before_any_launch():
+    # The allocation-free solve factors in a fixed device array; a system whose
+    # factor would not fit is refused on the host (no device is touched here).
+    import paper_2609_00891_amd as cb
+    lib = cb.library()
+    cap = int(lib.cb_ridge_solve_noalloc_max_bytes())
+    assert cap == 128 << 20
+    fake = ctypes.c_void_p(0x1000)
+    for P, d_t, ok in ((4032, 128, True), (4033, 128, False), (4097, 64, False)):
+        need = int(lib.cb_ridge_solve_workspace_bytes(P, d_t, 1))
+        assert (need <= cap) == ok
+    rc = lib.cb_ridge_solve_noalloc(1, 4033, 128, fake, fake, ctypes.c_float(1e-2), 1, fake, fake, None)
+    assert cb.cb_status_string(rc) == "CB_ERR_UNSUPPORTED"
+    assert b"scratch" in lib.cb_last_error()
+    rc = lib.cb_ridge_solve_noalloc(1, 4098, 128, fake, fake, ctypes.c_float(1e-2), 1, fake, fake, None)
+    assert cb.cb_status_string(rc) == "CB_ERR_UNSUPPORTED"
+    rc = lib.cb_ridge_solve_noalloc(1, 1025, 128, None, fake, ctypes.c_float(1e-2), 1, fake, fake, None)
+    assert cb.cb_status_string(rc) == "CB_ERR_INVALID_ARGUMENT"
