@@ -834,6 +834,30 @@ def test_attn_weights_small(cb, d, G, stride):
     assert not rg[:, (wl.seq_len - 1)::wl.seq_len].any()      # the last token is in no prefix
 
 
+@pytest.mark.parametrize("d,G,bounds,T,stride", [
+    (128, 4, [0, 5, 31, 32, 33, 100, 640, 1999, 2999], 3000, 3),     # a partial row tile; boundary 0
+    (64, 32, [7, 40, 90, 150, 260, 400, 555, 699], 700, 1),          # eight tiles of one boundary each
+    (128, 1, "geom", 4096, 4),                                       # two tiles, 64 boundaries, long keys
+    (128, 16, [511, 512, 513, 1023], 1024, 2),                        # two equal-length tiles
+])
+def test_attn_weights_work_splits(cb, d, G, bounds, T, stride):
+    # boundary sets that drive the key split differently (short-tile pass,
+    # tiles split over several waves, merges of partial sums)
+    wl = synth.Workload("attns", 2, 1, d, 2, 1, d, 2, T, "qwen", "scaled", 0.1, "lognormal")
+    src, tgt, _ = make_inputs(wl)
+    del src
+    if bounds == "geom":
+        bounds = np.unique(np.rint(np.geomspace(1, T - 1, 64)).astype(np.int32))
+        bounds = np.concatenate([bounds, np.arange(T - 1 - (64 - len(bounds)), T - 1)])
+        bounds = np.unique(bounds)[:64]
+    bounds = np.asarray(bounds, dtype=np.int32)
+    q = synth.gen_queries(wl, tgt, G * wl.H_t, len(bounds), device="cuda")
+    say(f"attn split: d={d} G={G} {len(bounds)} boundaries up to {int(bounds[-1])}, T={T}, stride {stride}")
+    rg, wg, ag = gpu_attn(cb, tgt, q, bounds, stride, p=d)
+    ro, wo, ao = oracle_attn(tgt, q, bounds, stride, p=d)
+    check_attn(rg, wg, ag, ro, wo, ao)
+
+
 def test_attn_weights_paper_configuration(cb):
     # Sec. 4.1: 1,024-token sequences, 32 boundaries from 12 to 1,023, every
     # fourth token; eight query heads per KV head (64 / 8), d = 128
