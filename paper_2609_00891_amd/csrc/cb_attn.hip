@@ -201,8 +201,8 @@ void attn_sens_kernel(AttnArgs a) {
         const char *row = lds + st * STAGE + slot * SLOTB + TB + key * D * 2;
         float s2 = 0.f;
 #pragma unroll
-        for (int cc = 0; cc < NCH / 4; ++cc) {
-            const uint4 v = *(const uint4 *)(row + (pq * (NCH / 4) + cc) * 16);
+        for (int cc = 0; cc < NCH / 4; ++cc) {                // chunks rotated by key: no bank conflicts
+            const uint4 v = *(const uint4 *)(row + ((pq * (NCH / 4) + cc + key) & (NCH - 1)) * 16);
             const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
             for (int e = 0; e < 4; ++e) s2 += bf_lo(w4[e]) * bf_lo(w4[e]) + bf_hi(w4[e]) * bf_hi(w4[e]);
@@ -221,11 +221,12 @@ void attn_sens_kernel(AttnArgs a) {
         for (int it = 0; it < n_it; ++it) {
             const int st = it & 1;
             wait_vm<0>();
-            __syncthreads();
+            __syncthreads();                                  // stage it landed; stage it - 1 is free
             key_norms(st);
             between(it);
             __syncthreads();
-            if (it + 1 < n_it) issue_stage(st ^ 1, nkt, [&](int s) __attribute__((always_inline)) { return kt_of_it(it + 1, s); });
+            if (it + 1 < n_it)
+                issue_stage(st ^ 1, nkt, [&](int s) __attribute__((always_inline)) { return kt_of_it(it + 1, s); });
             body(it, st);
         }
         __syncthreads();
@@ -505,6 +506,7 @@ void attn_sens_kernel(AttnArgs a) {
         }
         const int my_a = nt_a(t), my_c = nt_c(t);
         auto kt_pre = [](int it, int s) __attribute__((always_inline)) { return 4 * it + s; };
+        const int n_it_c = (pre_c + kSlots - 1) / kSlots;
         load_q(t);
         reset_a(t);
         sweep(S.pre_it, nka, kt_pre, [](int) __attribute__((always_inline)) {}, [&](int it, int st) __attribute__((always_inline)) {
@@ -514,7 +516,6 @@ void attn_sens_kernel(AttnArgs a) {
             }
         });
         if (t >= 0) finish_tile(t);
-        const int n_it_c = (pre_c + kSlots - 1) / kSlots;
         sweep(n_it_c, pre_c, kt_pre,
               [&](int it) __attribute__((always_inline)) { if (it > 0) reduce_store(it - 1, kt_pre, pre_c, 0); },
               [&](int it, int st) __attribute__((always_inline)) {
