@@ -108,6 +108,10 @@ def _load():
     lib.oracle_stats_multi.argtypes = [ctypes.c_int, ctypes.c_int] + [_i32p] * 6 + [
         _u16p, _i64p, ctypes.c_int, _u16p, _i64p, ctypes.c_int,
         _f32p, ctypes.c_int64, ctypes.c_int, ctypes.c_int, ctypes.c_int, _f64p, _f64p, ctypes.c_int]
+    lib.oracle_stats_multi_centered.restype = ctypes.c_int
+    lib.oracle_stats_multi_centered.argtypes = [ctypes.c_int, ctypes.c_int] + [_i32p] * 6 + [
+        _u16p, _i64p, ctypes.c_int, _u16p, _i64p, ctypes.c_int,
+        _f32p, ctypes.c_int64, ctypes.c_int, ctypes.c_int, ctypes.c_int, _f64p, _f64p, _f64p, ctypes.c_int]
     lib.oracle_apply_multi.restype = ctypes.c_int
     lib.oracle_apply_multi.argtypes = [ctypes.c_int, ctypes.c_int] + [_i32p] * 5 + [
         _f64p, _u16p, _i64p, ctypes.c_int, _u16p, _i64p, ctypes.c_int,
@@ -444,6 +448,30 @@ def stats_multi(head_map, src, src_strides, d_s, tgt, tgt_strides, d_t, weights,
                            int(n_seqs), int(seq_len), int(sample_stride), _ptr(G, _f64p), _ptr(C, _f64p),
                            int(n_threads))
     return G, C
+
+
+def stats_multi_centered(head_map, src, src_strides, d_s, tgt, tgt_strides, d_t, weights, w_row_stride,
+                         n_seqs, seq_len, sample_stride=1, n_threads: int = 0):
+    """Two-pass centered moments over the multi-layer feature x = [x_0; ...; x_{k-1}]
+    (width Dx = k d_s), tokens t with t mod sample_stride == 0: returns
+    (sums [n][1 + Dx + d_t], A [n][Dx][Dx], B [n][Dx][d_t]) in fp64; solve them
+    with :func:`ridge_solve_centered` (feature width Dx)."""
+    lib = _load()
+    n, k, hm = _multi_arrays(head_map)
+    Dx = k * d_s
+    sums = np.zeros((n, 1 + Dx + d_t), dtype=np.float64)
+    A = np.zeros((n, Dx, Dx), dtype=np.float64)
+    B = np.zeros((n, Dx, d_t), dtype=np.float64)
+    assert int(sample_stride) >= 1
+    src = np.ascontiguousarray(_u16(src))
+    tgt = np.ascontiguousarray(_u16(tgt))
+    w = np.ascontiguousarray(np.asarray(weights, dtype=np.float32))
+    ss, ts = _strides5(src_strides), _strides5(tgt_strides)
+    lib.oracle_stats_multi_centered(n, k, *[_ptr(a, _i32p) for a in hm], _ptr(src, _u16p), _ptr(ss, _i64p), d_s,
+                                    _ptr(tgt, _u16p), _ptr(ts, _i64p), d_t, _ptr(w, _f32p), int(w_row_stride),
+                                    int(n_seqs), int(seq_len), int(sample_stride), _ptr(sums, _f64p),
+                                    _ptr(A, _f64p), _ptr(B, _f64p), int(n_threads))
+    return sums, A, B
 
 
 def apply_multi(head_map, W, src, src_strides, d_s, out, out_strides, d_t, n_seqs, seq_len,

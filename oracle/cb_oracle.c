@@ -34,7 +34,8 @@
  *   Multi-layer feature (Sec. 3.2, Eq. localfeature with k selected source
  *   layers): x~ = [x_0 ; ... ; x_{k-1} ; 1], P = k d_s + 1, over the sampled
  *   calibration rows (oracle_stats_multi, oracle_apply_multi); the solve above
- *   takes any P.
+ *   takes any P.  Its two-pass centered form (oracle_stats_multi_centered)
+ *   feeds oracle_ridge_solve_centered with the feature width k d_s.
  *
  * Parity status: stats, solve and apply are pinned by the tests in
  * tests/test_oracle_pins.py (closed forms, invariants, library special cases,
@@ -721,6 +722,74 @@ int oracle_stats_multi(int n_maps, int k,
             }
         }
         free(xt);
+        free(y);
+    }
+    return 0;
+}
+
+/*
+ * Two-pass centered statistics (Sec. 3.4) over the multi-layer feature of
+ * Sec. 3.2: x = [x_0 ; ... ; x_{k-1}] (width Dx = k d_s, no bias entry), the
+ * calibration rows t with t mod sample_stride == 0.  Pass 1 sums w, w x and
+ * w y over every row; pass 2 revisits the rows and accumulates the moments
+ * about the weighted means of pass 1.  Outputs (overwritten, fp64):
+ *   sums [n_maps][1 + Dx + d_t] = (sum w, sum w x, sum w y),
+ *   A [n_maps][Dx][Dx] = sum w (x - mu_x)(x - mu_x)^T,
+ *   B [n_maps][Dx][d_t] = sum w (x - mu_x)(y - mu_y)^T.
+ * A map whose weights sum to zero gets zero means.  Returns 0.
+ */
+int oracle_stats_multi_centered(int n_maps, int k,
+                                const int32_t *tgt_layer, const int32_t *tgt_head, const int32_t *kv,
+                                const int32_t *src_layers, const int32_t *src_head, const int32_t *weight_row,
+                                const uint16_t *src, const int64_t *src_strides, int d_s,
+                                const uint16_t *tgt, const int64_t *tgt_strides, int d_t,
+                                const float *weights, int64_t w_row_stride,
+                                int n_seqs, int seq_len, int sample_stride,
+                                double *sums, double *A, double *B, int n_threads) {
+    const int Dx = k * d_s, NS = 1 + Dx + d_t;
+    set_threads(n_threads);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int m = 0; m < n_maps; ++m) {
+        double *sm = sums + (int64_t)m * NS;
+        double *Am = A + (int64_t)m * Dx * Dx;
+        double *Bm = B + (int64_t)m * Dx * d_t;
+        double *x = (double *)malloc(sizeof(double) * (size_t)Dx);
+        double *y = (double *)malloc(sizeof(double) * (size_t)d_t);
+        memset(sm, 0, sizeof(double) * (size_t)NS);
+        memset(Am, 0, sizeof(double) * (size_t)Dx * Dx);
+        memset(Bm, 0, sizeof(double) * (size_t)Dx * d_t);
+        for (int pass = 0; pass < 2; ++pass) {
+            const double sw = sm[0];
+            for (int b = 0; b < n_seqs; ++b) {
+                for (int t = 0; t < seq_len; t += sample_stride) {
+                    for (int i = 0; i < k; ++i) {
+                        const uint16_t *xr = src + row_offset(src_strides, src_layers[(int64_t)m * k + i], kv[m], b,
+                                                              src_head[m], t);
+                        for (int c = 0; c < d_s; ++c) x[i * d_s + c] = bf16_bits_to_double(xr[c]);
+                    }
+                    const uint16_t *yr = tgt + row_offset(tgt_strides, tgt_layer[m], kv[m], b, tgt_head[m], t);
+                    for (int j = 0; j < d_t; ++j) y[j] = bf16_bits_to_double(yr[j]);
+                    const double w = (double)weights[(int64_t)weight_row[m] * w_row_stride + (int64_t)b * seq_len + t];
+                    if (pass == 0) {                       /* pass 1: weighted sums */
+                        sm[0] += w;
+                        for (int i = 0; i < Dx; ++i) sm[1 + i] += w * x[i];
+                        for (int j = 0; j < d_t; ++j) sm[1 + Dx + j] += w * y[j];
+                        continue;
+                    }
+                    /* pass 2: moments about the means */
+                    for (int i = 0; i < Dx; ++i) x[i] -= sw != 0.0 ? sm[1 + i] / sw : 0.0;
+                    for (int j = 0; j < d_t; ++j) y[j] -= sw != 0.0 ? sm[1 + Dx + j] / sw : 0.0;
+                    for (int i = 0; i < Dx; ++i) {
+                        const double wi = w * x[i];
+                        double *ar = Am + (int64_t)i * Dx;
+                        double *br = Bm + (int64_t)i * d_t;
+                        for (int j = 0; j < Dx; ++j) ar[j] += wi * x[j];
+                        for (int j = 0; j < d_t; ++j) br[j] += wi * y[j];
+                    }
+                }
+            }
+        }
+        free(x);
         free(y);
     }
     return 0;

@@ -242,3 +242,91 @@ def test_qwen_k8_workload_shape_and_windows():
     for l in range(wl.L_t):
         S = synth.layer_window(wl, l)
         assert S[0] <= (2 * l * 39 + 63) // 126 <= S[-1]
+
+
+# ----------------------------------------------------------------------------- two-pass centered form
+#
+# stats_multi_centered (Sec. 3.4 two-pass form over the Sec. 3.2 multi-layer
+# feature) is pinned by: numpy's weighted covariance of the explicit feature
+# matrix (a library routine); exact invariance of A, B when integer data are
+# shifted by a constant vector; the Schur-complement identity between the
+# centered ridge and the unpenalized augmented ridge of stats_multi; k = 1
+# against the single-layer centered oracle; zero-weight maps; sampling equals
+# zero weights off the grid.
+
+def centered(p, stride, w=None):
+    return oracle.stats_multi_centered(p.hm, p.src, p.ss, p.d_s, p.tgt, p.ts, p.d_t, p.w if w is None else w,
+                                       p.B * p.T, p.B, p.T, stride)
+
+
+@pytest.mark.parametrize("stride", [1, 4])
+def test_multi_centered_equals_numpy_weighted_covariance(stride):
+    p = MultiProblem(np.random.default_rng(211 + stride))
+    sums, A, B = centered(p, stride)
+    Dx = p.k * p.d_s
+    assert sums.shape == (p.n_maps, 1 + Dx + p.d_t) and A.shape == (p.n_maps, Dx, Dx)
+    for m in range(p.n_maps):
+        x, y, w = p.design(m, stride)
+        x = x[:, :Dx]
+        S = w.sum()
+        assert sums[m, 0] == pytest.approx(S, rel=1e-14)
+        assert relF(sums[m, 1:1 + Dx], w @ x) < 1e-13 and relF(sums[m, 1 + Dx:], w @ y) < 1e-13
+        cov = np.cov(np.concatenate([x, y], axis=1).T, aweights=w, bias=True) * S
+        assert relF(A[m], cov[:Dx, :Dx]) < 1e-11
+        assert relF(B[m], cov[:Dx, Dx:]) < 1e-11
+
+
+def test_multi_centered_shift_invariance_on_integers():
+    rng = np.random.default_rng(17)
+    p = MultiProblem(rng, k=2, L_s=3, d_s=4, d_t=3, B=2, T=9, values="int")
+    q = MultiProblem(np.random.default_rng(17), k=2, L_s=3, d_s=4, d_t=3, B=2, T=9, values="int")
+    # shift every source channel and target channel by an integer constant (exact in bf16)
+    sx = rng.integers(-6, 7, size=p.d_s)
+    sy = rng.integers(-6, 7, size=p.d_t)
+    q.src = to_bf16_bits(p.X + sx)
+    q.tgt = to_bf16_bits(p.Y + sy)
+    q.w = np.ones_like(p.w)                       # means are then dyadic-free integers / n: keep weights exact
+    p.w = np.ones_like(p.w)
+    _, A1, B1 = centered(p, 1)
+    _, A2, B2 = centered(q, 1)
+    assert np.allclose(A1, A2, rtol=0, atol=1e-9 * np.abs(A1).max())
+    assert np.allclose(B1, B2, rtol=0, atol=1e-9 * max(np.abs(B1).max(), 1.0))
+
+
+@pytest.mark.parametrize("relative,lam", [(True, 1e-2), (False, 0.5)])
+def test_multi_centered_ridge_equals_unpenalized_augmented_ridge(relative, lam):
+    p = MultiProblem(np.random.default_rng(23), T=29)
+    stride = 2
+    sums, A, B = centered(p, stride)
+    G, C = p.stats(stride)
+    Wc, ic = oracle.ridge_solve_centered(sums, A, B, lam, relative=relative)
+    Wa, ia = oracle.ridge_solve(G, C, lam, relative=relative, bias_unpenalized=True)
+    assert (ic == 0).all() and (ia == 0).all()
+    for m in range(p.n_maps):
+        assert relF(Wc[m], Wa[m]) < 1e-9
+
+
+def test_multi_centered_k1_equals_single_layer_centered():
+    p = MultiProblem(np.random.default_rng(29), k=1)
+    sums, A, B = centered(p, 1)
+    hm1 = {"tgt_layer": p.hm["tgt_layer"], "tgt_head": p.hm["tgt_head"], "kv": p.hm["kv"],
+           "src_layer": p.hm["src_layers"][:, 0].copy(), "src_head": p.hm["src_head"],
+           "weight_row": p.hm["weight_row"]}
+    s1, A1, B1 = oracle.stats_centered(hm1, p.src, p.ss, p.d_s, p.tgt, p.ts, p.d_t, p.w, p.B * p.T, p.B, p.T)
+    assert np.array_equal(sums, s1) and np.array_equal(A, A1) and np.array_equal(B, B1)
+
+
+def test_multi_centered_zero_weights_and_sampling():
+    p = MultiProblem(np.random.default_rng(31), T=22)
+    w = p.w.copy()
+    w[0] = 0.0                                    # maps of weight row 0 see no weight
+    sums, A, B = centered(p, 3, w=w)
+    zero = np.where(p.hm["weight_row"] == 0)[0]
+    assert len(zero) > 0
+    for m in zero:
+        assert not sums[m].any() and not A[m].any() and not B[m].any()
+    w0 = p.w.copy().reshape(-1, p.B, p.T)
+    w0[:, :, np.arange(p.T) % 3 != 0] = 0.0
+    s1, A1, B1 = centered(p, 3)
+    s2, A2, B2 = centered(p, 1, w=w0.reshape(p.w.shape))
+    assert np.array_equal(s1, s2) and np.array_equal(A1, A2) and np.array_equal(B1, B2)
