@@ -212,7 +212,11 @@ cb_status cb_ridge_solve(int32_t n_maps, int32_t P, int32_t d_t, const float *G,
  * pass 2 revisits the batches and accumulates the moments about the means of
  * pass 1 (cb_stats_accumulate_centered).  Centering before the products keeps
  * A and B accurate when channels carry large means, where the uncentered
- * moments of cb_stats_accumulate lose digits to cancellation.  Per map m:
+ * moments of cb_stats_accumulate lose digits to cancellation.  A multi-layer
+ * plan (cb_plan_create_multi) is accepted too: x is then the concatenated
+ * feature [x_0; ...; x_{k-1}] of width d_x = k d_s in place of d_s below, the
+ * calibration rows are the plan's sampled tokens, sq must be NULL, and the
+ * maps are solved with cb_ridge_solve_centered_ws.  Per map m:
  *   sums [n_maps][1 + d_s + d_t] fp64 = (sum w, sum w x, sum w y)
  *   mu_x = (sum w x) / (sum w),  mu_y = (sum w y) / (sum w)   (0 if sum w = 0)
  *   A [n_maps][d_s][d_s] fp32 = sum w (x - mu_x)(x - mu_x)^T
@@ -266,6 +270,22 @@ cb_status cb_stats_accumulate_centered(cb_plan *plan, const cb_cache *src, const
 cb_status cb_ridge_solve_centered(int32_t n_maps, int32_t d_s, int32_t d_t, const double *sums, const float *A,
                                   const float *B, float lambda, uint32_t flags, float *maps, int32_t *info,
                                   void *stream);
+
+/*
+ * Centered ridge solve for any feature width (Sec. 3.1, Eq. closedform over
+ * the multi-layer feature of Sec. 3.2, d_x = k d_s): the arrays, lambda_m,
+ * bias and info of cb_ridge_solve_centered with d_x in place of d_s, maps
+ * [n_maps][d_x + 1][d_t].  d_x <= 128 runs cb_ridge_solve_centered (the
+ * workspace is ignored); otherwise (d_x <= 4096, d_t in {64, 96, 128}) each
+ * system A + lambda_m I is factored in fp64 in `workspace` (caller-owned device
+ * memory, 8-byte aligned, at least cb_ridge_solve_workspace_bytes(d_x, d_t, 1)
+ * bytes) by the blocked Cholesky of cb_ridge_solve_ws, batches as there, and
+ * the bias row b = mu_y - W^T mu_x is formed in fp64.  Errors: CB_ERR_SHAPE
+ * (workspace too small), else as cb_ridge_solve_centered.
+ */
+cb_status cb_ridge_solve_centered_ws(int32_t n_maps, int32_t d_x, int32_t d_t, const double *sums, const float *A,
+                                     const float *B, float lambda, uint32_t flags, void *workspace,
+                                     int64_t workspace_bytes, float *maps, int32_t *info, void *stream);
 
 /*
  * Held-in R^2 of layer-selection probes (Sec. 3.1: for each target layer,
@@ -447,8 +467,8 @@ typedef struct {
  * (coefficients as two bf16 terms, fp32 sums and bias, one rounding); the
  * rows of one source (layer, kv, head) must span fewer than 2^32 elements
  * ((n_seqs - 1) s_seq + (seq_len - 1) s_tok + 128), else CB_ERR_UNSUPPORTED
- * (apply in smaller batches).  The centered and means calls return
- * CB_ERR_UNSUPPORTED for such a plan.  Errors
+ * (apply in smaller batches).  The two-pass centered calls (cb_stats_means
+ * without sq, cb_stats_accumulate_centered) take such a plan too.  Errors
  * as in cb_plan_create, plus CB_ERR_INVALID_ARGUMENT for a source layer
  * selected twice by one map.
  */

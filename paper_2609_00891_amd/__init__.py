@@ -115,6 +115,9 @@ _lib.cb_ridge_solve.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, 
 _lib.cb_ridge_solve_ws.restype = ctypes.c_int
 _lib.cb_ridge_solve_ws.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp, _vp, ctypes.c_float,
                                    ctypes.c_uint32, _vp, ctypes.c_int64, _vp, _vp, _vp]
+_lib.cb_ridge_solve_centered_ws.restype = ctypes.c_int
+_lib.cb_ridge_solve_centered_ws.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp, _vp, _vp,
+                                            ctypes.c_float, ctypes.c_uint32, _vp, ctypes.c_int64, _vp, _vp, _vp]
 _lib.cb_ridge_solve_noalloc.restype = ctypes.c_int
 _lib.cb_ridge_solve_noalloc.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp, _vp, ctypes.c_float,
                                         ctypes.c_uint32, _vp, _vp, _vp]
@@ -190,6 +193,35 @@ def _ptr(t: Optional[torch.Tensor]):
     return None if t is None else t.data_ptr()
 
 
+def _need(t: Optional[torch.Tensor], shape, dtype, name: str):
+    """The library writes (or reads) exactly prod(shape) dense elements at t's
+    address: check that t holds them."""
+    if t is None:
+        raise ValueError(f"{name} is required")
+    if t.dtype != dtype or tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous {dtype} tensor of shape {tuple(shape)}, "
+                         f"got {t.dtype} {tuple(t.shape)}")
+
+
+def _check_weights(plan: "Plan", weights: torch.Tensor, row_stride: int, src: torch.Tensor):
+    """Every weight the kernels read, w[row * row_stride + seq * T + tok], lies inside
+    ``weights``' storage (a row stride shorter than a row is the library's own
+    CB_ERR_SHAPE)."""
+    if weights.dtype != torch.float32:
+        raise ValueError("weights are float32")
+    n_tok = src.shape[2] * src.shape[4]
+    if plan.n_weight_rows == 0 or n_tok == 0 or row_stride < n_tok:
+        return
+    if weights.numel() > 1 and weights.stride(-1) != 1:
+        raise ValueError("weights rows must be dense")
+    if weights.dim() == 2 and weights.shape[0] < plan.n_weight_rows:
+        raise ValueError(f"weights must have at least {plan.n_weight_rows} rows")
+    need = (plan.n_weight_rows - 1) * row_stride + n_tok
+    have = weights.untyped_storage().nbytes() // 4 - weights.storage_offset()
+    if have < need:
+        raise ValueError(f"weights must hold {need} float32 values from their first element")
+
+
 def cache_view(t: Optional[torch.Tensor], n_layers=None, n_heads=None, head_dim=None) -> CbCache:
     """Describe a [layer][kv][seq][head][tok][dim] bfloat16 tensor (any strides, unit channel stride)."""
     c = CbCache()
@@ -216,6 +248,8 @@ class Plan:
         self.P = d_s + 1 if P is None else P
         self.k = k
         self._keep = keep
+        wr = keep[-1]                                  # weight_row is the last head-map field
+        self.n_weight_rows = int(wr.max()) + 1 if wr.size else 0
 
     def close(self):
         if self.handle:
@@ -292,16 +326,19 @@ def cb_plan_destroy(plan: Plan):
 
 
 def cb_stats_zero(plan: Plan, G: torch.Tensor, C: torch.Tensor, stream=None):
+    _need(G, (plan.n_maps, plan.P, plan.P), torch.float32, "G")
+    _need(C, (plan.n_maps, plan.P, plan.d_t), torch.float32, "C")
     _check(_lib.cb_stats_zero(plan.handle, _ptr(G), _ptr(C), _stream(stream)))
 
 
 def cb_stats_accumulate(plan: Plan, src: torch.Tensor, tgt: torch.Tensor, weights: torch.Tensor,
                         G: torch.Tensor, C: torch.Tensor, w_row_stride: Optional[int] = None, stream=None):
     """G[m] += sum_t w x~ x~^T, C[m] += sum_t w x~ y^T over the batch (fp32 outputs)."""
-    if weights.dtype != torch.float32 or G.dtype != torch.float32 or C.dtype != torch.float32:
-        raise ValueError("weights, G and C are float32")
+    _need(G, (plan.n_maps, plan.P, plan.P), torch.float32, "G")
+    _need(C, (plan.n_maps, plan.P, plan.d_t), torch.float32, "C")
     if w_row_stride is None:
         w_row_stride = weights.stride(0) if weights.dim() == 2 else weights.numel()
+    _check_weights(plan, weights, int(w_row_stride), src)
     sv, tv = cache_view(src), cache_view(tgt)
     _check(_lib.cb_stats_accumulate(plan.handle, ctypes.byref(sv), ctypes.byref(tv), _ptr(weights),
                                     int(w_row_stride), _ptr(G), _ptr(C), _stream(stream)))
@@ -361,13 +398,23 @@ def _row_stride(weights: torch.Tensor, w_row_stride: Optional[int]) -> int:
     return weights.stride(0) if weights.dim() == 2 else weights.numel()
 
 
+def _need_centered(plan: Plan, sums, A, B, sq):
+    n, Dx, dt = plan.n_maps, plan.P - 1, plan.d_t
+    _need(sums, (n, 1 + Dx + dt), torch.float64, "sums")
+    if A is not None:
+        _need(A, (n, Dx, Dx), torch.float32, "A")
+    if B is not None:
+        _need(B, (n, Dx, dt), torch.float32, "B")
+    if sq is not None:
+        _need(sq, (n, Dx + dt), torch.float64, "sq")
+
+
 def cb_stats_zero_centered(plan: Plan, sums: torch.Tensor, A: torch.Tensor, B: torch.Tensor,
                            sq: Optional[torch.Tensor] = None, stream=None):
-    """Zero sums [n][1 + d_s + d_t] (float64), A [n][d_s][d_s], B [n][d_s][d_t] (float32)
-    and, if given, sq [n][d_s + d_t] (float64)."""
-    if sums.dtype != torch.float64 or A.dtype != torch.float32 or B.dtype != torch.float32 \
-            or (sq is not None and sq.dtype != torch.float64):
-        raise ValueError("sums and sq are float64, A and B are float32")
+    """Zero sums [n][1 + d_x + d_t] (float64), A [n][d_x][d_x], B [n][d_x][d_t] (float32)
+    and, if given (single-layer plans), sq [n][d_s + d_t] (float64); d_x = d_s, or k d_s
+    for a multi-layer plan."""
+    _need_centered(plan, sums, A, B, sq)
     _check(_lib.cb_stats_zero_centered(plan.handle, _ptr(sums), _ptr(sq), _ptr(A), _ptr(B), _stream(stream)))
 
 
@@ -375,23 +422,22 @@ def cb_stats_means(plan: Plan, src: torch.Tensor, tgt: torch.Tensor, weights: to
                    sq: Optional[torch.Tensor] = None, w_row_stride: Optional[int] = None, stream=None):
     """Pass 1: sums[m] += (sum w, sum w x, sum w y) and, if given, sq[m] += (sum w x^2, sum w y^2)
     over the batch (float64)."""
-    if weights.dtype != torch.float32 or sums.dtype != torch.float64 or (sq is not None and sq.dtype != torch.float64):
-        raise ValueError("weights are float32, sums and sq float64")
+    _need_centered(plan, sums, None, None, sq)
+    rs = _row_stride(weights, w_row_stride)
+    _check_weights(plan, weights, rs, src)
     sv, tv = cache_view(src), cache_view(tgt)
-    _check(_lib.cb_stats_means(plan.handle, ctypes.byref(sv), ctypes.byref(tv), _ptr(weights),
-                               _row_stride(weights, w_row_stride), _ptr(sums), _ptr(sq), _stream(stream)))
+    _check(_lib.cb_stats_means(plan.handle, ctypes.byref(sv), ctypes.byref(tv), _ptr(weights), rs, _ptr(sums), _ptr(sq), _stream(stream)))
 
 
 def cb_stats_accumulate_centered(plan: Plan, src: torch.Tensor, tgt: torch.Tensor, weights: torch.Tensor,
                                  sums: torch.Tensor, A: torch.Tensor, B: torch.Tensor,
                                  w_row_stride: Optional[int] = None, stream=None):
     """Pass 2: A[m] += sum w (x - mu_x)(x - mu_x)^T, B[m] += sum w (x - mu_x)(y - mu_y)^T."""
-    if weights.dtype != torch.float32 or sums.dtype != torch.float64 or A.dtype != torch.float32 \
-            or B.dtype != torch.float32:
-        raise ValueError("weights, A and B are float32, sums float64")
+    _need_centered(plan, sums, A, B, None)
+    rs = _row_stride(weights, w_row_stride)
+    _check_weights(plan, weights, rs, src)
     sv, tv = cache_view(src), cache_view(tgt)
-    _check(_lib.cb_stats_accumulate_centered(plan.handle, ctypes.byref(sv), ctypes.byref(tv), _ptr(weights),
-                                             _row_stride(weights, w_row_stride), _ptr(sums), _ptr(A), _ptr(B),
+    _check(_lib.cb_stats_accumulate_centered(plan.handle, ctypes.byref(sv), ctypes.byref(tv), _ptr(weights), rs, _ptr(sums), _ptr(A), _ptr(B),
                                              _stream(stream)))
 
 
@@ -407,6 +453,24 @@ def cb_ridge_solve_centered(sums: torch.Tensor, A: torch.Tensor, B: torch.Tensor
         raise ValueError("sums is float64, info int32")
     _check(_lib.cb_ridge_solve_centered(n, d_s, d_t, _ptr(sums), _ptr(A), _ptr(B), float(lam), int(flags),
                                         _ptr(maps), _ptr(info), _stream(stream)))
+
+
+def cb_ridge_solve_centered_ws(sums: torch.Tensor, A: torch.Tensor, B: torch.Tensor, lam: float, flags: int,
+                               maps: torch.Tensor, info: torch.Tensor, workspace: Optional[torch.Tensor],
+                               stream=None):
+    """The centered solve for any feature width d_x (the multi-layer feature: d_x = k d_s):
+    maps[m] = [W; b^T]; d_x > 128 factors in ``workspace`` (at least
+    cb_ridge_solve_workspace_bytes(d_x, d_t, 1) bytes)."""
+    n, d_x, d_x2 = A.shape
+    d_t = B.shape[2] if B.dim() == 3 else -1
+    if d_x != d_x2 or B.shape[:2] != (n, d_x) or sums.shape != (n, 1 + d_x + d_t) \
+            or maps.shape != (n, d_x + 1, d_t) or info.shape != (n,):
+        raise ValueError("sums [n][1+d_x+d_t], A [n][d_x][d_x], B [n][d_x][d_t], maps [n][d_x+1][d_t], info [n]")
+    if sums.dtype != torch.float64 or info.dtype != torch.int32:
+        raise ValueError("sums is float64, info int32")
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(_lib.cb_ridge_solve_centered_ws(n, d_x, d_t, _ptr(sums), _ptr(A), _ptr(B), float(lam), int(flags),
+                                           _ptr(workspace), int(ws_bytes), _ptr(maps), _ptr(info), _stream(stream)))
 
 
 def cb_probe_r2(sums: torch.Tensor, sq: torch.Tensor, A: torch.Tensor, B: torch.Tensor, maps: torch.Tensor,
@@ -497,8 +561,7 @@ def cb_rope(cache_in: torch.Tensor, cache_out: torch.Tensor, table: torch.Tensor
 
 def cb_apply(plan: Plan, maps: torch.Tensor, src: torch.Tensor, tgt_out: torch.Tensor, stream=None):
     """tgt_out[l, z, b, h, t, :] = RNE_bf16([x, 1] maps[m]) for every map and token."""
-    if maps.dtype != torch.float32:
-        raise ValueError("maps are float32")
+    _need(maps, (plan.n_maps, plan.P, plan.d_t), torch.float32, "maps")
     sv, ov = cache_view(src), cache_view(tgt_out)
     _check(_lib.cb_apply(plan.handle, _ptr(maps), ctypes.byref(sv), ctypes.byref(ov), _stream(stream)))
 
@@ -507,8 +570,9 @@ def cb_apply_rope(plan: Plan, maps: torch.Tensor, src: torch.Tensor, tgt_out: to
                   style: int = CB_ROPE_HALF_SPLIT, pos_offset: int = 0, stream=None):
     """cb_apply with the target RoPE (table from cb_rope_table, head_dim d_t) turning the K outputs in fp32
     before their single rounding."""
-    if maps.dtype != torch.float32 or table.dtype != torch.float32:
-        raise ValueError("maps and table are float32")
+    _need(maps, (plan.n_maps, plan.P, plan.d_t), torch.float32, "maps")
+    if table.dtype != torch.float32:
+        raise ValueError("table is float32")
     sv, ov = cache_view(src), cache_view(tgt_out)
     _check(_lib.cb_apply_rope(plan.handle, _ptr(maps), ctypes.byref(sv), ctypes.byref(ov), _ptr(table),
                               int(table.shape[0]), int(style), int(pos_offset), _stream(stream)))

@@ -34,6 +34,7 @@ struct cb_plan {
     cb::ApplyMultiMap *d_amaps = nullptr;   // multi-layer application: map records, visiting order, layers
     int32_t *d_aorder = nullptr;
     int32_t *d_alayers = nullptr;
+    int32_t *d_mwrow = nullptr;             // multi-layer: weight row of each map (means pass)
     // statistics schedule
     int32_t n_items = 0;
     int32_t max_chunks = 1;
@@ -237,11 +238,6 @@ bool exact_rect_cover(int k, std::vector<Rect> &out) {
     return true;
 }
 
-cb_status single_layer_only(const cb_plan *p, const char *call) {
-    if (p->multi)
-        return fail(CB_ERR_UNSUPPORTED, "%s takes plans of single-layer maps (cb_plan_create), not multi-layer ones", call);
-    return CB_OK;
-}
 
 // Validation and launch arguments of a multi-layer statistics call.
 cb_status prepare_multi(const cb_plan *p, const cb_cache *src, const cb_cache *tgt, const float *weights,
@@ -342,6 +338,7 @@ cb_status cb_plan_destroy(cb_plan *p) {
     (void)hipFree(p->d_amaps);
     (void)hipFree(p->d_aorder);
     (void)hipFree(p->d_alayers);
+    (void)hipFree(p->d_mwrow);
     delete p;
     return ok();
 }
@@ -679,6 +676,7 @@ cb_status cb_plan_create_multi(const cb_head_map_multi *map, const cb_cache *src
                hipMalloc(&p->d_amaps, sizeof(cb::ApplyMultiMap) * n) == hipSuccess &&
                hipMalloc(&p->d_aorder, sizeof(int32_t) * n) == hipSuccess &&
                hipMalloc(&p->d_alayers, sizeof(int32_t) * (size_t)n * k) == hipSuccess &&
+               hipMalloc(&p->d_mwrow, sizeof(int32_t) * (size_t)n) == hipSuccess &&
                hipMalloc(&p->d_whi, 2 * wsplit) == hipSuccess &&   // hi and lo fragment planes
                hipMalloc(&p->d_bias, sizeof(float) * n * d_t) == hipSuccess;
     if (!okm) {
@@ -690,7 +688,8 @@ cb_status cb_plan_create_multi(const cb_head_map_multi *map, const cb_cache *src
         hipMemcpy(p->d_tasks, tasks.data(), sizeof(cb::MultiTask) * tasks.size(), hipMemcpyHostToDevice) != hipSuccess ||
         hipMemcpy(p->d_amaps, amaps.data(), sizeof(cb::ApplyMultiMap) * n, hipMemcpyHostToDevice) != hipSuccess ||
         hipMemcpy(p->d_aorder, order.data(), sizeof(int32_t) * n, hipMemcpyHostToDevice) != hipSuccess ||
-        hipMemcpy(p->d_alayers, map->src_layers, sizeof(int32_t) * (size_t)n * k, hipMemcpyHostToDevice) != hipSuccess) {
+        hipMemcpy(p->d_alayers, map->src_layers, sizeof(int32_t) * (size_t)n * k, hipMemcpyHostToDevice) != hipSuccess ||
+        hipMemcpy(p->d_mwrow, map->weight_row, sizeof(int32_t) * (size_t)n, hipMemcpyHostToDevice) != hipSuccess) {
         cb_plan_destroy(p);
         return fail(CB_ERR_DEVICE, "copying the schedule to the device failed");
     }
@@ -757,9 +756,9 @@ cb_status cb_stats_accumulate(cb_plan *p, const cb_cache *src, const cb_cache *t
 
 cb_status cb_stats_zero_centered(const cb_plan *p, double *sums, double *sq, float *A, float *B, void *stream) {
     if (!p || !sums || !A || !B) return fail(CB_ERR_INVALID_ARGUMENT, "plan, sums, A and B must be non-NULL");
-    if (cb_status s = single_layer_only(p, "cb_stats_zero_centered")) return s;
+    if (p->multi && sq) return fail(CB_ERR_UNSUPPORTED, "sums of squares (probes) are single-layer only");
     if (cb_status s = check_device(p)) return s;
-    const int64_t n = p->n_maps, ds = p->d_s, dt = p->d_t;
+    const int64_t n = p->n_maps, ds = p->multi ? (int64_t)p->P - 1 : p->d_s, dt = p->d_t;
     hipStream_t st = (hipStream_t)stream;
     if (cb::launch_fill_zero((float *)sums, 2 * n * (1 + ds + dt), st) != hipSuccess ||
         (sq && cb::launch_fill_zero((float *)sq, 2 * n * (ds + dt), st) != hipSuccess) ||
@@ -772,8 +771,35 @@ cb_status cb_stats_means(cb_plan *p, const cb_cache *src, const cb_cache *tgt, c
                          int64_t w_row_stride, double *sums, double *sq, void *stream) {
     if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
     if (!sums) return fail(CB_ERR_INVALID_ARGUMENT, "sums must be non-NULL");
-    if (cb_status s = single_layer_only(p, "cb_stats_means")) return s;
     if (((uintptr_t)sums) % 8 || ((uintptr_t)sq) % 8) return fail(CB_ERR_MISALIGNED, "sums and sq must be 8-byte aligned");
+    if (p->multi) {
+        if (sq) return fail(CB_ERR_UNSUPPORTED, "sums of squares (probes) are single-layer only");
+        cb::MultiArgs ma = {};
+        bool empty = false;
+        if (cb_status s = prepare_multi(p, src, tgt, weights, w_row_stride, ma, empty)) return s;
+        if (empty) return ok();
+        cb::MeansMultiArgs m = {};
+        m.src = ma.src;
+        m.tgt = ma.tgt;
+        m.w = ma.w;
+        m.ss = ma.ss;
+        m.ts = ma.ts;
+        m.w_row_stride = ma.w_row_stride;
+        m.n_seqs = src->n_seqs;
+        m.seq_len = src->seq_len;
+        m.stride = p->sample_stride;
+        m.rows_per_seq = (int32_t)ma.rows_per_seq;
+        m.n_maps = p->n_maps;
+        m.k = p->k;
+        m.d_t = p->d_t;
+        m.maps = p->d_amaps;
+        m.layers = p->d_alayers;
+        m.wrow = p->d_mwrow;
+        m.sums = sums;
+        if (cb::launch_means_multi(m, (hipStream_t)stream) != hipSuccess)
+            return fail(CB_ERR_DEVICE, "multi-layer means kernel launch failed");
+        return ok();
+    }
     cb::StatsArgs a = {};
     bool empty = false;
     if (cb_status s = prepare_stats(p, src, tgt, weights, w_row_stride, a, empty)) return s;
@@ -801,9 +827,20 @@ cb_status cb_stats_accumulate_centered(cb_plan *p, const cb_cache *src, const cb
                                        int64_t w_row_stride, const double *sums, float *A, float *B, void *stream) {
     if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
     if (!sums || !A || !B) return fail(CB_ERR_INVALID_ARGUMENT, "sums, A and B must be non-NULL");
-    if (cb_status s = single_layer_only(p, "cb_stats_accumulate_centered")) return s;
     if (((uintptr_t)sums) % 8 || ((uintptr_t)A) % 4 || ((uintptr_t)B) % 4)
         return fail(CB_ERR_MISALIGNED, "sums must be 8-byte and A, B 4-byte aligned");
+    if (p->multi) {
+        cb::MultiArgs ma = {};
+        bool empty = false;
+        if (cb_status s = prepare_multi(p, src, tgt, weights, w_row_stride, ma, empty)) return s;
+        if (empty) return ok();
+        ma.G = A;
+        ma.C = B;
+        ma.sums = sums;
+        if (cb::launch_stats_multi_centered(ma, (hipStream_t)stream) != hipSuccess)
+            return fail(CB_ERR_DEVICE, "multi-layer centered statistics kernel launch failed");
+        return ok();
+    }
     cb::StatsArgs a = {};
     bool empty = false;
     if (cb_status s = prepare_stats(p, src, tgt, weights, w_row_stride, a, empty)) return s;
@@ -916,6 +953,32 @@ cb_status cb_ridge_solve_centered(int32_t n_maps, int32_t d_s, int32_t d_t, cons
     if (cb::launch_solve_centered(n_maps, d_s, d_t, sums, A, B, lambda, flags, maps, info, (hipStream_t)stream) !=
         hipSuccess)
         return fail(CB_ERR_DEVICE, "centered ridge solve launch failed");
+    return ok();
+}
+
+cb_status cb_ridge_solve_centered_ws(int32_t n_maps, int32_t d_x, int32_t d_t, const double *sums, const float *A,
+                                     const float *B, float lambda, uint32_t flags, void *workspace,
+                                     int64_t workspace_bytes, float *maps, int32_t *info, void *stream) {
+    if (d_x <= 128) return cb_ridge_solve_centered(n_maps, d_x, d_t, sums, A, B, lambda, flags, maps, info, stream);
+    if (n_maps < 0) return fail(CB_ERR_INVALID_ARGUMENT, "n_maps is negative");
+    if (d_x > 4096 || !supported_width(d_t))
+        return fail(CB_ERR_UNSUPPORTED, "need d_x <= 4096 and d_t in {64, 96, 128} (got d_x=%d, d_t=%d)", d_x, d_t);
+    if (flags & ~(uint32_t)(CB_LAMBDA_RELATIVE | CB_RIDGE_BIAS_UNPENALIZED))
+        return fail(CB_ERR_INVALID_ARGUMENT, "unknown flag bits 0x%x", flags);
+    if (!std::isfinite(lambda) || lambda < 0.f) return fail(CB_ERR_INVALID_ARGUMENT, "lambda must be finite and >= 0");
+    if (n_maps == 0) return ok();
+    if (!sums || !A || !B || !maps || !info || !workspace)
+        return fail(CB_ERR_INVALID_ARGUMENT, "sums, A, B, maps, info and workspace must be non-NULL");
+    if (((uintptr_t)sums) % 8 || ((uintptr_t)A) % 4 || ((uintptr_t)B) % 4 || ((uintptr_t)maps) % 4 ||
+        ((uintptr_t)info) % 4 || ((uintptr_t)workspace) % 8)
+        return fail(CB_ERR_MISALIGNED, "sums and workspace must be 8-byte and A, B, maps, info 4-byte aligned");
+    const int64_t need = cb::solve_blocked_bytes_per_system(d_x, d_t);
+    if (workspace_bytes < need)
+        return fail(CB_ERR_SHAPE, "workspace of %lld bytes is below one system's %lld bytes", (long long)workspace_bytes,
+                    (long long)need);
+    if (cb::launch_solve_blocked(n_maps, d_x, d_t, A, B, lambda, flags, workspace, workspace_bytes, maps, info,
+                                 (hipStream_t)stream, sums) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "blocked centered ridge solve launch failed");
     return ok();
 }
 

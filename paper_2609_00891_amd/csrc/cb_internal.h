@@ -152,12 +152,30 @@ struct MultiArgs {
     int32_t k, P, d_t;
     const MultiTask *tasks;
     const void *zero;         // >= 256 zero bytes
-    float *G, *C;
+    float *G, *C;             // centered: A [n][P-1][P-1], B [n][P-1][d_t]
+    const double *sums;       // centered only: [n][P + d_t] = (sum w, sum w x, sum w y)
 };
+
 
 // One map of the multi-layer application.
 struct ApplyMultiMap {
     int32_t tgt_layer, tgt_head, kv, src_head;
+};
+
+// Pass 1 of the centered multi-layer statistics: per map, sums of w, w x over
+// its k source blocks and w y over its target block, on the calibration rows.
+struct MeansMultiArgs {
+    const uint16_t *src;
+    const uint16_t *tgt;
+    const float *w;
+    Strides ss, ts;
+    int64_t w_row_stride;
+    int32_t n_seqs, seq_len, stride, rows_per_seq;
+    int32_t n_maps, k, d_t;
+    const ApplyMultiMap *maps;
+    const int32_t *layers;    // [n_maps][k]
+    const int32_t *wrow;      // [n_maps]
+    double *sums;             // [n_maps][1 + 128 k + d_t], added to
 };
 
 struct ApplyMultiArgs {
@@ -197,13 +215,17 @@ hipError_t launch_solve_centered(int32_t n_maps, int32_t d_s, int32_t d_t, const
                                  hipStream_t s);
 hipError_t launch_fill_zero(float *p, int64_t n, hipStream_t s);
 hipError_t launch_stats_multi(const MultiArgs &a, hipStream_t s);
+hipError_t launch_stats_multi_centered(const MultiArgs &a, hipStream_t s);
+hipError_t launch_means_multi(const MeansMultiArgs &a, hipStream_t s);
 hipError_t launch_split_maps_frag(int32_t n_maps, int32_t k, const float *maps, uint16_t *wfrag, float *bias,
                                   hipStream_t s);
 hipError_t launch_apply_multi(const ApplyMultiArgs &a, int32_t n_cu, hipStream_t s);
 int64_t solve_blocked_bytes_per_system(int32_t P, int32_t d_t);
+// csums != nullptr: centered systems (A, B of the feature without bias entry,
+// sums (sum w, sum w x, sum w y)); maps then get P + 1 rows (W, then the bias).
 hipError_t launch_solve_blocked(int32_t n_maps, int32_t P, int32_t d_t, const float *G, const float *C, float lambda,
                                 uint32_t flags, void *ws, int64_t ws_bytes, float *maps, int32_t *info,
-                                hipStream_t s);
+                                hipStream_t s, const double *csums = nullptr);
 constexpr int kMultiTileRows = 16;      // calibration rows per multi-layer tile
 constexpr int kMultiFlushTiles = 2046;  // at most 32,736 rows summed in fp32 before a flush (a multiple of 6)
 // Size of the fixed device array of the allocation-free blocked solve.

@@ -65,10 +65,17 @@ __device__ __forceinline__ void wave_sync_lds() {
     __builtin_amdgcn_wave_barrier();
 }
 
+// csums != nullptr: the centered form (Sec. 3.1, Eq. closedform as written).
+// G and C are then A [P][P] and B [P][d_t] of the feature x (no bias entry),
+// csums [n][1 + P + d_t] holds (sum w, sum w x, sum w y); every diagonal entry
+// gets lambda_m, lambda_m = lambda (tr A + S |mu_x|^2 + S) / (P + 1) when
+// relative (the trace of the augmented matrix of the same data), and each map
+// gets P + 1 rows: W, then the bias b = mu_y - W^T mu_x.
 __global__ __launch_bounds__(NT) void chol_solve_kernel(int32_t P, int32_t d_t, const float *__restrict__ G,
                                                         const float *__restrict__ C, float lambda, uint32_t flags,
                                                         double *__restrict__ ws, int64_t ws_stride, int32_t m0,
-                                                        float *__restrict__ maps, int32_t *__restrict__ info) {
+                                                        float *__restrict__ maps, int32_t *__restrict__ info,
+                                                        const double *__restrict__ csums) {
     __shared__ double sh[SH_WORK];
     __shared__ double sD[NB * DP];         // the diagonal block of the current panel
     __shared__ double sInv[NB];            // reciprocals of its diagonal
@@ -82,18 +89,25 @@ __global__ __launch_bounds__(NT) void chol_solve_kernel(int32_t P, int32_t d_t, 
     double *Z = L + (int64_t)P * P;
     const float *Gm = G + (int64_t)m * P * P;
     const float *Cm = C + (int64_t)m * P * d_t;
-    float *Wm = maps + (int64_t)m * P * d_t;
+    const int out_rows = csums ? P + 1 : P;
+    float *Wm = maps + (int64_t)m * out_rows * d_t;
+    const double *sm = csums ? csums + (int64_t)m * (1 + P + d_t) : nullptr;
+    const double sw = sm ? sm[0] : 0.0;
 
     // ---- lambda_m
     double tr = 0.0;
-    for (int i = tid; i < P; i += NT) tr += (double)Gm[(int64_t)i * P + i];
+    for (int i = tid; i < P; i += NT) {
+        tr += (double)Gm[(int64_t)i * P + i];
+        if (sm && sw != 0.0) tr += sm[1 + i] * (sm[1 + i] / sw);       // S mu_i^2
+    }
     for (int o = 32; o > 0; o >>= 1) tr += __shfl_xor(tr, o);
     if (lane == 0) red[wave] = tr;
     if (tid == 0) s_bad = 0;
     __syncthreads();
-    const double trace = (red[0] + red[1]) + (red[2] + red[3]);
-    const double lam = (flags & CB_LAMBDA_RELATIVE) ? (double)lambda * trace / (double)P : (double)lambda;
-    const int lam_last = (flags & CB_RIDGE_BIAS_UNPENALIZED) ? P - 1 : P;   // diagonal entries < lam_last get lambda
+    const double trace = (red[0] + red[1]) + (red[2] + red[3]) + sw;
+    const double lam = (flags & CB_LAMBDA_RELATIVE) ? (double)lambda * trace / (double)(sm ? P + 1 : P)
+                                                    : (double)lambda;
+    const int lam_last = (!sm && (flags & CB_RIDGE_BIAS_UNPENALIZED)) ? P - 1 : P;   // entries < lam_last get lambda
 
     // Loads the inverse V of the 32 x 32 diagonal block at (c0, c0) into sV
     // (lower triangular, zero outside the nb x nb block): its diagonal is
@@ -266,7 +280,7 @@ __global__ __launch_bounds__(NT) void chol_solve_kernel(int32_t P, int32_t d_t, 
     }
     if (s_bad) {
         if (tid == 0) info[m] = s_bad;
-        for (int64_t e = tid; e < (int64_t)P * d_t; e += NT) Wm[e] = 0.f;
+        for (int64_t e = tid; e < (int64_t)out_rows * d_t; e += NT) Wm[e] = 0.f;
         return;
     }
 
@@ -401,8 +415,16 @@ __global__ __launch_bounds__(NT) void chol_solve_kernel(int32_t P, int32_t d_t, 
         __syncthreads();
     }
 
-    // ================= 4. maps
+    // ================= 4. maps (and, centered, the bias row b = mu_y - W^T mu_x in fp64)
     for (int64_t e = tid; e < (int64_t)P * d_t; e += NT) Wm[e] = (float)Z[e];
+    if (sm) {
+        for (int c = tid; c < d_t; c += NT) {
+            double b = sw != 0.0 ? sm[1 + P + c] / sw : 0.0;
+            if (sw != 0.0)
+                for (int i = 0; i < P; ++i) b -= Z[(int64_t)i * d_t + c] * (sm[1 + i] / sw);
+            Wm[(int64_t)P * d_t + c] = (float)b;
+        }
+    }
     if (tid == 0) info[m] = 0;
 }
 
@@ -414,7 +436,7 @@ int64_t solve_blocked_bytes_per_system(int32_t P, int32_t d_t) {
 
 hipError_t launch_solve_blocked(int32_t n_maps, int32_t P, int32_t d_t, const float *G, const float *C, float lambda,
                                 uint32_t flags, void *ws, int64_t ws_bytes, float *maps, int32_t *info,
-                                hipStream_t s) {
+                                hipStream_t s, const double *csums) {
     if (n_maps == 0) return hipSuccess;
     if (d_t > DTMAX || P < 2) return hipErrorInvalidValue;
     const int64_t per = solve_blocked_bytes_per_system(P, d_t);
@@ -424,7 +446,7 @@ hipError_t launch_solve_blocked(int32_t n_maps, int32_t P, int32_t d_t, const fl
     for (int32_t m0 = 0; m0 < n_maps; m0 += (int32_t)std::min<int64_t>(batch, n_maps)) {
         const int32_t nb = (int32_t)std::min<int64_t>(batch, n_maps - m0);
         hipLaunchKernelGGL(chol_solve_kernel, dim3(nb), dim3(NT), 0, s, P, d_t, G, C, lambda, flags, (double *)ws,
-                           stride, m0, maps, info);
+                           stride, m0, maps, info, csums);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }

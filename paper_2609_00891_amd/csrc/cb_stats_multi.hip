@@ -56,7 +56,8 @@ struct MCfg {
     static constexpr int NST = 6;                  // ring stages (one per iteration of a loop trip)
     static constexpr int TRS = 33;                 // row stride (floats) of the transpose scratch
     static constexpr int OFF_T = NST * STAGE;
-    static constexpr int LDS = OFF_T + 4 * 32 * TRS * 4;
+    static constexpr int OFF_E = OFF_T + 4 * 32 * TRS * 4;  // centered: each wave's row sums e [2][32]
+    static constexpr int LDS = OFF_E + 4 * 2 * 32 * 4;
     static_assert(KT == 16, "one tile is one MFMA K step");
     static_assert(LDS <= 160 * 1024, "the ring must fit in LDS");
 };
@@ -157,7 +158,11 @@ __device__ __forceinline__ void flush_rows(const float *tr, int lane, int mode, 
 // of them is the target block (it is only ever the second column block).
 // YS: the task also owns sum w y of its map: wave w sums w y over 32 of the
 // target's channels.
-template <int NL, bool HASY, bool YS>
+// CENTER: moments about the map's weighted means (the paper's two-pass form):
+// the row operand is w (x - mu), the column operands stay the exact bf16 rows,
+// and every flush subtracts e mu^T with e = sum w (x - mu) as multiplied (hi +
+// lo); the outputs are A (ld P - 1) and B, with no bias row or column.
+template <int NL, bool HASY, bool YS, bool CENTER>
 __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &tk, const MultiCtx &c,
                                            lds_char_t *lds, int wave, int lane) {
     using K = MCfg;
@@ -232,8 +237,15 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
     for (int e = 0; e < E; ++e)
         coff[e] = (uint32_t)tk.col_slot[e >> 2] * K::BLK + lrow + 64u * ((uint32_t)(e & 3) ^ (uint32_t)kk);
     const uint32_t lw = K::OFF_W + (lane >> 5) * 32;
-    const bool own_sumx = (tk.flags >> rs) & 1;
-    const bool own_sumw = (tk.flags & 4) && wave == 0;
+    const bool own_sumx = !CENTER && ((tk.flags >> rs) & 1);
+    const bool own_sumw = !CENTER && (tk.flags & 4) && wave == 0;
+    // centered: the weighted means of the map (fp64 sums of pass 1)
+    const double *sm = CENTER ? a.sums + (int64_t)tk.map * (a.P + a.d_t) : nullptr;
+    const double s_w = CENTER ? sm[0] : 0.0;
+    auto mean_of = [&](int ch) { return (CENTER && s_w != 0.0) ? (float)(sm[1 + ch] / s_w) : 0.f; };
+    float mu_row[2];
+#pragma unroll
+    for (int r = 0; r < 2; ++r) mu_row[r] = mean_of(32 * (4 * tk.rows[rs] + 2 * half + r) + (lane & 31));
     // the target block is column block 1 of a YS task: wave w sums w y over its window w
     auto ycol = [&](int e) { return YS && e == 4 + wave; };
 
@@ -274,8 +286,13 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
         float av[8];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            av[2 * e] = o.w[2 * e] * bf_lo(xv[e]);
-            av[2 * e + 1] = o.w[2 * e + 1] * bf_hi(xv[e]);
+            if constexpr (CENTER) {
+                av[2 * e] = o.w[2 * e] * (bf_lo(xv[e]) - mu_row[r]);
+                av[2 * e + 1] = o.w[2 * e + 1] * (bf_hi(xv[e]) - mu_row[r]);
+            } else {
+                av[2 * e] = o.w[2 * e] * bf_lo(xv[e]);
+                av[2 * e + 1] = o.w[2 * e + 1] * bf_hi(xv[e]);
+            }
         }
         uint32_t hv[4], lv[4];
 #pragma unroll
@@ -283,12 +300,21 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
             hv[e] = pack_bf16(av[2 * e], av[2 * e + 1]);
             lv[e] = pack_bf16(av[2 * e] - bf_lo(hv[e]), av[2 * e + 1] - bf_hi(hv[e]));
         }
-        sumx[r] += ((av[0] + av[1]) + (av[2] + av[3])) + ((av[4] + av[5]) + (av[6] + av[7]));
+        if constexpr (CENTER) {
+            // e = sum of the folded operand exactly as multiplied (hi + lo)
+            float q[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) q[e] = (bf_lo(hv[e]) + bf_lo(lv[e])) + (bf_hi(hv[e]) + bf_hi(lv[e]));
+            sumx[r] += (q[0] + q[1]) + (q[2] + q[3]);
+        } else {
+            sumx[r] += ((av[0] + av[1]) + (av[2] + av[3])) + ((av[4] + av[5]) + (av[6] + av[7]));
+        }
         f.hi[r] = __builtin_bit_cast(bf16x8_t, make_uint4(hv[0], hv[1], hv[2], hv[3]));
         f.lo[r] = __builtin_bit_cast(bf16x8_t, make_uint4(lv[0], lv[1], lv[2], lv[3]));
     };
     auto sum_w = [&](const Ops &o) {
-        sumw += ((o.w[0] + o.w[1]) + (o.w[2] + o.w[3])) + ((o.w[4] + o.w[5]) + (o.w[6] + o.w[7]));
+        if constexpr (!CENTER)
+            sumw += ((o.w[0] + o.w[1]) + (o.w[2] + o.w[3])) + ((o.w[4] + o.w[5]) + (o.w[6] + o.w[7]));
     };
     auto sum_y = [&](const Ops &o) {
         // entry 4 + wave: selected with a uniform switch-free blend of the four candidates
@@ -328,11 +354,20 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
 
     // ---- flush: add the wave's tiles (and bias sums) into G and C
     float *tr = (float *)(lds + K::OFF_T) + wave * 32 * K::TRS;
-    float *Gm = a.G + (int64_t)tk.map * a.P * a.P;
-    float *Cm = a.C + (int64_t)tk.map * a.P * a.d_t;
-    const int P = a.P;
+    float *es = (float *)(lds + K::OFF_E) + wave * 64;       // centered: e of the wave's 2 x 32 rows
+    const int P = CENTER ? a.P - 1 : a.P;                    // leading dimension of G (or A)
+    float *Gm = a.G + (int64_t)tk.map * P * P;
+    float *Cm = a.C + (int64_t)tk.map * P * a.d_t;
     auto flush = [&]() {
         const int rb = tk.rows[rs];                          // feature block of this wave's rows
+        if constexpr (CENTER) {
+#pragma unroll
+            for (int r = 0; r < 2; ++r) {
+                const float ex = sumx[r] + __shfl_xor(sumx[r], 32);
+                if (lane < 32) es[32 * r + lane] = ex;
+            }
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        }
 #pragma unroll
         for (int r = 0; r < 2; ++r) {
             const int R = 4 * rb + 2 * half + r;             // 32-row block of G
@@ -345,10 +380,13 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
                 const int Cc = 4 * col + win;                // 32-column block (of G, or of C if is_y)
                 if (!is_y && col == rb && Cc < R) continue;  // below the diagonal of a diagonal block
                 const f32x16_t &t = acc[r * E + e];
+                // centered: minus e_i mu_j, mu_j the mean of this lane's column
+                const float muc = CENTER ? mean_of(is_y ? 128 * a.k + 32 * win + (lane & 31) : 32 * Cc + (lane & 31))
+                                         : 0.f;
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {
                     const int i = 8 * (v >> 2) + (v & 3) + 4 * (lane >> 5);
-                    tr[i * K::TRS + (lane & 31)] = t[v];
+                    tr[i * K::TRS + (lane & 31)] = CENTER ? t[v] - es[32 * r + i] * muc : t[v];
                 }
                 asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
                 // mode 0: cross tile of C; 1: diagonal tile of G; 2: any other tile of G (+ its mirror)
@@ -359,6 +397,11 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
                 const int64_t ld = is_y ? a.d_t : P;
                 flush_rows(tr, lane, mode, dst, mir, ld);
             }
+        }
+        if constexpr (CENTER) {
+            sumx[0] = sumx[1] = 0.f;
+            zero_acc();
+            return;
         }
         // bias row / column: lanes l and l + 32 hold the two halves of each K step
         if (own_sumx) {
@@ -472,6 +515,7 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
     wait_vm<0>();                                            // drain the trailing copies
 }
 
+template <bool CENTER>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
 void stats_multi_kernel(MultiArgs a) {
     using K = MCfg;
@@ -495,15 +539,64 @@ void stats_multi_kernel(MultiArgs a) {
     }
     // variant: staged blocks (1..4), target block staged (HASY), sum w y owned (YS)
     const bool hasy = tk.slot_layer[tk.n_lds - 1] < 0;
-    const int var = (tk.n_lds - 1) * 3 + (hasy ? ((tk.flags & 8) ? 2 : 1) : 0);
+    const int var = (tk.n_lds - 1) * 3 + (hasy ? ((!CENTER && (tk.flags & 8)) ? 2 : 1) : 0);
     switch (var) {
-#define CB_V(NL_)                                                                   \
-        case (NL_ - 1) * 3 + 0: multi_wave<NL_, false, false>(a, tk, c, lds, wave, lane); break; \
-        case (NL_ - 1) * 3 + 1: multi_wave<NL_, true, false>(a, tk, c, lds, wave, lane); break;  \
-        case (NL_ - 1) * 3 + 2: multi_wave<NL_, true, true>(a, tk, c, lds, wave, lane); break;
+#define CB_V(NL_)                                                                                  \
+        case (NL_ - 1) * 3 + 0: multi_wave<NL_, false, false, CENTER>(a, tk, c, lds, wave, lane); break; \
+        case (NL_ - 1) * 3 + 1: multi_wave<NL_, true, false, CENTER>(a, tk, c, lds, wave, lane); break;  \
+        case (NL_ - 1) * 3 + 2:                                                                     \
+            if constexpr (!CENTER) multi_wave<NL_, true, true, false>(a, tk, c, lds, wave, lane);    \
+            break;
         CB_V(1) CB_V(2) CB_V(3) CB_V(4)
 #undef CB_V
         default: break;
+    }
+}
+
+// Pass 1 of the centered form: one workgroup per (map, feature block), 16
+// threads per row (16-byte chunks), 16 rows at a time; fp64 sums of w x (and
+// of w on the target block), each thread's 8 channels over its rows, then a
+// fixed-order sum over the 16 row groups through LDS, added into sums.
+__global__ __launch_bounds__(256) void means_multi_kernel(MeansMultiArgs a) {
+    __shared__ double red[16][16][9];
+    const int m = blockIdx.x / (a.k + 1), blk = blockIdx.x % (a.k + 1);
+    const int tid = threadIdx.x, ch = tid & 15, rg = tid >> 4;
+    const ApplyMultiMap mp = a.maps[m];
+    const bool tgt = blk == a.k;
+    const uint16_t *base = tgt ? a.tgt + mp.tgt_layer * a.ts.layer + mp.kv * a.ts.kv + mp.tgt_head * a.ts.head
+                               : a.src + a.layers[(int64_t)m * a.k + blk] * a.ss.layer + mp.kv * a.ss.kv +
+                                     mp.src_head * a.ss.head;
+    const int64_t s_seq = tgt ? a.ts.seq : a.ss.seq, s_tok = tgt ? a.ts.tok : a.ss.tok;
+    const float *wr = a.w + (int64_t)a.wrow[m] * a.w_row_stride;
+    double acc[8] = {0, 0, 0, 0, 0, 0, 0, 0}, accw = 0.0;
+    for (int b = 0; b < a.n_seqs; ++b) {
+        const uint16_t *rowb = base + (int64_t)b * s_seq + ch * 8;
+        const float *wb = wr + (int64_t)b * a.seq_len;
+#pragma unroll 4
+        for (int r = rg; r < a.rows_per_seq; r += 16) {
+            const int tok = r * a.stride;
+            const uint4 v = *(const uint4 *)(rowb + (int64_t)tok * s_tok);
+            const double w = (double)wb[tok];
+            const uint32_t u[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                acc[2 * e] += w * (double)bf_lo(u[e]);
+                acc[2 * e + 1] += w * (double)bf_hi(u[e]);
+            }
+            accw += w;
+        }
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) red[rg][ch][e] = acc[e];
+    red[rg][ch][8] = accw;
+    __syncthreads();
+    if (tid < 16 * 9) {
+        const int c = tid / 9, e = tid % 9;
+        double s = 0.0;
+        for (int g = 0; g < 16; ++g) s += red[g][c][e];
+        double *out = a.sums + (int64_t)m * (1 + 128 * a.k + a.d_t);
+        if (e < 8) out[1 + 128 * blk + 8 * c + e] += s;
+        else if (tgt && c == 0) out[0] += s;
     }
 }
 
@@ -511,7 +604,19 @@ void stats_multi_kernel(MultiArgs a) {
 
 hipError_t launch_stats_multi(const MultiArgs &a, hipStream_t s) {
     if (a.n_tasks == 0 || a.n_tiles == 0) return hipSuccess;
-    hipLaunchKernelGGL(stats_multi_kernel, dim3(8 * a.per_xcd), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(stats_multi_kernel<false>, dim3(8 * a.per_xcd), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_stats_multi_centered(const MultiArgs &a, hipStream_t s) {
+    if (a.n_tasks == 0 || a.n_tiles == 0) return hipSuccess;
+    hipLaunchKernelGGL(stats_multi_kernel<true>, dim3(8 * a.per_xcd), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_means_multi(const MeansMultiArgs &a, hipStream_t s) {
+    if (a.n_maps == 0 || a.n_seqs == 0 || a.rows_per_seq == 0) return hipSuccess;
+    hipLaunchKernelGGL(means_multi_kernel, dim3((unsigned)(a.n_maps * (a.k + 1))), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 

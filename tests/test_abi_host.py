@@ -240,3 +240,44 @@ def test_noalloc_solve_rejects_systems_beyond_its_scratch_before_any_launch():
     assert cb.cb_status_string(rc) == "CB_ERR_UNSUPPORTED"
     rc = lib.cb_ridge_solve_noalloc(1, 1025, 128, None, fake, ctypes.c_float(1e-2), 1, fake, fake, None)
     assert cb.cb_status_string(rc) == "CB_ERR_INVALID_ARGUMENT"
+
+
+def test_centered_wide_solve_rejects_bad_arguments_on_the_host():
+    import paper_2609_00891_amd as cb
+    lib = cb.library()
+    f = ctypes.c_float
+    sv = lib.cb_ridge_solve_centered_ws
+    fake = ctypes.c_void_p(256)
+    assert sv(4, 1024, 128, None, None, None, f(0.1), 1, None, 0, None, None, None) == 1      # NULL pointers
+    assert sv(4, 5000, 128, fake, fake, fake, f(0.1), 1, fake, 1 << 40, fake, fake, None) == 6   # d_x too wide
+    assert sv(4, 1024, 100, fake, fake, fake, f(0.1), 1, fake, 1 << 40, fake, fake, None) == 6   # d_t
+    assert sv(4, 1024, 128, fake, fake, fake, f(-1.0), 1, fake, 1 << 40, fake, fake, None) == 1  # lambda < 0
+    assert sv(4, 1024, 128, fake, fake, fake, f(0.1), 4, fake, 1 << 40, fake, fake, None) == 1   # unknown flag
+    assert sv(4, 1024, 128, fake, fake, fake, f(0.1), 1, fake, 1024, fake, fake, None) == 2      # workspace too small
+    assert sv(0, 1024, 128, None, None, None, f(0.1), 1, None, 0, None, None, None) == 0
+
+
+def test_bindings_check_output_sizes_against_the_plan():
+    # the C ABI takes bare pointers; the binding refuses tensors that do not hold
+    # what the plan's kernels write or read, before any call into the library
+    import torch
+    import paper_2609_00891_amd as cb
+    keep = [np.zeros(4, np.int32)] * 5 + [np.arange(4, dtype=np.int32)]
+    plan = cb.Plan(None, 4, 128, 128, keep, P=385, k=3)
+    z32 = lambda *s: torch.zeros(s, dtype=torch.float32)           # noqa: E731
+    z64 = lambda *s: torch.zeros(s, dtype=torch.float64)           # noqa: E731
+    src = torch.zeros((4, 2, 2, 1, 8, 128), dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="sums"):
+        cb.cb_stats_zero_centered(plan, z64(4, 257), z32(4, 384, 384), z32(4, 384, 128))
+    with pytest.raises(ValueError, match="A"):
+        cb.cb_stats_zero_centered(plan, z64(4, 513), z32(4, 128, 128), z32(4, 384, 128))
+    with pytest.raises(ValueError, match="G"):
+        cb.cb_stats_zero(plan, z32(4, 129, 129), z32(4, 385, 128))
+    with pytest.raises(ValueError, match="maps"):
+        cb.cb_apply(plan, z32(4, 129, 128), src, src)
+    with pytest.raises(ValueError, match="weights"):
+        cb.cb_stats_means(plan, src, src, z32(3, 16), z64(4, 513))                  # 3 rows, the map reads 4
+    with pytest.raises(ValueError, match="weights"):
+        cb.cb_stats_means(plan, src, src, z32(4, 16)[:, 1:], z64(4, 513), w_row_stride=16)    # 63 < 64 values
+    with pytest.raises(ValueError, match="weights"):
+        cb.cb_stats_means(plan, src, src, z32(16, 4).t(), z64(4, 513), w_row_stride=16)   # strided rows

@@ -318,9 +318,17 @@ def test_multi_device_side_argument_errors(cb):
         cb.cb_apply(plan, C, src, tgt[:1])                               # wrong target layer count
     with pytest.raises(cb.CacheBridgeError, match="CB_ERR_SHAPE"):
         cb.cb_apply(plan, C, src[:, :, :, :, :16], tgt)                  # token counts disagree
+    # outputs the plan does not fit are refused before any launch: the centered
+    # sums of a k = 2 plan are [n][1 + 256 + 128], not the single-layer [n][257]
     sums = torch.zeros((n, 257), dtype=torch.float64, device="cuda")
-    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_UNSUPPORTED"):
+    with pytest.raises(ValueError, match="sums"):
         cb.cb_stats_means(plan, src, tgt, w, sums)
+    with pytest.raises(ValueError, match="G"):
+        cb.cb_stats_accumulate(plan, src, tgt, w, G[:, :-1], C)
+    with pytest.raises(ValueError, match="maps"):
+        cb.cb_apply(plan, C[:1], src, tgt)
+    with pytest.raises(ValueError, match="weights"):
+        cb.cb_stats_accumulate(plan, src, tgt, w[:1], G, C)
     maps = torch.empty_like(C)
     info = torch.empty((n,), dtype=torch.int32, device="cuda")
     small = torch.empty((1024,), dtype=torch.uint8, device="cuda")
@@ -540,4 +548,222 @@ def test_multi_plan_rejects_fused_rotary_apply(cb):
         cb.cb_apply_rope(plan, maps, src, out, table)
     torch.cuda.synchronize()
     assert not out.view(torch.int16).any()
+    plan.close()
+
+
+# ----------------------------------------------------------------------------- two-pass centered form, k > 1
+
+TOL_SUMS = 1e-9        # fp64 sums of exact fp64 products: only the summation order differs
+
+
+def gpu_centered_multi(cb, plan, batches):
+    """Pass 1 (means) over every batch, then pass 2 (centered moments) over every batch."""
+    n, Dx, dt = plan.n_maps, plan.P - 1, plan.d_t
+    sums = torch.empty((n, 1 + Dx + dt), dtype=torch.float64, device="cuda")
+    A = torch.empty((n, Dx, Dx), dtype=torch.float32, device="cuda")
+    B = torch.empty((n, Dx, dt), dtype=torch.float32, device="cuda")
+    cb.cb_stats_zero_centered(plan, sums, A, B)
+    for s, t, w in batches:
+        cb.cb_stats_means(plan, s, t, w, sums)
+    for s, t, w in batches:
+        cb.cb_stats_accumulate_centered(plan, s, t, w, sums, A, B)
+    torch.cuda.synchronize()
+    return sums, A, B
+
+
+def gpu_solve_centered_ws(cb, sums, A, B, lam=1e-2, flags=None):
+    if flags is None:
+        flags = cb.CB_LAMBDA_RELATIVE
+    n, Dx, _ = A.shape
+    dt = B.shape[2]
+    maps = torch.empty((n, Dx + 1, dt), dtype=torch.float32, device="cuda")
+    info = torch.empty((n,), dtype=torch.int32, device="cuda")
+    per = cb.cb_ridge_solve_workspace_bytes(Dx, dt, 1)
+    nsys = max(1, min(n, (8 << 30) // max(per, 1)))
+    ws = torch.empty((max(per * nsys, 8),), dtype=torch.uint8, device="cuda")
+    cb.cb_ridge_solve_centered_ws(sums, A, B, lam, flags, maps, info, ws)
+    torch.cuda.synchronize()
+    return maps, info
+
+
+def oracle_centered_full(hm, src, tgt, w, stride):
+    sb, tb = bits(src), bits(tgt)
+    L_s, _, Bn, H_s, T, d_s = src.shape
+    L_t, _, _, H_t, _, d_t = tgt.shape
+    return oracle.stats_multi_centered(hm, sb, synth.cache_strides(L_s, H_s, Bn, T, d_s), d_s, tb,
+                                       synth.cache_strides(L_t, H_t, Bn, T, d_t), d_t, w.cpu().numpy(), Bn * T, Bn,
+                                       T, stride, n_threads=NTHREADS)
+
+
+def check_centered_multi(cb, sums, A, B, so, Ao, Bo, sel, label=""):
+    """Sums to 1e-9, A and B to the stats bar, A exactly symmetric; then the solve
+    end to end and alone (both sides on the oracle's moments rounded to fp32)."""
+    idx = torch.as_tensor(np.asarray(sel), device=A.device)
+    sg = sums[idx].cpu().numpy()
+    Ag = A[idx].double().cpu().numpy()
+    Bg = B[idx].double().cpu().numpy()
+    es = max(relF(sg[i], so[i]) for i in range(len(sel)))
+    ea = max(relF(Ag[i], Ao[i]) for i in range(len(sel)))
+    eb = max(relF(Bg[i], Bo[i]) for i in range(len(sel)))
+    say(f"  centered{label}: sums {es:.3e}, A {ea:.3e}, B {eb:.3e}")
+    assert es <= TOL_SUMS and ea <= TOL_STATS and eb <= TOL_STATS
+    assert np.array_equal(Ag, np.transpose(Ag, (0, 2, 1))), "A must be exactly symmetric"
+    Wo, io = oracle.ridge_solve_centered(so, Ao, Bo, 1e-2, relative=True, n_threads=NTHREADS)
+    assert (io == 0).all()
+    return Wo
+
+
+@pytest.mark.parametrize("offset", [False, True])
+def test_multi_centered_tiny_k3_end_to_end(cb, offset):
+    # tiny_k3 (k = 3, P = 385, every fourth token), streamed in two batches; with
+    # `offset` the source channels carry means far above their spread
+    wl = synth.WORKLOADS["tiny_k3"]
+    if offset:
+        wl = wl.with_(source_kind="offset")
+    src = synth.gen_source(wl, device="cuda")
+    tgt = synth.gen_target(wl, src, device="cuda")
+    w = synth.gen_weights(wl, device="cuda")
+    hm = synth.head_map_multi(wl)
+    plan = cb.cb_plan_create_multi(hm, src, tgt, wl.sample_stride)
+    B_ = wl.n_seqs
+    T = wl.seq_len
+    batches = [(src[:, :, a:b], tgt[:, :, a:b], w.reshape(-1, B_, T)[:, a:b].reshape(w.shape[0], -1))
+               for a, b in ((0, 1), (1, B_))]
+    sums, A, B = gpu_centered_multi(cb, plan, batches)
+    so, Ao, Bo = oracle_centered_full(hm, src, tgt, w, wl.sample_stride)
+    sel = list(range(plan.n_maps))
+    Wo = check_centered_multi(cb, sums, A, B, so, Ao, Bo, sel, " (tiny_k3, offset)" if offset else " (tiny_k3)")
+    maps, info = gpu_solve_centered_ws(cb, sums, A, B)
+    assert int((info != 0).sum()) == 0
+    e2e = max(relF(maps[m].double().cpu().numpy(), Wo[m]) for m in sel)
+    # the solver alone: the oracle's sums, A, B (A, B rounded once to fp32) on both sides
+    (At, A64), (Bt, B64) = shared_f32(Ao), shared_f32(Bo)
+    st = torch.from_numpy(np.ascontiguousarray(so)).to("cuda")
+    ms, inf2 = gpu_solve_centered_ws(cb, st, At, Bt)
+    Ws, _ = oracle.ridge_solve_centered(so, A64, B64, 1e-2, relative=True, n_threads=NTHREADS)
+    alone = max(relF(ms[m].double().cpu().numpy(), Ws[m]) for m in sel)
+    say(f"  centered solve: maps end-to-end {e2e:.3e}, solver alone {alone:.3e}")
+    assert e2e <= TOL_MAPS and alone <= TOL_SOLVER and int((inf2 != 0).sum()) == 0
+    if not offset:
+        # the same problem as the unpenalized augmented ridge of the one-pass moments (Schur complement)
+        G, C = gpu_stats(cb, plan, [(src, tgt, w)])
+        mu, _ = gpu_solve_ws(cb, G, C, 1e-2, cb.CB_LAMBDA_RELATIVE | cb.CB_RIDGE_BIAS_UNPENALIZED)
+        d = max(relF(maps[m].double().cpu().numpy(), mu[m].double().cpu().numpy()) for m in sel)
+        say(f"  centered maps vs unpenalized augmented maps: {d:.3e}")
+        assert d <= TOL_MAPS
+    plan.close()
+
+
+@pytest.mark.parametrize("k,stride,T", [(2, 3, 520), (5, 2, 858)])
+def test_multi_centered_widths_ragged_offset_and_uncentered_gap(cb, k, stride, T):
+    # large channel means (the purpose of the centered form): the centered A is
+    # within the bar, while A recovered from the one-pass uncentered moments of
+    # the same data is far worse
+    rng = np.random.default_rng(3000 + 10 * k + stride)
+    L_s, H_s, L_t, H_t, B_ = 6, 2, 2, 2, 3
+    src, tgt, w = small_inputs(rng, L_s, H_s, L_t, H_t, B_, T)
+    g = torch.Generator(device="cpu")
+    g.manual_seed(77 + k)
+    mu = (40.0 * torch.randn((L_s, 2, 1, H_s, 1, 128), generator=g)).to("cuda")
+    src = (src.float() + mu).to(torch.bfloat16)
+    hm = random_multi_map(rng, k, L_s, H_s, L_t, H_t)
+    plan = cb.cb_plan_create_multi(hm, src, tgt, stride)
+    cuts = [(0, 1), (1, 1), (1, 3)]
+    batches = [(src[:, :, a:b], tgt[:, :, a:b], w.reshape(-1, B_, T)[:, a:b].reshape(w.shape[0], -1))
+               for a, b in cuts]
+    sums, A, B = gpu_centered_multi(cb, plan, batches)
+    so, Ao, Bo = oracle_centered_full(hm, src, tgt, w, stride)
+    sel = list(range(plan.n_maps))
+    check_centered_multi(cb, sums, A, B, so, Ao, Bo, sel, f" (k={k}, stride {stride}, offset means)")
+    # A from the uncentered G: G_xx - s s^T / S
+    G, C = gpu_stats(cb, plan, [(src, tgt, w)])
+    Gd = G.double().cpu().numpy()
+    P = plan.P
+    gap = []
+    for m in sel:
+        s_ = Gd[m, :P - 1, P - 1]
+        Au = Gd[m, :P - 1, :P - 1] - np.outer(s_, s_) / Gd[m, P - 1, P - 1]
+        gap.append(relF(Au, Ao[m]))
+    ea = max(relF(A[m].double().cpu().numpy(), Ao[m]) for m in sel)
+    say(f"  A from the uncentered moments: {max(gap):.3e} (centered {ea:.3e})")
+    assert max(gap) >= 10 * ea
+    maps, info = gpu_solve_centered_ws(cb, sums, A, B)
+    assert int((info != 0).sum()) == 0
+    plan.close()
+
+
+def test_multi_centered_zero_weights_and_determinism(cb):
+    rng = np.random.default_rng(41)
+    k, stride, L_s, H_s, L_t, H_t, B_, T = 3, 4, 5, 2, 2, 2, 2, 600
+    src, tgt, w = small_inputs(rng, L_s, H_s, L_t, H_t, B_, T)
+    w[1] = 0.0                                           # maps of weight row 1 see no weight
+    hm = random_multi_map(rng, k, L_s, H_s, L_t, H_t)
+    plan = cb.cb_plan_create_multi(hm, src, tgt, stride)
+    s1, A1, B1 = gpu_centered_multi(cb, plan, [(src, tgt, w)])
+    s2, A2, B2 = gpu_centered_multi(cb, plan, [(src, tgt, w)])
+    assert torch.equal(s1, s2) and torch.equal(A1, A2) and torch.equal(B1, B2)
+    zero = [m for m in range(plan.n_maps) if int(hm["weight_row"][m]) == 1]
+    assert zero
+    for m in zero:
+        assert not s1[m].any() and not A1[m].any() and not B1[m].any()
+    # empty call: nothing changes
+    cb.cb_stats_means(plan, src[:, :, :0], tgt[:, :, :0], w[:, :0], s1)
+    cb.cb_stats_accumulate_centered(plan, src[:, :, :0], tgt[:, :, :0], w[:, :0], s1, A1, B1)
+    torch.cuda.synchronize()
+    assert torch.equal(s1, s2) and torch.equal(A1, A2)
+    maps, info = gpu_solve_centered_ws(cb, s1, A1, B1, 0.5, 0)          # absolute lambda: W = 0, b = 0
+    for m in zero:
+        assert int(info[m]) == 0 and not maps[m].any()
+    plan.close()
+
+
+def compact_multi_centered(hm, sel, src, tgt, w, stride):
+    """Oracle centered moments of the maps `sel` on host copies of only their sampled rows."""
+    k = hm["src_layers"].shape[1]
+    B_, T = src.shape[2], src.shape[4]
+    xs, ys, ws = [], [], []
+    for m in sel:
+        z, a = int(hm["kv"][m]), int(hm["src_head"][m])
+        for j in hm["src_layers"][m]:
+            xs.append(src[int(j), z, :, a, ::stride])
+        ys.append(tgt[int(hm["tgt_layer"][m]), z, :, int(hm["tgt_head"][m]), ::stride])
+        ws.append(w[int(hm["weight_row"][m])].reshape(B_, T)[:, ::stride].reshape(-1))
+    n, Ts = len(sel), xs[0].shape[1]
+    d_s, d_t = xs[0].shape[-1], ys[0].shape[-1]
+    xb = bits(torch.stack(xs)).reshape(n * k, 1, B_, 1, Ts, d_s)
+    yb = bits(torch.stack(ys)).reshape(n, 1, B_, 1, Ts, d_t)
+    wb = torch.stack(ws).cpu().numpy()
+    chm = {"tgt_layer": np.arange(n, dtype=np.int32), "tgt_head": np.zeros(n, np.int32),
+           "kv": np.zeros(n, np.int32), "src_layers": np.arange(n * k, dtype=np.int32).reshape(n, k),
+           "src_head": np.zeros(n, np.int32), "weight_row": np.arange(n, dtype=np.int32)}
+    ss = (B_ * Ts * d_s, 0, Ts * d_s, 0, d_s)
+    ts = (B_ * Ts * d_t, 0, Ts * d_t, 0, d_t)
+    return oracle.stats_multi_centered(chm, xb, ss, d_s, yb, ts, d_t, np.ascontiguousarray(wb), B_ * Ts, B_, Ts, 1,
+                                       n_threads=NTHREADS)
+
+
+def test_multi_centered_qwen_k8_batch_full_size_sampled_maps(cb):
+    """The k = 8 construction's resident batch (100 x 1,024 tokens, every fourth),
+    both centered passes as the benchmark launches them; four sampled maps against
+    the oracle, all 1,024 centered systems solved."""
+    wl = synth.WORKLOADS["qwen_k8"]
+    bw = wl.with_(n_seqs=wl.batch_seqs)
+    say(f"multi centered qwen_k8 batch: {bw.n_seqs} x {bw.seq_len} tokens, stride {bw.sample_stride}")
+    src = synth.gen_source(bw, device="cuda")
+    tgt = synth.gen_target(bw, src, device="cuda")
+    w = synth.gen_weights(bw, device="cuda", chunk=50)
+    hm = synth.head_map_multi(wl)
+    plan = cb.cb_plan_create_multi(hm, src, tgt, wl.sample_stride)
+    sums, A, B = gpu_centered_multi(cb, plan, [(src, tgt, w)])
+    sel = [0, 300, 777, 1023]
+    say("  oracle on the sampled maps ...")
+    so, Ao, Bo = compact_multi_centered(hm, sel, src, tgt, w, wl.sample_stride)
+    del src, tgt
+    torch.cuda.empty_cache()
+    Wo = check_centered_multi(cb, sums, A, B, so, Ao, Bo, sel, " (qwen_k8 batch)")
+    maps, info = gpu_solve_centered_ws(cb, sums, A, B)
+    assert int((info != 0).sum()) == 0
+    e2e = max(relF(maps[m].double().cpu().numpy(), Wo[i]) for i, m in enumerate(sel))
+    say(f"  centered maps end-to-end {e2e:.3e}")
+    assert e2e <= TOL_MAPS
     plan.close()
