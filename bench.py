@@ -630,8 +630,51 @@ def multi_leg(cb, synth, steps):
     flop_per_row = 2 * n * (P * P + P * d_t)                  # dense P x P Gram, algorithmic
     tflops = flop_per_row * rows_per_call / (call_ms / 1e3) / 1e12
     bad = int((info != 0).sum().item())
+    # the same build in the two-pass centered form (Sec. 3.4): means over the
+    # five calls, centered moments over the five calls, centered blocked solve
+    Dx = P - 1
+    del G, C
+    torch.cuda.empty_cache()
+    sums = torch.empty((n, 1 + Dx + d_t), dtype=torch.float64, device="cuda")
+    A = torch.empty((n, Dx, Dx), dtype=torch.float32, device="cuda")
+    Bc = torch.empty((n, Dx, d_t), dtype=torch.float32, device="cuda")
+    cmaps = torch.empty_like(maps)
+    cinfo = torch.empty_like(info)
+    crecs = []
+    for it in range(steps + 1):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(2 * n_calls + 3)]
+        e[0].record(stream)
+        cb.cb_stats_zero_centered(plan, sums, A, Bc)
+        e[1].record(stream)
+        for i in range(n_calls):
+            cb.cb_stats_means(plan, src, tgt, w, sums)
+            e[2 + i].record(stream)
+        for i in range(n_calls):
+            cb.cb_stats_accumulate_centered(plan, src, tgt, w, sums, A, Bc)
+            e[2 + n_calls + i].record(stream)
+        cb.cb_ridge_solve_centered_ws(sums, A, Bc, wl.lam_rel, cb.CB_LAMBDA_RELATIVE, cmaps, cinfo, ws)
+        e[2 * n_calls + 2].record(stream)
+        if it > 0:
+            crecs.append(e)
+    torch.cuda.synchronize()
+    c_means_ms = mean([e[1 + i].elapsed_time(e[2 + i]) for e in crecs for i in range(n_calls)])
+    c_call_ms = mean([e[1 + n_calls + i].elapsed_time(e[2 + n_calls + i]) for e in crecs for i in range(n_calls)])
+    c_solve_ms = mean([e[2 * n_calls + 1].elapsed_time(e[2 * n_calls + 2]) for e in crecs])
+    c_build_ms = mean([e[0].elapsed_time(e[2 * n_calls + 2]) for e in crecs])
+    # the centered maps solve the unpenalized-bias augmented problem of the same data
+    cdiff = max(relF(cmaps[m].double().cpu().numpy(), maps[m].double().cpu().numpy()) for m in (0, 511, 1023))
+    cbad = int((cinfo != 0).sum().item())
+    c_tflops = flop_per_row * rows_per_call / (c_call_ms / 1e3) / 1e12
+    centered = {
+        "s_per_500seq_build": c_build_ms / 1e3,
+        "legs_ms": {"means_call": c_means_ms, "centered_stats_call": c_call_ms, "solve": c_solve_ms},
+        "stats_call_TFLOPs": c_tflops,
+        "maps_relF_vs_unpenalized_augmented_form": float(cdiff),
+        "nonpositive_pivots": cbad,
+    }
+    del sums, A, Bc, cmaps, cinfo
     # online application of the fitted maps to the resident sender batch
-    del tgt, w, G, C, ws
+    del tgt, w, ws
     torch.cuda.empty_cache()
     out = torch.empty((wl.L_t, 2, B, wl.H_t, wl.seq_len, d_t), dtype=torch.bfloat16, device="cuda")
     ea = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 2)]
@@ -660,6 +703,7 @@ def multi_leg(cb, synth, steps):
                      "peak": 2500.0, "unit": "TFLOP/s", "frac": tflops / 2500.0,
                      "algorithmic_flops_per_launch": flop_per_row * rows_per_call},
         "nonpositive_pivots": bad,
+        "centered_two_pass": centered,
     }
 
 
