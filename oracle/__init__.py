@@ -116,6 +116,10 @@ def _load():
     lib.oracle_apply_multi.argtypes = [ctypes.c_int, ctypes.c_int] + [_i32p] * 5 + [
         _f64p, _u16p, _i64p, ctypes.c_int, _u16p, _i64p, ctypes.c_int,
         ctypes.c_int, ctypes.c_int, ctypes.c_int]
+    lib.oracle_apply_multi_rope.restype = ctypes.c_int
+    lib.oracle_apply_multi_rope.argtypes = [ctypes.c_int, ctypes.c_int] + [_i32p] * 5 + [
+        _f64p, _u16p, _i64p, ctypes.c_int, _u16p, _i64p, ctypes.c_int,
+        ctypes.c_int, ctypes.c_int, ctypes.c_double, ctypes.c_int, ctypes.c_int, ctypes.c_int]
     lib.oracle_double_to_bf16_array.restype = ctypes.c_int
     lib.oracle_double_to_bf16_array.argtypes = [ctypes.c_int64, _f64p, _u16p]
     _lib = lib
@@ -488,4 +492,22 @@ def apply_multi(head_map, W, src, src_strides, d_s, out, out_strides, d_t, n_seq
     lib.oracle_apply_multi(n, k, *[_ptr(a, _i32p) for a in hm], _ptr(W, _f64p), _ptr(src, _u16p),
                            _ptr(ss, _i64p), d_s, _ptr(out, _u16p), _ptr(os_, _i64p), d_t,
                            int(n_seqs), int(seq_len), int(n_threads))
+    return out
+
+
+def apply_multi_rope(head_map, W, src, src_strides, d_s, out, out_strides, d_t, n_seqs, seq_len, theta: float,
+                     style: int = 0, pos_offset: int = 0, n_threads: int = 0):
+    """Like :func:`apply_multi`, with the K outputs turned by the target RoPE (fp64) before the one rounding."""
+    lib = _load()
+    n, k, hm = _multi_arrays(head_map, MULTI_MAP_FIELDS[:5])
+    W = np.ascontiguousarray(np.asarray(W, dtype=np.float64))
+    assert W.shape == (n, k * d_s + 1, d_t)
+    src = np.ascontiguousarray(_u16(src))
+    if not (out.dtype == np.uint16 and out.flags.c_contiguous):
+        raise TypeError("out must be a C-contiguous uint16 array")
+    ss, os_ = _strides5(src_strides), _strides5(out_strides)
+    lib.oracle_apply_multi_rope(n, k, *[_ptr(a, _i32p) for a in hm], _ptr(W, _f64p), _ptr(src, _u16p),
+                                _ptr(ss, _i64p), d_s, _ptr(out, _u16p), _ptr(os_, _i64p), d_t,
+                                int(n_seqs), int(seq_len), float(theta), int(style), int(pos_offset),
+                                int(n_threads))
     return out

@@ -892,6 +892,66 @@ int oracle_apply_multi(int n_maps, int k,
     return 0;
 }
 
+/*
+ * Multi-layer application with the target's rotary transform (Sec. 3.2
+ * feature, Sec. 1 pipeline; Sec. 2.1, Sec. 3.1: the mapped keys receive the
+ * target RoPE before decoding).  s = x~ W~ in fp64 as in oracle_apply_multi;
+ * for a K map (kv = 0) every channel pair of s (style 0: (i, i + d_t/2),
+ * style 1: (2i, 2i + 1)) is turned by the angle pos * theta^(-2 i / d_t),
+ * pos = pos_offset + t, in fp64:
+ *   (a, b) -> (a cos - b sin, b cos + a sin);
+ * then every channel is rounded once to bf16 (RNE).  V maps write
+ * RNE_bf16(s).  Returns 0.
+ */
+int oracle_apply_multi_rope(int n_maps, int k,
+                            const int32_t *tgt_layer, const int32_t *tgt_head, const int32_t *kv,
+                            const int32_t *src_layers, const int32_t *src_head,
+                            const double *W,
+                            const uint16_t *src, const int64_t *src_strides, int d_s,
+                            uint16_t *out, const int64_t *out_strides, int d_t,
+                            int n_seqs, int seq_len, double theta, int style, int pos_offset, int n_threads) {
+    const int P = k * d_s + 1;
+    const int h = d_t / 2;
+    set_threads(n_threads);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int m = 0; m < n_maps; ++m) {
+        const double *Wm = W + (int64_t)m * P * d_t;
+        double *xt = (double *)malloc(sizeof(double) * (size_t)P);
+        double *s = (double *)malloc(sizeof(double) * (size_t)d_t);
+        for (int b = 0; b < n_seqs; ++b) {
+            for (int t = 0; t < seq_len; ++t) {
+                for (int i = 0; i < k; ++i) {
+                    const uint16_t *xr = src + row_offset(src_strides, src_layers[(int64_t)m * k + i], kv[m], b,
+                                                          src_head[m], t);
+                    for (int c = 0; c < d_s; ++c) xt[i * d_s + c] = bf16_bits_to_double(xr[c]);
+                }
+                xt[k * d_s] = 1.0;
+                for (int j = 0; j < d_t; ++j) {
+                    double acc = 0.0;
+                    for (int p = 0; p < P; ++p) acc += xt[p] * Wm[(int64_t)p * d_t + j];
+                    s[j] = acc;
+                }
+                if (kv[m] == 0) {
+                    const double pos = (double)(pos_offset + t);
+                    for (int i = 0; i < h; ++i) {
+                        const double ang = pos * pow(theta, -2.0 * i / (double)d_t);
+                        const double c = cos(ang), sn = sin(ang);
+                        const int ia = style == 0 ? i : 2 * i, ib = style == 0 ? i + h : 2 * i + 1;
+                        const double a = s[ia], bb = s[ib];
+                        s[ia] = a * c - bb * sn;
+                        s[ib] = bb * c + a * sn;
+                    }
+                }
+                uint16_t *orow = out + row_offset(out_strides, tgt_layer[m], kv[m], b, tgt_head[m], t);
+                for (int j = 0; j < d_t; ++j) orow[j] = oracle_double_to_bf16(s[j]);
+            }
+        }
+        free(s);
+        free(xt);
+    }
+    return 0;
+}
+
 /* Element-wise oracle_double_to_bf16 over n values.  Returns 0. */
 int oracle_double_to_bf16_array(int64_t n, const double *v, uint16_t *out) {
     for (int64_t i = 0; i < n; ++i) out[i] = oracle_double_to_bf16(v[i]);

@@ -330,3 +330,95 @@ def test_multi_centered_zero_weights_and_sampling():
     s1, A1, B1 = centered(p, 3)
     s2, A2, B2 = centered(p, 1, w=w0.reshape(p.w.shape))
     assert np.array_equal(s1, s2) and np.array_equal(A1, A2) and np.array_equal(B1, B2)
+
+
+# ----------------------------------------------------------------------------- target rotation, k > 1
+
+def _rope_f64(x, pos, theta, style):
+    """Exact rotation of fp64 rows x [..., d] at positions pos: the transform that
+    RoFormer's relative-position property pins in test_oracle_pins."""
+    d = x.shape[-1]
+    h = d // 2
+    f = theta ** (-2.0 * np.arange(h) / d)
+    ang = np.asarray(pos, dtype=np.float64)[..., None] * f
+    c, s = np.cos(ang), np.sin(ang)
+    ia = np.arange(h) if style == 0 else 2 * np.arange(h)
+    ib = ia + h if style == 0 else ia + 1
+    y = x.copy()
+    y[..., ia] = x[..., ia] * c - x[..., ib] * s
+    y[..., ib] = x[..., ib] * c + x[..., ia] * s
+    return y
+
+
+@pytest.mark.parametrize("style", [0, 1])
+def test_multi_apply_rope_is_rotation_of_the_unrounded_output(style):
+    # K maps: the rotation of the exact x~ W~ (dyadic coefficients with few
+    # bits: exact in fp64 in any order), rounded once; V maps: oracle_apply_multi
+    rng = np.random.default_rng(61)
+    k, d = 3, 8
+    src, hm, ss, os_ = _apply_setup(rng)
+    X = oracle.bf16_to_double(src)
+    W = rng.integers(-64, 65, size=(2, k * d + 1, d)) / 64.0
+    theta, off = 1e4, 11
+    out = np.zeros((1, 2, 2, 1, 9, d), np.uint16)
+    oracle.apply_multi_rope(hm, W, src, ss, d, out, os_, d, 2, 9, theta, style, off)
+    plain = np.zeros_like(out)
+    oracle.apply_multi(hm, W, src, ss, d, plain, os_, d, 2, 9)
+    pos = off + np.arange(9)
+    for m in range(2):
+        z = hm["kv"][m]
+        if z == 1:
+            assert np.array_equal(out[0, 1], plain[0, 1])
+            continue
+        feat = np.concatenate([X[j, z, :, 0] for j in hm["src_layers"][m]] + [np.ones((2, 9, 1))], axis=-1)
+        s = feat @ W[m]
+        assert np.array_equal(out[0, z, :, 0], oracle.double_to_bf16(_rope_f64(s, pos[None, :], theta, style)))
+    # position 0 turns nothing: a one-token call at offset 0 equals oracle_apply_multi
+    o1, p1 = (np.zeros((1, 2, 2, 1, 1, d), np.uint16) for _ in range(2))
+    s1 = np.ascontiguousarray(src[..., :1, :])
+    ss1, os1 = synth.cache_strides(4, 1, 2, 1, d), synth.cache_strides(1, 1, 2, 1, d)
+    oracle.apply_multi_rope(hm, W, s1, ss1, d, o1, os1, d, 2, 1, theta, style, 0)
+    oracle.apply_multi(hm, W, s1, ss1, d, p1, os1, d, 2, 1)
+    assert np.array_equal(o1, p1)
+
+
+def test_multi_apply_rope_k1_equals_single_layer_apply_rope():
+    rng = np.random.default_rng(62)
+    L_s, H_s, L_t, H_t, B, T, d = 3, 2, 2, 2, 2, 13, 16
+    src = to_bf16_bits(rng.standard_normal((L_s, 2, B, H_s, T, d)) * 2)
+    hm1 = {f: [] for f in oracle.HEAD_MAP_FIELDS}
+    for l in range(L_t):
+        for z in range(2):
+            for h in range(H_t):
+                for f, v in zip(oracle.HEAD_MAP_FIELDS, (l, h, z, (l + h) % L_s, (h + 1) % H_s, l * H_t + h)):
+                    hm1[f].append(v)
+    hm1 = {f: np.asarray(v, np.int32) for f, v in hm1.items()}
+    hmk = {f: hm1[f] for f in ("tgt_layer", "tgt_head", "kv", "src_head", "weight_row")}
+    hmk["src_layers"] = hm1["src_layer"].reshape(-1, 1)
+    n = hm1["kv"].shape[0]
+    W = rng.standard_normal((n, d + 1, d))
+    ss, os_ = synth.cache_strides(L_s, H_s, B, T, d), synth.cache_strides(L_t, H_t, B, T, d)
+    for style in (0, 1):
+        a = np.zeros((L_t, 2, B, H_t, T, d), np.uint16)
+        b = np.zeros_like(a)
+        oracle.apply_rope(hm1, W, src, ss, d, a, os_, d, B, T, 5e5, style, 40)
+        oracle.apply_multi_rope(hmk, W, src, ss, d, b, os_, d, B, T, 5e5, style, 40)
+        assert np.array_equal(a, b)
+
+
+def test_multi_apply_rope_inverse_rotation_recovers_apply_multi():
+    # de-rotating with the pinned inverse transform gives the unrotated mapped
+    # cache back up to the two extra roundings
+    rng = np.random.default_rng(63)
+    k, d = 3, 32
+    src, hm, ss, os_ = _apply_setup(rng, d_s=d, d_t=d)
+    W = rng.standard_normal((2, k * d + 1, d)) * 0.2
+    out = np.zeros((1, 2, 2, 1, 9, d), np.uint16)
+    oracle.apply_multi_rope(hm, W, src, ss, d, out, os_, d, 2, 9, 1e6, 0, 2000)
+    plain = np.zeros_like(out)
+    oracle.apply_multi(hm, W, src, ss, d, plain, os_, d, 2, 9)
+    back = oracle.rope(out, os_, 1, 1, d, 2, 9, 1e6, 0, inverse=True, pos_offset=2000)
+    a, b = oracle.bf16_to_double(plain), oracle.bf16_to_double(back)
+    assert np.array_equal(out[:, 1], plain[:, 1])
+    assert relF(b, a) < 2 ** -7
+    assert not np.array_equal(out[:, 0], plain[:, 0])
