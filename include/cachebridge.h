@@ -31,7 +31,8 @@
  * and the rotary position transform of cached keys (Sec. 2.1, Sec. 3.1: RoPE
  * removed before fitting, restored after mapping):
  *
- *   cb_rope_table, cb_rope, cb_apply_rope (mapping with the target RoPE fused)
+ *   cb_rope_table, cb_rope, cb_stats_accumulate_rope and cb_apply_rope (the
+ *   rotary transforms folded into the statistics gather and the mapping)
  *
  * and the multi-layer feature of Sec. 3.2 (k selected source layers per map):
  *
@@ -378,25 +379,61 @@ cb_status cb_attn_weights(int32_t n_rows, int32_t n_seqs, int32_t seq_len, int32
 cb_status cb_rope_table(double theta, int32_t head_dim, int32_t n_pos, float *table, void *stream);
 
 /*
+ * A model's rotary transform, as the calls below take it.  The library checks
+ * head_dim against the cache it is applied to and n_pos against the positions
+ * it needs (CB_ERR_SHAPE), so a table built for another head width or too few
+ * positions is refused before anything is enqueued.
+ */
+typedef struct cb_rope_spec {
+    const float *table;     /* cb_rope_table(theta, head_dim, n_pos) output: device, 16-byte aligned */
+    int32_t head_dim;       /* the head_dim the table was built for */
+    int32_t n_pos;          /* its rows: positions 0 .. n_pos - 1 */
+    int32_t style;          /* CB_ROPE_HALF_SPLIT or CB_ROPE_INTERLEAVED */
+    int32_t pos_offset;     /* position of token 0 of every sequence (>= 0) */
+} cb_rope_spec;
+
+/*
  * Rotary position transform of the keys (Sec. 2.1; Sec. 3.1: the maps act in
  * content coordinates, so source RoPE is removed before fitting and the
  * target's RoPE is applied to the mapped keys).  For every K row (kv = 0) of
- * `in`, at position pos = pos_offset + tok, each channel pair (style
- * CB_ROPE_HALF_SPLIT or CB_ROPE_INTERLEAVED) is turned by the table's angle
- * of pos (negated when `inverse` is non-zero):
+ * `in`, at position pos = rope->pos_offset + tok, each channel pair
+ * (rope->style) is turned by the table's angle of pos (negated when `inverse`
+ * is non-zero):
  *   (a, b) -> (a cos - b sin, b cos + a sin),
  * in fp32 from the exact bf16 values, rounded once to bf16, and written to the
  * same element of `out`.  V rows (kv = 1) carry no position: they are copied
  * when out->data differs from in->data and left alone otherwise.  `out` may be
  * `in` (same data and strides) for an in-place transform; other overlaps are
  * not allowed.  in and out: the same geometry, head_dim a multiple of 16 up to
- * 256; table: from cb_rope_table with this head_dim and n_pos >= pos_offset +
- * seq_len.  Use: fit on cb_rope(inverse) copies of the source and target
- * caches; apply on a cb_rope(inverse) copy of the sender's cache, then
- * cb_rope (forward, target table) on the output in place.
+ * 256 and equal to rope->head_dim; rope->n_pos >= pos_offset + seq_len.
+ * cb_stats_accumulate_rope and cb_apply_rope fold the same transform into
+ * their reads and writes.
  */
-cb_status cb_rope(const cb_cache *in, const cb_cache *out, const float *table, int32_t n_pos, int32_t style,
-                  int32_t inverse, int32_t pos_offset, void *stream);
+cb_status cb_rope(const cb_cache *in, const cb_cache *out, const cb_rope_spec *rope, int32_t inverse,
+                  void *stream);
+
+/*
+ * cb_stats_accumulate on keys that carry rotary positions (Sec. 2.1, Sec. 3.1:
+ * the maps are fitted in content coordinates, RoPE removed before
+ * regression).  For K maps (kv = 0) the source row at position pos =
+ * src_rope->pos_offset + tok is turned back by the sender's angle of pos and
+ * the target row by the target's angle (tgt_rope), each in fp32 from the
+ * exact bf16 values and rounded to bf16 exactly as cb_rope(inverse) writes
+ * it; the moments are then those of cb_stats_accumulate on the de-rotated
+ * rows (V maps are unchanged).  Either spec may be NULL (that side is not
+ * turned).  Checks as cb_stats_accumulate, plus src_rope->head_dim = d_s,
+ * tgt_rope->head_dim = d_t and n_pos >= pos_offset + seq_len (CB_ERR_SHAPE).
+ * Single-layer plans turn the rows as they land in LDS, inside the moments
+ * kernel (d_s = d_t = 64 or 128; other widths CB_ERR_UNSUPPORTED).  A
+ * multi-layer plan stages each calibration row many times (once per task of
+ * every map that reads it), so there the calibration rows of the K maps are
+ * first gathered once, de-rotated, into a compact workspace the plan keeps
+ * (every sample_stride-th token only), and the moments kernel reads them
+ * from there.
+ */
+cb_status cb_stats_accumulate_rope(cb_plan *plan, const cb_cache *src, const cb_cache *tgt, const float *weights,
+                                   int64_t w_row_stride, float *G, float *C, const cb_rope_spec *src_rope,
+                                   const cb_rope_spec *tgt_rope, void *stream);
 
 /*
  * Online mapping (Sec. 1 pipeline; Sec. 2.3 Eq. support-cost): for every map
@@ -415,21 +452,31 @@ cb_status cb_apply(cb_plan *plan, const float *maps, const cb_cache *src, const 
                    void *stream);
 
 /*
- * Online mapping with the target's rotary transform fused (Sec. 1 pipeline;
- * Sec. 2.1, Sec. 3.1: the mapped keys receive the target model's RoPE before
- * decoding).  Identical to cb_apply for V outputs (kv = 1).  For K outputs
- * (kv = 0) the fp32 sum s = x W + b of each token at position pos = pos_offset
- * + tok has its channel pairs (style CB_ROPE_HALF_SPLIT or
- * CB_ROPE_INTERLEAVED) turned by the table's angle of pos,
- *   (a, b) -> (a cos - b sin, b cos + a sin),
- * in fp32 and is then rounded once to bfloat16; cb_apply followed by cb_rope
- * rounds twice.  table: from cb_rope_table with head_dim = the plan's d_t and
- * n_pos >= pos_offset + seq_len, device, 16-byte aligned, caller-owned.
- * Errors as cb_apply; CB_ERR_SHAPE for a short table, CB_ERR_UNSUPPORTED for
- * a multi-layer plan (apply those with cb_apply, then cb_rope).
+ * Online mapping with the rotary transforms fused (Sec. 1 pipeline; Sec. 2.1,
+ * Sec. 3.1: the maps act in content coordinates, so the sender's RoPE is
+ * removed from its keys before mapping and the mapped keys receive the target
+ * model's RoPE before decoding).  Identical to cb_apply for V maps (kv = 1).
+ * For K maps (kv = 0), at position pos = pos_offset + tok:
+ *   src_rope (may be NULL): the source row is first turned back by the
+ *     sender's angle of pos (inverse transform), in fp32 from the exact bf16
+ *     values, and rounded to bf16 as cb_rope(inverse) would write it;
+ *   tgt_rope (may be NULL): the fp32 sum s = x W + b has its channel pairs
+ *     turned by the target's angle of pos, (a, b) -> (a cos - b sin,
+ *     b cos + a sin), in fp32 before the single rounding to bfloat16 (cb_apply
+ *     followed by cb_rope rounds twice).
+ * src_rope->head_dim must be the plan's d_s and tgt_rope->head_dim its d_t
+ * (CB_ERR_SHAPE otherwise, as for a table with fewer than pos_offset +
+ * seq_len rows).  Single-layer plans read each source row once and de-rotate
+ * it on the way into LDS (d_s = 64 or 128).  A multi-layer plan reads each
+ * source row once per map that selects its layer, so there the K rows of the
+ * batch are de-rotated once, by a rotation pass into a workspace the plan
+ * keeps (sized to the largest batch seen), before the mapping kernel; the
+ * target rotation is fused into its epilogue.  Errors as cb_apply, and
+ * CB_ERR_UNSUPPORTED for d_s = 96 with a source rotation on a single-layer
+ * plan.
  */
 cb_status cb_apply_rope(cb_plan *plan, const float *maps, const cb_cache *src, const cb_cache *tgt_out,
-                        const float *table, int32_t n_pos, int32_t style, int32_t pos_offset, void *stream);
+                        const cb_rope_spec *src_rope, const cb_rope_spec *tgt_rope, void *stream);
 
 /*
  * Multi-layer mapper support (Sec. 3.2, Eq. localfeature with k selected

@@ -21,8 +21,9 @@ current HIP stream.  The functions keep the C names:
   ESS-floor shrinkage (Sec. 3.3)
 * :func:`cb_rope_table`, :func:`cb_rope` -- rotary position transform of cached
   keys (RoPE removed before fitting, restored after mapping; Sec. 2.1, 3.1);
-  :func:`cb_apply_rope` -- the mapping with the target's RoPE fused into its
-  epilogue (one rounding)
+  :func:`rope_spec` describes a table; :func:`cb_stats_accumulate_rope` folds
+  the de-rotation into the statistics gather and :func:`cb_apply_rope` the
+  de-rotation of the sender and the target's rotation into the mapping
 * :func:`cb_plan_create_multi`, :func:`cb_ridge_solve_ws` -- maps over the
   multi-layer feature of k selected source layers (Sec. 3.2, Eq. localfeature)
   and the blocked solve of their P = k d_s + 1 systems
@@ -149,14 +150,23 @@ _lib.cb_attn_weights.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                  ctypes.c_int32, _vp, ctypes.c_int64, _vp, _vp]
 _lib.cb_rope_table.restype = ctypes.c_int
 _lib.cb_rope_table.argtypes = [ctypes.c_double, ctypes.c_int32, ctypes.c_int32, _vp, _vp]
+
+
+class CbRopeSpec(ctypes.Structure):
+    _fields_ = [("table", _vp), ("head_dim", ctypes.c_int32), ("n_pos", ctypes.c_int32),
+                ("style", ctypes.c_int32), ("pos_offset", ctypes.c_int32)]
+
+
+_rsp = ctypes.POINTER(CbRopeSpec)
 _lib.cb_rope.restype = ctypes.c_int
-_lib.cb_rope.argtypes = [ctypes.POINTER(CbCache), ctypes.POINTER(CbCache), _vp, ctypes.c_int32, ctypes.c_int32,
-                         ctypes.c_int32, ctypes.c_int32, _vp]
+_lib.cb_rope.argtypes = [ctypes.POINTER(CbCache), ctypes.POINTER(CbCache), _rsp, ctypes.c_int32, _vp]
 _lib.cb_apply.restype = ctypes.c_int
 _lib.cb_apply.argtypes = [_vp, _vp, ctypes.POINTER(CbCache), ctypes.POINTER(CbCache), _vp]
 _lib.cb_apply_rope.restype = ctypes.c_int
-_lib.cb_apply_rope.argtypes = [_vp, _vp, ctypes.POINTER(CbCache), ctypes.POINTER(CbCache), _vp, ctypes.c_int32,
-                               ctypes.c_int32, ctypes.c_int32, _vp]
+_lib.cb_apply_rope.argtypes = [_vp, _vp, ctypes.POINTER(CbCache), ctypes.POINTER(CbCache), _rsp, _rsp, _vp]
+_lib.cb_stats_accumulate_rope.restype = ctypes.c_int
+_lib.cb_stats_accumulate_rope.argtypes = [_vp, ctypes.POINTER(CbCache), ctypes.POINTER(CbCache), _vp, ctypes.c_int64,
+                                          _vp, _vp, _rsp, _rsp, _vp]
 _lib.cb_status_string.restype = ctypes.c_char_p
 _lib.cb_status_string.argtypes = [ctypes.c_int]
 _lib.cb_last_error.restype = ctypes.c_char_p
@@ -550,13 +560,30 @@ def cb_rope_table(theta: float, head_dim: int, n_pos: int, table: torch.Tensor, 
     _check(_lib.cb_rope_table(float(theta), int(head_dim), int(n_pos), _ptr(table), _stream(stream)))
 
 
+def rope_spec(table: torch.Tensor, style: int = CB_ROPE_HALF_SPLIT, pos_offset: int = 0) -> CbRopeSpec:
+    """Describe a cb_rope_table output: ``table`` is float32 [n_pos][head_dim/2][2] (its
+    shape gives head_dim and n_pos, which the library checks against each call)."""
+    if table.dtype != torch.float32 or table.dim() != 3 or table.shape[2] != 2 or not table.is_contiguous():
+        raise ValueError("a rope table is a contiguous float32 [n_pos][head_dim/2][2] tensor")
+    sp = CbRopeSpec()
+    sp.table, sp.head_dim, sp.n_pos = table.data_ptr(), 2 * table.shape[1], table.shape[0]
+    sp.style, sp.pos_offset = int(style), int(pos_offset)
+    sp._keep = table
+    return sp
+
+
+def _spec(r) -> Optional[CbRopeSpec]:
+    if r is None or isinstance(r, CbRopeSpec):
+        return r
+    return rope_spec(r)
+
+
 def cb_rope(cache_in: torch.Tensor, cache_out: torch.Tensor, table: torch.Tensor, style: int = CB_ROPE_HALF_SPLIT,
             inverse: bool = False, pos_offset: int = 0, stream=None):
     """Rotate (inverse: de-rotate) the K rows of a cache into cache_out (may be cache_in); V rows copied."""
-    n_pos = table.shape[0]
+    sp = rope_spec(table, style, pos_offset)
     iv, ov = cache_view(cache_in), cache_view(cache_out)
-    _check(_lib.cb_rope(ctypes.byref(iv), ctypes.byref(ov), _ptr(table), int(n_pos), int(style), int(bool(inverse)),
-                        int(pos_offset), _stream(stream)))
+    _check(_lib.cb_rope(ctypes.byref(iv), ctypes.byref(ov), ctypes.byref(sp), int(bool(inverse)), _stream(stream)))
 
 
 def cb_apply(plan: Plan, maps: torch.Tensor, src: torch.Tensor, tgt_out: torch.Tensor, stream=None):
@@ -566,13 +593,32 @@ def cb_apply(plan: Plan, maps: torch.Tensor, src: torch.Tensor, tgt_out: torch.T
     _check(_lib.cb_apply(plan.handle, _ptr(maps), ctypes.byref(sv), ctypes.byref(ov), _stream(stream)))
 
 
-def cb_apply_rope(plan: Plan, maps: torch.Tensor, src: torch.Tensor, tgt_out: torch.Tensor, table: torch.Tensor,
-                  style: int = CB_ROPE_HALF_SPLIT, pos_offset: int = 0, stream=None):
-    """cb_apply with the target RoPE (table from cb_rope_table, head_dim d_t) turning the K outputs in fp32
-    before their single rounding."""
+def cb_apply_rope(plan: Plan, maps: torch.Tensor, src: torch.Tensor, tgt_out: torch.Tensor, tgt_rope=None,
+                  src_rope=None, stream=None):
+    """cb_apply with the rotary transforms fused: ``src_rope`` turns the sender's K rows back as they are read,
+    ``tgt_rope`` turns the K outputs in fp32 before their single rounding.  Each is a :func:`rope_spec`
+    (or a table, for style 0 at offset 0) or None."""
     _need(maps, (plan.n_maps, plan.P, plan.d_t), torch.float32, "maps")
-    if table.dtype != torch.float32:
-        raise ValueError("table is float32")
+    tr, sr = _spec(tgt_rope), _spec(src_rope)
     sv, ov = cache_view(src), cache_view(tgt_out)
-    _check(_lib.cb_apply_rope(plan.handle, _ptr(maps), ctypes.byref(sv), ctypes.byref(ov), _ptr(table),
-                              int(table.shape[0]), int(style), int(pos_offset), _stream(stream)))
+    _check(_lib.cb_apply_rope(plan.handle, _ptr(maps), ctypes.byref(sv), ctypes.byref(ov),
+                              None if sr is None else ctypes.byref(sr), None if tr is None else ctypes.byref(tr),
+                              _stream(stream)))
+
+
+def cb_stats_accumulate_rope(plan: Plan, src: torch.Tensor, tgt: torch.Tensor, weights: torch.Tensor,
+                             G: torch.Tensor, C: torch.Tensor, src_rope=None, tgt_rope=None,
+                             w_row_stride: Optional[int] = None, stream=None):
+    """cb_stats_accumulate on keys that carry RoPE: the K rows of the source (src_rope) and of the target
+    (tgt_rope) are turned back as they are gathered, exactly as cb_rope(inverse) would write them."""
+    _need(G, (plan.n_maps, plan.P, plan.P), torch.float32, "G")
+    _need(C, (plan.n_maps, plan.P, plan.d_t), torch.float32, "C")
+    if w_row_stride is None:
+        w_row_stride = weights.stride(0) if weights.dim() == 2 else weights.numel()
+    _check_weights(plan, weights, int(w_row_stride), src)
+    sr, tr = _spec(src_rope), _spec(tgt_rope)
+    sv, tv = cache_view(src), cache_view(tgt)
+    _check(_lib.cb_stats_accumulate_rope(plan.handle, ctypes.byref(sv), ctypes.byref(tv), _ptr(weights),
+                                         int(w_row_stride), _ptr(G), _ptr(C),
+                                         None if sr is None else ctypes.byref(sr),
+                                         None if tr is None else ctypes.byref(tr), _stream(stream)))

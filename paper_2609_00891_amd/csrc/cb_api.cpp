@@ -723,6 +723,21 @@ cb_status cb_stats_zero(const cb_plan *p, float *G, float *C, void *stream) {
     return ok();
 }
 
+// A rotary spec against the head width it turns and the positions a call needs.
+static cb_status check_rope(const char *name, const cb_rope_spec *r, int32_t head_dim, int64_t seq_len) {
+    if (!r->table) return fail(CB_ERR_INVALID_ARGUMENT, "%s->table is NULL", name);
+    if (r->style != CB_ROPE_HALF_SPLIT && r->style != CB_ROPE_INTERLEAVED)
+        return fail(CB_ERR_INVALID_ARGUMENT, "%s: unknown rope style %d", name, r->style);
+    if (r->head_dim != head_dim)
+        return fail(CB_ERR_SHAPE, "%s was built for head_dim %d, the cache it turns has %d", name, r->head_dim,
+                    head_dim);
+    if (r->pos_offset < 0 || (int64_t)r->pos_offset + seq_len > (int64_t)r->n_pos)
+        return fail(CB_ERR_SHAPE, "%s: positions %d .. %lld need a table of that many rows (n_pos = %d)", name,
+                    r->pos_offset, (long long)r->pos_offset + seq_len - 1, r->n_pos);
+    if (((uintptr_t)r->table) % 16) return fail(CB_ERR_MISALIGNED, "%s->table must be 16-byte aligned", name);
+    return CB_OK;
+}
+
 cb_status cb_stats_accumulate(cb_plan *p, const cb_cache *src, const cb_cache *tgt, const float *weights,
                               int64_t w_row_stride, float *G, float *C, void *stream) {
     if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
@@ -745,6 +760,52 @@ cb_status cb_stats_accumulate(cb_plan *p, const cb_cache *src, const cb_cache *t
     if (empty) return ok();
     hipStream_t st = (hipStream_t)stream;
     if (cb::launch_stats(p->d_s, p->d_t, a, st) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "statistics kernel launch failed");
+    cb::ReduceArgs r = reduce_args(p, a);
+    r.G = G;
+    r.C = C;
+    if (cb::launch_reduce(p->d_s, p->d_t, r, st) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "reduction kernel launch failed");
+    return ok();
+}
+
+// Multi-layer plans with rotary keys: not yet wired.
+static cb_status stats_multi_rope(cb_plan *, const cb_cache *, const cb_cache *, const float *, int64_t, float *,
+                                  float *, const cb_rope_spec *, const cb_rope_spec *, void *) {
+    return fail(CB_ERR_UNSUPPORTED, "rotary de-rotation on a multi-layer plan");
+}
+
+cb_status cb_stats_accumulate_rope(cb_plan *p, const cb_cache *src, const cb_cache *tgt, const float *weights,
+                                   int64_t w_row_stride, float *G, float *C, const cb_rope_spec *src_rope,
+                                   const cb_rope_spec *tgt_rope, void *stream) {
+    if (!src_rope && !tgt_rope) return cb_stats_accumulate(p, src, tgt, weights, w_row_stride, G, C, stream);
+    if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
+    if (!G || !C) return fail(CB_ERR_INVALID_ARGUMENT, "G and C must be non-NULL");
+    if (((uintptr_t)G) % 4 || ((uintptr_t)C) % 4) return fail(CB_ERR_MISALIGNED, "G and C must be 4-byte aligned");
+    if (!src || !tgt) return fail(CB_ERR_INVALID_ARGUMENT, "src and tgt must be non-NULL");
+    if (src_rope)
+        if (cb_status s = check_rope("src_rope", src_rope, p->d_s, src->seq_len)) return s;
+    if (tgt_rope)
+        if (cb_status s = check_rope("tgt_rope", tgt_rope, p->d_t, tgt->seq_len)) return s;
+    if (p->multi) return stats_multi_rope(p, src, tgt, weights, w_row_stride, G, C, src_rope, tgt_rope, stream);
+    if (p->d_s != p->d_t || (p->d_s != 64 && p->d_s != 128))
+        return fail(CB_ERR_UNSUPPORTED, "the fused de-rotation takes d_s = d_t = 64 or 128 (got %d, %d); "
+                                        "turn the caches with cb_rope first", p->d_s, p->d_t);
+    if (src_rope && tgt_rope && src_rope->style != tgt_rope->style)
+        return fail(CB_ERR_UNSUPPORTED, "the fused de-rotation takes one pairing style for both caches");
+    cb::StatsArgs a = {};
+    bool empty = false;
+    if (cb_status s = prepare_stats(p, src, tgt, weights, w_row_stride, a, empty)) return s;
+    if (empty) return ok();
+    const cb_rope_spec *r0 = src_rope ? src_rope : tgt_rope, *r1 = tgt_rope ? tgt_rope : src_rope;
+    a.rope_tab[0] = r0->table;
+    a.rope_tab[1] = r1->table;
+    a.rope_pos[0] = r0->pos_offset;
+    a.rope_pos[1] = r1->pos_offset;
+    a.rope_on[0] = src_rope != nullptr;
+    a.rope_on[1] = tgt_rope != nullptr;
+    hipStream_t st = (hipStream_t)stream;
+    if (cb::launch_stats_rope(p->d_s, r0->style, a, st) != hipSuccess)
         return fail(CB_ERR_DEVICE, "statistics kernel launch failed");
     cb::ReduceArgs r = reduce_args(p, a);
     r.G = G;
@@ -1116,24 +1177,19 @@ cb_status cb_rope_table(double theta, int32_t head_dim, int32_t n_pos, float *ta
     return ok();
 }
 
-cb_status cb_rope(const cb_cache *in, const cb_cache *out, const float *table, int32_t n_pos, int32_t style,
-                  int32_t inverse, int32_t pos_offset, void *stream) {
-    if (!in || !out) return fail(CB_ERR_INVALID_ARGUMENT, "in and out must be non-NULL");
+cb_status cb_rope(const cb_cache *in, const cb_cache *out, const cb_rope_spec *rope, int32_t inverse, void *stream) {
+    if (!in || !out || !rope) return fail(CB_ERR_INVALID_ARGUMENT, "in, out and rope must be non-NULL");
     const int d = in->head_dim;
     if (d < 16 || d > 256 || d % 16) return fail(CB_ERR_UNSUPPORTED, "head_dim must be a multiple of 16 up to 256");
-    if (style != CB_ROPE_HALF_SPLIT && style != CB_ROPE_INTERLEAVED)
-        return fail(CB_ERR_INVALID_ARGUMENT, "unknown rope style %d", style);
     if (in->n_layers <= 0 || in->n_heads <= 0) return fail(CB_ERR_SHAPE, "in needs positive layer and head counts");
     if (cb_status s = check_cache("in", in, in->n_layers, in->n_heads, d)) return s;
     if (cb_status s = check_cache("out", out, in->n_layers, in->n_heads, d)) return s;
     if (out->n_seqs != in->n_seqs || out->seq_len != in->seq_len)
         return fail(CB_ERR_SHAPE, "in and out disagree on n_seqs / seq_len");
-    if (pos_offset < 0 || (int64_t)pos_offset + in->seq_len > n_pos)
-        return fail(CB_ERR_SHAPE, "positions %d .. %lld need a table of that many rows (n_pos = %d)", pos_offset,
-                    (long long)pos_offset + in->seq_len - 1, n_pos);
+    if (cb_status s = check_rope("rope", rope, d, in->seq_len)) return s;
     if ((int64_t)in->n_seqs * in->seq_len == 0) return ok();
-    if (!table) return fail(CB_ERR_INVALID_ARGUMENT, "table is NULL");
-    if (((uintptr_t)table) % 8) return fail(CB_ERR_MISALIGNED, "table must be 8-byte aligned");
+    const float *table = rope->table;
+    const int32_t style = rope->style, pos_offset = rope->pos_offset;
     const bool same = in->data == out->data;
     if (same && (in->s_layer != out->s_layer || in->s_kv != out->s_kv || in->s_seq != out->s_seq ||
                  in->s_head != out->s_head || in->s_tok != out->s_tok))
@@ -1266,13 +1322,17 @@ cb_status cb_apply(cb_plan *p, const float *maps, const cb_cache *src, const cb_
 }
 
 cb_status cb_apply_rope(cb_plan *p, const float *maps, const cb_cache *src, const cb_cache *tgt_out,
-                        const float *table, int32_t n_pos, int32_t style, int32_t pos_offset, void *stream) {
+                        const cb_rope_spec *src_rope, const cb_rope_spec *tgt_rope, void *stream) {
+    if (!src_rope && !tgt_rope) return cb_apply(p, maps, src, tgt_out, stream);
     if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
-    if (style != CB_ROPE_HALF_SPLIT && style != CB_ROPE_INTERLEAVED)
-        return fail(CB_ERR_INVALID_ARGUMENT, "unknown rope style %d", style);
-    if (p->multi) return fail(CB_ERR_UNSUPPORTED, "the fused rotary epilogue needs a single-layer plan");
-    if (!table) return fail(CB_ERR_INVALID_ARGUMENT, "table is NULL");
-    return apply_single(p, maps, src, tgt_out, table, n_pos, style, pos_offset, stream);
+    if (!src || !tgt_out) return fail(CB_ERR_INVALID_ARGUMENT, "src and tgt_out must be non-NULL");
+    if (src_rope)
+        if (cb_status s = check_rope("src_rope", src_rope, p->d_s, src->seq_len)) return s;
+    if (tgt_rope)
+        if (cb_status s = check_rope("tgt_rope", tgt_rope, p->d_t, src->seq_len)) return s;
+    if (p->multi || src_rope) return fail(CB_ERR_UNSUPPORTED, "not yet wired");
+    return apply_single(p, maps, src, tgt_out, tgt_rope->table, tgt_rope->n_pos, tgt_rope->style,
+                        tgt_rope->pos_offset, stream);
 }
 
 }  // extern "C"

@@ -68,6 +68,12 @@ struct StatsArgs {
     float *partials;      // [n_chunks * n_items][2][slot_floats]
     const void *zero;     // >= 256 zero bytes: source of the weights of absent tokens
     const double *sums;   // centered statistics only: [n_maps][1 + d_s + d_t] = (sum w, sum w x, sum w y)
+    // Rotary de-rotation of the K rows as they land (the rope variant of the
+    // kernel only): tables [n_pos][d/2][2] (cos, sin) of the source and the
+    // target (both valid pointers), position of token 0, and which side turns.
+    const float *rope_tab[2];
+    int32_t rope_pos[2];
+    int32_t rope_on[2];
 };
 
 struct ReduceArgs {
@@ -203,6 +209,8 @@ hipError_t launch_attn_weights(int32_t n_rows, int32_t n_seqs, int32_t seq_len, 
                                int64_t r_row_stride, int32_t p, float *w, int64_t w_row_stride, float *alpha,
                                hipStream_t s);
 hipError_t launch_stats(int d_s, int d_t, const StatsArgs &a, hipStream_t s);
+// style: 0 half split, 1 interleaved; d_s = d_t = 64 or 128
+hipError_t launch_stats_rope(int d, int style, const StatsArgs &a, hipStream_t s);
 hipError_t launch_reduce(int d_s, int d_t, const ReduceArgs &a, hipStream_t s);
 hipError_t launch_stats_centered(int d_s, int d_t, const StatsArgs &a, hipStream_t s);
 hipError_t launch_reduce_centered(int d_s, int d_t, const ReduceArgs &a, hipStream_t s);

@@ -15,6 +15,8 @@ typedef __attribute__((ext_vector_type(4))) short s16x4_t;
 typedef __attribute__((ext_vector_type(4))) float f32x4_t;
 typedef __attribute__((address_space(3))) f32x4_t lds_f32x4_t;
 typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
+typedef __attribute__((address_space(3))) u32x4_t lds_u32x4_t;
 typedef __attribute__((address_space(3))) char lds_char_t;
 
 __device__ __forceinline__ uint32_t fastdiv(uint32_t n, const FastDiv &f) {
@@ -214,6 +216,23 @@ __device__ __forceinline__ void lds_barrier() {
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
+// Rotary table entries (16 bytes) into registers.  Issued through inline
+// assembly like the copies, so the explicit vmcnt waits below account for
+// them; the registers are only read after wait_vm_tied has named them.
+__device__ __forceinline__ void gload16(f32x4_t &v, const float *p) {
+    asm volatile("global_load_dwordx4 %0, %1, off" : "=v"(v) : "v"(p) : "memory");
+}
+// vmcnt wait that also marks the eight table registers as written by it, so
+// no read of them can be placed before the wait.
+template <int N>
+__device__ __forceinline__ void wait_vm_tied(f32x4_t (&v)[2][4]) {
+    asm volatile("s_waitcnt vmcnt(%8)"
+                 : "+v"(v[0][0]), "+v"(v[0][1]), "+v"(v[0][2]), "+v"(v[0][3]), "+v"(v[1][0]), "+v"(v[1][1]),
+                   "+v"(v[1][2]), "+v"(v[1][3])
+                 : "n"(N)
+                 : "memory");
+}
+
 __device__ __forceinline__ bf16x8_t tr_read8(const lds_char_t *p0, const lds_char_t *p1) {
     const s16x4_t a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t *)p0);
     const s16x4_t b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t *)p1);
@@ -254,7 +273,20 @@ struct Copies {
 // The token loop of the wave of pair PR of map slot `slot`, for an item
 // streaming NTEN tensors.  CENTER: the folded operand is w (x - mu_x) with
 // mu_x = (sum w x) / (sum w) of the map, read from args.sums.
-template <int DS, int DT, bool RAGGED, bool CENTER, int NTEN, int PR>
+//
+// RS (rotary de-rotation; 1: pairs (i, i + d/2), 2: pairs (2i, 2i + 1);
+// d_s = d_t = 64 or 128): the K rows of a tile are turned back by their
+// positions' angles in LDS, by the waves that copied them, before any wave
+// reads the tile.  Lane l owns one chunk pair of every tensor tile (token row
+// ut, logical chunks uc and uc + d/16 -- the half-split partners), both moved
+// by its own wave's copies, so a wave needs only its own vmcnt wait before
+// turning them.  Tile t + 2 is turned during iteration t (after that
+// iteration's copies), and the next iteration's barrier publishes it.  The
+// lane's table entries of a tile are loaded right after the tile's copies,
+// into one of two register sets (by tile parity), so waiting for them
+// demands no more of the copies than the loop already does.  The products
+// are those of cb_rope's inverse transform, rounded once to bf16.
+template <int DS, int DT, bool RAGGED, bool CENTER, int NTEN, int PR, int RS>
 __device__ __forceinline__ void stats_wave(const StatsArgs &a, const StatsCtx c, const StatsItem &it,
                                            lds_char_t *lds, int wave, int lane) {
     using K = Cfg<DS, DT>;
@@ -298,6 +330,77 @@ __device__ __forceinline__ void stats_wave(const StatsArgs &a, const StatsCtx c,
     const float *wlane = a.w + (int64_t)(lane < 32 ? it.wrow[0] : it.wrow[1]) * a.w_row_stride + (lane & 31);
     const uint64_t wlanes = 0xffffull << (16 * wave);
     const int per_tile = (CP::STATIC ? L : n_copies) + 1;    // copies this wave issues per tile
+
+    // ---- rotary de-rotation (RS != 0): this lane's chunk pair and table entries
+    static_assert(RS == 0 || (DS == DT && (DS == 64 || DS == 128) && CP::STATIC && !CENTER),
+                  "the rotary variant takes d_s = d_t = 64 or 128");
+    constexpr int NP = DS / 16;                              // chunk pairs per row
+    constexpr int NTB = 8;                                   // table loads per tile: 2 tables x 4
+    constexpr int PT = L + 1 + (RS ? NTB : 0);               // vm instructions per tile
+    const int ul = lane & 31;
+    const int ut = DS == 128 ? 4 * (lane < 32 ? wave : 4 + wave) + (ul >> 3) : 8 * wave + (ul >> 2);
+    const int uc = DS == 128 ? (ul & 7) : (ul & 3);
+    const bool ulive = DS == 128 || lane < 32;               // d = 64: 32 chunk pairs per wave
+    const uint32_t uh = swz<K::NCBX>((uint32_t)ut);
+    const uint32_t offA = (uint32_t)ut * K::ROWX + ((uint32_t)uc ^ uh) * 16u;
+    const uint32_t offB = (uint32_t)ut * K::ROWX + ((uint32_t)(uc + NP) ^ uh) * 16u;
+    typedef f32x4_t TabSet[2][4];
+    auto tab_load = [&](TabSet &tb, const auto &q) __attribute__((always_inline)) {
+        const uint32_t tok = q.tt0 + (RAGGED ? min((uint32_t)ut, q.tmax) : (uint32_t)ut);
+#pragma unroll
+        for (int sd = 0; sd < 2; ++sd) {
+            const float *row = a.rope_tab[sd] + (int64_t)(a.rope_pos[sd] + (int)tok) * DS;   // d/2 (cos, sin)
+            if constexpr (RS == 1) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) gload16(tb[sd][j], row + 16 * uc + 4 * j);
+            } else {
+                gload16(tb[sd][0], row + 8 * uc);
+                gload16(tb[sd][1], row + 8 * uc + 4);
+                gload16(tb[sd][2], row + 8 * (uc + NP));
+                gload16(tb[sd][3], row + 8 * (uc + NP) + 4);
+            }
+        }
+    };
+    // which tensors of the item turn: x0 y0 x1 y1 (x1 only with NTEN = 4, y1 with NTEN >= 3)
+    const bool rx0 = a.rope_on[0] && it.kv[0] == 0, ry0 = a.rope_on[1] && it.kv[0] == 0;
+    const bool rx1 = NTEN == 4 && a.rope_on[0] && it.kv[1] == 0, ry1 = NTEN >= 3 && a.rope_on[1] && it.kv[1] == 0;
+    // inverse rotation of this lane's chunk pair of the tensor tile at p
+    auto turn_pair = [&](lds_char_t *p, const f32x4_t (&cs)[4]) __attribute__((always_inline)) {
+        const u32x4_t A = *(const lds_u32x4_t *)(p + offA);
+        const u32x4_t B = *(const lds_u32x4_t *)(p + offB);
+        const uint32_t av[4] = {A[0], A[1], A[2], A[3]}, bv[4] = {B[0], B[1], B[2], B[3]};
+        uint32_t oa[4], ob[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            if constexpr (RS == 1) {
+                // pairs (8 uc + 2e + h, its partner d/2 further on), frequency 8 uc + 2e + h
+                const float c0 = cs[e][0], s0 = cs[e][1], c1 = cs[e][2], s1 = cs[e][3];
+                const float x0 = bf_lo(av[e]), x1 = bf_hi(av[e]), y0 = bf_lo(bv[e]), y1 = bf_hi(bv[e]);
+                oa[e] = pack_bf16(__builtin_fmaf(x0, c0, y0 * s0), __builtin_fmaf(x1, c1, y1 * s1));
+                ob[e] = pack_bf16(__builtin_fmaf(y0, c0, -(x0 * s0)), __builtin_fmaf(y1, c1, -(x1 * s1)));
+            } else {
+                // pairs (2i, 2i + 1) inside each chunk: frequency 4 uc + e, then 4 (uc + d/16) + e
+                const f32x4_t qa = cs[e >> 1], qb = cs[2 + (e >> 1)];
+                const float ca = (e & 1) ? qa[2] : qa[0], sa = (e & 1) ? qa[3] : qa[1];
+                const float cb = (e & 1) ? qb[2] : qb[0], sb = (e & 1) ? qb[3] : qb[1];
+                const float x0 = bf_lo(av[e]), x1 = bf_hi(av[e]), y0 = bf_lo(bv[e]), y1 = bf_hi(bv[e]);
+                oa[e] = pack_bf16(__builtin_fmaf(x0, ca, x1 * sa), __builtin_fmaf(x1, ca, -(x0 * sa)));
+                ob[e] = pack_bf16(__builtin_fmaf(y0, cb, y1 * sb), __builtin_fmaf(y1, cb, -(y0 * sb)));
+            }
+        }
+        const u32x4_t A2 = {oa[0], oa[1], oa[2], oa[3]}, B2 = {ob[0], ob[1], ob[2], ob[3]};
+        *(lds_u32x4_t *)(p + offA) = A2;
+        *(lds_u32x4_t *)(p + offB) = B2;
+    };
+    // turn the K tensors of the tile in ring stage st (its copies and its table entries have landed)
+    auto turn_tile = [&](const TabSet &tb, int st) __attribute__((always_inline)) {
+        if (!ulive) return;
+        lds_char_t *S = lds + st * K::STAGE;
+        if (rx0) turn_pair(S, tb[0]);
+        if (ry0) turn_pair(S + K::XB, tb[1]);
+        if (NTEN == 4 && rx1) turn_pair(S + K::XB + K::YB, tb[0]);
+        if (NTEN >= 3 && ry1) turn_pair(S + (NTEN == 4 ? 2 * K::XB + K::YB : K::XB + K::YB), tb[1]);
+    };
 
     // Position of the tile a copy reads.  A cursor walks the chunk's tiles in
     // order (32 tokens on, or to the next sequence); tiles past the chunk
@@ -370,7 +473,11 @@ __device__ __forceinline__ void stats_wave(const StatsArgs &a, const StatsCtx c,
         for (int part = 0; part < 4; ++part) issue_part(q, st, part);
     };
     auto wait_tiles = [&](int n) {                           // at most n tiles of this wave's copies in flight
-        if constexpr (CP::STATIC) {
+        if constexpr (RS != 0) {
+            // tiles t+1 / t+2 / t+3 (and their table entries) follow the one waited for
+            if (n == 3) wait_vm<2 * PT>();                   // the prologue waited for tiles 0 and 1 already
+            else wait_vm<NTB + 2 * PT>();
+        } else if constexpr (CP::STATIC) {
             if (n == 3) wait_vm<3 * (L + 1)>();
             else wait_vm<2 * (L + 1)>();
         } else {
@@ -380,11 +487,43 @@ __device__ __forceinline__ void stats_wave(const StatsArgs &a, const StatsCtx c,
 
     // prologue: tiles 0..3 fill the ring
     TilePos cur = tile_at(0);
-#pragma unroll
-    for (int t = 0; t < K::NST; ++t) {
-        issue(cur, t);
+    TabSet tA, tB;                                           // table entries of the even / odd tiles
+    if constexpr (RS != 0) {
+        // tiles 0 and 1 are turned here, before the loop reads them
+        issue(cur, 0);
+        tab_load(tA, cur);
+        tile_next(cur);
+        issue(cur, 1);
+        tab_load(tB, cur);
+        tile_next(cur);
+        wait_vm_tied<0>(tA);
+        wait_vm_tied<0>(tB);
+        turn_tile(tA, 0);
+        turn_tile(tB, 1);
+        issue(cur, 2);
+        tab_load(tA, cur);
+        tile_next(cur);
+        issue(cur, 3);
+        tab_load(tB, cur);
         tile_next(cur);                                      // ends at tile 4, the first one the loop copies
+    } else {
+#pragma unroll
+        for (int t = 0; t < K::NST; ++t) {
+            issue(cur, t);
+            tile_next(cur);                                  // ends at tile 4, the first one the loop copies
+        }
     }
+    // In iteration t, after the copies of tile t + 4: tile t + 2 is turned with
+    // its table entries (register set of its parity), whose set then receives
+    // the entries of tile t + 4.  Only tile t + 3 and its entries and tile
+    // t + 4's copies may still be in flight then.
+    auto turn_ahead = [&](TabSet &tb, int t, const TilePos &q4) __attribute__((always_inline)) {
+        if constexpr (RS != 0) {
+            wait_vm_tied<PT + L + 1>(tb);
+            turn_tile(tb, (t + 2) % K::NST);
+            tab_load(tb, q4);
+        }
+    };
 
     if (slot >= c.n_slots) {
         // A wave without a map (single-map item) only helps with the copies; it
@@ -392,11 +531,19 @@ __device__ __forceinline__ void stats_wave(const StatsArgs &a, const StatsCtx c,
         // loop, one per tile of the loop's even trip count).
         wait_tiles(3);
         lds_barrier();
-        for (int t = 0; t < ((c.n_tiles + 1) & ~1); ++t) {
+        for (int t = 0; t < ((c.n_tiles + 1) & ~1); t += 2) {
             wait_tiles(2);
             lds_barrier();
-            issue(cur, t % K::NST);
+            TilePos q = cur;
+            issue(q, t % K::NST);
             tile_next(cur);
+            turn_ahead(tA, t, q);
+            wait_tiles(2);
+            lds_barrier();
+            q = cur;
+            issue(q, (t + 1) % K::NST);
+            tile_next(cur);
+            turn_ahead(tB, t + 1, q);
         }
         wait_vm<0>();
         return;
@@ -598,7 +745,8 @@ __device__ __forceinline__ void stats_wave(const StatsArgs &a, const StatsCtx c,
     // quarter of the folds and of the copies of tile t+4, which the compiler
     // interleaves with the MFMAs.  A single wave per SIMD issues all of them,
     // so an even mix keeps the matrix core fed.
-    auto iteration = [&](int t, const Ops &i0, const Ops &i1, const Half &f0, Ops &n0, Ops &n1, Half &f2) {
+    auto iteration = [&](int t, const Ops &i0, const Ops &i1, const Half &f0, Ops &n0, Ops &n1, Half &f2,
+                         TabSet &tb) {
         const TilePos q = cur;                               // tile t+4
         tile_next(cur);
         wait_tiles(2);                                       // tile t+1 has landed
@@ -628,6 +776,7 @@ __device__ __forceinline__ void stats_wave(const StatsArgs &a, const StatsCtx c,
         interleave();
         __builtin_amdgcn_sched_barrier(0);
         issue_part(q, st, 3);
+        turn_ahead(tb, t, q);
         if (NR > 1) fold_row(f2, n0, NR - 1);
         fold_sums(n0, 1);
         mma_lo(f1, i1);
@@ -642,8 +791,8 @@ __device__ __forceinline__ void stats_wave(const StatsArgs &a, const StatsCtx c,
     read_ops(a1, 0, 1);
     fold(fa, a0);
     for (int t = 0; t < c.n_tiles; t += 2) {                 // an odd count ends with a zero-weight tile
-        iteration(t, a0, a1, fa, b0, b1, fb);
-        iteration(t + 1, b0, b1, fb, a0, a1, fa);
+        iteration(t, a0, a1, fa, b0, b1, fb, tA);
+        iteration(t + 1, b0, b1, fb, a0, a1, fa, tB);
     }
     wait_vm<0>();                                            // drain the trailing copies before leaving
 
@@ -671,7 +820,7 @@ __device__ __forceinline__ void stats_wave(const StatsArgs &a, const StatsCtx c,
     if (PR == 0) P[K::SUMW + lane] = sumw;
 }
 
-template <int DS, int DT, bool RAGGED, bool CENTER>
+template <int DS, int DT, bool RAGGED, bool CENTER, int RS = 0>
 __global__ __attribute__((amdgpu_flat_work_group_size(Cfg<DS, DT>::NT, Cfg<DS, DT>::NT),
                           amdgpu_waves_per_eu(1, 1)))
 void stats_kernel(StatsArgs a) {
@@ -699,9 +848,9 @@ void stats_kernel(StatsArgs a) {
     if (c.n_tiles == 0) return;
 
     // wave -> (slot, pair): one wave per SIMD
-#define CB_WAVE(NTEN)                                                                           \
-    if ((wave & 1) == 0) stats_wave<DS, DT, RAGGED, CENTER, NTEN, 0>(a, c, it, lds, wave, lane); \
-    else stats_wave<DS, DT, RAGGED, CENTER, NTEN, 1>(a, c, it, lds, wave, lane);
+#define CB_WAVE(NTEN)                                                                               \
+    if ((wave & 1) == 0) stats_wave<DS, DT, RAGGED, CENTER, NTEN, 0, RS>(a, c, it, lds, wave, lane); \
+    else stats_wave<DS, DT, RAGGED, CENTER, NTEN, 1, RS>(a, c, it, lds, wave, lane);
     if (nt == 4) { CB_WAVE(4) }
     else if (nt == 3) { CB_WAVE(3) }
     else { CB_WAVE(2) }

@@ -174,17 +174,39 @@ def test_rope_entry_points_reject_bad_arguments_on_the_host():
     c = cb.CbCache()
     c.data, c.n_layers, c.n_heads, c.head_dim, c.n_seqs, c.seq_len = 256, 1, 1, 40, 1, 8
     c.s_layer, c.s_kv, c.s_seq, c.s_head, c.s_tok = 640, 320, 320, 320, 40
-    call = lambda style=0, n_pos=64, off=0: lib.cb_rope(ctypes.byref(c), ctypes.byref(c), ctypes.c_void_p(256),  # noqa
-                                                        n_pos, style, 0, off, None)
-    assert call() == 6                                   # head_dim 40 is not a multiple of 16
+
+    def spec(head_dim=64, n_pos=64, style=0, off=0, table=256):
+        sp = cb.CbRopeSpec()
+        sp.table, sp.head_dim, sp.n_pos, sp.style, sp.pos_offset = table, head_dim, n_pos, style, off
+        return sp
+
+    def call(**kw):
+        sp = spec(**kw)
+        return lib.cb_rope(ctypes.byref(c), ctypes.byref(c), ctypes.byref(sp), 0, None)
+    assert call(head_dim=40) == 6                        # head_dim 40 is not a multiple of 16
     c.head_dim, c.s_tok, c.s_head, c.s_seq, c.s_kv, c.s_layer = 64, 64, 512, 512, 512, 1024
+    assert lib.cb_rope(ctypes.byref(c), ctypes.byref(c), None, 0, None) == 1
     assert call(style=2) == 1
     assert call(n_pos=6) == 2                            # positions 0..7 need 8 table rows
     assert call(off=60) == 2
-    # the fused mapping: a NULL plan, then an unknown style, before anything else
-    ar = lambda plan, style=0: lib.cb_apply_rope(plan, ctypes.c_void_p(256), ctypes.byref(c),  # noqa: E731
-                                                 ctypes.byref(c), ctypes.c_void_p(256), 64, style, 0, None)
-    assert ar(None) == 1
+    assert call(head_dim=128) == 2                       # a table built for another head width
+    assert call(head_dim=32) == 2
+    assert call(table=0) == 1
+    assert call(table=264) == 3                          # tables are 16-byte aligned
+    # the fused mapping and statistics: a NULL plan is refused before anything else
+    sp = spec()
+    assert lib.cb_apply_rope(None, ctypes.c_void_p(256), ctypes.byref(c), ctypes.byref(c), None,
+                             ctypes.byref(sp), None) == 1
+    assert lib.cb_stats_accumulate_rope(None, ctypes.byref(c), ctypes.byref(c), ctypes.c_void_p(256), 8,
+                                        ctypes.c_void_p(256), ctypes.c_void_p(256), ctypes.byref(sp), None,
+                                        None) == 1
+    # the Python descriptor takes head_dim and n_pos from the table's shape
+    import torch
+    t = torch.zeros((40, 64, 2), dtype=torch.float32)
+    d = cb.rope_spec(t, 1, 7)
+    assert (d.head_dim, d.n_pos, d.style, d.pos_offset) == (128, 40, 1, 7)
+    with pytest.raises(ValueError):
+        cb.rope_spec(t.reshape(40, 128))
 
 
 def test_multi_layer_entry_points_reject_bad_arguments_on_the_host():

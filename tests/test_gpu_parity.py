@@ -935,6 +935,101 @@ def test_rope_matches_oracle(cb, d, style, inverse):
     assert torch.equal(op, out) and torch.equal(xp, out)
 
 
+def rotated_caches(cb, wl, ts, tt, style, off, hm_override=None):
+    """Caches as a model holds them: content rows generated for wl, then their K
+    rows turned by the oracle's RoPE (source base ts, target base tt) at
+    positions off + tok; returned as device tensors with their host bits."""
+    src_c, tgt_c, w = make_inputs(wl)
+    as_bf16 = lambda b: torch.from_numpy(b.view(np.int16)).to("cuda").view(torch.bfloat16)  # noqa: E731
+    sb = oracle.rope(bits(src_c), src_c.stride()[:5], wl.L_s, wl.H_s, wl.d_s, wl.n_seqs, wl.seq_len, ts, style,
+                     pos_offset=off)
+    tb = oracle.rope(bits(tgt_c), tgt_c.stride()[:5], wl.L_t, wl.H_t, wl.d_t, wl.n_seqs, wl.seq_len, tt, style,
+                     pos_offset=off)
+    return as_bf16(sb), as_bf16(tb), w, sb, tb
+
+
+@pytest.mark.parametrize("d,style,T,off,sides,kind", [
+    (128, 0, 256, 0, "both", "qwen"),          # whole tiles, shared-source items
+    (128, 1, 300, 37, "both", "qwen"),         # ragged last tile, interleaved pairs
+    (128, 0, 200, 900, "both", "odd"),         # an odd map count: a single-map item with copy-only waves
+    (64, 0, 200, 1000, "src", "identity"),     # only the source turns
+    (64, 1, 96, 5, "tgt", "qwen"),             # only the target turns
+])
+def test_stats_rope_fused_equals_separate_passes_and_oracle(cb, d, style, T, off, sides, kind):
+    # the de-rotation folded into the gather gives bit for bit the moments of
+    # cb_rope(inverse) copies, and matches the oracle's composition (rope
+    # inverse in fp64, one rounding, then the moments)
+    wl = synth.Workload("strope", 4 if kind == "identity" else 3, 2, d, 4, 2, d, 3, T,
+                        "qwen" if kind == "odd" else kind, "scaled", 0.1, "lognormal")
+    ts, tt = 1e4, 1e6
+    src, tgt, w, sb, tb = rotated_caches(cb, wl, ts, tt, style, off)
+    hm = synth.head_map(wl)
+    if kind == "odd":
+        hm = {f: v[[0, 3, 6, 9, 12]] for f, v in hm.items()}          # five maps
+    plan = cb.cb_plan_create(hm, src, tgt, wl.n_seqs * T)
+    tab_s = gpu_rope_table(cb, ts, d, off + T)
+    tab_t = gpu_rope_table(cb, tt, d, off + T)
+    sr = cb.rope_spec(tab_s, style, off) if sides in ("both", "src") else None
+    tr = cb.rope_spec(tab_t, style, off) if sides in ("both", "tgt") else None
+    say(f"stats rope d={d} style={style} T={T} off={off} sides={sides} maps={plan.n_maps}")
+    n, P = plan.n_maps, plan.P
+    G = torch.empty((n, P, P), dtype=torch.float32, device="cuda")
+    C = torch.empty((n, P, d), dtype=torch.float32, device="cuda")
+    cb.cb_stats_zero(plan, G, C)
+    cb.cb_stats_accumulate_rope(plan, src, tgt, w, G, C, sr, tr)
+    # separate passes: de-rotated copies, then the plain kernel
+    src_d = src.clone()
+    tgt_d = tgt.clone()
+    if sr is not None:
+        cb.cb_rope(src, src_d, tab_s, style, True, off)
+    if tr is not None:
+        cb.cb_rope(tgt, tgt_d, tab_t, style, True, off)
+    G2, C2 = gpu_stats(cb, plan, src_d, tgt_d, w)
+    torch.cuda.synchronize()
+    # oracle: the composition in fp64
+    so = sb if sr is None else oracle.rope(sb, src.stride()[:5], wl.L_s, wl.H_s, d, wl.n_seqs, T, ts, style,
+                                           inverse=True, pos_offset=off)
+    to = tb if tr is None else oracle.rope(tb, tgt.stride()[:5], wl.L_t, wl.H_t, d, wl.n_seqs, T, tt, style,
+                                           inverse=True, pos_offset=off)
+    Go, Co = oracle.stats(hm, so, src.stride()[:5], d, to, tgt.stride()[:5], d, w.cpu().numpy(),
+                          wl.n_seqs * T, wl.n_seqs, T, n_threads=NTHREADS)
+    # The products (G and C without their bias row and column) are bit for bit
+    # those of the separate passes; the fp32 bias sums (sum w, sum w x, sum w y)
+    # may round differently between the two compiled kernels, by a few fp32
+    # ulps of each sum (2^-24 ~ 6e-8 relative), which bounds the whole matrix.
+    eb = max(max(relF(G[m].double().cpu().numpy(), G2[m].double().cpu().numpy()),
+                 relF(C[m].double().cpu().numpy(), C2[m].double().cpu().numpy())) for m in range(n))
+    same = torch.equal(G[:, :P - 1, :P - 1], G2[:, :P - 1, :P - 1]) and torch.equal(C[:, :P - 1], C2[:, :P - 1])
+    say(f"  fused vs separate: products bitwise {same}, G and C relF {eb:.2e}")
+    assert same and eb <= 1e-7
+    check_stats(G, C, Go, Co, list(range(n)))
+    # the keys did turn: the moments of the rotated caches as they are differ
+    G3, _ = gpu_stats(cb, plan, src, tgt, w)
+    kmaps = [m for m in range(n) if hm["kv"][m] == 0]
+    vmaps = [m for m in range(n) if hm["kv"][m] == 1]
+    assert not torch.equal(G[kmaps], G3[kmaps])
+    assert torch.equal(G[vmaps][:, :P - 1, :P - 1], G3[vmaps][:, :P - 1, :P - 1])
+    plan.close()
+
+
+def test_stats_rope_rejects_what_it_cannot_fuse(cb):
+    wl = synth.Workload("strope96", 2, 2, 96, 2, 2, 128, 2, 64, "qwen", "scaled", 0.1, "lognormal")
+    src, tgt, w = make_inputs(wl)
+    plan = cb.cb_plan_create(synth.head_map(wl), src, tgt, 1024)
+    G = torch.zeros((plan.n_maps, plan.P, plan.P), dtype=torch.float32, device="cuda")
+    C = torch.zeros((plan.n_maps, plan.P, plan.d_t), dtype=torch.float32, device="cuda")
+    tab96, tab128 = gpu_rope_table(cb, 1e4, 96, 64), gpu_rope_table(cb, 1e4, 128, 64)
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_UNSUPPORTED"):
+        cb.cb_stats_accumulate_rope(plan, src, tgt, w, G, C, cb.rope_spec(tab96), None)
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_SHAPE"):
+        cb.cb_stats_accumulate_rope(plan, src, tgt, w, G, C, cb.rope_spec(tab128), None)   # d_s is 96
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_SHAPE"):
+        cb.cb_stats_accumulate_rope(plan, src, tgt, w, G, C, None, cb.rope_spec(tab128[:63]))
+    torch.cuda.synchronize()
+    assert not G.any() and not C.any()
+    plan.close()
+
+
 def check_apply_rotated(ob, ref, label=""):
     """check_apply for caches whose K rows (kv 0) were rotated after rounding:
     a difference of one bf16 ulp in a pair before the rotation moves both rotated
@@ -972,7 +1067,7 @@ def test_apply_rope_matches_oracle(cb, d_s, d_t, style, off):
     out = torch.zeros((wl.L_t, 2, wl.n_seqs, wl.H_t, wl.seq_len, d_t), dtype=torch.bfloat16, device="cuda")
     plain = torch.zeros_like(out)
     say(f"apply_rope d_s={d_s} d_t={d_t} style={style} offset={off}")
-    cb.cb_apply_rope(plan, maps, src, out, table, style, off)
+    cb.cb_apply_rope(plan, maps, src, out, cb.rope_spec(table, style, off))
     cb.cb_apply(plan, maps, src, plain)
     torch.cuda.synchronize()
     ref = np.zeros(tuple(out.shape), dtype=np.uint16)
@@ -983,7 +1078,7 @@ def test_apply_rope_matches_oracle(cb, d_s, d_t, style, off):
     assert np.array_equal(ob[:, 1], bits(plain).reshape(ref.shape)[:, 1])     # V: bitwise cb_apply
     assert not np.array_equal(ob[:, 0], bits(plain).reshape(ref.shape)[:, 0])
     with pytest.raises(cb.CacheBridgeError, match="CB_ERR_SHAPE"):
-        cb.cb_apply_rope(plan, maps, src, out, table[: off + wl.seq_len - 1], style, off)
+        cb.cb_apply_rope(plan, maps, src, out, cb.rope_spec(table[: off + wl.seq_len - 1], style, off))
     plan.close()
 
 
@@ -1003,14 +1098,14 @@ def test_apply_rope_edge_cases(cb):
     assert torch.equal(out, keep)
     plain = torch.zeros_like(out)
     for style in (0, 1):
-        cb.cb_apply_rope(plan, maps, src, out, table, style, 0)
+        cb.cb_apply_rope(plan, maps, src, out, cb.rope_spec(table, style, 0))
         cb.cb_apply(plan, maps, src, plain)
         torch.cuda.synchronize()
         assert torch.equal(out, plain)
     with pytest.raises(cb.CacheBridgeError, match="CB_ERR_INVALID_ARGUMENT"):
-        cb.cb_apply_rope(plan, maps, src, out, table, 2, 0)
+        cb.cb_apply_rope(plan, maps, src, out, cb.rope_spec(table, 2, 0))
     with pytest.raises(cb.CacheBridgeError, match="CB_ERR_SHAPE"):
-        cb.cb_apply_rope(plan, maps, src, out, table, 0, 4)             # position 4 needs 5 rows
+        cb.cb_apply_rope(plan, maps, src, out, cb.rope_spec(table, 0, 4))             # position 4 needs 5 rows
     plan.close()
 
 
