@@ -1213,11 +1213,12 @@ cb_status cb_rope(const cb_cache *in, const cb_cache *out, const cb_rope_spec *r
     return ok();
 }
 
-// Single-layer application, optionally with the target's rotary transform
-// applied to the K outputs before their rounding (rope_table non-NULL).
+// Single-layer application, optionally with the sender's rotary transform
+// removed from the K source rows as they land (src_rope) and the target's
+// applied to the K outputs before their rounding (tgt_rope); both specs are
+// checked by the caller.
 static cb_status apply_single(cb_plan *p, const float *maps, const cb_cache *src, const cb_cache *tgt_out,
-                              const float *rope_table, int32_t rope_n_pos, int32_t rope_style,
-                              int32_t rope_pos_offset, void *stream) {
+                              const cb_rope_spec *src_rope, const cb_rope_spec *tgt_rope, void *stream) {
     if (p->duplicate_targets)
         return fail(CB_ERR_INVALID_ARGUMENT, "the plan maps some target (layer, kv, head) more than once; "
                                              "cb_apply needs one map per target");
@@ -1229,12 +1230,9 @@ static cb_status apply_single(cb_plan *p, const float *maps, const cb_cache *src
     if (((uintptr_t)maps) % 4) return fail(CB_ERR_MISALIGNED, "maps must be 4-byte aligned");
     const int64_t N = (int64_t)src->n_seqs * src->seq_len;
     if (N > (int64_t)INT32_MAX - 4096) return fail(CB_ERR_UNSUPPORTED, "too many tokens in one call");
-    if (rope_table) {
-        if (rope_pos_offset < 0 || (int64_t)rope_pos_offset + src->seq_len > rope_n_pos)
-            return fail(CB_ERR_SHAPE, "positions %d .. %lld need a table of that many rows (n_pos = %d)",
-                        rope_pos_offset, (long long)rope_pos_offset + src->seq_len - 1, rope_n_pos);
-        if (((uintptr_t)rope_table) % 16) return fail(CB_ERR_MISALIGNED, "table must be 16-byte aligned");
-    }
+    if (src_rope && p->d_s != 64 && p->d_s != 128)
+        return fail(CB_ERR_UNSUPPORTED, "the fused source de-rotation takes d_s = 64 or 128 (got %d); "
+                                        "turn the sender with cb_rope first", p->d_s);
     if (cb_status s = check_device(p)) return s;
     hipStream_t st = (hipStream_t)stream;
     if (cb::launch_split_maps(p->n_maps, p->d_s, p->d_t, maps, p->d_whi, p->d_wlo, p->d_bias, st) != hipSuccess)
@@ -1262,9 +1260,12 @@ static cb_status apply_single(cb_plan *p, const float *maps, const cb_cache *src
     a.w_hi = p->d_whi;
     a.w_lo = p->d_wlo;
     a.bias = p->d_bias;
-    a.rope_table = rope_table;
-    a.rope_style = rope_style;
-    a.rope_pos_offset = rope_pos_offset;
+    a.rope_table = tgt_rope ? tgt_rope->table : nullptr;
+    a.rope_style = tgt_rope ? tgt_rope->style : 0;
+    a.rope_pos_offset = tgt_rope ? tgt_rope->pos_offset : 0;
+    a.src_rope_table = src_rope ? src_rope->table : nullptr;
+    a.src_rope_style = src_rope ? src_rope->style : 0;
+    a.src_rope_pos_offset = src_rope ? src_rope->pos_offset : 0;
     if ((int64_t)p->n_groups * a.n_tiles > (int64_t)INT32_MAX)
         return fail(CB_ERR_UNSUPPORTED, "too many application workgroups");
     if (cb::launch_apply(p->d_s, p->d_t, p->n_groups, a, st) != hipSuccess)
@@ -1318,7 +1319,7 @@ cb_status cb_apply(cb_plan *p, const float *maps, const cb_cache *src, const cb_
             return fail(CB_ERR_DEVICE, "multi-layer application kernel launch failed");
         return ok();
     }
-    return apply_single(p, maps, src, tgt_out, nullptr, 0, 0, 0, stream);
+    return apply_single(p, maps, src, tgt_out, nullptr, nullptr, stream);
 }
 
 cb_status cb_apply_rope(cb_plan *p, const float *maps, const cb_cache *src, const cb_cache *tgt_out,
@@ -1330,9 +1331,8 @@ cb_status cb_apply_rope(cb_plan *p, const float *maps, const cb_cache *src, cons
         if (cb_status s = check_rope("src_rope", src_rope, p->d_s, src->seq_len)) return s;
     if (tgt_rope)
         if (cb_status s = check_rope("tgt_rope", tgt_rope, p->d_t, src->seq_len)) return s;
-    if (p->multi || src_rope) return fail(CB_ERR_UNSUPPORTED, "not yet wired");
-    return apply_single(p, maps, src, tgt_out, tgt_rope->table, tgt_rope->n_pos, tgt_rope->style,
-                        tgt_rope->pos_offset, stream);
+    if (p->multi) return fail(CB_ERR_UNSUPPORTED, "not yet wired");
+    return apply_single(p, maps, src, tgt_out, src_rope, tgt_rope, stream);
 }
 
 }  // extern "C"

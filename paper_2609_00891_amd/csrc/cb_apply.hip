@@ -18,6 +18,15 @@
 //   staging buffer and leaves as whole target rows.  A source block shared by
 //   two target maps is read once.
 //
+// With the sender's rotary transform removed on the way in (Sec. 2.1, Sec.
+// 3.1: the maps act on content coordinates), the copy wave also moves each
+// sub-block's slice of the source table, [32 tokens][d_s/2][cos, sin], into
+// LDS behind its rows, and the computing waves turn sub-block sb + 1 back in
+// LDS (one chunk pair per lane, products as cb_rope's inverse, one rounding
+// to bf16) while they multiply sub-block sb; the next barrier publishes it.
+// The copy wave therefore waits for one more sub-block before each barrier,
+// and the ring is five stages deep (rows and table slice per stage).
+//
 // With the target's rotary transform fused (Sec. 2.1, Sec. 3.1: the mapped
 // keys receive the target's RoPE), the K outputs are turned in fp32 before
 // the single rounding.  Style (2i, 2i+1) pairs sit in accumulator registers
@@ -78,7 +87,7 @@ __global__ __launch_bounds__(256) void split_maps_kernel(int n_maps, int d_s, in
     }
 }
 
-template <int DS, int DT>
+template <int DS, int DT, int SR = 0>
 struct ACfg {
     static constexpr int KS = DS / 16;              // MFMA K steps over source channels
     static constexpr int RBT = DT / 32;             // 32-row blocks of target channels
@@ -89,9 +98,13 @@ struct ACfg {
     static constexpr int NCB = DS / 8;              // 16-byte blocks per source row
     static constexpr int ROWB = DS * 2;             // bytes per source row
     static constexpr int BUFB = SB * ROWB;          // bytes per ring stage
-    static constexpr int COPIES = BUFB / 1024;      // copy instructions per stage (64 lanes x 16 B)
-    static constexpr int NST = 8;                   // ring stages
+    static constexpr int RCOPIES = BUFB / 1024;     // row copy instructions per stage (64 lanes x 16 B)
+    static constexpr int TABB = SR ? SB * DS * 4 : 0;   // table slice: [SB tokens][DS/2][cos, sin] fp32
+    static constexpr int COPIES = RCOPIES + TABB / 1024;
+    static constexpr int STB = BUFB + TABB;         // bytes per ring stage
+    static constexpr int NST = SR ? 5 : 8;          // ring stages
     static_assert(BUFB % 1024 == 0, "a stage is a whole number of copy instructions");
+    static_assert(SR == 0 || DS == 64 || DS == 128, "the source de-rotation takes d_s = 64 or 128");
 };
 
 // Rotated position of 16-byte block cb of token row t in LDS: 16 consecutive
@@ -131,10 +144,10 @@ __device__ __forceinline__ int out_channel(int rb, int i) {
 // vmcnt waits are exact.  One barrier per sub-block publishes the landed
 // stage to the computing waves and tells the copy wave that the stage read
 // one sub-block earlier is free again.
-template <int DS, int DT, int RS>
+template <int DS, int DT, int RS, int SR>
 __global__ __attribute__((amdgpu_flat_work_group_size(ACfg<DS, DT>::NT, ACfg<DS, DT>::NT))) void apply_kernel(ApplyArgs a) {
-    using K = ACfg<DS, DT>;
-    __shared__ __attribute__((aligned(16))) char lds[K::NST * K::BUFB];
+    using K = ACfg<DS, DT, SR>;
+    __shared__ __attribute__((aligned(16))) char lds[K::NST * K::STB];
     // Without the rotation the outputs go through an LDS staging buffer and
     // leave as whole target rows (16 lanes per row): about 4% faster than
     // each wave storing its 32-channel slices.  With it, the direct stores
@@ -158,12 +171,13 @@ __global__ __attribute__((amdgpu_flat_work_group_size(ACfg<DS, DT>::NT, ACfg<DS,
     const int kv = grp->kv;
     const uint16_t *xsrc = a.src + grp->src_layer * a.ss.layer + kv * a.ss.kv + grp->src_head * a.ss.head;
 
+    const bool turn_src = SR != 0 && kv == 0;                 // only keys carry positions
     if (wave == K::NWC) {
         // ---- copy wave: copy i of a stage moves LDS chunks 64 i + lane
         const uint32_t lds_base = (uint32_t)(uintptr_t)lds;
         auto issue = [&](int sb, int st) {
 #pragma unroll
-            for (int i = 0; i < K::COPIES; ++i) {
+            for (int i = 0; i < K::RCOPIES; ++i) {
                 const int q = 64 * i + lane;
                 const int t = q / K::NCB, p = q - (q / K::NCB) * K::NCB;
                 const int cb = (p + K::NCB - t % K::NCB) % K::NCB;     // inverse of the rotation
@@ -171,13 +185,30 @@ __global__ __attribute__((amdgpu_flat_work_group_size(ACfg<DS, DT>::NT, ACfg<DS,
                 const uint32_t b = fastdiv((uint32_t)tau, a.T);
                 const uint32_t tt = (uint32_t)tau - b * a.T.d;
                 const uint16_t *src = xsrc + (int64_t)b * a.ss.seq + (int64_t)tt * a.ss.tok + cb * 8;
-                dma16(src, __builtin_amdgcn_readfirstlane(lds_base + st * K::BUFB + i * 1024));
+                dma16(src, __builtin_amdgcn_readfirstlane(lds_base + st * K::STB + i * 1024));
+            }
+            if constexpr (SR != 0) {
+                // the rows' table entries: token t's DS floats at slice byte t * DS * 4
+#pragma unroll
+                for (int i = 0; i < K::COPIES - K::RCOPIES; ++i) {
+                    const int q = 1024 * i + 16 * lane;                // byte in the slice
+                    const int t = q / (DS * 4), off = q - t * (DS * 4);
+                    const int tau = min(tok0 + sb * K::SB + t, tok1 - 1);
+                    const uint32_t tt = (uint32_t)tau - fastdiv((uint32_t)tau, a.T) * a.T.d;
+                    const char *g = (const char *)(a.src_rope_table + (int64_t)(a.src_rope_pos_offset + (int)tt) * DS) + off;
+                    dma16(g, __builtin_amdgcn_readfirstlane(lds_base + st * K::STB + K::BUFB + i * 1024));
+                }
             }
         };
 #pragma unroll
         for (int s = 0; s < K::NST - 1; ++s) issue(s, s);
+        if constexpr (SR != 0) {
+            wait_vm<(K::NST - 3) * K::COPIES>();               // sub-blocks 0 and 1 have landed
+            lds_barrier();
+        }
         for (int sb = 0; sb < n_sb; ++sb) {
-            wait_vm<(K::NST - 2) * K::COPIES>();               // sub-block sb has landed
+            // sub-block sb has landed (and, with the de-rotation, sb + 1, which is turned during sb)
+            wait_vm<(K::NST - 2 - (SR != 0 ? 1 : 0)) * K::COPIES>();
             lds_barrier();
             issue(sb + K::NST - 1, (sb + K::NST - 1) % K::NST);
         }
@@ -222,10 +253,64 @@ __global__ __attribute__((amdgpu_flat_work_group_size(ACfg<DS, DT>::NT, ACfg<DS,
     // exchange below: MFMA rows 8 lhalf .. +7 and 16 + 8 lhalf .. +7)
     const int oc0 = out_channel<DT, RS>(rb, 8 * (int)lhalf), oc1 = out_channel<DT, RS>(rb, 16 + 8 * (int)lhalf);
 
+    // ---- de-rotation of a landed sub-block (SR != 0): pair u = 64 wave + lane
+    // of its rows, token row t = u / (NCB/2), logical chunks c and c + NCB/2
+    constexpr int HP = K::NCB / 2;
+    auto turn_sub = [&](int sb) __attribute__((always_inline)) {
+        if constexpr (SR != 0) {
+            const int u = 64 * wave + lane;
+            if (u >= K::SB * HP) return;
+            const int t = u / HP, c = u - (u / HP) * HP;
+            char *B = lds + (sb % K::NST) * K::STB;
+            char *pa = B + t * (K::NCB * 16) + ((c + t) % K::NCB) * 16;
+            char *pb = B + t * (K::NCB * 16) + ((c + HP + t) % K::NCB) * 16;
+            const float *row = (const float *)(B + K::BUFB + t * DS * 4);
+            float4 cs[4];
+            if constexpr (SR == 1) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) cs[j] = *reinterpret_cast<const float4 *>(row + 16 * c + 4 * j);
+            } else {
+                cs[0] = *reinterpret_cast<const float4 *>(row + 8 * c);
+                cs[1] = *reinterpret_cast<const float4 *>(row + 8 * c + 4);
+                cs[2] = *reinterpret_cast<const float4 *>(row + 8 * (c + HP));
+                cs[3] = *reinterpret_cast<const float4 *>(row + 8 * (c + HP) + 4);
+            }
+            const uint4 A = *reinterpret_cast<const uint4 *>(pa);
+            const uint4 Bv = *reinterpret_cast<const uint4 *>(pb);
+            const uint32_t av[4] = {A.x, A.y, A.z, A.w}, bv[4] = {Bv.x, Bv.y, Bv.z, Bv.w};
+            uint32_t oa[4], ob[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float x0 = __uint_as_float(av[e] << 16), x1 = __uint_as_float(av[e] & 0xffff0000u);
+                const float y0 = __uint_as_float(bv[e] << 16), y1 = __uint_as_float(bv[e] & 0xffff0000u);
+                if constexpr (SR == 1) {
+                    // pairs (8c + 2e + h, d/2 further on), frequency 8c + 2e + h: the inverse turn
+                    const float c0 = cs[e].x, s0 = cs[e].y, c1 = cs[e].z, s1 = cs[e].w;
+                    oa[e] = pack_bf16(__builtin_fmaf(x0, c0, y0 * s0), __builtin_fmaf(x1, c1, y1 * s1));
+                    ob[e] = pack_bf16(__builtin_fmaf(y0, c0, -(x0 * s0)), __builtin_fmaf(y1, c1, -(x1 * s1)));
+                } else {
+                    // pairs (2i, 2i + 1) inside each chunk: frequencies 4c + e and 4(c + NCB/2) + e
+                    const float4 qa = cs[e >> 1], qb = cs[2 + (e >> 1)];
+                    const float ca = (e & 1) ? qa.z : qa.x, sa = (e & 1) ? qa.w : qa.y;
+                    const float cb2 = (e & 1) ? qb.z : qb.x, sb2 = (e & 1) ? qb.w : qb.y;
+                    oa[e] = pack_bf16(__builtin_fmaf(x0, ca, x1 * sa), __builtin_fmaf(x1, ca, -(x0 * sa)));
+                    ob[e] = pack_bf16(__builtin_fmaf(y0, cb2, y1 * sb2), __builtin_fmaf(y1, cb2, -(y0 * sb2)));
+                }
+            }
+            *reinterpret_cast<uint4 *>(pa) = make_uint4(oa[0], oa[1], oa[2], oa[3]);
+            *reinterpret_cast<uint4 *>(pb) = make_uint4(ob[0], ob[1], ob[2], ob[3]);
+        }
+    };
+    if constexpr (SR != 0) {
+        lds_barrier();                                         // sub-blocks 0 and 1 have landed
+        if (turn_src) turn_sub(0);
+    }
+
     // With staging, iteration sb stores the rows of sub-block sb - 1 (written to
     // the staging buffer before the barrier), and one more iteration follows.
     for (int sb = 0; sb < n_sb + (STAGE ? 1 : 0); ++sb) {
-        lds_barrier();                                         // sub-block sb has landed
+        lds_barrier();                                         // sub-block sb has landed (and is turned)
+        if (SR != 0 && turn_src && sb + 1 < n_sb) turn_sub(sb + 1);
         if (STAGE && active && sb > 0) {
             // 4 DT chunks of 16 bytes: two rounds of the slot's RBT waves
             const char *ob = obuf + (((sb - 1) & 1) * 2 + slot) * OBUF;
@@ -244,7 +329,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(ACfg<DS, DT>::NT, ACfg<DS,
         }
         if (STAGE && sb == n_sb) break;
         if (!active) continue;
-        const char *B = lds + (sb % K::NST) * K::BUFB;
+        const char *B = lds + (sb % K::NST) * K::STB;
         const int tau = tok0 + sb * K::SB + (int)lrow;
         const uint32_t bseq = fastdiv((uint32_t)min(tau, tok1 - 1), a.T);
         const uint32_t tt = (uint32_t)min(tau, tok1 - 1) - bseq * a.T.d;
@@ -327,18 +412,28 @@ __global__ __attribute__((amdgpu_flat_work_group_size(ACfg<DS, DT>::NT, ACfg<DS,
     }
 }
 
+template <int DS, int DT, int SR>
+hipError_t launch_apply_sr(int64_t grid, const ApplyArgs &a, hipStream_t s) {
+    using K = ACfg<DS, DT>;
+    if (!a.rope_table)
+        hipLaunchKernelGGL((apply_kernel<DS, DT, kRopeNone, SR>), dim3((unsigned)grid), dim3(K::NT), 0, s, a);
+    else if (a.rope_style == 0)
+        hipLaunchKernelGGL((apply_kernel<DS, DT, kRopeHalf, SR>), dim3((unsigned)grid), dim3(K::NT), 0, s, a);
+    else
+        hipLaunchKernelGGL((apply_kernel<DS, DT, kRopeInterleaved, SR>), dim3((unsigned)grid), dim3(K::NT), 0, s, a);
+    return hipGetLastError();
+}
+
 template <int DS, int DT>
 hipError_t launch_apply_t(int n_groups, const ApplyArgs &a, hipStream_t s) {
-    using K = ACfg<DS, DT>;
     const int64_t grid = (int64_t)n_groups * a.n_tiles;
     if (grid == 0) return hipSuccess;
-    if (!a.rope_table)
-        hipLaunchKernelGGL((apply_kernel<DS, DT, kRopeNone>), dim3((unsigned)grid), dim3(K::NT), 0, s, a);
-    else if (a.rope_style == 0)
-        hipLaunchKernelGGL((apply_kernel<DS, DT, kRopeHalf>), dim3((unsigned)grid), dim3(K::NT), 0, s, a);
-    else
-        hipLaunchKernelGGL((apply_kernel<DS, DT, kRopeInterleaved>), dim3((unsigned)grid), dim3(K::NT), 0, s, a);
-    return hipGetLastError();
+    if (!a.src_rope_table) return launch_apply_sr<DS, DT, 0>(grid, a, s);
+    if constexpr (DS == 64 || DS == 128) {
+        if (a.src_rope_style == 0) return launch_apply_sr<DS, DT, 1>(grid, a, s);
+        return launch_apply_sr<DS, DT, 2>(grid, a, s);
+    }
+    return hipErrorInvalidValue;
 }
 
 }  // namespace

@@ -102,6 +102,9 @@ struct ApplyArgs {
     const float *rope_table;  // NULL, or the target's (cos, sin) [n_pos][d_t/2][2]: K outputs are rotated
     int32_t rope_style;       // 0: pairs (i, i + d_t/2), 1: pairs (2i, 2i + 1)
     int32_t rope_pos_offset;  // position of token 0 of every sequence
+    const float *src_rope_table;  // NULL, or the sender's table [n_pos][d_s/2][2]: K source rows are turned back
+    int32_t src_rope_style;
+    int32_t src_rope_pos_offset;
 };
 
 // Attention-aligned sensitivities of one call (host side of the launch).

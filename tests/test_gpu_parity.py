@@ -1082,6 +1082,77 @@ def test_apply_rope_matches_oracle(cb, d_s, d_t, style, off):
     plan.close()
 
 
+@pytest.mark.parametrize("d_s,d_t,style,off,tgt_too", [(128, 128, 0, 0, False), (128, 128, 1, 11, True),
+                                                        (64, 96, 0, 5, False), (64, 64, 0, 3000, True),
+                                                        (128, 64, 1, 700, False)])
+def test_apply_rope_source_derotation(cb, d_s, d_t, style, off, tgt_too):
+    # a sender whose keys carry RoPE: turning its K rows back as they land gives
+    # the mapping of cb_rope(inverse) copies, and matches the oracle's composition
+    # (rope inverse in fp64, one rounding, then the mapping, with the target
+    # rotation when asked)
+    wl = synth.Workload("srope", 3, 2, d_s, 4, 2, d_t, 2, 300, "qwen", "scaled", 0.1, "lognormal")
+    src_c = synth.gen_source(wl, device="cuda")
+    ts, tt = 1e4, 1e6
+    sb = oracle.rope(bits(src_c), src_c.stride()[:5], wl.L_s, wl.H_s, d_s, wl.n_seqs, wl.seq_len, ts, style,
+                     pos_offset=off)
+    src = torch.from_numpy(sb.view(np.int16)).to("cuda").view(torch.bfloat16)
+    hm = synth.head_map(wl)
+    plan = cb.cb_plan_create(hm, (wl.L_s, wl.H_s, d_s), (wl.L_t, wl.H_t, d_t), 1024)
+    maps = synth.planted_maps(wl, device="cuda")
+    tab_s = gpu_rope_table(cb, ts, d_s, off + wl.seq_len)
+    tab_t = gpu_rope_table(cb, tt, d_t, off + wl.seq_len)
+    sr = cb.rope_spec(tab_s, style, off)
+    tr = cb.rope_spec(tab_t, style, off) if tgt_too else None
+    say(f"apply source de-rotation d_s={d_s} d_t={d_t} style={style} off={off} target rotation={tgt_too}")
+    out = torch.zeros((wl.L_t, 2, wl.n_seqs, wl.H_t, wl.seq_len, d_t), dtype=torch.bfloat16, device="cuda")
+    cb.cb_apply_rope(plan, maps, src, out, tr, sr)
+    src_d = torch.empty_like(src)
+    cb.cb_rope(src, src_d, tab_s, style, True, off)
+    sep = torch.zeros_like(out)
+    cb.cb_apply_rope(plan, maps, src_d, sep, tr)
+    torch.cuda.synchronize()
+    same = float((bits(out) == bits(sep)).mean())
+    say(f"  fused vs separate passes: bitwise-equal {same:.6f}")
+    assert torch.equal(out, sep)
+    so = oracle.rope(sb, src.stride()[:5], wl.L_s, wl.H_s, d_s, wl.n_seqs, wl.seq_len, ts, style, inverse=True,
+                     pos_offset=off)
+    ref = np.zeros(tuple(out.shape), dtype=np.uint16)
+    W = maps.double().cpu().numpy()
+    if tgt_too:
+        oracle.apply_rope(hm, W, so, src.stride()[:5], d_s, ref, tuple(out.stride()[:5]), d_t, wl.n_seqs,
+                          wl.seq_len, tt, style, off, n_threads=NTHREADS)
+    else:
+        oracle.apply(hm, W, so, src.stride()[:5], d_s, ref, tuple(out.stride()[:5]), d_t, wl.n_seqs, wl.seq_len,
+                     n_threads=NTHREADS)
+    # The oracle turns the sender back in fp64, the kernel in fp32: a few inputs
+    # differ by one bf16 ulp (test_rope_matches_oracle), so the element-wise
+    # bound of check_apply (which assumes equal inputs) does not apply here.
+    # The element-wise bars are carried by that test and by
+    # test_apply_rope_matches_oracle on equal inputs; the composition is held
+    # to the relative bar and to a bitwise-equal share.
+    ob = bits(out).reshape(ref.shape)
+    e = relF(oracle.bf16_to_double(ob), oracle.bf16_to_double(ref))
+    eq = float((ob == ref).mean())
+    say(f"  against the oracle's composition: relF {e:.3e}, bitwise-equal {eq:.6f}")
+    assert e <= TOL_APPLY and eq >= 0.99
+    plan.close()
+
+
+def test_apply_rope_source_derotation_rejects_d96(cb):
+    wl = synth.Workload("srope96", 2, 2, 96, 2, 2, 128, 2, 64, "qwen", "scaled", 0.1, "lognormal")
+    src = synth.gen_source(wl, device="cuda")
+    plan = cb.cb_plan_create(synth.head_map(wl), (wl.L_s, wl.H_s, 96), (wl.L_t, wl.H_t, 128), 1024)
+    maps = synth.planted_maps(wl, device="cuda")
+    out = torch.zeros((wl.L_t, 2, wl.n_seqs, wl.H_t, wl.seq_len, 128), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_UNSUPPORTED"):
+        cb.cb_apply_rope(plan, maps, src, out, None, cb.rope_spec(gpu_rope_table(cb, 1e4, 96, 64)))
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_SHAPE"):
+        cb.cb_apply_rope(plan, maps, src, out, None, cb.rope_spec(gpu_rope_table(cb, 1e4, 128, 64)))
+    torch.cuda.synchronize()
+    assert not out.view(torch.int16).any()
+    plan.close()
+
+
 def test_apply_rope_edge_cases(cb):
     # an empty sender changes nothing; one token at position 0 equals cb_apply;
     # an unknown style is rejected before anything is enqueued
