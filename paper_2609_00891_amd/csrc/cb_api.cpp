@@ -50,6 +50,9 @@ struct cb_plan {
     uint16_t *d_whi = nullptr;
     uint16_t *d_wlo = nullptr;
     float *d_bias = nullptr;
+    // multi-layer plans with rotary keys: de-rotated K rows of the current call
+    uint16_t *d_rws = nullptr;
+    int64_t rws_bytes = 0;
 };
 
 namespace {
@@ -339,6 +342,7 @@ cb_status cb_plan_destroy(cb_plan *p) {
     (void)hipFree(p->d_aorder);
     (void)hipFree(p->d_alayers);
     (void)hipFree(p->d_mwrow);
+    (void)hipFree(p->d_rws);
     delete p;
     return ok();
 }
@@ -769,10 +773,83 @@ cb_status cb_stats_accumulate(cb_plan *p, const cb_cache *src, const cb_cache *t
     return ok();
 }
 
-// Multi-layer plans with rotary keys: not yet wired.
-static cb_status stats_multi_rope(cb_plan *, const cb_cache *, const cb_cache *, const float *, int64_t, float *,
-                                  float *, const cb_rope_spec *, const cb_rope_spec *, void *) {
-    return fail(CB_ERR_UNSUPPORTED, "rotary de-rotation on a multi-layer plan");
+// The rotation workspace of a multi-layer plan, grown to `bytes` (the old one
+// is released once the device has finished with it).
+static cb_status ensure_rws(cb_plan *p, int64_t bytes) {
+    if (bytes <= p->rws_bytes) return CB_OK;
+    (void)hipDeviceSynchronize();
+    (void)hipFree(p->d_rws);
+    p->d_rws = nullptr;
+    p->rws_bytes = 0;
+    if (hipMalloc((void **)&p->d_rws, (size_t)bytes) != hipSuccess)
+        return fail(CB_ERR_OUT_OF_MEMORY, "rotation workspace of %lld bytes", (long long)bytes);
+    p->rws_bytes = bytes;
+    return CB_OK;
+}
+
+// The K rows of cache c at tokens 0, stride, 2 stride, ... turned back by
+// their positions' angles (cb_rope's inverse arithmetic) into dst, compact:
+// [layer][seq][head][row][d] with rows = ceil(seq_len / stride); its strides
+// go to *view (kv unused).
+static cb_status derotate_rows(const cb_cache *c, const cb_rope_spec *r, int32_t stride, uint16_t *dst,
+                               cb::Strides *view, hipStream_t st) {
+    const int64_t rows = (c->seq_len + stride - 1) / stride;
+    const int64_t d = c->head_dim;
+    view->tok = d;
+    view->head = rows * d;
+    view->seq = (int64_t)c->n_heads * rows * d;
+    view->layer = (int64_t)c->n_seqs * view->seq;
+    view->kv = 0;
+    cb::RopeLaunch L = {};
+    L.in = (const uint16_t *)c->data;
+    L.out = dst;
+    L.is = strides_of(c);
+    L.is.tok = c->s_tok * stride;
+    L.os = *view;
+    L.table = r->table;
+    L.n_layers = c->n_layers;
+    L.n_heads = c->n_heads;
+    L.n_seqs = c->n_seqs;
+    L.seq_len = (int32_t)rows;
+    L.d = (int32_t)d;
+    L.style = r->style;
+    L.pos_offset = r->pos_offset;
+    L.pos_step = stride;
+    L.inverse = 1;
+    L.copy_v = 0;                                        // K rows only
+    if (cb::launch_rope(L, st) != hipSuccess) return fail(CB_ERR_DEVICE, "rope launch failed");
+    return CB_OK;
+}
+
+// Multi-layer statistics with rotary keys: each calibration row of a K block
+// is staged by many tasks (every task of every map that reads the block), so
+// the calibration rows are turned back once, gathered into a compact
+// workspace, and the K tasks read them from there.
+static cb_status stats_multi_rope(cb_plan *p, const cb_cache *src, const cb_cache *tgt, const float *weights,
+                                  int64_t w_row_stride, float *G, float *C, const cb_rope_spec *src_rope,
+                                  const cb_rope_spec *tgt_rope, void *stream) {
+    cb::MultiArgs ma = {};
+    bool empty = false;
+    if (cb_status s = prepare_multi(p, src, tgt, weights, w_row_stride, ma, empty)) return s;
+    if (empty) return ok();
+    const int64_t rows = ma.rows_per_seq;
+    const int64_t sb = src_rope ? (int64_t)p->L_s * src->n_seqs * p->H_s * rows * p->d_s : 0;
+    const int64_t tb = tgt_rope ? (int64_t)p->L_t * tgt->n_seqs * p->H_t * rows * p->d_t : 0;
+    if (cb_status s = ensure_rws(p, 2 * (sb + tb))) return s;
+    hipStream_t st = (hipStream_t)stream;
+    if (src_rope) {
+        if (cb_status s = derotate_rows(src, src_rope, p->sample_stride, p->d_rws, &ma.ssk, st)) return s;
+        ma.srck = p->d_rws;
+    }
+    if (tgt_rope) {
+        if (cb_status s = derotate_rows(tgt, tgt_rope, p->sample_stride, p->d_rws + sb, &ma.tsk, st)) return s;
+        ma.tgtk = p->d_rws + sb;
+    }
+    ma.G = G;
+    ma.C = C;
+    if (cb::launch_stats_multi(ma, st) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "multi-layer statistics kernel launch failed");
+    return ok();
 }
 
 cb_status cb_stats_accumulate_rope(cb_plan *p, const cb_cache *src, const cb_cache *tgt, const float *weights,
@@ -1209,6 +1286,7 @@ cb_status cb_rope(const cb_cache *in, const cb_cache *out, const cb_rope_spec *r
     L.pos_offset = pos_offset;
     L.inverse = inverse ? 1 : 0;
     L.copy_v = same ? 0 : 1;
+    L.pos_step = 1;
     if (cb::launch_rope(L, (hipStream_t)stream) != hipSuccess) return fail(CB_ERR_DEVICE, "rope launch failed");
     return ok();
 }
@@ -1273,52 +1351,72 @@ static cb_status apply_single(cb_plan *p, const float *maps, const cb_cache *src
     return ok();
 }
 
+// Multi-layer application, optionally with the sender's K rows turned back
+// first (src_rope: one rotation pass into the plan's workspace, which the K
+// maps then read; every source row is read by several maps) and the target's
+// rotation fused into the epilogue (tgt_rope); both specs checked by the caller.
+static cb_status apply_multi(cb_plan *p, const float *maps, const cb_cache *src, const cb_cache *tgt_out,
+                             const cb_rope_spec *src_rope, const cb_rope_spec *tgt_rope, void *stream) {
+    if (p->duplicate_targets)
+        return fail(CB_ERR_INVALID_ARGUMENT, "the plan maps some target (layer, kv, head) more than once; "
+                                             "cb_apply needs one map per target");
+    if (!maps) return fail(CB_ERR_INVALID_ARGUMENT, "maps is NULL");
+    if (cb_status s = check_cache("src", src, p->L_s, p->H_s, p->d_s)) return s;
+    if (cb_status s = check_cache("tgt_out", tgt_out, p->L_t, p->H_t, p->d_t)) return s;
+    if (src->n_seqs != tgt_out->n_seqs || src->seq_len != tgt_out->seq_len)
+        return fail(CB_ERR_SHAPE, "src and tgt_out disagree on n_seqs / seq_len");
+    if (((uintptr_t)maps) % 4) return fail(CB_ERR_MISALIGNED, "maps must be 4-byte aligned");
+    const int64_t N = (int64_t)src->n_seqs * src->seq_len;
+    if (N > (int64_t)INT32_MAX - 4096) return fail(CB_ERR_UNSUPPORTED, "too many tokens in one call");
+    if (N > 0 && (int64_t)(src->n_seqs - 1) * src->s_seq + (int64_t)(src->seq_len - 1) * src->s_tok + 128 >
+                     (int64_t)UINT32_MAX)
+        return fail(CB_ERR_UNSUPPORTED, "src rows of one (layer, kv, head) span more than 2^32 elements; "
+                                        "apply in smaller batches");
+    if (src_rope && N > 0 &&
+        (int64_t)(src->n_seqs - 1) * p->H_s * src->seq_len * p->d_s + (int64_t)src->seq_len * p->d_s > (int64_t)UINT32_MAX)
+        return fail(CB_ERR_UNSUPPORTED, "the de-rotated rows of one (layer, head) would span more than 2^32 elements; "
+                                        "apply in smaller batches");
+    if (cb_status s = check_device(p)) return s;
+    hipStream_t st = (hipStream_t)stream;
+    if (cb::launch_split_maps_frag(p->n_maps, p->k, maps, p->d_whi, p->d_bias,
+                                   tgt_rope && tgt_rope->style == CB_ROPE_HALF_SPLIT ? 1 : 0, st) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "map split launch failed");
+    if (N == 0) return ok();
+    cb::ApplyMultiArgs a = {};
+    if (src_rope) {
+        if (cb_status s = ensure_rws(p, 2 * (int64_t)p->L_s * N * p->H_s * p->d_s)) return s;
+        if (cb_status s = derotate_rows(src, src_rope, 1, p->d_rws, &a.ssk, st)) return s;
+        a.srck = p->d_rws;
+    }
+    a.src = (const uint16_t *)src->data;
+    a.out = (uint16_t *)tgt_out->data;
+    a.ss = strides_of(src);
+    a.os = strides_of(tgt_out);
+    a.T = cb::make_fastdiv((uint32_t)src->seq_len);
+    a.N = N;
+    a.k = p->k;
+    a.n_maps = p->n_maps;
+    a.n_tiles = (int32_t)((N + 255) / 256);
+    const int64_t n_tasks = (int64_t)p->n_maps * a.n_tiles;
+    if (n_tasks > (int64_t)INT32_MAX - 8) return fail(CB_ERR_UNSUPPORTED, "too many application tasks");
+    a.n_tasks = (int32_t)n_tasks;
+    a.per_xcd = (a.n_tasks + 7) / 8;
+    a.maps = p->d_amaps;
+    a.order = p->d_aorder;
+    a.src_layers = p->d_alayers;
+    a.wfrag = p->d_whi;
+    a.bias = p->d_bias;
+    a.rope_table = tgt_rope ? tgt_rope->table : nullptr;
+    a.rope_style = tgt_rope ? tgt_rope->style : 0;
+    a.rope_pos_offset = tgt_rope ? tgt_rope->pos_offset : 0;
+    if (cb::launch_apply_multi(a, p->n_cu, st) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "multi-layer application kernel launch failed");
+    return ok();
+}
+
 cb_status cb_apply(cb_plan *p, const float *maps, const cb_cache *src, const cb_cache *tgt_out, void *stream) {
     if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
-    if (p->multi) {
-        if (p->duplicate_targets)
-            return fail(CB_ERR_INVALID_ARGUMENT, "the plan maps some target (layer, kv, head) more than once; "
-                                                 "cb_apply needs one map per target");
-        if (!maps) return fail(CB_ERR_INVALID_ARGUMENT, "maps is NULL");
-        if (cb_status s = check_cache("src", src, p->L_s, p->H_s, p->d_s)) return s;
-        if (cb_status s = check_cache("tgt_out", tgt_out, p->L_t, p->H_t, p->d_t)) return s;
-        if (src->n_seqs != tgt_out->n_seqs || src->seq_len != tgt_out->seq_len)
-            return fail(CB_ERR_SHAPE, "src and tgt_out disagree on n_seqs / seq_len");
-        if (((uintptr_t)maps) % 4) return fail(CB_ERR_MISALIGNED, "maps must be 4-byte aligned");
-        const int64_t N = (int64_t)src->n_seqs * src->seq_len;
-        if (N > (int64_t)INT32_MAX - 4096) return fail(CB_ERR_UNSUPPORTED, "too many tokens in one call");
-        if (N > 0 && (int64_t)(src->n_seqs - 1) * src->s_seq + (int64_t)(src->seq_len - 1) * src->s_tok + 128 >
-                         (int64_t)UINT32_MAX)
-            return fail(CB_ERR_UNSUPPORTED, "src rows of one (layer, kv, head) span more than 2^32 elements; "
-                                            "apply in smaller batches");
-        if (cb_status s = check_device(p)) return s;
-        hipStream_t st = (hipStream_t)stream;
-        if (cb::launch_split_maps_frag(p->n_maps, p->k, maps, p->d_whi, p->d_bias, st) != hipSuccess)
-            return fail(CB_ERR_DEVICE, "map split launch failed");
-        if (N == 0) return ok();
-        cb::ApplyMultiArgs a = {};
-        a.src = (const uint16_t *)src->data;
-        a.out = (uint16_t *)tgt_out->data;
-        a.ss = strides_of(src);
-        a.os = strides_of(tgt_out);
-        a.T = cb::make_fastdiv((uint32_t)src->seq_len);
-        a.N = N;
-        a.k = p->k;
-        a.n_maps = p->n_maps;
-        a.n_tiles = (int32_t)((N + 255) / 256);
-        const int64_t n_tasks = (int64_t)p->n_maps * a.n_tiles;
-        if (n_tasks > (int64_t)INT32_MAX - 8) return fail(CB_ERR_UNSUPPORTED, "too many application tasks");
-        a.n_tasks = (int32_t)n_tasks;
-        a.per_xcd = (a.n_tasks + 7) / 8;
-        a.maps = p->d_amaps;
-        a.order = p->d_aorder;
-        a.src_layers = p->d_alayers;
-        a.wfrag = p->d_whi;
-        a.bias = p->d_bias;
-        if (cb::launch_apply_multi(a, p->n_cu, st) != hipSuccess)
-            return fail(CB_ERR_DEVICE, "multi-layer application kernel launch failed");
-        return ok();
-    }
+    if (p->multi) return apply_multi(p, maps, src, tgt_out, nullptr, nullptr, stream);
     return apply_single(p, maps, src, tgt_out, nullptr, nullptr, stream);
 }
 
@@ -1331,7 +1429,7 @@ cb_status cb_apply_rope(cb_plan *p, const float *maps, const cb_cache *src, cons
         if (cb_status s = check_rope("src_rope", src_rope, p->d_s, src->seq_len)) return s;
     if (tgt_rope)
         if (cb_status s = check_rope("tgt_rope", tgt_rope, p->d_t, src->seq_len)) return s;
-    if (p->multi) return fail(CB_ERR_UNSUPPORTED, "not yet wired");
+    if (p->multi) return apply_multi(p, maps, src, tgt_out, src_rope, tgt_rope, stream);
     return apply_single(p, maps, src, tgt_out, src_rope, tgt_rope, stream);
 }
 

@@ -33,6 +33,15 @@
 //       its step has just consumed.
 //   At the end of a task the bias is added, the sum rounded once to bf16 and
 //   stored as 16-byte chunks of target rows.
+//
+// With the target's rotary transform (Sec. 2.1, Sec. 3.1: the mapped keys
+// receive the target's RoPE) the K outputs are turned in fp32 before that one
+// rounding.  For the half-split pairing (i, i + 64) the fragments put output
+// channels 16 w .. 16 w + 15 and 64 + 16 w .. + 15 on wave w's 32 rows (the
+// perm flag of split_maps_frag_kernel), so each pair sits in registers v and
+// v + 8 of one lane; the interleaved pairs (2i, 2i + 1) are registers v, v + 1
+// in either layout.  K maps may read their source rows from a separate view
+// (a de-rotated copy of the sender's keys).
 #include "cb_internal.h"
 
 namespace cb {
@@ -70,8 +79,15 @@ __device__ __forceinline__ void lds_sync() {
     asm volatile("" ::: "memory");
 }
 
+// Output channel of row r (0..31) of wave w: 32 w + r, or with `perm` the
+// half-split layout 16 w + r (r < 16), 64 + 16 w + r - 16.
+__host__ __device__ __forceinline__ int frag_channel(int w, int r, bool perm) {
+    return perm ? (r < 16 ? 16 * w + r : 64 + 16 * w + (r - 16)) : 32 * w + r;
+}
+
 __global__ __launch_bounds__(256) void split_maps_frag_kernel(int n_maps, int k, const float *__restrict__ maps,
-                                                              uint16_t *__restrict__ wfrag, float *__restrict__ bias) {
+                                                              uint16_t *__restrict__ wfrag, float *__restrict__ bias,
+                                                              int perm) {
     const int P = 128 * k + 1;
     const int64_t total = (int64_t)n_maps * k * 8 * 4 * 64;
     for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
@@ -80,7 +96,7 @@ __global__ __launch_bounds__(256) void split_maps_frag_kernel(int n_maps, int k,
         const int64_t mi = e >> 11;                       // map * k + block
         const int64_t m = mi / k;
         const int i = (int)(mi - m * k);
-        const int c = 32 * w + (lane & 31);
+        const int c = frag_channel(w, lane & 31, perm != 0);
         const int K0 = 128 * i + 16 * ks + 8 * (lane >> 5);
         const float *src = maps + (m * P + K0) * 128 + c;
         uint32_t hi[4], lo[4];
@@ -105,6 +121,7 @@ struct Task {
     int64_t tok0;       // first token of the tile
     const uint16_t *x;  // source base of the map's (kv, head), layer 0
     const int32_t *layers;
+    int64_t s_layer, s_seq, s_tok;   // strides of the view the map reads
 };
 
 __device__ __forceinline__ Task task_of(const ApplyMultiArgs &a, int task) {
@@ -127,11 +144,18 @@ __device__ __forceinline__ Task task_of(const ApplyMultiArgs &a, int task) {
     t.m = __builtin_amdgcn_readfirstlane(a.order[gm]);
     t.tok0 = (int64_t)tile * TT;
     const ApplyMultiMap mp = a.maps[t.m];
-    t.x = a.src + mp.kv * a.ss.kv + mp.src_head * a.ss.head;
+    const bool kview = mp.kv == 0 && a.srck != nullptr;
+    const Strides &v = kview ? a.ssk : a.ss;
+    t.x = kview ? a.srck + mp.src_head * v.head : a.src + mp.kv * v.kv + mp.src_head * v.head;
+    t.s_layer = v.layer;
+    t.s_seq = v.seq;
+    t.s_tok = v.tok;
     t.layers = a.src_layers + (int64_t)t.m * a.k;
     return t;
 }
 
+// RS: target rotation of the K outputs, 0 none, 1 pairs (i, i + 64), 2 pairs (2i, 2i + 1).
+template <int RS>
 __global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
 void apply_multi_kernel(ApplyMultiArgs a) {
     __shared__ __attribute__((aligned(16))) char lds[2 * BUFB];
@@ -152,14 +176,14 @@ void apply_multi_kernel(ApplyMultiArgs a) {
     const uint32_t sdst = (uint32_t)rsub * ROWB + (uint32_t)((lane & 15) ^ rsub) * 16u;
     // element offset of the lane's chunk inside a (layer, kv, head) block (below 2^32: checked on the host)
     uint32_t rowoff[CPW];
-    auto set_rows = [&](int64_t tok0) {
+    auto set_rows = [&](const Task &tk_) {
 #pragma unroll
         for (int j = 0; j < CPW; ++j) {
-            int64_t n = tok0 + 16 * j + rsub;
+            int64_t n = tk_.tok0 + 16 * j + rsub;
             if (n >= a.N) n = a.N - 1;                    // rows past the end repeat the last token
             const uint32_t seq = fastdiv_u((uint32_t)n, a.T);
             const uint32_t tk = (uint32_t)n - seq * a.T.d;
-            rowoff[j] = (uint32_t)(seq * a.ss.seq + tk * a.ss.tok) + (lane & 15) * 8;
+            rowoff[j] = (uint32_t)(seq * tk_.s_seq + tk * tk_.s_tok) + (lane & 15) * 8;
         }
     };
     // half h of a block: chunks 8 h .. 8 h + 7 of the lane
@@ -204,9 +228,9 @@ void apply_multi_kernel(ApplyMultiArgs a) {
 
     // ---- prologue: block 0 of the first task in LDS buffer 0, its W fragments, x of step 0
     Task cur = task_of(a, task);
-    set_rows(cur.tok0);
+    set_rows(cur);
     {
-        const uint16_t *xb = cur.x + cur.layers[0] * a.ss.layer;
+        const uint16_t *xb = cur.x + cur.layers[0] * cur.s_layer;
         u32x4_t st0[HC], st1[HC];
         load_half(st0, xb, 0);
         load_half(st1, xb, 1);
@@ -232,13 +256,13 @@ void apply_multi_kernel(ApplyMultiArgs a) {
                 more = next_task < t_end;
                 if (more) {
                     nxt = task_of(a, next_task);
-                    set_rows(nxt.tok0);
+                    set_rows(nxt);
                 }
                 ni = 0;
             }
             const uint16_t *nw = more ? wptr(nxt.m, ni) : wptr(cur.m, i);  // past the end: reload valid fragments
             // past the end of the stream the current block is loaded again (and never read)
-            const uint16_t *nxb = more ? nxt.x + nxt.layers[ni] * a.ss.layer : cur.x + cur.layers[i] * a.ss.layer;
+            const uint16_t *nxb = more ? nxt.x + nxt.layers[ni] * nxt.s_layer : cur.x + cur.layers[i] * cur.s_layer;
             u32x4_t st0[HC], st1[HC];
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) {
@@ -282,37 +306,77 @@ void apply_multi_kernel(ApplyMultiArgs a) {
         // D[i][t]: t = lane & 31, channel 32 wave + 8 (v / 4) + 4 (lane / 32) + (v & 3)
         {
             const ApplyMultiMap mp = a.maps[cur.m];
+            constexpr bool PERM = RS == 1;
+            const bool rotate = RS != 0 && mp.kv == 0;
             float bias[16];
 #pragma unroll
-            for (int v = 0; v < 16; ++v) bias[v] = a.bias[(int64_t)cur.m * 128 + 32 * wave + 8 * (v >> 2) + 4 * lhalf + (v & 3)];
-            uint16_t *obase = a.out + mp.tgt_layer * a.os.layer + mp.kv * a.os.kv + mp.tgt_head * a.os.head + 32 * wave;
+            for (int v = 0; v < 16; ++v)
+                bias[v] = a.bias[(int64_t)cur.m * 128 + frag_channel(wave, 8 * (v >> 2) + 4 * lhalf + (v & 3), PERM)];
+            uint16_t *obase = a.out + mp.tgt_layer * a.os.layer + mp.kv * a.os.kv + mp.tgt_head * a.os.head;
+            const int oc0 = frag_channel(wave, 8 * lhalf, PERM), oc1 = frag_channel(wave, 16 + 8 * lhalf, PERM);
 #pragma unroll
             for (int s = 0; s < 8; ++s) {
+                const int64_t n = cur.tok0 + 32 * s + (int64_t)lrow;
+                const int64_t nc = n < a.N ? n : a.N - 1;
+                const uint32_t seq = fastdiv_u((uint32_t)nc, a.T);
+                const uint32_t tk = (uint32_t)nc - seq * a.T.d;
+                float o[16];
+#pragma unroll
+                for (int v = 0; v < 16; ++v) o[v] = acc[s][v] + bias[v];
+                if (RS != 0 && rotate) {
+                    // (cos, sin) of the lane's eight pairs at this token's position
+                    const float *row = a.rope_table + (int64_t)(a.rope_pos_offset + (int)tk) * 128;
+                    float4 cs[4];
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        // half split: frequencies 16 w + 8 (g / 2) + 4 lhalf + 2 (g % 2) + {0, 1}
+                        // interleaved: frequencies 16 w + 4 g + 2 lhalf + {0, 1}
+                        const int f = RS == 1 ? 16 * wave + 8 * (g >> 1) + 4 * lhalf + 2 * (g & 1)
+                                              : 16 * wave + 4 * g + 2 * lhalf;
+                        cs[g] = *reinterpret_cast<const float4 *>(row + 2 * f);
+                    }
+                    if constexpr (RS == 1) {
+#pragma unroll
+                        for (int v = 0; v < 8; ++v) {          // pair (v, v + 8): channels c and c + 64
+                            const float4 q = cs[2 * (v >> 2) + ((v & 3) >> 1)];
+                            const float c = (v & 1) ? q.z : q.x, sn = (v & 1) ? q.w : q.y;
+                            const float x0 = o[v], x1 = o[v + 8];
+                            o[v] = __builtin_fmaf(x0, c, -x1 * sn);
+                            o[v + 8] = __builtin_fmaf(x1, c, x0 * sn);
+                        }
+                    } else {
+#pragma unroll
+                        for (int v = 0; v < 16; v += 2) {      // pair (v, v + 1): channels 2f and 2f + 1
+                            const float4 q = cs[v >> 2];
+                            const float c = (v & 2) ? q.z : q.x, sn = (v & 2) ? q.w : q.y;
+                            const float x0 = o[v], x1 = o[v + 1];
+                            o[v] = __builtin_fmaf(x0, c, -x1 * sn);
+                            o[v + 1] = __builtin_fmaf(x1, c, x0 * sn);
+                        }
+                    }
+                }
                 uint32_t pk[8];
 #pragma unroll
                 for (int gq = 0; gq < 4; ++gq) {
-                    pk[2 * gq] = pack_bf16(acc[s][4 * gq + 0] + bias[4 * gq + 0], acc[s][4 * gq + 1] + bias[4 * gq + 1]);
-                    pk[2 * gq + 1] = pack_bf16(acc[s][4 * gq + 2] + bias[4 * gq + 2], acc[s][4 * gq + 3] + bias[4 * gq + 3]);
+                    pk[2 * gq] = pack_bf16(o[4 * gq + 0], o[4 * gq + 1]);
+                    pk[2 * gq + 1] = pack_bf16(o[4 * gq + 2], o[4 * gq + 3]);
                 }
                 // exchange with lane ^ 32 so that each lane owns 8 consecutive channels:
                 // lanes < 32 get channels 0-7 and 16-23, lanes >= 32 get 8-15 and 24-31
-                uint4 o[2];
+                uint4 ov[2];
 #pragma unroll
                 for (int p = 0; p < 2; ++p) {
                     const uint32_t s0 = lhalf ? pk[4 * p + 0] : pk[4 * p + 2];
                     const uint32_t s1 = lhalf ? pk[4 * p + 1] : pk[4 * p + 3];
                     const uint32_t r0 = (uint32_t)__shfl_xor((int)s0, 32);
                     const uint32_t r1 = (uint32_t)__shfl_xor((int)s1, 32);
-                    o[p] = lhalf ? make_uint4(r0, r1, pk[4 * p + 2], pk[4 * p + 3])
-                                 : make_uint4(pk[4 * p + 0], pk[4 * p + 1], r0, r1);
+                    ov[p] = lhalf ? make_uint4(r0, r1, pk[4 * p + 2], pk[4 * p + 3])
+                                  : make_uint4(pk[4 * p + 0], pk[4 * p + 1], r0, r1);
                 }
-                const int64_t n = cur.tok0 + 32 * s + (int64_t)lrow;
                 if (n < a.N) {
-                    const uint32_t seq = fastdiv_u((uint32_t)n, a.T);
-                    const uint32_t tk = (uint32_t)n - seq * a.T.d;
-                    uint16_t *orow = obase + (int64_t)seq * a.os.seq + (int64_t)tk * a.os.tok + 8 * lhalf;
-                    *reinterpret_cast<uint4 *>(orow) = o[0];
-                    *reinterpret_cast<uint4 *>(orow + 16) = o[1];
+                    uint16_t *orow = obase + (int64_t)seq * a.os.seq + (int64_t)tk * a.os.tok;
+                    *reinterpret_cast<uint4 *>(orow + oc0) = ov[0];
+                    *reinterpret_cast<uint4 *>(orow + oc1) = ov[1];
                 }
 #pragma unroll
                 for (int v = 0; v < 16; ++v) acc[s][v] = 0.f;
@@ -327,12 +391,13 @@ void apply_multi_kernel(ApplyMultiArgs a) {
 }  // namespace
 
 hipError_t launch_split_maps_frag(int32_t n_maps, int32_t k, const float *maps, uint16_t *wfrag, float *bias,
-                                  hipStream_t s) {
+                                  int perm, hipStream_t s) {
     const int64_t n = (int64_t)n_maps * k * 8 * 4 * 64;
     if (n == 0) return hipSuccess;
     int64_t blocks = (n + 255) / 256;
     if (blocks > 16384) blocks = 16384;
-    hipLaunchKernelGGL(split_maps_frag_kernel, dim3((unsigned)blocks), dim3(256), 0, s, n_maps, k, maps, wfrag, bias);
+    hipLaunchKernelGGL(split_maps_frag_kernel, dim3((unsigned)blocks), dim3(256), 0, s, n_maps, k, maps, wfrag, bias,
+                       perm);
     return hipGetLastError();
 }
 
@@ -341,7 +406,12 @@ hipError_t launch_apply_multi(const ApplyMultiArgs &a, int32_t n_cu, hipStream_t
     // one workgroup per compute unit, a multiple of 8 so every XCD gets the same count
     int per_xcd_wg = n_cu / 8 > 0 ? n_cu / 8 : 1;
     if (per_xcd_wg > a.per_xcd) per_xcd_wg = a.per_xcd;
-    hipLaunchKernelGGL(apply_multi_kernel, dim3(8 * per_xcd_wg), dim3(256), 0, s, a);
+    if (!a.rope_table)
+        hipLaunchKernelGGL(apply_multi_kernel<0>, dim3(8 * per_xcd_wg), dim3(256), 0, s, a);
+    else if (a.rope_style == 0)
+        hipLaunchKernelGGL(apply_multi_kernel<1>, dim3(8 * per_xcd_wg), dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL(apply_multi_kernel<2>, dim3(8 * per_xcd_wg), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 

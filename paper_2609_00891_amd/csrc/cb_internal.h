@@ -126,6 +126,7 @@ struct RopeLaunch {
     Strides is, os;
     const float *table;       // [n_pos][d/2][2] (cos, sin)
     int32_t n_layers, n_heads, n_seqs, seq_len, d, style, pos_offset, inverse, copy_v;
+    int32_t pos_step;         // token t of a sequence is at position pos_offset + t * pos_step
 };
 
 // One workgroup task of the multi-layer statistics (feature x~ = [x_0; ...;
@@ -163,6 +164,10 @@ struct MultiArgs {
     const void *zero;         // >= 256 zero bytes
     float *G, *C;             // centered: A [n][P-1][P-1], B [n][P-1][d_t]
     const double *sums;       // centered only: [n][P + d_t] = (sum w, sum w x, sum w y)
+    // NULL, or compact de-rotated calibration rows of the K maps, [layer][seq][head][row][d]:
+    // K tasks read their source / target blocks there (tok stride = one calibration row)
+    const uint16_t *srck, *tgtk;
+    Strides ssk, tsk;
 };
 
 
@@ -202,6 +207,11 @@ struct ApplyMultiArgs {
     const int32_t *src_layers;// [n_maps][k]
     const uint16_t *wfrag;    // W^T as MFMA fragments, [n_maps][k][8][4][2][64][8] bf16 (hi, lo planes)
     const float *bias;        // [n_maps][128]
+    const uint16_t *srck;     // NULL, or the K maps' source view (a de-rotated copy of the sender's keys)
+    Strides ssk;              // its strides (kv unused)
+    const float *rope_table;  // NULL, or the target's (cos, sin) [n_pos][64][2]: K outputs are rotated
+    int32_t rope_style;       // 0: pairs (i, i + 64), with the permuted fragments; 1: pairs (2i, 2i + 1)
+    int32_t rope_pos_offset;
 };
 
 // Launchers (return hipError_t of the launch).
@@ -229,7 +239,7 @@ hipError_t launch_stats_multi(const MultiArgs &a, hipStream_t s);
 hipError_t launch_stats_multi_centered(const MultiArgs &a, hipStream_t s);
 hipError_t launch_means_multi(const MeansMultiArgs &a, hipStream_t s);
 hipError_t launch_split_maps_frag(int32_t n_maps, int32_t k, const float *maps, uint16_t *wfrag, float *bias,
-                                  hipStream_t s);
+                                  int perm, hipStream_t s);
 hipError_t launch_apply_multi(const ApplyMultiArgs &a, int32_t n_cu, hipStream_t s);
 int64_t solve_blocked_bytes_per_system(int32_t P, int32_t d_t);
 // csums != nullptr: centered systems (A, B of the feature without bias entry,

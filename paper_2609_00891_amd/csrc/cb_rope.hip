@@ -16,7 +16,8 @@
 //   half-split partners -- and a group of 16 (layer, head) rows that share the
 //   token's angles; fp32 products from the exact bf16 values and the fp32
 //   table, one rounding to bf16.  V rows are copied when out is not in.
-//   HBM-bound.
+//   HBM-bound.  A position step other than one turns a strided selection of
+//   tokens (every sample_stride-th, gathered into a compact copy).
 #include "cb_internal.h"
 
 namespace cb {
@@ -52,7 +53,7 @@ struct RopeArgs {
     uint16_t *out;
     Strides is, os;
     const float2 *table;      // [n_pos][d/2]
-    int32_t n_layers, n_heads, n_seqs, seq_len, d, style, pos_offset;
+    int32_t n_layers, n_heads, n_seqs, seq_len, d, style, pos_offset, pos_step;
     float sign;               // +1 rotate, -1 de-rotate
     int32_t copy_v;           // out is not in: V rows are copied
 };
@@ -76,7 +77,7 @@ __global__ __launch_bounds__(256) void rope_kernel(RopeArgs a) {
         const int b = (int)(r % a.n_seqs);
         const int rg = (int)(r / a.n_seqs);
         // this token's angles for the thread's 8 channel pairs
-        const float2 *cs = a.table + (int64_t)(a.pos_offset + t) * h;
+        const float2 *cs = a.table + (int64_t)(a.pos_offset + (int64_t)t * a.pos_step) * h;
         float cw[8], sw[8];
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
@@ -153,6 +154,7 @@ hipError_t launch_rope(const RopeLaunch &L, hipStream_t s) {
     a.d = L.d;
     a.style = L.style;
     a.pos_offset = L.pos_offset;
+    a.pos_step = L.pos_step > 0 ? L.pos_step : 1;
     a.sign = L.inverse ? -1.f : 1.f;
     a.copy_v = L.copy_v;
     const int64_t n_rg = ((int64_t)L.n_layers * L.n_heads + kRows - 1) / kRows;

@@ -65,6 +65,8 @@ struct MCfg {
 // Per-workgroup state that is uniform across the wave.
 struct MultiCtx {
     const uint16_t *slot_base[MCfg::MAXS];   // (layer, kv, head) base of each staged block
+    int64_t s_row, t_row;                    // elements between calibration rows (source, target view)
+    int64_t s_seq, t_seq;                    // elements between sequences
 };
 
 // All copies of one tile by one wave, under one save of M0 (and EXEC): NL
@@ -176,8 +178,8 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
     // sequence); tiles past the end repeat the last one with zero weights.
     const int crow = 4 * wave + (lane >> 4);
     const uint32_t cchunk = (uint32_t)((lane & 15) ^ (4 * (crow & 3))) * 16u;
-    const uint32_t sstep = (uint32_t)(a.ss.tok * 2 * (int64_t)a.stride);   // bytes between calibration rows
-    const uint32_t tstep = (uint32_t)(a.ts.tok * 2 * (int64_t)a.stride);
+    const uint32_t sstep = (uint32_t)(c.s_row * 2);          // bytes between calibration rows
+    const uint32_t tstep = (uint32_t)(c.t_row * 2);
     uint32_t voff_full[NL];                     // lane offsets of a full tile
     auto slot_y = [](int s) { return HASY && s == NL - 1; };
 #pragma unroll
@@ -190,7 +192,7 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
         int64_t soff, toff;                     // element offsets of the tile in the source / target blocks
         const float *wp;                        // weight of the tile's first row
     } cur = {0, 0u, 0u, 0, 0, wrow};
-    const int64_t sadv = (int64_t)K::KT * a.stride * a.ss.tok, tadv = (int64_t)K::KT * a.stride * a.ts.tok;
+    const int64_t sadv = (int64_t)K::KT * c.s_row, tadv = (int64_t)K::KT * c.t_row;
     auto issue = [&](int st) {
         const bool live = cur.u < a.n_tiles;
         const uint32_t tmax = min((uint32_t)K::KT - 1, a.rows_per_seq - 1 - cur.r0);
@@ -212,8 +214,8 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
             if (cur.r0 >= a.rows_per_seq) {
                 cur.r0 = 0;
                 cur.seq += 1;
-                cur.soff = (int64_t)cur.seq * a.ss.seq;
-                cur.toff = (int64_t)cur.seq * a.ts.seq;
+                cur.soff = (int64_t)cur.seq * c.s_seq;
+                cur.toff = (int64_t)cur.seq * c.t_seq;
                 cur.wp = wrow + (int64_t)cur.seq * a.seq_len;
             } else {
                 cur.soff += sadv;
@@ -531,11 +533,19 @@ void stats_multi_kernel(MultiArgs a) {
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const MultiTask &tk = a.tasks[task];          // uniform: read with scalar loads
     MultiCtx c;
+    // K maps may read compact de-rotated calibration rows (one per row, no sampling stride)
+    const bool ks = tk.kv == 0 && a.srck != nullptr, kt = tk.kv == 0 && a.tgtk != nullptr;
+    c.s_row = ks ? a.ssk.tok : a.ss.tok * (int64_t)a.stride;
+    c.t_row = kt ? a.tsk.tok : a.ts.tok * (int64_t)a.stride;
+    c.s_seq = ks ? a.ssk.seq : a.ss.seq;
+    c.t_seq = kt ? a.tsk.seq : a.ts.seq;
 #pragma unroll
     for (int s = 0; s < K::MAXS; ++s) {
         const int L = tk.slot_layer[s];
-        c.slot_base[s] = L < 0 ? a.tgt + tk.tgt_layer * a.ts.layer + tk.kv * a.ts.kv + tk.tgt_head * a.ts.head
-                               : a.src + L * a.ss.layer + tk.kv * a.ss.kv + tk.src_head * a.ss.head;
+        c.slot_base[s] = L < 0 ? (kt ? a.tgtk + tk.tgt_layer * a.tsk.layer + tk.tgt_head * a.tsk.head
+                                     : a.tgt + tk.tgt_layer * a.ts.layer + tk.kv * a.ts.kv + tk.tgt_head * a.ts.head)
+                               : (ks ? a.srck + L * a.ssk.layer + tk.src_head * a.ssk.head
+                                     : a.src + L * a.ss.layer + tk.kv * a.ss.kv + tk.src_head * a.ss.head);
     }
     // variant: staged blocks (1..4), target block staged (HASY), sum w y owned (YS)
     const bool hasy = tk.slot_layer[tk.n_lds - 1] < 0;

@@ -534,20 +534,139 @@ def test_multi_apply_qwen_k8_batch_sampled(cb):
     plan.close()
 
 
-def test_multi_plan_rejects_fused_rotary_apply(cb):
-    # the fused target rotation is a single-layer epilogue: a multi-layer plan
-    # is refused before anything is enqueued, and the output is untouched
-    rng = np.random.default_rng(41)
-    src, tgt, _ = small_inputs(rng, 4, 1, 1, 1, 1, 32)
-    hm = random_multi_map(rng, 2, 4, 1, 1, 1)
+# ----------------------------------------------------------------------------- rotary keys, k > 1
+
+def gpu_rope_table(cb, theta, d, n_pos):
+    t = torch.empty((n_pos, d // 2, 2), dtype=torch.float32, device="cuda")
+    cb.cb_rope_table(theta, d, n_pos, t)
+    return t
+
+
+def rotated(x, theta, style, off):
+    """A cache as a model holds it: the K rows of content cache x turned by the
+    oracle's RoPE at positions off + tok; device tensor and host bits."""
+    L, _, B, H, T, d = x.shape
+    b = oracle.rope(bits(x), synth.cache_strides(L, H, B, T, d), L, H, d, B, T, theta, style, pos_offset=off)
+    return torch.from_numpy(b.view(np.int16)).to("cuda").view(torch.bfloat16), b
+
+
+def unrotated(b, theta, style, off):
+    """The oracle's inverse turn of cache bits b (fp64, one rounding)."""
+    L, _, B, H, T, d = b.shape
+    return oracle.rope(b, synth.cache_strides(L, H, B, T, d), L, H, d, B, T, theta, style, inverse=True,
+                       pos_offset=off)
+
+
+@pytest.mark.parametrize("style,off", [(0, 0), (1, 300)])
+def test_multi_apply_rope_target_rotation(cb, style, off):
+    # the K outputs turned in fp32 before the one rounding (the half split on
+    # permuted fragments); V outputs bit for bit those of cb_apply
+    rng = np.random.default_rng(70 + style)
+    k, L_s, H_s, L_t, H_t, B, T = 3, 5, 2, 2, 2, 2, 300
+    src, tgt, _ = small_inputs(rng, L_s, H_s, L_t, H_t, B, T)
+    hm = random_multi_map(rng, k, L_s, H_s, L_t, H_t)
     plan = cb.cb_plan_create_multi(hm, src, tgt, 1)
     maps = random_maps(rng, plan.n_maps, plan.P, plan.d_t)
-    table = torch.zeros((32, 64, 2), dtype=torch.float32, device="cuda")
-    out = torch.zeros_like(tgt)
-    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_UNSUPPORTED"):
-        cb.cb_apply_rope(plan, maps, src, out, table)
+    table = gpu_rope_table(cb, 1e6, 128, off + T)
+    say(f"multi apply target rotation style={style} off={off}")
+    out = torch.zeros((L_t, 2, B, H_t, T, 128), dtype=torch.bfloat16, device="cuda")
+    cb.cb_apply_rope(plan, maps, src, out, cb.rope_spec(table, style, off))
+    plain = gpu_apply(cb, plan, maps, src, L_t, H_t)
+    ref = np.zeros(tuple(out.shape), dtype=np.uint16)
+    oracle.apply_multi_rope(hm, maps.double().cpu().numpy(), bits(src), synth.cache_strides(L_s, H_s, B, T, 128),
+                            128, ref, synth.cache_strides(L_t, H_t, B, T, 128), 128, B, T, 1e6, style, off,
+                            n_threads=NTHREADS)
+    ob = bits(out)
+    check_apply_multi(ob, ref, hm, range(plan.n_maps), " (target rotation)")
+    assert np.array_equal(ob[:, 1], bits(plain)[:, 1]) and not np.array_equal(ob[:, 0], bits(plain)[:, 0])
+    plan.close()
+
+
+@pytest.mark.parametrize("style,off,tgt_too", [(0, 0, False), (1, 77, True)])
+def test_multi_apply_rope_source_derotation(cb, style, off, tgt_too):
+    # the sender's keys carry RoPE: one rotation pass into the plan's workspace
+    # gives bit for bit cb_rope(inverse) + the mapping, and matches the
+    # oracle's composition (the oracle turns back in fp64, the kernel in fp32,
+    # so a few inputs differ by one ulp: relative bar and bitwise share)
+    rng = np.random.default_rng(80 + style)
+    k, L_s, H_s, L_t, H_t, B, T = 3, 5, 2, 2, 2, 2, 300
+    src_c, tgt, _ = small_inputs(rng, L_s, H_s, L_t, H_t, B, T)
+    src, sb = rotated(src_c, 1e4, style, off)
+    hm = random_multi_map(rng, k, L_s, H_s, L_t, H_t)
+    plan = cb.cb_plan_create_multi(hm, src, tgt, 1)
+    maps = random_maps(rng, plan.n_maps, plan.P, plan.d_t)
+    tab_s, tab_t = gpu_rope_table(cb, 1e4, 128, off + T), gpu_rope_table(cb, 1e6, 128, off + T)
+    sr = cb.rope_spec(tab_s, style, off)
+    tr = cb.rope_spec(tab_t, style, off) if tgt_too else None
+    say(f"multi apply source de-rotation style={style} off={off} target rotation={tgt_too}")
+    out = torch.zeros((L_t, 2, B, H_t, T, 128), dtype=torch.bfloat16, device="cuda")
+    cb.cb_apply_rope(plan, maps, src, out, tr, sr)
+    src_d = torch.empty_like(src)
+    cb.cb_rope(src, src_d, tab_s, style, True, off)
+    sep = torch.zeros_like(out)
+    cb.cb_apply_rope(plan, maps, src_d, sep, tr)
     torch.cuda.synchronize()
-    assert not out.view(torch.int16).any()
+    assert torch.equal(out, sep)
+    so = unrotated(sb, 1e4, style, off)
+    ref = np.zeros(tuple(out.shape), dtype=np.uint16)
+    W = maps.double().cpu().numpy()
+    ss, os_ = synth.cache_strides(L_s, H_s, B, T, 128), synth.cache_strides(L_t, H_t, B, T, 128)
+    if tgt_too:
+        oracle.apply_multi_rope(hm, W, so, ss, 128, ref, os_, 128, B, T, 1e6, style, off, n_threads=NTHREADS)
+    else:
+        oracle.apply_multi(hm, W, so, ss, 128, ref, os_, 128, B, T, n_threads=NTHREADS)
+    ob = bits(out)
+    e = relF(oracle.bf16_to_double(ob), oracle.bf16_to_double(ref))
+    eq = float((ob == ref).mean())
+    say(f"  fused == separate passes; against the oracle's composition: relF {e:.3e}, bitwise-equal {eq:.6f}")
+    assert e <= TOL_APPLY and eq >= 0.99
+    plan.close()
+
+
+@pytest.mark.parametrize("stride,sides,style", [(4, "both", 0), (3, "src", 1), (1, "tgt", 0)])
+def test_multi_stats_rope_compact_derotation(cb, stride, sides, style):
+    # the K calibration rows turned back once into a compact workspace: moments
+    # bit for bit those of cb_rope(inverse) copies (same kernel, same rows),
+    # streamed over two uneven batches (the workspace is reused), and the
+    # oracle's composition within the statistics bar
+    rng = np.random.default_rng(90 + stride)
+    k, L_s, H_s, L_t, H_t, B, T, off = 3, 5, 2, 2, 2, 3, 520, 41
+    src_c, tgt_c, w = small_inputs(rng, L_s, H_s, L_t, H_t, B, T)
+    src, sb = rotated(src_c, 1e4, style, off)
+    tgt, tb = rotated(tgt_c, 1e6, style, off)
+    hm = random_multi_map(rng, k, L_s, H_s, L_t, H_t)
+    plan = cb.cb_plan_create_multi(hm, src, tgt, stride)
+    tab_s, tab_t = gpu_rope_table(cb, 1e4, 128, off + T), gpu_rope_table(cb, 1e6, 128, off + T)
+    sr = cb.rope_spec(tab_s, style, off) if sides in ("both", "src") else None
+    tr = cb.rope_spec(tab_t, style, off) if sides in ("both", "tgt") else None
+    say(f"multi stats rope stride={stride} sides={sides} style={style}")
+    n, P = plan.n_maps, plan.P
+    G = torch.empty((n, P, P), dtype=torch.float32, device="cuda")
+    C = torch.empty((n, P, 128), dtype=torch.float32, device="cuda")
+    cb.cb_stats_zero(plan, G, C)
+    for a, b in ((0, 1), (1, B)):
+        wb = w.reshape(-1, B, T)[:, a:b].reshape(w.shape[0], -1)
+        cb.cb_stats_accumulate_rope(plan, src[:, :, a:b], tgt[:, :, a:b], wb, G, C, sr, tr)
+    src_d, tgt_d = src.clone(), tgt.clone()
+    if sr is not None:
+        cb.cb_rope(src, src_d, tab_s, style, True, off)
+    if tr is not None:
+        cb.cb_rope(tgt, tgt_d, tab_t, style, True, off)
+    batches = [(src_d[:, :, a:b], tgt_d[:, :, a:b], w.reshape(-1, B, T)[:, a:b].reshape(w.shape[0], -1))
+               for a, b in ((0, 1), (1, B))]
+    G2, C2 = gpu_stats(cb, plan, batches)
+    assert torch.equal(G, G2) and torch.equal(C, C2)
+    so = unrotated(sb, 1e4, style, off) if sr is not None else sb
+    to = unrotated(tb, 1e6, style, off) if tr is not None else tb
+    ss, ts = synth.cache_strides(L_s, H_s, B, T, 128), synth.cache_strides(L_t, H_t, B, T, 128)
+    Go, Co = oracle.stats_multi(hm, so, ss, 128, to, ts, 128, w.cpu().numpy(), B * T, B, T, stride,
+                                n_threads=NTHREADS)
+    check_stats(G, C, Go, Co, list(range(n)))
+    G3, _ = gpu_stats(cb, plan, [(src, tgt, w)])
+    kmaps = [m for m in range(n) if hm["kv"][m] == 0]
+    vmaps = [m for m in range(n) if hm["kv"][m] == 1]
+    assert not torch.equal(G[kmaps], G3[kmaps])
+    assert relF(G[vmaps].double().cpu().numpy(), G3[vmaps].double().cpu().numpy()) <= 1e-6
     plan.close()
 
 
