@@ -549,6 +549,42 @@ def attn_leg(cb, synth, bw, tgt, steps):
     }
 
 
+def timed_on_stream(fn, steps):
+    """Mean event time of fn(i) over `steps` calls after one warm-up call (ms)."""
+    import torch
+    stream = torch.cuda.current_stream()
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    fn(0)
+    e[0].record(stream)
+    for i in range(steps):
+        fn(i)
+        e[i + 1].record(stream)
+    torch.cuda.synchronize()
+    return sum(e[i].elapsed_time(e[i + 1]) for i in range(steps)) / steps
+
+
+def rope_stats_leg(cb, plan, src, tgt, w, G, C, steps):
+    """Keys that carry RoPE (Sec. 2.1, Sec. 3.1): one statistics call of the resident
+    100-sequence batch with the source and target K rows turned back inside the
+    gather (cb_stats_accumulate_rope), against the separate passes it replaces
+    (cb_rope inverse over each cache's K rows, in place, then cb_stats_accumulate).
+    Base 1e6, half-split pairs, d = 128.  The caches are turned back and forth in
+    place by the timing (the parity samples were taken before)."""
+    import torch
+    T, d = src.shape[4], src.shape[5]
+    table = torch.empty((T, d // 2, 2), dtype=torch.float32, device="cuda")
+    cb.cb_rope_table(1e6, d, T, table)
+    spec = cb.rope_spec(table)
+    plain = timed_on_stream(lambda i: cb.cb_stats_accumulate(plan, src, tgt, w, G, C), steps)
+    rs = timed_on_stream(lambda i: cb.cb_rope(src, src, table, inverse=(i % 2 == 0)), steps)
+    rt = timed_on_stream(lambda i: cb.cb_rope(tgt, tgt, table, inverse=(i % 2 == 0)), steps)
+    fused = timed_on_stream(lambda i: cb.cb_stats_accumulate_rope(plan, src, tgt, w, G, C, spec, spec), steps)
+    sep = rs + rt + plain
+    return {"workload": "one 100-seq statistics call of the main build (1024 maps, P=129), keys with RoPE",
+            "stats_call_ms": plain, "rope_src_inplace_ms": rs, "rope_tgt_inplace_ms": rt,
+            "separate_ms": sep, "fused_ms": fused, "saving_ms": sep - fused, "fused_over_plain": fused / plain}
+
+
 def rope_leg(cb, plan, maps, asrc, cache, steps):
     """Target RoPE restored on mapped keys (Sec. 3.1) for the applied 8 x 32,768-token
     target cache (base 1e6, half-split pairs): the in-place rotation pass over its
@@ -579,6 +615,14 @@ def rope_leg(cb, plan, maps, asrc, cache, steps):
         fused_ms = timed(lambda i: cb.cb_apply_rope(plan, maps, asrc, cache, table))
         res.update({"apply_ms": apply_ms, "apply_rope_fused_ms": fused_ms,
                     "apply_then_rope_ms": apply_ms + ms})
+        # the sender's keys carry RoPE too: turned back in place, or inside the apply's gather
+        sL, _, sB, sH, sT, sd = asrc.shape
+        stab = torch.empty((sT, sd // 2, 2), dtype=torch.float32, device="cuda")
+        cb.cb_rope_table(1e6, sd, sT, stab)
+        sms = timed(lambda i: cb.cb_rope(asrc, asrc, stab, inverse=(i % 2 == 0)))
+        both_ms = timed(lambda i: cb.cb_apply_rope(plan, maps, asrc, cache, cb.rope_spec(table), cb.rope_spec(stab)))
+        res.update({"sender_rope_inplace_ms": sms, "apply_rope_both_fused_ms": both_ms,
+                    "separate_passes_ms": sms + apply_ms + ms, "saving_ms": sms + apply_ms + ms - both_ms})
     return res
 
 
@@ -673,6 +717,23 @@ def multi_leg(cb, synth, steps):
         "nonpositive_pivots": cbad,
     }
     del sums, A, Bc, cmaps, cinfo
+    # keys with RoPE: calibration rows turned back once into a compact workspace
+    # (cb_stats_accumulate_rope) against cb_rope inverse over both caches in place
+    # and the plain call; the caches are turned back and forth by the timing
+    T = wl.seq_len
+    table = torch.empty((T, 64, 2), dtype=torch.float32, device="cuda")
+    cb.cb_rope_table(1e6, 128, T, table)
+    spec = cb.rope_spec(table)
+    G = torch.zeros((n, P, P), dtype=torch.float32, device="cuda")
+    C = torch.zeros((n, P, d_t), dtype=torch.float32, device="cuda")
+    r_plain = timed_on_stream(lambda i: cb.cb_stats_accumulate(plan, src, tgt, w, G, C), steps)
+    r_src = timed_on_stream(lambda i: cb.cb_rope(src, src, table, inverse=(i % 2 == 0)), steps)
+    r_tgt = timed_on_stream(lambda i: cb.cb_rope(tgt, tgt, table, inverse=(i % 2 == 0)), steps)
+    r_fused = timed_on_stream(lambda i: cb.cb_stats_accumulate_rope(plan, src, tgt, w, G, C, spec, spec), steps)
+    rope = {"stats_call_ms": r_plain, "rope_src_inplace_ms": r_src, "rope_tgt_inplace_ms": r_tgt,
+            "stats_separate_ms": r_plain + r_src + r_tgt, "stats_fused_ms": r_fused,
+            "stats_saving_ms": r_plain + r_src + r_tgt - r_fused}
+    del G, C
     # online application of the fitted maps to the resident sender batch
     del tgt, w, ws
     torch.cuda.empty_cache()
@@ -686,6 +747,14 @@ def multi_leg(cb, synth, steps):
     torch.cuda.synchronize()
     apply_ms = ea[1].elapsed_time(ea[steps + 1]) / steps
     apply_flop = 2.0 * n * B * wl.seq_len * P * d_t
+    # keys with RoPE on the apply: the sender turned back (one pass into the plan's
+    # workspace) and the target rotation in the epilogue, against cb_rope inverse
+    # on the sender in place + cb_apply + cb_rope on the output in place
+    a_tgt = timed_on_stream(lambda i: cb.cb_rope(out, out, table, inverse=(i % 2 == 0)), steps)
+    a_fused = timed_on_stream(lambda i: cb.cb_apply_rope(plan, maps, src, out, spec, spec), steps)
+    rope.update({"apply_ms": apply_ms, "rope_sender_inplace_ms": r_src, "rope_output_inplace_ms": a_tgt,
+                 "apply_separate_ms": r_src + apply_ms + a_tgt, "apply_fused_ms": a_fused,
+                 "apply_saving_ms": r_src + apply_ms + a_tgt - a_fused})
     del out
     plan.close()
     return {
@@ -704,6 +773,7 @@ def multi_leg(cb, synth, steps):
                      "algorithmic_flops_per_launch": flop_per_row * rows_per_call},
         "nonpositive_pivots": bad,
         "centered_two_pass": centered,
+        "rope": rope,
     }
 
 
@@ -929,6 +999,8 @@ def main():
             "weighted_means_pass_GBps": res["centered"]["means_GBps"],
             "stats_call_rate_over_means_pass_rate": achieved / res["centered"]["means_GBps"],
             "note": "a measured streaming rate of the same bytes, not a roofline; roofline.frac is against 8 TB/s"}
+    if args.rope_steps > 0:
+        res["rope_stats"] = rope_stats_leg(cb, plan, src, tgt, w, G, C, args.rope_steps)
     if args.probe_steps > 0 or args.attn_steps > 0:
         del G, C
     if args.probe_steps > 0:

@@ -19,13 +19,24 @@
 //   two target maps is read once.
 //
 // With the sender's rotary transform removed on the way in (Sec. 2.1, Sec.
-// 3.1: the maps act on content coordinates), the copy wave also moves each
-// sub-block's slice of the source table, [32 tokens][d_s/2][cos, sin], into
-// LDS behind its rows, and the computing waves turn sub-block sb + 1 back in
-// LDS (one chunk pair per lane, products as cb_rope's inverse, one rounding
-// to bf16) while they multiply sub-block sb; the next barrier publishes it.
-// The copy wave therefore waits for one more sub-block before each barrier,
-// and the ring is five stages deep (rows and table slice per stage).
+// 3.1: the maps act on content coordinates), the computing waves turn
+// sub-block sb + 1 back in LDS (one chunk pair per lane, in fp32, one
+// rounding to bf16) in the iteration of sub-block sb; the next barrier
+// publishes it, so the copy wave waits for one more sub-block before each
+// barrier.
+//
+// Angles of the de-rotation.  A sender's table covers tens of thousands of
+// positions (16 MiB at 32,768 x 128), far more than L2, and each K group
+// would stream its rows: twice the bytes of the K rows themselves.  The
+// de-rotation therefore forms the (cos, sin) of position P = Q + r, Q = P - P
+// mod 32, from the table rows of Q and of r by the angle-addition formulas in
+// fp32: rows r < 32 are the same 16 KiB for every call and a whole sub-block
+// shares one or two rows Q, so its table traffic is about 1/32 of direct
+// reads.  Those angles carry about 1.5 fp32 ulp more error than the table's,
+// which moves a de-rotated bf16 input by one ulp only where it lies within
+// that distance of a rounding boundary.  The target rotation of the epilogue
+// reads the table directly (measured faster there: its entries are shared by
+// the two slots' waves, and its loads overlap the products).
 //
 // With the target's rotary transform fused (Sec. 2.1, Sec. 3.1: the mapped
 // keys receive the target's RoPE), the K outputs are turned in fp32 before
@@ -98,11 +109,9 @@ struct ACfg {
     static constexpr int NCB = DS / 8;              // 16-byte blocks per source row
     static constexpr int ROWB = DS * 2;             // bytes per source row
     static constexpr int BUFB = SB * ROWB;          // bytes per ring stage
-    static constexpr int RCOPIES = BUFB / 1024;     // row copy instructions per stage (64 lanes x 16 B)
-    static constexpr int TABB = SR ? SB * DS * 4 : 0;   // table slice: [SB tokens][DS/2][cos, sin] fp32
-    static constexpr int COPIES = RCOPIES + TABB / 1024;
-    static constexpr int STB = BUFB + TABB;         // bytes per ring stage
-    static constexpr int NST = SR ? 5 : 8;          // ring stages
+    static constexpr int COPIES = BUFB / 1024;      // copy instructions per stage (64 lanes x 16 B)
+    static constexpr int STB = BUFB;                // bytes per ring stage
+    static constexpr int NST = 8;                   // ring stages
     static_assert(BUFB % 1024 == 0, "a stage is a whole number of copy instructions");
     static_assert(SR == 0 || DS == 64 || DS == 128, "the source de-rotation takes d_s = 64 or 128");
 };
@@ -136,6 +145,21 @@ template <int DT, int RS>
 __device__ __forceinline__ int out_channel(int rb, int i) {
     if (RS == kRopeHalf) return i < 16 ? rb * 16 + i : DT / 2 + rb * 16 + (i - 16);
     return rb * 32 + i;
+}
+
+// (cos, sin) of position P for frequencies f and f + 1 (float offset 2 f of a
+// table row), from the rows of Q = P - P mod 32 and r = P mod 32:
+// cos(Q + r) = cos Q cos r - sin Q sin r, sin(Q + r) = sin Q cos r + cos Q sin r,
+// in fp32.  Returns (cos f, sin f, cos f+1, sin f+1) like a table read.
+__device__ __forceinline__ float4 angles2(const float *table, int row_floats, int P, int f) {
+    const float4 q = *reinterpret_cast<const float4 *>(table + (int64_t)(P & ~31) * row_floats + 2 * f);
+    const float4 r = *reinterpret_cast<const float4 *>(table + (int64_t)(P & 31) * row_floats + 2 * f);
+    float4 o;
+    o.x = __builtin_fmaf(q.x, r.x, -(q.y * r.y));
+    o.y = __builtin_fmaf(q.y, r.x, q.x * r.y);
+    o.z = __builtin_fmaf(q.z, r.z, -(q.w * r.w));
+    o.w = __builtin_fmaf(q.w, r.z, q.z * r.w);
+    return o;
 }
 
 // One workgroup per (group, token tile).  The copy wave streams 32-token
@@ -177,7 +201,7 @@ __global__ __attribute__((amdgpu_flat_work_group_size(ACfg<DS, DT>::NT, ACfg<DS,
         const uint32_t lds_base = (uint32_t)(uintptr_t)lds;
         auto issue = [&](int sb, int st) {
 #pragma unroll
-            for (int i = 0; i < K::RCOPIES; ++i) {
+            for (int i = 0; i < K::COPIES; ++i) {
                 const int q = 64 * i + lane;
                 const int t = q / K::NCB, p = q - (q / K::NCB) * K::NCB;
                 const int cb = (p + K::NCB - t % K::NCB) % K::NCB;     // inverse of the rotation
@@ -186,18 +210,6 @@ __global__ __attribute__((amdgpu_flat_work_group_size(ACfg<DS, DT>::NT, ACfg<DS,
                 const uint32_t tt = (uint32_t)tau - b * a.T.d;
                 const uint16_t *src = xsrc + (int64_t)b * a.ss.seq + (int64_t)tt * a.ss.tok + cb * 8;
                 dma16(src, __builtin_amdgcn_readfirstlane(lds_base + st * K::STB + i * 1024));
-            }
-            if constexpr (SR != 0) {
-                // the rows' table entries: token t's DS floats at slice byte t * DS * 4
-#pragma unroll
-                for (int i = 0; i < K::COPIES - K::RCOPIES; ++i) {
-                    const int q = 1024 * i + 16 * lane;                // byte in the slice
-                    const int t = q / (DS * 4), off = q - t * (DS * 4);
-                    const int tau = min(tok0 + sb * K::SB + t, tok1 - 1);
-                    const uint32_t tt = (uint32_t)tau - fastdiv((uint32_t)tau, a.T) * a.T.d;
-                    const char *g = (const char *)(a.src_rope_table + (int64_t)(a.src_rope_pos_offset + (int)tt) * DS) + off;
-                    dma16(g, __builtin_amdgcn_readfirstlane(lds_base + st * K::STB + K::BUFB + i * 1024));
-                }
             }
         };
 #pragma unroll
@@ -256,25 +268,29 @@ __global__ __attribute__((amdgpu_flat_work_group_size(ACfg<DS, DT>::NT, ACfg<DS,
     // ---- de-rotation of a landed sub-block (SR != 0): pair u = 64 wave + lane
     // of its rows, token row t = u / (NCB/2), logical chunks c and c + NCB/2
     constexpr int HP = K::NCB / 2;
-    auto turn_sub = [&](int sb) __attribute__((always_inline)) {
+    const int tu = (64 * wave + lane) / HP, cu = (64 * wave + lane) % HP;
+    const bool ulive = SR != 0 && 64 * wave + lane < K::SB * HP;
+    // the lane's (cos, sin) entries for sub-block sb: half split, frequencies
+    // 8c .. 8c + 7; interleaved, 4c .. 4c + 3 and 4(c + NCB/2) .. + 3
+    auto tab_load = [&](float4 (&cs)[4], int sb) __attribute__((always_inline)) {
         if constexpr (SR != 0) {
-            const int u = 64 * wave + lane;
-            if (u >= K::SB * HP) return;
-            const int t = u / HP, c = u - (u / HP) * HP;
+            const int tau = min(tok0 + sb * K::SB + tu, tok1 - 1);
+            const uint32_t tt = (uint32_t)tau - fastdiv((uint32_t)tau, a.T) * a.T.d;
+            const int P = a.src_rope_pos_offset + (int)tt;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int f = SR == 1 ? 8 * cu + 2 * j : 4 * (j < 2 ? cu : cu + HP) + 2 * (j & 1);
+                cs[j] = angles2(a.src_rope_table, DS, P, f);
+            }
+        }
+    };
+    auto turn_sub = [&](int sb, const float4 (&cs)[4]) __attribute__((always_inline)) {
+        if constexpr (SR != 0) {
+            if (!ulive) return;
+            const int t = tu, c = cu;
             char *B = lds + (sb % K::NST) * K::STB;
             char *pa = B + t * (K::NCB * 16) + ((c + t) % K::NCB) * 16;
             char *pb = B + t * (K::NCB * 16) + ((c + HP + t) % K::NCB) * 16;
-            const float *row = (const float *)(B + K::BUFB + t * DS * 4);
-            float4 cs[4];
-            if constexpr (SR == 1) {
-#pragma unroll
-                for (int j = 0; j < 4; ++j) cs[j] = *reinterpret_cast<const float4 *>(row + 16 * c + 4 * j);
-            } else {
-                cs[0] = *reinterpret_cast<const float4 *>(row + 8 * c);
-                cs[1] = *reinterpret_cast<const float4 *>(row + 8 * c + 4);
-                cs[2] = *reinterpret_cast<const float4 *>(row + 8 * (c + HP));
-                cs[3] = *reinterpret_cast<const float4 *>(row + 8 * (c + HP) + 4);
-            }
             const uint4 A = *reinterpret_cast<const uint4 *>(pa);
             const uint4 Bv = *reinterpret_cast<const uint4 *>(pb);
             const uint32_t av[4] = {A.x, A.y, A.z, A.w}, bv[4] = {Bv.x, Bv.y, Bv.z, Bv.w};
@@ -303,14 +319,36 @@ __global__ __attribute__((amdgpu_flat_work_group_size(ACfg<DS, DT>::NT, ACfg<DS,
     };
     if constexpr (SR != 0) {
         lds_barrier();                                         // sub-blocks 0 and 1 have landed
-        if (turn_src) turn_sub(0);
+        if (turn_src) {
+            float4 cs[4];
+            tab_load(cs, 0);
+            turn_sub(0, cs);
+        }
     }
+    // target rotation: (cos, sin) of the lane's eight rotated pairs in a sub-block
+    auto tcs_load = [&](float4 (&cs)[4], int sb) __attribute__((always_inline)) {
+        if constexpr (RS != kRopeNone) {
+            const int tau = min(tok0 + sb * K::SB + (int)lrow, tok1 - 1);
+            const uint32_t tt = (uint32_t)tau - fastdiv((uint32_t)tau, a.T) * a.T.d;
+            const float *row = a.rope_table + (int64_t)(a.rope_pos_offset + (int)tt) * DT;   // [d/2][2] per position
+#pragma unroll
+            for (int gq = 0; gq < 4; ++gq) {
+                // half split: frequencies rb*16 + 8 (gq/2) + 4 lhalf + 2 (gq%2) + {0, 1}
+                // interleaved: frequencies rb*16 + 4 gq + 2 lhalf + {0, 1}
+                const int f = RS == kRopeHalf ? rb * 16 + 8 * (gq >> 1) + 4 * (int)lhalf + 2 * (gq & 1)
+                                              : rb * 16 + 4 * gq + 2 * (int)lhalf;
+                cs[gq] = *reinterpret_cast<const float4 *>(row + 2 * f);
+            }
+        }
+    };
 
     // With staging, iteration sb stores the rows of sub-block sb - 1 (written to
     // the staging buffer before the barrier), and one more iteration follows.
     for (int sb = 0; sb < n_sb + (STAGE ? 1 : 0); ++sb) {
         lds_barrier();                                         // sub-block sb has landed (and is turned)
-        if (SR != 0 && turn_src && sb + 1 < n_sb) turn_sub(sb + 1);
+        const bool turn_next = SR != 0 && turn_src && sb + 1 < n_sb;
+        float4 scs[4];
+        if (turn_next) tab_load(scs, sb + 1);
         if (STAGE && active && sb > 0) {
             // 4 DT chunks of 16 bytes: two rounds of the slot's RBT waves
             const char *ob = obuf + (((sb - 1) & 1) * 2 + slot) * OBUF;
@@ -327,26 +365,16 @@ __global__ __attribute__((amdgpu_flat_work_group_size(ACfg<DS, DT>::NT, ACfg<DS,
                 }
             }
         }
+        if (turn_next) turn_sub(sb + 1, scs);
         if (STAGE && sb == n_sb) break;
         if (!active) continue;
         const char *B = lds + (sb % K::NST) * K::STB;
         const int tau = tok0 + sb * K::SB + (int)lrow;
         const uint32_t bseq = fastdiv((uint32_t)min(tau, tok1 - 1), a.T);
         const uint32_t tt = (uint32_t)min(tau, tok1 - 1) - bseq * a.T.d;
-        // (cos, sin) of the lane's eight rotated pairs, loaded before the
-        // products so that their latency hides behind the MFMA chains
+        // this sub-block's rotation entries, requested before the products
         float4 cs[4];
-        if (RS != kRopeNone && rotate) {
-            const float *row = a.rope_table + (int64_t)(a.rope_pos_offset + (int)tt) * DT;   // [d/2][2] per position
-#pragma unroll
-            for (int gq = 0; gq < 4; ++gq) {
-                // half split: frequencies rb*16 + 8 (gq/2) + 4 lhalf + {0..3}, two float4 per group of four
-                // interleaved: frequencies rb*16 + 4 gq + 2 lhalf + {0, 1}, one float4
-                const int f = RS == kRopeHalf ? rb * 16 + 8 * (gq >> 1) + 4 * (int)lhalf + 2 * (gq & 1)
-                                              : rb * 16 + 4 * gq + 2 * (int)lhalf;
-                cs[gq] = *reinterpret_cast<const float4 *>(row + 2 * f);
-            }
-        }
+        if (RS != kRopeNone && rotate) tcs_load(cs, sb);
         // hi and lo terms in two accumulators: two independent MFMA chains
         f32x16_t acc, acl;
 #pragma unroll

@@ -314,27 +314,41 @@ void apply_multi_kernel(ApplyMultiArgs a) {
                 bias[v] = a.bias[(int64_t)cur.m * 128 + frag_channel(wave, 8 * (v >> 2) + 4 * lhalf + (v & 3), PERM)];
             uint16_t *obase = a.out + mp.tgt_layer * a.os.layer + mp.kv * a.os.kv + mp.tgt_head * a.os.head;
             const int oc0 = frag_channel(wave, 8 * lhalf, PERM), oc1 = frag_channel(wave, 16 + 8 * lhalf, PERM);
+            // (cos, sin) of the lane's eight pairs at token 32 s + lane mod 32 of the tile,
+            // loaded one token group ahead of their use
+            auto tok_of = [&](int s) {
+                const int64_t n = cur.tok0 + 32 * s + (int64_t)lrow;
+                return n < a.N ? n : a.N - 1;
+            };
+            auto cs_load = [&](float4 (&cs)[4], int s) __attribute__((always_inline)) {
+                const int64_t nc = tok_of(s);
+                const uint32_t tk = (uint32_t)nc - fastdiv_u((uint32_t)nc, a.T) * a.T.d;
+                const float *row = a.rope_table + (int64_t)(a.rope_pos_offset + (int)tk) * 128;
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    // half split: frequencies 16 w + 8 (g / 2) + 4 lhalf + 2 (g % 2) + {0, 1}
+                    // interleaved: frequencies 16 w + 4 g + 2 lhalf + {0, 1}
+                    const int f = RS == 1 ? 16 * wave + 8 * (g >> 1) + 4 * lhalf + 2 * (g & 1)
+                                          : 16 * wave + 4 * g + 2 * lhalf;
+                    cs[g] = *reinterpret_cast<const float4 *>(row + 2 * f);
+                }
+            };
+            float4 csn[4];
+            if (RS != 0 && rotate) cs_load(csn, 0);
 #pragma unroll
             for (int s = 0; s < 8; ++s) {
                 const int64_t n = cur.tok0 + 32 * s + (int64_t)lrow;
-                const int64_t nc = n < a.N ? n : a.N - 1;
+                const int64_t nc = tok_of(s);
                 const uint32_t seq = fastdiv_u((uint32_t)nc, a.T);
                 const uint32_t tk = (uint32_t)nc - seq * a.T.d;
                 float o[16];
 #pragma unroll
                 for (int v = 0; v < 16; ++v) o[v] = acc[s][v] + bias[v];
                 if (RS != 0 && rotate) {
-                    // (cos, sin) of the lane's eight pairs at this token's position
-                    const float *row = a.rope_table + (int64_t)(a.rope_pos_offset + (int)tk) * 128;
                     float4 cs[4];
 #pragma unroll
-                    for (int g = 0; g < 4; ++g) {
-                        // half split: frequencies 16 w + 8 (g / 2) + 4 lhalf + 2 (g % 2) + {0, 1}
-                        // interleaved: frequencies 16 w + 4 g + 2 lhalf + {0, 1}
-                        const int f = RS == 1 ? 16 * wave + 8 * (g >> 1) + 4 * lhalf + 2 * (g & 1)
-                                              : 16 * wave + 4 * g + 2 * lhalf;
-                        cs[g] = *reinterpret_cast<const float4 *>(row + 2 * f);
-                    }
+                    for (int g = 0; g < 4; ++g) cs[g] = csn[g];
+                    if (s < 7) cs_load(csn, s + 1);
                     if constexpr (RS == 1) {
 #pragma unroll
                         for (int v = 0; v < 8; ++v) {          // pair (v, v + 8): channels c and c + 64

@@ -1111,9 +1111,14 @@ def test_apply_rope_source_derotation(cb, d_s, d_t, style, off, tgt_too):
     sep = torch.zeros_like(out)
     cb.cb_apply_rope(plan, maps, src_d, sep, tr)
     torch.cuda.synchronize()
+    # the fused turn forms its angles by angle addition (about 1.5 fp32 ulp from
+    # the table's), so a share p ~ 3 * 2^-16 of the de-rotated inputs lies one
+    # bf16 ulp (2^-8) from cb_rope's: outputs then differ by about
+    # sqrt(p) * 2^-8 ~ 3e-5 relative; the bar is 1e-4
     same = float((bits(out) == bits(sep)).mean())
-    say(f"  fused vs separate passes: bitwise-equal {same:.6f}")
-    assert torch.equal(out, sep)
+    es = relF(oracle.bf16_to_double(bits(out)), oracle.bf16_to_double(bits(sep)))
+    say(f"  fused vs separate passes: bitwise-equal {same:.6f}, relF {es:.2e}")
+    assert same >= 0.999 and es <= 1e-4
     so = oracle.rope(sb, src.stride()[:5], wl.L_s, wl.H_s, d_s, wl.n_seqs, wl.seq_len, ts, style, inverse=True,
                      pos_offset=off)
     ref = np.zeros(tuple(out.shape), dtype=np.uint16)
