@@ -125,7 +125,7 @@ def write_traffic(fetch_dir, write_dir, cfetch_dir, cwrite_dir, copy_gib):
     and its reduction), each scaled by what the same counter reads for the
     plain device copy of `copy_gib` GiB (--hbm-copy-probe)."""
     n = copy_gib * (1 << 30)
-    main = lambda k: "::stats_kernel<128, 128, false, false>" in k or \
+    main = lambda k: "::stats_kernel<128, 128, false, false, 0>" in k or \
         "::reduce_kernel<128, 128, false>" in k  # noqa: E731
     f = _pmc_means(fetch_dir, "FETCH_SIZE", main)
     w = _pmc_means(write_dir, "WRITE_SIZE", main)
