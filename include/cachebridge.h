@@ -134,7 +134,7 @@ typedef struct {
     int64_t s_layer, s_seq, s_bnd, s_head;
 } cb_queries;
 
-/* Validated head map, static gather schedule and workspace (opaque). */
+/* Validated head map, its precomputed read plan and workspace (opaque). */
 typedef struct cb_plan cb_plan;
 
 /* cb_ridge_solve flags. */

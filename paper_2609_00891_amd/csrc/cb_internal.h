@@ -8,7 +8,7 @@
 
 namespace cb {
 
-// One unit of the static gather schedule for the statistics: up to two maps
+// One unit of the precomputed read plan of the statistics: up to two maps
 // that are processed by one workgroup over a token range.  When both maps read
 // the same source block (a source layer feeding two target layers) the source
 // rows are loaded once ("shared").
