@@ -670,6 +670,58 @@ def test_multi_stats_rope_compact_derotation(cb, stride, sides, style):
     plan.close()
 
 
+def test_multi_stats_rope_qwen_k8_batch_full_size_sampled_maps(cb):
+    """The compact de-rotated gather at the k = 8 construction's resident batch
+    (100 x 1,024 tokens, every fourth): the synthetic caches taken as caches whose
+    keys carry RoPE; four sampled maps against the oracle's composition (its inverse
+    turn of all their rows, then its moments on every fourth token)."""
+    wl = synth.WORKLOADS["qwen_k8"]
+    bw = wl.with_(n_seqs=wl.batch_seqs)
+    say(f"multi rope qwen_k8 batch: {bw.n_seqs} x {bw.seq_len} tokens, stride {bw.sample_stride}")
+    src = synth.gen_source(bw, device="cuda")
+    tgt = synth.gen_target(bw, src, device="cuda")
+    w = synth.gen_weights(bw, device="cuda", chunk=50)
+    hm = synth.head_map_multi(wl)
+    plan = cb.cb_plan_create_multi(hm, src, tgt, wl.sample_stride)
+    T = bw.seq_len
+    tab = gpu_rope_table(cb, 1e6, 128, T)
+    n, P = plan.n_maps, plan.P
+    G = torch.empty((n, P, P), dtype=torch.float32, device="cuda")
+    C = torch.empty((n, P, 128), dtype=torch.float32, device="cuda")
+    cb.cb_stats_zero(plan, G, C)
+    cb.cb_stats_accumulate_rope(plan, src, tgt, w, G, C, cb.rope_spec(tab), cb.rope_spec(tab))
+    torch.cuda.synchronize()
+    sel = [3, 400, 641, 1020]
+    say(f"  oracle on maps {sel}")
+    k, B_ = wl.k, bw.n_seqs
+    xs, ys, ws = [], [], []
+    for m in sel:
+        z, a = int(hm["kv"][m]), int(hm["src_head"][m])
+        for j in hm["src_layers"][m]:
+            xs.append(src[int(j), z, :, a])
+        ys.append(tgt[int(hm["tgt_layer"][m]), z, :, int(hm["tgt_head"][m])])
+        ws.append(w[int(hm["weight_row"][m])])
+    ns = len(sel)
+    xb = bits(torch.stack(xs)).reshape(ns * k, 1, B_, 1, T, 128)
+    yb = bits(torch.stack(ys)).reshape(ns, 1, B_, 1, T, 128)
+    del src, tgt
+    torch.cuda.empty_cache()
+    ss = (B_ * T * 128, 0, T * 128, 0, 128)
+    xd = oracle.rope(xb, ss, ns * k, 1, 128, B_, T, 1e6, 0, inverse=True)[:, 0:1]
+    yd = oracle.rope(yb, ss, ns, 1, 128, B_, T, 1e6, 0, inverse=True)[:, 0:1]
+    for i, m in enumerate(sel):                    # V maps carry no positions
+        if hm["kv"][m] == 1:
+            xd[i * k:(i + 1) * k], yd[i] = xb[i * k:(i + 1) * k], yb[i]
+    chm = {"tgt_layer": np.arange(ns, dtype=np.int32), "tgt_head": np.zeros(ns, np.int32),
+           "kv": np.zeros(ns, np.int32), "src_layers": np.arange(ns * k, dtype=np.int32).reshape(ns, k),
+           "src_head": np.zeros(ns, np.int32), "weight_row": np.arange(ns, dtype=np.int32)}
+    Go, Co = oracle.stats_multi(chm, np.ascontiguousarray(xd), ss, 128, np.ascontiguousarray(yd), ss, 128,
+                                np.ascontiguousarray(torch.stack(ws).cpu().numpy()), B_ * T, B_, T,
+                                wl.sample_stride, n_threads=NTHREADS)
+    check_stats(G, C, Go, Co, sel)
+    plan.close()
+
+
 # ----------------------------------------------------------------------------- two-pass centered form, k > 1
 
 TOL_SUMS = 1e-9        # fp64 sums of exact fp64 products: only the summation order differs

@@ -1012,6 +1012,41 @@ def test_stats_rope_fused_equals_separate_passes_and_oracle(cb, d, style, T, off
     plan.close()
 
 
+def test_stats_rope_qwen50_full_size_sampled_maps(cb):
+    """The fused de-rotation at the 14B->32B shape (50 x 2048 tokens, 1024 maps, one
+    call): the synthetic caches are taken as caches whose keys carry RoPE (source
+    base 1e4, target base 1e6); eight sampled maps against the oracle's composition
+    (its fp64 inverse turn of those rows, then its moments)."""
+    wl = synth.WORKLOADS["qwen50"]
+    say(f"{wl.name}: generating {wl.n_seqs} x {wl.seq_len} tokens")
+    src, tgt, w = make_inputs(wl)
+    hm = synth.head_map(wl)
+    plan = cb.cb_plan_create(hm, src, tgt, wl.n_seqs * wl.seq_len)
+    ts_, tt_ = 1e4, 1e6
+    tab_s, tab_t = gpu_rope_table(cb, ts_, wl.d_s, wl.seq_len), gpu_rope_table(cb, tt_, wl.d_t, wl.seq_len)
+    n, P = plan.n_maps, plan.P
+    G = torch.empty((n, P, P), dtype=torch.float32, device="cuda")
+    C = torch.empty((n, P, wl.d_t), dtype=torch.float32, device="cuda")
+    cb.cb_stats_zero(plan, G, C)
+    say(f"{wl.name}: GPU statistics with the de-rotation fused")
+    cb.cb_stats_accumulate_rope(plan, src, tgt, w, G, C, cb.rope_spec(tab_s), cb.rope_spec(tab_t))
+    torch.cuda.synchronize()
+    sel = sample_maps(wl.n_maps, 8, seed=5)
+    say(f"{wl.name}: oracle on maps {sel}")
+    chm, xb, ss, yb, ts, ws, B, T = compact(hm, sel, src, tgt, w)
+    m = len(sel)
+    xd = oracle.rope(xb, ss, m, 1, wl.d_s, B, T, ts_, 0, inverse=True)[:, 0:1]
+    yd = oracle.rope(yb, ts, m, 1, wl.d_t, B, T, tt_, 0, inverse=True)[:, 0:1]
+    for i, mm in enumerate(sel):                   # V maps carry no positions
+        if hm["kv"][mm] == 1:
+            xd[i], yd[i] = xb[i], yb[i]
+    Go, Co = oracle.stats(chm, np.ascontiguousarray(xd), ss, wl.d_s, np.ascontiguousarray(yd), ts, wl.d_t, ws,
+                          B * T, B, T, n_threads=NTHREADS)
+    check_stats(G, C, Go, Co, sel)
+    del src, tgt, w
+    plan.close()
+
+
 def test_stats_rope_rejects_what_it_cannot_fuse(cb):
     wl = synth.Workload("strope96", 2, 2, 96, 2, 2, 128, 2, 64, "qwen", "scaled", 0.1, "lognormal")
     src, tgt, w = make_inputs(wl)
