@@ -25,18 +25,18 @@
 // publishes it, so the copy wave waits for one more sub-block before each
 // barrier.
 //
-// Angles of the de-rotation.  A sender's table covers tens of thousands of
-// positions (16 MiB at 32,768 x 128), far more than L2, and each K group
-// would stream its rows: twice the bytes of the K rows themselves.  The
-// de-rotation therefore forms the (cos, sin) of position P = Q + r, Q = P - P
-// mod 32, from the table rows of Q and of r by the angle-addition formulas in
-// fp32: rows r < 32 are the same 16 KiB for every call and a whole sub-block
-// shares one or two rows Q, so its table traffic is about 1/32 of direct
-// reads.  Those angles carry about 1.5 fp32 ulp more error than the table's,
-// which moves a de-rotated bf16 input by one ulp only where it lies within
-// that distance of a rounding boundary.  The target rotation of the epilogue
-// reads the table directly (measured faster there: its entries are shared by
-// the two slots' waves, and its loads overlap the products).
+// Angles of the rotations.  A table covers tens of thousands of positions
+// (16 MiB at 32,768 x 128), far more than L2, and per-lane reads of each
+// token's row would move twice the bytes of the K rows themselves (the two
+// maps of a shared source read the same entries).  Both rotations therefore
+// form the (cos, sin) of position P = Q + r, Q = P - P mod 32, from the table
+// rows of Q and of r by the angle-addition formulas in fp32.  The copy wave
+// puts rows 0..31 of each table in LDS once per workgroup and, with every
+// sub-block, the one or two rows Q its 32 positions need; the lanes read
+// both from LDS.  Only a sub-block whose tokens cross into the next sequence
+// reads its rows from global memory.  Those angles carry about 1.5 fp32 ulp
+// more error than the table's, which moves a rotated bf16 value by one ulp
+// only where it lies within that distance of a rounding boundary.
 //
 // With the target's rotary transform fused (Sec. 2.1, Sec. 3.1: the mapped
 // keys receive the target's RoPE), the K outputs are turned in fp32 before
@@ -151,9 +151,7 @@ __device__ __forceinline__ int out_channel(int rb, int i) {
 // table row), from the rows of Q = P - P mod 32 and r = P mod 32:
 // cos(Q + r) = cos Q cos r - sin Q sin r, sin(Q + r) = sin Q cos r + cos Q sin r,
 // in fp32.  Returns (cos f, sin f, cos f+1, sin f+1) like a table read.
-__device__ __forceinline__ float4 angles2(const float *table, int row_floats, int P, int f) {
-    const float4 q = *reinterpret_cast<const float4 *>(table + (int64_t)(P & ~31) * row_floats + 2 * f);
-    const float4 r = *reinterpret_cast<const float4 *>(table + (int64_t)(P & 31) * row_floats + 2 * f);
+__device__ __forceinline__ float4 add_angles(const float4 q, const float4 r) {
     float4 o;
     o.x = __builtin_fmaf(q.x, r.x, -(q.y * r.y));
     o.y = __builtin_fmaf(q.y, r.x, q.x * r.y);
@@ -161,6 +159,20 @@ __device__ __forceinline__ float4 angles2(const float *table, int row_floats, in
     o.w = __builtin_fmaf(q.w, r.z, q.z * r.w);
     return o;
 }
+__device__ __forceinline__ float4 angles2(const float *table, int row_floats, int P, int f) {
+    const float4 q = *reinterpret_cast<const float4 *>(table + (int64_t)(P & ~31) * row_floats + 2 * f);
+    const float4 r = *reinterpret_cast<const float4 *>(table + (int64_t)(P & 31) * row_floats + 2 * f);
+    return add_angles(q, r);
+}
+
+// Position run of a 32-token sub-block: the in-sequence position tt0 of its
+// first token and whether its stored tokens stay in that sequence (then
+// token j sits at tt0 + j).  `last` is the offset of its last stored token.
+struct SubRun {
+    int tt0;
+    int last;
+    bool simple;
+};
 
 // One workgroup per (group, token tile).  The copy wave streams 32-token
 // sub-blocks of the group's source rows HBM -> LDS through an NST-stage ring
@@ -181,6 +193,21 @@ __global__ __attribute__((amdgpu_flat_work_group_size(ACfg<DS, DT>::NT, ACfg<DS,
     constexpr int NCBT = DT / 8;
     constexpr int OBUF = K::SB * DT * 2;
     __shared__ __attribute__((aligned(16))) char obuf[STAGE ? 2 * 2 * OBUF : 16];
+    // Rotation angles in LDS (a sub-block whose tokens stay in one sequence):
+    // per stage, table rows Q0 and Q0 + 32 of the sub-block's positions
+    // (Q0 = first position rounded down to a multiple of 32), one 1 KiB slot
+    // per table; per workgroup, table rows 0..31, 16-byte chunk c of row r at
+    // chunk (c + r) mod (chunks per row).  Position P's angles are those of
+    // Q + (P mod 32) by angle addition, as in the de-rotation below.  Slot 0
+    // is the target's table (RS), the last slot the sender's (SR).
+    constexpr int NQ = (RS != kRopeNone ? 1 : 0) + (SR != 0 ? 1 : 0);
+    constexpr int QSLOT = 1024;
+    constexpr int NCHT = DT / 4, NCHS = DS / 4;           // 16-byte chunks per table row
+    constexpr int RROWT = RS != kRopeNone ? 32 * DT * 4 : 0;
+    constexpr int RROWS = SR != 0 ? 32 * DS * 4 : 0;
+    __shared__ __attribute__((aligned(16))) char qbuf[NQ ? K::NST * NQ * QSLOT : 16];
+    __shared__ __attribute__((aligned(16))) char rrows[RROWT + RROWS ? RROWT + RROWS : 16];
+    constexpr int PER = K::COPIES + NQ;                   // copy instructions per stage
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -196,9 +223,19 @@ __global__ __attribute__((amdgpu_flat_work_group_size(ACfg<DS, DT>::NT, ACfg<DS,
     const uint16_t *xsrc = a.src + grp->src_layer * a.ss.layer + kv * a.ss.kv + grp->src_head * a.ss.head;
 
     const bool turn_src = SR != 0 && kv == 0;                 // only keys carry positions
+    auto sub_run = [&](int sb) __attribute__((always_inline)) {
+        const int tau0 = min(tok0 + sb * K::SB, tok1 - 1);
+        const uint32_t b0 = fastdiv((uint32_t)tau0, a.T);
+        SubRun u;
+        u.tt0 = (int)((uint32_t)tau0 - b0 * a.T.d);
+        u.last = min(tau0 + K::SB - 1, tok1 - 1) - tau0;
+        u.simple = u.tt0 + u.last < (int)a.T.d;
+        return u;
+    };
     if (wave == K::NWC) {
         // ---- copy wave: copy i of a stage moves LDS chunks 64 i + lane
         const uint32_t lds_base = (uint32_t)(uintptr_t)lds;
+        const uint32_t lds_q = (uint32_t)(uintptr_t)qbuf, lds_r = (uint32_t)(uintptr_t)rrows;
         auto issue = [&](int sb, int st) {
 #pragma unroll
             for (int i = 0; i < K::COPIES; ++i) {
@@ -211,16 +248,44 @@ __global__ __attribute__((amdgpu_flat_work_group_size(ACfg<DS, DT>::NT, ACfg<DS,
                 const uint16_t *src = xsrc + (int64_t)b * a.ss.seq + (int64_t)tt * a.ss.tok + cb * 8;
                 dma16(src, __builtin_amdgcn_readfirstlane(lds_base + st * K::STB + i * 1024));
             }
+            if constexpr (NQ != 0) {
+                // rows Q0 and Q0 + 32 of each table (Q0 alone when the run ends
+                // below Q0 + 32, or when its tokens leave the sequence: then the
+                // rows are not used and any valid row will do)
+                const SubRun u = sub_run(sb);
+                auto qrows = [&](const float *tab, int nch, int off, int qs) __attribute__((always_inline)) {
+                    const int p0 = off + u.tt0, q0 = p0 & ~31;
+                    const int q1 = (u.simple && q0 + 32 <= p0 + u.last) ? q0 + 32 : q0;
+                    const int row = min(lane / nch, 1), ch = min(lane - row * nch, nch - 1);
+                    const float *src = tab + (int64_t)(row ? q1 : q0) * (4 * nch) + 4 * ch;
+                    dma16(src, __builtin_amdgcn_readfirstlane(lds_q + (st * NQ + qs) * QSLOT));
+                };
+                if constexpr (RS != kRopeNone) qrows(a.rope_table, NCHT, a.rope_pos_offset, 0);
+                if constexpr (SR != 0) qrows(a.src_rope_table, NCHS, a.src_rope_pos_offset, NQ - 1);
+            }
         };
+        // rows 0..31 of each table (rows past the last position any call
+        // reads are clamped to it: they are never used)
+        auto rrows_copy = [&](const float *tab, int nch, int off, uint32_t dst) __attribute__((always_inline)) {
+            const int maxpos = off + (int)a.T.d - 1;
+            for (int i = 0; i < nch / 2; ++i) {
+                const int q = 64 * i + lane;
+                const int r = q / nch, pch = q - r * nch;
+                const int c = (pch - r % nch + nch) % nch;
+                dma16(tab + (int64_t)min(r, maxpos) * (4 * nch) + 4 * c, __builtin_amdgcn_readfirstlane(dst + i * 1024));
+            }
+        };
+        if constexpr (RS != kRopeNone) rrows_copy(a.rope_table, NCHT, a.rope_pos_offset, lds_r);
+        if constexpr (SR != 0) rrows_copy(a.src_rope_table, NCHS, a.src_rope_pos_offset, lds_r + RROWT);
 #pragma unroll
         for (int s = 0; s < K::NST - 1; ++s) issue(s, s);
         if constexpr (SR != 0) {
-            wait_vm<(K::NST - 3) * K::COPIES>();               // sub-blocks 0 and 1 have landed
+            wait_vm<(K::NST - 3) * PER>();                     // sub-blocks 0 and 1 have landed
             lds_barrier();
         }
         for (int sb = 0; sb < n_sb; ++sb) {
             // sub-block sb has landed (and, with the de-rotation, sb + 1, which is turned during sb)
-            wait_vm<(K::NST - 2 - (SR != 0 ? 1 : 0)) * K::COPIES>();
+            wait_vm<(K::NST - 2 - (SR != 0 ? 1 : 0)) * PER>();
             lds_barrier();
             issue(sb + K::NST - 1, (sb + K::NST - 1) % K::NST);
         }
@@ -274,6 +339,22 @@ __global__ __attribute__((amdgpu_flat_work_group_size(ACfg<DS, DT>::NT, ACfg<DS,
     // 8c .. 8c + 7; interleaved, 4c .. 4c + 3 and 4(c + NCB/2) .. + 3
     auto tab_load = [&](float4 (&cs)[4], int sb) __attribute__((always_inline)) {
         if constexpr (SR != 0) {
+            const SubRun u = sub_run(sb);
+            if (u.simple) {
+                // rows Q0 / Q0 + 32 of the stage and rows 0..31 of the workgroup, in LDS
+                const int P = a.src_rope_pos_offset + u.tt0 + (ulive ? tu : 0);   // idle lanes: any row
+                const int qi = (P >> 5) - ((a.src_rope_pos_offset + u.tt0) >> 5), r = P & 31;
+                const char *Q = qbuf + ((sb % K::NST) * NQ + NQ - 1) * QSLOT + qi * (NCHS * 16);
+                const char *R = rrows + RROWT + r * (NCHS * 16);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int ch = SR == 1 ? 4 * cu + j : 2 * (j < 2 ? cu : cu + HP) + (j & 1);   // frequency / 2
+                    const float4 q = *reinterpret_cast<const float4 *>(Q + ch * 16);
+                    const float4 rr = *reinterpret_cast<const float4 *>(R + ((ch + r) % NCHS) * 16);
+                    cs[j] = add_angles(q, rr);
+                }
+                return;
+            }
             const int tau = min(tok0 + sb * K::SB + tu, tok1 - 1);
             const uint32_t tt = (uint32_t)tau - fastdiv((uint32_t)tau, a.T) * a.T.d;
             const int P = a.src_rope_pos_offset + (int)tt;
@@ -328,6 +409,23 @@ __global__ __attribute__((amdgpu_flat_work_group_size(ACfg<DS, DT>::NT, ACfg<DS,
     // target rotation: (cos, sin) of the lane's eight rotated pairs in a sub-block
     auto tcs_load = [&](float4 (&cs)[4], int sb) __attribute__((always_inline)) {
         if constexpr (RS != kRopeNone) {
+            const SubRun u = sub_run(sb);
+            if (u.simple) {
+                const int P = a.rope_pos_offset + u.tt0 + (int)lrow;
+                const int qi = (P >> 5) - ((a.rope_pos_offset + u.tt0) >> 5), r = P & 31;
+                const char *Q = qbuf + (sb % K::NST) * NQ * QSLOT + qi * (NCHT * 16);
+                const char *R = rrows + r * (NCHT * 16);
+#pragma unroll
+                for (int gq = 0; gq < 4; ++gq) {
+                    // chunk = frequency / 2 (as in the table reads below)
+                    const int ch = RS == kRopeHalf ? rb * 8 + 4 * (gq >> 1) + 2 * (int)lhalf + (gq & 1)
+                                                   : rb * 8 + 2 * gq + (int)lhalf;
+                    const float4 q = *reinterpret_cast<const float4 *>(Q + ch * 16);
+                    const float4 rr = *reinterpret_cast<const float4 *>(R + ((ch + r) % NCHT) * 16);
+                    cs[gq] = add_angles(q, rr);
+                }
+                return;
+            }
             const int tau = min(tok0 + sb * K::SB + (int)lrow, tok1 - 1);
             const uint32_t tt = (uint32_t)tau - fastdiv((uint32_t)tau, a.T) * a.T.d;
             const float *row = a.rope_table + (int64_t)(a.rope_pos_offset + (int)tt) * DT;   // [d/2][2] per position
@@ -347,8 +445,6 @@ __global__ __attribute__((amdgpu_flat_work_group_size(ACfg<DS, DT>::NT, ACfg<DS,
     for (int sb = 0; sb < n_sb + (STAGE ? 1 : 0); ++sb) {
         lds_barrier();                                         // sub-block sb has landed (and is turned)
         const bool turn_next = SR != 0 && turn_src && sb + 1 < n_sb;
-        float4 scs[4];
-        if (turn_next) tab_load(scs, sb + 1);
         if (STAGE && active && sb > 0) {
             // 4 DT chunks of 16 bytes: two rounds of the slot's RBT waves
             const char *ob = obuf + (((sb - 1) & 1) * 2 + slot) * OBUF;
@@ -365,7 +461,12 @@ __global__ __attribute__((amdgpu_flat_work_group_size(ACfg<DS, DT>::NT, ACfg<DS,
                 }
             }
         }
-        if (turn_next) turn_sub(sb + 1, scs);
+        if (turn_next) {
+            // the angles come from LDS (global reads only for a run that leaves its sequence)
+            float4 scs[4];
+            tab_load(scs, sb + 1);
+            turn_sub(sb + 1, scs);
+        }
         if (STAGE && sb == n_sb) break;
         if (!active) continue;
         const char *B = lds + (sb % K::NST) * K::STB;
