@@ -17,7 +17,8 @@
  * fusedstats; Sec. 3.1, Eq. closedform):
  *
  *   cb_stats_zero_centered, cb_stats_means, cb_stats_accumulate_centered,
- *   cb_ridge_solve_centered
+ *   cb_ridge_solve_centered (and its one-pass form cb_stats_accumulate_shifted,
+ *   cb_stats_shift_finish)
  *
  * and the layer-selection probes of Sec. 3.1 (centered single-source-layer
  * fits ranked by held-in R^2):
@@ -254,6 +255,41 @@ cb_status cb_stats_means(cb_plan *plan, const cb_cache *src, const cb_cache *tgt
 cb_status cb_stats_accumulate_centered(cb_plan *plan, const cb_cache *src, const cb_cache *tgt,
                                        const float *weights, int64_t w_row_stride, const double *sums,
                                        float *A, float *B, void *stream);
+
+/*
+ * One-pass form of the same centered statistics (Sec. 3.4, Eq. fusedstats:
+ * moments about the weighted means).  Pass 1 of the two-pass form reads every
+ * calibration row once more only to learn the means; here the moments are
+ * formed about the means of a pilot instead (`shift`: the sums that
+ * cb_stats_means left for any subset of the data, e.g. the first few
+ * sequences; zero sums mean no shift), while the same pass also sums the
+ * weights, the residuals and the targets, and cb_stats_shift_finish then moves
+ * the moments to the data's own means:
+ *   shift [n_maps][1 + d_x + d_t] fp64, read: mu'_x = shift_x / shift_w, mu'_y likewise
+ *   accumulate, per batch:  A[m] += sum w (x - mu'_x)(x - mu'_x)^T
+ *                           B[m] += sum w (x - mu'_x)(y - mu'_y)^T
+ *                           sums[m] += (sum w, sum w (x - mu'_x), sum w y)
+ *   finish, once:  with S = sum w, delta = (sum w (x - mu'_x)) / S = mu_x - mu'_x,
+ *                  A[m] -= S delta delta^T,  B[m] -= S delta (mu_y - mu'_y)^T  (fp64, rounded once)
+ *                  and sums[m] becomes (sum w, sum w x, sum w y)
+ * after which sums, A and B are those of the two-pass form (the same exact
+ * values; the differences are rounding) and go to cb_ridge_solve_centered or
+ * cb_ridge_solve_centered_ws.  The closer the pilot means are to the data's,
+ * the smaller the correction: the pilot only has to remove the channels'
+ * large common offsets.  Products, splits and fp32 sums as in
+ * cb_stats_accumulate_centered; the three sums run in fp32 within a work unit
+ * and in fp64 across units and calls (about 1e-7 relative), where pass 1 is
+ * exact.  Zero sums, A and B before the first call (cb_stats_zero_centered);
+ * shift must not change between the calls of one fit and must not be sums.
+ * Single- and multi-layer plans; d_x = d_s or k d_s.  Arguments, limits and
+ * errors as in cb_stats_accumulate_centered, plus CB_ERR_INVALID_ARGUMENT
+ * when shift is NULL or equals sums.
+ */
+cb_status cb_stats_accumulate_shifted(cb_plan *plan, const cb_cache *src, const cb_cache *tgt,
+                                      const float *weights, int64_t w_row_stride, const double *shift,
+                                      double *sums, float *A, float *B, void *stream);
+cb_status cb_stats_shift_finish(const cb_plan *plan, const double *shift, double *sums, float *A, float *B,
+                                void *stream);
 
 /*
  * Centered ridge solve (Sec. 3.1, Eq. closedform):

@@ -13,7 +13,10 @@ current HIP stream.  The functions keep the C names:
 * :func:`cb_stats_zero_centered`, :func:`cb_stats_means`,
   :func:`cb_stats_accumulate_centered`, :func:`cb_ridge_solve_centered` -- the
   two-pass centered form: weighted sums, centered moments A, B (Sec. 3.4) and
-  W = (A + lambda I)^-1 B, b = mu_y - W^T mu_x (Sec. 3.1)
+  W = (A + lambda I)^-1 B, b = mu_y - W^T mu_x (Sec. 3.1);
+  :func:`cb_stats_accumulate_shifted`, :func:`cb_stats_shift_finish` -- the same
+  moments in one pass over the data, formed about a pilot's means and moved to
+  the data's own means at the end
 * :func:`cb_probe_r2`, :func:`cb_select_layers` -- layer-selection probes: held-in
   R^2 per probe map and the top-k source layers per target layer (Sec. 3.1)
 * :func:`cb_attn_sensitivity`, :func:`cb_attn_weights` -- attention-aligned
@@ -139,6 +142,11 @@ _lib.cb_select_layers.argtypes = [ctypes.POINTER(CbHeadMap), _vp, ctypes.c_int32
 _lib.cb_stats_accumulate_centered.restype = ctypes.c_int
 _lib.cb_stats_accumulate_centered.argtypes = [_vp, ctypes.POINTER(CbCache), ctypes.POINTER(CbCache), _vp,
                                               ctypes.c_int64, _vp, _vp, _vp, _vp]
+_lib.cb_stats_accumulate_shifted.restype = ctypes.c_int
+_lib.cb_stats_accumulate_shifted.argtypes = [_vp, ctypes.POINTER(CbCache), ctypes.POINTER(CbCache), _vp,
+                                             ctypes.c_int64, _vp, _vp, _vp, _vp, _vp]
+_lib.cb_stats_shift_finish.restype = ctypes.c_int
+_lib.cb_stats_shift_finish.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp]
 _lib.cb_ridge_solve_centered.restype = ctypes.c_int
 _lib.cb_ridge_solve_centered.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _vp, _vp, _vp,
                                          ctypes.c_float, ctypes.c_uint32, _vp, _vp, _vp]
@@ -449,6 +457,30 @@ def cb_stats_accumulate_centered(plan: Plan, src: torch.Tensor, tgt: torch.Tenso
     sv, tv = cache_view(src), cache_view(tgt)
     _check(_lib.cb_stats_accumulate_centered(plan.handle, ctypes.byref(sv), ctypes.byref(tv), _ptr(weights), rs, _ptr(sums), _ptr(A), _ptr(B),
                                              _stream(stream)))
+
+
+def cb_stats_accumulate_shifted(plan: Plan, src: torch.Tensor, tgt: torch.Tensor, weights: torch.Tensor,
+                                shift: torch.Tensor, sums: torch.Tensor, A: torch.Tensor, B: torch.Tensor,
+                                w_row_stride: Optional[int] = None, stream=None):
+    """One-pass centered moments: A[m] += sum w (x - mu'_x)(x - mu'_x)^T, B[m] += sum w (x - mu'_x)(y - mu'_y)^T
+    about the means mu' of ``shift`` (a pilot's sums from :func:`cb_stats_means`), and sums[m] +=
+    (sum w, sum w (x - mu'_x), sum w y); :func:`cb_stats_shift_finish` completes them."""
+    _need_centered(plan, shift, None, None, None)
+    _need_centered(plan, sums, A, B, None)
+    rs = _row_stride(weights, w_row_stride)
+    _check_weights(plan, weights, rs, src)
+    sv, tv = cache_view(src), cache_view(tgt)
+    _check(_lib.cb_stats_accumulate_shifted(plan.handle, ctypes.byref(sv), ctypes.byref(tv), _ptr(weights), rs,
+                                            _ptr(shift), _ptr(sums), _ptr(A), _ptr(B), _stream(stream)))
+
+
+def cb_stats_shift_finish(plan: Plan, shift: torch.Tensor, sums: torch.Tensor, A: torch.Tensor, B: torch.Tensor,
+                          stream=None):
+    """Moves A, B from the pilot's means to the data's (A -= S d d^T, B -= S d (mu_y - mu'_y)^T, d = mu - mu')
+    and turns sums into (sum w, sum w x, sum w y): then they are those of the two-pass form."""
+    _need_centered(plan, shift, None, None, None)
+    _need_centered(plan, sums, A, B, None)
+    _check(_lib.cb_stats_shift_finish(plan.handle, _ptr(shift), _ptr(sums), _ptr(A), _ptr(B), _stream(stream)))
 
 
 def cb_ridge_solve_centered(sums: torch.Tensor, A: torch.Tensor, B: torch.Tensor, lam: float, flags: int,

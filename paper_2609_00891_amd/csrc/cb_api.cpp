@@ -996,6 +996,59 @@ cb_status cb_stats_accumulate_centered(cb_plan *p, const cb_cache *src, const cb
     return ok();
 }
 
+cb_status cb_stats_accumulate_shifted(cb_plan *p, const cb_cache *src, const cb_cache *tgt, const float *weights,
+                                      int64_t w_row_stride, const double *shift, double *sums, float *A, float *B,
+                                      void *stream) {
+    if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
+    if (!shift || !sums || !A || !B) return fail(CB_ERR_INVALID_ARGUMENT, "shift, sums, A and B must be non-NULL");
+    if (((uintptr_t)shift) % 8 || ((uintptr_t)sums) % 8 || ((uintptr_t)A) % 4 || ((uintptr_t)B) % 4)
+        return fail(CB_ERR_MISALIGNED, "shift and sums must be 8-byte and A, B 4-byte aligned");
+    if (shift == sums) return fail(CB_ERR_INVALID_ARGUMENT, "shift and sums must be different arrays");
+    if (p->multi) {
+        cb::MultiArgs ma = {};
+        bool empty = false;
+        if (cb_status s = prepare_multi(p, src, tgt, weights, w_row_stride, ma, empty)) return s;
+        if (empty) return ok();
+        ma.G = A;
+        ma.C = B;
+        ma.sums = shift;
+        ma.resid = sums;
+        if (cb::launch_stats_multi_centered(ma, (hipStream_t)stream) != hipSuccess)
+            return fail(CB_ERR_DEVICE, "multi-layer centered statistics kernel launch failed");
+        return ok();
+    }
+    cb::StatsArgs a = {};
+    bool empty = false;
+    if (cb_status s = prepare_stats(p, src, tgt, weights, w_row_stride, a, empty)) return s;
+    if (empty) return ok();
+    a.sums = shift;
+    a.bias_sums = 1;
+    hipStream_t st = (hipStream_t)stream;
+    if (cb::launch_stats_centered(p->d_s, p->d_t, a, st) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "centered statistics kernel launch failed");
+    cb::ReduceArgs r = reduce_args(p, a);
+    r.G = A;
+    r.C = B;
+    r.sums = const_cast<double *>(shift);     // read only by the centered reduction
+    r.resid = sums;
+    if (cb::launch_reduce_centered(p->d_s, p->d_t, r, st) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "centered reduction launch failed");
+    return ok();
+}
+
+cb_status cb_stats_shift_finish(const cb_plan *p, const double *shift, double *sums, float *A, float *B, void *stream) {
+    if (!p || !shift || !sums || !A || !B)
+        return fail(CB_ERR_INVALID_ARGUMENT, "plan, shift, sums, A and B must be non-NULL");
+    if (((uintptr_t)shift) % 8 || ((uintptr_t)sums) % 8 || ((uintptr_t)A) % 4 || ((uintptr_t)B) % 4)
+        return fail(CB_ERR_MISALIGNED, "shift and sums must be 8-byte and A, B 4-byte aligned");
+    if (shift == sums) return fail(CB_ERR_INVALID_ARGUMENT, "shift and sums must be different arrays");
+    if (cb_status s = check_device(p)) return s;
+    const int32_t dx = p->multi ? p->P - 1 : p->d_s;
+    if (cb::launch_shift_finish(p->n_maps, dx, p->d_t, shift, sums, A, B, (hipStream_t)stream) != hipSuccess)
+        return fail(CB_ERR_DEVICE, "shift finish launch failed");
+    return ok();
+}
+
 cb_status cb_ridge_solve(int32_t n_maps, int32_t P, int32_t d_t, const float *G, const float *C, float lambda,
                          uint32_t flags, float *maps, int32_t *info, void *stream) {
     if (n_maps < 0) return fail(CB_ERR_INVALID_ARGUMENT, "n_maps is negative");

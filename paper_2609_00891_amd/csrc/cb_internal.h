@@ -68,6 +68,7 @@ struct StatsArgs {
     float *partials;      // [n_chunks * n_items][2][slot_floats]
     const void *zero;     // >= 256 zero bytes: source of the weights of absent tokens
     const double *sums;   // centered statistics only: [n_maps][1 + d_s + d_t] = (sum w, sum w x, sum w y)
+    int32_t bias_sums;    // centered kernels: 1 = also sum w and w y (the shifted form needs them)
     // Rotary de-rotation of the K rows as they land (the rope variant of the
     // kernel only): tables [n_pos][d/2][2] (cos, sin) of the source and the
     // target (both valid pointers), position of token 0, and which side turns.
@@ -85,6 +86,7 @@ struct ReduceArgs {
     float *G, *C;         // plain: G [n][P][P], C [n][P][d_t]; centered: A [n][d_s][d_s], B [n][d_s][d_t]
     double *sums;         // centered: read; means: added to.  [n_maps][1 + d_s + d_t] = (sum w, sum w x, sum w y)
     double *sq;           // means only, optional: added to.  [n_maps][d_s + d_t] = (sum w x^2, sum w y^2)
+    double *resid;        // centered, optional: added to.  [n_maps][1 + d_s + d_t] = (sum w, sum w (x - mu), sum w y)
 };
 
 struct ApplyArgs {
@@ -164,6 +166,7 @@ struct MultiArgs {
     const void *zero;         // >= 256 zero bytes
     float *G, *C;             // centered: A [n][P-1][P-1], B [n][P-1][d_t]
     const double *sums;       // centered only: [n][P + d_t] = (sum w, sum w x, sum w y)
+    double *resid;            // centered, optional: added to.  [n][P + d_t] = (sum w, sum w (x - mu), sum w y)
     // NULL, or compact de-rotated calibration rows of the K maps, [layer][seq][head][row][d]:
     // K tasks read their source / target blocks there (tok stride = one calibration row)
     const uint16_t *srck, *tgtk;
@@ -235,6 +238,10 @@ hipError_t launch_solve_centered(int32_t n_maps, int32_t d_s, int32_t d_t, const
                                  const float *B, float lambda, uint32_t flags, float *maps, int32_t *info,
                                  hipStream_t s);
 hipError_t launch_fill_zero(float *p, int64_t n, hipStream_t s);
+// Shifted centered form: turns moments about the shift means into moments
+// about the data's means, and the residual sums into (sum w, sum w x, sum w y).
+hipError_t launch_shift_finish(int32_t n_maps, int32_t d_x, int32_t d_t, const double *shift, double *sums, float *A,
+                               float *B, hipStream_t s);
 hipError_t launch_stats_multi(const MultiArgs &a, hipStream_t s);
 hipError_t launch_stats_multi_centered(const MultiArgs &a, hipStream_t s);
 hipError_t launch_means_multi(const MeansMultiArgs &a, hipStream_t s);

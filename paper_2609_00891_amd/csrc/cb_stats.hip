@@ -26,6 +26,8 @@
 // reduce_kernel (one workgroup per map) adds the partials of all chunks in a
 // fixed order, mirrors the Gram block so G is exactly symmetric, and adds the
 // result into the caller's G and C.
+#include <algorithm>
+
 #include "cb_stats_kernel.h"
 
 namespace cb {
@@ -144,7 +146,25 @@ __global__ __launch_bounds__(256) void reduce_kernel(ReduceArgs a) {
         }
         return;
     }
-    if constexpr (CENTER) return;                             // no bias row / column
+    if constexpr (CENTER) {
+        // no bias row / column; the shifted form adds the batch's (sum w,
+        // sum w (x - mu), sum w y) to resid, summed over the chunks in fp64
+        if (!a.resid) return;
+        double *rs = a.resid + (int64_t)m * (1 + DS + DT);
+        for (int e = tid; e < DS + DT + 1; e += 256) {
+            int i0;
+            if (e == 0) i0 = K::SUMW;
+            else if (e <= DS) i0 = K::SUMX + ((e - 1) >> 5) * 64 + ((e - 1) & 31);
+            else i0 = K::SUMY + ((e - 1 - DS) >> 5) * 64 + ((e - 1 - DS) & 31);
+            double acc = 0.0;
+            for (int ch = 0; ch < a.n_chunks; ++ch) {
+                const float *pp = base + ch * chunk_stride;
+                acc += (double)pp[i0] + (double)pp[i0 + 32];
+            }
+            rs[e] += acc;
+        }
+        return;
+    }
 
     // bias sums: row / column P-1 of G and row P-1 of C (two lane halves each)
     for (int e = tid; e < DS + DT + 1; e += 256) {
@@ -198,11 +218,73 @@ template <int DS, int DT>
 hipError_t launch_reduce_centered_t(const ReduceArgs &a, hipStream_t s) {
     if (a.n_maps == 0) return hipSuccess;
     using K = Cfg<DS, DT>;
-    hipLaunchKernelGGL((reduce_kernel<DS, DT, true>), dim3(a.n_maps, K::NTG + K::NTC), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((reduce_kernel<DS, DT, true>), dim3(a.n_maps, K::NTG + K::NTC + (a.resid ? 1 : 0)), dim3(256), 0,
+                       s, a);
     return hipGetLastError();
 }
 
+// Shifted centered form, last step.  The moments were formed about the means
+// mu' of `shift` (a pilot's sums), resid holds (S, e = sum w (x - mu'), sum w y)
+// of all the data.  With delta = e / S = mu - mu' and mu_y = (sum w y) / S:
+//     sum w (x - mu)(x - mu)^T = A' - S delta delta^T
+//     sum w (x - mu)(y - mu_y)^T = B' - S delta (mu_y - mu'_y)^T
+// (fp64, rounded once to fp32), then sum w x = e + S mu' replaces e.
+__device__ __forceinline__ double mean_of(const double *sm, int i) { return sm[0] != 0.0 ? sm[1 + i] / sm[0] : 0.0; }
+
+__global__ __launch_bounds__(256) void shift_moments_kernel(int32_t n_maps, int32_t d_x, int32_t d_t,
+                                                            const double *__restrict__ shift,
+                                                            const double *__restrict__ sums, float *__restrict__ A,
+                                                            float *__restrict__ B) {
+    const int64_t na = (int64_t)d_x * d_x, per = na + (int64_t)d_x * d_t, n = per * n_maps;
+    for (int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x; g < n; g += (int64_t)gridDim.x * 256) {
+        const int64_t m = g / per, e = g - m * per;
+        const double *sh = shift + m * (1 + d_x + d_t);
+        const double *su = sums + m * (1 + d_x + d_t);
+        const double S = su[0];
+        if (S == 0.0) continue;                               // no data: nothing to move
+        if (e < na) {
+            const int i = (int)(e / d_x), j = (int)(e - (int64_t)i * d_x);
+            const double di = su[1 + i] / S, dj = su[1 + j] / S;
+            float *p = A + m * na + e;
+            *p = (float)((double)*p - S * (di * dj));           // the same value at (j, i): A stays symmetric
+        } else {
+            const int64_t f = e - na;
+            const int i = (int)(f / d_t), j = (int)(f - (int64_t)i * d_t);
+            const double di = su[1 + i] / S;
+            const double dy = su[1 + d_x + j] / S - mean_of(sh, d_x + j);
+            float *p = B + m * (int64_t)d_x * d_t + f;
+            *p = (float)((double)*p - S * di * dy);
+        }
+    }
+}
+
+__global__ __launch_bounds__(256) void shift_sums_kernel(int32_t n_maps, int32_t d_x, int32_t d_t,
+                                                         const double *__restrict__ shift, double *__restrict__ sums) {
+    const int64_t n = (int64_t)n_maps * d_x;
+    for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < n; e += (int64_t)gridDim.x * 256) {
+        const int64_t m = e / d_x;
+        const int i = (int)(e - m * d_x);
+        const double *sh = shift + m * (1 + d_x + d_t);
+        double *su = sums + m * (1 + d_x + d_t);
+        su[1 + i] += su[0] * mean_of(sh, i);
+    }
+}
+
 }  // namespace
+
+hipError_t launch_shift_finish(int32_t n_maps, int32_t d_x, int32_t d_t, const double *shift, double *sums, float *A,
+                               float *B, hipStream_t s) {
+    if (n_maps == 0) return hipSuccess;
+    const int64_t tot = (int64_t)n_maps * d_x * (d_x + d_t);
+    const unsigned bx = (unsigned)std::min<int64_t>((tot + 255) / 256, 16384);
+    hipLaunchKernelGGL(shift_moments_kernel, dim3(bx), dim3(256), 0, s, n_maps, d_x, d_t, shift, sums, A, B);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int64_t n = (int64_t)n_maps * d_x;
+    const unsigned g = (unsigned)std::min<int64_t>((n + 255) / 256, 8192);
+    hipLaunchKernelGGL(shift_sums_kernel, dim3(g), dim3(256), 0, s, n_maps, d_x, d_t, shift, sums);
+    return hipGetLastError();
+}
 
 hipError_t launch_stats(int d_s, int d_t, const StatsArgs &a, hipStream_t s) {
     CB_DISPATCH(launch_stats_t, d_s, d_t, a, s);

@@ -658,7 +658,9 @@ __device__ __forceinline__ void stats_wave(const StatsArgs &a, const StatsCtx c,
     // halves: half k adds sum w y over this pair's k-th y column block (blocks
     // PR, PR + 2), and half 1 also sum w (pair 0 only).
     auto fold_sums = [&](const Ops &o, int half) {
-        if constexpr (CENTER) return;                        // only sum w (x - mu) is needed
+        if constexpr (CENTER) {
+            if (!a.bias_sums) return;                        // two-pass form: only sum w (x - mu) is needed
+        }
         if (PR == 0 && half == 1)
             sumw += ((o.w[0] + o.w[1]) + (o.w[2] + o.w[3])) + ((o.w[4] + o.w[5]) + (o.w[6] + o.w[7]));
         const int cc = PR + 2 * half;

@@ -863,6 +863,58 @@ def test_multi_centered_widths_ragged_offset_and_uncentered_gap(cb, k, stride, T
     plan.close()
 
 
+TOL_SUMS_SHIFTED = 1e-6   # one-pass form: sums of fp32 partials, added in fp64 at every flush
+
+
+@pytest.mark.parametrize("k,stride,T", [(2, 3, 520), (5, 2, 858)])
+def test_multi_shifted_one_pass_offset_means(cb, k, stride, T):
+    # the offset-means inputs of the two-pass test, in one pass about the means
+    # of a one-sequence pilot, then moved to the data's means: the oracle's
+    # centered sums, A and B, and the two-pass GPU moments
+    rng = np.random.default_rng(3000 + 10 * k + stride)
+    L_s, H_s, L_t, H_t, B_ = 6, 2, 2, 2, 3
+    src, tgt, w = small_inputs(rng, L_s, H_s, L_t, H_t, B_, T)
+    g = torch.Generator(device="cpu")
+    g.manual_seed(77 + k)
+    mu = (40.0 * torch.randn((L_s, 2, 1, H_s, 1, 128), generator=g)).to("cuda")
+    src = (src.float() + mu).to(torch.bfloat16)
+    hm = random_multi_map(rng, k, L_s, H_s, L_t, H_t)
+    plan = cb.cb_plan_create_multi(hm, src, tgt, stride)
+    cut = lambda a, b: (src[:, :, a:b], tgt[:, :, a:b], w.reshape(-1, B_, T)[:, a:b].reshape(w.shape[0], -1))  # noqa: E731
+    batches = [cut(0, 1), cut(1, 3)]
+    n, Dx, dt = plan.n_maps, plan.P - 1, plan.d_t
+    shift = torch.zeros((n, 1 + Dx + dt), dtype=torch.float64, device="cuda")
+    sums = torch.empty_like(shift)
+    A = torch.empty((n, Dx, Dx), dtype=torch.float32, device="cuda")
+    B = torch.empty((n, Dx, dt), dtype=torch.float32, device="cuda")
+    cb.cb_stats_zero_centered(plan, sums, A, B)
+    cb.cb_stats_means(plan, *cut(0, 1), shift)
+    for s_, t_, w_ in batches:
+        cb.cb_stats_accumulate_shifted(plan, s_, t_, w_, shift, sums, A, B)
+    cb.cb_stats_shift_finish(plan, shift, sums, A, B)
+    torch.cuda.synchronize()
+    so, Ao, Bo = oracle_centered_full(hm, src, tgt, w, stride)
+    sel = list(range(n))
+    Ag, Bg, sg = A.double().cpu().numpy(), B.double().cpu().numpy(), sums.cpu().numpy()
+    es = max(relF(sg[m], so[m]) for m in sel)
+    ea = max(relF(Ag[m], Ao[m]) for m in sel)
+    eb = max(relF(Bg[m], Bo[m]) for m in sel)
+    say(f"  shifted (k={k}, stride {stride}): sums {es:.3e}, A {ea:.3e}, B {eb:.3e}")
+    assert es <= TOL_SUMS_SHIFTED and ea <= TOL_STATS and eb <= TOL_STATS
+    assert np.array_equal(Ag, np.transpose(Ag, (0, 2, 1))), "A must be exactly symmetric"
+    s2, A2, B2 = gpu_centered_multi(cb, plan, batches)
+    d = max(relF(Ag[m], A2[m].double().cpu().numpy()) for m in sel)
+    say(f"  shifted vs two-pass A: {d:.3e}")
+    assert d <= TOL_STATS
+    Wo, io = oracle.ridge_solve_centered(so, Ao, Bo, 1e-2, relative=True, n_threads=NTHREADS)
+    maps, info = gpu_solve_centered_ws(cb, sums, A, B)
+    assert int((info != 0).sum()) == 0 and (io == 0).all()
+    e2e = max(relF(maps[m].double().cpu().numpy(), Wo[m]) for m in sel)
+    say(f"  shifted maps end to end: {e2e:.3e}")
+    assert e2e <= TOL_MAPS
+    plan.close()
+
+
 def test_multi_centered_zero_weights_and_determinism(cb):
     rng = np.random.default_rng(41)
     k, stride, L_s, H_s, L_t, H_t, B_, T = 3, 4, 5, 2, 2, 2, 2, 600

@@ -456,7 +456,7 @@ def oracle_centered_sel(hm, sel, src, tgt, w):
                                  n_threads=NTHREADS)
 
 
-def check_centered(sums, A, B, so, Ao, Bo, sel, tol=TOL_STATS):
+def check_centered(sums, A, B, so, Ao, Bo, sel, tol=TOL_STATS, tol_sums=TOL_SUMS):
     idx = torch.as_tensor(sel, device=A.device)
     sg = sums[idx].cpu().numpy()
     Ag = A[idx].double().cpu().numpy()
@@ -465,7 +465,7 @@ def check_centered(sums, A, B, so, Ao, Bo, sel, tol=TOL_STATS):
     ea = max(relF(Ag[i], Ao[i]) for i in range(len(sel)))
     eb = max(relF(Bg[i], Bo[i]) for i in range(len(sel)))
     say(f"  centered parity: max relF sums {es:.3e}, A {ea:.3e}, B {eb:.3e}")
-    assert es <= TOL_SUMS and ea <= tol and eb <= tol
+    assert es <= tol_sums and ea <= tol and eb <= tol
     assert np.array_equal(Ag, np.transpose(Ag, (0, 2, 1))), "A must be exactly symmetric"
     return es, ea, eb
 
@@ -614,6 +614,102 @@ def test_centered_zero_weights_empty_calls_and_determinism(cb):
     assert all(inf[m] == 1 for m in zero_maps) and all(inf[m] == 0 for m in sel if m not in zero_maps)
     for m in zero_maps:
         assert not maps[m].any()
+    plan.close()
+
+
+# one-pass (shifted) form of the centered moments: the sums come from fp32
+# partial sums within a work unit, added in fp64 across units (pass 1 is exact)
+TOL_SUMS_SHIFTED = 1e-6
+
+
+def gpu_shifted(cb, plan, pilot, batches, zero_shift=False):
+    """Pilot means (cb_stats_means over ``pilot``, or no shift), the moments about
+    them in one pass over ``batches``, then cb_stats_shift_finish."""
+    n, dx, dt = plan.n_maps, plan.P - 1, plan.d_t
+    shift = torch.zeros((n, 1 + dx + dt), dtype=torch.float64, device="cuda")
+    sums = torch.empty_like(shift)
+    A = torch.empty((n, dx, dx), dtype=torch.float32, device="cuda")
+    B = torch.empty((n, dx, dt), dtype=torch.float32, device="cuda")
+    cb.cb_stats_zero_centered(plan, sums, A, B)
+    if not zero_shift:
+        for s, t, w in pilot:
+            cb.cb_stats_means(plan, s, t, w, shift)
+    for s, t, w in batches:
+        cb.cb_stats_accumulate_shifted(plan, s, t, w, shift, sums, A, B)
+    cb.cb_stats_shift_finish(plan, shift, sums, A, B)
+    torch.cuda.synchronize()
+    return sums, A, B
+
+
+@pytest.mark.parametrize("d_s,d_t", WIDTHS)
+def test_shifted_one_pass_matches_oracle_and_two_pass(cb, d_s, d_t):
+    # the workload of the two-pass ragged test; the pilot is the first sequence
+    wl = synth.Workload("cragged", 2, 3, d_s, 3, 2, d_t, 4, 45, "cyclic1", "offset", 0.1, "lognormal")
+    src, tgt, w = make_inputs(wl)
+    hm = synth.head_map(wl)
+    plan = cb.cb_plan_create(hm, src, tgt, 4096)
+    batches = seq_batches(src, tgt, w, [(0, 1), (1, 3), (3, 4)])
+    sums, A, B = gpu_shifted(cb, plan, batches[:1], batches)
+    sel = list(range(wl.n_maps))
+    so, Ao, Bo = oracle_centered_sel(hm, sel, src, tgt, w)
+    check_centered(sums, A, B, so, Ao, Bo, sel, tol_sums=TOL_SUMS_SHIFTED)
+    check_centered_maps(cb, sums, A, B, so, Ao, Bo, sel, 1e-2)
+    s2, A2, B2 = gpu_centered(cb, plan, batches)
+    ea = max(relF(A[m].double().cpu().numpy(), A2[m].double().cpu().numpy()) for m in sel)
+    eb = max(relF(B[m].double().cpu().numpy(), B2[m].double().cpu().numpy()) for m in sel)
+    say(f"  shifted vs two-pass: A {ea:.3e}, B {eb:.3e}")
+    assert ea <= TOL_STATS and eb <= TOL_STATS
+    plan.close()
+
+
+def test_shifted_large_channel_means_and_no_shift(cb):
+    # channel means 30 x their spread: a pilot of one sequence in eight removes
+    # the offsets, so the one-pass moments hold the stats bar like the two-pass
+    # ones; with no shift (zero pilot sums) the same call is the uncentered form
+    # with its cancellation, which the finishing step cannot undo
+    wl = synth.Workload("coffset", 2, 2, 128, 3, 2, 128, 8, 2048, "qwen", "offset", 0.1, "colmass")
+    src, tgt, w = make_inputs(wl)
+    hm = synth.head_map(wl)
+    plan = cb.cb_plan_create(hm, src, tgt, wl.n_seqs * wl.seq_len)
+    batches = seq_batches(src, tgt, w, [(0, 4), (4, 8)])
+    pilot = seq_batches(src, tgt, w, [(0, 1)])
+    sums, A, B = gpu_shifted(cb, plan, pilot, batches)
+    sel = list(range(wl.n_maps))
+    so, Ao, Bo = oracle_centered_sel(hm, sel, src, tgt, w)
+    es, ea, eb = check_centered(sums, A, B, so, Ao, Bo, sel, tol_sums=TOL_SUMS_SHIFTED)
+    check_centered_maps(cb, sums, A, B, so, Ao, Bo, sel, wl.lam_rel)
+    s0, A0, B0 = gpu_shifted(cb, plan, pilot, batches, zero_shift=True)
+    e0 = max(relF(A0[m].double().cpu().numpy(), Ao[m]) for m in sel)
+    say(f"  no shift: A relF {e0:.3e} (pilot shift {ea:.3e})")
+    assert ea * 10 < e0
+    plan.close()
+
+
+def test_shifted_zero_weights_empty_calls_and_determinism(cb):
+    wl = synth.Workload("czero", 2, 2, 128, 2, 2, 96, 3, 70, "qwen", "offset", 0.1, "lognormal")
+    src, tgt, w = make_inputs(wl)
+    w[1].zero_()
+    hm = synth.head_map(wl)
+    zero_maps = [m for m in range(wl.n_maps) if hm["weight_row"][m] == 1]
+    plan = cb.cb_plan_create(hm, src, tgt, 4096)
+    pilot = seq_batches(src, tgt, w, [(0, 1)])
+    s1, A1, B1 = gpu_shifted(cb, plan, pilot, [(src, tgt, w)])
+    s2, A2, B2 = gpu_shifted(cb, plan, pilot, [(src, tgt, w)])
+    assert torch.equal(s1, s2) and torch.equal(A1, A2) and torch.equal(B1, B2), "bitwise determinism"
+    shift = torch.zeros_like(s1)
+    cb.cb_stats_accumulate_shifted(plan, src[:, :, :0], tgt[:, :, :0], w[:, :0], shift, s2, A2, B2, w_row_stride=1)
+    torch.cuda.synchronize()
+    assert torch.equal(s1, s2) and torch.equal(A1, A2) and torch.equal(B1, B2), "an empty call changes nothing"
+    for m in zero_maps:
+        assert not s1[m].any() and not A1[m].any() and not B1[m].any()
+    sel = list(range(wl.n_maps))
+    so, Ao, Bo = oracle_centered_sel(hm, sel, src, tgt, w)
+    check_centered(s1, A1, B1, so, Ao, Bo, sel, tol_sums=TOL_SUMS_SHIFTED)
+    n, dx, dt = plan.n_maps, plan.P - 1, plan.d_t
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_INVALID_ARGUMENT"):
+        cb.cb_stats_accumulate_shifted(plan, src, tgt, w, s1, s1, A1, B1)
+    with pytest.raises(cb.CacheBridgeError, match="CB_ERR_INVALID_ARGUMENT"):
+        cb.cb_stats_shift_finish(plan, s1, s1, A1, B1)
     plan.close()
 
 
