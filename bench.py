@@ -431,6 +431,45 @@ def centered_leg(cb, plan, wl, src, tgt, w, n_calls, maps_plain, bytes_per_call,
     solve_ms = mean([e[2 * n_calls + 1].elapsed_time(e[2 * n_calls + 2]) for e in recs])
     build_ms = mean([e[0].elapsed_time(e[2 * n_calls + 2]) for e in recs])
     diff = (maps - maps_plain).double().norm() / maps_plain.double().norm()
+    two_pass_maps = maps.clone()
+    # the one-pass form: moments about the means of a 10-sequence pilot (one
+    # tenth of the resident batch), moved to the data's means at the end
+    T = wl.seq_len
+    n_pilot = 10
+    shift = torch.empty_like(sums)
+    precs = []
+    for it in range(steps + 1):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(n_calls + 5)]
+        e[0].record(stream)
+        cb.cb_stats_zero_centered(plan, sums, A, B)
+        cb.cb_stats_zero_centered(plan, shift, A, B)
+        e[1].record(stream)
+        cb.cb_stats_means(plan, src[:, :, :n_pilot], tgt[:, :, :n_pilot], w[:, :n_pilot * T], shift)
+        e[2].record(stream)
+        for i in range(n_calls):
+            cb.cb_stats_accumulate_shifted(plan, src, tgt, w, shift, sums, A, B)
+            e[3 + i].record(stream)
+        cb.cb_stats_shift_finish(plan, shift, sums, A, B)
+        e[3 + n_calls].record(stream)
+        cb.cb_ridge_solve_centered(sums, A, B, wl.lam_rel, cb.CB_LAMBDA_RELATIVE, maps, info)
+        e[4 + n_calls].record(stream)
+        if it > 0:
+            precs.append(e)
+    torch.cuda.synchronize()
+    p_build = mean([e[0].elapsed_time(e[4 + n_calls]) for e in precs])
+    one_pass = {
+        "s_per_500seq_build": p_build / 1e3,
+        "calib_tokens_per_s": wl.n_seqs * wl.seq_len / (p_build / 1e3),
+        "pilot": f"cb_stats_means over the first {n_pilot} sequences of the resident batch",
+        "legs_ms": {"zero": mean([e[0].elapsed_time(e[1]) for e in precs]),
+                    "pilot_means": mean([e[1].elapsed_time(e[2]) for e in precs]),
+                    "shifted_stats_call": mean([e[2 + i].elapsed_time(e[3 + i]) for e in precs for i in range(n_calls)]),
+                    "shift_finish": mean([e[2 + n_calls].elapsed_time(e[3 + n_calls]) for e in precs]),
+                    "solve": mean([e[3 + n_calls].elapsed_time(e[4 + n_calls]) for e in precs])},
+        "maps_relF_vs_two_pass": float((maps - two_pass_maps).double().norm() / two_pass_maps.double().norm()),
+        "over_uncentered_build": None,
+        "nonpositive_pivots": int((info != 0).sum().item()),
+    }
     return {
         "s_per_500seq_build": build_ms / 1e3,
         "calib_tokens_per_s": wl.n_seqs * wl.seq_len / (build_ms / 1e3),
@@ -439,6 +478,7 @@ def centered_leg(cb, plan, wl, src, tgt, w, n_calls, maps_plain, bytes_per_call,
         "centered_stats_GBps": bytes_per_call / (stats_ms / 1e3) / 1e9,
         "maps_relF_vs_uncentered_form": float(diff),
         "nonpositive_pivots": int((info != 0).sum().item()),
+        "one_pass": one_pass,
     }
 
 
@@ -716,7 +756,43 @@ def multi_leg(cb, synth, steps):
         "maps_relF_vs_unpenalized_augmented_form": float(cdiff),
         "nonpositive_pivots": cbad,
     }
-    del sums, A, Bc, cmaps, cinfo
+    # the one-pass form: moments about the means of a 10-sequence pilot, moved
+    # to the data's means at the end
+    two_pass = cmaps.clone()
+    shift = torch.empty_like(sums)
+    n_pilot = 10
+    srecs = []
+    for it in range(steps + 1):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(n_calls + 5)]
+        e[0].record(stream)
+        cb.cb_stats_zero_centered(plan, sums, A, Bc)
+        cb.cb_stats_zero_centered(plan, shift, A, Bc)
+        e[1].record(stream)
+        cb.cb_stats_means(plan, src[:, :, :n_pilot], tgt[:, :, :n_pilot], w[:, :n_pilot * wl.seq_len], shift)
+        e[2].record(stream)
+        for i in range(n_calls):
+            cb.cb_stats_accumulate_shifted(plan, src, tgt, w, shift, sums, A, Bc)
+            e[3 + i].record(stream)
+        cb.cb_stats_shift_finish(plan, shift, sums, A, Bc)
+        e[3 + n_calls].record(stream)
+        cb.cb_ridge_solve_centered_ws(sums, A, Bc, wl.lam_rel, cb.CB_LAMBDA_RELATIVE, cmaps, cinfo, ws)
+        e[4 + n_calls].record(stream)
+        if it > 0:
+            srecs.append(e)
+    torch.cuda.synchronize()
+    s_build_ms = mean([e[0].elapsed_time(e[4 + n_calls]) for e in srecs])
+    centered["one_pass"] = {
+        "s_per_500seq_build": s_build_ms / 1e3,
+        "pilot": f"cb_stats_means over the first {n_pilot} sequences of the resident batch",
+        "legs_ms": {"pilot_means": mean([e[1].elapsed_time(e[2]) for e in srecs]),
+                    "shifted_stats_call": mean([e[2 + i].elapsed_time(e[3 + i]) for e in srecs for i in range(n_calls)]),
+                    "shift_finish": mean([e[2 + n_calls].elapsed_time(e[3 + n_calls]) for e in srecs]),
+                    "solve": mean([e[3 + n_calls].elapsed_time(e[4 + n_calls]) for e in srecs])},
+        "maps_relF_vs_two_pass": max(relF(cmaps[m].double().cpu().numpy(), two_pass[m].double().cpu().numpy())
+                                     for m in (0, 511, 1023)),
+        "nonpositive_pivots": int((cinfo != 0).sum().item()),
+    }
+    del sums, A, Bc, cmaps, cinfo, shift, two_pass
     # keys with RoPE: calibration rows turned back once into a compact workspace
     # (cb_stats_accumulate_rope) against cb_rope inverse over both caches in place
     # and the plain call; the caches are turned back and forth by the timing
@@ -993,6 +1069,8 @@ def main():
         samples["C1"], samples["C2"] = sw_samples.get(50), sw_samples.get(500)
     if args.centered_steps > 0:
         res["centered"] = centered_leg(cb, plan, wl, src, tgt, w, n_calls, maps, bytes_per_call, args.centered_steps)
+        res["centered"]["one_pass"]["over_uncentered_build"] = (res["centered"]["one_pass"]["s_per_500seq_build"]
+                                                                 / res["s_per_500seq_build"])
         # diagnostic only: the weighted-means pass streams exactly the statistics call's bytes with no matrix
         # work, so its rate is the read rate this workload reaches on this board; the roofline stays 8 TB/s
         res["diagnostics"] = {

@@ -263,8 +263,9 @@ cb_status cb_stats_accumulate_centered(cb_plan *plan, const cb_cache *src, const
  * formed about the means of a pilot instead (`shift`: the sums that
  * cb_stats_means left for any subset of the data, e.g. the first few
  * sequences; zero sums mean no shift), while the same pass also sums the
- * weights, the residuals and the targets, and cb_stats_shift_finish then moves
- * the moments to the data's own means:
+ * weights, the residuals and the targets (a multi-layer plan sums the weights
+ * and targets in a second, small pass over the call's target rows alone), and
+ * cb_stats_shift_finish then moves the moments to the data's own means:
  *   shift [n_maps][1 + d_x + d_t] fp64, read: mu'_x = shift_x / shift_w, mu'_y likewise
  *   accumulate, per batch:  A[m] += sum w (x - mu'_x)(x - mu'_x)^T
  *                           B[m] += sum w (x - mu'_x)(y - mu'_y)^T
@@ -277,9 +278,10 @@ cb_status cb_stats_accumulate_centered(cb_plan *plan, const cb_cache *src, const
  * cb_ridge_solve_centered_ws.  The closer the pilot means are to the data's,
  * the smaller the correction: the pilot only has to remove the channels'
  * large common offsets.  Products, splits and fp32 sums as in
- * cb_stats_accumulate_centered; the three sums run in fp32 within a work unit
- * and in fp64 across units and calls (about 1e-7 relative), where pass 1 is
- * exact.  Zero sums, A and B before the first call (cb_stats_zero_centered);
+ * cb_stats_accumulate_centered; the sums of a single-layer plan run in fp32
+ * within a work unit and in fp64 across units and calls (about 1e-7
+ * relative; pass 1 is exact), those of a multi-layer plan in fp32 between two
+ * flushes (sum w (x - mu')) or in fp64 (sum w, sum w y).  Zero sums, A and B before the first call (cb_stats_zero_centered);
  * shift must not change between the calls of one fit and must not be sums.
  * Single- and multi-layer plans; d_x = d_s or k d_s.  Arguments, limits and
  * errors as in cb_stats_accumulate_centered, plus CB_ERR_INVALID_ARGUMENT

@@ -905,6 +905,31 @@ cb_status cb_stats_zero_centered(const cb_plan *p, double *sums, double *sq, flo
     return ok();
 }
 
+// Pass-1 arguments of a multi-layer call (tgt_only: sum w and sum w y alone).
+static cb::MeansMultiArgs means_multi_args(const cb_plan *p, const cb_cache *src, const cb::MultiArgs &ma,
+                                           double *sums, bool tgt_only) {
+    cb::MeansMultiArgs m = {};
+    m.src = ma.src;
+    m.tgt = ma.tgt;
+    m.w = ma.w;
+    m.ss = ma.ss;
+    m.ts = ma.ts;
+    m.w_row_stride = ma.w_row_stride;
+    m.n_seqs = src->n_seqs;
+    m.seq_len = src->seq_len;
+    m.stride = p->sample_stride;
+    m.rows_per_seq = (int32_t)ma.rows_per_seq;
+    m.n_maps = p->n_maps;
+    m.k = p->k;
+    m.d_t = p->d_t;
+    m.maps = p->d_amaps;
+    m.layers = p->d_alayers;
+    m.wrow = p->d_mwrow;
+    m.sums = sums;
+    m.tgt_only = tgt_only ? 1 : 0;
+    return m;
+}
+
 cb_status cb_stats_means(cb_plan *p, const cb_cache *src, const cb_cache *tgt, const float *weights,
                          int64_t w_row_stride, double *sums, double *sq, void *stream) {
     if (!p) return fail(CB_ERR_INVALID_ARGUMENT, "plan is NULL");
@@ -916,24 +941,7 @@ cb_status cb_stats_means(cb_plan *p, const cb_cache *src, const cb_cache *tgt, c
         bool empty = false;
         if (cb_status s = prepare_multi(p, src, tgt, weights, w_row_stride, ma, empty)) return s;
         if (empty) return ok();
-        cb::MeansMultiArgs m = {};
-        m.src = ma.src;
-        m.tgt = ma.tgt;
-        m.w = ma.w;
-        m.ss = ma.ss;
-        m.ts = ma.ts;
-        m.w_row_stride = ma.w_row_stride;
-        m.n_seqs = src->n_seqs;
-        m.seq_len = src->seq_len;
-        m.stride = p->sample_stride;
-        m.rows_per_seq = (int32_t)ma.rows_per_seq;
-        m.n_maps = p->n_maps;
-        m.k = p->k;
-        m.d_t = p->d_t;
-        m.maps = p->d_amaps;
-        m.layers = p->d_alayers;
-        m.wrow = p->d_mwrow;
-        m.sums = sums;
+        const cb::MeansMultiArgs m = means_multi_args(p, src, ma, sums, false);
         if (cb::launch_means_multi(m, (hipStream_t)stream) != hipSuccess)
             return fail(CB_ERR_DEVICE, "multi-layer means kernel launch failed");
         return ok();
@@ -1013,7 +1021,10 @@ cb_status cb_stats_accumulate_shifted(cb_plan *p, const cb_cache *src, const cb_
         ma.C = B;
         ma.sums = shift;
         ma.resid = sums;
-        if (cb::launch_stats_multi_centered(ma, (hipStream_t)stream) != hipSuccess)
+        // the moments and sum w (x - mu') here; sum w and sum w y from the target rows alone
+        const cb::MeansMultiArgs m = means_multi_args(p, src, ma, sums, true);
+        if (cb::launch_stats_multi_centered(ma, (hipStream_t)stream) != hipSuccess ||
+            cb::launch_means_multi(m, (hipStream_t)stream) != hipSuccess)
             return fail(CB_ERR_DEVICE, "multi-layer centered statistics kernel launch failed");
         return ok();
     }

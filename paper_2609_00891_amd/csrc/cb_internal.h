@@ -193,6 +193,7 @@ struct MeansMultiArgs {
     const int32_t *layers;    // [n_maps][k]
     const int32_t *wrow;      // [n_maps]
     double *sums;             // [n_maps][1 + 128 k + d_t], added to
+    int32_t tgt_only;         // 1: only sum w and sum w y (the target block)
 };
 
 struct ApplyMultiArgs {

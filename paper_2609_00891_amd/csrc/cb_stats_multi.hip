@@ -239,9 +239,9 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
     for (int e = 0; e < E; ++e)
         coff[e] = (uint32_t)tk.col_slot[e >> 2] * K::BLK + lrow + 64u * ((uint32_t)(e & 3) ^ (uint32_t)kk);
     const uint32_t lw = K::OFF_W + (lane >> 5) * 32;
-    const bool own_x = (tk.flags >> rs) & 1, own_w = (tk.flags & 4) && wave == 0;
+    const bool own_x = (tk.flags >> rs) & 1;
     const bool own_sumx = !CENTER && own_x;
-    const bool own_sumw = !CENTER && own_w;
+    const bool own_sumw = !CENTER && (tk.flags & 4) && wave == 0;
     // centered: the weighted means of the map (fp64 sums of pass 1)
     const double *sm = CENTER ? a.sums + (int64_t)tk.map * (a.P + a.d_t) : nullptr;
     const double s_w = CENTER ? sm[0] : 0.0;
@@ -316,7 +316,8 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
         f.lo[r] = __builtin_bit_cast(bf16x8_t, make_uint4(lv[0], lv[1], lv[2], lv[3]));
     };
     auto sum_w = [&](const Ops &o) {
-        sumw += ((o.w[0] + o.w[1]) + (o.w[2] + o.w[3])) + ((o.w[4] + o.w[5]) + (o.w[6] + o.w[7]));
+        if constexpr (!CENTER)
+            sumw += ((o.w[0] + o.w[1]) + (o.w[2] + o.w[3])) + ((o.w[4] + o.w[5]) + (o.w[6] + o.w[7]));
     };
     auto sum_y = [&](const Ops &o) {
         // entry 4 + wave: selected with a uniform switch-free blend of the four candidates
@@ -401,27 +402,17 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
             }
         }
         if constexpr (CENTER) {
-            if (a.resid) {
-                // shifted form: the rows' (sum w, sum w (x - mu), sum w y), one owner per entry
+            if (a.resid && own_x) {
+                // shifted form: sum w (x - mu) of the rows, one owner per entry (sum w
+                // and sum w y come from the target-block pass of the same call)
                 double *rsum = a.resid + (int64_t)tk.map * (a.P + a.d_t);
-                if (own_x) {
 #pragma unroll
-                    for (int r = 0; r < 2; ++r) {
-                        const float ex = sumx[r] + __shfl_xor(sumx[r], 32);
-                        if (lane < 32) rsum[1 + 128 * rb + 64 * half + 32 * r + lane] += (double)ex;
-                    }
-                }
-                if (YS) {
-                    const float sy = sumy + __shfl_xor(sumy, 32);
-                    if (lane < 32) rsum[a.P + 32 * wave + lane] += (double)sy;
-                }
-                if (own_w) {
-                    const float sw = sumw + __shfl_xor(sumw, 32);
-                    if (lane == 0) rsum[0] += (double)sw;
+                for (int r = 0; r < 2; ++r) {
+                    const float ex = sumx[r] + __shfl_xor(sumx[r], 32);
+                    if (lane < 32) rsum[1 + 128 * rb + 64 * half + 32 * r + lane] += (double)ex;
                 }
             }
             sumx[0] = sumx[1] = 0.f;
-            sumy = sumw = 0.f;
             zero_acc();
             return;
         }
@@ -569,13 +560,13 @@ void stats_multi_kernel(MultiArgs a) {
     }
     // variant: staged blocks (1..4), target block staged (HASY), sum w y owned (YS)
     const bool hasy = tk.slot_layer[tk.n_lds - 1] < 0;
-    const int var = (tk.n_lds - 1) * 3 + (hasy ? (((!CENTER || a.resid) && (tk.flags & 8)) ? 2 : 1) : 0);
+    const int var = (tk.n_lds - 1) * 3 + (hasy ? ((!CENTER && (tk.flags & 8)) ? 2 : 1) : 0);
     switch (var) {
 #define CB_V(NL_)                                                                                  \
         case (NL_ - 1) * 3 + 0: multi_wave<NL_, false, false, CENTER>(a, tk, c, lds, wave, lane); break; \
         case (NL_ - 1) * 3 + 1: multi_wave<NL_, true, false, CENTER>(a, tk, c, lds, wave, lane); break;  \
         case (NL_ - 1) * 3 + 2:                                                                     \
-            multi_wave<NL_, true, true, CENTER>(a, tk, c, lds, wave, lane);                         \
+            if constexpr (!CENTER) multi_wave<NL_, true, true, false>(a, tk, c, lds, wave, lane);    \
             break;
         CB_V(1) CB_V(2) CB_V(3) CB_V(4)
 #undef CB_V
@@ -589,7 +580,8 @@ void stats_multi_kernel(MultiArgs a) {
 // fixed-order sum over the 16 row groups through LDS, added into sums.
 __global__ __launch_bounds__(256) void means_multi_kernel(MeansMultiArgs a) {
     __shared__ double red[16][16][9];
-    const int m = blockIdx.x / (a.k + 1), blk = blockIdx.x % (a.k + 1);
+    // tgt_only: one workgroup per map, its target block (sum w, sum w y)
+    const int m = a.tgt_only ? blockIdx.x : blockIdx.x / (a.k + 1), blk = a.tgt_only ? a.k : blockIdx.x % (a.k + 1);
     const int tid = threadIdx.x, ch = tid & 15, rg = tid >> 4;
     const ApplyMultiMap mp = a.maps[m];
     const bool tgt = blk == a.k;
@@ -646,7 +638,7 @@ hipError_t launch_stats_multi_centered(const MultiArgs &a, hipStream_t s) {
 
 hipError_t launch_means_multi(const MeansMultiArgs &a, hipStream_t s) {
     if (a.n_maps == 0 || a.n_seqs == 0 || a.rows_per_seq == 0) return hipSuccess;
-    hipLaunchKernelGGL(means_multi_kernel, dim3((unsigned)(a.n_maps * (a.k + 1))), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(means_multi_kernel, dim3((unsigned)(a.n_maps * (a.tgt_only ? 1 : a.k + 1))), dim3(256), 0, s, a);
     return hipGetLastError();
 }
 
