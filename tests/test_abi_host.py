@@ -99,6 +99,8 @@ def test_centered_entry_points_reject_bad_arguments_on_the_host():
     assert lib.cb_stats_zero_centered(None, None, None, None, None, None) == 1
     assert lib.cb_stats_means(None, None, None, None, 0, None, None, None) == 1
     assert lib.cb_stats_accumulate_centered(None, None, None, None, 0, None, None, None, None) == 1
+    assert lib.cb_stats_accumulate_shifted(None, None, None, None, 0, None, None, None, None, None) == 1
+    assert lib.cb_stats_shift_finish(None, None, None, None, None, None) == 1
     f = ctypes.c_float
     solve = lib.cb_ridge_solve_centered
     assert solve(4, 80, 128, None, None, None, f(0.1), 0, None, None, None) == 6      # d_s not supported
@@ -293,6 +295,10 @@ def test_bindings_check_output_sizes_against_the_plan():
         cb.cb_stats_zero_centered(plan, z64(4, 257), z32(4, 384, 384), z32(4, 384, 128))
     with pytest.raises(ValueError, match="A"):
         cb.cb_stats_zero_centered(plan, z64(4, 513), z32(4, 128, 128), z32(4, 384, 128))
+    with pytest.raises(ValueError, match="sums"):                 # the pilot sums are sized like sums
+        cb.cb_stats_shift_finish(plan, z64(4, 257), z64(4, 513), z32(4, 384, 384), z32(4, 384, 128))
+    with pytest.raises(ValueError, match="B"):
+        cb.cb_stats_shift_finish(plan, z64(4, 513), z64(4, 513), z32(4, 384, 384), z32(4, 128, 128))
     with pytest.raises(ValueError, match="G"):
         cb.cb_stats_zero(plan, z32(4, 129, 129), z32(4, 385, 128))
     with pytest.raises(ValueError, match="maps"):
