@@ -60,6 +60,15 @@ constexpr int LQ = NB * KS / NT, ZQ = KS * DTMAX / NT;   // operand elements per
 static_assert(LQ * NT == NB * KS && ZQ * NT == KS * DTMAX, "substitution chunks split evenly over the threads");
 constexpr int SH_WORK = std::max(OFF_B + 2 * NB * KP, OFF_R + NB * ZP);
 
+typedef __attribute__((ext_vector_type(4))) double f64x4_t;
+
+// fp64 matrix-core product D += A B of a 16 x 4 by 4 x 16 block: lane l
+// supplies A[l % 16][l / 16] and B[l / 16][l % 16] and holds D[l / 16 + 4 i][l % 16]
+// in element i.
+__device__ __forceinline__ f64x4_t mfma_f64(double a, double b, f64x4_t c) {
+    return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+}
+
 __device__ __forceinline__ void wave_sync_lds() {
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     __builtin_amdgcn_wave_barrier();
@@ -71,7 +80,7 @@ __device__ __forceinline__ void wave_sync_lds() {
 // gets lambda_m, lambda_m = lambda (tr A + S |mu_x|^2 + S) / (P + 1) when
 // relative (the trace of the augmented matrix of the same data), and each map
 // gets P + 1 rows: W, then the bias b = mu_y - W^T mu_x.
-__global__ __launch_bounds__(NT) void chol_solve_kernel(int32_t P, int32_t d_t, const float *__restrict__ G,
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2))) void chol_solve_kernel(int32_t P, int32_t d_t, const float *__restrict__ G,
                                                         const float *__restrict__ C, float lambda, uint32_t flags,
                                                         double *__restrict__ ws, int64_t ws_stride, int32_t m0,
                                                         float *__restrict__ maps, int32_t *__restrict__ info,
@@ -127,7 +136,6 @@ __global__ __launch_bounds__(NT) void chol_solve_kernel(int32_t P, int32_t d_t, 
 
     // ================= 1. blocked Cholesky
     double *sA = sh + OFF_A, *sB = sh + OFF_B;
-    const int cg = tid & 7, rg = tid >> 3;             // GEMM: columns 4cg..4cg+3, rows rg + 32 i
     for (int c0 = 0; c0 < P; c0 += NB) {
         const int nb = min(NB, P - c0);
         const int nch = c0 / KC;                        // c0 is a multiple of 32
@@ -136,11 +144,13 @@ __global__ __launch_bounds__(NT) void chol_solve_kernel(int32_t P, int32_t d_t, 
         // spent on rows past P
         auto gemm_pass = [&](auto NIc, int rt) {
             constexpr int NI = decltype(NIc)::value;
-            double acc[NI][4];
+            constexpr int NRT = 2 * NI;                 // 16-row tiles of the pass
+            constexpr int MAXT = (NRT + 3) / 4;         // tiles of one wave (wave w: w, w + 4, ...)
+            f64x4_t acc[MAXT][2];
 #pragma unroll
-            for (int i = 0; i < NI; ++i)
+            for (int j = 0; j < MAXT; ++j)
 #pragma unroll
-                for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
+                for (int ct = 0; ct < 2; ++ct) acc[j][ct] = f64x4_t{0.0, 0.0, 0.0, 0.0};
             double pa[2 * NI], pb[2];
             auto fetch = [&](int ch) {                  // chunk ch of L[rt:rt+32NI, :] and L[c0:c0+32, :]
                 const int k0 = ch * KC, kk = tid & 15;
@@ -162,36 +172,45 @@ __global__ __launch_bounds__(NT) void chol_solve_kernel(int32_t P, int32_t d_t, 
 #pragma unroll
                 for (int q = 0; q < 2; ++q) sB[buf * NB * KP + ((tid >> 4) + 16 * q) * KP + kk] = pb[q];
             };
+            const int lr = lane & 15, lk = lane >> 4;   // fragment row / column, inner index
             if (nch > 0) fetch(0);
             for (int ch = 0; ch < nch; ++ch) {
                 stash(ch & 1);
                 __syncthreads();
                 if (ch + 1 < nch) fetch(ch + 1);
                 const double *a = sA + (ch & 1) * TR * KP, *b = sB + (ch & 1) * NB * KP;
-#pragma unroll 4
-                for (int kk = 0; kk < KC; ++kk) {
-                    double av[NI], bv[4];
 #pragma unroll
-                    for (int i = 0; i < NI; ++i) av[i] = a[(rg + 32 * i) * KP + kk];
+                for (int s4 = 0; s4 < KC / 4; ++s4) {
+                    const int kk = 4 * s4 + lk;
+                    const double b0 = b[lr * KP + kk], b1 = b[(16 + lr) * KP + kk];
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) bv[j] = b[(4 * cg + j) * KP + kk];
-#pragma unroll
-                    for (int i = 0; i < NI; ++i)
-#pragma unroll
-                        for (int j = 0; j < 4; ++j) acc[i][j] = fma(av[i], bv[j], acc[i][j]);
+                    for (int j = 0; j < MAXT; ++j) {
+                        const int t = wave + 4 * j;
+                        if (t < NRT) {
+                            const double av = a[(16 * t + lr) * KP + kk];
+                            acc[j][0] = mfma_f64(av, b0, acc[j][0]);
+                            acc[j][1] = mfma_f64(av, b1, acc[j][1]);
+                        }
+                    }
                 }
             }
 #pragma unroll
-            for (int i = 0; i < NI; ++i) {
-                const int r = rt + rg + 32 * i;
-                if (r >= P) continue;
+            for (int j = 0; j < MAXT; ++j) {
+                const int t = wave + 4 * j;
+                if (t >= NRT) continue;
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int c = c0 + 4 * cg + j;
-                    if (4 * cg + j >= nb) continue;
-                    double v = (double)Gm[(int64_t)r * P + c];
-                    if (r == c && c < lam_last) v += lam;
-                    L[(int64_t)r * P + c] = v - acc[i][j];
+                for (int ct = 0; ct < 2; ++ct) {
+                    const int cc = 16 * ct + lr;
+                    if (cc >= nb) continue;
+                    const int c = c0 + cc;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int r = rt + 16 * t + lk + 4 * i;
+                        if (r >= P) continue;
+                        double v = (double)Gm[(int64_t)r * P + c];
+                        if (r == c && c < lam_last) v += lam;
+                        L[(int64_t)r * P + c] = v - acc[j][ct][i];
+                    }
                 }
             }
             __syncthreads();
@@ -286,14 +305,20 @@ __global__ __launch_bounds__(NT) void chol_solve_kernel(int32_t P, int32_t d_t, 
 
     // ================= 2., 3. substitutions (Z then W~ in Z)
     double *sL = sh + OFF_L, *sZ = sh + OFF_Z, *sR = sh + OFF_R;
-    const int ri = tid >> 5, cj = tid & 31;            // GEMM: rows ri + 8 q, columns cj + 32 n
-    // acc[q][n] = sum over k in [k_lo, k_hi) of Lop(i, k) Z[k][c], i = ri + 8 q, c = cj + 32 n, where
+    const int ri = tid >> 5, cj = tid & 31;            // apply_inv: rows ri + 8 q, columns cj + 32 n
+    // The panel products on the matrix cores: wave w owns columns 32 w .. 32 w + 31
+    // (two 16-column tiles) of both 16-row tiles; element e of acc[rt][ct] is
+    // row 16 rt + lane / 16 + 4 e, column 32 w + 16 ct + lane % 16.
+    const int lr = lane & 15, lk = lane >> 4;
+    auto out_row = [&](int rt, int e) { return 16 * rt + lk + 4 * e; };
+    auto out_col = [&](int ct) { return 32 * wave + 16 * ct + lr; };
+    // acc = sum over k in [k_lo, k_hi) of Lop(i, k) Z[k][c], where
     // Lop(i, k) = L[c0 + i][k] (forward) or L[k][c0 + i] (backward).
-    auto panel_gemm = [&](double (&acc)[4][4], int c0, int nb, int k_lo, int k_hi, bool backward) {
+    auto panel_gemm = [&](f64x4_t (&acc)[2][2], int c0, int nb, int k_lo, int k_hi, bool backward) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
+        for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
-            for (int n = 0; n < 4; ++n) acc[q][n] = 0.0;
+            for (int ct = 0; ct < 2; ++ct) acc[rt][ct] = f64x4_t{0.0, 0.0, 0.0, 0.0};
         const int nch = (k_hi - k_lo + KS - 1) / KS;
         double pl[LQ], pz[ZQ];
         auto fetch = [&](int ch) {
@@ -335,17 +360,15 @@ __global__ __launch_bounds__(NT) void chol_solve_kernel(int32_t P, int32_t d_t, 
             __syncthreads();
             if (ch + 1 < nch) fetch(ch + 1);
             const double *a = sL + (ch & 1) * NB * KSP, *b = sZ + (ch & 1) * KS * ZP;
-#pragma unroll 4
-            for (int kk = 0; kk < KS; ++kk) {
-                double av[4], bv[4];
 #pragma unroll
-                for (int q = 0; q < 4; ++q) av[q] = a[(ri + 8 * q) * KSP + kk];
-#pragma unroll
-                for (int n = 0; n < 4; ++n) bv[n] = b[kk * ZP + cj + 32 * n];
-#pragma unroll
-                for (int q = 0; q < 4; ++q)
-#pragma unroll
-                    for (int n = 0; n < 4; ++n) acc[q][n] = fma(av[q], bv[n], acc[q][n]);
+            for (int s4 = 0; s4 < KS / 4; ++s4) {
+                const int kk = 4 * s4 + lk;
+                const double a0 = a[lr * KSP + kk], a1 = a[(16 + lr) * KSP + kk];
+                const double b0 = b[kk * ZP + out_col(0)], b1 = b[kk * ZP + out_col(1)];
+                acc[0][0] = mfma_f64(a0, b0, acc[0][0]);
+                acc[0][1] = mfma_f64(a0, b1, acc[0][1]);
+                acc[1][0] = mfma_f64(a1, b0, acc[1][0]);
+                acc[1][1] = mfma_f64(a1, b1, acc[1][1]);
             }
         }
     };
@@ -382,15 +405,17 @@ __global__ __launch_bounds__(NT) void chol_solve_kernel(int32_t P, int32_t d_t, 
     // forward: Z[c0:c1] = L_dd^-1 (C[c0:c1] - L[c0:c1, :c0] Z[:c0])
     for (int c0 = 0; c0 < P; c0 += NB) {
         const int nb = min(NB, P - c0);
-        double acc[4][4];
+        f64x4_t acc[2][2];
         panel_gemm(acc, c0, nb, 0, c0, false);
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
+        for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
-            for (int n = 0; n < 4; ++n) {
-                const int i = ri + 8 * q, c = cj + 32 * n;
-                sR[i * ZP + c] = (i < nb && c < d_t) ? (double)Cm[(int64_t)(c0 + i) * d_t + c] - acc[q][n] : 0.0;
-            }
+            for (int ct = 0; ct < 2; ++ct)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int i = out_row(rt, e), c = out_col(ct);
+                    sR[i * ZP + c] = (i < nb && c < d_t) ? (double)Cm[(int64_t)(c0 + i) * d_t + c] - acc[rt][ct][e] : 0.0;
+                }
         load_inv(c0, nb);
         __syncthreads();
         apply_inv(c0, nb, false);
@@ -400,15 +425,17 @@ __global__ __launch_bounds__(NT) void chol_solve_kernel(int32_t P, int32_t d_t, 
     const int last = ((P - 1) / NB) * NB;
     for (int c0 = last; c0 >= 0; c0 -= NB) {
         const int nb = min(NB, P - c0), c1 = c0 + nb;
-        double acc[4][4];
+        f64x4_t acc[2][2];
         panel_gemm(acc, c0, nb, c1, P, true);
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
+        for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
-            for (int n = 0; n < 4; ++n) {
-                const int i = ri + 8 * q, c = cj + 32 * n;
-                sR[i * ZP + c] = (i < nb && c < d_t) ? Z[(int64_t)(c0 + i) * d_t + c] - acc[q][n] : 0.0;
-            }
+            for (int ct = 0; ct < 2; ++ct)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int i = out_row(rt, e), c = out_col(ct);
+                    sR[i * ZP + c] = (i < nb && c < d_t) ? Z[(int64_t)(c0 + i) * d_t + c] - acc[rt][ct][e] : 0.0;
+                }
         load_inv(c0, nb);
         __syncthreads();
         apply_inv(c0, nb, true);
