@@ -69,6 +69,13 @@ __device__ __forceinline__ f64x4_t mfma_f64(double a, double b, f64x4_t c) {
     return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
 }
 
+// Lane l's value of v, read by every lane (l uniform).
+__device__ __forceinline__ double readlane_f64(double v, int l) {
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)u, l), hi = __builtin_amdgcn_readlane((uint32_t)(u >> 32), l);
+    return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
 __device__ __forceinline__ void wave_sync_lds() {
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     __builtin_amdgcn_wave_barrier();
@@ -225,50 +232,66 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2))) void
                 default: gemm_pass(std::integral_constant<int, TR / 32>(), rt); break;
             }
         }
-        // factor the diagonal block: one wave, right-looking, in LDS
+        // Factor the diagonal block and invert it: one wave, in registers.  Lane
+        // i (and its mirror i + 32) holds row i of the block in a[] and, after
+        // the factorization, row i of V = L_dd^-1 in v[]; the entries of other
+        // rows that a step needs arrive by readlane.  Right-looking: step j
+        // scales column j and subtracts its outer product from the columns to
+        // its right.  (Entries right of the diagonal collect junk that no step
+        // reads; they are dropped when the rows are stored.)
         if (wave == 0) {
-            for (int e = lane; e < NB * NB; e += 64) {
-                const int i = e / NB, j = e % NB;
-                sD[i * DP + j] = (i < nb && j <= i) ? L[(int64_t)(c0 + i) * P + c0 + j] : 0.0;
-            }
-            wave_sync_lds();
+            const int i = lane & 31;
+            double a[NB];
+#pragma unroll
+            for (int c = 0; c < NB; ++c) a[c] = (i < nb && c <= i) ? L[(int64_t)(c0 + i) * P + c0 + c] : 0.0;
             int bad = 0;
-            for (int j = 0; j < nb; ++j) {
-                const double d = sD[j * DP + j];
-                if (!(d > 0.0) || !isfinite(d)) {
-                    bad = c0 + j + 1;
-                    break;
+            double dinv = 0.0;                          // 1 / L[i][i]
+#pragma unroll
+            for (int j = 0; j < NB; ++j) {
+                // (no break: a fixed trip count keeps the loop unrolled and a[] in registers)
+                if (j < nb && !bad) {
+                    const double d = readlane_f64(a[j], j);
+                    if (!(d > 0.0) || !isfinite(d)) {
+                        bad = c0 + j + 1;
+                    } else {
+                        const double sq = sqrt(d), inv = 1.0 / sq;
+                        if (i == j) dinv = inv;
+                        a[j] = i > j ? a[j] * inv : (i == j ? sq : 0.0);
+#pragma unroll
+                        for (int l = j + 1; l < NB; ++l) a[l] = fma(-a[j], readlane_f64(a[j], l), a[l]);
+                    }
                 }
-                const double s = sqrt(d), inv = 1.0 / s;
-                wave_sync_lds();
-                if (lane == 0) {
-                    sD[j * DP + j] = s;
-                    sInv[j] = inv;
-                }
-                if (lane > j && lane < nb) sD[lane * DP + j] *= inv;
-                wave_sync_lds();
-                for (int e = lane; e < NB * NB; e += 64) {
-                    const int i = e / NB, l = e % NB;
-                    if (i > j && l > j && l <= i && i < nb) sD[i * DP + l] -= sD[i * DP + j] * sD[l * DP + j];
-                }
-                wave_sync_lds();
             }
             if (lane == 0) s_bad = bad;
             if (!bad) {
-                // V = L_dd^-1 by forward elimination on the identity, one row of V per step
-                for (int e = lane; e < NB * NB; e += 64) {
-                    const int i = e / NB, c = e % NB;
-                    sV[i * DP + c] = i == c ? 1.0 : 0.0;
+                if (lane < NB) {
+#pragma unroll
+                    for (int c = 0; c < NB; ++c) sD[i * DP + c] = (i < nb && c < nb && c <= i) ? a[c] : 0.0;
+                    sInv[i] = i < nb ? dinv : 0.0;
                 }
                 wave_sync_lds();
-                for (int j = 0; j < nb; ++j) {
-                    if (lane < NB) sV[j * DP + lane] *= sInv[j];
-                    wave_sync_lds();
-                    for (int e = lane; e < (nb - 1 - j) * NB; e += 64) {
-                        const int i = j + 1 + e / NB, c = e % NB;
-                        sV[i * DP + c] -= sD[i * DP + j] * sV[j * DP + c];
+                // V = L_dd^-1 by forward elimination on the identity: step j
+                // scales row j by 1 / L[j][j] and removes L[i][j] times it from
+                // the rows i > j (L[i][j] read back from LDS, so only v[] stays
+                // in registers)
+                double v[NB];
+#pragma unroll
+                for (int c = 0; c < NB; ++c) v[c] = i == c ? 1.0 : 0.0;
+#pragma unroll
+                for (int j = 0; j < NB; ++j) {
+                    if (j < nb) {
+                        const double m = i > j ? sD[i * DP + j] : 0.0;
+                        const double sj = i == j ? sInv[i] : 1.0;
+#pragma unroll
+                        for (int c = 0; c <= j; ++c) {
+                            v[c] *= sj;
+                            v[c] = fma(-m, readlane_f64(v[c], j), v[c]);
+                        }
                     }
-                    wave_sync_lds();
+                }
+                if (lane < NB) {
+#pragma unroll
+                    for (int c = 0; c < NB; ++c) sV[i * DP + c] = (i < nb && c < nb && c <= i) ? v[c] : 0.0;
                 }
             }
         }
