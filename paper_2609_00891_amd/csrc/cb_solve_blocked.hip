@@ -45,6 +45,7 @@ static_assert(TR == 6 * 32, "the pass dispatch below covers 1 .. 6 groups of 32 
 constexpr int KS = 8;           // inner-dimension chunk of the substitutions
 constexpr int KSP = KS + 1;
 constexpr int DP = NB + 1;      // padded row of the diagonal block
+constexpr int RP = NB + 1;      // padded row of a pass's M - acc (solved rows below the diagonal block)
 constexpr int DTMAX = 128;
 constexpr int ZP = DTMAX + 1;   // padded row of a right-hand-side chunk
 
@@ -149,8 +150,12 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2))) void
         // rows c0 .. P-1 in passes of up to TR rows; a pass of NI 32-row groups
         // (the last one may be shorter) is compiled for its NI so that no FMA is
         // spent on rows past P
-        auto gemm_pass = [&](auto NIc, int rt) {
+        // SOLVE: rows below the diagonal block, whose panel entries are
+        // x = (M - acc) L_dd^-T = (M - acc) V^T: the pass puts M - acc in LDS
+        // and multiplies it by V^T on the matrix cores before storing it.
+        auto gemm_pass = [&](auto NIc, auto SOLVEc, int rt) {
             constexpr int NI = decltype(NIc)::value;
+            constexpr bool SOLVE = decltype(SOLVEc)::value;
             constexpr int NRT = 2 * NI;                 // 16-row tiles of the pass
             constexpr int MAXT = (NRT + 3) / 4;         // tiles of one wave (wave w: w, w + 4, ...)
             f64x4_t acc[MAXT][2];
@@ -201,37 +206,70 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2))) void
                     }
                 }
             }
+            if constexpr (SOLVE) {
+                // R = M - acc of this wave's rows, [16 t + row][RP] over the chunk buffers
+                __syncthreads();                        // every wave is done with the chunks
 #pragma unroll
-            for (int j = 0; j < MAXT; ++j) {
-                const int t = wave + 4 * j;
-                if (t >= NRT) continue;
+                for (int j = 0; j < MAXT; ++j) {
+                    const int t = wave + 4 * j;
+                    if (t >= NRT) continue;
 #pragma unroll
-                for (int ct = 0; ct < 2; ++ct) {
-                    const int cc = 16 * ct + lr;
-                    if (cc >= nb) continue;
-                    const int c = c0 + cc;
+                    for (int ct = 0; ct < 2; ++ct) {
+                        const int cc = 16 * ct + lr;
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const int rl = 16 * t + lk + 4 * i, r = rt + rl;
+                            const double g = (r < P && cc < nb) ? (double)Gm[(int64_t)r * P + c0 + cc] : 0.0;
+                            sA[rl * RP + cc] = (r < P && cc < nb) ? g - acc[j][ct][i] : 0.0;
+                        }
+                    }
+                }
+                wave_sync_lds();                        // a wave reads back only its own rows
+#pragma unroll
+                for (int j = 0; j < MAXT; ++j) {
+                    const int t = wave + 4 * j;
+                    if (t >= NRT) continue;
+                    f64x4_t x0 = {0.0, 0.0, 0.0, 0.0}, x1 = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+                    for (int s4 = 0; s4 < NB / 4; ++s4) {
+                        const int kk = 4 * s4 + lk;
+                        const double av = sA[(16 * t + lr) * RP + kk];
+                        x0 = mfma_f64(av, sV[lr * DP + kk], x0);            // V^T[k][c] = V[c][k]
+                        x1 = mfma_f64(av, sV[(16 + lr) * DP + kk], x1);
+                    }
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
                         const int r = rt + 16 * t + lk + 4 * i;
                         if (r >= P) continue;
-                        double v = (double)Gm[(int64_t)r * P + c];
-                        if (r == c && c < lam_last) v += lam;
-                        L[(int64_t)r * P + c] = v - acc[j][ct][i];
+                        if (lr < nb) L[(int64_t)r * P + c0 + lr] = x0[i];
+                        if (16 + lr < nb) L[(int64_t)r * P + c0 + 16 + lr] = x1[i];
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int j = 0; j < MAXT; ++j) {
+                    const int t = wave + 4 * j;
+                    if (t >= NRT) continue;
+#pragma unroll
+                    for (int ct = 0; ct < 2; ++ct) {
+                        const int cc = 16 * ct + lr;
+                        if (cc >= nb) continue;
+                        const int c = c0 + cc;
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const int r = rt + 16 * t + lk + 4 * i;
+                            if (r >= P) continue;
+                            double v = (double)Gm[(int64_t)r * P + c];
+                            if (r == c && c < lam_last) v += lam;
+                            L[(int64_t)r * P + c] = v - acc[j][ct][i];
+                        }
                     }
                 }
             }
             __syncthreads();
         };
-        for (int rt = c0; rt < P; rt += TR) {
-            switch (min((P - rt + 31) / 32, TR / 32)) {
-                case 1: gemm_pass(std::integral_constant<int, 1>(), rt); break;
-                case 2: gemm_pass(std::integral_constant<int, 2>(), rt); break;
-                case 3: gemm_pass(std::integral_constant<int, 3>(), rt); break;
-                case 4: gemm_pass(std::integral_constant<int, 4>(), rt); break;
-                case 5: gemm_pass(std::integral_constant<int, 5>(), rt); break;
-                default: gemm_pass(std::integral_constant<int, TR / 32>(), rt); break;
-            }
-        }
+        // the diagonal block's rows first: it is factored before the rows below
+        gemm_pass(std::integral_constant<int, 1>(), std::false_type(), c0);
         // Factor the diagonal block and invert it: one wave, in registers.  Lane
         // i (and its mirror i + 32) holds row i of the block in a[] and, after
         // the factorization, row i of V = L_dd^-1 in v[]; the entries of other
@@ -302,23 +340,17 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2))) void
             if (i < nb && j <= i) L[(int64_t)(c0 + i) * P + c0 + j] = sD[i * DP + j];
             if (i < nb && j < i) L[(int64_t)(c0 + j) * P + c0 + i] = sV[i * DP + j];   // V, transposed, above
         }
-        // rows below: x L_dd^T = panel row, column by column
-        for (int r = c0 + NB + tid; r < P; r += NT) {
-            const double *dd = sD, *iv = sInv;          // opaque: one base register, immediate offsets
-            asm volatile("" : "+v"(dd), "+v"(iv));
-            double x[NB];
-#pragma unroll
-            for (int j = 0; j < NB; ++j) x[j] = L[(int64_t)r * P + c0 + j];
-#pragma unroll
-            for (int j = 0; j < NB; ++j) {
-                x[j] *= iv[j];
-#pragma unroll
-                for (int i = j + 1; i < NB; ++i) x[i] = fma(-x[j], dd[i * DP + j], x[i]);
+        // rows below, solved against the diagonal block inside their passes
+        for (int rt = c0 + NB; rt < P; rt += TR) {
+            switch (min((P - rt + 31) / 32, TR / 32)) {
+                case 1: gemm_pass(std::integral_constant<int, 1>(), std::true_type(), rt); break;
+                case 2: gemm_pass(std::integral_constant<int, 2>(), std::true_type(), rt); break;
+                case 3: gemm_pass(std::integral_constant<int, 3>(), std::true_type(), rt); break;
+                case 4: gemm_pass(std::integral_constant<int, 4>(), std::true_type(), rt); break;
+                case 5: gemm_pass(std::integral_constant<int, 5>(), std::true_type(), rt); break;
+                default: gemm_pass(std::integral_constant<int, TR / 32>(), std::true_type(), rt); break;
             }
-#pragma unroll
-            for (int j = 0; j < NB; ++j) L[(int64_t)r * P + c0 + j] = x[j];
         }
-        __syncthreads();
     }
     if (s_bad) {
         if (tid == 0) info[m] = s_bad;
