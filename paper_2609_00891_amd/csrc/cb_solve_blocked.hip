@@ -42,7 +42,7 @@ constexpr int KC = 16;          // inner-dimension chunk
 constexpr int KP = KC + 1;      // padded LDS row of a chunk (doubles)
 constexpr int TR = 192;         // rows per GEMM pass of the factorization
 static_assert(TR == 6 * 32, "the pass dispatch below covers 1 .. 6 groups of 32 rows");
-constexpr int KS = 8;           // inner-dimension chunk of the substitutions
+constexpr int KS = 16;          // inner-dimension chunk of the substitutions
 constexpr int KSP = KS + 1;
 constexpr int DP = NB + 1;      // padded row of the diagonal block
 constexpr int RP = NB + 1;      // padded row of a pass's M - acc (solved rows below the diagonal block)
@@ -50,16 +50,17 @@ constexpr int DTMAX = 128;
 constexpr int ZP = DTMAX + 1;   // padded row of a right-hand-side chunk
 
 // LDS (doubles): factorization: A chunks [2][TR][KP], B chunks [2][NB][KP];
-// substitutions: L chunks [2][NB][KSP], Z chunks [2][KS][ZP], panel rhs [NB][ZP].
+// substitutions: L chunks [2][NB][KSP], Z chunks [2][KS][ZP]; the panel rhs [NB][ZP] reuses the chunks'
+// space once a panel's products are done.
 // About 78 KB in all, so two systems share a compute unit.
 constexpr int OFF_A = 0;
 constexpr int OFF_B = OFF_A + 2 * TR * KP;
 constexpr int OFF_L = 0;
 constexpr int OFF_Z = OFF_L + 2 * NB * KSP;
-constexpr int OFF_R = OFF_Z + 2 * KS * ZP;
+constexpr int OFF_R = 0;
 constexpr int LQ = NB * KS / NT, ZQ = KS * DTMAX / NT;   // operand elements per thread and chunk
 static_assert(LQ * NT == NB * KS && ZQ * NT == KS * DTMAX, "substitution chunks split evenly over the threads");
-constexpr int SH_WORK = std::max(OFF_B + 2 * NB * KP, OFF_R + NB * ZP);
+constexpr int SH_WORK = std::max(OFF_B + 2 * NB * KP, std::max(OFF_Z + 2 * KS * ZP, OFF_R + NB * ZP));
 
 typedef __attribute__((ext_vector_type(4))) double f64x4_t;
 
@@ -426,6 +427,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(2, 2))) void
                 acc[1][1] = mfma_f64(a1, b1, acc[1][1]);
             }
         }
+        __syncthreads();                                // the chunks' space becomes the panel rhs
     };
 
     // Z[c0 + i][c] = sum_k V[i][k] R[k][c]  (forward, V = L_dd^-1), or
