@@ -7,18 +7,20 @@
 //
 //   M = G + lambda_m D  (lambda_m = lambda, or lambda tr(G) / P; D = I, or
 //                        diag(1, .., 1, 0) with CB_RIDGE_BIAS_UNPENALIZED)
-//   1. left-looking blocked Cholesky M = L L^T in panels of 32 columns:
-//      panel = M[c0:, c0:c0+32] - L[c0:, :c0] L[c0:c0+32, :c0]^T as a
-//      register-blocked GEMM (up to 6 x 4 outputs per thread, 16-wide chunks of the
-//      inner dimension double-buffered through LDS so the next chunk's global
-//      loads overlap this chunk's FMAs); the 32 x 32 diagonal block factored
-//      by one wave in LDS, which also forms its inverse by forward
-//      elimination and stores it, transposed, in the block's unused upper
-//      half; the rows below solved against it, one row per thread;
-//   2. forward substitution L Z = C by 32-row panels: the panel GEMM (8-wide
-//      chunks of the inner dimension through LDS), then
-//      the panel's rows times the inverse of its diagonal block (formed and
-//      kept by the factorization), both 4 x 4 outputs per thread;
+//   1. left-looking blocked Cholesky M = L L^T in panels of 32 columns.  The
+//      panel M[c0:, c0:c0+32] - L[c0:, :c0] L[c0:c0+32, :c0]^T is a product on
+//      the fp64 matrix cores (v_mfma_f64_16x16x4: wave w owns the 16-row tiles
+//      w, w + 4, ... of a pass of up to 192 rows), its inner dimension in
+//      16-wide chunks double-buffered through LDS so the next chunk's global
+//      loads overlap this chunk's products.  The diagonal block's 32 rows go
+//      first; one wave factors the block and forms its inverse V in
+//      registers (lane i holds row i; the other rows' entries arrive by
+//      readlane) and V is kept, transposed, in the block's unused upper half.
+//      Each later pass then stores (M - L L^T) V^T for its rows, a second
+//      matrix-core product on its LDS copy of M - L L^T;
+//   2. forward substitution L Z = C by 32-row panels: the panel product on
+//      the matrix cores (16-wide chunks through LDS), then the panel's rows
+//      times the kept inverse of its diagonal block (4 x 4 outputs per thread);
 //   3. back substitution L^T W~ = Z by 32-row panels, in place of Z;
 //   4. maps = (float) W~.
 // A pivot that is not positive and finite stops the system: info = its
@@ -52,7 +54,8 @@ constexpr int ZP = DTMAX + 1;   // padded row of a right-hand-side chunk
 // LDS (doubles): factorization: A chunks [2][TR][KP], B chunks [2][NB][KP];
 // substitutions: L chunks [2][NB][KSP], Z chunks [2][KS][ZP]; the panel rhs [NB][ZP] reuses the chunks'
 // space once a panel's products are done.
-// About 78 KB in all, so two systems share a compute unit.
+// About 78 KB in all, so two systems share a compute unit (with at most
+// 256 registers per lane: two waves per SIMD).
 constexpr int OFF_A = 0;
 constexpr int OFF_B = OFF_A + 2 * TR * KP;
 constexpr int OFF_L = 0;
