@@ -272,6 +272,32 @@ def test_multi_wide_solve_p2049_solver_alone(cb):
     plan.close()
 
 
+def test_multi_wide_solve_pivot_failures_inside_and_in_the_last_panel(cb):
+    # the blocked solve's first non-positive pivot, in the middle of a 32-column
+    # panel (column 101, panel 3) and in the last one-column panel (column 385),
+    # reported like the oracle's and with zero maps; the other systems of the
+    # same call solve as in the oracle (absolute lambda 0, SPD Gram matrices)
+    rng = np.random.default_rng(385)
+    n, P, d_t = 5, 385, 128
+    X = rng.standard_normal((n, 2 * P, P))
+    G = np.einsum("nrp,nrq->npq", X, X) / (2 * P) + 0.1 * np.eye(P)
+    C = rng.standard_normal((n, P, d_t))
+    G[1, 100, 100] = -1.0                       # fails at column 101
+    G[3, 384, 384] = -1.0                       # fails in the last panel
+    G[4, 200, :] = G[4, :, 200] = 0.0           # a zero row and column: pivot 201 is 0
+    (Gt, G64), (Ct, C64) = shared_f32(G), shared_f32(C)
+    maps, info = gpu_solve_ws(cb, Gt, Ct, 0.0, 0)
+    Wo, io = oracle.ridge_solve(G64, C64, 0.0, relative=False, n_threads=NTHREADS)
+    inf = info.cpu().numpy()
+    say(f"  pivots: gpu {inf.tolist()}, oracle {io.tolist()}")
+    assert inf.tolist() == [0, 101, 0, 385, 201] and io.tolist() == inf.tolist()
+    for m in (1, 3, 4):
+        assert not maps[m].any()
+    e = max(relF(maps[m].double().cpu().numpy(), Wo[m]) for m in (0, 2))
+    say(f"  healthy systems: maps relF {e:.3e}")
+    assert e <= TOL_SOLVER
+
+
 def test_multi_determinism_scaling_and_zero_weights(cb):
     rng = np.random.default_rng(77)
     L_s, H_s, L_t, H_t, B, T, k, stride = 5, 2, 2, 2, 2, 150, 3, 4
