@@ -55,9 +55,10 @@ struct MCfg {
     static constexpr int STAGE = OFF_W + KT * 4;
     static constexpr int NST = 6;                  // ring stages (one per iteration of a loop trip)
     static constexpr int TRS = 33;                 // row stride (floats) of the transpose scratch
+    static constexpr int NW = 8;                   // waves: two per SIMD
     static constexpr int OFF_T = NST * STAGE;
-    static constexpr int OFF_E = OFF_T + 4 * 32 * TRS * 4;  // centered: each wave's row sums e [2][32]
-    static constexpr int LDS = OFF_E + 4 * 2 * 32 * 4;
+    static constexpr int OFF_E = OFF_T + NW * 32 * TRS * 4;  // centered: each wave's row sums e [32]
+    static constexpr int LDS = OFF_E + NW * 32 * 4;
     static_assert(KT == 16, "one tile is one MFMA K step");
     static_assert(LDS <= 160 * 1024, "the ring must fit in LDS");
 };
@@ -158,25 +159,27 @@ __device__ __forceinline__ void flush_rows(const float *tr, int lane, int mode, 
 
 // NL: blocks staged per tile (distinct blocks of the task).  HASY: the last
 // of them is the target block (it is only ever the second column block).
-// YS: the task also owns sum w y of its map: wave w sums w y over 32 of the
-// target's channels.
+// YS: the task also owns sum w y of its map: waves 0..3 sum w y over 32 of
+// the target's channels each.
 // CENTER: moments about the map's weighted means (the paper's two-pass form):
 // the row operand is w (x - mu), the column operands stay the exact bf16 rows,
 // and every flush subtracts e mu^T with e = sum w (x - mu) as multiplied (hi +
 // lo); the outputs are A (ld P - 1) and B, with no bias row or column.
-template <int NL, bool HASY, bool YS, bool CENTER>
+template <int NL, bool HASY, bool YS, bool CENTER, bool FOLD_FIRST>
 __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &tk, const MultiCtx &c,
                                            lds_char_t *lds, int wave, int lane) {
     using K = MCfg;
     constexpr int E = 8;                        // 32-column blocks of every wave
-    constexpr int PER_TILE = NL + 1;            // copy instructions per tile and wave
-    const int rs = wave >> 1, half = wave & 1;  // row slot (0: rows[0], 1: rows[1]), 64-row half
+    constexpr int PER_TILE = NL + 1;            // copy instructions per tile of a copying wave
+    const int rs = wave >> 2, sub = wave & 3;   // row slot (0: rows[0], 1: rows[1]), 32-row sub-block
+    const bool copier = wave < 4;               // waves 0..3 stage the tiles
     const uint32_t lds_base = (uint32_t)(uintptr_t)lds;
 
-    // ---- copy descriptors: wave w copies rows 4w..4w+3 of every staged block.
-    // A cursor walks the call's tiles in order (16 rows on, or on to the next
-    // sequence); tiles past the end repeat the last one with zero weights.
-    const int crow = 4 * wave + (lane >> 4);
+    // ---- copy descriptors: copying wave w moves rows 4w..4w+3 of every staged
+    // block.  A cursor walks the call's tiles in order (16 rows on, or on to the
+    // next sequence); tiles past the end repeat the last one with zero weights.
+    const int cw = wave & 3;
+    const int crow = 4 * cw + (lane >> 4);
     const uint32_t cchunk = (uint32_t)((lane & 15) ^ (4 * (crow & 3))) * 16u;
     const uint32_t sstep = (uint32_t)(c.s_row * 2);          // bytes between calibration rows
     const uint32_t tstep = (uint32_t)(c.t_row * 2);
@@ -185,7 +188,7 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
 #pragma unroll
     for (int s = 0; s < NL; ++s) voff_full[s] = (uint32_t)crow * (slot_y(s) ? tstep : sstep) + cchunk;
     const float *wrow = a.w + (int64_t)tk.wrow * a.w_row_stride;
-    const uint32_t wr = 4 * wave + (lane & 3);  // the weight row this lane copies (lanes 0..3)
+    const uint32_t wr = 4 * cw + (lane & 3);    // the weight row this lane copies (lanes 0..3)
     struct Cursor {
         int u;                                  // tile index
         uint32_t seq, r0;                       // sequence, first row of the tile
@@ -207,8 +210,8 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
         }
         const bool ok = live && wr <= tmax;
         const void *g = ok ? (const void *)(cur.wp + (int64_t)wr * a.stride) : a.zero;
-        dma_tile<NL>(voff, base, __builtin_amdgcn_readfirstlane(stage + wave * 1024), g,
-                     __builtin_amdgcn_readfirstlane(stage + K::OFF_W + 16 * wave));
+        dma_tile<NL>(voff, base, __builtin_amdgcn_readfirstlane(stage + cw * 1024), g,
+                     __builtin_amdgcn_readfirstlane(stage + K::OFF_W + 16 * cw));
         if (cur.u + 1 < a.n_tiles) {
             cur.r0 += K::KT;
             if (cur.r0 >= a.rows_per_seq) {
@@ -231,10 +234,8 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
     const int tok_l = 8 * (g16 >> 1) + kk;
     const int cl = 2 * (g16 & 1) + (aa >> 1);
     const uint32_t lrow = tok_l * K::ROW + cl * 16 + (aa & 1) * 8;
-    uint32_t xoff[2], coff[E];
-    const uint32_t xslot = (uint32_t)tk.row_slot[rs] * K::BLK;
-#pragma unroll
-    for (int r = 0; r < 2; ++r) xoff[r] = xslot + lrow + 64u * ((uint32_t)(2 * half + r) ^ (uint32_t)kk);
+    const uint32_t xoff = (uint32_t)tk.row_slot[rs] * K::BLK + lrow + 64u * ((uint32_t)sub ^ (uint32_t)kk);
+    uint32_t coff[E];
 #pragma unroll
     for (int e = 0; e < E; ++e)
         coff[e] = (uint32_t)tk.col_slot[e >> 2] * K::BLK + lrow + 64u * ((uint32_t)(e & 3) ^ (uint32_t)kk);
@@ -242,59 +243,47 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
     const bool own_x = (tk.flags >> rs) & 1;
     const bool own_sumx = !CENTER && own_x;
     const bool own_sumw = !CENTER && (tk.flags & 4) && wave == 0;
-    // centered: the weighted means of the map (fp64 sums of pass 1)
+    // centered: the weighted means of the map (fp64 sums of pass 1, or a pilot's)
     const double *sm = CENTER ? a.sums + (int64_t)tk.map * (a.P + a.d_t) : nullptr;
     const double s_w = CENTER ? sm[0] : 0.0;
     auto mean_of = [&](int ch) { return (CENTER && s_w != 0.0) ? (float)(sm[1 + ch] / s_w) : 0.f; };
-    float mu_row[2];
-#pragma unroll
-    for (int r = 0; r < 2; ++r) mu_row[r] = mean_of(32 * (4 * tk.rows[rs] + 2 * half + r) + (lane & 31));
-    // the target block is column block 1 of a YS task: wave w sums w y over its window w
-    auto ycol = [&](int e) { return YS && e == 4 + wave; };
+    const int rb = tk.rows[rs];                                 // feature block of this wave's rows
+    const float mu_row = mean_of(32 * (4 * rb + sub) + (lane & 31));
+    // the target block is column block 1 of a YS task: copying wave w sums w y over its window w
+    const bool ysum = YS && copier;
 
-    struct Ops {
-        bf16x8_t xr[2], cf[E];
-        float w[8];
-    };
     struct Folded {
-        bf16x8_t hi[2], lo[2];
+        bf16x8_t hi, lo;
     };
-    f32x16_t acc[2 * E];
-    float sumx[2] = {0.f, 0.f}, sumy = 0.f, sumw = 0.f;
+    f32x16_t acc[E];
+    float sumx = 0.f, sumy = 0.f, sumw = 0.f;
     auto zero_acc = [&]() {
 #pragma unroll
-        for (int t = 0; t < 2 * E; ++t)
+        for (int t = 0; t < E; ++t)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[t][v] = 0.f;
     };
     zero_acc();
 
-    auto read_ops = [&](Ops &o, int st) {
+    // a = w x for the lane's 8 rows of one channel of the wave's rows, split
+    // into hi + lo; sum w x (or, centered, e) and sum w on the side
+    auto fold = [&](Folded &f, int st) {
         const lds_char_t *S = lds + st * K::STAGE;
-#pragma unroll
-        for (int r = 0; r < 2; ++r) o.xr[r] = tr_read8(S + xoff[r], S + xoff[r] + 4 * K::ROW);
-#pragma unroll
-        for (int e = 0; e < E; ++e) o.cf[e] = tr_read8(S + coff[e], S + coff[e] + 4 * K::ROW);
+        const bf16x8_t xr = tr_read8(S + xoff, S + xoff + 4 * K::ROW);
         const f32x4_t w0 = *(const lds_f32x4_t *)(S + lw);
         const f32x4_t w1 = *(const lds_f32x4_t *)(S + lw + 16);
-        o.w[0] = w0[0]; o.w[1] = w0[1]; o.w[2] = w0[2]; o.w[3] = w0[3];
-        o.w[4] = w1[0]; o.w[5] = w1[1]; o.w[6] = w1[2]; o.w[7] = w1[3];
-    };
-    // a = w x for the lane's 8 rows of one channel of row block r, split into
-    // hi + lo; sum w x on the side (kept by every wave: it is branch free and
-    // written only by the owner).
-    auto fold_row = [&](Folded &f, const Ops &o, int r) {
-        const uint4 ax = __builtin_bit_cast(uint4, o.xr[r]);
+        const float w[8] = {w0[0], w0[1], w0[2], w0[3], w1[0], w1[1], w1[2], w1[3]};
+        const uint4 ax = __builtin_bit_cast(uint4, xr);
         const uint32_t xv[4] = {ax.x, ax.y, ax.z, ax.w};
         float av[8];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             if constexpr (CENTER) {
-                av[2 * e] = o.w[2 * e] * (bf_lo(xv[e]) - mu_row[r]);
-                av[2 * e + 1] = o.w[2 * e + 1] * (bf_hi(xv[e]) - mu_row[r]);
+                av[2 * e] = w[2 * e] * (bf_lo(xv[e]) - mu_row);
+                av[2 * e + 1] = w[2 * e + 1] * (bf_hi(xv[e]) - mu_row);
             } else {
-                av[2 * e] = o.w[2 * e] * bf_lo(xv[e]);
-                av[2 * e + 1] = o.w[2 * e + 1] * bf_hi(xv[e]);
+                av[2 * e] = w[2 * e] * bf_lo(xv[e]);
+                av[2 * e + 1] = w[2 * e + 1] * bf_hi(xv[e]);
             }
         }
         uint32_t hv[4], lv[4];
@@ -308,130 +297,90 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
             float q[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) q[e] = (bf_lo(hv[e]) + bf_lo(lv[e])) + (bf_hi(hv[e]) + bf_hi(lv[e]));
-            sumx[r] += (q[0] + q[1]) + (q[2] + q[3]);
+            sumx += (q[0] + q[1]) + (q[2] + q[3]);
         } else {
-            sumx[r] += ((av[0] + av[1]) + (av[2] + av[3])) + ((av[4] + av[5]) + (av[6] + av[7]));
+            sumx += ((av[0] + av[1]) + (av[2] + av[3])) + ((av[4] + av[5]) + (av[6] + av[7]));
+            sumw += ((w[0] + w[1]) + (w[2] + w[3])) + ((w[4] + w[5]) + (w[6] + w[7]));
         }
-        f.hi[r] = __builtin_bit_cast(bf16x8_t, make_uint4(hv[0], hv[1], hv[2], hv[3]));
-        f.lo[r] = __builtin_bit_cast(bf16x8_t, make_uint4(lv[0], lv[1], lv[2], lv[3]));
+        f.hi = __builtin_bit_cast(bf16x8_t, make_uint4(hv[0], hv[1], hv[2], hv[3]));
+        f.lo = __builtin_bit_cast(bf16x8_t, make_uint4(lv[0], lv[1], lv[2], lv[3]));
     };
-    auto sum_w = [&](const Ops &o) {
-        if constexpr (!CENTER)
-            sumw += ((o.w[0] + o.w[1]) + (o.w[2] + o.w[3])) + ((o.w[4] + o.w[5]) + (o.w[6] + o.w[7]));
-    };
-    auto sum_y = [&](const Ops &o) {
-        // entry 4 + wave: selected with a uniform switch-free blend of the four candidates
-        if constexpr (YS) {
-            const bf16x8_t yf = wave == 0 ? o.cf[4] : wave == 1 ? o.cf[5] : wave == 2 ? o.cf[6] : o.cf[7];
-            const uint4 yv = __builtin_bit_cast(uint4, yf);
-            const uint32_t yy[4] = {yv.x, yv.y, yv.z, yv.w};
-            float py[8];
+    // sum w y over this copying wave's 32 target channels, from the column
+    // fragments of the tile (entry 4 + w)
+    auto sum_y = [&](const bf16x8_t &yf, int st) {
+        const lds_char_t *S = lds + st * K::STAGE;
+        const f32x4_t w0 = *(const lds_f32x4_t *)(S + lw);
+        const f32x4_t w1 = *(const lds_f32x4_t *)(S + lw + 16);
+        const float w[8] = {w0[0], w0[1], w0[2], w0[3], w1[0], w1[1], w1[2], w1[3]};
+        const uint4 yv = __builtin_bit_cast(uint4, yf);
+        const uint32_t yy[4] = {yv.x, yv.y, yv.z, yv.w};
+        float py[8];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                py[2 * i] = o.w[2 * i] * bf_lo(yy[i]);
-                py[2 * i + 1] = o.w[2 * i + 1] * bf_hi(yy[i]);
-            }
-            sumy += ((py[0] + py[1]) + (py[2] + py[3])) + ((py[4] + py[5]) + (py[6] + py[7]));
+        for (int i = 0; i < 4; ++i) {
+            py[2 * i] = w[2 * i] * bf_lo(yy[i]);
+            py[2 * i + 1] = w[2 * i + 1] * bf_hi(yy[i]);
         }
-    };
-    auto fold = [&](Folded &f, const Ops &o) {
-        fold_row(f, o, 0);
-        fold_row(f, o, 1);
-        sum_w(o);
-        sum_y(o);
-    };
-    auto mma_hi = [&](const Folded &f, const Ops &o) {
-#pragma unroll
-        for (int r = 0; r < 2; ++r)
-#pragma unroll
-            for (int e = 0; e < E; ++e)
-                acc[r * E + e] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.hi[r], o.cf[e], acc[r * E + e], 0, 0, 0);
-    };
-    auto mma_lo = [&](const Folded &f, const Ops &o) {
-#pragma unroll
-        for (int r = 0; r < 2; ++r)
-#pragma unroll
-            for (int e = 0; e < E; ++e)
-                acc[r * E + e] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.lo[r], o.cf[e], acc[r * E + e], 0, 0, 0);
+        sumy += ((py[0] + py[1]) + (py[2] + py[3])) + ((py[4] + py[5]) + (py[6] + py[7]));
     };
 
     // ---- flush: add the wave's tiles (and bias sums) into G and C
     float *tr = (float *)(lds + K::OFF_T) + wave * 32 * K::TRS;
-    float *es = (float *)(lds + K::OFF_E) + wave * 64;       // centered: e of the wave's 2 x 32 rows
+    float *es = (float *)(lds + K::OFF_E) + wave * 32;       // centered: e of the wave's 32 rows
     const int P = CENTER ? a.P - 1 : a.P;                    // leading dimension of G (or A)
     float *Gm = a.G + (int64_t)tk.map * P * P;
     float *Cm = a.C + (int64_t)tk.map * P * a.d_t;
     auto flush = [&]() {
-        const int rb = tk.rows[rs];                          // feature block of this wave's rows
+        const float ex = sumx + __shfl_xor(sumx, 32);         // lanes l and l + 32: the two token halves
         if constexpr (CENTER) {
-#pragma unroll
-            for (int r = 0; r < 2; ++r) {
-                const float ex = sumx[r] + __shfl_xor(sumx[r], 32);
-                if (lane < 32) es[32 * r + lane] = ex;
-            }
+            if (lane < 32) es[lane] = ex;
             asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
         }
+        const int R = 4 * rb + sub;                          // 32-row block of G
 #pragma unroll
-        for (int r = 0; r < 2; ++r) {
-            const int R = 4 * rb + 2 * half + r;             // 32-row block of G
+        for (int e = 0; e < E; ++e) {
+            const int cb = e >> 2, win = e & 3;
+            if (!((tk.cell_mask >> (2 * rs + cb)) & 1)) continue;      // an unused cell
+            const int col = tk.cols[cb];
+            const bool is_y = col == a.k;
+            const int Cc = 4 * col + win;                    // 32-column block (of G, or of C if is_y)
+            if (!is_y && col == rb && Cc < R) continue;      // below the diagonal of a diagonal block
+            const f32x16_t &t = acc[e];
+            // centered: minus e_i mu_j, mu_j the mean of this lane's column
+            const float muc = CENTER ? mean_of(is_y ? 128 * a.k + 32 * win + (lane & 31) : 32 * Cc + (lane & 31))
+                                     : 0.f;
 #pragma unroll
-            for (int e = 0; e < E; ++e) {
-                const int cb = e >> 2, win = e & 3;
-                if (!((tk.cell_mask >> (2 * rs + cb)) & 1)) continue;      // an unused cell
-                const int col = tk.cols[cb];
-                const bool is_y = col == a.k;
-                const int Cc = 4 * col + win;                // 32-column block (of G, or of C if is_y)
-                if (!is_y && col == rb && Cc < R) continue;  // below the diagonal of a diagonal block
-                const f32x16_t &t = acc[r * E + e];
-                // centered: minus e_i mu_j, mu_j the mean of this lane's column
-                const float muc = CENTER ? mean_of(is_y ? 128 * a.k + 32 * win + (lane & 31) : 32 * Cc + (lane & 31))
-                                         : 0.f;
-#pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const int i = 8 * (v >> 2) + (v & 3) + 4 * (lane >> 5);
-                    tr[i * K::TRS + (lane & 31)] = CENTER ? t[v] - es[32 * r + i] * muc : t[v];
-                }
-                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-                // mode 0: cross tile of C; 1: diagonal tile of G; 2: any other tile of G (+ its mirror)
-                const int mode = is_y ? 0 : (Cc == R ? 1 : 2);
-                float *dst = is_y ? Cm + (int64_t)(32 * R) * a.d_t + 32 * win
-                                  : Gm + (int64_t)(32 * R) * P + 32 * Cc;
-                float *mir = Gm + (int64_t)(32 * Cc) * P + 32 * R;
-                const int64_t ld = is_y ? a.d_t : P;
-                flush_rows(tr, lane, mode, dst, mir, ld);
+            for (int v = 0; v < 16; ++v) {
+                const int i = 8 * (v >> 2) + (v & 3) + 4 * (lane >> 5);
+                tr[i * K::TRS + (lane & 31)] = CENTER ? t[v] - es[i] * muc : t[v];
             }
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            // mode 0: cross tile of C; 1: diagonal tile of G; 2: any other tile of G (+ its mirror)
+            const int mode = is_y ? 0 : (Cc == R ? 1 : 2);
+            float *dst = is_y ? Cm + (int64_t)(32 * R) * a.d_t + 32 * win : Gm + (int64_t)(32 * R) * P + 32 * Cc;
+            float *mir = Gm + (int64_t)(32 * Cc) * P + 32 * R;
+            const int64_t ld = is_y ? a.d_t : P;
+            flush_rows(tr, lane, mode, dst, mir, ld);
         }
         if constexpr (CENTER) {
-            if (a.resid && own_x) {
+            if (a.resid && own_x && lane < 32) {
                 // shifted form: sum w (x - mu) of the rows, one owner per entry (sum w
                 // and sum w y come from the target-block pass of the same call)
-                double *rsum = a.resid + (int64_t)tk.map * (a.P + a.d_t);
-#pragma unroll
-                for (int r = 0; r < 2; ++r) {
-                    const float ex = sumx[r] + __shfl_xor(sumx[r], 32);
-                    if (lane < 32) rsum[1 + 128 * rb + 64 * half + 32 * r + lane] += (double)ex;
-                }
+                a.resid[(int64_t)tk.map * (a.P + a.d_t) + 1 + 128 * rb + 32 * sub + lane] += (double)ex;
             }
-            sumx[0] = sumx[1] = 0.f;
+            sumx = 0.f;
             zero_acc();
             return;
         }
-        // bias row / column: lanes l and l + 32 hold the two halves of each K step
-        if (own_sumx) {
-#pragma unroll
-            for (int r = 0; r < 2; ++r) {
-                const float sx = sumx[r] + __shfl_xor(sumx[r], 32);
-                if (lane < 32) {
-                    const int ch = 128 * rb + 64 * half + 32 * r + lane;
-                    Gm[(int64_t)ch * P + P - 1] += sx;
-                    Gm[(int64_t)(P - 1) * P + ch] += sx;
-                }
-            }
+        // bias row / column
+        if (own_sumx && lane < 32) {
+            const int ch = 128 * rb + 32 * sub + lane;
+            Gm[(int64_t)ch * P + P - 1] += ex;
+            Gm[(int64_t)(P - 1) * P + ch] += ex;
         }
-        sumx[0] = sumx[1] = 0.f;
-        if (YS) {
+        sumx = 0.f;
+        if (ysum) {
             const float sy = sumy + __shfl_xor(sumy, 32);
-            if (lane < 32) Cm[(int64_t)(P - 1) * a.d_t + 32 * wave + lane] += sy;
+            if (lane < 32) Cm[(int64_t)(P - 1) * a.d_t + 32 * cw + lane] += sy;
         }
         sumy = 0.f;
         if (own_sumw) {
@@ -442,94 +391,64 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
         zero_acc();
     };
 
-    // ---- pipeline.  Tile t's operands are read from LDS two iterations ahead
-    // (iteration t-2), folded one iteration ahead (t-1) and multiplied in
-    // iteration t, so no LDS latency sits in front of a fold and no fold in
-    // front of an MFMA.  Iteration t: tile t+2 has landed (wait + barrier);
-    // tile t+6 is issued into the stage of tile t, whose reads finished two
-    // iterations ago; the hi MFMAs of tile t run with the fold of row block 0
-    // of tile t+1 and half of the reads of tile t+2, the lo MFMAs with the
-    // rest (an MFMA keeps the matrix core busy for about as long as the wave
-    // needs to issue five other instructions).  Operand sets rotate with
-    // period 3, folded sets with period 2: six iterations per loop trip.
+    // ---- pipeline.  Eight waves, two per SIMD: while one wave waits for its
+    // operands or folds, the other keeps the matrix core busy.  Iteration t:
+    // tile t+1 has landed (the copying waves' wait, then the barrier); tile
+    // t+NST-1 is issued into the stage of tile t-1, which every wave finished
+    // reading before the barrier; the wave reads tile t's column fragments,
+    // runs its 16 MFMAs with tile t's folded rows (folded in iteration t-1),
+    // and folds tile t+1.
+    if (copier) {
 #pragma unroll
-    for (int u = 0; u < K::NST; ++u) issue(u);                // tiles 0 .. NST-1 into stages 0 .. NST-1
+        for (int u = 0; u < K::NST - 1; ++u) issue(u);        // tiles 0 .. NST-2 into stages 0 .. NST-2
+        wait_vm<(K::NST - 2) * PER_TILE>();                   // tile 0 has landed
+    }
+    lds_barrier();
     const int n_iter = (a.n_tiles + 5) / 6 * 6;              // padded with zero-weight tiles
-    Ops o0, o1, o2;
     Folded f0, f1;
-    wait_vm<(K::NST - 1) * PER_TILE>();                      // tile 0 has landed
-    lds_barrier();
-    read_ops(o0, 0);
-    wait_vm<(K::NST - 2) * PER_TILE>();                      // tile 1 has landed
-    lds_barrier();
-    read_ops(o1, 1);
-    fold(f0, o0);
-    auto pin = [&](const Folded &f) {
-#pragma unroll
-        for (int r = 0; r < 2; ++r) asm volatile("" ::"v"(f.hi[r]), "v"(f.lo[r]));
-        asm volatile("" ::"v"(sumx[0]), "v"(sumx[1]), "v"(sumw));
-    };
-    auto read_half = [&](Ops &o, int st, int half) {
-        const lds_char_t *S = lds + st * K::STAGE;
-        if (half == 0) {
-#pragma unroll
-            for (int r = 0; r < 2; ++r) o.xr[r] = tr_read8(S + xoff[r], S + xoff[r] + 4 * K::ROW);
-            const f32x4_t w0 = *(const lds_f32x4_t *)(S + lw);
-            const f32x4_t w1 = *(const lds_f32x4_t *)(S + lw + 16);
-            o.w[0] = w0[0]; o.w[1] = w0[1]; o.w[2] = w0[2]; o.w[3] = w0[3];
-            o.w[4] = w1[0]; o.w[5] = w1[1]; o.w[6] = w1[2]; o.w[7] = w1[3];
-        }
-#pragma unroll
-        for (int e = 0; e < E; ++e)
-            if ((e < E / 2) == (half == 0)) o.cf[e] = tr_read8(S + coff[e], S + coff[e] + 4 * K::ROW);
-    };
-    auto iteration = [&](const int i, const Ops &oa, const Folded &fa, const Ops &ob, Folded &fb, Ops &oc) {
-        wait_vm<(K::NST - 3) * PER_TILE>();                  // tile t+2 has landed
+    fold(f0, 0);
+    auto iteration = [&](int t, const Folded &fa, Folded &fb) {
+        const int st = t % K::NST, sn = (t + 1) % K::NST, sp = (t + K::NST - 1) % K::NST;
+        if (copier) wait_vm<(K::NST - 3) * PER_TILE>();       // tile t+1 has landed
         lds_barrier();
-        issue(i);                                            // tile t + NST into the stage of tile t
-        __builtin_amdgcn_sched_barrier(0);
-        read_half(oc, (i + 2) % K::NST, 0);
-        mma_hi(fa, oa);
-        fold_row(fb, ob, 0);
+        if (copier) issue(sp);                                // tile t+NST-1 into the stage of tile t-1
+        const lds_char_t *S = lds + st * K::STAGE;
+        auto products = [&]() __attribute__((always_inline)) {
+            bf16x8_t cf[E];
 #pragma unroll
-        for (int i = 0; i < 2 * E; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);            // one MFMA
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);            // one LDS read
-            __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);            // up to five VALU
-        }
-        __builtin_amdgcn_sched_barrier(0);
-        read_half(oc, (i + 2) % K::NST, 1);
-        fold_row(fb, ob, 1);
-        sum_w(ob);
-        mma_lo(fa, oa);
-        pin(fb);
+            for (int e = 0; e < E; ++e) cf[e] = tr_read8(S + coff[e], S + coff[e] + 4 * K::ROW);
 #pragma unroll
-        for (int i = 0; i < 2 * E; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);            // up to five VALU
+            for (int e = 0; e < E; ++e) acc[e] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa.hi, cf[e], acc[e], 0, 0, 0);
+#pragma unroll
+            for (int e = 0; e < E; ++e) acc[e] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa.lo, cf[e], acc[e], 0, 0, 0);
+            if (ysum) {
+                const bf16x8_t yf = cw == 0 ? cf[4] : cw == 1 ? cf[5] : cw == 2 ? cf[6] : cf[7];
+                sum_y(yf, st);
+            }
+        };
+        // the two waves of a SIMD (w and w + 4) take the steps in opposite
+        // orders, so one folds while the other keeps the matrix core busy
+        if constexpr (FOLD_FIRST) {
+            fold(fb, sn);
+            products();
+        } else {
+            products();
+            fold(fb, sn);
         }
-        __builtin_amdgcn_sched_barrier(0);
-        if constexpr (YS) sum_y(ob);
     };
-    // t = 6 j + i: the stage of tile t is i, a constant in each unrolled iteration
     for (int c0 = 0; c0 < n_iter; c0 += a.chunk_tiles) {
         const int c1 = min(c0 + a.chunk_tiles, n_iter);
-        for (int t = c0; t < c1; t += 6) {
-            iteration(0, o0, f0, o1, f1, o2);
-            iteration(1, o1, f1, o2, f0, o0);
-            iteration(2, o2, f0, o0, f1, o1);
-            iteration(3, o0, f1, o1, f0, o2);
-            iteration(4, o1, f0, o2, f1, o0);
-            iteration(5, o2, f1, o0, f0, o1);
+        for (int t = c0; t < c1; t += 2) {
+            iteration(t, f0, f1);
+            iteration(t + 1, f1, f0);
         }
         flush();
     }
-    wait_vm<0>();                                            // drain the trailing copies
+    if (copier) wait_vm<0>();                                 // drain the trailing copies
 }
 
 template <bool CENTER>
-__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
+__global__ __attribute__((amdgpu_flat_work_group_size(512, 512), amdgpu_waves_per_eu(2, 2)))
 void stats_multi_kernel(MultiArgs a) {
     using K = MCfg;
     __shared__ __attribute__((aligned(16))) char lds_raw[K::LDS];
@@ -562,14 +481,18 @@ void stats_multi_kernel(MultiArgs a) {
     const bool hasy = tk.slot_layer[tk.n_lds - 1] < 0;
     const int var = (tk.n_lds - 1) * 3 + (hasy ? ((!CENTER && (tk.flags & 8)) ? 2 : 1) : 0);
     switch (var) {
+#define CB_W(NL_, HY, Y)                                                                            \
+    if (wave < 4) multi_wave<NL_, HY, Y, CENTER, false>(a, tk, c, lds, wave, lane);                 \
+    else multi_wave<NL_, HY, Y, CENTER, true>(a, tk, c, lds, wave, lane);
 #define CB_V(NL_)                                                                                  \
-        case (NL_ - 1) * 3 + 0: multi_wave<NL_, false, false, CENTER>(a, tk, c, lds, wave, lane); break; \
-        case (NL_ - 1) * 3 + 1: multi_wave<NL_, true, false, CENTER>(a, tk, c, lds, wave, lane); break;  \
+        case (NL_ - 1) * 3 + 0: CB_W(NL_, false, false) break;                                     \
+        case (NL_ - 1) * 3 + 1: CB_W(NL_, true, false) break;                                      \
         case (NL_ - 1) * 3 + 2:                                                                     \
-            if constexpr (!CENTER) multi_wave<NL_, true, true, false>(a, tk, c, lds, wave, lane);    \
+            if constexpr (!CENTER) { CB_W(NL_, true, true) }                                        \
             break;
         CB_V(1) CB_V(2) CB_V(3) CB_V(4)
 #undef CB_V
+#undef CB_W
         default: break;
     }
 }
@@ -626,13 +549,13 @@ __global__ __launch_bounds__(256) void means_multi_kernel(MeansMultiArgs a) {
 
 hipError_t launch_stats_multi(const MultiArgs &a, hipStream_t s) {
     if (a.n_tasks == 0 || a.n_tiles == 0) return hipSuccess;
-    hipLaunchKernelGGL(stats_multi_kernel<false>, dim3(8 * a.per_xcd), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(stats_multi_kernel<false>, dim3(8 * a.per_xcd), dim3(512), 0, s, a);
     return hipGetLastError();
 }
 
 hipError_t launch_stats_multi_centered(const MultiArgs &a, hipStream_t s) {
     if (a.n_tasks == 0 || a.n_tiles == 0) return hipSuccess;
-    hipLaunchKernelGGL(stats_multi_kernel<true>, dim3(8 * a.per_xcd), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(stats_multi_kernel<true>, dim3(8 * a.per_xcd), dim3(512), 0, s, a);
     return hipGetLastError();
 }
 
