@@ -22,19 +22,23 @@
 // the call and adds its fp32 sums into G and C itself (it is the only writer
 // of those elements): no partial sums, no reduction pass, no atomics.
 //
-// Per workgroup: four waves, one per SIMD.  Wave w owns 64 rows of row block
-// rows[w / 2] (two 32-row MFMA blocks) and all eight 32-column blocks of the
-// two column blocks: 16 accumulator tiles, 32 v_mfma_f32_32x32x16_bf16 per
-// 16-row K step.  It folds the fp32 weight into its two x fragments and
-// splits w x into hi = RNE_bf16(w x) and lo = RNE_bf16(w x - hi); the
-// column operands are the exact bf16 rows.
+// Per workgroup: eight waves, two per SIMD.  Wave w owns the 32 rows
+// 32 (w mod 4) .. + 31 of row block rows[w / 4] and all eight 32-column
+// blocks of the two column blocks: 8 accumulator tiles, 16
+// v_mfma_f32_32x32x16_bf16 per 16-row K step.  It folds the fp32 weight
+// into its x fragment and splits w x into hi = RNE_bf16(w x) and lo =
+// RNE_bf16(w x - hi); the column operands are the exact bf16 rows.  The two
+// waves of a SIMD (w and w + 4) take each tile's steps in opposite orders
+// (products then fold, fold then products), so one folds while the other
+// keeps the matrix core busy.
 //
 // Staging.  A tile is 16 calibration rows of one sequence.  Its blocks (the
 // distinct blocks among its two row and two column blocks) move HBM -> LDS
-// by global_load_lds_dwordx4 through a six-stage ring, six tiles ahead; each
-// 16-byte chunk c of row t sits at chunk c ^ 4(t mod 4) so the transposed
-// operand reads (ds_read_b64_tr_b16) are conflict free.  Rows past the end of
-// a sequence repeat its last row with weight zero.
+// by global_load_lds_dwordx4, issued by waves 0..3, through a six-stage
+// ring, five tiles ahead; each 16-byte chunk c of row t sits at chunk
+// c ^ 4(t mod 4) so the transposed operand reads (ds_read_b64_tr_b16) are
+// conflict free.  Rows past the end of a sequence repeat its last row with
+// weight zero.
 //
 // Flush.  Every at most 2,046 tiles (32,736 rows) and at the end of the call
 // each wave adds its tiles into G (and C): a tile above the diagonal goes to
@@ -421,6 +425,12 @@ __device__ __forceinline__ void multi_wave(const MultiArgs &a, const MultiTask &
             for (int e = 0; e < E; ++e) acc[e] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa.hi, cf[e], acc[e], 0, 0, 0);
 #pragma unroll
             for (int e = 0; e < E; ++e) acc[e] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa.lo, cf[e], acc[e], 0, 0, 0);
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);     // the two reads of fragment e
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // its hi product
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
             if (ysum) {
                 const bf16x8_t yf = cw == 0 ? cf[4] : cw == 1 ? cf[5] : cw == 2 ? cf[6] : cf[7];
                 sum_y(yf, st);
