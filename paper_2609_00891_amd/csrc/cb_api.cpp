@@ -34,6 +34,10 @@ struct cb_plan {
     cb::ApplyMultiMap *d_amaps = nullptr;   // multi-layer application: map records, visiting order, layers
     int32_t *d_aorder = nullptr;
     int32_t *d_alayers = nullptr;
+    int32_t *d_apairs = nullptr;            // multi-layer application: pair records (see ApplyMultiArgs)
+    int32_t n_apairs = 0, apair_stride = 0;
+    int32_t *d_asingles = nullptr;          // and the maps without a partner, in visiting order
+    int32_t n_asingles = 0;
     int32_t *d_mwrow = nullptr;             // multi-layer: weight row of each map (means pass)
     // statistics schedule
     int32_t n_items = 0;
@@ -341,6 +345,8 @@ cb_status cb_plan_destroy(cb_plan *p) {
     (void)hipFree(p->d_amaps);
     (void)hipFree(p->d_aorder);
     (void)hipFree(p->d_alayers);
+    (void)hipFree(p->d_apairs);
+    (void)hipFree(p->d_asingles);
     (void)hipFree(p->d_mwrow);
     (void)hipFree(p->d_rws);
     delete p;
@@ -521,6 +527,69 @@ cb_status cb_plan_create(const cb_head_map *map, const cb_cache *src_geom, const
     return ok();
 }
 
+// Pairs of maps for the multi-layer application: two maps of one (kv, source
+// head) whose source-layer sets are equal (as multisets) share every staged
+// block.  Maps are taken in visiting order (kv, source head, target layer,
+// target head); within a run of one (kv, source head) the maps of each layer
+// set pair up in that order, and an odd one out stays single.  Record of a
+// pair (stride 4 + 3k): [0] map A, [1] map B, [2], [3] unused, [4 + j] the
+// j-th layer of the set in ascending order, [4 + k + j] and [4 + 2k + j] A's
+// and B's block index of that layer.
+static std::vector<int32_t> build_pairs(const cb_head_map_multi *map, int n, int k, const std::vector<int> &order,
+                                        int32_t *n_pairs, std::vector<int32_t> *singles) {
+    const int stride = 4 + 3 * k;
+    std::vector<int32_t> rec;
+    auto sorted_blocks = [&](int m) {
+        std::vector<std::pair<int32_t, int32_t>> v(k);       // (layer, block index)
+        for (int i = 0; i < k; ++i) v[i] = {map->src_layers[(int64_t)m * k + i], i};
+        std::stable_sort(v.begin(), v.end());
+        return v;
+    };
+    int32_t np = 0;
+    singles->clear();
+    for (int g0 = 0; g0 < n;) {
+        int g1 = g0 + 1;
+        while (g1 < n && map->kv[order[g1]] == map->kv[order[g0]] &&
+               map->src_head[order[g1]] == map->src_head[order[g0]])
+            ++g1;
+        std::map<std::vector<int32_t>, int> waiting;          // layer set -> a map still without partner
+        std::vector<std::pair<int, int>> pr;                  // in the order the second member is met
+        for (int i = g0; i < g1; ++i) {
+            const int m = order[i];
+            std::vector<int32_t> key;
+            for (const auto &e : sorted_blocks(m)) key.push_back(e.first);
+            auto it = waiting.find(key);
+            if (it == waiting.end()) {
+                waiting[key] = m;
+            } else {
+                pr.push_back({it->second, m});
+                waiting.erase(it);
+            }
+        }
+        for (const auto &ab : pr) {
+            const auto A = sorted_blocks(ab.first), B = sorted_blocks(ab.second);
+            std::vector<int32_t> r(stride, 0);
+            r[0] = ab.first;
+            r[1] = ab.second;
+            for (int j = 0; j < k; ++j) {
+                r[4 + j] = A[j].first;
+                r[4 + k + j] = A[j].second;
+                r[4 + 2 * k + j] = B[j].second;
+            }
+            rec.insert(rec.end(), r.begin(), r.end());
+            ++np;
+        }
+        for (int i = g0; i < g1; ++i) {                       // the maps left alone, in visiting order
+            const int m = order[i];
+            for (const auto &w : waiting)
+                if (w.second == m) singles->push_back(m);
+        }
+        g0 = g1;
+    }
+    *n_pairs = np;
+    return rec;
+}
+
 cb_status cb_plan_create_multi(const cb_head_map_multi *map, const cb_cache *src_geom, const cb_cache *tgt_geom,
                                int32_t sample_stride, cb_plan **out) {
     if (!out) return fail(CB_ERR_INVALID_ARGUMENT, "out is NULL");
@@ -671,6 +740,10 @@ cb_status cb_plan_create_multi(const cb_head_map_multi *map, const cb_cache *src
         }
     }
     p->n_tasks = (int32_t)tasks.size();
+    std::vector<int32_t> singles;
+    const std::vector<int32_t> pairs = build_pairs(map, n, k, order, &p->n_apairs, &singles);
+    p->apair_stride = 4 + 3 * k;
+    p->n_asingles = (int32_t)singles.size();
 
     std::vector<cb::ApplyMultiMap> amaps(n);
     for (int m = 0; m < n; ++m) amaps[m] = {map->tgt_layer[m], map->tgt_head[m], map->kv[m], map->src_head[m]};
@@ -680,6 +753,8 @@ cb_status cb_plan_create_multi(const cb_head_map_multi *map, const cb_cache *src
                hipMalloc(&p->d_amaps, sizeof(cb::ApplyMultiMap) * n) == hipSuccess &&
                hipMalloc(&p->d_aorder, sizeof(int32_t) * n) == hipSuccess &&
                hipMalloc(&p->d_alayers, sizeof(int32_t) * (size_t)n * k) == hipSuccess &&
+               hipMalloc(&p->d_apairs, sizeof(int32_t) * (pairs.size() + 1)) == hipSuccess &&
+               hipMalloc(&p->d_asingles, sizeof(int32_t) * (singles.size() + 1)) == hipSuccess &&
                hipMalloc(&p->d_mwrow, sizeof(int32_t) * (size_t)n) == hipSuccess &&
                hipMalloc(&p->d_whi, 2 * wsplit) == hipSuccess &&   // hi and lo fragment planes
                hipMalloc(&p->d_bias, sizeof(float) * n * d_t) == hipSuccess;
@@ -693,6 +768,10 @@ cb_status cb_plan_create_multi(const cb_head_map_multi *map, const cb_cache *src
         hipMemcpy(p->d_amaps, amaps.data(), sizeof(cb::ApplyMultiMap) * n, hipMemcpyHostToDevice) != hipSuccess ||
         hipMemcpy(p->d_aorder, order.data(), sizeof(int32_t) * n, hipMemcpyHostToDevice) != hipSuccess ||
         hipMemcpy(p->d_alayers, map->src_layers, sizeof(int32_t) * (size_t)n * k, hipMemcpyHostToDevice) != hipSuccess ||
+        (!pairs.empty() &&
+         hipMemcpy(p->d_apairs, pairs.data(), sizeof(int32_t) * pairs.size(), hipMemcpyHostToDevice) != hipSuccess) ||
+        (!singles.empty() &&
+         hipMemcpy(p->d_asingles, singles.data(), sizeof(int32_t) * singles.size(), hipMemcpyHostToDevice) != hipSuccess) ||
         hipMemcpy(p->d_mwrow, map->weight_row, sizeof(int32_t) * (size_t)n, hipMemcpyHostToDevice) != hipSuccess) {
         cb_plan_destroy(p);
         return fail(CB_ERR_DEVICE, "copying the schedule to the device failed");
@@ -1432,13 +1511,15 @@ static cb_status apply_multi(cb_plan *p, const float *maps, const cb_cache *src,
     if (((uintptr_t)maps) % 4) return fail(CB_ERR_MISALIGNED, "maps must be 4-byte aligned");
     const int64_t N = (int64_t)src->n_seqs * src->seq_len;
     if (N > (int64_t)INT32_MAX - 4096) return fail(CB_ERR_UNSUPPORTED, "too many tokens in one call");
-    if (N > 0 && (int64_t)(src->n_seqs - 1) * src->s_seq + (int64_t)(src->seq_len - 1) * src->s_tok + 128 >
+    // the kernel addresses a row by a 32-bit byte offset from its (layer, kv, head) base
+    if (N > 0 && 2 * ((int64_t)(src->n_seqs - 1) * src->s_seq + (int64_t)(src->seq_len - 1) * src->s_tok + 128) >
                      (int64_t)UINT32_MAX)
-        return fail(CB_ERR_UNSUPPORTED, "src rows of one (layer, kv, head) span more than 2^32 elements; "
+        return fail(CB_ERR_UNSUPPORTED, "src rows of one (layer, kv, head) span more than 4 GiB; "
                                         "apply in smaller batches");
     if (src_rope && N > 0 &&
-        (int64_t)(src->n_seqs - 1) * p->H_s * src->seq_len * p->d_s + (int64_t)src->seq_len * p->d_s > (int64_t)UINT32_MAX)
-        return fail(CB_ERR_UNSUPPORTED, "the de-rotated rows of one (layer, head) would span more than 2^32 elements; "
+        2 * ((int64_t)(src->n_seqs - 1) * p->H_s * src->seq_len * p->d_s + (int64_t)src->seq_len * p->d_s) >
+            (int64_t)UINT32_MAX)
+        return fail(CB_ERR_UNSUPPORTED, "the de-rotated rows of one (layer, head) would span more than 4 GiB; "
                                         "apply in smaller batches");
     if (cb_status s = check_device(p)) return s;
     hipStream_t st = (hipStream_t)stream;
@@ -1461,20 +1542,36 @@ static cb_status apply_multi(cb_plan *p, const float *maps, const cb_cache *src,
     a.k = p->k;
     a.n_maps = p->n_maps;
     a.n_tiles = (int32_t)((N + 255) / 256);
-    const int64_t n_tasks = (int64_t)p->n_maps * a.n_tiles;
-    if (n_tasks > (int64_t)INT32_MAX - 8) return fail(CB_ERR_UNSUPPORTED, "too many application tasks");
-    a.n_tasks = (int32_t)n_tasks;
-    a.per_xcd = (a.n_tasks + 7) / 8;
+    if ((int64_t)p->n_maps * a.n_tiles > (int64_t)INT32_MAX - 8)
+        return fail(CB_ERR_UNSUPPORTED, "too many application tasks");
     a.maps = p->d_amaps;
-    a.order = p->d_aorder;
     a.src_layers = p->d_alayers;
     a.wfrag = p->d_whi;
     a.bias = p->d_bias;
     a.rope_table = tgt_rope ? tgt_rope->table : nullptr;
     a.rope_style = tgt_rope ? tgt_rope->style : 0;
     a.rope_pos_offset = tgt_rope ? tgt_rope->pos_offset : 0;
-    if (cb::launch_apply_multi(a, p->n_cu, st) != hipSuccess)
-        return fail(CB_ERR_DEVICE, "multi-layer application kernel launch failed");
+    // pairs of maps that share their source blocks, then the maps left alone
+    if (p->n_apairs > 0) {
+        cb::ApplyMultiArgs ap = a;
+        ap.pairs = p->d_apairs;
+        ap.n_pairs = p->n_apairs;
+        ap.pair_stride = p->apair_stride;
+        ap.n_tasks = p->n_apairs * a.n_tiles;
+        ap.per_xcd = (ap.n_tasks + 7) / 8;
+        if (cb::launch_apply_multi(ap, p->n_cu, st) != hipSuccess)
+            return fail(CB_ERR_DEVICE, "multi-layer application kernel launch failed");
+    }
+    if (p->n_asingles > 0) {
+        cb::ApplyMultiArgs as = a;
+        as.pairs = nullptr;
+        as.order = p->d_asingles;
+        as.n_maps = p->n_asingles;
+        as.n_tasks = p->n_asingles * a.n_tiles;
+        as.per_xcd = (as.n_tasks + 7) / 8;
+        if (cb::launch_apply_multi(as, p->n_cu, st) != hipSuccess)
+            return fail(CB_ERR_DEVICE, "multi-layer application kernel launch failed");
+    }
     return ok();
 }
 

@@ -13,6 +13,10 @@
 //   output channel 32 w + (l mod 32), inputs 128 i + 16 ks + 8 (l / 32) .. + 7.
 //   One fragment load is 1 KiB contiguous.  The fp32 bias is kept apart.
 //
+// Two application kernels share that layout.  apply_pair_kernel (below) takes
+// pairs of maps that read the same source blocks, staging each block once for
+// both; apply_multi_kernel takes the maps left without such a partner.
+//
 // apply_multi_kernel: a task is (map, tile of 256 tokens).  The grid is
 //   persistent, one workgroup of four waves per compute unit; the workgroups
 //   of one XCD walk a contiguous run of tasks (maps in groups of four
@@ -402,6 +406,410 @@ void apply_multi_kernel(ApplyMultiArgs a) {
     }
 }
 
+
+// ---------------------------------------------------------------------------
+// The paired form.  A task is (pair of maps, tile of 256 tokens); the two maps
+// of a pair read the same k source blocks (one (kv, head) of the sender, the
+// same set of layers), so each block is staged once for both: half the staged
+// source rows per output.  At k = 8 with L_t > L_s many neighbouring target
+// layers select the same source layers.  The pair's record holds its blocks in
+// ascending layer order with each map's block index i for them.  Maps without
+// such a partner run in apply_multi_kernel.
+//
+// Four waves, one per SIMD.  Wave w owns output channels 32 w .. 32 w + 31 of
+// both maps: sixteen 32 x 32 accumulator tiles (256 registers), so each x
+// fragment read from LDS feeds four MFMAs (A hi, B hi, A lo, B lo).  Staged
+// blocks move HBM -> LDS with global_load_lds_dwordx4 (no register staging),
+// one block ahead through two 64 KiB buffers; each map's W^T fragments run four
+// K steps ahead through a ring of four register slots, across blocks and tasks.
+typedef __attribute__((address_space(3))) char lds_char_t;
+typedef __attribute__((address_space(3))) bf16x8_t lds_bf16x8_t;
+
+constexpr int PG = 4;                   // pairs per tile-major group of the task order
+
+// The pair records are written before the launch and never during it, so they are read through the
+// constant address space (scalar loads).
+typedef const __attribute__((address_space(4))) int32_t *crec_t;
+
+struct PairTask {
+    int32_t mA, mB;
+    crec_t rec;                         // the pair's record
+    int64_t tok0;
+    const uint16_t *x;                  // source view of the pair's (kv, head), layer 0
+    int64_t s_layer, s_seq, s_tok;
+};
+
+__device__ __forceinline__ PairTask pair_task(const ApplyMultiArgs &a, int task) {
+    const int full = a.n_pairs & ~(PG - 1);
+    const int in_full = full * a.n_tiles;
+    int tile, p;
+    if (task < in_full) {
+        const int per = PG * a.n_tiles;
+        const int g = task / per, r = task - g * per;
+        tile = r / PG;
+        p = PG * g + (r - tile * PG);
+    } else {
+        const int rem = a.n_pairs - full;
+        const int r = task - in_full;
+        tile = r / rem;
+        p = full + (r - tile * rem);
+    }
+    PairTask t;
+    t.rec = (crec_t)(a.pairs + (int64_t)p * a.pair_stride);
+    t.mA = __builtin_amdgcn_readfirstlane(t.rec[0]);
+    t.mB = __builtin_amdgcn_readfirstlane(t.rec[1]);
+    t.tok0 = (int64_t)tile * TT;
+    const crec_t mp = (crec_t)(a.maps + t.mA);            // tgt_layer, tgt_head, kv, src_head
+    const int kv = mp[2], src_head = mp[3];
+    const bool kview = kv == 0 && a.srck != nullptr;
+    const Strides &v = kview ? a.ssk : a.ss;
+    t.x = kview ? a.srck + src_head * v.head : a.src + kv * v.kv + src_head * v.head;
+    t.s_layer = v.layer;
+    t.s_seq = v.seq;
+    t.s_tok = v.tok;
+    return t;
+}
+
+// Eight 16-byte copies global -> LDS under one save of M0: copy j reads
+// base + off[J + j] per lane and writes lane l's chunk at m0 + 1024 j + 16 l.
+// The compiler does not count these loads in its own vmcnt waits, so every
+// earlier load is waited for first (J = 0): a later compiler wait for a load
+// issued before the copies would otherwise also wait for the copies.
+template <int J>
+__device__ __forceinline__ void dma8(const uint32_t (&off)[16], const void *base, uint32_t m0) {
+    uint32_t keep_m0;
+    if constexpr (J == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    asm volatile("s_mov_b32 %[km], m0\n\ts_mov_b32 m0, %[m0]\n\t"
+                 "global_load_lds_dwordx4 %[v0], %[sb]\n\ts_add_u32 m0, m0, 0x400\n\t"
+                 "global_load_lds_dwordx4 %[v1], %[sb]\n\ts_add_u32 m0, m0, 0x400\n\t"
+                 "global_load_lds_dwordx4 %[v2], %[sb]\n\ts_add_u32 m0, m0, 0x400\n\t"
+                 "global_load_lds_dwordx4 %[v3], %[sb]\n\ts_add_u32 m0, m0, 0x400\n\t"
+                 "global_load_lds_dwordx4 %[v4], %[sb]\n\ts_add_u32 m0, m0, 0x400\n\t"
+                 "global_load_lds_dwordx4 %[v5], %[sb]\n\ts_add_u32 m0, m0, 0x400\n\t"
+                 "global_load_lds_dwordx4 %[v6], %[sb]\n\ts_add_u32 m0, m0, 0x400\n\t"
+                 "global_load_lds_dwordx4 %[v7], %[sb]\n\t"
+                 "s_mov_b32 m0, %[km]"
+                 : [km] "=&s"(keep_m0)
+                 : [m0] "s"(m0), [sb] "s"(base), [v0] "v"(off[J + 0]), [v1] "v"(off[J + 1]), [v2] "v"(off[J + 2]),
+                   [v3] "v"(off[J + 3]), [v4] "v"(off[J + 4]), [v5] "v"(off[J + 5]), [v6] "v"(off[J + 6]),
+                   [v7] "v"(off[J + 7])
+                 : "memory", "scc");
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// A copy of a per-lane value that the compiler cannot see through: values derived from it are rebuilt where
+// they are used instead of being held in registers (or spilled) across the whole kernel.
+__device__ __forceinline__ uint32_t opaque(uint32_t v) {
+    asm volatile("" : "+v"(v));
+    return v;
+}
+
+// RS: target rotation of the K outputs, 0 none, 1 pairs (i, i + 64), 2 pairs (2i, 2i + 1).
+template <int RS>
+__global__ __attribute__((amdgpu_flat_work_group_size(256, 256), amdgpu_waves_per_eu(1, 1)))
+void apply_pair_kernel(ApplyMultiArgs a) {
+    __shared__ __attribute__((aligned(16))) char lds_raw[2 * BUFB + 256 * 64];
+    lds_char_t *lds = (lds_char_t *)lds_raw;
+    const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+    const int per_wg = gridDim.x >> 3;                    // workgroups per XCD (the grid is a multiple of 8)
+    const int t_end = min(xcd * a.per_xcd + a.per_xcd, a.n_tasks);
+    int task = xcd * a.per_xcd + slot;
+    if (task >= t_end) return;
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int k = a.k;
+    constexpr int RING = 4;                               // K steps of W^T fragments held ahead
+    const uint32_t lrow = lane & 31, lhalf = lane >> 5;
+
+    // ---- copies: instruction i (0..15) of wave w moves token rows 64 w + 4 i + lane / 16; lane l writes LDS
+    // position l mod 16 of its row, which holds chunk (l mod 16) ^ (row mod 16) of the row.  The lane's 16
+    // source offsets of the copy cursor's task are kept in LDS (its own 64 bytes), not in registers.
+    lds_char_t *coff_lds = lds + 2 * BUFB + tid * 64;
+    auto set_rows = [&](const PairTask &t) {
+        uint32_t o[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+            int64_t n = t.tok0 + 64 * wave + 4 * i + (lane >> 4);
+            if (n >= a.N) n = a.N - 1;                    // rows past the end repeat the last token
+            const uint32_t seq = fastdiv_u((uint32_t)n, a.T);
+            const uint32_t tk = (uint32_t)n - seq * a.T.d;
+            const uint32_t r16 = (uint32_t)((4 * i + (lane >> 4)) & 15);
+            o[i] = (uint32_t)(2 * ((int64_t)seq * t.s_seq + (int64_t)tk * t.s_tok)) + 16u * ((lane & 15) ^ r16);
+        }
+#pragma unroll
+        for (int i = 0; i < 16; i += 4)
+            *(__attribute__((address_space(3))) u32x4_t *)(coff_lds + 4 * i) = u32x4_t{o[i], o[i + 1], o[i + 2], o[i + 3]};
+    };
+    const uint32_t m0w = (uint32_t)(uintptr_t)lds + (uint32_t)(64 * wave * ROWB);
+    PairTask C = pair_task(a, task);                      // the copy cursor: task ctask, staged block cu
+    int ctask = task, cu = 0;
+    bool cvalid = true;
+    set_rows(C);
+    auto issue = [&](int b) {
+        const int layer = C.rec[4 + cu];
+        const uint16_t *base = C.x + (int64_t)layer * C.s_layer;
+        uint32_t coff[16];
+        uint32_t cbase = (uint32_t)(uintptr_t)coff_lds;
+        asm volatile("" : "+v"(cbase));                   // one address register, small constant offsets
+#pragma unroll
+        for (int i = 0; i < 16; i += 4) {
+            const u32x4_t v = *(const __attribute__((address_space(3))) u32x4_t *)(uintptr_t)(cbase + 4 * i);
+            coff[i] = v[0];
+            coff[i + 1] = v[1];
+            coff[i + 2] = v[2];
+            coff[i + 3] = v[3];
+        }
+        dma8<0>(coff, base, m0w + b * BUFB);
+        dma8<8>(coff, base, m0w + b * BUFB + 8 * 1024);
+    };
+    auto advance = [&]() {
+        if (++cu == k) {
+            ctask += per_wg;
+            cu = 0;
+            cvalid = ctask < t_end;
+            if (cvalid) {
+                C = pair_task(a, ctask);
+                set_rows(C);
+            }
+        }
+    };
+
+    // ---- operands.  The lane's LDS read offsets are rebuilt in every block from an opaque copy of the lane
+    // index, so that they are not held in registers across the whole loop.
+    uint32_t lrow_b = lrow, lhalf_b = lhalf;
+    auto read_x = [&](bf16x8_t &x, int b, int ks, int s) __attribute__((always_inline)) {
+        x = *(const lds_bf16x8_t *)(lds + b * BUFB + (s * 32 + (int)lrow_b) * ROWB +
+                                    (int)(((2 * ks + lhalf_b) ^ (lrow_b & 15)) * 16));
+    };
+    auto wptr = [&](int m, int i) {
+        return a.wfrag + ((int64_t)m * k + i) * WBLK + wave * (2 * FRAG) + opaque((uint32_t)lane) * 8;
+    };
+    bf16x8_t whA[RING], wlA[RING], whB[RING], wlB[RING];
+    f32x16_t accA[8], accB[8];
+
+    // ---- epilogue of a task: bias, the K outputs' rotation, one rounding, 16-byte stores of target rows.
+    // D[i][t]: t = lane & 31, channel 32 wave + 8 (v / 4) + 4 (lane / 32) + (v & 3).  Every load of the
+    // epilogue (both maps' bias, the (cos, sin) of the tile's positions, which the two maps share) is issued
+    // before its first store: a load issued after a store is waited for only once that store has completed
+    // (loads and stores complete in order).
+    constexpr bool PERM = RS == 1;
+    auto epilogue = [&](const PairTask &t) __attribute__((always_inline)) {
+        // the lane's row and half, rebuilt here (see opaque)
+        const uint32_t ln = opaque((uint32_t)lane), lr = ln & 31, lh = ln >> 5;
+        const int64_t tok0 = t.tok0;
+        const crec_t mra = (crec_t)(a.maps + t.mA), mrb = (crec_t)(a.maps + t.mB);
+        const bool rotate = RS != 0 && mra[2] == 0;           // both maps of a pair have the same kv
+        float bias[2][16];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int c = frag_channel(wave, 8 * (v >> 2) + 4 * lh + (v & 3), PERM);
+            bias[0][v] = a.bias[(int64_t)t.mA * 128 + c];
+            bias[1][v] = a.bias[(int64_t)t.mB * 128 + c];
+        }
+        auto tok_of = [&](int s) {
+            const int64_t n = tok0 + (int64_t)(32 * s + lr);
+            return n < a.N ? n : a.N - 1;
+        };
+        // (cos, sin) of the lane's eight pairs at token 32 s + lane mod 32 of the tile
+        float4 csa[8][4];
+        if (RS != 0 && rotate) {
+#pragma unroll
+            for (int s = 0; s < 8; ++s) {
+                const int64_t nc = tok_of(s);
+                const uint32_t tk = (uint32_t)nc - fastdiv_u((uint32_t)nc, a.T) * a.T.d;
+                const float *row = a.rope_table + (int64_t)(a.rope_pos_offset + (int)tk) * 128;
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    // half split: frequencies 16 w + 8 (g / 2) + 4 lh + 2 (g % 2) + {0, 1}
+                    // interleaved: frequencies 16 w + 4 g + 2 lh + {0, 1}
+                    const int f = RS == 1 ? 16 * wave + 8 * (g >> 1) + 4 * lh + 2 * (g & 1) : 16 * wave + 4 * g + 2 * lh;
+                    csa[s][g] = *reinterpret_cast<const float4 *>(row + 2 * f);
+                }
+            }
+        }
+        const int oc0 = frag_channel(wave, 8 * lh, PERM), oc1 = frag_channel(wave, 16 + 8 * lh, PERM);
+#pragma unroll
+        for (int mi = 0; mi < 2; ++mi) {
+            const crec_t mr = mi == 0 ? mra : mrb;          // tgt_layer, tgt_head, kv, src_head
+            uint16_t *obase = a.out + mr[0] * a.os.layer + mr[2] * a.os.kv + mr[1] * a.os.head;
+            const f32x16_t(&acc)[8] = mi == 0 ? accA : accB;
+#pragma unroll
+            for (int s = 0; s < 8; ++s) {
+                // one token group at a time: its accumulators are read only here
+                __builtin_amdgcn_sched_barrier(0);
+                const int64_t n = tok0 + (int64_t)(32 * s + lr);
+                const int64_t nc = tok_of(s);
+                const uint32_t seq = fastdiv_u((uint32_t)nc, a.T);
+                const uint32_t tk = (uint32_t)nc - seq * a.T.d;
+                float o[16];
+#pragma unroll
+                for (int v = 0; v < 16; ++v) o[v] = acc[s][v] + bias[mi][v];
+                if (RS != 0 && rotate) {
+                    const float4(&cs)[4] = csa[s];
+                    if constexpr (RS == 1) {
+#pragma unroll
+                        for (int v = 0; v < 8; ++v) {      // pair (v, v + 8): channels c and c + 64
+                            const float4 q = cs[2 * (v >> 2) + ((v & 3) >> 1)];
+                            const float c = (v & 1) ? q.z : q.x, sn = (v & 1) ? q.w : q.y;
+                            const float x0 = o[v], x1 = o[v + 8];
+                            o[v] = __builtin_fmaf(x0, c, -x1 * sn);
+                            o[v + 8] = __builtin_fmaf(x1, c, x0 * sn);
+                        }
+                    } else {
+#pragma unroll
+                        for (int v = 0; v < 16; v += 2) {  // pair (v, v + 1): channels 2f and 2f + 1
+                            const float4 q = cs[v >> 2];
+                            const float c = (v & 2) ? q.z : q.x, sn = (v & 2) ? q.w : q.y;
+                            const float x0 = o[v], x1 = o[v + 1];
+                            o[v] = __builtin_fmaf(x0, c, -x1 * sn);
+                            o[v + 1] = __builtin_fmaf(x1, c, x0 * sn);
+                        }
+                    }
+                }
+                uint32_t pk[8];
+#pragma unroll
+                for (int gq = 0; gq < 4; ++gq) {
+                    pk[2 * gq] = pack_bf16(o[4 * gq + 0], o[4 * gq + 1]);
+                    pk[2 * gq + 1] = pack_bf16(o[4 * gq + 2], o[4 * gq + 3]);
+                }
+                // exchange with lane ^ 32 so that each lane owns 8 consecutive channels:
+                // lanes < 32 get channels 0-7 and 16-23, lanes >= 32 get 8-15 and 24-31
+                uint4 ov[2];
+#pragma unroll
+                for (int p = 0; p < 2; ++p) {
+                    const uint32_t s0 = lh ? pk[4 * p + 0] : pk[4 * p + 2];
+                    const uint32_t s1 = lh ? pk[4 * p + 1] : pk[4 * p + 3];
+                    const uint32_t r0 = (uint32_t)__shfl_xor((int)s0, 32);
+                    const uint32_t r1 = (uint32_t)__shfl_xor((int)s1, 32);
+                    ov[p] = lh ? make_uint4(r0, r1, pk[4 * p + 2], pk[4 * p + 3])
+                               : make_uint4(pk[4 * p + 0], pk[4 * p + 1], r0, r1);
+                }
+                if (n < a.N) {
+                    uint16_t *orow = obase + (int64_t)seq * a.os.seq + (int64_t)tk * a.os.tok;
+                    *reinterpret_cast<uint4 *>(orow + oc0) = ov[0];
+                    *reinterpret_cast<uint4 *>(orow + oc1) = ov[1];
+                }
+            }
+        }
+    };
+
+    // ---- prologue: the first staged block in buffer 0
+    issue(0);
+    advance();
+    PairTask T = pair_task(a, task);
+    wait_vm<0>();
+    lds_sync();
+
+    // the first K steps of both maps' fragments.  Without the rotation the ring runs ahead across blocks and
+    // tasks; with it the rotation's epilogue needs the registers, and each task loads its first steps anew.
+    constexpr bool CARRY = RS == 0;
+    auto first_steps = [&](const PairTask &t) {
+        const uint16_t *pa = wptr(t.mA, t.rec[4 + k]);
+        const uint16_t *pb = wptr(t.mB, t.rec[4 + 2 * k]);
+#pragma unroll
+        for (int r = 0; r < RING; ++r) {
+            whA[r] = *reinterpret_cast<const bf16x8_t *>(pa + r * 8 * FRAG);
+            wlA[r] = *reinterpret_cast<const bf16x8_t *>(pa + r * 8 * FRAG + FRAG);
+            whB[r] = *reinterpret_cast<const bf16x8_t *>(pb + r * 8 * FRAG);
+            wlB[r] = *reinterpret_cast<const bf16x8_t *>(pb + r * 8 * FRAG + FRAG);
+        }
+    };
+    if constexpr (CARRY) first_steps(T);
+    bool has_next = task + per_wg < t_end;
+    PairTask NT = T;
+    if (has_next) NT = pair_task(a, task + per_wg);
+    int buf = 0;
+    while (true) {
+        if constexpr (!CARRY) first_steps(T);
+        // the task's accumulators live only from here to its epilogue; zeroed by products of zeros so that
+        // they are born in the accumulation registers
+        {
+            const bf16x8_t z8 = {};
+            const f32x16_t z16 = {};
+#pragma unroll
+            for (int s = 0; s < 8; ++s) {
+                accA[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(z8, z8, z16, 0, 0, 0);
+                accB[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(z8, z8, z16, 0, 0, 0);
+            }
+        }
+        for (int u = 0; u < k; ++u) {
+            // the block after this one goes into the other buffer, which every wave finished reading before
+            // the last barrier
+            const bool issued = cvalid;
+            if (cvalid) issue(buf ^ 1);
+            // fragments: this block's, and the first steps of the next block (of this task, else of the next
+            // task; past the last task, or with the rotation, this block's again, never used)
+            const uint16_t *wcurA = wptr(T.mA, T.rec[4 + k + u]);
+            const uint16_t *wcurB = wptr(T.mB, T.rec[4 + 2 * k + u]);
+            const uint16_t *wnextA = wcurA, *wnextB = wcurB;
+            if (u + 1 < k) {
+                wnextA = wptr(T.mA, T.rec[4 + k + u + 1]);
+                wnextB = wptr(T.mB, T.rec[4 + 2 * k + u + 1]);
+            } else if (CARRY && has_next) {
+                wnextA = wptr(NT.mA, NT.rec[4 + k]);
+                wnextB = wptr(NT.mB, NT.rec[4 + 2 * k]);
+            }
+            // eight K steps; per x fragment A hi, B hi, A lo, B lo; after step ks each map refills its ring slot
+            // ks mod 4 with step ks + 4 (this block's, or the next block's first four)
+            lrow_b = lrow;
+            lhalf_b = lhalf;
+            asm volatile("" : "+v"(lrow_b), "+v"(lhalf_b));
+            bf16x8_t xr[4];
+            read_x(xr[0], buf, 0, 0);
+            read_x(xr[1], buf, 0, 1);
+            read_x(xr[2], buf, 0, 2);
+#pragma unroll
+            for (int ks = 0; ks < 8; ++ks) {
+                const int r = ks % RING;
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int s = 0; s < 8; ++s) {
+                    const int f = 8 * ks + s;
+                    if (f + 3 < 64) read_x(xr[(f + 3) & 3], buf, (f + 3) >> 3, (f + 3) & 7);
+                    const bf16x8_t x = xr[f & 3];
+                    accA[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(whA[r], x, accA[s], 0, 0, 0);
+                    accB[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(whB[r], x, accB[s], 0, 0, 0);
+                    accA[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wlA[r], x, accA[s], 0, 0, 0);
+                    accB[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wlB[r], x, accB[s], 0, 0, 0);
+                }
+                {
+                    const uint16_t *pa = ks + RING < 8 ? wcurA + (ks + RING) * 8 * FRAG : wnextA + (ks + RING - 8) * 8 * FRAG;
+                    const uint16_t *pb = ks + RING < 8 ? wcurB + (ks + RING) * 8 * FRAG : wnextB + (ks + RING - 8) * 8 * FRAG;
+                    whA[r] = *reinterpret_cast<const bf16x8_t *>(pa);
+                    wlA[r] = *reinterpret_cast<const bf16x8_t *>(pa + FRAG);
+                    whB[r] = *reinterpret_cast<const bf16x8_t *>(pb);
+                    wlB[r] = *reinterpret_cast<const bf16x8_t *>(pb + FRAG);
+                }
+                // one x read ahead of each fragment's products, the ring loads after the step
+#pragma unroll
+                for (int s = 0; s < 8; ++s) {
+                    if (8 * ks + s + 3 < 64) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+                }
+                __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            if (issued) advance();                        // the copy cursor moves on (to the next task: its rows)
+            // this wave's copies of the next block have landed (loads complete in order and this block's 32
+            // ring loads were issued after them); the barrier publishes every wave's
+            wait_vm<32>();
+            lds_sync();
+            buf ^= 1;
+        }
+        epilogue(T);
+        if (!has_next) break;
+        task += per_wg;
+        T = NT;
+        has_next = task + per_wg < t_end;
+        if (has_next) NT = pair_task(a, task + per_wg);
+    }
+}
+
 }  // namespace
 
 hipError_t launch_split_maps_frag(int32_t n_maps, int32_t k, const float *maps, uint16_t *wfrag, float *bias,
@@ -420,6 +828,15 @@ hipError_t launch_apply_multi(const ApplyMultiArgs &a, int32_t n_cu, hipStream_t
     // one workgroup per compute unit, a multiple of 8 so every XCD gets the same count
     int per_xcd_wg = n_cu / 8 > 0 ? n_cu / 8 : 1;
     if (per_xcd_wg > a.per_xcd) per_xcd_wg = a.per_xcd;
+    if (a.pairs) {
+        if (!a.rope_table)
+            hipLaunchKernelGGL(apply_pair_kernel<0>, dim3(8 * per_xcd_wg), dim3(256), 0, s, a);
+        else if (a.rope_style == 0)
+            hipLaunchKernelGGL(apply_pair_kernel<1>, dim3(8 * per_xcd_wg), dim3(256), 0, s, a);
+        else
+            hipLaunchKernelGGL(apply_pair_kernel<2>, dim3(8 * per_xcd_wg), dim3(256), 0, s, a);
+        return hipGetLastError();
+    }
     if (!a.rope_table)
         hipLaunchKernelGGL(apply_multi_kernel<0>, dim3(8 * per_xcd_wg), dim3(256), 0, s, a);
     else if (a.rope_style == 0)

@@ -216,6 +216,12 @@ struct ApplyMultiArgs {
     const float *rope_table;  // NULL, or the target's (cos, sin) [n_pos][64][2]: K outputs are rotated
     int32_t rope_style;       // 0: pairs (i, i + 64), with the permuted fragments; 1: pairs (2i, 2i + 1)
     int32_t rope_pos_offset;
+    // NULL, or the paired form: tasks are (pair, tile), n_tasks = n_pairs * n_tiles.  Record of a pair
+    // (pair_stride int32): [0] map A, [1] map B or -1, [2] staged blocks nb (<= 2k), [3] unused,
+    // [4 + j] (j < nb) 4 * source layer + (A uses it) + 2 (B uses it), ascending layers,
+    // [4 + 2k + q] (q < k) A's block index of its q-th used block, [4 + 3k + q] the same for B.
+    const int32_t *pairs;
+    int32_t n_pairs, pair_stride;
 };
 
 // Launchers (return hipError_t of the launch).

@@ -503,6 +503,43 @@ def test_multi_apply_random_maps_ragged_tokens(cb, k, B, T):
     plan.close()
 
 
+@pytest.mark.parametrize("style", [None, 1])
+def test_multi_apply_paired_maps_permuted_and_lone(cb, style):
+    # maps of one (kv, source head) whose source-layer sets are equal share
+    # their staged blocks: equal sets listed in different orders (each map's
+    # block order differs from the staging order), and maps with no partner
+    # (which take the single-map path), against the oracle, plain and with the
+    # target rotation
+    rng = np.random.default_rng(31)
+    k, L_s, H_s, L_t, H_t, B, T = 3, 6, 2, 6, 2, 2, 600
+    src, tgt, _ = small_inputs(rng, L_s, H_s, L_t, H_t, B, T)
+    sets = [[0, 1, 2], [2, 0, 1], [3, 4, 1], [1, 3, 4], [4, 5, 0], [1, 2, 5]]
+    hm = {f: [] for f in oracle.MULTI_MAP_FIELDS}
+    for l in range(L_t):
+        for z in range(2):
+            for h in range(H_t):
+                for f, v in zip(oracle.MULTI_MAP_FIELDS, (l, h, z, sets[l], h, l * H_t + h)):
+                    hm[f].append(v)
+    hm = {f: np.asarray(v, np.int32) for f, v in hm.items()}
+    plan = cb.cb_plan_create_multi(hm, src, tgt, 1)
+    maps = random_maps(rng, plan.n_maps, plan.P, plan.d_t)
+    say(f"multi apply paired maps (permuted, lone), rotation style {style}")
+    out = torch.zeros((L_t, 2, B, H_t, T, 128), dtype=torch.bfloat16, device="cuda")
+    ref = np.zeros(tuple(out.shape), dtype=np.uint16)
+    ss, os_ = synth.cache_strides(L_s, H_s, B, T, 128), synth.cache_strides(L_t, H_t, B, T, 128)
+    W = maps.double().cpu().numpy()
+    if style is None:
+        cb.cb_apply(plan, maps, src, out)
+        oracle.apply_multi(hm, W, bits(src), ss, 128, ref, os_, 128, B, T, n_threads=NTHREADS)
+    else:
+        table = gpu_rope_table(cb, 1e6, 128, T)
+        cb.cb_apply_rope(plan, maps, src, out, cb.rope_spec(table, style, 0))
+        oracle.apply_multi_rope(hm, W, bits(src), ss, 128, ref, os_, 128, B, T, 1e6, style, 0, n_threads=NTHREADS)
+    torch.cuda.synchronize()
+    check_apply_multi(bits(out), ref, hm, range(plan.n_maps), " (paired maps)")
+    plan.close()
+
+
 def test_multi_apply_selector_maps_copy_bits_strided_output(cb):
     # map m copies source layer j_m of its window (identity block, zero bias): the
     # output bits equal the sender's bits.  The target is a view with room for
