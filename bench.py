@@ -841,7 +841,7 @@ def multi_leg(cb, synth, steps):
         "calib_rows_per_s": wl.n_seqs * rows_per_call // B / (build_ms / 1e3),
         "legs_ms": {"stats_call": call_ms, "solve": solve_ms, "apply_100seq": apply_ms},
         "apply_tokens_per_s": B * wl.seq_len / (apply_ms / 1e3),
-        "apply_roofline": {"bound": "mfma", "kernel": "split_maps_kernel + apply_multi_kernel per 100-seq call",
+        "apply_roofline": {"bound": "mfma", "kernel": "split_maps_frag_kernel + apply_pair_kernel + apply_multi_kernel per 100-seq call",
                            "achieved": apply_flop / (apply_ms / 1e3) / 1e12, "peak": 2500.0, "unit": "TFLOP/s",
                            "frac": apply_flop / (apply_ms / 1e3) / 1e12 / 2500.0},
         "roofline": {"bound": "mfma", "kernel": "stats_multi_kernel per 100-seq call", "achieved": tflops,
