@@ -116,6 +116,19 @@ struct ACfg {
     static_assert(SR == 0 || DS == 64 || DS == 128, "the source de-rotation takes d_s = 64 or 128");
 };
 
+// Lanes l and l ^ 32 trade halves so that each lane owns 8 consecutive channels of its 32-channel
+// block (lanes < 32: channels 0-7 and 16-23, lanes >= 32: 8-15 and 24-31).  pk holds the lane's packed
+// pairs, its channels 8 g + 4 (lane / 32) + {0 .. 3} in pk[2 g], pk[2 g + 1].  v_permlane32_swap trades
+// the upper 32 lanes of its first operand with the lower 32 lanes of its second.
+__device__ __forceinline__ void exchange32(const uint32_t (&pk)[8], uint4 (&o)[2]) {
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+        const auto x = __builtin_amdgcn_permlane32_swap(pk[4 * p + 0], pk[4 * p + 2], false, false);
+        const auto y = __builtin_amdgcn_permlane32_swap(pk[4 * p + 1], pk[4 * p + 3], false, false);
+        o[p] = make_uint4(x[0], y[0], x[1], y[1]);
+    }
+}
+
 // Rotated position of 16-byte block cb of token row t in LDS: 16 consecutive
 // tokens reading the same block hit distinct banks (when NCB = 16).
 template <int NCB>
@@ -516,19 +529,8 @@ __global__ __attribute__((amdgpu_flat_work_group_size(ACfg<DS, DT>::NT, ACfg<DS,
             pk[2 * gq] = pack_bf16(acc[4 * gq + 0], acc[4 * gq + 1]);
             pk[2 * gq + 1] = pack_bf16(acc[4 * gq + 2], acc[4 * gq + 3]);
         }
-        // Exchange with lane ^ 32 so that each lane owns 8 consecutive
-        // channels: lanes < 32 get channels 0-7 and 16-23, lanes >= 32 get
-        // 8-15 and 24-31 of the 32-channel block.
         uint4 o[2];
-#pragma unroll
-        for (int p = 0; p < 2; ++p) {
-            const uint32_t s0 = lhalf ? pk[4 * p + 0] : pk[4 * p + 2];
-            const uint32_t s1 = lhalf ? pk[4 * p + 1] : pk[4 * p + 3];
-            const uint32_t r0 = (uint32_t)__shfl_xor((int)s0, 32);
-            const uint32_t r1 = (uint32_t)__shfl_xor((int)s1, 32);
-            o[p] = lhalf ? make_uint4(r0, r1, pk[4 * p + 2], pk[4 * p + 3])
-                         : make_uint4(pk[4 * p + 0], pk[4 * p + 1], r0, r1);
-        }
+        exchange32(pk, o);
         if (STAGE) {
             char *ob = obuf + ((sb & 1) * 2 + slot) * OBUF + lrow * (DT * 2);
             *reinterpret_cast<uint4 *>(ob + ((oc0 / 8 + (int)lrow) % NCBT) * 16) = o[0];

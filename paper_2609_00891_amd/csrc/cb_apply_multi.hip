@@ -75,6 +75,19 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
     return __builtin_bit_cast(uint32_t, p);
 }
 
+// Lanes l and l ^ 32 trade halves so that each lane owns 8 consecutive channels of its 32-channel
+// block (lanes < 32: channels 0-7 and 16-23, lanes >= 32: 8-15 and 24-31).  pk holds the lane's packed
+// pairs, its channels 8 g + 4 (lane / 32) + {0 .. 3} in pk[2 g], pk[2 g + 1].  v_permlane32_swap trades
+// the upper 32 lanes of its first operand with the lower 32 lanes of its second.
+__device__ __forceinline__ void exchange32(const uint32_t (&pk)[8], uint4 (&o)[2]) {
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+        const auto x = __builtin_amdgcn_permlane32_swap(pk[4 * p + 0], pk[4 * p + 2], false, false);
+        const auto y = __builtin_amdgcn_permlane32_swap(pk[4 * p + 1], pk[4 * p + 3], false, false);
+        o[p] = make_uint4(x[0], y[0], x[1], y[1]);
+    }
+}
+
 // This wave's LDS reads and writes have completed, then the workgroup barrier;
 // the empty asm keeps the compiler from moving memory operations across it.
 __device__ __forceinline__ void lds_sync() {
@@ -379,18 +392,8 @@ void apply_multi_kernel(ApplyMultiArgs a) {
                     pk[2 * gq] = pack_bf16(o[4 * gq + 0], o[4 * gq + 1]);
                     pk[2 * gq + 1] = pack_bf16(o[4 * gq + 2], o[4 * gq + 3]);
                 }
-                // exchange with lane ^ 32 so that each lane owns 8 consecutive channels:
-                // lanes < 32 get channels 0-7 and 16-23, lanes >= 32 get 8-15 and 24-31
                 uint4 ov[2];
-#pragma unroll
-                for (int p = 0; p < 2; ++p) {
-                    const uint32_t s0 = lhalf ? pk[4 * p + 0] : pk[4 * p + 2];
-                    const uint32_t s1 = lhalf ? pk[4 * p + 1] : pk[4 * p + 3];
-                    const uint32_t r0 = (uint32_t)__shfl_xor((int)s0, 32);
-                    const uint32_t r1 = (uint32_t)__shfl_xor((int)s1, 32);
-                    ov[p] = lhalf ? make_uint4(r0, r1, pk[4 * p + 2], pk[4 * p + 3])
-                                  : make_uint4(pk[4 * p + 0], pk[4 * p + 1], r0, r1);
-                }
+                exchange32(pk, ov);
                 if (n < a.N) {
                     uint16_t *orow = obase + (int64_t)seq * a.os.seq + (int64_t)tk * a.os.tok;
                     *reinterpret_cast<uint4 *>(orow + oc0) = ov[0];
@@ -532,14 +535,15 @@ void apply_pair_kernel(ApplyMultiArgs a) {
     lds_char_t *coff_lds = lds + 2 * BUFB + tid * 64;
     auto set_rows = [&](const PairTask &t) {
         uint32_t o[16];
+        const uint32_t ln = opaque((uint32_t)lane);        // (see opaque)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-            int64_t n = t.tok0 + 64 * wave + 4 * i + (lane >> 4);
+            int64_t n = t.tok0 + (int64_t)(64 * wave + 4 * i + (ln >> 4));
             if (n >= a.N) n = a.N - 1;                    // rows past the end repeat the last token
             const uint32_t seq = fastdiv_u((uint32_t)n, a.T);
             const uint32_t tk = (uint32_t)n - seq * a.T.d;
-            const uint32_t r16 = (uint32_t)((4 * i + (lane >> 4)) & 15);
-            o[i] = (uint32_t)(2 * ((int64_t)seq * t.s_seq + (int64_t)tk * t.s_tok)) + 16u * ((lane & 15) ^ r16);
+            const uint32_t r16 = (uint32_t)((4 * i + (ln >> 4)) & 15);
+            o[i] = (uint32_t)(2 * ((int64_t)seq * t.s_seq + (int64_t)tk * t.s_tok)) + 16u * ((ln & 15) ^ r16);
         }
 #pragma unroll
         for (int i = 0; i < 16; i += 4)
@@ -677,18 +681,8 @@ void apply_pair_kernel(ApplyMultiArgs a) {
                     pk[2 * gq] = pack_bf16(o[4 * gq + 0], o[4 * gq + 1]);
                     pk[2 * gq + 1] = pack_bf16(o[4 * gq + 2], o[4 * gq + 3]);
                 }
-                // exchange with lane ^ 32 so that each lane owns 8 consecutive channels:
-                // lanes < 32 get channels 0-7 and 16-23, lanes >= 32 get 8-15 and 24-31
                 uint4 ov[2];
-#pragma unroll
-                for (int p = 0; p < 2; ++p) {
-                    const uint32_t s0 = lh ? pk[4 * p + 0] : pk[4 * p + 2];
-                    const uint32_t s1 = lh ? pk[4 * p + 1] : pk[4 * p + 3];
-                    const uint32_t r0 = (uint32_t)__shfl_xor((int)s0, 32);
-                    const uint32_t r1 = (uint32_t)__shfl_xor((int)s1, 32);
-                    ov[p] = lh ? make_uint4(r0, r1, pk[4 * p + 2], pk[4 * p + 3])
-                               : make_uint4(pk[4 * p + 0], pk[4 * p + 1], r0, r1);
-                }
+                exchange32(pk, ov);
                 if (n < a.N) {
                     uint16_t *orow = obase + (int64_t)seq * a.os.seq + (int64_t)tk * a.os.tok;
                     *reinterpret_cast<uint4 *>(orow + oc0) = ov[0];
