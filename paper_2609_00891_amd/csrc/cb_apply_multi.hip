@@ -475,13 +475,10 @@ __device__ __forceinline__ PairTask pair_task(const ApplyMultiArgs &a, int task)
 
 // Eight 16-byte copies global -> LDS under one save of M0: copy j reads
 // base + off[J + j] per lane and writes lane l's chunk at m0 + 1024 j + 16 l.
-// The compiler does not count these loads in its own vmcnt waits, so every
-// earlier load is waited for first (J = 0): a later compiler wait for a load
-// issued before the copies would otherwise also wait for the copies.
+// The compiler does not count these loads in its own vmcnt waits.
 template <int J>
 __device__ __forceinline__ void dma8(const uint32_t (&off)[16], const void *base, uint32_t m0) {
     uint32_t keep_m0;
-    if constexpr (J == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     asm volatile("s_mov_b32 %[km], m0\n\ts_mov_b32 m0, %[m0]\n\t"
                  "global_load_lds_dwordx4 %[v0], %[sb]\n\ts_add_u32 m0, m0, 0x400\n\t"
                  "global_load_lds_dwordx4 %[v1], %[sb]\n\ts_add_u32 m0, m0, 0x400\n\t"
@@ -734,6 +731,12 @@ void apply_pair_kernel(ApplyMultiArgs a) {
         for (int u = 0; u < k; ++u) {
             // the block after this one goes into the other buffer, which every wave finished reading before
             // the last barrier
+            // this block's fragments, requested during the last block (or at the task's start), are waited
+            // for before the copies: the compiler's own waits do not count the copies, so a wait for a load
+            // issued before them, placed after them, would also wait for the copies
+            asm volatile("" ::"v"(whA[0]), "v"(wlA[0]), "v"(whB[0]), "v"(wlB[0]), "v"(whA[1]), "v"(wlA[1]),
+                         "v"(whB[1]), "v"(wlB[1]), "v"(whA[2]), "v"(wlA[2]), "v"(whB[2]), "v"(wlB[2]),
+                         "v"(whA[3]), "v"(wlA[3]), "v"(whB[3]), "v"(wlB[3]));
             const bool issued = cvalid;
             if (cvalid) issue(buf ^ 1);
             // fragments: this block's, and the first steps of the next block (of this task, else of the next
