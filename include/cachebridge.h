@@ -550,9 +550,11 @@ typedef struct {
  * the call.  Solve with cb_ridge_solve_ws.  cb_apply maps a sender cache with
  * the P x d_t maps, every token: out = RNE_bf16([x_0, ..., x_{k-1}, 1] maps[m])
  * (coefficients as two bf16 terms, fp32 sums and bias, one rounding); the
- * rows of one source (layer, kv, head) must span fewer than 2^32 elements
- * ((n_seqs - 1) s_seq + (seq_len - 1) s_tok + 128), else CB_ERR_UNSUPPORTED
- * (apply in smaller batches).  The two-pass centered calls (cb_stats_means
+ * rows of one source (layer, kv, head) must span fewer than 4 GiB
+ * (2 ((n_seqs - 1) s_seq + (seq_len - 1) s_tok + 128) bytes), else
+ * CB_ERR_UNSUPPORTED (apply in smaller batches).  Maps of one (kv, source
+ * head) with equal source-layer sets are applied in pairs that read their
+ * source rows once.  The two-pass centered calls (cb_stats_means
  * without sq, cb_stats_accumulate_centered) take such a plan too.  Errors
  * as in cb_plan_create, plus CB_ERR_INVALID_ARGUMENT for a source layer
  * selected twice by one map.

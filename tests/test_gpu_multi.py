@@ -503,13 +503,14 @@ def test_multi_apply_random_maps_ragged_tokens(cb, k, B, T):
     plan.close()
 
 
-@pytest.mark.parametrize("style", [None, 1])
-def test_multi_apply_paired_maps_permuted_and_lone(cb, style):
+@pytest.mark.parametrize("style,both", [(None, False), (1, False), (0, True)])
+def test_multi_apply_paired_maps_permuted_and_lone(cb, style, both):
     # maps of one (kv, source head) whose source-layer sets are equal share
     # their staged blocks: equal sets listed in different orders (each map's
     # block order differs from the staging order), and maps with no partner
-    # (which take the single-map path), against the oracle, plain and with the
-    # target rotation
+    # (which take the single-map path), against the oracle: plain, with the
+    # target rotation, and with the sender's keys turned back as well (the K
+    # pairs then read the de-rotated copy)
     rng = np.random.default_rng(31)
     k, L_s, H_s, L_t, H_t, B, T = 3, 6, 2, 6, 2, 2, 600
     src, tgt, _ = small_inputs(rng, L_s, H_s, L_t, H_t, B, T)
@@ -531,12 +532,26 @@ def test_multi_apply_paired_maps_permuted_and_lone(cb, style):
     if style is None:
         cb.cb_apply(plan, maps, src, out)
         oracle.apply_multi(hm, W, bits(src), ss, 128, ref, os_, 128, B, T, n_threads=NTHREADS)
-    else:
+    elif not both:
         table = gpu_rope_table(cb, 1e6, 128, T)
         cb.cb_apply_rope(plan, maps, src, out, cb.rope_spec(table, style, 0))
         oracle.apply_multi_rope(hm, W, bits(src), ss, 128, ref, os_, 128, B, T, 1e6, style, 0, n_threads=NTHREADS)
+    else:
+        src_r, sb = rotated(src, 1e4, style, 0)
+        tab_s, tab_t = gpu_rope_table(cb, 1e4, 128, T), gpu_rope_table(cb, 1e6, 128, T)
+        cb.cb_apply_rope(plan, maps, src_r, out, cb.rope_spec(tab_t, style, 0), cb.rope_spec(tab_s, style, 0))
+        oracle.apply_multi_rope(hm, W, unrotated(sb, 1e4, style, 0), ss, 128, ref, os_, 128, B, T, 1e6, style, 0,
+                                n_threads=NTHREADS)
     torch.cuda.synchronize()
-    check_apply_multi(bits(out), ref, hm, range(plan.n_maps), " (paired maps)")
+    if not both:
+        check_apply_multi(bits(out), ref, hm, range(plan.n_maps), " (paired maps)")
+    else:
+        # the oracle turns back in fp64, the kernel in fp32: a few inputs differ by one ulp
+        ob = bits(out)
+        e = relF(oracle.bf16_to_double(ob), oracle.bf16_to_double(ref))
+        eq = float((ob == ref).mean())
+        say(f"  paired maps, both rotations: relF {e:.3e}, bitwise-equal {eq:.6f}")
+        assert e <= TOL_APPLY and eq >= 0.99
     plan.close()
 
 
