@@ -496,6 +496,17 @@ __device__ __forceinline__ void dma8(const uint32_t (&off)[16], const void *base
                  : "memory", "scc");
 }
 
+__device__ __forceinline__ void dma2(uint32_t off0, uint32_t off1, const void *base, uint32_t m0) {
+    uint32_t keep_m0;
+    asm volatile("s_mov_b32 %[km], m0\n\ts_mov_b32 m0, %[m0]\n\t"
+                 "global_load_lds_dwordx4 %[v0], %[sb]\n\ts_add_u32 m0, m0, 0x400\n\t"
+                 "global_load_lds_dwordx4 %[v1], %[sb]\n\t"
+                 "s_mov_b32 m0, %[km]"
+                 : [km] "=&s"(keep_m0)
+                 : [m0] "s"(m0), [sb] "s"(base), [v0] "v"(off0), [v1] "v"(off1)
+                 : "memory", "scc");
+}
+
 template <int N>
 __device__ __forceinline__ void wait_vm() {
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
@@ -567,6 +578,19 @@ void apply_pair_kernel(ApplyMultiArgs a) {
         }
         dma8<0>(coff, base, m0w + b * BUFB);
         dma8<8>(coff, base, m0w + b * BUFB + 8 * 1024);
+    };
+    // the same copies in eight pairs, spread over a step's products; each pair's offsets read from LDS
+    const uint16_t *pbase = a.wfrag;
+    auto prep = [&]() {
+        const int layer = C.rec[4 + cu];
+        pbase = C.x + (int64_t)layer * C.s_layer;
+    };
+    auto pair_copy = [&](int j, uint32_t m0) __attribute__((always_inline)) {
+        uint32_t cbase = (uint32_t)(uintptr_t)coff_lds;
+        asm volatile("" : "+v"(cbase));
+        typedef __attribute__((ext_vector_type(2))) uint32_t u32x2_t;
+        const u32x2_t v = *(const __attribute__((address_space(3))) u32x2_t *)(uintptr_t)(cbase + 4 * j);
+        dma2(v[0], v[1], pbase, m0);
     };
     auto advance = [&]() {
         if (++cu == k) {
@@ -729,16 +753,17 @@ void apply_pair_kernel(ApplyMultiArgs a) {
             }
         }
         for (int u = 0; u < k; ++u) {
-            // the block after this one goes into the other buffer, which every wave finished reading before
-            // the last barrier
             // this block's fragments, requested during the last block (or at the task's start), are waited
             // for before the copies: the compiler's own waits do not count the copies, so a wait for a load
             // issued before them, placed after them, would also wait for the copies
             asm volatile("" ::"v"(whA[0]), "v"(wlA[0]), "v"(whB[0]), "v"(wlB[0]), "v"(whA[1]), "v"(wlA[1]),
                          "v"(whB[1]), "v"(wlB[1]), "v"(whA[2]), "v"(wlA[2]), "v"(whB[2]), "v"(wlB[2]),
                          "v"(whA[3]), "v"(wlA[3]), "v"(whB[3]), "v"(wlB[3]));
+            // the block after this one goes, in eight pairs of copies spread over step 0's products, into
+            // the other buffer, which every wave finished reading before the last barrier
             const bool issued = cvalid;
-            if (cvalid) issue(buf ^ 1);
+            if (cvalid) prep();
+            const uint32_t pm0 = m0w + (buf ^ 1) * BUFB;
             // fragments: this block's, and the first steps of the next block (of this task, else of the next
             // task; past the last task, or with the rotation, this block's again, never used)
             const uint16_t *wcurA = wptr(T.mA, T.rec[4 + k + u]);
@@ -773,6 +798,7 @@ void apply_pair_kernel(ApplyMultiArgs a) {
                     accB[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(whB[r], x, accB[s], 0, 0, 0);
                     accA[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wlA[r], x, accA[s], 0, 0, 0);
                     accB[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wlB[r], x, accB[s], 0, 0, 0);
+                    if (ks == 0 && issued) pair_copy(2 * s, pm0 + 2 * s * 1024);
                 }
                 {
                     const uint16_t *pa = ks + RING < 8 ? wcurA + (ks + RING) * 8 * FRAG : wnextA + (ks + RING - 8) * 8 * FRAG;
